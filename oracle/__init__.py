@@ -90,6 +90,8 @@ def _load():
         lib.orc_owner_support.argtypes = [dp, ctypes.c_int, dp, ctypes.c_int, P(Params), ctypes.c_int,
                                           ctypes.c_int64, ip, dp, dp]
         lib.orc_owner_support.restype = ctypes.c_int64
+        lib.orc_max_threads.argtypes = []
+        lib.orc_max_threads.restype = ctypes.c_int
         _lib = lib
         return lib
 
@@ -181,6 +183,11 @@ def run_batch(X, Y, prm: Optional[Params] = None, grad: bool = True,
         if grad:
             gx[b], gy[b] = r.grad_x, r.grad_y
     return loss, gx, gy
+
+
+def max_threads() -> int:
+    """OpenMP threads the oracle uses by default (OMP_NUM_THREADS or all cores)."""
+    return int(_load().orc_max_threads())
 
 
 def owner_stats(P, Q, owners, prm: Optional[Params] = None, threads: int = 0) -> Dict[str, np.ndarray]:

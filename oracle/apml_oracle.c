@@ -517,6 +517,16 @@ fail:
 /* accessors                                                                */
 /* ------------------------------------------------------------------------ */
 
+/* Threads an OpenMP region of the oracle uses when nthreads <= 0. */
+int orc_max_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
 int64_t orc_nnz(const orc_result *r) { return r->nnz; }
 double orc_loss(const orc_result *r) { return r->loss; }
 

@@ -1,0 +1,974 @@
+// Host side of libapml: argument validation, device memory (pool or caller
+// allocator), per-phase event timing, and the launch sequence of the forward
+// and backward passes (Algorithm 1 of the paper, redesigned as described at
+// the top of kernels.hip).
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <unordered_map>
+#include <utility>
+#include <vector>
+
+#include "../../include/apml.h"
+#include "apml_internal.h"
+
+using namespace apml;
+
+// ---------------------------------------------------------------------------
+// errors
+// ---------------------------------------------------------------------------
+
+namespace {
+
+thread_local std::string g_last_error;
+
+apml_status fail(apml_status st, const std::string &msg)
+{
+    g_last_error = msg;
+    return st;
+}
+
+#define HIP_TRY(expr)                                                                          \
+    do {                                                                                       \
+        hipError_t e_ = (expr);                                                                \
+        if (e_ != hipSuccess)                                                                  \
+            return fail(APML_ERR_DEVICE, std::string(#expr) + ": " + hipGetErrorString(e_));   \
+    } while (0)
+
+// ---------------------------------------------------------------------------
+// device memory: caller allocator or a per-(device, stream) block pool
+// ---------------------------------------------------------------------------
+
+struct Memory {
+    std::mutex mu;
+    apml_alloc_fn user_alloc = nullptr;
+    apml_free_fn user_free = nullptr;
+    void *user = nullptr;
+    // free blocks of the pool, by (device, stream), keyed by block size
+    std::map<std::pair<int, hipStream_t>, std::multimap<size_t, void *>> free_blocks;
+    std::unordered_map<void *, size_t> block_size; // every block the pool owns
+    int64_t in_use = 0, peak = 0, reserved = 0;
+    int live_plans = 0;
+};
+
+Memory &mem()
+{
+    static Memory m;
+    return m;
+}
+
+size_t round_block(size_t n)
+{
+    if (n <= (1u << 20))
+        return (n + 511) & ~size_t(511);
+    return (n + (size_t(1) << 20) - 1) & ~((size_t(1) << 20) - 1);
+}
+
+void *pool_alloc(size_t bytes, hipStream_t s, size_t *got)
+{
+    Memory &m = mem();
+    std::lock_guard<std::mutex> lk(m.mu);
+    if (m.user_alloc) {
+        void *p = m.user_alloc(bytes, (apml_stream)s, m.user);
+        if (p) {
+            *got = bytes;
+            m.in_use += (int64_t)bytes;
+            m.peak = std::max(m.peak, m.in_use);
+        }
+        return p;
+    }
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return nullptr;
+    const size_t want = round_block(bytes);
+    auto &fl = m.free_blocks[{dev, s}];
+    auto it = fl.lower_bound(want);
+    void *p = nullptr;
+    size_t size = want;
+    if (it != fl.end() && it->first <= 2 * want + (size_t(1) << 20)) {
+        p = it->second;
+        size = it->first;
+        fl.erase(it);
+    } else {
+        if (hipMalloc(&p, want) != hipSuccess) {
+            // give the cached blocks back and try once more
+            (void)hipGetLastError();
+            (void)hipDeviceSynchronize();
+            for (auto &kv : m.free_blocks)
+                for (auto &blk : kv.second) {
+                    (void)hipFree(blk.second);
+                    m.reserved -= (int64_t)m.block_size[blk.second];
+                    m.block_size.erase(blk.second);
+                }
+            m.free_blocks.clear();
+            if (hipMalloc(&p, want) != hipSuccess) {
+                (void)hipGetLastError();
+                return nullptr;
+            }
+        }
+        m.block_size[p] = want;
+        m.reserved += (int64_t)want;
+    }
+    *got = size;
+    m.in_use += (int64_t)size;
+    m.peak = std::max(m.peak, m.in_use);
+    return p;
+}
+
+void pool_free(void *p, size_t size, hipStream_t s)
+{
+    if (!p)
+        return;
+    Memory &m = mem();
+    std::lock_guard<std::mutex> lk(m.mu);
+    m.in_use -= (int64_t)size;
+    if (m.user_free) {
+        m.user_free(p, size, (apml_stream)s, m.user);
+        return;
+    }
+    int dev = 0;
+    (void)hipGetDevice(&dev);
+    m.free_blocks[{dev, s}].insert({size, p});
+}
+
+// A set of device blocks released together.
+struct Arena {
+    hipStream_t stream = nullptr;
+    std::vector<std::pair<void *, size_t>> blocks;
+    int64_t bytes = 0;
+    bool failed = false;
+
+    template <typename T> T *get(size_t count)
+    {
+        if (failed)
+            return nullptr;
+        size_t got = 0;
+        void *p = pool_alloc(std::max<size_t>(count * sizeof(T), 16), stream, &got);
+        if (!p) {
+            failed = true;
+            return nullptr;
+        }
+        blocks.push_back({p, got});
+        bytes += (int64_t)got;
+        return static_cast<T *>(p);
+    }
+    void release()
+    {
+        for (auto &b : blocks)
+            pool_free(b.first, b.second, stream);
+        blocks.clear();
+        bytes = 0;
+    }
+    ~Arena() { release(); }
+};
+
+// ---------------------------------------------------------------------------
+// per-phase event timing
+// ---------------------------------------------------------------------------
+
+const char *kPhaseNames[APML_N_PHASES] = {"stats",    "support", "build",        "softmax",
+                                          "sinkhorn", "loss",    "bwd_sinkhorn", "bwd_softmax"};
+enum Phase { PH_STATS, PH_SUPPORT, PH_BUILD, PH_SOFTMAX, PH_SINKHORN, PH_LOSS, PH_BWD_SINK, PH_BWD_SOFTMAX };
+
+struct Profiler {
+    std::mutex mu;
+    bool on = false;
+    std::vector<hipEvent_t> spare;
+    struct Pending {
+        int phase;
+        hipEvent_t a, b;
+    };
+    std::vector<Pending> pending;
+    double total[APML_N_PHASES] = {};
+    int64_t count[APML_N_PHASES] = {};
+};
+
+Profiler &prof()
+{
+    static Profiler p;
+    return p;
+}
+
+hipEvent_t take_event()
+{
+    Profiler &p = prof();
+    if (!p.spare.empty()) {
+        hipEvent_t e = p.spare.back();
+        p.spare.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess)
+        return nullptr;
+    return e;
+}
+
+class PhaseTimer {
+  public:
+    PhaseTimer(int phase, hipStream_t s) : phase_(phase), s_(s)
+    {
+        Profiler &p = prof();
+        std::lock_guard<std::mutex> lk(p.mu);
+        if (!p.on)
+            return;
+        a_ = take_event();
+        b_ = take_event();
+        if (a_ && b_)
+            (void)hipEventRecord(a_, s_);
+    }
+    void stop()
+    {
+        if (!a_ || !b_)
+            return;
+        (void)hipEventRecord(b_, s_);
+        Profiler &p = prof();
+        std::lock_guard<std::mutex> lk(p.mu);
+        p.pending.push_back({phase_, a_, b_});
+        a_ = b_ = nullptr;
+    }
+    ~PhaseTimer()
+    {
+        if (a_ || b_) { // abandoned (error path): recycle the events
+            Profiler &p = prof();
+            std::lock_guard<std::mutex> lk(p.mu);
+            if (a_) p.spare.push_back(a_);
+            if (b_) p.spare.push_back(b_);
+        }
+    }
+
+  private:
+    int phase_;
+    hipStream_t s_;
+    hipEvent_t a_ = nullptr, b_ = nullptr;
+};
+
+} // namespace
+
+// ---------------------------------------------------------------------------
+// the plan
+// ---------------------------------------------------------------------------
+
+struct apml_plan {
+    int B = 0, N = 0, M = 0, L = 0;
+    apml_params prm{};
+    Params kp{};
+    int device = 0;
+    hipStream_t stream = nullptr;
+    int64_t stored = 0; // stored pairs
+    Arena keep;         // everything backward and export need
+    // sparse structure (row-major order t, column-major order q)
+    int32_t *row_ptr = nullptr, *col_ptr = nullptr, *csr_col = nullptr, *csc_row = nullptr,
+            *csc_perm = nullptr;
+    uint8_t *flags = nullptr;
+    float *p_row = nullptr, *p_col = nullptr, *p0r = nullptr, *p0c = nullptr;
+    float2 *m12_row = nullptr, *m12_col = nullptr;
+    double *T_row = nullptr, *C1_row = nullptr, *g_row = nullptr;
+    double *T_col = nullptr, *C1_col = nullptr, *g_col = nullptr;
+    int32_t *pos_row = nullptr, *pos_col = nullptr;
+    uint8_t *clamp_row = nullptr, *clamp_col = nullptr;
+    double *alpha = nullptr, *beta = nullptr, *rden = nullptr, *sden = nullptr;
+    Counters *ctr = nullptr;
+};
+
+namespace {
+
+apml_status validate(const float *x, const float *y, int32_t B, int32_t N, int32_t M, int32_t d,
+                     const apml_params &p, const float *loss)
+{
+    if (!x || !y || !loss)
+        return fail(APML_ERR_INVALID_ARG, "x, y and loss must be non-NULL device pointers");
+    if (B < 1 || N < 2 || M < 2)
+        return fail(APML_ERR_INVALID_ARG, "need B >= 1, N >= 2 and M >= 2 (Eq. 1 needs K > 1)");
+    if (d != 3)
+        return fail(APML_ERR_UNSUPPORTED, "only d == 3 is supported");
+    if ((int64_t)B * N > INT32_MAX / 4 || (int64_t)B * M > INT32_MAX / 4)
+        return fail(APML_ERR_UNSUPPORTED, "B*N and B*M must stay below 2^29");
+    if (p.struct_size != 0 && p.struct_size < sizeof(apml_params))
+        return fail(APML_ERR_INVALID_ARG, "apml_params.struct_size is smaller than this library's struct");
+    if (!(p.p_min > 0.0 && p.p_min < 1.0) || !(p.p_min * N > 1.0) || !(p.p_min * M > 1.0))
+        return fail(APML_ERR_INVALID_ARG, "need 1/min(N, M) < p_min < 1 (Eq. 1 gives T > 0)");
+    if (!(p.tau >= 0.0 && p.tau <= 1.0))
+        return fail(APML_ERR_INVALID_ARG, "need 0 <= tau <= 1");
+    if (p.n_iter < 0 || p.n_iter > 100000)
+        return fail(APML_ERR_INVALID_ARG, "need 0 <= n_iter <= 100000");
+    if (!(p.delta >= 0.0) || !(p.eps_gap > 0.0) || !(p.eps_stab >= 0.0) || !(p.eps_dist >= 0.0) ||
+        !std::isfinite(p.delta) || !std::isfinite(p.eps_gap) || !std::isfinite(p.eps_stab) ||
+        !std::isfinite(p.eps_dist))
+        return fail(APML_ERR_INVALID_ARG, "need delta >= 0, eps_gap > 0, eps_stab >= 0, eps_dist >= 0, all finite");
+    return APML_OK;
+}
+
+// Eq. 1: -log((1 - p) / ((K - 1) p)).
+double log_ratio(int K, double p) { return -std::log((1.0 - p) / ((double)(K - 1) * p)); }
+
+int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+// Chunks of the broadcast range so that a dense scan has about 8 waves per
+// SIMD on 256 CUs, each chunk at least 512 points long.
+void choose_chunks(int B, int n_own, int n_bc, int *S, int *chunk)
+{
+    const int64_t waves = (int64_t)B * ceil_div(n_own, 64);
+    const int64_t target = 8192;
+    int s = (int)std::max<int64_t>(1, (target + waves - 1) / waves);
+    s = std::min(s, std::max(1, n_bc / 512));
+    int len = ceil_div(n_bc, s);
+    len = ceil_div(len, kUnroll) * kUnroll;
+    *chunk = len;
+    *S = ceil_div(n_bc, len);
+}
+
+} // namespace
+
+extern "C" {
+
+void apml_params_default(apml_params *p)
+{
+    if (!p)
+        return;
+    p->struct_size = sizeof(apml_params);
+    p->n_iter = 10;
+    p->p_min = 0.8;
+    p->tau = 1e-8;
+    p->eps_stab = 1e-8;
+    p->delta = 1e-8;
+    p->eps_gap = 1e-6;
+    p->eps_dist = 1e-12;
+}
+
+apml_status apml_plan_destroy(apml_plan *plan)
+{
+    if (!plan)
+        return APML_OK;
+    {
+        std::lock_guard<std::mutex> lk(mem().mu);
+        mem().live_plans--;
+    }
+    int prev = 0;
+    (void)hipGetDevice(&prev);
+    if (prev != plan->device)
+        (void)hipSetDevice(plan->device);
+    plan->keep.release();
+    if (prev != plan->device)
+        (void)hipSetDevice(prev);
+    delete plan;
+    return APML_OK;
+}
+
+apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, int32_t M,
+                         int32_t d, const apml_params *params, float *loss, apml_plan **plan_out,
+                         apml_stream stream)
+{
+    g_last_error.clear();
+    if (plan_out)
+        *plan_out = nullptr;
+    apml_params prm;
+    apml_params_default(&prm);
+    if (params)
+        prm = *params;
+    apml_status st = validate(x, y, B, N, M, d, prm, loss);
+    if (st != APML_OK)
+        return st;
+    hipStream_t s = (hipStream_t)stream;
+
+    apml_plan *plan = new apml_plan();
+    {
+        std::lock_guard<std::mutex> lk(mem().mu);
+        mem().live_plans++;
+    }
+    struct Guard {
+        apml_plan *p;
+        ~Guard() { apml_plan_destroy(p); }
+    } guard{plan};
+    HIP_TRY(hipGetDevice(&plan->device));
+    plan->B = B;
+    plan->N = N;
+    plan->M = M;
+    plan->L = prm.n_iter;
+    plan->prm = prm;
+    plan->stream = s;
+    plan->keep.stream = s;
+    Params &kp = plan->kp;
+    kp.p_min = prm.p_min;
+    kp.tau = prm.tau;
+    kp.eps_stab = prm.eps_stab;
+    kp.delta = prm.delta;
+    kp.eps_gap = prm.eps_gap;
+    kp.eps_dist = prm.eps_dist;
+    kp.log_inv_tau = prm.tau > 0.0 ? -std::log(prm.tau) : HUGE_VAL;
+    kp.lk_row = log_ratio(M, prm.p_min);
+    kp.lk_col = log_ratio(N, prm.p_min);
+    kp.n_iter = prm.n_iter;
+
+    const int BN = B * N, BM = B * M;
+    Arena tmp;
+    tmp.stream = s;
+    Arena &keep = plan->keep;
+
+    // ---- dense scan 1: minima -------------------------------------------
+    ScanDir rows{}, cols{};
+    rows.own = x;
+    rows.bcast = y;
+    rows.n_own = N;
+    rows.n_bc = M;
+    choose_chunks(B, N, M, &rows.S, &rows.chunk);
+    rows.owner_blocks = ceil_div(N, kBlock);
+    rows.tiles = B * rows.S * rows.owner_blocks;
+    cols.own = y;
+    cols.bcast = x;
+    cols.n_own = M;
+    cols.n_bc = N;
+    choose_chunks(B, M, N, &cols.S, &cols.chunk);
+    cols.owner_blocks = ceil_div(M, kBlock);
+    cols.tiles = B * cols.S * cols.owner_blocks;
+    rows.partial = tmp.get<float2>((size_t)rows.S * BN);
+    cols.partial = tmp.get<float2>((size_t)cols.S * BM);
+    plan->m12_row = keep.get<float2>(BN);
+    plan->m12_col = keep.get<float2>(BM);
+    float *E_row = tmp.get<float>(BN);
+    float4 *ypack = tmp.get<float4>(BM);
+    plan->ctr = keep.get<Counters>(1);
+    if (tmp.failed || keep.failed)
+        return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (statistics)");
+
+    {
+        PhaseTimer pt(PH_STATS, s);
+        launch_top2(rows, cols, B, s);
+        HIP_TRY(hipGetLastError());
+        pt.stop();
+    }
+    FinalizeDir fr{rows.partial, x, plan->m12_row, E_row, nullptr, N, rows.S, kp.lk_row};
+    FinalizeDir fc{cols.partial, y, plan->m12_col, nullptr, ypack, M, cols.S, kp.lk_col};
+    launch_finalize(fr, fc, B, kp, s);
+    HIP_TRY(hipGetLastError());
+
+    // ---- dense scan 2: candidate support ---------------------------------
+    EmitArgs ea{};
+    ea.x = x;
+    ea.ypack = ypack;
+    ea.E_row = E_row;
+    ea.B = B;
+    ea.N = N;
+    ea.M = M;
+    ea.S = rows.S;
+    ea.chunk = rows.chunk;
+    ea.owner_blocks = rows.owner_blocks;
+    {
+        const double per_row = 12.0 * (1.0 + (double)M / N);
+        int K = (int)std::ceil(per_row / ea.S);
+        K = std::max(4, std::min(64, (K + 3) / 4 * 4));
+        ea.K = K;
+    }
+    ea.slots = tmp.get<int32_t>((size_t)BN * ea.S * ea.K);
+    ea.cnt = tmp.get<int32_t>((size_t)BN * ea.S);
+    ea.col_cnt = tmp.get<int32_t>(BM);
+    ea.ovf_cap = (unsigned)std::max<int64_t>(65536, 2 * (int64_t)(BN + BM));
+    ea.ovf = tmp.get<OverflowEntry>(ea.ovf_cap);
+    ea.ctr = plan->ctr;
+    if (tmp.failed)
+        return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (support)");
+    Counters hc{};
+    for (int attempt = 0; attempt < 2; ++attempt) {
+        HIP_TRY(hipMemsetAsync(ea.col_cnt, 0, sizeof(int32_t) * BM, s));
+        HIP_TRY(hipMemsetAsync(plan->ctr, 0, sizeof(Counters), s));
+        {
+            PhaseTimer pt(PH_SUPPORT, s);
+            launch_emit(ea, s);
+            HIP_TRY(hipGetLastError());
+            pt.stop();
+        }
+        HIP_TRY(hipMemcpyAsync(&hc, plan->ctr, sizeof(Counters), hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipStreamSynchronize(s));
+        if (hc.overflow <= ea.ovf_cap)
+            break;
+        // more overflow pairs than room: enlarge and scan again
+        ea.ovf_cap = hc.overflow;
+        ea.ovf = tmp.get<OverflowEntry>(ea.ovf_cap);
+        if (tmp.failed)
+            return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (overflow)");
+    }
+    if (hc.overflow > ea.ovf_cap)
+        return fail(APML_ERR_INTERNAL, "overflow count changed between identical scans");
+    if (hc.stored > (unsigned long long)(INT32_MAX - 1))
+        return fail(APML_ERR_UNSUPPORTED, "more than 2^31 stored pairs: raise tau or lower N*M");
+    const int64_t nnz = (int64_t)hc.stored;
+    plan->stored = nnz;
+
+    // ---- sparse structure -------------------------------------------------
+    PhaseTimer pt_build(PH_BUILD, s);
+    plan->row_ptr = keep.get<int32_t>((size_t)BN + 1);
+    plan->col_ptr = keep.get<int32_t>((size_t)BM + 1);
+    const int tile = scan_tile_items();
+    ScanArray sr{ea.cnt, BN, ea.S, plan->row_ptr, nullptr, ceil_div(BN, tile)};
+    ScanArray sc{ea.col_cnt, BM, 1, plan->col_ptr, nullptr, ceil_div(BM, tile)};
+    sr.tile_sums = tmp.get<int32_t>(sr.tiles);
+    sc.tile_sums = tmp.get<int32_t>(sc.tiles);
+    plan->csr_col = keep.get<int32_t>(nnz);
+    plan->csc_row = keep.get<int32_t>(nnz);
+    plan->csc_perm = keep.get<int32_t>(nnz);
+    plan->flags = keep.get<uint8_t>(nnz);
+    plan->p_row = keep.get<float>(nnz);
+    plan->p_col = keep.get<float>(nnz);
+    plan->p0r = keep.get<float>(nnz);
+    plan->p0c = keep.get<float>(nnz);
+    int32_t *col_fill = tmp.get<int32_t>(BM);
+    int32_t *tmp_row = tmp.get<int32_t>(nnz);
+    int32_t *tmp_src = tmp.get<int32_t>(nnz);
+    int32_t *tmp_gc = tmp.get<int32_t>(nnz);
+    if (tmp.failed || keep.failed)
+        return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (sparse arrays)");
+    launch_scan(sr, sc, s);
+    HIP_TRY(hipMemsetAsync(col_fill, 0, sizeof(int32_t) * BM, s));
+    BuildArgs ba{};
+    ba.B = B;
+    ba.N = N;
+    ba.M = M;
+    ba.S = ea.S;
+    ba.K = ea.K;
+    ba.slots = ea.slots;
+    ba.cnt = ea.cnt;
+    ba.row_ptr = plan->row_ptr;
+    ba.col_ptr = plan->col_ptr;
+    ba.ovf = ea.ovf;
+    ba.n_ovf = (int)hc.overflow;
+    ba.csr_col = plan->csr_col;
+    ba.col_fill = col_fill;
+    ba.tmp_row = tmp_row;
+    ba.tmp_src = tmp_src;
+    ba.tmp_gc = tmp_gc;
+    ba.csc_row = plan->csc_row;
+    ba.csc_perm = plan->csc_perm;
+    ba.nnz = nnz;
+    launch_build(ba, s);
+    HIP_TRY(hipGetLastError());
+    pt_build.stop();
+
+    // ---- temperatures, softmaxes, P0 ---------------------------------------
+    plan->T_row = keep.get<double>(BN);
+    plan->C1_row = keep.get<double>(BN);
+    plan->g_row = keep.get<double>(BN);
+    plan->T_col = keep.get<double>(BM);
+    plan->C1_col = keep.get<double>(BM);
+    plan->g_col = keep.get<double>(BM);
+    plan->pos_row = keep.get<int32_t>(2 * (size_t)BN);
+    plan->pos_col = keep.get<int32_t>(2 * (size_t)BM);
+    plan->clamp_row = keep.get<uint8_t>(BN);
+    plan->clamp_col = keep.get<uint8_t>(BM);
+    const int L = prm.n_iter;
+    plan->alpha = keep.get<double>((size_t)(L + 1) * BN);
+    plan->beta = keep.get<double>((size_t)(L + 1) * BM);
+    plan->rden = keep.get<double>((size_t)std::max(L, 1) * BN);
+    plan->sden = keep.get<double>((size_t)std::max(L, 1) * BM);
+    double *loss_rows = tmp.get<double>(BN);
+    if (tmp.failed || keep.failed)
+        return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (plan)");
+    {
+        PhaseTimer pt(PH_SOFTMAX, s);
+        SoftmaxArgs sa{};
+        sa.x = x;
+        sa.y = y;
+        sa.B = B;
+        sa.N = N;
+        sa.M = M;
+        sa.row_ptr = plan->row_ptr;
+        sa.col_ptr = plan->col_ptr;
+        sa.csr_col = plan->csr_col;
+        sa.csc_row = plan->csc_row;
+        sa.csc_perm = plan->csc_perm;
+        sa.m12_row = plan->m12_row;
+        sa.m12_col = plan->m12_col;
+        sa.flags = plan->flags;
+        sa.p_row = plan->p_row;
+        sa.p_col = plan->p_col;
+        sa.p0r = plan->p0r;
+        sa.p0c = plan->p0c;
+        sa.T_row = plan->T_row;
+        sa.C1_row = plan->C1_row;
+        sa.g_row = plan->g_row;
+        sa.T_col = plan->T_col;
+        sa.C1_col = plan->C1_col;
+        sa.g_col = plan->g_col;
+        sa.pos_row = plan->pos_row;
+        sa.pos_col = plan->pos_col;
+        sa.clamp_row = plan->clamp_row;
+        sa.clamp_col = plan->clamp_col;
+        sa.ctr = plan->ctr;
+        launch_softmax(sa, kp, s);
+        HIP_TRY(hipGetLastError());
+        pt.stop();
+    }
+
+    // ---- Sinkhorn (Eq. 3, Eq. 4) -------------------------------------------
+    SinkhornArgs ka{B, N, M, L, plan->row_ptr, plan->col_ptr, plan->csr_col, plan->csc_row,
+                    plan->p0r, plan->p0c, plan->alpha, plan->beta, plan->rden, plan->sden};
+    {
+        PhaseTimer pt(PH_SINKHORN, s);
+        launch_sinkhorn_init(ka, s);
+        for (int l = 1; l <= L; ++l)
+            launch_sinkhorn_step(ka, l, prm.eps_stab, s);
+        HIP_TRY(hipGetLastError());
+        pt.stop();
+    }
+
+    // ---- loss --------------------------------------------------------------
+    {
+        PhaseTimer pt(PH_LOSS, s);
+        LossArgs la{x, y, B, N, M, plan->row_ptr, plan->csr_col, plan->p0r,
+                    plan->alpha + (size_t)L * BN, plan->beta + (size_t)L * BM, loss_rows, loss};
+        launch_loss(la, s);
+        HIP_TRY(hipGetLastError());
+        pt.stop();
+    }
+    tmp.release();
+    if (plan_out) {
+        guard.p = nullptr;
+        *plan_out = plan;
+    }
+    return APML_OK;
+}
+
+apml_status apml_backward(apml_plan *plan, const float *x, const float *y, const float *grad_loss,
+                          float *grad_x, float *grad_y, apml_stream stream)
+{
+    g_last_error.clear();
+    if (!plan || !x || !y || !grad_loss || !grad_x)
+        return fail(APML_ERR_INVALID_ARG, "plan, x, y, grad_loss and grad_x must be non-NULL");
+    hipStream_t s = (hipStream_t)stream;
+    const int B = plan->B, N = plan->N, M = plan->M, L = plan->L;
+    const int64_t nnz = plan->stored;
+    Arena tmp;
+    tmp.stream = s;
+    BackwardArgs a{};
+    a.x = x;
+    a.y = y;
+    a.grad_loss = grad_loss;
+    a.grad_x = grad_x;
+    a.grad_y = grad_y;
+    a.B = B;
+    a.N = N;
+    a.M = M;
+    a.L = L;
+    a.row_ptr = plan->row_ptr;
+    a.col_ptr = plan->col_ptr;
+    a.csr_col = plan->csr_col;
+    a.csc_row = plan->csc_row;
+    a.csc_perm = plan->csc_perm;
+    a.flags = plan->flags;
+    a.p_row = plan->p_row;
+    a.p_col = plan->p_col;
+    a.p0r = plan->p0r;
+    a.p0c = plan->p0c;
+    a.alpha = plan->alpha;
+    a.beta = plan->beta;
+    a.rden = plan->rden;
+    a.sden = plan->sden;
+    a.T_row = plan->T_row;
+    a.C1_row = plan->C1_row;
+    a.g_row = plan->g_row;
+    a.T_col = plan->T_col;
+    a.C1_col = plan->C1_col;
+    a.g_col = plan->g_col;
+    a.pos_row = plan->pos_row;
+    a.pos_col = plan->pos_col;
+    a.clamp_row = plan->clamp_row;
+    a.clamp_col = plan->clamp_col;
+    a.adj = tmp.get<double>(nnz);
+    a.cbar = tmp.get<double>(nnz);
+    if (tmp.failed)
+        return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (backward)");
+    {
+        PhaseTimer pt(PH_BWD_SINK, s);
+        for (int l = L; l >= 1; --l)
+            launch_bwd_sinkhorn_step(a, l, s);
+        HIP_TRY(hipGetLastError());
+        pt.stop();
+    }
+    {
+        PhaseTimer pt(PH_BWD_SOFTMAX, s);
+        launch_bwd_softmax(a, plan->kp, s);
+        HIP_TRY(hipGetLastError());
+        pt.stop();
+    }
+    tmp.release();
+    return APML_OK;
+}
+
+apml_status apml_plan_get_info(const apml_plan *plan, apml_plan_info *info)
+{
+    if (!plan || !info)
+        return fail(APML_ERR_INVALID_ARG, "plan and info must be non-NULL");
+    info->B = plan->B;
+    info->N = plan->N;
+    info->M = plan->M;
+    info->n_iter = plan->L;
+    info->stored_pairs = plan->stored;
+    info->bytes = plan->keep.bytes;
+    return APML_OK;
+}
+
+apml_status apml_plan_nnz(const apml_plan *plan, int64_t *nnz)
+{
+    if (!plan || !nnz)
+        return fail(APML_ERR_INVALID_ARG, "plan and nnz must be non-NULL");
+    hipStream_t s = plan->stream;
+    Arena tmp;
+    tmp.stream = s;
+    unsigned long long *d = tmp.get<unsigned long long>(plan->B);
+    if (tmp.failed)
+        return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed");
+    launch_count_support(plan->row_ptr, plan->flags, plan->B, plan->N, d, s);
+    HIP_TRY(hipGetLastError());
+    std::vector<unsigned long long> h(plan->B);
+    Counters hc{};
+    HIP_TRY(hipMemcpyAsync(h.data(), d, sizeof(unsigned long long) * plan->B, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(&hc, plan->ctr, sizeof(Counters), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    for (int b = 0; b < plan->B; ++b)
+        nnz[b] = (int64_t)h[b];
+    if (hc.error)
+        return fail(APML_ERR_INTERNAL, "a row or column minimum was not found among its stored pairs");
+    return APML_OK;
+}
+
+} // extern "C"
+
+namespace {
+
+template <typename T>
+apml_status copy_range(std::vector<T> &dst, const T *src, int64_t begin, int64_t count, hipStream_t s)
+{
+    dst.resize((size_t)std::max<int64_t>(count, 0));
+    if (count > 0)
+        HIP_TRY(hipMemcpyAsync(dst.data(), src + begin, sizeof(T) * count, hipMemcpyDeviceToHost, s));
+    return APML_OK;
+}
+
+#define TRY(expr)                                                                              \
+    do {                                                                                       \
+        apml_status st_ = (expr);                                                              \
+        if (st_ != APML_OK)                                                                    \
+            return st_;                                                                        \
+    } while (0)
+
+} // namespace
+
+extern "C" {
+
+apml_status apml_plan_export(const apml_plan *plan, int32_t b, int64_t capacity, int32_t *oi,
+                             int32_t *oj, uint8_t *oflags, float *op_row, float *op_col, float *op0,
+                             float *ov)
+{
+    if (!plan)
+        return fail(APML_ERR_INVALID_ARG, "plan must be non-NULL");
+    if (b < 0 || b >= plan->B)
+        return fail(APML_ERR_INVALID_ARG, "sample index out of range");
+    const int N = plan->N, M = plan->M, L = plan->L;
+    hipStream_t s = plan->stream;
+    std::vector<int32_t> rp, cp;
+    TRY(copy_range(rp, plan->row_ptr, (int64_t)b * N, N + 1, s));
+    TRY(copy_range(cp, plan->col_ptr, (int64_t)b * M, M + 1, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    const int64_t t0 = rp[0], t1 = rp[N], q0 = cp[0], q1 = cp[M];
+    std::vector<int32_t> col, perm;
+    std::vector<uint8_t> fl;
+    std::vector<float> prow, pcol, p0;
+    std::vector<double> al, be;
+    TRY(copy_range(col, plan->csr_col, t0, t1 - t0, s));
+    TRY(copy_range(fl, plan->flags, t0, t1 - t0, s));
+    TRY(copy_range(prow, plan->p_row, t0, t1 - t0, s));
+    TRY(copy_range(p0, plan->p0r, t0, t1 - t0, s));
+    TRY(copy_range(perm, plan->csc_perm, q0, q1 - q0, s));
+    TRY(copy_range(pcol, plan->p_col, q0, q1 - q0, s));
+    const size_t BN = (size_t)plan->B * N, BM = (size_t)plan->B * M;
+    TRY(copy_range(al, plan->alpha, (int64_t)(L * BN + (size_t)b * N), N, s));
+    TRY(copy_range(be, plan->beta, (int64_t)(L * BM + (size_t)b * M), M, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    std::vector<float> pcol_rm(t1 - t0, 0.0f);
+    for (int64_t q = 0; q < q1 - q0; ++q)
+        pcol_rm[perm[q] - t0] = pcol[q];
+    int64_t n = 0;
+    for (int i = 0; i < N; ++i)
+        for (int64_t t = rp[i]; t < rp[i + 1]; ++t) {
+            const int64_t k = t - t0;
+            if (!fl[k])
+                continue;
+            if (n >= capacity)
+                return fail(APML_ERR_INVALID_ARG, "capacity is smaller than the sample's support");
+            const int j = col[k];
+            if (oi) oi[n] = i;
+            if (oj) oj[n] = j;
+            if (oflags) oflags[n] = fl[k];
+            if (op_row) op_row[n] = prow[k];
+            if (op_col) op_col[n] = pcol_rm[k];
+            if (op0) op0[n] = p0[k];
+            if (ov) ov[n] = (float)(al[i] * (double)p0[k] * be[j]);
+            ++n;
+        }
+    return APML_OK;
+}
+
+apml_status apml_plan_export_stats(const apml_plan *plan, int32_t b, double *T_row, int32_t *j1,
+                                   int32_t *j2, uint8_t *row_clamped, double *T_col, int32_t *i1,
+                                   int32_t *i2, uint8_t *col_clamped)
+{
+    if (!plan)
+        return fail(APML_ERR_INVALID_ARG, "plan must be non-NULL");
+    if (b < 0 || b >= plan->B)
+        return fail(APML_ERR_INVALID_ARG, "sample index out of range");
+    const int N = plan->N, M = plan->M;
+    hipStream_t s = plan->stream;
+    std::vector<double> tr, tc;
+    std::vector<int32_t> pr, pc, col, row;
+    std::vector<uint8_t> cr, cc;
+    TRY(copy_range(tr, plan->T_row, (int64_t)b * N, N, s));
+    TRY(copy_range(tc, plan->T_col, (int64_t)b * M, M, s));
+    TRY(copy_range(pr, plan->pos_row, 2 * (int64_t)b * N, 2 * (int64_t)N, s));
+    TRY(copy_range(pc, plan->pos_col, 2 * (int64_t)b * M, 2 * (int64_t)M, s));
+    TRY(copy_range(cr, plan->clamp_row, (int64_t)b * N, N, s));
+    TRY(copy_range(cc, plan->clamp_col, (int64_t)b * M, M, s));
+    TRY(copy_range(col, plan->csr_col, 0, plan->stored, s));
+    TRY(copy_range(row, plan->csc_row, 0, plan->stored, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    auto at = [](const std::vector<int32_t> &v, int32_t k) { return k >= 0 && (size_t)k < v.size() ? v[k] : -1; };
+    for (int i = 0; i < N; ++i) {
+        if (T_row) T_row[i] = tr[i];
+        if (j1) j1[i] = at(col, pr[2 * i]);
+        if (j2) j2[i] = at(col, pr[2 * i + 1]);
+        if (row_clamped) row_clamped[i] = cr[i];
+    }
+    for (int j = 0; j < M; ++j) {
+        if (T_col) T_col[j] = tc[j];
+        if (i1) i1[j] = at(row, pc[2 * j]);
+        if (i2) i2[j] = at(row, pc[2 * j + 1]);
+        if (col_clamped) col_clamped[j] = cc[j];
+    }
+    return APML_OK;
+}
+
+apml_status apml_set_allocator(apml_alloc_fn alloc, apml_free_fn free_fn, void *user)
+{
+    if ((alloc == nullptr) != (free_fn == nullptr))
+        return fail(APML_ERR_INVALID_ARG, "alloc and free must both be set or both be NULL");
+    Memory &m = mem();
+    std::lock_guard<std::mutex> lk(m.mu);
+    if (m.live_plans > 0)
+        return fail(APML_ERR_INVALID_ARG, "cannot change the allocator while plans are alive");
+    m.user_alloc = alloc;
+    m.user_free = free_fn;
+    m.user = user;
+    return APML_OK;
+}
+
+apml_status apml_get_memory_stats(apml_memory_stats *stats)
+{
+    if (!stats)
+        return fail(APML_ERR_INVALID_ARG, "stats must be non-NULL");
+    Memory &m = mem();
+    std::lock_guard<std::mutex> lk(m.mu);
+    stats->in_use = m.in_use;
+    stats->peak_in_use = m.peak;
+    stats->reserved = m.reserved;
+    return APML_OK;
+}
+
+apml_status apml_reset_peak_memory(void)
+{
+    Memory &m = mem();
+    std::lock_guard<std::mutex> lk(m.mu);
+    m.peak = m.in_use;
+    return APML_OK;
+}
+
+apml_status apml_release_cached_memory(void)
+{
+    Memory &m = mem();
+    std::lock_guard<std::mutex> lk(m.mu);
+    if (m.free_blocks.empty())
+        return APML_OK;
+    HIP_TRY(hipDeviceSynchronize());
+    for (auto &kv : m.free_blocks)
+        for (auto &blk : kv.second) {
+            (void)hipFree(blk.second);
+            m.reserved -= (int64_t)m.block_size[blk.second];
+            m.block_size.erase(blk.second);
+        }
+    m.free_blocks.clear();
+    return APML_OK;
+}
+
+apml_status apml_profile_enable(int32_t on)
+{
+    Profiler &p = prof();
+    std::lock_guard<std::mutex> lk(p.mu);
+    p.on = on != 0;
+    return APML_OK;
+}
+
+apml_status apml_profile_reset(void)
+{
+    Profiler &p = prof();
+    std::lock_guard<std::mutex> lk(p.mu);
+    for (auto &e : p.pending) {
+        (void)hipEventSynchronize(e.b);
+        p.spare.push_back(e.a);
+        p.spare.push_back(e.b);
+    }
+    p.pending.clear();
+    for (int k = 0; k < APML_N_PHASES; ++k) {
+        p.total[k] = 0.0;
+        p.count[k] = 0;
+    }
+    return APML_OK;
+}
+
+apml_status apml_profile_read(int32_t n, double *total_ms, int64_t *count)
+{
+    if (n < 0 || n > APML_N_PHASES || (n > 0 && (!total_ms || !count)))
+        return fail(APML_ERR_INVALID_ARG, "need 0 <= n <= APML_N_PHASES and output arrays");
+    Profiler &p = prof();
+    std::lock_guard<std::mutex> lk(p.mu);
+    for (auto &e : p.pending) {
+        HIP_TRY(hipEventSynchronize(e.b));
+        float ms = 0.0f;
+        HIP_TRY(hipEventElapsedTime(&ms, e.a, e.b));
+        p.total[e.phase] += ms;
+        p.count[e.phase] += 1;
+        p.spare.push_back(e.a);
+        p.spare.push_back(e.b);
+    }
+    p.pending.clear();
+    for (int k = 0; k < n; ++k) {
+        total_ms[k] = p.total[k];
+        count[k] = p.count[k];
+    }
+    return APML_OK;
+}
+
+const char *apml_phase_name(int32_t phase)
+{
+    if (phase < 0 || phase >= APML_N_PHASES)
+        return "";
+    return kPhaseNames[phase];
+}
+
+const char *apml_status_string(apml_status status)
+{
+    switch (status) {
+    case APML_OK: return "ok";
+    case APML_ERR_INVALID_ARG: return "invalid argument";
+    case APML_ERR_UNSUPPORTED: return "unsupported";
+    case APML_ERR_OUT_OF_MEMORY: return "out of memory";
+    case APML_ERR_DEVICE: return "device error";
+    case APML_ERR_INTERNAL: return "internal error";
+    }
+    return "unknown status";
+}
+
+const char *apml_last_error(void) { return g_last_error.c_str(); }
+
+int32_t apml_version(void) { return APML_VERSION; }
+
+} // extern "C"

@@ -1,0 +1,216 @@
+"""GPU parity: the C-ABI path (libapml on the MI355X) against the CPU oracle,
+element by element on seeded inputs. Tolerances are in tests/_parity.py."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2512_19743_amd as apml
+from workloads import batch, config, custom
+
+from ._parity import compare_sample, note, oracle_params, rel_norm, run_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    apml.load()
+
+
+def _check_batch(X, Y, label, samples=None, check_grad_y=True, **prm):
+    note(f"{label}: B={X.shape[0]} N={X.shape[1]} M={Y.shape[1]} {prm}")
+    g = run_gpu(X, Y, **prm)
+    tau = prm.get("tau", 1e-8)
+    out = []
+    for b in (range(X.shape[0]) if samples is None else samples):
+        ref = oracle.run_sample(X[b], Y[b], oracle_params(**prm), grad=True)
+        out.append(compare_sample(g, b, X[b], Y[b], ref, tau, check_grad_y=check_grad_y))
+    return g, out
+
+
+def test_tiny_config_full():
+    w = config(1)
+    X, Y = batch(w)
+    _, res = _check_batch(X, Y, "config 1", n_iter=w.n_iter)
+    assert all(r["flips"] == 0 for r in res), res
+
+
+def test_ragged_unequal_sizes():
+    # sizes that are not multiples of the wave, the workgroup or the chunk
+    X, Y = custom(21, 3, 300, 517, reference="sphere", prediction="uniform_cube")
+    _check_batch(X, Y, "ragged", n_iter=7)
+
+
+def test_unequal_cardinality_primitives():
+    X, Y = custom(22, 2, 700, 2100, reference="primitives", prediction="uniform_cube")
+    _check_batch(X, Y, "unequal", n_iter=10)
+
+
+def test_minimum_size():
+    X, Y = custom(23, 4, 2, 2, sigma=0.1)
+    _check_batch(X, Y, "N=M=2", n_iter=10)
+
+
+def test_single_sample_odd_shapes():
+    X, Y = custom(24, 1, 65, 3, reference="sphere", prediction="uniform_cube")
+    _check_batch(X, Y, "N=65 M=3", n_iter=3)
+
+
+@pytest.mark.parametrize("L", [0, 1, 20])
+def test_iteration_counts(L):
+    X, Y = custom(25, 2, 200, 180, sigma=0.05)
+    _check_batch(X, Y, f"L={L}", n_iter=L)
+
+
+def test_dense_threshold_zero_with_overflow():
+    # tau = 0 keeps every pair: every row overflows its slots and the overflow
+    # list itself has to grow once (retry path)
+    X, Y = custom(26, 1, 400, 400, sigma=0.05)
+    g, res = _check_batch(X, Y, "tau=0", tau=0.0, n_iter=5)
+    assert res[0]["nnz_gpu"] == 400 * 400
+
+
+def test_threshold_one_is_half_chamfer():
+    X, Y = custom(27, 2, 150, 170, sigma=0.05)
+    g, _ = _check_batch(X, Y, "tau=1", tau=1.0, n_iter=0)
+    for b in range(2):
+        D = np.linalg.norm(X[b].astype(np.float64)[:, None] - Y[b].astype(np.float64)[None], axis=-1)
+        assert g["loss"][b] == pytest.approx(0.5 * (D.min(1).sum() + D.min(0).sum()), rel=1e-5)
+
+
+@pytest.mark.parametrize("p_min", [0.5, 0.95])
+def test_other_p_min(p_min):
+    X, Y = custom(28, 2, 256, 256, sigma=0.03)
+    _check_batch(X, Y, f"p_min={p_min}", p_min=p_min)
+
+
+def test_duplicates_ties_and_clamps():
+    X, Y = custom(29, 2, 128, 100, sigma=0.05)
+    Y = np.ascontiguousarray(np.concatenate([Y, Y[:, :30]], axis=1))  # exact ties
+    X = np.ascontiguousarray(np.concatenate([X, X[:, :10]], axis=1))
+    g, _ = _check_batch(X, Y, "ties")
+    st = g["plan"].export_stats(0)
+    assert st["clamp_row"].any() and st["clamp_col"].any()
+
+
+def test_identical_clouds():
+    _, Y = custom(30, 2, 300, 300, sigma=0.05)
+    _check_batch(Y.copy(), Y, "x == y")
+
+
+def test_upstream_gradient_scaling():
+    X, Y = custom(31, 3, 128, 128, sigma=0.05)
+    gbar = np.array([1.0, -2.5, 0.0], np.float32)
+    note("upstream gradient")
+    g = run_gpu(X, Y, gbar=gbar)
+    for b in range(3):
+        ref = oracle.run_sample(X[b], Y[b], oracle_params(), grad=True, gbar=float(gbar[b]))
+        if gbar[b] == 0:
+            assert np.all(g["gx"][b] == 0)
+        else:
+            assert rel_norm(g["gx"][b], ref.grad_x) <= 1e-4
+
+
+def test_deterministic_bitwise():
+    X, Y = batch(config(1))
+    note("determinism")
+    a = run_gpu(X, Y)
+    b = run_gpu(X, Y)
+    assert np.array_equal(a["loss"], b["loss"])
+    assert np.array_equal(a["gx"], b["gx"]) and np.array_equal(a["gy"], b["gy"])
+
+
+def test_autograd_wrapper_mean_reduction():
+    X, Y = custom(32, 4, 96, 80, sigma=0.05)
+    note("autograd wrapper")
+    x = torch.from_numpy(X).cuda().requires_grad_(True)
+    y = torch.from_numpy(Y).cuda().requires_grad_(True)
+    loss = apml.apml_loss(x, y, reduction="mean")
+    loss.backward()
+    ref_l, ref_gx, ref_gy = oracle.run_batch(X, Y, oracle_params(), grad=True)
+    assert loss.item() == pytest.approx(ref_l.mean(), rel=1e-5)
+    assert rel_norm(x.grad.cpu().numpy().astype(np.float64), ref_gx / 4) <= 1e-4
+    assert rel_norm(y.grad.cpu().numpy().astype(np.float64), ref_gy / 4) <= 1e-4
+
+
+def test_rejects_bad_input_on_gpu():
+    x = torch.zeros(2, 8, 3, device="cuda")
+    with pytest.raises(apml.ApmlError):
+        apml.apml_forward(x, torch.zeros(2, 1, 3, device="cuda"))
+    with pytest.raises(ValueError):
+        apml.apml_forward(x.double(), x.double())
+
+
+def test_plan_reports_and_memory_returns():
+    X, Y = custom(33, 2, 256, 256, sigma=0.05)
+    note("plan info")
+    before = apml.apml_get_memory_stats()["in_use"]
+    g = run_gpu(X, Y)
+    info = g["plan"].info()
+    assert info.B == 2 and info.N == 256 and info.stored_pairs >= g["plan"].nnz().sum()
+    assert apml.apml_get_memory_stats()["in_use"] - before == info.bytes
+    g["plan"].close()
+    assert apml.apml_get_memory_stats()["in_use"] == before
+
+
+# ---------------------------------------------------------------------------
+# full-size configurations, in the launch configuration the benchmark times
+# ---------------------------------------------------------------------------
+
+def test_config2_full_batch():
+    w = config(2)
+    X, Y = batch(w)
+    _, res = _check_batch(X, Y, "config 2", n_iter=w.n_iter)
+    note(f"config 2 nnz per sample: {[r['nnz_gpu'] for r in res[:4]]} flips {sum(r['flips'] for r in res)}")
+
+
+@pytest.mark.parametrize("cfg", [3, 4])
+def test_large_configs_one_sample_exact(cfg):
+    # the whole batch runs on the GPU; sample 0 is checked against a full oracle run
+    w = config(cfg)
+    X, Y = batch(w)
+    _check_batch(X, Y, f"config {cfg}", samples=[0], n_iter=w.n_iter)
+
+
+def test_config5_sampled_owners_and_invariants():
+    w = config(5)
+    X, Y = batch(w)
+    note("config 5")
+    g = run_gpu(X, Y, n_iter=w.n_iter)
+    plan = g["plan"]
+    nnz = plan.nnz()
+    prm = oracle_params(n_iter=w.n_iter)
+    rng = np.random.default_rng(5)
+    for b in range(w.B):
+        assert np.isfinite(g["loss"][b]) and g["loss"][b] > 0
+        # translation invariance of the loss: the gradients sum to zero
+        scale = np.abs(g["gx"][b]).sum() + np.abs(g["gy"][b]).sum()
+        assert np.abs(g["gx"][b].sum(0) + g["gy"][b].sum(0)).max() <= 1e-4 * scale
+    for b in (0, w.B - 1):
+        ex = plan.export(b)
+        st = plan.export_stats(b)
+        # P0 has mass (N + M)/2: every row of P_row and every column of P_col sums to 1
+        assert ex["p0"].astype(np.float64).sum() == pytest.approx((w.N + w.M) / 2, rel=1e-5)
+        assert len(ex["i"]) == nnz[b]
+        rows = rng.choice(w.N, 48, replace=False)
+        ref = oracle.owner_stats(X[b], Y[b], rows, prm)
+        np.testing.assert_array_equal(st["j1"][rows], ref["k1"])
+        np.testing.assert_array_equal(st["j2"][rows], ref["k2"])
+        np.testing.assert_allclose(st["T_row"][rows], ref["T"], rtol=1e-12)
+        for r in rows[:16]:
+            idx, s, p = oracle.owner_support(X[b], Y[b], int(r), prm)
+            sel = (ex["i"] == r) & ((ex["flags"] & 1) > 0)
+            np.testing.assert_array_equal(ex["j"][sel], idx)
+            np.testing.assert_allclose(ex["p_row"][sel], p, rtol=2e-6)
+        cols = rng.choice(w.M, 32, replace=False)
+        refc = oracle.owner_stats(Y[b], X[b], cols, prm)
+        np.testing.assert_array_equal(st["i1"][cols], refc["k1"])
+        np.testing.assert_allclose(st["T_col"][cols], refc["T"], rtol=1e-12)
+        for c in cols[:12]:
+            idx, s, p = oracle.owner_support(Y[b], X[b], int(c), prm)
+            sel = (ex["j"] == c) & ((ex["flags"] & 2) > 0)
+            np.testing.assert_array_equal(ex["i"][sel], idx)
+            np.testing.assert_allclose(ex["p_col"][sel], p, rtol=2e-6)
