@@ -258,20 +258,10 @@ struct apml_plan {
     Params kp{};
     int device = 0;
     hipStream_t stream = nullptr;
-    int64_t stored = 0; // stored pairs
+    int64_t stored = 0;     // stored pairs
+    int64_t max_sample = 0; // stored pairs of the largest sample
     Arena keep;         // everything backward and export need
-    // sparse structure (row-major order t, column-major order q)
-    int32_t *row_ptr = nullptr, *col_ptr = nullptr, *csr_col = nullptr, *csc_row = nullptr,
-            *csc_perm = nullptr;
-    uint8_t *flags = nullptr;
-    float *p_row = nullptr, *p_col = nullptr, *p0r = nullptr, *p0c = nullptr;
-    float2 *m12_row = nullptr, *m12_col = nullptr;
-    double *T_row = nullptr, *C1_row = nullptr, *g_row = nullptr;
-    double *T_col = nullptr, *C1_col = nullptr, *g_col = nullptr;
-    int32_t *pos_row = nullptr, *pos_col = nullptr;
-    uint8_t *clamp_row = nullptr, *clamp_col = nullptr;
-    double *alpha = nullptr, *beta = nullptr, *rden = nullptr, *sden = nullptr;
-    Counters *ctr = nullptr;
+    DevPlan dv{};       // device arrays (x, y and the backward fields are set per call)
 };
 
 namespace {
@@ -384,10 +374,11 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         ~Guard() { apml_plan_destroy(p); }
     } guard{plan};
     HIP_TRY(hipGetDevice(&plan->device));
+    const int L = prm.n_iter;
     plan->B = B;
     plan->N = N;
     plan->M = M;
-    plan->L = prm.n_iter;
+    plan->L = L;
     plan->prm = prm;
     plan->stream = s;
     plan->keep.stream = s;
@@ -401,12 +392,20 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     kp.log_inv_tau = prm.tau > 0.0 ? -std::log(prm.tau) : HUGE_VAL;
     kp.lk_row = log_ratio(M, prm.p_min);
     kp.lk_col = log_ratio(N, prm.p_min);
-    kp.n_iter = prm.n_iter;
+    kp.n_iter = L;
 
     const int BN = B * N, BM = B * M;
     Arena tmp;
     tmp.stream = s;
     Arena &keep = plan->keep;
+    DevPlan &dv = plan->dv;
+    dv.B = B;
+    dv.N = N;
+    dv.M = M;
+    dv.L = L;
+    dv.x = x;
+    dv.y = y;
+    dv.loss = loss;
 
     // ---- dense scan 1: minima -------------------------------------------
     ScanDir rows{}, cols{};
@@ -426,11 +425,16 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     cols.tiles = B * cols.S * cols.owner_blocks;
     rows.partial = tmp.get<float2>((size_t)rows.S * BN);
     cols.partial = tmp.get<float2>((size_t)cols.S * BM);
-    plan->m12_row = keep.get<float2>(BN);
-    plan->m12_col = keep.get<float2>(BM);
+    dv.m12_row = keep.get<float2>(BN);
+    dv.m12_col = keep.get<float2>(BM);
     float *E_row = tmp.get<float>(BN);
     float4 *ypack = tmp.get<float4>(BM);
-    plan->ctr = keep.get<Counters>(1);
+    dv.ctr = keep.get<Counters>(1);
+    BuildArgs ba{};
+    ba.col_cnt = tmp.get<int32_t>(BM);
+    ba.col_fill = tmp.get<int32_t>(BM);
+    dv.row_ptr = keep.get<int32_t>((size_t)BN + 1);
+    dv.col_ptr = keep.get<int32_t>((size_t)BM + 1);
     if (tmp.failed || keep.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (statistics)");
 
@@ -440,9 +444,9 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         HIP_TRY(hipGetLastError());
         pt.stop();
     }
-    FinalizeDir fr{rows.partial, x, plan->m12_row, E_row, nullptr, N, rows.S, kp.lk_row};
-    FinalizeDir fc{cols.partial, y, plan->m12_col, nullptr, ypack, M, cols.S, kp.lk_col};
-    launch_finalize(fr, fc, B, kp, s);
+    FinalizeDir fr{rows.partial, x, dv.m12_row, E_row, nullptr, nullptr, nullptr, N, rows.S, kp.lk_row};
+    FinalizeDir fc{cols.partial, y, dv.m12_col, nullptr, ypack, ba.col_cnt, ba.col_fill, M, cols.S, kp.lk_col};
+    launch_finalize(fr, fc, B, kp, dv.ctr, s); // also clears the counters
     HIP_TRY(hipGetLastError());
 
     // ---- dense scan 2: candidate support ---------------------------------
@@ -464,27 +468,35 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     }
     ea.slots = tmp.get<int32_t>((size_t)BN * ea.S * ea.K);
     ea.cnt = tmp.get<int32_t>((size_t)BN * ea.S);
-    ea.col_cnt = tmp.get<int32_t>(BM);
     ea.ovf_cap = (unsigned)std::max<int64_t>(65536, 2 * (int64_t)(BN + BM));
     ea.ovf = tmp.get<OverflowEntry>(ea.ovf_cap);
-    ea.ctr = plan->ctr;
+    ea.ctr = dv.ctr;
+    const int tile = scan_tile_items();
+    ScanArray sr{ea.cnt, BN, ea.S, dv.row_ptr, tmp.get<int32_t>(ceil_div(BN, tile)), ceil_div(BN, tile)};
+    if (tmp.failed)
+        return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (support)");
+    int32_t *offsets_dev = tmp.get<int32_t>((size_t)B + 1);
+    std::vector<int32_t> offsets((size_t)B + 1);
     if (tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (support)");
     Counters hc{};
     for (int attempt = 0; attempt < 2; ++attempt) {
-        HIP_TRY(hipMemsetAsync(ea.col_cnt, 0, sizeof(int32_t) * BM, s));
-        HIP_TRY(hipMemsetAsync(plan->ctr, 0, sizeof(Counters), s));
+        if (attempt > 0)
+            HIP_TRY(hipMemsetAsync(dv.ctr, 0, sizeof(Counters), s));
         {
             PhaseTimer pt(PH_SUPPORT, s);
             launch_emit(ea, s);
             HIP_TRY(hipGetLastError());
             pt.stop();
         }
-        HIP_TRY(hipMemcpyAsync(&hc, plan->ctr, sizeof(Counters), hipMemcpyDeviceToHost, s));
+        launch_scan(sr, s); // row offsets, while the host waits for the count
+        launch_sample_offsets(dv.row_ptr, B, N, offsets_dev, s);
+        HIP_TRY(hipMemcpyAsync(&hc, dv.ctr, sizeof(Counters), hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipMemcpyAsync(offsets.data(), offsets_dev, sizeof(int32_t) * (B + 1), hipMemcpyDeviceToHost, s));
         HIP_TRY(hipStreamSynchronize(s));
         if (hc.overflow <= ea.ovf_cap)
             break;
-        // more overflow pairs than room: enlarge and scan again
+        // more overflow pairs than room: enlarge the list and scan again
         ea.ovf_cap = hc.overflow;
         ea.ovf = tmp.get<OverflowEntry>(ea.ovf_cap);
         if (tmp.failed)
@@ -496,130 +508,76 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         return fail(APML_ERR_UNSUPPORTED, "more than 2^31 stored pairs: raise tau or lower N*M");
     const int64_t nnz = (int64_t)hc.stored;
     plan->stored = nnz;
+    if (offsets[B] != nnz)
+        return fail(APML_ERR_INTERNAL, "row offsets disagree with the emitted pair count");
+    for (int b = 0; b < B; ++b)
+        plan->max_sample = std::max<int64_t>(plan->max_sample, offsets[b + 1] - offsets[b]);
+    dv.nnz = nnz;
 
     // ---- sparse structure -------------------------------------------------
     PhaseTimer pt_build(PH_BUILD, s);
-    plan->row_ptr = keep.get<int32_t>((size_t)BN + 1);
-    plan->col_ptr = keep.get<int32_t>((size_t)BM + 1);
-    const int tile = scan_tile_items();
-    ScanArray sr{ea.cnt, BN, ea.S, plan->row_ptr, nullptr, ceil_div(BN, tile)};
-    ScanArray sc{ea.col_cnt, BM, 1, plan->col_ptr, nullptr, ceil_div(BM, tile)};
-    sr.tile_sums = tmp.get<int32_t>(sr.tiles);
-    sc.tile_sums = tmp.get<int32_t>(sc.tiles);
-    plan->csr_col = keep.get<int32_t>(nnz);
-    plan->csc_row = keep.get<int32_t>(nnz);
-    plan->csc_perm = keep.get<int32_t>(nnz);
-    plan->flags = keep.get<uint8_t>(nnz);
-    plan->p_row = keep.get<float>(nnz);
-    plan->p_col = keep.get<float>(nnz);
-    plan->p0r = keep.get<float>(nnz);
-    plan->p0c = keep.get<float>(nnz);
-    int32_t *col_fill = tmp.get<int32_t>(BM);
-    int32_t *tmp_row = tmp.get<int32_t>(nnz);
-    int32_t *tmp_src = tmp.get<int32_t>(nnz);
-    int32_t *tmp_gc = tmp.get<int32_t>(nnz);
-    if (tmp.failed || keep.failed)
-        return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (sparse arrays)");
-    launch_scan(sr, sc, s);
-    HIP_TRY(hipMemsetAsync(col_fill, 0, sizeof(int32_t) * BM, s));
-    BuildArgs ba{};
-    ba.B = B;
-    ba.N = N;
-    ba.M = M;
+    dv.csr_col = keep.get<int32_t>(nnz);
+    dv.csr_row = keep.get<int32_t>(nnz);
+    dv.csc_row = keep.get<int32_t>(nnz);
+    dv.csc_col = keep.get<int32_t>(nnz);
+    dv.csc_perm = keep.get<int32_t>(nnz);
+    dv.flags = keep.get<uint8_t>(nnz);
+    dv.p_row = keep.get<float>(nnz);
+    dv.p_col = keep.get<float>(nnz);
+    dv.p0r = keep.get<float>(nnz);
+    dv.p0c = keep.get<float>(nnz);
+    dv.cost = keep.get<double>(nnz);
     ba.S = ea.S;
     ba.K = ea.K;
     ba.slots = ea.slots;
     ba.cnt = ea.cnt;
-    ba.row_ptr = plan->row_ptr;
-    ba.col_ptr = plan->col_ptr;
     ba.ovf = ea.ovf;
     ba.n_ovf = (int)hc.overflow;
-    ba.csr_col = plan->csr_col;
-    ba.col_fill = col_fill;
-    ba.tmp_row = tmp_row;
-    ba.tmp_src = tmp_src;
-    ba.tmp_gc = tmp_gc;
-    ba.csc_row = plan->csc_row;
-    ba.csc_perm = plan->csc_perm;
-    ba.nnz = nnz;
-    launch_build(ba, s);
+    ba.col_tiles = tmp.get<int32_t>(ceil_div(BM, tile));
+    ba.tmp_row = tmp.get<int32_t>(nnz);
+    ba.tmp_src = tmp.get<int32_t>(nnz);
+    if (tmp.failed || keep.failed)
+        return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (sparse arrays)");
+    launch_csr_fill(dv, ba, s);
+    launch_csc_build(dv, ba, s);
     HIP_TRY(hipGetLastError());
     pt_build.stop();
 
     // ---- temperatures, softmaxes, P0 ---------------------------------------
-    plan->T_row = keep.get<double>(BN);
-    plan->C1_row = keep.get<double>(BN);
-    plan->g_row = keep.get<double>(BN);
-    plan->T_col = keep.get<double>(BM);
-    plan->C1_col = keep.get<double>(BM);
-    plan->g_col = keep.get<double>(BM);
-    plan->pos_row = keep.get<int32_t>(2 * (size_t)BN);
-    plan->pos_col = keep.get<int32_t>(2 * (size_t)BM);
-    plan->clamp_row = keep.get<uint8_t>(BN);
-    plan->clamp_col = keep.get<uint8_t>(BM);
-    const int L = prm.n_iter;
-    plan->alpha = keep.get<double>((size_t)(L + 1) * BN);
-    plan->beta = keep.get<double>((size_t)(L + 1) * BM);
-    plan->rden = keep.get<double>((size_t)std::max(L, 1) * BN);
-    plan->sden = keep.get<double>((size_t)std::max(L, 1) * BM);
-    double *loss_rows = tmp.get<double>(BN);
-    if (tmp.failed || keep.failed)
+    dv.T_row = keep.get<double>(BN);
+    dv.C1_row = keep.get<double>(BN);
+    dv.g_row = keep.get<double>(BN);
+    dv.T_col = keep.get<double>(BM);
+    dv.C1_col = keep.get<double>(BM);
+    dv.g_col = keep.get<double>(BM);
+    dv.pos_row = keep.get<int32_t>(2 * (size_t)BN);
+    dv.pos_col = keep.get<int32_t>(2 * (size_t)BM);
+    dv.clamp_row = keep.get<uint8_t>(BN);
+    dv.clamp_col = keep.get<uint8_t>(BM);
+    dv.alpha = keep.get<double>((size_t)(L + 1) * BN);
+    dv.beta = keep.get<double>((size_t)(L + 1) * BM);
+    dv.rden = keep.get<double>((size_t)std::max(L, 1) * BN);
+    dv.sden = keep.get<double>((size_t)std::max(L, 1) * BM);
+    dv.dvec = keep.get<double>(BN);
+    dv.evec = keep.get<double>(BM);
+    if (keep.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (plan)");
     {
         PhaseTimer pt(PH_SOFTMAX, s);
-        SoftmaxArgs sa{};
-        sa.x = x;
-        sa.y = y;
-        sa.B = B;
-        sa.N = N;
-        sa.M = M;
-        sa.row_ptr = plan->row_ptr;
-        sa.col_ptr = plan->col_ptr;
-        sa.csr_col = plan->csr_col;
-        sa.csc_row = plan->csc_row;
-        sa.csc_perm = plan->csc_perm;
-        sa.m12_row = plan->m12_row;
-        sa.m12_col = plan->m12_col;
-        sa.flags = plan->flags;
-        sa.p_row = plan->p_row;
-        sa.p_col = plan->p_col;
-        sa.p0r = plan->p0r;
-        sa.p0c = plan->p0c;
-        sa.T_row = plan->T_row;
-        sa.C1_row = plan->C1_row;
-        sa.g_row = plan->g_row;
-        sa.T_col = plan->T_col;
-        sa.C1_col = plan->C1_col;
-        sa.g_col = plan->g_col;
-        sa.pos_row = plan->pos_row;
-        sa.pos_col = plan->pos_col;
-        sa.clamp_row = plan->clamp_row;
-        sa.clamp_col = plan->clamp_col;
-        sa.ctr = plan->ctr;
-        launch_softmax(sa, kp, s);
+        launch_softmax(dv, kp, s);
         HIP_TRY(hipGetLastError());
         pt.stop();
     }
 
-    // ---- Sinkhorn (Eq. 3, Eq. 4) -------------------------------------------
-    SinkhornArgs ka{B, N, M, L, plan->row_ptr, plan->col_ptr, plan->csr_col, plan->csc_row,
-                    plan->p0r, plan->p0c, plan->alpha, plan->beta, plan->rden, plan->sden};
+    // ---- Sinkhorn (Eq. 3, Eq. 4) and the loss ------------------------------
     {
         PhaseTimer pt(PH_SINKHORN, s);
-        launch_sinkhorn_init(ka, s);
-        for (int l = 1; l <= L; ++l)
-            launch_sinkhorn_step(ka, l, prm.eps_stab, s);
-        HIP_TRY(hipGetLastError());
-        pt.stop();
-    }
-
-    // ---- loss --------------------------------------------------------------
-    {
-        PhaseTimer pt(PH_LOSS, s);
-        LossArgs la{x, y, B, N, M, plan->row_ptr, plan->csr_col, plan->p0r,
-                    plan->alpha + (size_t)L * BN, plan->beta + (size_t)L * BM, loss_rows, loss};
-        launch_loss(la, s);
-        HIP_TRY(hipGetLastError());
+        if (sinkhorn_per_sample_ok(N, M)) {
+            HIP_TRY(launch_sinkhorn_fwd(dv, prm.eps_stab, s));
+        } else {
+            launch_sinkhorn_fwd_steps(dv, prm.eps_stab, s);
+            HIP_TRY(hipGetLastError());
+        }
         pt.stop();
     }
     tmp.release();
@@ -637,58 +595,33 @@ apml_status apml_backward(apml_plan *plan, const float *x, const float *y, const
     if (!plan || !x || !y || !grad_loss || !grad_x)
         return fail(APML_ERR_INVALID_ARG, "plan, x, y, grad_loss and grad_x must be non-NULL");
     hipStream_t s = (hipStream_t)stream;
-    const int B = plan->B, N = plan->N, M = plan->M, L = plan->L;
-    const int64_t nnz = plan->stored;
     Arena tmp;
     tmp.stream = s;
-    BackwardArgs a{};
-    a.x = x;
-    a.y = y;
-    a.grad_loss = grad_loss;
-    a.grad_x = grad_x;
-    a.grad_y = grad_y;
-    a.B = B;
-    a.N = N;
-    a.M = M;
-    a.L = L;
-    a.row_ptr = plan->row_ptr;
-    a.col_ptr = plan->col_ptr;
-    a.csr_col = plan->csr_col;
-    a.csc_row = plan->csc_row;
-    a.csc_perm = plan->csc_perm;
-    a.flags = plan->flags;
-    a.p_row = plan->p_row;
-    a.p_col = plan->p_col;
-    a.p0r = plan->p0r;
-    a.p0c = plan->p0c;
-    a.alpha = plan->alpha;
-    a.beta = plan->beta;
-    a.rden = plan->rden;
-    a.sden = plan->sden;
-    a.T_row = plan->T_row;
-    a.C1_row = plan->C1_row;
-    a.g_row = plan->g_row;
-    a.T_col = plan->T_col;
-    a.C1_col = plan->C1_col;
-    a.g_col = plan->g_col;
-    a.pos_row = plan->pos_row;
-    a.pos_col = plan->pos_col;
-    a.clamp_row = plan->clamp_row;
-    a.clamp_col = plan->clamp_col;
-    a.adj = tmp.get<double>(nnz);
-    a.cbar = tmp.get<double>(nnz);
+    DevPlan dv = plan->dv;
+    dv.x = x;
+    dv.y = y;
+    dv.grad_loss = grad_loss;
+    dv.grad_x = grad_x;
+    dv.grad_y = grad_y;
+    dv.adj = tmp.get<double>(plan->stored);
+    dv.cbar = tmp.get<double>(plan->stored);
     if (tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (backward)");
     {
         PhaseTimer pt(PH_BWD_SINK, s);
-        for (int l = L; l >= 1; --l)
-            launch_bwd_sinkhorn_step(a, l, s);
-        HIP_TRY(hipGetLastError());
+        if (dv.L > 0) {
+            if (sinkhorn_per_sample_ok(dv.N, dv.M)) {
+                HIP_TRY(launch_sinkhorn_bwd(dv, plan->max_sample, s));
+            } else {
+                launch_sinkhorn_bwd_steps(dv, s);
+                HIP_TRY(hipGetLastError());
+            }
+        }
         pt.stop();
     }
     {
         PhaseTimer pt(PH_BWD_SOFTMAX, s);
-        launch_bwd_softmax(a, plan->kp, s);
+        launch_bwd_softmax(dv, plan->kp, s);
         HIP_TRY(hipGetLastError());
         pt.stop();
     }
@@ -719,12 +652,12 @@ apml_status apml_plan_nnz(const apml_plan *plan, int64_t *nnz)
     unsigned long long *d = tmp.get<unsigned long long>(plan->B);
     if (tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed");
-    launch_count_support(plan->row_ptr, plan->flags, plan->B, plan->N, d, s);
+    launch_count_support(plan->dv.row_ptr, plan->dv.flags, plan->B, plan->N, d, s);
     HIP_TRY(hipGetLastError());
     std::vector<unsigned long long> h(plan->B);
     Counters hc{};
     HIP_TRY(hipMemcpyAsync(h.data(), d, sizeof(unsigned long long) * plan->B, hipMemcpyDeviceToHost, s));
-    HIP_TRY(hipMemcpyAsync(&hc, plan->ctr, sizeof(Counters), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(&hc, plan->dv.ctr, sizeof(Counters), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
     for (int b = 0; b < plan->B; ++b)
         nnz[b] = (int64_t)h[b];
@@ -768,23 +701,23 @@ apml_status apml_plan_export(const apml_plan *plan, int32_t b, int64_t capacity,
     const int N = plan->N, M = plan->M, L = plan->L;
     hipStream_t s = plan->stream;
     std::vector<int32_t> rp, cp;
-    TRY(copy_range(rp, plan->row_ptr, (int64_t)b * N, N + 1, s));
-    TRY(copy_range(cp, plan->col_ptr, (int64_t)b * M, M + 1, s));
+    TRY(copy_range(rp, plan->dv.row_ptr, (int64_t)b * N, N + 1, s));
+    TRY(copy_range(cp, plan->dv.col_ptr, (int64_t)b * M, M + 1, s));
     HIP_TRY(hipStreamSynchronize(s));
     const int64_t t0 = rp[0], t1 = rp[N], q0 = cp[0], q1 = cp[M];
     std::vector<int32_t> col, perm;
     std::vector<uint8_t> fl;
     std::vector<float> prow, pcol, p0;
     std::vector<double> al, be;
-    TRY(copy_range(col, plan->csr_col, t0, t1 - t0, s));
-    TRY(copy_range(fl, plan->flags, t0, t1 - t0, s));
-    TRY(copy_range(prow, plan->p_row, t0, t1 - t0, s));
-    TRY(copy_range(p0, plan->p0r, t0, t1 - t0, s));
-    TRY(copy_range(perm, plan->csc_perm, q0, q1 - q0, s));
-    TRY(copy_range(pcol, plan->p_col, q0, q1 - q0, s));
+    TRY(copy_range(col, plan->dv.csr_col, t0, t1 - t0, s));
+    TRY(copy_range(fl, plan->dv.flags, t0, t1 - t0, s));
+    TRY(copy_range(prow, plan->dv.p_row, t0, t1 - t0, s));
+    TRY(copy_range(p0, plan->dv.p0r, t0, t1 - t0, s));
+    TRY(copy_range(perm, plan->dv.csc_perm, q0, q1 - q0, s));
+    TRY(copy_range(pcol, plan->dv.p_col, q0, q1 - q0, s));
     const size_t BN = (size_t)plan->B * N, BM = (size_t)plan->B * M;
-    TRY(copy_range(al, plan->alpha, (int64_t)(L * BN + (size_t)b * N), N, s));
-    TRY(copy_range(be, plan->beta, (int64_t)(L * BM + (size_t)b * M), M, s));
+    TRY(copy_range(al, plan->dv.alpha, (int64_t)(L * BN + (size_t)b * N), N, s));
+    TRY(copy_range(be, plan->dv.beta, (int64_t)(L * BM + (size_t)b * M), M, s));
     HIP_TRY(hipStreamSynchronize(s));
     std::vector<float> pcol_rm(t1 - t0, 0.0f);
     for (int64_t q = 0; q < q1 - q0; ++q)
@@ -823,14 +756,14 @@ apml_status apml_plan_export_stats(const apml_plan *plan, int32_t b, double *T_r
     std::vector<double> tr, tc;
     std::vector<int32_t> pr, pc, col, row;
     std::vector<uint8_t> cr, cc;
-    TRY(copy_range(tr, plan->T_row, (int64_t)b * N, N, s));
-    TRY(copy_range(tc, plan->T_col, (int64_t)b * M, M, s));
-    TRY(copy_range(pr, plan->pos_row, 2 * (int64_t)b * N, 2 * (int64_t)N, s));
-    TRY(copy_range(pc, plan->pos_col, 2 * (int64_t)b * M, 2 * (int64_t)M, s));
-    TRY(copy_range(cr, plan->clamp_row, (int64_t)b * N, N, s));
-    TRY(copy_range(cc, plan->clamp_col, (int64_t)b * M, M, s));
-    TRY(copy_range(col, plan->csr_col, 0, plan->stored, s));
-    TRY(copy_range(row, plan->csc_row, 0, plan->stored, s));
+    TRY(copy_range(tr, plan->dv.T_row, (int64_t)b * N, N, s));
+    TRY(copy_range(tc, plan->dv.T_col, (int64_t)b * M, M, s));
+    TRY(copy_range(pr, plan->dv.pos_row, 2 * (int64_t)b * N, 2 * (int64_t)N, s));
+    TRY(copy_range(pc, plan->dv.pos_col, 2 * (int64_t)b * M, 2 * (int64_t)M, s));
+    TRY(copy_range(cr, plan->dv.clamp_row, (int64_t)b * N, N, s));
+    TRY(copy_range(cc, plan->dv.clamp_col, (int64_t)b * M, M, s));
+    TRY(copy_range(col, plan->dv.csr_col, 0, plan->stored, s));
+    TRY(copy_range(row, plan->dv.csc_row, 0, plan->stored, s));
     HIP_TRY(hipStreamSynchronize(s));
     auto at = [](const std::vector<int32_t> &v, int32_t k) { return k >= 0 && (size_t)k < v.size() ? v[k] : -1; };
     for (int i = 0; i < N; ++i) {

@@ -9,8 +9,9 @@
 
 namespace apml {
 
-constexpr int kBlock = 256;   // threads per workgroup (4 wave64)
-constexpr int kUnroll = 8;    // broadcast points per inner step of the dense scans
+constexpr int kBlock = 256;       // threads per workgroup of the grid-wide kernels
+constexpr int kUnroll = 8;        // broadcast points per inner step of the dense scans
+constexpr int kGroup = 4;         // lanes per row / column in the sparse kernels
 
 // Device-side counters of one forward call.
 struct Counters {
@@ -27,17 +28,28 @@ struct OverflowEntry {
     int32_t col;   // column j within the sample
 };
 
+struct Params {
+    double p_min, tau, eps_stab, delta, eps_gap, eps_dist;
+    double log_inv_tau;    // log(1/tau); +inf when tau == 0
+    double lk_row, lk_col; // -log((1-p) / ((K-1) p)) for rows (K = M) and columns (K = N)
+    int n_iter;
+};
+
+// ---------------------------------------------------------------------------
+// dense phase
+// ---------------------------------------------------------------------------
+
 // One direction of the dense minimum / second-minimum scan. Owners are the
 // points whose statistics are computed (X for rows, Y for columns); the
 // broadcast set is scanned against every owner.
 struct ScanDir {
-    const float *own;    // [B, n_own, 3]
-    const float *bcast;  // [B, n_bc, 3]
-    float2 *partial;     // [S][B * n_own]: (min, second min) of squared distance per chunk
+    const float *own;   // [B, n_own, 3]
+    const float *bcast; // [B, n_bc, 3]
+    float2 *partial;    // [S][B * n_own]: (min, second min) of squared distance per chunk
     int n_own, n_bc;
-    int S, chunk;        // chunks of the broadcast range and their length
-    int owner_blocks;    // workgroups per sample over the owners
-    int tiles;           // B * S * owner_blocks
+    int S, chunk;       // chunks of the broadcast range and their length
+    int owner_blocks;   // workgroups per sample over the owners
+    int tiles;          // B * S * owner_blocks
 };
 
 struct FinalizeDir {
@@ -46,21 +58,15 @@ struct FinalizeDir {
     float2 *m12;           // out: (m1, m2) per owner
     float *E;              // out (rows): emission threshold on the squared distance
     float4 *packed;        // out (columns): (x, y, z, emission threshold)
+    int32_t *zero_a, *zero_b; // (columns) per-owner counters cleared here
     int n_own, S;
-    double log_ratio;      // log((K-1) p_min / (1 - p_min)), K = length of the other set
+    double log_ratio;      // -log((1-p)/((K-1)p)), K = length of the other set
 };
 
-struct Params {
-    double p_min, tau, eps_stab, delta, eps_gap, eps_dist;
-    double log_inv_tau; // log(1/tau); +inf when tau == 0
-    double lk_row, lk_col; // log((K-1) p / (1-p)) for rows (K = M) and columns (K = N)
-    int n_iter;
-};
-
-// Host launch wrappers (kernels.hip).
 void launch_top2(const ScanDir &rows, const ScanDir &cols, int B, hipStream_t s);
 void launch_finalize(const FinalizeDir &rows, const FinalizeDir &cols, int B, const Params &p,
-                     hipStream_t s);
+                     Counters *ctr, hipStream_t s);
+
 struct EmitArgs {
     const float *x;      // [B, N, 3]
     const float4 *ypack; // [B, M]: y and its column threshold
@@ -68,15 +74,18 @@ struct EmitArgs {
     int B, N, M, S, chunk, K, owner_blocks;
     int32_t *slots;      // [B*N][S][K]
     int32_t *cnt;        // [B*N][S]
-    int32_t *col_cnt;    // [B*M]
     OverflowEntry *ovf;
     unsigned ovf_cap;
     Counters *ctr;
 };
 void launch_emit(const EmitArgs &a, hipStream_t s);
 
-// Exclusive prefix sums of two count arrays at once. Element k of array a
-// is the sum of in[k*S .. k*S+S-1]; out has n+1 entries (out[n] = total).
+// ---------------------------------------------------------------------------
+// sparse structure
+// ---------------------------------------------------------------------------
+
+// Exclusive prefix sum: element k is the sum of in[k*S .. k*S+S-1]; out has
+// n+1 entries (out[n] = total).
 struct ScanArray {
     const int32_t *in;
     int n, S;
@@ -85,74 +94,62 @@ struct ScanArray {
     int tiles;
 };
 int scan_tile_items();
-void launch_scan(const ScanArray &a0, const ScanArray &a1, hipStream_t s);
+void launch_scan(const ScanArray &a, hipStream_t s);
+
+// Device view of a plan, passed by value to the sparse kernels.
+struct DevPlan {
+    int B, N, M, L;
+    int64_t nnz;
+    const float *x, *y;
+    int32_t *row_ptr, *col_ptr;   // [B*N+1], [B*M+1] global offsets
+    int32_t *csr_col, *csr_row;   // [nnz] row-major: column j in sample, global row b*N+i
+    int32_t *csc_row, *csc_col;   // [nnz] column-major: row i in sample, global column b*M+j
+    int32_t *csc_perm;            // [nnz] row-major position of each column-major entry
+    uint8_t *flags;               // bit 0: s_row >= tau, bit 1: s_col >= tau
+    float *p_row, *p0r;           // row-major
+    float *p_col, *p0c;           // column-major
+    double *cost;                 // row-major C_t
+    float2 *m12_row, *m12_col;
+    double *T_row, *C1_row, *g_row, *T_col, *C1_col, *g_col;
+    int32_t *pos_row;             // [2*B*N] row-major positions of the two minima
+    int32_t *pos_col;             // [2*B*M] column-major positions
+    uint8_t *clamp_row, *clamp_col;
+    double *alpha, *beta;         // [(L+1)][B*N], [(L+1)][B*M] Sinkhorn scalings
+    double *rden, *sden;          // [L][B*N], [L][B*M]: R + eps, S + eps
+    Counters *ctr;
+    float *loss;                  // [B]
+    // backward
+    const float *grad_loss;
+    float *grad_x, *grad_y;
+    double *adj, *cbar;           // [nnz] row-major
+    double *dvec, *evec;          // [B*N], [B*M] scratch when the scalings do not fit in LDS
+};
 
 struct BuildArgs {
-    int B, N, M, S, K;
-    const int32_t *slots, *cnt, *row_ptr, *col_ptr;
+    int S, K;
+    const int32_t *slots, *cnt;
     const OverflowEntry *ovf;
     int n_ovf;
-    int32_t *csr_col;
-    int32_t *col_fill;                  // [B*M], zeroed
-    int32_t *tmp_row, *tmp_src, *tmp_gc; // column-major staging [nnz]
-    int32_t *csc_row, *csc_perm;
-    int64_t nnz;
+    int32_t *col_cnt, *col_fill; // [B*M], cleared by the finalize kernel
+    int32_t *col_tiles;          // tile sums of the column-count scan
+    int32_t *tmp_row, *tmp_src;  // column-major staging [nnz]
 };
-void launch_build(const BuildArgs &a, hipStream_t s);
+void launch_csr_fill(const DevPlan &d, const BuildArgs &a, hipStream_t s);
+void launch_csc_build(const DevPlan &d, const BuildArgs &a, hipStream_t s);
 
-struct SoftmaxArgs {
-    const float *x, *y;
-    int B, N, M;
-    const int32_t *row_ptr, *col_ptr, *csr_col, *csc_row, *csc_perm;
-    const float2 *m12_row, *m12_col;
-    uint8_t *flags;
-    float *p_row, *p_col, *p0r, *p0c;
-    double *T_row, *C1_row, *g_row, *T_col, *C1_col, *g_col;
-    int32_t *pos_row, *pos_col; // [2 * B*N], [2 * B*M]: positions of the two minima
-    uint8_t *clamp_row, *clamp_col;
-    Counters *ctr;
-};
-void launch_softmax(const SoftmaxArgs &a, const Params &p, hipStream_t s);
+void launch_softmax(const DevPlan &d, const Params &p, hipStream_t s);
+void launch_bwd_softmax(const DevPlan &d, const Params &p, hipStream_t s);
 
-struct SinkhornArgs {
-    int B, N, M, L;
-    const int32_t *row_ptr, *col_ptr, *csr_col, *csc_row;
-    const float *p0r, *p0c;
-    double *alpha; // [(L+1) * B*N]
-    double *beta;  // [(L+1) * B*M]
-    double *rden;  // [L * B*N]: R + eps per iteration
-    double *sden;  // [L * B*M]: S + eps per iteration
-};
-void launch_sinkhorn_init(const SinkhornArgs &a, hipStream_t s);
-void launch_sinkhorn_step(const SinkhornArgs &a, int l, double eps, hipStream_t s);
+// Sinkhorn. The per-sample kernels run all iterations in one workgroup per
+// sample (needs N, M <= 65536); the per-iteration kernels are the fallback.
+bool sinkhorn_per_sample_ok(int N, int M);
+hipError_t launch_sinkhorn_fwd(const DevPlan &d, double eps, hipStream_t s);
+hipError_t launch_sinkhorn_bwd(const DevPlan &d, int64_t max_pairs, hipStream_t s);
+void launch_sinkhorn_fwd_steps(const DevPlan &d, double eps, hipStream_t s);
+void launch_sinkhorn_bwd_steps(const DevPlan &d, hipStream_t s);
 
-struct LossArgs {
-    const float *x, *y;
-    int B, N, M;
-    const int32_t *row_ptr, *csr_col;
-    const float *p0r;
-    const double *alpha_L, *beta_L;
-    double *loss_rows; // [B*N] scratch
-    float *loss;       // [B]
-};
-void launch_loss(const LossArgs &a, hipStream_t s);
-
-struct BackwardArgs {
-    const float *x, *y, *grad_loss;
-    float *grad_x, *grad_y;
-    int B, N, M, L;
-    const int32_t *row_ptr, *col_ptr, *csr_col, *csc_row, *csc_perm;
-    const uint8_t *flags;
-    const float *p_row, *p_col, *p0r, *p0c;
-    const double *alpha, *beta, *rden, *sden;
-    const double *T_row, *C1_row, *g_row, *T_col, *C1_col, *g_col;
-    const int32_t *pos_row, *pos_col;
-    const uint8_t *clamp_row, *clamp_col;
-    double *adj;  // [nnz] adjoint of the plan, row-major order
-    double *cbar; // [nnz] adjoint of the cost, row-major order
-};
-void launch_bwd_sinkhorn_step(const BackwardArgs &a, int l, hipStream_t s);
-void launch_bwd_softmax(const BackwardArgs &a, const Params &p, hipStream_t s);
+// out[b] = row_ptr[b*N] for b = 0..B (pair offsets of the samples).
+void launch_sample_offsets(const int32_t *row_ptr, int B, int N, int32_t *out, hipStream_t s);
 
 void launch_count_support(const int32_t *row_ptr, const uint8_t *flags, int B, int N,
                           unsigned long long *out, hipStream_t s);

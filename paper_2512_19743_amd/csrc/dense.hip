@@ -1,0 +1,210 @@
+// Dense phase of the sparse APML loss: the two scans over all B*N*M pairs.
+// VALU-bound; no matrix cores (the K=3 contraction is not a GEMM).
+//
+//   k_top2     per row and per column, the minimum and second minimum of the
+//              single-precision squared distance (Sec. III-A). Each lane owns
+//              one point; the other cloud is streamed through scalar registers
+//              (wave-uniform loads), so a pair costs 6 VALU ops for the
+//              distance and 2 (min, med3) for the statistics.
+//   k_finalize merges the per-chunk statistics and derives each row's and
+//              column's emission threshold: the kept set s >= tau is the ball
+//              C <= C1 + log(1/tau)/T (Sec. III-B, Eq. 1), widened by a small
+//              relative margin and never below the second minimum.
+//   k_emit     the candidate support: every pair inside its row's or its
+//              column's threshold. Per pair 6 VALU ops for the distance and two
+//              compares whose wave masks are combined on the scalar unit. Each
+//              lane appends its row's pairs, in column order, to a private slot
+//              group; the exact test s >= tau is applied later in double
+//              precision on this candidate set.
+#include "apml_internal.h"
+#include "device_common.h"
+
+namespace apml {
+namespace {
+
+struct Top2Args {
+    ScanDir dir[2];
+    int B;
+};
+
+__global__ __launch_bounds__(kBlock) void k_top2(Top2Args args)
+{
+    int t = blockIdx.x;
+    const int which = t < args.dir[0].tiles ? 0 : 1;
+    if (which)
+        t -= args.dir[0].tiles;
+    const ScanDir &d = args.dir[which];
+    const int ob = t % d.owner_blocks;
+    const int rest = t / d.owner_blocks;
+    const int ch = rest % d.S;
+    const int b = rest / d.S;
+    const int a = ob * kBlock + threadIdx.x;
+    const bool valid = a < d.n_own;
+    const float *p = d.own + ((size_t)b * d.n_own + (valid ? a : d.n_own - 1)) * 3;
+    const float ax = p[0], ay = p[1], az = p[2];
+    const float *__restrict__ q = d.bcast + (size_t)b * d.n_bc * 3;
+    const int j0 = ch * d.chunk;
+    const int j1 = min(d.n_bc, j0 + d.chunk);
+    float m1 = kInf, m2 = kInf;
+    int j = j0;
+    for (; j + kUnroll <= j1; j += kUnroll) {
+        const float *__restrict__ qq = q + 3 * (size_t)j;
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const float s = sqdist_f32(ax, ay, az, qq[3 * u], qq[3 * u + 1], qq[3 * u + 2]);
+            m2 = __builtin_amdgcn_fmed3f(m1, m2, s); // second order statistic of the multiset
+            m1 = fminf(m1, s);
+        }
+    }
+    for (; j < j1; ++j) {
+        const float s = sqdist_f32(ax, ay, az, q[3 * j], q[3 * j + 1], q[3 * j + 2]);
+        m2 = __builtin_amdgcn_fmed3f(m1, m2, s);
+        m1 = fminf(m1, s);
+    }
+    if (valid)
+        d.partial[(size_t)ch * args.B * d.n_own + (size_t)b * d.n_own + a] = make_float2(m1, m2);
+}
+
+struct FinalizeArgs {
+    FinalizeDir dir[2];
+    int B;
+    int rows; // B * n_own of dir[0]
+    Params p;
+    Counters *ctr;
+};
+
+__global__ __launch_bounds__(kBlock) void k_finalize(FinalizeArgs args)
+{
+    int k = blockIdx.x * kBlock + threadIdx.x;
+    if (k == 0)
+        *args.ctr = Counters{0, 0, 0};
+    const int which = k < args.rows ? 0 : 1;
+    if (which)
+        k -= args.rows;
+    const FinalizeDir &d = args.dir[which];
+    if (k >= args.B * d.n_own)
+        return;
+    const size_t stride = (size_t)args.B * d.n_own;
+    float m1 = kInf, m2 = kInf;
+    for (int c = 0; c < d.S; ++c) {
+        const float2 v = d.partial[c * stride + k];
+        // top-2 of the union of two top-2 multisets
+        m2 = fminf(fmaxf(m1, v.x), fminf(m2, v.y));
+        m1 = fminf(m1, v.x);
+    }
+    d.m12[k] = make_float2(m1, m2);
+    // Radius of the kept ball from the single-precision minima. The margin
+    // covers the rounding of this estimate (relative ~1e-7 (1 + 2 kappa)) and
+    // of the single-precision distance.
+    const Params &p = args.p;
+    const double c1 = sqrt((double)m1), c2 = sqrt((double)m2);
+    const double gap = (c2 - c1) + p.delta;
+    const double g = gap < p.eps_gap ? p.eps_gap : gap;
+    const double kappa = p.log_inv_tau / d.log_ratio; // log(1/tau) / (T g)
+    const double radius = c1 + g * kappa;
+    const double margin = 1e-5 * (1.0 + kappa);
+    double e = radius * radius * (1.0 + margin);
+    e = fmax(e, (double)m2); // the second minimum is always emitted
+    const float E = isinf(e) ? kInf : __double2float_ru(e);
+    if (which == 0) {
+        d.E[k] = E;
+    } else {
+        const float *o = d.own + (size_t)k * 3;
+        d.packed[k] = make_float4(o[0], o[1], o[2], E);
+        d.zero_a[k] = 0;
+        d.zero_b[k] = 0;
+    }
+}
+
+// Appends pair (row, j) to the lane's slot group, or to the overflow list.
+__device__ __forceinline__ void emit_pair(const EmitArgs &a, int32_t *slot, int row, int ch, int j,
+                                          int &cnt)
+{
+    if (cnt < a.K) {
+        slot[cnt] = j;
+    } else {
+        const unsigned o = atomicAdd(&a.ctr->overflow, 1u);
+        if (o < a.ovf_cap)
+            a.ovf[o] = OverflowEntry{row, ch, cnt, j};
+    }
+    ++cnt;
+}
+
+__global__ __launch_bounds__(kBlock) void k_emit(EmitArgs a)
+{
+    const int t = blockIdx.x;
+    const int ob = t % a.owner_blocks;
+    const int rest = t / a.owner_blocks;
+    const int ch = rest % a.S;
+    const int b = rest / a.S;
+    const int i = ob * kBlock + threadIdx.x;
+    const bool valid = i < a.N;
+    const unsigned long long valid_mask = __builtin_amdgcn_ballot_w64(valid);
+    const int row = b * a.N + (valid ? i : a.N - 1);
+    const float *p = a.x + (size_t)row * 3;
+    const float ax = p[0], ay = p[1], az = p[2];
+    const float E = a.E_row[row];
+    const_ptr<f32x4> q = as_const(reinterpret_cast<const f32x4 *>(a.ypack + (size_t)b * a.M));
+    const int j0 = ch * a.chunk;
+    const int j1 = min(a.M, j0 + a.chunk);
+    int32_t *slot = a.slots + ((size_t)row * a.S + ch) * a.K;
+    const int lane = lane_id();
+    int cnt = 0;
+    int j = j0;
+    // Common path: per column the distance and two compares whose wave masks
+    // are OR'ed on the scalar unit; one branch per 4 columns.
+    for (; j + 4 <= j1; j += 4) {
+        unsigned long long mk[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const f32x4 yv = q[j + u];
+            const float s = sqdist_f32(ax, ay, az, yv.x, yv.y, yv.z);
+            mk[u] = (__builtin_amdgcn_ballot_w64(s <= E) | __builtin_amdgcn_ballot_w64(s <= yv.w)) &
+                    valid_mask;
+        }
+        if (mk[0] | mk[1] | mk[2] | mk[3]) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if ((mk[u] >> lane) & 1ull)
+                    emit_pair(a, slot, row, ch, j + u, cnt);
+        }
+    }
+    for (; j < j1; ++j) {
+        const f32x4 yv = q[j];
+        const float s = sqdist_f32(ax, ay, az, yv.x, yv.y, yv.z);
+        const unsigned long long m =
+            (__builtin_amdgcn_ballot_w64(s <= E) | __builtin_amdgcn_ballot_w64(s <= yv.w)) & valid_mask;
+        if ((m >> lane) & 1ull)
+            emit_pair(a, slot, row, ch, j, cnt);
+    }
+    if (valid)
+        a.cnt[(size_t)row * a.S + ch] = cnt;
+    int w = cnt;
+    for (int off = 32; off > 0; off >>= 1)
+        w += __shfl_xor(w, off);
+    if (lane == 0 && w)
+        atomicAdd(&a.ctr->stored, (unsigned long long)w);
+}
+
+} // namespace
+
+void launch_top2(const ScanDir &rows, const ScanDir &cols, int B, hipStream_t s)
+{
+    Top2Args a{{rows, cols}, B};
+    hipLaunchKernelGGL(k_top2, dim3(rows.tiles + cols.tiles), dim3(kBlock), 0, s, a);
+}
+
+void launch_finalize(const FinalizeDir &rows, const FinalizeDir &cols, int B, const Params &p,
+                     Counters *ctr, hipStream_t s)
+{
+    FinalizeArgs a{{rows, cols}, B, B * rows.n_own, p, ctr};
+    hipLaunchKernelGGL(k_finalize, dim3(blocks_for((int64_t)B * (rows.n_own + cols.n_own), kBlock)),
+                       dim3(kBlock), 0, s, a);
+}
+
+void launch_emit(const EmitArgs &a, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_emit, dim3(a.B * a.S * a.owner_blocks), dim3(kBlock), 0, s, a);
+}
+
+} // namespace apml

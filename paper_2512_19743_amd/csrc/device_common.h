@@ -1,0 +1,75 @@
+// Device helpers shared by the libapml kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cstdint>
+
+namespace apml {
+
+constexpr float kInf = __builtin_huge_valf();
+
+// Squared distance in single precision, as d = a - b per coordinate, then
+// dx*dx, fma(dy,dy,.), fma(dz,dz,.). The dense scans and the sparse passes
+// evaluate exactly this sequence (the library is built without floating-point
+// contraction), so their values agree bit for bit; the argmin decisions rest
+// on it.
+__device__ __forceinline__ float sqdist_f32(float ax, float ay, float az, float bx, float by,
+                                            float bz)
+{
+    const float dx = ax - bx, dy = ay - by, dz = az - bz;
+    float s = dx * dx;
+    s = __builtin_fmaf(dy, dy, s);
+    s = __builtin_fmaf(dz, dz, s);
+    return s;
+}
+
+// Cost C = ||a - b||_2 (Sec. III-A) in double precision from float coordinates.
+__device__ __forceinline__ double dist_f64(const float *a, const float *b)
+{
+    const double dx = (double)a[0] - (double)b[0];
+    const double dy = (double)a[1] - (double)b[1];
+    const double dz = (double)a[2] - (double)b[2];
+    return sqrt(dx * dx + dy * dy + dz * dz);
+}
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+
+// Read-only data seen through the constant address space: wave-uniform loads
+// from it become scalar loads even in kernels that also store to memory.
+template <typename T> using const_ptr = const __attribute__((address_space(4))) T *;
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+template <typename T> __device__ __forceinline__ const_ptr<T> as_const(const T *p)
+{
+    return (const_ptr<T>)p;
+}
+
+// Reductions over aligned groups of G lanes (G divides 64). Butterfly order:
+// every lane of a group ends with the same, order-independent bits.
+template <int G> __device__ __forceinline__ double group_sum(double v)
+{
+#pragma unroll
+    for (int o = 1; o < G; o <<= 1)
+        v += __shfl_xor(v, o);
+    return v;
+}
+
+template <int G> __device__ __forceinline__ int group_min(int v)
+{
+#pragma unroll
+    for (int o = 1; o < G; o <<= 1)
+        v = min(v, __shfl_xor(v, o));
+    return v;
+}
+
+__device__ __forceinline__ double wave_sum(double v)
+{
+    for (int o = 32; o > 0; o >>= 1)
+        v += __shfl_xor(v, o);
+    return v;
+}
+
+inline unsigned blocks_for(int64_t n, int per_block) { return (unsigned)((n + per_block - 1) / per_block); }
+
+} // namespace apml
