@@ -610,7 +610,7 @@ apml_status apml_backward(apml_plan *plan, const float *x, const float *y, const
     {
         PhaseTimer pt(PH_BWD_SINK, s);
         if (dv.L > 0) {
-            if (sinkhorn_per_sample_ok(dv.N, dv.M)) {
+            if (sinkhorn_bwd_per_sample_ok(dv.N, dv.M, plan->max_sample)) {
                 HIP_TRY(launch_sinkhorn_bwd(dv, plan->max_sample, s));
             } else {
                 launch_sinkhorn_bwd_steps(dv, s);

@@ -70,6 +70,26 @@ __device__ __forceinline__ double wave_sum(double v)
     return v;
 }
 
+// Workgroup barrier that orders LDS accesses only: global stores issued
+// before it may still be in flight (use __syncthreads when other threads of
+// the workgroup read them back).
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Barrier for a workgroup that shares data through LDS (LDS_ONLY) or also
+// through global memory.
+template <bool LDS_ONLY> __device__ __forceinline__ void wg_barrier()
+{
+    if (LDS_ONLY)
+        lds_barrier();
+    else
+        __syncthreads();
+}
+
 inline unsigned blocks_for(int64_t n, int per_block) { return (unsigned)((n + per_block - 1) / per_block); }
 
 } // namespace apml

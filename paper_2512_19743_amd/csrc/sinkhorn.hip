@@ -9,297 +9,251 @@
 // which is Eq. 3 / Eq. 4 exactly, including eps. A sweep reads P0 and the
 // indices once and writes no per-pair values.
 //
-// Per-sample kernels: one workgroup per sample runs all 2L sweeps with
-// workgroup barriers only. The sample's pairs are split into equal contiguous
-// slices, one per thread (row-major slices for row sweeps, column-major
-// slices for column sweeps); a slice that fits the register cache is loaded
-// once for the whole kernel. Sums over a row or column are taken in a fixed
-// order: each thread sums the runs of equal owner in its slice; a run that
-// continues into the following threads is completed by its first thread from
-// their partial sums, in thread order. Each round gathers all of its loads
-// before any store. The scalings (and, backward, the plan adjoint) live in
-// LDS when the sample fits.
+// Per-sample kernels (N, M <= kCover): one workgroup per sample runs all 2L
+// sweeps with workgroup barriers only. A group of kG lanes owns kKC rows (and
+// kKC columns); each lane keeps kC pairs of each in registers for the whole
+// kernel (zero padded; longer rows stream the rest), so a row sum is kC
+// multiply-adds per lane and a fixed butterfly over the group. The sums land
+// in LDS and a per-owner pass applies the division. Scalings, sums and (in
+// reverse) the per-pair plan adjoint live in LDS. Global memory is only read
+// at setup and for the saved scalings, which are prefetched into registers
+// one phase ahead; layer stores are not waited for.
 //
 // Reverse sweeps: for u = w/(R + eps) with R = sum over the row of w,
-//   wbar = (ubar - sum_row ubar*u) / (R + eps),
-// and likewise for the columns; the adjoint of the plan is a per-pair array.
+//   wbar = (ubar - sum_row ubar*u) / (R + eps) = ubar r - (sum_row ubar*u) r,
+// r = 1/(R + eps), and likewise for the columns.
 #include "apml_internal.h"
 #include "device_common.h"
 
 namespace apml {
 namespace {
 
-// forward: 1024 threads, 12 pairs per thread and order in registers
-constexpr int kFwdThreads = 1024, kFwdCache = 12;
-// backward (also keeps the row-major position of column-major pairs):
-// 512 threads, 24 pairs per thread and order
-constexpr int kBwdThreads = 512, kBwdCache = 24;
+constexpr int kT = 1024;          // threads of a per-sample workgroup
+constexpr int kG = 4;             // lanes per row / column
+constexpr int kNG = kT / kG;      // groups
+constexpr int kKC = 8;            // rows (and columns) per group
+constexpr int kC = 2;             // pairs per lane and row kept in registers
+constexpr int kCover = kKC * kNG; // rows or columns a workgroup covers
+constexpr int kPer = kCover / kT; // owners per thread in the per-owner passes
 
-template <int T> constexpr int header_doubles() { return (T * 8 + 2 * T + 7) / 8; }
-
-// One ordering of a sample's pairs and this thread's slice of it.
-struct Slice {
-    int a, b;    // this thread's slice, global positions
-    bool head;   // its first run continues the previous thread's last run
-    bool tail;   // its last run continues into the next thread
-    bool cached; // the slice fits the register cache
+// One order of a sample's pairs: owners are rows (row-major) or columns
+// (column-major).
+struct VOrder {
+    const int32_t *ptr;    // [n_own + 1]: global positions of the owners' segments
+    const int32_t *gather; // per pair: index of the other side, within the sample
+    const float *val;      // per pair: P0
+    const int32_t *perm;   // per pair: row-major position (column-major order) or nullptr
+    int n_own;
 };
 
-template <int T, int R> __device__ Slice make_slice(const int32_t *owner, int lo, int hi)
-{
-    Slice s;
-    const int64_t n = hi - lo, e = (n + T - 1) / T;
-    s.a = (int)min((int64_t)hi, lo + (int64_t)threadIdx.x * e);
-    s.b = (int)min((int64_t)hi, s.a + e);
-    s.head = s.a < s.b && s.a > lo && owner[s.a - 1] == owner[s.a];
-    s.tail = s.a < s.b && s.b < hi && owner[s.b] == owner[s.b - 1];
-    s.cached = e <= R;
-    return s;
-}
-
-__device__ bool through(const Slice &s, const int32_t *owner)
-{
-    return s.head && s.tail && owner[s.a] == owner[s.b - 1];
-}
-
-// Up to R pairs of a slice: owner and gathered index (local, 16 bits each),
-// P0, and optionally the row-major position.
-template <int R, bool POS> struct Cache {
-    uint32_t key[R];
-    float val[R];
-    int pos[POS ? R : 1];
-    int n;
+// A lane's share of one order: kKC owners, kC pairs each, zero padded.
+template <bool POS> struct VCache {
+    uint32_t gi[kKC];     // the kC gathered indices, 16 bits each
+    float p0[kKC][kC];
+    uint32_t pos[POS ? kKC : 1]; // the kC row-major positions within the sample, 16 bits each
+    uint32_t start[kKC / 2];     // first pair of owner k, within the sample, 16 bits each
+    uint32_t longm;       // bit k: owner k has more than kG*kC pairs
+    uint32_t validm;      // bit k*kC + c: cached pair c of owner k exists
 };
 
-// Where the pairs of one ordering live in the plan.
-struct Order {
-    const int32_t *owner; // global owner index per pair
-    int owner_base;       // b*N or b*M
-    const int32_t *gather;
-    const float *val;
-    const int32_t *perm;  // row-major position (column-major order), or nullptr
-};
+__device__ __forceinline__ int lane_g() { return threadIdx.x % kG; }
+__device__ __forceinline__ int group() { return threadIdx.x / kG; }
+__device__ __forceinline__ int gidx(uint32_t w, int c) { return (int)((w >> (16 * c)) & 0xFFFFu); }
 
-template <int R, bool POS>
-__device__ __forceinline__ void load(Cache<R, POS> &c, const Order &o, int at, int end)
+template <bool POS> __device__ void vload(VCache<POS> &c, const VOrder &o, int lo)
 {
-    c.n = min(R, end - at);
+    c.longm = 0;
+    c.validm = 0;
 #pragma unroll
-    for (int e = 0; e < R; ++e)
-        if (e < c.n) {
-            c.key[e] = ((uint32_t)(o.owner[at + e] - o.owner_base) << 16) | (uint32_t)o.gather[at + e];
-            c.val[e] = o.val[at + e];
+    for (int k = 0; k < kKC; ++k) {
+        const int own = group() + k * kNG;
+        int s = 0, e = 0;
+        if (own < o.n_own) {
+            s = o.ptr[own];
+            e = o.ptr[own + 1];
+        }
+        if (k % 2 == 0)
+            c.start[k / 2] = 0;
+        c.start[k / 2] |= ((uint32_t)(s - lo) & 0xFFFFu) << (16 * (k % 2));
+        if (e - s > kG * kC)
+            c.longm |= 1u << k;
+        uint32_t w = 0, wp = 0;
+#pragma unroll
+        for (int cc = 0; cc < kC; ++cc) {
+            const int t = s + lane_g() + kG * cc;
+            const bool v = t < e;
+            w |= (uint32_t)(v ? o.gather[t] : 0) << (16 * cc);
+            c.p0[k][cc] = v ? o.val[t] : 0.0f;
             if (POS)
-                c.pos[e] = o.perm[at + e];
+                wp |= ((uint32_t)(v ? o.perm[t] - lo : 0) & 0xFFFFu) << (16 * cc);
+            if (v)
+                c.validm |= 1u << (k * kC + cc);
         }
+        c.gi[k] = w;
+        if (POS)
+            c.pos[k] = wp;
+    }
 }
 
-template <int R, bool POS>
-__device__ __forceinline__ void refill(Cache<R, POS> &c, const Slice &s, const Order &o, int at)
+// For every owner of this lane's group: total = group sum of
+// contrib(gathered, p0, row-major position, owner) over its pairs; the
+// first lane stores it to tot[owner]. Cached pairs first (one owner slot at a
+// time), then the pairs of long owners beyond the cache.
+template <bool POS, class Contrib>
+__device__ __forceinline__ void vsum(const VCache<POS> &c, const VOrder &o, int lo, double *tot, Contrib contrib)
 {
-    if (!s.cached)
-        load(c, o, at, s.b);
-}
-
-template <int R> __device__ __forceinline__ int pair_pos(const Cache<R, true> &c, int e, int at)
-{
-    return c.pos[e];
-}
-template <int R> __device__ __forceinline__ int pair_pos(const Cache<R, false> &c, int e, int at)
-{
-    return at + e;
-}
-
-// Sum of contrib over the pairs of every owner that starts in this thread's
-// slice, handed to fin(owner, sum). Ends with the workgroup synchronised.
-template <int T, int R, bool POS, class Contrib, class Fin>
-__device__ void seg_pass(Cache<R, POS> &c, const Slice &s, const Order &o, double *part,
-                         const uint8_t *thr, Contrib contrib, Fin fin)
-{
-    int cur = -1, pend = -1;
-    double acc = 0.0, pend_sum = 0.0;
-    bool first = true;
-    for (int at = s.a; at < s.b; at += R) {
-        refill(c, s, o, at);
-        double vals[R]; // all loads of the round first: none waits behind a store of fin
 #pragma unroll
-        for (int e = 0; e < R; ++e)
-            if (e < c.n)
-                vals[e] = contrib((int)(c.key[e] >> 16), (int)(c.key[e] & 0xFFFFu), c.val[e],
-                                  pair_pos(c, e, at));
+    for (int k = 0; k < kKC; ++k) {
+        const int own = group() + k * kNG;
+        double acc = 0.0;
 #pragma unroll
-        for (int e = 0; e < R; ++e) {
-            if (e < c.n) {
-                const int own = (int)(c.key[e] >> 16);
-                if (own != cur) {
-                    if (cur >= 0) {
-                        if (first && s.head)
-                            part[threadIdx.x] = acc;
-                        else
-                            fin(cur, acc);
-                        first = false;
-                    }
-                    cur = own;
-                    acc = vals[e];
-                } else {
-                    acc += vals[e];
+        for (int cc = 0; cc < kC; ++cc)
+            acc += contrib(gidx(c.gi[k], cc), c.p0[k][cc],
+                           POS ? gidx(c.pos[k], cc) : gidx(c.start[k / 2], k % 2) + lane_g() + kG * cc, own);
+        acc = group_sum<kG>(acc);
+        if (lane_g() == 0 && own < o.n_own)
+            tot[own] = acc;
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    for (uint32_t m = c.longm; m; m &= m - 1) { // uniform within the group
+        const int own = group() + (__builtin_ctz(m)) * kNG;
+        const int e = o.ptr[own + 1];
+        double acc = 0.0;
+        for (int t = o.ptr[own] + lane_g() + kG * kC; t < e; t += kG)
+            acc += contrib(o.gather[t], o.val[t], POS ? o.perm[t] - lo : t - lo, own);
+        acc = group_sum<kG>(acc);
+        if (lane_g() == 0)
+            tot[own] += acc;
+    }
+}
+
+// adj[position] = adj[position] * r[owner] - q[owner] for every pair of the
+// lane's owners (positions within the sample, row-major).
+template <bool POS>
+__device__ __forceinline__ void vupdate(const VCache<POS> &c, const VOrder &o, int lo, double *adj, const double *r,
+                                        const double *q)
+{
+#pragma unroll
+    for (int k = 0; k < kKC; ++k) {
+        const int own = group() + k * kNG;
+        if (own < o.n_own) {
+            const double rr = r[own], qq = q[own];
+#pragma unroll
+            for (int cc = 0; cc < kC; ++cc)
+                if (c.validm & (1u << (k * kC + cc))) {
+                    const int p = POS ? gidx(c.pos[k], cc) : gidx(c.start[k / 2], k % 2) + lane_g() + kG * cc;
+                    adj[p] = adj[p] * rr - qq;
                 }
-            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    for (uint32_t m = c.longm; m; m &= m - 1) {
+        const int own = group() + (__builtin_ctz(m)) * kNG;
+        const double rr = r[own], qq = q[own];
+        const int e = o.ptr[own + 1];
+        for (int t = o.ptr[own] + lane_g() + kG * kC; t < e; t += kG) {
+            const int p = POS ? o.perm[t] - lo : t - lo;
+            adj[p] = adj[p] * rr - qq;
         }
     }
-    if (cur >= 0) {
-        if (first && s.head)
-            part[threadIdx.x] = acc;
-        else if (s.tail) {
-            pend = cur;
-            pend_sum = acc;
-        } else
-            fin(cur, acc);
-    }
-    __syncthreads();
-    if (pend >= 0) {
-        double t = pend_sum;
-        for (int k = threadIdx.x + 1; k < T; ++k) {
-            t += part[k];
-            if (!thr[k])
-                break;
-        }
-        fin(pend, t);
-    }
-    __syncthreads();
 }
 
-// Visits every pair of this thread's slice: f(owner, gathered, p0, position).
-template <int R, bool POS, class F>
-__device__ __forceinline__ void for_each(Cache<R, POS> &c, const Slice &s, const Order &o, F f)
+// Values of a length-n vector at this thread's owner-pass indices tid, tid+kT.
+__device__ __forceinline__ void prefetch(const double *v, int n, double out[kPer])
 {
-    for (int at = s.a; at < s.b; at += R) {
-        refill(c, s, o, at);
 #pragma unroll
-        for (int e = 0; e < R; ++e)
-            if (e < c.n)
-                f((int)(c.key[e] >> 16), (int)(c.key[e] & 0xFFFFu), c.val[e], pair_pos(c, e, at));
+    for (int u = 0; u < kPer; ++u) {
+        const int k = threadIdx.x + u * kT;
+        out[u] = k < n ? v[k] : 0.0;
     }
 }
 
-// Per pair of the slice: v = compute(owner, gathered, p0, position), then
-// store(position, v), all computes of a round before its stores.
-template <int R, bool POS, class Compute, class Store>
-__device__ __forceinline__ void update_each(Cache<R, POS> &c, const Slice &s, const Order &o,
-                                            Compute compute, Store store)
+__device__ __forceinline__ void to_lds(double *lds, int n, const double in[kPer])
 {
-    for (int at = s.a; at < s.b; at += R) {
-        refill(c, s, o, at);
-        double nv[R];
 #pragma unroll
-        for (int e = 0; e < R; ++e)
-            if (e < c.n)
-                nv[e] = compute((int)(c.key[e] >> 16), (int)(c.key[e] & 0xFFFFu), c.val[e],
-                                pair_pos(c, e, at));
-#pragma unroll
-        for (int e = 0; e < R; ++e)
-            if (e < c.n)
-                store(pair_pos(c, e, at), nv[e]);
+    for (int u = 0; u < kPer; ++u) {
+        const int k = threadIdx.x + u * kT;
+        if (k < n)
+            lds[k] = in[u];
     }
 }
 
-// LDS layout: partial sums [T], through flags [2T] (row-major, column-major),
-// then the scalings [N], [M] if they fit, then the plan adjoint if it fits.
-template <int T> struct Shared {
-    double *part;
-    uint8_t *thr;
-    double *va, *vb, *adj;
-    __device__ Shared(double *lds, int N, int M, int vec_lds)
+// LDS: va [kCover], vb [kCover], vc [kCover], part [kT/64], then (reverse,
+// ADJ_LDS) the plan adjoint of the largest sample.
+struct VShared {
+    double *va, *vb, *vc, *part, *adj;
+    __device__ explicit VShared(double *lds)
     {
-        part = lds;
-        thr = reinterpret_cast<uint8_t *>(lds + T);
-        va = lds + header_doubles<T>();
-        vb = va + N;
-        adj = vec_lds ? vb + M : va;
+        va = lds;
+        vb = va + kCover;
+        vc = vb + kCover;
+        part = vc + kCover;
+        adj = part + kT / 64;
     }
 };
+constexpr size_t kVSharedBytes = 8 * (3 * (size_t)kCover + kT / 64);
 
-__global__ __launch_bounds__(kFwdThreads) void k_sinkhorn_fwd(DevPlan d, double eps, int vec_lds)
+__global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
 {
-    constexpr int T = kFwdThreads, R = kFwdCache;
     extern __shared__ double lds[];
+    VShared sh(lds);
     const int b = blockIdx.x, tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
-    Shared<T> sh(lds, N, M, vec_lds);
-    const Order orow{d.csr_row, b * N, d.csr_col, d.p0r, nullptr};
-    const Order ocol{d.csc_col, b * M, d.csc_row, d.p0c, nullptr};
-    const Slice sr = make_slice<T, R>(d.csr_row, d.row_ptr[(size_t)b * N], d.row_ptr[(size_t)(b + 1) * N]);
-    const Slice sc = make_slice<T, R>(d.csc_col, d.col_ptr[(size_t)b * M], d.col_ptr[(size_t)(b + 1) * M]);
-    sh.thr[tid] = through(sr, d.csr_row);
-    sh.thr[T + tid] = through(sc, d.csc_col);
-    double *alpha0 = d.alpha + (size_t)b * N, *beta0 = d.beta + (size_t)b * M;
-    for (int k = tid; k < N; k += T) {
-        alpha0[k] = 1.0;
-        if (vec_lds)
-            sh.va[k] = 1.0;
+    const VOrder orow{d.row_ptr + (size_t)b * N, d.csr_col, d.p0r, nullptr, N};
+    const VOrder ocol{d.col_ptr + (size_t)b * M, d.csc_row, d.p0c, nullptr, M};
+    VCache<false> cr, cc;
+    vload(cr, orow, 0);
+    vload(cc, ocol, 0);
+    for (int k = tid; k < N; k += kT) {
+        sh.va[k] = 1.0;
+        d.alpha[(size_t)b * N + k] = 1.0;
     }
-    for (int k = tid; k < M; k += T) {
-        beta0[k] = 1.0;
-        if (vec_lds)
-            sh.vb[k] = 1.0;
+    for (int k = tid; k < M; k += kT) {
+        sh.vb[k] = 1.0;
+        d.beta[(size_t)b * M + k] = 1.0;
     }
-    Cache<R, false> cr, cc;
-    if (sr.cached)
-        load(cr, orow, sr.a, sr.b);
-    if (sc.cached)
-        load(cc, ocol, sc.a, sc.b);
-    __syncthreads();
+    lds_barrier();
 
     for (int l = 1; l <= L; ++l) {
-        // column scaling (Eq. 3)
-        const double *a_prev = vec_lds ? sh.va : d.alpha + (l - 1) * BN + (size_t)b * N;
-        const double *b_prev = vec_lds ? sh.vb : d.beta + (l - 1) * BM + (size_t)b * M;
-        double *beta_l = d.beta + l * BM + (size_t)b * M;
-        double *sden_l = d.sden + (l - 1) * BM + (size_t)b * M;
-        seg_pass<T>(
-            cc, sc, ocol, sh.part, sh.thr + T,
-            [&](int j, int i, float p0, int) { return (double)p0 * a_prev[i]; },
-            [&](int j, double tot) {
-                const double bo = b_prev[j];
-                const double den = bo * tot + eps;
-                const double bn = bo / den;
-                beta_l[j] = bn;
-                sden_l[j] = den;
-                if (vec_lds)
-                    sh.vb[j] = bn;
-            });
-        // row scaling (Eq. 4)
-        const double *b_cur = vec_lds ? sh.vb : beta_l;
-        double *alpha_l = d.alpha + l * BN + (size_t)b * N;
-        double *rden_l = d.rden + (l - 1) * BN + (size_t)b * N;
-        seg_pass<T>(
-            cr, sr, orow, sh.part, sh.thr,
-            [&](int i, int j, float p0, int) { return (double)p0 * b_cur[j]; },
-            [&](int i, double tot) {
-                const double ao = a_prev[i];
-                const double den = ao * tot + eps;
-                const double an = ao / den;
-                alpha_l[i] = an;
-                rden_l[i] = den;
-                if (vec_lds)
-                    sh.va[i] = an;
-            });
+        // column scaling (Eq. 3): S_j = sum_i alpha_i P0_ij, beta_j /= beta_j S_j + eps
+        vsum(cc, ocol, 0, sh.vc, [&](int i, float p0, int, int) { return (double)p0 * sh.va[i]; });
+        lds_barrier();
+        for (int j = tid; j < M; j += kT) {
+            const double o = sh.vb[j];
+            const double den = o * sh.vc[j] + eps;
+            const double v = o / den;
+            sh.vb[j] = v;
+            d.beta[l * BM + (size_t)b * M + j] = v;
+            d.sden[(l - 1) * BM + (size_t)b * M + j] = den;
+        }
+        lds_barrier();
+        // row scaling (Eq. 4): R_i = sum_j P0_ij beta_j, alpha_i /= alpha_i R_i + eps
+        vsum(cr, orow, 0, sh.vc, [&](int j, float p0, int, int) { return (double)p0 * sh.vb[j]; });
+        lds_barrier();
+        for (int i = tid; i < N; i += kT) {
+            const double o = sh.va[i];
+            const double den = o * sh.vc[i] + eps;
+            const double v = o / den;
+            sh.va[i] = v;
+            d.alpha[l * BN + (size_t)b * N + i] = v;
+            d.rden[(l - 1) * BN + (size_t)b * N + i] = den;
+        }
+        lds_barrier();
     }
 
     // loss = sum_t v_t C_t (Sec. III-D)
-    const double *aL = vec_lds ? sh.va : d.alpha + L * BN + (size_t)b * N;
-    const double *bL = vec_lds ? sh.vb : d.beta + L * BM + (size_t)b * M;
+    const int lo = d.row_ptr[(size_t)b * N], hi = d.row_ptr[(size_t)(b + 1) * N];
     double acc = 0.0;
-    for_each(cr, sr, orow, [&](int i, int j, float p0, int t) { acc += aL[i] * (double)p0 * bL[j] * d.cost[t]; });
+    for (int t = lo + tid; t < hi; t += kT)
+        acc += sh.va[d.csr_row[t] - b * N] * (double)d.p0r[t] * sh.vb[d.csr_col[t]] * d.cost[t];
     acc = wave_sum(acc);
-    __syncthreads();
     if (lane_id() == 0)
         sh.part[tid >> 6] = acc;
-    __syncthreads();
+    lds_barrier();
     if (tid == 0) {
         double s = 0.0;
-        for (int w = 0; w < T / 64; ++w)
+        for (int w = 0; w < kT / 64; ++w)
             s += sh.part[w];
         d.loss[b] = (float)s;
     }
@@ -307,84 +261,82 @@ __global__ __launch_bounds__(kFwdThreads) void k_sinkhorn_fwd(DevPlan d, double 
 
 // Reverse sweeps, last iteration first. The plan adjoint starts as
 // grad_loss * C (loss = sum v C) and ends as dLoss/dP0 in d.adj. ADJ_LDS keeps
-// it in LDS for the whole kernel (indexed by row-major position in the sample).
-template <bool ADJ_LDS>
-__global__ __launch_bounds__(kBwdThreads) void k_sinkhorn_bwd(DevPlan d, int vec_lds)
+// it in LDS (indexed by row-major position within the sample).
+template <bool ADJ_LDS> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
 {
-    constexpr int T = kBwdThreads, R = kBwdCache;
     extern __shared__ double lds[];
+    VShared sh(lds);
     const int b = blockIdx.x, tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
-    Shared<T> sh(lds, N, M, vec_lds);
-    const Order orow{d.csr_row, b * N, d.csr_col, d.p0r, nullptr};
-    const Order ocol{d.csc_col, b * M, d.csc_row, d.p0c, d.csc_perm};
     const int lo = d.row_ptr[(size_t)b * N], hi = d.row_ptr[(size_t)(b + 1) * N];
-    const Slice sr = make_slice<T, R>(d.csr_row, lo, hi);
-    const Slice sc = make_slice<T, R>(d.csc_col, d.col_ptr[(size_t)b * M], d.col_ptr[(size_t)(b + 1) * M]);
-    sh.thr[tid] = through(sr, d.csr_row);
-    sh.thr[T + tid] = through(sc, d.csc_col);
-    Cache<R, false> cr;
-    Cache<R, true> cc;
-    if (sr.cached)
-        load(cr, orow, sr.a, sr.b);
-    if (sc.cached)
-        load(cc, ocol, sc.a, sc.b);
-    // adjoint storage: LDS slot t - lo, or the global array
-    double *adj = ADJ_LDS ? sh.adj - lo : d.adj;
+    const VOrder orow{d.row_ptr + (size_t)b * N, d.csr_col, d.p0r, nullptr, N};
+    const VOrder ocol{d.col_ptr + (size_t)b * M, d.csc_row, d.p0c, d.csc_perm, M};
+    VCache<false> cr;
+    VCache<true> cc;
+    vload(cr, orow, lo);
+    vload(cc, ocol, lo);
+    double *adj = ADJ_LDS ? sh.adj : d.adj + lo; // indexed by position within the sample
     const double gl = d.grad_loss[b];
-    for (int t = lo + tid; t < hi; t += T)
-        adj[t] = gl * d.cost[t];
-    __syncthreads();
+    for (int t = lo + tid; t < hi; t += kT)
+        adj[t - lo] = gl * d.cost[t];
+    // saved scalings, one phase ahead: alpha^L into LDS now, beta^L, rden^L,
+    // alpha^(L-1), sden^L in registers
+    double nb[kPer], nr[kPer], na[kPer], ns[kPer];
+    {
+        double a0[kPer];
+        prefetch(d.alpha + L * BN + (size_t)b * N, N, a0);
+        to_lds(sh.va, N, a0);
+    }
+    prefetch(d.beta + L * BM + (size_t)b * M, M, nb);
+    wg_barrier<ADJ_LDS>();
 
     for (int l = L; l >= 1; --l) {
-        // adjoint of the row scaling of iteration l
-        const double *al = d.alpha + l * BN + (size_t)b * N;
-        const double *bl = d.beta + l * BM + (size_t)b * M;
-        if (vec_lds) {
-            for (int k = tid; k < N; k += T)
-                sh.va[k] = al[k];
-            for (int k = tid; k < M; k += T)
-                sh.vb[k] = bl[k];
-            __syncthreads();
+        prefetch(d.rden + (l - 1) * BN + (size_t)b * N, N, nr);
+        prefetch(d.alpha + (l - 1) * BN + (size_t)b * N, N, na);
+        prefetch(d.sden + (l - 1) * BM + (size_t)b * M, M, ns);
+        to_lds(sh.vb, M, nb); // beta^l (alpha^l is in va)
+        lds_barrier();
+        // adjoint of the row scaling: d_i = sum_row ubar alpha_i P0 beta_j
+        vsum(cr, orow, lo, sh.vc, [&](int j, float p0, int p, int i) { return adj[p] * (sh.va[i] * (double)p0 * sh.vb[j]); });
+        lds_barrier();
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int i = tid + u * kT;
+            if (i < N) {
+                const double r = 1.0 / nr[u];
+                sh.va[i] = r;
+                sh.vc[i] *= r;
+            }
         }
-        const double *A = vec_lds ? sh.va : al;
-        const double *Bv = vec_lds ? sh.vb : bl;
-        double *dv = vec_lds ? sh.va : d.dvec + (size_t)b * N;
-        seg_pass<T>(
-            cr, sr, orow, sh.part, sh.thr,
-            [&](int i, int j, float p0, int t) { return adj[t] * (A[i] * (double)p0 * Bv[j]); },
-            [&](int i, double tot) { dv[i] = tot; });
-        const double *rd = d.rden + (l - 1) * BN + (size_t)b * N;
-        update_each(
-            cr, sr, orow, [&](int i, int j, float p0, int t) { return (adj[t] - dv[i]) / rd[i]; },
-            [&](int t, double v) { adj[t] = v; });
-        __syncthreads();
-        // adjoint of the column scaling of iteration l
-        const double *ap = d.alpha + (l - 1) * BN + (size_t)b * N;
-        if (vec_lds) {
-            for (int k = tid; k < N; k += T)
-                sh.va[k] = ap[k];
-            __syncthreads();
+        lds_barrier();
+        vupdate(cr, orow, lo, adj, sh.va, sh.vc);
+        wg_barrier<ADJ_LDS>();
+        // adjoint of the column scaling: e_j = sum_col wbar alpha^(l-1)_i P0 beta_j
+        to_lds(sh.va, N, na);
+        if (l > 1)
+            prefetch(d.beta + (l - 1) * BM + (size_t)b * M, M, nb);
+        lds_barrier();
+        vsum(cc, ocol, lo, sh.vc, [&](int i, float p0, int p, int j) { return adj[p] * (sh.va[i] * (double)p0 * sh.vb[j]); });
+        lds_barrier();
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int j = tid + u * kT;
+            if (j < M) {
+                const double r = 1.0 / ns[u];
+                sh.vb[j] = r;
+                sh.vc[j] *= r;
+            }
         }
-        const double *A2 = vec_lds ? sh.va : ap;
-        double *ev = vec_lds ? sh.vb : d.evec + (size_t)b * M;
-        seg_pass<T>(
-            cc, sc, ocol, sh.part, sh.thr + T,
-            [&](int j, int i, float p0, int t) { return adj[t] * (A2[i] * (double)p0 * Bv[j]); },
-            [&](int j, double tot) { ev[j] = tot; });
-        const double *sd = d.sden + (l - 1) * BM + (size_t)b * M;
-        update_each(
-            cc, sc, ocol, [&](int j, int i, float p0, int t) { return (adj[t] - ev[j]) / sd[j]; },
-            [&](int t, double v) { adj[t] = v; });
-        __syncthreads();
+        lds_barrier();
+        vupdate(cc, ocol, lo, adj, sh.vb, sh.vc);
+        wg_barrier<ADJ_LDS>();
     }
     if (ADJ_LDS)
-        for (int t = lo + tid; t < hi; t += T)
-            d.adj[t] = adj[t];
+        for (int t = lo + tid; t < hi; t += kT)
+            d.adj[t] = adj[t - lo];
 }
 
-// ---------------------------------------------------------------------------
 // per-iteration fallback (any N, M): one launch per sweep
 // ---------------------------------------------------------------------------
 
@@ -508,50 +460,40 @@ __global__ __launch_bounds__(kBlock) void k_bwd_sink_col(DevPlan d, int l)
 
 } // namespace
 
-bool sinkhorn_per_sample_ok(int N, int M) { return N <= 65536 && M <= 65536; }
+bool sinkhorn_per_sample_ok(int N, int M) { return N <= kCover && M <= kCover; }
 
-namespace {
-
-// LDS of a per-sample kernel with T threads: header, the scalings if N + M
-// fit, and (max_pairs >= 0) the plan adjoint of the largest sample if it fits.
-template <int T>
-size_t lds_bytes(int N, int M, int64_t max_pairs, bool *vectors_in_lds, bool *adj_in_lds)
+bool sinkhorn_bwd_per_sample_ok(int N, int M, int64_t max_pairs)
 {
-    const size_t header = 8 * (size_t)header_doubles<T>();
-    const size_t budget = 160 * 1024;
-    const size_t vec = 8 * ((size_t)N + M);
-    *vectors_in_lds = header + vec <= budget;
-    const size_t used = header + (*vectors_in_lds ? vec : 0);
-    *adj_in_lds = max_pairs >= 0 && used + 8 * (size_t)max_pairs <= budget;
-    return used + (*adj_in_lds ? 8 * (size_t)max_pairs : 0);
+    return sinkhorn_per_sample_ok(N, M) && max_pairs <= 65536; // positions are packed in 16 bits
 }
 
-} // namespace
+// The packed 16-bit positions of the reverse kernel need samples below 65536 pairs.
+static_assert(kCover <= 65536, "gathered indices are packed in 16 bits");
 
 hipError_t launch_sinkhorn_fwd(const DevPlan &d, double eps, hipStream_t s)
 {
-    bool vec_lds = false, unused = false;
-    const size_t bytes = lds_bytes<kFwdThreads>(d.N, d.M, -1, &vec_lds, &unused);
+    const size_t bytes = kVSharedBytes;
     hipError_t e = hipFuncSetAttribute((const void *)k_sinkhorn_fwd,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(k_sinkhorn_fwd, dim3(d.B), dim3(kFwdThreads), bytes, s, d, eps, vec_lds ? 1 : 0);
+    hipLaunchKernelGGL(k_sinkhorn_fwd, dim3(d.B), dim3(kT), bytes, s, d, eps);
     return hipGetLastError();
 }
 
 hipError_t launch_sinkhorn_bwd(const DevPlan &d, int64_t max_pairs, hipStream_t s)
 {
-    bool vec_lds = false, adj_lds = false;
-    const size_t bytes = lds_bytes<kBwdThreads>(d.N, d.M, max_pairs, &vec_lds, &adj_lds);
+    const size_t budget = 160 * 1024;
+    const bool adj_lds = kVSharedBytes + 8 * (size_t)max_pairs <= budget;
+    const size_t bytes = adj_lds ? kVSharedBytes + 8 * (size_t)max_pairs : kVSharedBytes;
     const void *k = adj_lds ? (const void *)k_sinkhorn_bwd<true> : (const void *)k_sinkhorn_bwd<false>;
     hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess)
         return e;
     if (adj_lds)
-        hipLaunchKernelGGL(k_sinkhorn_bwd<true>, dim3(d.B), dim3(kBwdThreads), bytes, s, d, vec_lds ? 1 : 0);
+        hipLaunchKernelGGL(k_sinkhorn_bwd<true>, dim3(d.B), dim3(kT), bytes, s, d);
     else
-        hipLaunchKernelGGL(k_sinkhorn_bwd<false>, dim3(d.B), dim3(kBwdThreads), bytes, s, d, vec_lds ? 1 : 0);
+        hipLaunchKernelGGL(k_sinkhorn_bwd<false>, dim3(d.B), dim3(kT), bytes, s, d);
     return hipGetLastError();
 }
 
