@@ -10,35 +10,37 @@
 // indices once and writes no per-pair values.
 //
 // Per-sample kernels (N, M <= kCover): one workgroup per sample runs all 2L
-// sweeps with workgroup barriers only. A group of kG lanes owns kKC rows (and
-// kKC columns); each lane keeps kC pairs of each in registers for the whole
-// kernel (zero padded; longer rows stream the rest), so a row sum is kC
-// multiply-adds per lane and a fixed butterfly over the group. The sums land
-// in LDS and a per-owner pass applies the division. Scalings, sums and (in
-// reverse) the per-pair plan adjoint live in LDS. Global memory is only read
-// at setup and for the saved scalings, which are prefetched into registers
-// one phase ahead; layer stores are not waited for.
+// sweeps. Each lane owns SL rows and SL columns. The first kMax pairs of each
+// are kept in registers for the whole kernel and the rest in an LDS tail
+// buffer, so a lane sums its rows (or columns) sequentially in pair order and
+// applies the scaling itself: one workgroup barrier per sweep, no cross-lane
+// reduction, bitwise reproducible. The scalings live in LDS; the saved
+// scalings of the reverse pass are prefetched one phase ahead.
 //
 // Reverse sweeps: for u = w/(R + eps) with R = sum over the row of w,
-//   wbar = (ubar - sum_row ubar*u) / (R + eps) = ubar r - (sum_row ubar*u) r,
-// r = 1/(R + eps), and likewise for the columns.
+//   wbar = (ubar - sum_row ubar*u) / (R + eps),
+// and likewise for the columns. The per-pair plan adjoint lives in LDS
+// (indexed by row-major position within the sample) when it fits; the lane
+// owning a row (or column) reads its pairs' adjoints, forms the sum and
+// rewrites them.
+#include <algorithm>
+
 #include "apml_internal.h"
 #include "device_common.h"
 
 namespace apml {
 namespace {
 
-constexpr int kT = 1024;          // threads of a per-sample workgroup
-constexpr int kG = 4;             // lanes per row / column
-constexpr int kNG = kT / kG;      // groups
-constexpr int kKC = 8;            // rows (and columns) per group
-constexpr int kC = 2;             // pairs per lane and row kept in registers
-constexpr int kCover = kKC * kNG; // rows or columns a workgroup covers
-constexpr int kPer = kCover / kT; // owners per thread in the per-owner passes
+constexpr int kCover = 2048;   // rows or columns a per-sample workgroup covers
+constexpr int kMax = 8;        // pairs per owner kept in registers
+constexpr int kTailCap = 2048; // LDS tail entries per order
+constexpr int kFwdT = 1024;    // forward: 1024 lanes x 2 owners
+constexpr int kBwdT = 512;     // reverse: 512 lanes x 4 owners (more registers per lane)
+constexpr int kMaxWaves = 16;
 
 // One order of a sample's pairs: owners are rows (row-major) or columns
 // (column-major).
-struct VOrder {
+struct LOrder {
     const int32_t *ptr;    // [n_own + 1]: global positions of the owners' segments
     const int32_t *gather; // per pair: index of the other side, within the sample
     const float *val;      // per pair: P0
@@ -46,215 +48,287 @@ struct VOrder {
     int n_own;
 };
 
-// A lane's share of one order: kKC owners, kC pairs each, zero padded.
-template <bool POS> struct VCache {
-    uint32_t gi[kKC];     // the kC gathered indices, 16 bits each
-    float p0[kKC][kC];
-    uint32_t pos[POS ? kKC : 1]; // the kC row-major positions within the sample, 16 bits each
-    uint32_t start[kKC / 2];     // first pair of owner k, within the sample, 16 bits each
-    uint32_t longm;       // bit k: owner k has more than kG*kC pairs
-    uint32_t validm;      // bit k*kC + c: cached pair c of owner k exists
+// The pairs beyond kMax of long owners, in LDS.
+struct Tail {
+    uint32_t *gp; // gathered index | (row-major position within the sample) << 16
+    float *p0;
 };
 
-__device__ __forceinline__ int lane_g() { return threadIdx.x % kG; }
-__device__ __forceinline__ int group() { return threadIdx.x / kG; }
-__device__ __forceinline__ int gidx(uint32_t w, int c) { return (int)((w >> (16 * c)) & 0xFFFFu); }
+// A lane's SL owners: the first kMax pairs of each in registers. Gathered
+// indices and positions are packed two per word.
+template <int SL, bool POS> struct LCache {
+    float p0[SL][kMax];
+    uint32_t gi[SL][kMax / 2];
+    uint32_t pos[POS ? SL : 1][POS ? kMax / 2 : 1];
+    int own[SL];   // owner index within the sample (-1: none)
+    int start[SL]; // global position of the owner's first pair
+    int len[SL];   // its number of pairs (0: no owner)
+    int toff[SL];  // its first tail entry
+    int wmax[SL];  // the longest len[s] in the wave (wave-uniform)
+};
 
-template <bool POS> __device__ void vload(VCache<POS> &c, const VOrder &o, int lo)
+__device__ __forceinline__ int h16(uint32_t w, int k) { return (int)((w >> (16 * (k & 1))) & 0xFFFFu); }
+
+// A copy of v that the compiler cannot see through.
+template <typename V> __device__ __forceinline__ V opaque(V v)
 {
-    c.longm = 0;
-    c.validm = 0;
+    asm volatile("" : "+v"(v));
+    return v;
+}
+
+// Workgroup-wide exclusive scan of one int per thread (T threads, part holds
+// T/64 ints).
+template <int T> __device__ int block_scan(int v, int *part)
+{
+    const int lane = lane_id(), wave = threadIdx.x >> 6;
+    int inc = v;
+    for (int off = 1; off < 64; off <<= 1) {
+        const int n = __shfl_up(inc, off);
+        if (lane >= off)
+            inc += n;
+    }
+    if (lane == 63)
+        part[wave] = inc;
+    lds_barrier();
+    int base = 0;
+    for (int w = 0; w < wave; ++w)
+        base += part[w];
+    lds_barrier();
+    return base + inc - v;
+}
+
+constexpr int kBuckets = 16;
+
+// Loads the lane's owners of one order. Owners are dealt to lanes in order of
+// decreasing length (counting sort on min(len, kBuckets - 1)), so the lanes
+// of a wave have similar lengths and a wave visits only as many cached entries
+// as its longest owner has. The result does not depend on this assignment:
+// each owner's sums are formed by one lane in pair order. Long owners' extra
+// pairs go to the LDS tail (capacity kTailCap; entries beyond it stay in
+// global memory). Padding entries of the cache get P0 = 0, gathered index 0
+// and position 0. scratch: kCover + kBuckets ints of LDS.
+template <int T, int SL, bool POS>
+__device__ void lload(LCache<SL, POS> &c, const LOrder &o, int lo, Tail tl, int *part, int *scratch)
+{
+    int *order = scratch, *hist = scratch + kCover;
+    if (threadIdx.x < kBuckets)
+        hist[threadIdx.x] = 0;
+    lds_barrier();
+    int bk[SL], rk[SL];
 #pragma unroll
-    for (int k = 0; k < kKC; ++k) {
-        const int own = group() + k * kNG;
-        int s = 0, e = 0;
+    for (int s = 0; s < SL; ++s) {
+        const int own = threadIdx.x + s * T;
         if (own < o.n_own) {
-            s = o.ptr[own];
-            e = o.ptr[own + 1];
+            const int n = o.ptr[own + 1] - o.ptr[own];
+            bk[s] = kBuckets - 1 - min(n, kBuckets - 1);
+            rk[s] = atomicAdd(&hist[bk[s]], 1);
         }
-        if (k % 2 == 0)
-            c.start[k / 2] = 0;
-        c.start[k / 2] |= ((uint32_t)(s - lo) & 0xFFFFu) << (16 * (k % 2));
-        if (e - s > kG * kC)
-            c.longm |= 1u << k;
-        uint32_t w = 0, wp = 0;
+    }
+    lds_barrier();
+    if (threadIdx.x == 0) {
+        int run = 0;
+        for (int k = 0; k < kBuckets; ++k) {
+            const int h = hist[k];
+            hist[k] = run;
+            run += h;
+        }
+    }
+    lds_barrier();
 #pragma unroll
-        for (int cc = 0; cc < kC; ++cc) {
-            const int t = s + lane_g() + kG * cc;
-            const bool v = t < e;
-            w |= (uint32_t)(v ? o.gather[t] : 0) << (16 * cc);
-            c.p0[k][cc] = v ? o.val[t] : 0.0f;
+    for (int s = 0; s < SL; ++s) {
+        const int own = threadIdx.x + s * T;
+        if (own < o.n_own)
+            order[hist[bk[s]] + rk[s]] = own;
+    }
+    lds_barrier();
+
+    int tails = 0;
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+        const int k = threadIdx.x + s * T;
+        const int own = k < o.n_own ? order[k] : -1;
+        int st = 0, n = 0;
+        if (own >= 0) {
+            st = o.ptr[own];
+            n = o.ptr[own + 1] - st;
+        }
+        c.own[s] = own;
+        c.start[s] = st;
+        c.len[s] = n;
+        int m = n;
+        for (int off = 32; off > 0; off >>= 1)
+            m = max(m, __shfl_xor(m, off));
+        c.wmax[s] = __builtin_amdgcn_readfirstlane(m);
+#pragma unroll
+        for (int e = 0; e < kMax; e += 2) {
+            uint32_t w = 0, wp = 0;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const bool v = e + h < n;
+                const int t = st + e + h;
+                w |= (uint32_t)(v ? o.gather[t] : 0) << (16 * h);
+                c.p0[s][e + h] = v ? o.val[t] : 0.0f;
+                if (POS)
+                    wp |= ((uint32_t)(v ? o.perm[t] - lo : 0) & 0xFFFFu) << (16 * h);
+            }
+            c.gi[s][e / 2] = w;
             if (POS)
-                wp |= ((uint32_t)(v ? o.perm[t] - lo : 0) & 0xFFFFu) << (16 * cc);
-            if (v)
-                c.validm |= 1u << (k * kC + cc);
+                c.pos[s][e / 2] = wp;
         }
-        c.gi[k] = w;
-        if (POS)
-            c.pos[k] = wp;
+        tails += max(0, n - kMax);
+    }
+    int base = block_scan<T>(tails, part);
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+        c.toff[s] = base;
+        for (int e = kMax; e < c.len[s]; ++e, ++base)
+            if (base < kTailCap) {
+                const int t = c.start[s] + e;
+                tl.gp[base] = (uint32_t)o.gather[t] | (((uint32_t)(POS ? o.perm[t] - lo : t - lo) & 0xFFFFu) << 16);
+                tl.p0[base] = o.val[t];
+            }
     }
 }
 
-// For every owner of this lane's group: total = group sum of
-// contrib(gathered, p0, row-major position, owner) over its pairs; the
-// first lane stores it to tot[owner]. Cached pairs first (one owner slot at a
-// time), then the pairs of long owners beyond the cache.
-template <bool POS, class Contrib>
-__device__ __forceinline__ void vsum(const VCache<POS> &c, const VOrder &o, int lo, double *tot, Contrib contrib)
+// Number of slot s's pairs beyond kMax that sit in the LDS tail; the rest of
+// them are read from global memory.
+template <int SL, bool POS> __device__ __forceinline__ int tail_in_lds(const LCache<SL, POS> &c, int s)
 {
-#pragma unroll
-    for (int k = 0; k < kKC; ++k) {
-        const int own = group() + k * kNG;
-        double acc = 0.0;
-#pragma unroll
-        for (int cc = 0; cc < kC; ++cc)
-            acc += contrib(gidx(c.gi[k], cc), c.p0[k][cc],
-                           POS ? gidx(c.pos[k], cc) : gidx(c.start[k / 2], k % 2) + lane_g() + kG * cc, own);
-        acc = group_sum<kG>(acc);
-        if (lane_g() == 0 && own < o.n_own)
-            tot[own] = acc;
-        __builtin_amdgcn_sched_barrier(0);
-    }
-    for (uint32_t m = c.longm; m; m &= m - 1) { // uniform within the group
-        const int own = group() + (__builtin_ctz(m)) * kNG;
-        const int e = o.ptr[own + 1];
-        double acc = 0.0;
-        for (int t = o.ptr[own] + lane_g() + kG * kC; t < e; t += kG)
-            acc += contrib(o.gather[t], o.val[t], POS ? o.perm[t] - lo : t - lo, own);
-        acc = group_sum<kG>(acc);
-        if (lane_g() == 0)
-            tot[own] += acc;
-    }
+    return max(0, min(c.len[s] - kMax, kTailCap - c.toff[s]));
 }
 
-// adj[position] = adj[position] * r[owner] - q[owner] for every pair of the
-// lane's owners (positions within the sample, row-major).
-template <bool POS>
-__device__ __forceinline__ void vupdate(const VCache<POS> &c, const VOrder &o, int lo, double *adj, const double *r,
-                                        const double *q)
+// Visits the pairs of slot s in order: f(gathered, p0, row-major position,
+// real). The kMax cached entries are visited unconditionally: padding entries
+// (real == false) carry P0 = 0, gathered index 0 and position 0, all valid, so
+// they add exact zeros to sums; f must skip stores for them.
+template <int SL, bool POS, class F>
+__device__ __forceinline__ void leach(const LCache<SL, POS> &c, const LOrder &o, int lo, Tail tl, int s, F f)
 {
+    // The cached words pass through opaque() at each use: values derived from
+    // them (widened P0, unpacked indices, positions) are loop invariants of
+    // the sweep loop, and hoisting them would multiply the registers held.
+    const int st = opaque(c.start[s] - lo), n = opaque(c.len[s]);
 #pragma unroll
-    for (int k = 0; k < kKC; ++k) {
-        const int own = group() + k * kNG;
-        if (own < o.n_own) {
-            const double rr = r[own], qq = q[own];
-#pragma unroll
-            for (int cc = 0; cc < kC; ++cc)
-                if (c.validm & (1u << (k * kC + cc))) {
-                    const int p = POS ? gidx(c.pos[k], cc) : gidx(c.start[k / 2], k % 2) + lane_g() + kG * cc;
-                    adj[p] = adj[p] * rr - qq;
-                }
-        }
-        __builtin_amdgcn_sched_barrier(0);
-    }
-    for (uint32_t m = c.longm; m; m &= m - 1) {
-        const int own = group() + (__builtin_ctz(m)) * kNG;
-        const double rr = r[own], qq = q[own];
-        const int e = o.ptr[own + 1];
-        for (int t = o.ptr[own] + lane_g() + kG * kC; t < e; t += kG) {
-            const int p = POS ? o.perm[t] - lo : t - lo;
-            adj[p] = adj[p] * rr - qq;
+    for (int e = 0; e < kMax; ++e) {
+        if (e < c.wmax[s]) { // wave-uniform
+            const float p0 = opaque(c.p0[s][e]);
+            const bool real = e < n;
+            const int pos = POS ? h16(opaque(c.pos[s][e / 2]), e) : (real ? st + e : 0);
+            f(h16(opaque(c.gi[s][e / 2]), e), p0, pos, real);
         }
     }
-}
-
-// Values of a length-n vector at this thread's owner-pass indices tid, tid+kT.
-__device__ __forceinline__ void prefetch(const double *v, int n, double out[kPer])
-{
-#pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-        const int k = threadIdx.x + u * kT;
-        out[u] = k < n ? v[k] : 0.0;
+    const int nl = tail_in_lds(c, s);
+    for (int k = c.toff[s]; k < c.toff[s] + nl; ++k) {
+        const uint32_t w = tl.gp[k];
+        f((int)(w & 0xFFFFu), tl.p0[k], (int)(w >> 16), true);
     }
+    for (int t = c.start[s] + kMax + nl; t < c.start[s] + c.len[s]; ++t)
+        f(o.gather[t], o.val[t], POS ? o.perm[t] - lo : t - lo, true);
 }
 
-__device__ __forceinline__ void to_lds(double *lds, int n, const double in[kPer])
+// Sum over the pairs of slot s, in order, of f(gathered, p0, row-major position).
+template <int SL, bool POS, class F>
+__device__ __forceinline__ double lsum(const LCache<SL, POS> &c, const LOrder &o, int lo, Tail tl, int s, F f)
 {
-#pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-        const int k = threadIdx.x + u * kT;
-        if (k < n)
-            lds[k] = in[u];
-    }
+    double acc = 0.0;
+    leach(c, o, lo, tl, s, [&](int g, float p0, int pos, bool) { acc += f(g, p0, pos); });
+    return acc;
 }
 
-// LDS: va [kCover], vb [kCover], vc [kCover], part [kT/64], then (reverse,
-// ADJ_LDS) the plan adjoint of the largest sample.
-struct VShared {
-    double *va, *vb, *vc, *part, *adj;
-    __device__ explicit VShared(double *lds)
+// LDS: va [kCover], vb [kCover], part [2 kMaxWaves ints], row tail, column
+// tail, then a region that holds the loader's scratch during set-up and
+// afterwards (reverse, adjoint in LDS) the plan adjoint.
+struct LShared {
+    double *va, *vb, *adj;
+    int *part;
+    Tail tr, tc;
+    __device__ explicit LShared(double *lds)
     {
         va = lds;
         vb = va + kCover;
-        vc = vb + kCover;
-        part = vc + kCover;
-        adj = part + kT / 64;
+        part = reinterpret_cast<int *>(vb + kCover);
+        tr.gp = reinterpret_cast<uint32_t *>(part + 2 * kMaxWaves);
+        tr.p0 = reinterpret_cast<float *>(tr.gp + kTailCap);
+        tc.gp = reinterpret_cast<uint32_t *>(tr.p0 + kTailCap);
+        tc.p0 = reinterpret_cast<float *>(tc.gp + kTailCap);
+        adj = reinterpret_cast<double *>(tc.p0 + kTailCap);
+        scratch = reinterpret_cast<int *>(adj);
     }
+    int *scratch;
 };
-constexpr size_t kVSharedBytes = 8 * (3 * (size_t)kCover + kT / 64);
+constexpr size_t kLSharedBytes = 8 * 2 * (size_t)kCover + 8 * kMaxWaves + 4 * 4 * (size_t)kTailCap;
+constexpr size_t kLoadScratchBytes = 4 * (size_t)(kCover + kBuckets);
 
-__global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
+__global__ __launch_bounds__(kFwdT) void k_sinkhorn_fwd(DevPlan d, double eps)
 {
+    constexpr int T = kFwdT, SL = kCover / kFwdT;
     extern __shared__ double lds[];
-    VShared sh(lds);
+    LShared sh(lds);
     const int b = blockIdx.x, tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
-    const VOrder orow{d.row_ptr + (size_t)b * N, d.csr_col, d.p0r, nullptr, N};
-    const VOrder ocol{d.col_ptr + (size_t)b * M, d.csc_row, d.p0c, nullptr, M};
-    VCache<false> cr, cc;
-    vload(cr, orow, 0);
-    vload(cc, ocol, 0);
-    for (int k = tid; k < N; k += kT) {
+    const LOrder orow{d.row_ptr + (size_t)b * N, d.csr_col, d.p0r, nullptr, N};
+    const LOrder ocol{d.col_ptr + (size_t)b * M, d.csc_row, d.p0c, nullptr, M};
+    const int lo = d.row_ptr[(size_t)b * N], hi = d.row_ptr[(size_t)(b + 1) * N];
+    LCache<SL, false> cr, cc;
+    lload<T>(cr, orow, lo, sh.tr, sh.part, sh.scratch);
+    lload<T>(cc, ocol, lo, sh.tc, sh.part, sh.scratch);
+    for (int k = tid; k < N; k += T) {
         sh.va[k] = 1.0;
         d.alpha[(size_t)b * N + k] = 1.0;
     }
-    for (int k = tid; k < M; k += kT) {
+    for (int k = tid; k < M; k += T) {
         sh.vb[k] = 1.0;
         d.beta[(size_t)b * M + k] = 1.0;
     }
     lds_barrier();
 
     for (int l = 1; l <= L; ++l) {
-        // column scaling (Eq. 3): S_j = sum_i alpha_i P0_ij, beta_j /= beta_j S_j + eps
-        vsum(cc, ocol, 0, sh.vc, [&](int i, float p0, int, int) { return (double)p0 * sh.va[i]; });
-        lds_barrier();
-        for (int j = tid; j < M; j += kT) {
-            const double o = sh.vb[j];
-            const double den = o * sh.vc[j] + eps;
-            const double v = o / den;
-            sh.vb[j] = v;
-            d.beta[l * BM + (size_t)b * M + j] = v;
-            d.sden[(l - 1) * BM + (size_t)b * M + j] = den;
+        // column scaling (Eq. 3): beta_j /= beta_j sum_i alpha_i P0_ij + eps
+#pragma unroll
+        for (int s = 0; s < SL; ++s) {
+            const int j = cc.own[s];
+            if (j >= 0) {
+                const double S = lsum(cc, ocol, lo, sh.tc, s, [&](int i, float p0, int) { return (double)p0 * sh.va[i]; });
+                const double o = sh.vb[j];
+                const double den = o * S + eps;
+                const double v = o / den;
+                sh.vb[j] = v;
+                d.beta[l * BM + (size_t)b * M + j] = v;
+                d.sden[(l - 1) * BM + (size_t)b * M + j] = den;
+            }
         }
         lds_barrier();
-        // row scaling (Eq. 4): R_i = sum_j P0_ij beta_j, alpha_i /= alpha_i R_i + eps
-        vsum(cr, orow, 0, sh.vc, [&](int j, float p0, int, int) { return (double)p0 * sh.vb[j]; });
-        lds_barrier();
-        for (int i = tid; i < N; i += kT) {
-            const double o = sh.va[i];
-            const double den = o * sh.vc[i] + eps;
-            const double v = o / den;
-            sh.va[i] = v;
-            d.alpha[l * BN + (size_t)b * N + i] = v;
-            d.rden[(l - 1) * BN + (size_t)b * N + i] = den;
+        // row scaling (Eq. 4): alpha_i /= alpha_i sum_j P0_ij beta_j + eps
+#pragma unroll
+        for (int s = 0; s < SL; ++s) {
+            const int i = cr.own[s];
+            if (i >= 0) {
+                const double R = lsum(cr, orow, lo, sh.tr, s, [&](int j, float p0, int) { return (double)p0 * sh.vb[j]; });
+                const double o = sh.va[i];
+                const double den = o * R + eps;
+                const double v = o / den;
+                sh.va[i] = v;
+                d.alpha[l * BN + (size_t)b * N + i] = v;
+                d.rden[(l - 1) * BN + (size_t)b * N + i] = den;
+            }
         }
         lds_barrier();
     }
 
-    // loss = sum_t v_t C_t (Sec. III-D)
-    const int lo = d.row_ptr[(size_t)b * N], hi = d.row_ptr[(size_t)(b + 1) * N];
+    // loss = sum_t v_t C_t (Sec. III-D), over the sample's pairs in row-major order
     double acc = 0.0;
-    for (int t = lo + tid; t < hi; t += kT)
+    for (int t = lo + tid; t < hi; t += T)
         acc += sh.va[d.csr_row[t] - b * N] * (double)d.p0r[t] * sh.vb[d.csr_col[t]] * d.cost[t];
     acc = wave_sum(acc);
+    double *part = reinterpret_cast<double *>(sh.tc.p0); // the tails are no longer read
     if (lane_id() == 0)
-        sh.part[tid >> 6] = acc;
+        part[tid >> 6] = acc;
     lds_barrier();
     if (tid == 0) {
         double s = 0.0;
-        for (int w = 0; w < kT / 64; ++w)
-            s += sh.part[w];
+        for (int w = 0; w < T / 64; ++w)
+            s += part[w];
         d.loss[b] = (float)s;
     }
 }
@@ -262,79 +336,100 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
 // Reverse sweeps, last iteration first. The plan adjoint starts as
 // grad_loss * C (loss = sum v C) and ends as dLoss/dP0 in d.adj. ADJ_LDS keeps
 // it in LDS (indexed by row-major position within the sample).
-template <bool ADJ_LDS> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
+template <bool ADJ_LDS> __global__ __launch_bounds__(kBwdT) void k_sinkhorn_bwd(DevPlan d)
 {
+    constexpr int T = kBwdT, SL = kCover / kBwdT;
     extern __shared__ double lds[];
-    VShared sh(lds);
+    LShared sh(lds);
     const int b = blockIdx.x, tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
     const int lo = d.row_ptr[(size_t)b * N], hi = d.row_ptr[(size_t)(b + 1) * N];
-    const VOrder orow{d.row_ptr + (size_t)b * N, d.csr_col, d.p0r, nullptr, N};
-    const VOrder ocol{d.col_ptr + (size_t)b * M, d.csc_row, d.p0c, d.csc_perm, M};
-    VCache<false> cr;
-    VCache<true> cc;
-    vload(cr, orow, lo);
-    vload(cc, ocol, lo);
+    const LOrder orow{d.row_ptr + (size_t)b * N, d.csr_col, d.p0r, nullptr, N};
+    const LOrder ocol{d.col_ptr + (size_t)b * M, d.csc_row, d.p0c, d.csc_perm, M};
+    LCache<SL, false> cr;
+    LCache<SL, true> cc;
+    lload<T>(cr, orow, lo, sh.tr, sh.part, sh.scratch);
+    lload<T>(cc, ocol, lo, sh.tc, sh.part, sh.scratch);
     double *adj = ADJ_LDS ? sh.adj : d.adj + lo; // indexed by position within the sample
     const double gl = d.grad_loss[b];
-    for (int t = lo + tid; t < hi; t += kT)
+    for (int t = lo + tid; t < hi; t += T)
         adj[t - lo] = gl * d.cost[t];
-    // saved scalings, one phase ahead: alpha^L into LDS now, beta^L, rden^L,
-    // alpha^(L-1), sden^L in registers
-    double nb[kPer], nr[kPer], na[kPer], ns[kPer];
-    {
-        double a0[kPer];
-        prefetch(d.alpha + L * BN + (size_t)b * N, N, a0);
-        to_lds(sh.va, N, a0);
+    // own scalings, loaded one phase ahead
+    double a_own[SL], b_own[SL];
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+        const int i = cr.own[s], j = cc.own[s];
+        a_own[s] = i >= 0 ? d.alpha[L * BN + (size_t)b * N + i] : 0.0;
+        b_own[s] = j >= 0 ? d.beta[L * BM + (size_t)b * M + j] : 0.0;
     }
-    prefetch(d.beta + L * BM + (size_t)b * M, M, nb);
-    wg_barrier<ADJ_LDS>();
 
     for (int l = L; l >= 1; --l) {
-        prefetch(d.rden + (l - 1) * BN + (size_t)b * N, N, nr);
-        prefetch(d.alpha + (l - 1) * BN + (size_t)b * N, N, na);
-        prefetch(d.sden + (l - 1) * BM + (size_t)b * M, M, ns);
-        to_lds(sh.vb, M, nb); // beta^l (alpha^l is in va)
-        lds_barrier();
-        // adjoint of the row scaling: d_i = sum_row ubar alpha_i P0 beta_j
-        vsum(cr, orow, lo, sh.vc, [&](int j, float p0, int p, int i) { return adj[p] * (sh.va[i] * (double)p0 * sh.vb[j]); });
-        lds_barrier();
+        double a_prev[SL], r_own[SL], s_own[SL];
 #pragma unroll
-        for (int u = 0; u < kPer; ++u) {
-            const int i = tid + u * kT;
-            if (i < N) {
-                const double r = 1.0 / nr[u];
-                sh.va[i] = r;
-                sh.vc[i] *= r;
+        for (int s = 0; s < SL; ++s) {
+            const int i = cr.own[s], j = cc.own[s];
+            r_own[s] = i >= 0 ? d.rden[(l - 1) * BN + (size_t)b * N + i] : 1.0;
+            a_prev[s] = i >= 0 ? d.alpha[(l - 1) * BN + (size_t)b * N + i] : 0.0;
+            s_own[s] = j >= 0 ? d.sden[(l - 1) * BM + (size_t)b * M + j] : 1.0;
+            if (j >= 0)
+                sh.vb[j] = b_own[s];
+        }
+        // orders the previous column step's adjoint updates (or the initial
+        // adjoint) before this row step, and publishes vb = beta^l
+        wg_barrier<ADJ_LDS>();
+        // adjoint of the row scaling: d_i = sum_row ubar alpha^l_i P0 beta^l_j;
+        // ubar <- (ubar - d_i) / (R_i + eps) on the row's pairs
+#pragma unroll
+        for (int s = 0; s < SL; ++s) {
+            if (cr.own[s] >= 0) {
+                const double ai = a_own[s];
+                const double dsum =
+                    lsum(cr, orow, lo, sh.tr, s, [&](int j, float p0, int p) { return adj[p] * (ai * (double)p0 * sh.vb[j]); });
+                const double ri = 1.0 / r_own[s], q = dsum * ri;
+                leach(cr, orow, lo, sh.tr, s, [&](int, float, int p, bool real) {
+                    if (real)
+                        adj[p] = adj[p] * ri - q;
+                });
             }
         }
-        lds_barrier();
-        vupdate(cr, orow, lo, adj, sh.va, sh.vc);
-        wg_barrier<ADJ_LDS>();
-        // adjoint of the column scaling: e_j = sum_col wbar alpha^(l-1)_i P0 beta_j
-        to_lds(sh.va, N, na);
-        if (l > 1)
-            prefetch(d.beta + (l - 1) * BM + (size_t)b * M, M, nb);
-        lds_barrier();
-        vsum(cc, ocol, lo, sh.vc, [&](int i, float p0, int p, int j) { return adj[p] * (sh.va[i] * (double)p0 * sh.vb[j]); });
-        lds_barrier();
 #pragma unroll
-        for (int u = 0; u < kPer; ++u) {
-            const int j = tid + u * kT;
-            if (j < M) {
-                const double r = 1.0 / ns[u];
-                sh.vb[j] = r;
-                sh.vc[j] *= r;
+        for (int s = 0; s < SL; ++s) {
+            const int i = cr.own[s];
+            if (i >= 0)
+                sh.va[i] = a_prev[s];
+        }
+        wg_barrier<ADJ_LDS>();
+        // adjoint of the column scaling: e_j = sum_col wbar alpha^(l-1)_i P0 beta^l_j
+#pragma unroll
+        for (int s = 0; s < SL; ++s) {
+            if (cc.own[s] >= 0) {
+                const double bj = b_own[s];
+                const double esum =
+                    lsum(cc, ocol, lo, sh.tc, s, [&](int i, float p0, int p) { return adj[p] * (sh.va[i] * (double)p0 * bj); });
+                const double ri = 1.0 / s_own[s], q = esum * ri;
+                leach(cc, ocol, lo, sh.tc, s, [&](int, float, int p, bool real) {
+                    if (real)
+                        adj[p] = adj[p] * ri - q;
+                });
             }
         }
-        lds_barrier();
-        vupdate(cc, ocol, lo, adj, sh.vb, sh.vc);
-        wg_barrier<ADJ_LDS>();
+        // the next iteration's own values; vb is rewritten at the top of the
+        // next iteration, after every lane has passed this iteration's second
+        // barrier, the last point where it was read
+#pragma unroll
+        for (int s = 0; s < SL; ++s) {
+            const int j = cc.own[s];
+            a_own[s] = a_prev[s];
+            if (l > 1)
+                b_own[s] = j >= 0 ? d.beta[(l - 1) * BM + (size_t)b * M + j] : 0.0;
+        }
     }
-    if (ADJ_LDS)
-        for (int t = lo + tid; t < hi; t += kT)
+    if (ADJ_LDS) {
+        lds_barrier();
+        for (int t = lo + tid; t < hi; t += T)
             d.adj[t] = adj[t - lo];
+    }
 }
 
 // per-iteration fallback (any N, M): one launch per sweep
@@ -467,33 +562,31 @@ bool sinkhorn_bwd_per_sample_ok(int N, int M, int64_t max_pairs)
     return sinkhorn_per_sample_ok(N, M) && max_pairs <= 65536; // positions are packed in 16 bits
 }
 
-// The packed 16-bit positions of the reverse kernel need samples below 65536 pairs.
-static_assert(kCover <= 65536, "gathered indices are packed in 16 bits");
-
 hipError_t launch_sinkhorn_fwd(const DevPlan &d, double eps, hipStream_t s)
 {
-    const size_t bytes = kVSharedBytes;
+    const size_t bytes = kLSharedBytes + kLoadScratchBytes;
     hipError_t e = hipFuncSetAttribute((const void *)k_sinkhorn_fwd,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(k_sinkhorn_fwd, dim3(d.B), dim3(kT), bytes, s, d, eps);
+    hipLaunchKernelGGL(k_sinkhorn_fwd, dim3(d.B), dim3(kFwdT), bytes, s, d, eps);
     return hipGetLastError();
 }
 
 hipError_t launch_sinkhorn_bwd(const DevPlan &d, int64_t max_pairs, hipStream_t s)
 {
     const size_t budget = 160 * 1024;
-    const bool adj_lds = kVSharedBytes + 8 * (size_t)max_pairs <= budget;
-    const size_t bytes = adj_lds ? kVSharedBytes + 8 * (size_t)max_pairs : kVSharedBytes;
+    const size_t adj_bytes = 8 * (size_t)max_pairs;
+    const bool adj_lds = kLSharedBytes + std::max(adj_bytes, kLoadScratchBytes) <= budget;
+    const size_t bytes = kLSharedBytes + (adj_lds ? std::max(adj_bytes, kLoadScratchBytes) : kLoadScratchBytes);
     const void *k = adj_lds ? (const void *)k_sinkhorn_bwd<true> : (const void *)k_sinkhorn_bwd<false>;
     hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess)
         return e;
     if (adj_lds)
-        hipLaunchKernelGGL(k_sinkhorn_bwd<true>, dim3(d.B), dim3(kT), bytes, s, d);
+        hipLaunchKernelGGL(k_sinkhorn_bwd<true>, dim3(d.B), dim3(kBwdT), bytes, s, d);
     else
-        hipLaunchKernelGGL(k_sinkhorn_bwd<false>, dim3(d.B), dim3(kT), bytes, s, d);
+        hipLaunchKernelGGL(k_sinkhorn_bwd<false>, dim3(d.B), dim3(kBwdT), bytes, s, d);
     return hipGetLastError();
 }
 
