@@ -22,8 +22,7 @@
  *   7. reverse mode through 6..1 written out by hand, with the distance
  *      gradient of Eq. 5.
  *
- * Readings where the paper is silent or ambiguous (all also listed in the
- * design notes of the repository):
+ * Readings where the paper is silent or ambiguous:
  *   R1  The cost is the Euclidean (not squared) distance.
  *   R2  The minimum and second minimum are decided on the squared distance in
  *       single precision (the paper's precision), from the coordinates rounded

@@ -572,7 +572,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     // ---- Sinkhorn (Eq. 3, Eq. 4) and the loss ------------------------------
     {
         PhaseTimer pt(PH_SINKHORN, s);
-        if (sinkhorn_per_sample_ok(N, M)) {
+        if (sinkhorn_per_sample_ok(N, M, plan->max_sample)) {
             HIP_TRY(launch_sinkhorn_fwd(dv, prm.eps_stab, s));
         } else {
             launch_sinkhorn_fwd_steps(dv, prm.eps_stab, s);
@@ -611,7 +611,7 @@ apml_status apml_backward(apml_plan *plan, const float *x, const float *y, const
         PhaseTimer pt(PH_BWD_SINK, s);
         if (dv.L > 0) {
             if (sinkhorn_bwd_per_sample_ok(dv.N, dv.M, plan->max_sample)) {
-                HIP_TRY(launch_sinkhorn_bwd(dv, plan->max_sample, s));
+                HIP_TRY(launch_sinkhorn_bwd(dv, s));
             } else {
                 launch_sinkhorn_bwd_steps(dv, s);
                 HIP_TRY(hipGetLastError());

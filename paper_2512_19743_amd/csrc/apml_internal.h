@@ -141,11 +141,13 @@ void launch_softmax(const DevPlan &d, const Params &p, hipStream_t s);
 void launch_bwd_softmax(const DevPlan &d, const Params &p, hipStream_t s);
 
 // Sinkhorn. The per-sample kernels run all iterations in one workgroup per
-// sample (needs N, M <= 65536); the per-iteration kernels are the fallback.
-bool sinkhorn_per_sample_ok(int N, int M);
+// sample with the sample's pairs in registers (N, M <= 2048 and a bounded
+// number of pairs per sample, max_pairs); the per-iteration kernels are the
+// general fallback.
+bool sinkhorn_per_sample_ok(int N, int M, int64_t max_pairs);
 bool sinkhorn_bwd_per_sample_ok(int N, int M, int64_t max_pairs);
 hipError_t launch_sinkhorn_fwd(const DevPlan &d, double eps, hipStream_t s);
-hipError_t launch_sinkhorn_bwd(const DevPlan &d, int64_t max_pairs, hipStream_t s);
+hipError_t launch_sinkhorn_bwd(const DevPlan &d, hipStream_t s);
 void launch_sinkhorn_fwd_steps(const DevPlan &d, double eps, hipStream_t s);
 void launch_sinkhorn_bwd_steps(const DevPlan &d, hipStream_t s);
 

@@ -10,19 +10,25 @@
 // indices once and writes no per-pair values.
 //
 // Per-sample kernels (N, M <= kCover): one workgroup per sample runs all 2L
-// sweeps. Each lane owns SL rows and SL columns. The first kMax pairs of each
-// are kept in registers for the whole kernel and the rest in an LDS tail
-// buffer, so a lane sums its rows (or columns) sequentially in pair order and
-// applies the scaling itself: one workgroup barrier per sweep, no cross-lane
-// reduction, bitwise reproducible. The scalings live in LDS; the saved
-// scalings of the reverse pass are prefetched one phase ahead.
+// sweeps with the sample's pairs held in registers. Each row's (column's)
+// pairs are cut into pieces of kP consecutive pairs; piece k sits in lane
+// k mod kT, slot k / kT, for the whole kernel. A sweep is two phases:
+//   piece phase  each lane forms the partial sum of each of its pieces
+//                (gathering the other side's scalings from LDS) and stores it
+//                in LDS;
+//   owner phase  the lane owning a row (column) adds its pieces' partials in
+//                piece order and applies the scaling.
+// Every sum has a fixed order, so the result is bitwise reproducible, and no
+// lane walks a long row alone.
 //
 // Reverse sweeps: for u = w/(R + eps) with R = sum over the row of w,
 //   wbar = (ubar - sum_row ubar*u) / (R + eps),
-// and likewise for the columns. The per-pair plan adjoint lives in LDS
-// (indexed by row-major position within the sample) when it fits; the lane
-// owning a row (or column) reads its pairs' adjoints, forms the sum and
-// rewrites them.
+// and likewise for the columns. The per-pair adjoint lives in global memory
+// (it stays in L2). An update is applied lazily: the owner phase of a row step
+// only publishes 1/(R + eps) and q = (sum_row ubar*u)/(R + eps) per row, and
+// the next piece phase, which visits the pairs in column order, applies
+// wbar = ubar/(R + eps) - q to each pair it reads and writes the result back.
+// So each pair's adjoint is read and written once per sweep.
 #include <algorithm>
 
 #include "apml_internal.h"
@@ -31,16 +37,16 @@
 namespace apml {
 namespace {
 
-constexpr int kCover = 2048;   // rows or columns a per-sample workgroup covers
-constexpr int kMax = 8;        // pairs per owner kept in registers
-constexpr int kTailCap = 2048; // LDS tail entries per order
-constexpr int kFwdT = 1024;    // forward: 1024 lanes x 2 owners
-constexpr int kBwdT = 512;     // reverse: 512 lanes x 4 owners (more registers per lane)
-constexpr int kMaxWaves = 16;
+constexpr int kT = 1024;            // threads of a per-sample workgroup
+constexpr int kSL = 2;              // owners per lane: owner o sits in lane o / kSL
+constexpr int kCover = kT * kSL;    // rows or columns a workgroup covers
+constexpr int kP = 4;               // pairs per piece
+constexpr int kFwdSLP = 6;          // piece slots per lane and order, forward
+constexpr int kBwdSLP = 5;          // and reverse
 
 // One order of a sample's pairs: owners are rows (row-major) or columns
 // (column-major).
-struct LOrder {
+struct POrder {
     const int32_t *ptr;    // [n_own + 1]: global positions of the owners' segments
     const int32_t *gather; // per pair: index of the other side, within the sample
     const float *val;      // per pair: P0
@@ -48,37 +54,40 @@ struct LOrder {
     int n_own;
 };
 
-// The pairs beyond kMax of long owners, in LDS.
-struct Tail {
-    uint32_t *gp; // gathered index | (row-major position within the sample) << 16
-    float *p0;
+enum PosMode { kNoPos, kRunPos, kPairPos };
+
+// A lane's pieces of one order. Per pair: P0, and the gathered index with a
+// 'real' bit (bit 15), two per word; padding entries have P0 = 0, index 0.
+// kRunPos: the first pair's row-major position within the sample (the pairs of
+// a row piece are consecutive); kPairPos: each pair's position, two per word.
+template <int SLP, int PM> struct Pieces {
+    float p0[SLP][kP];
+    uint32_t gi[SLP][kP / 2];
+    uint32_t pos[SLP][PM == kPairPos ? kP / 2 : 1];
+    int n; // number of pieces of the order in this sample (wave-uniform)
 };
 
-// A lane's SL owners: the first kMax pairs of each in registers. Gathered
-// indices and positions are packed two per word.
-template <int SL, bool POS> struct LCache {
-    float p0[SL][kMax];
-    uint32_t gi[SL][kMax / 2];
-    uint32_t pos[POS ? SL : 1][POS ? kMax / 2 : 1];
-    int own[SL];   // owner index within the sample (-1: none)
-    int start[SL]; // global position of the owner's first pair
-    int len[SL];   // its number of pairs (0: no owner)
-    int toff[SL];  // its first tail entry
-    int wmax[SL];  // the longest len[s] in the wave (wave-uniform)
+// A lane's owners: first piece | piece count << 16.
+struct Owners {
+    uint32_t pp[kSL];
 };
 
-__device__ __forceinline__ int h16(uint32_t w, int k) { return (int)((w >> (16 * (k & 1))) & 0xFFFFu); }
+__device__ __forceinline__ int half16(uint32_t w, int e) { return (int)((w >> (16 * (e & 1))) & 0xFFFFu); }
+__device__ __forceinline__ int gidx(uint32_t w, int e) { return half16(w, e) & 0x7FFF; }
+__device__ __forceinline__ bool greal(uint32_t w, int e) { return (half16(w, e) >> 15) != 0; }
 
-// A copy of v that the compiler cannot see through.
+// A copy of v that the compiler cannot see through: keeps values derived from
+// the cached words (widened P0, unpacked indices) from being hoisted out of
+// the sweep loop, which would multiply the registers held.
 template <typename V> __device__ __forceinline__ V opaque(V v)
 {
     asm volatile("" : "+v"(v));
     return v;
 }
 
-// Workgroup-wide exclusive scan of one int per thread (T threads, part holds
-// T/64 ints).
-template <int T> __device__ int block_scan(int v, int *part)
+// Workgroup-wide exclusive scan of one int per thread; also returns the total.
+// part: kT/64 ints of LDS.
+__device__ int block_scan(int v, int *part, int &total)
 {
     const int lane = lane_id(), wave = threadIdx.x >> 6;
     int inc = v;
@@ -90,195 +99,159 @@ template <int T> __device__ int block_scan(int v, int *part)
     if (lane == 63)
         part[wave] = inc;
     lds_barrier();
-    int base = 0;
-    for (int w = 0; w < wave; ++w)
-        base += part[w];
+    int base = 0, tot = 0;
+    for (int w = 0; w < kT / 64; ++w) {
+        const int p = part[w];
+        base += w < wave ? p : 0;
+        tot += p;
+    }
     lds_barrier();
+    total = tot;
     return base + inc - v;
 }
 
-constexpr int kBuckets = 16;
-
-// Loads the lane's owners of one order. Owners are dealt to lanes in order of
-// decreasing length (counting sort on min(len, kBuckets - 1)), so the lanes
-// of a wave have similar lengths and a wave visits only as many cached entries
-// as its longest owner has. The result does not depend on this assignment:
-// each owner's sums are formed by one lane in pair order. Long owners' extra
-// pairs go to the LDS tail (capacity kTailCap; entries beyond it stay in
-// global memory). Padding entries of the cache get P0 = 0, gathered index 0
-// and position 0. scratch: kCover + kBuckets ints of LDS.
-template <int T, int SL, bool POS>
-__device__ void lload(LCache<SL, POS> &c, const LOrder &o, int lo, Tail tl, int *part, int *scratch)
+// Cuts one order into pieces and loads the lane's pieces into registers.
+// owner_of: SLP*kT words of LDS scratch (free again on return). Returns false
+// when the sample has more pieces than the workgroup holds.
+template <int SLP, int PM>
+__device__ bool pload(Pieces<SLP, PM> &pc, Owners &ow, const POrder &o, int lo, int *part, uint32_t *owner_of)
 {
-    int *order = scratch, *hist = scratch + kCover;
-    if (threadIdx.x < kBuckets)
-        hist[threadIdx.x] = 0;
-    lds_barrier();
-    int bk[SL], rk[SL];
+    const int tid = threadIdx.x;
+    constexpr int cap = SLP * kT;
+    int np[kSL], local = 0;
 #pragma unroll
-    for (int s = 0; s < SL; ++s) {
-        const int own = threadIdx.x + s * T;
-        if (own < o.n_own) {
-            const int n = o.ptr[own + 1] - o.ptr[own];
-            bk[s] = kBuckets - 1 - min(n, kBuckets - 1);
-            rk[s] = atomicAdd(&hist[bk[s]], 1);
-        }
+    for (int s = 0; s < kSL; ++s) {
+        const int own = kSL * tid + s;
+        const int n = own < o.n_own ? o.ptr[own + 1] - o.ptr[own] : 0;
+        np[s] = (n + kP - 1) / kP;
+        local += np[s];
+    }
+    int total;
+    int base = block_scan(local, part, total);
+#pragma unroll
+    for (int s = 0; s < kSL; ++s) {
+        ow.pp[s] = (uint32_t)base | ((uint32_t)np[s] << 16);
+        for (int q = 0; q < np[s]; ++q)
+            if (base + q < cap)
+                owner_of[base + q] = (uint32_t)(kSL * tid + s) | ((uint32_t)q << 16);
+        base += np[s];
     }
     lds_barrier();
-    if (threadIdx.x == 0) {
-        int run = 0;
-        for (int k = 0; k < kBuckets; ++k) {
-            const int h = hist[k];
-            hist[k] = run;
-            run += h;
-        }
+    pc.n = __builtin_amdgcn_readfirstlane(total);
+    // all slots' loads are independent: no branches between them
+    int t0s[SLP], ns[SLP];
+#pragma unroll
+    for (int s = 0; s < SLP; ++s) {
+        const int k = s * kT + tid;
+        const bool v = k < min(total, cap);
+        const uint32_t w = owner_of[v ? k : 0];
+        const int own = v ? (int)(w & 0xFFFFu) : 0, q = (int)(w >> 16);
+        const int a = o.ptr[own], e = o.ptr[own + 1];
+        t0s[s] = v ? a + q * kP : 0;
+        ns[s] = v ? min(kP, e - (a + q * kP)) : 0;
     }
-    lds_barrier();
 #pragma unroll
-    for (int s = 0; s < SL; ++s) {
-        const int own = threadIdx.x + s * T;
-        if (own < o.n_own)
-            order[hist[bk[s]] + rk[s]] = own;
-    }
-    lds_barrier();
-
-    int tails = 0;
+    for (int s = 0; s < SLP; ++s) {
+        const int t0 = t0s[s], n = ns[s];
 #pragma unroll
-    for (int s = 0; s < SL; ++s) {
-        const int k = threadIdx.x + s * T;
-        const int own = k < o.n_own ? order[k] : -1;
-        int st = 0, n = 0;
-        if (own >= 0) {
-            st = o.ptr[own];
-            n = o.ptr[own + 1] - st;
-        }
-        c.own[s] = own;
-        c.start[s] = st;
-        c.len[s] = n;
-        int m = n;
-        for (int off = 32; off > 0; off >>= 1)
-            m = max(m, __shfl_xor(m, off));
-        c.wmax[s] = __builtin_amdgcn_readfirstlane(m);
-#pragma unroll
-        for (int e = 0; e < kMax; e += 2) {
-            uint32_t w = 0, wp = 0;
+        for (int e = 0; e < kP; e += 2) {
+            uint32_t g = 0, wp = 0;
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const bool v = e + h < n;
-                const int t = st + e + h;
-                w |= (uint32_t)(v ? o.gather[t] : 0) << (16 * h);
-                c.p0[s][e + h] = v ? o.val[t] : 0.0f;
-                if (POS)
-                    wp |= ((uint32_t)(v ? o.perm[t] - lo : 0) & 0xFFFFu) << (16 * h);
+                const int t = v ? t0 + e + h : lo; // position lo always exists
+                const uint32_t gv = (uint32_t)o.gather[t];
+                const float pv = o.val[t];
+                g |= (v ? gv | 0x8000u : 0u) << (16 * h);
+                pc.p0[s][e + h] = v ? pv : 0.0f;
+                if (PM == kPairPos) {
+                    const int pp = o.perm[t] - lo;
+                    wp |= ((uint32_t)(v ? pp : 0) & 0xFFFFu) << (16 * h);
+                }
             }
-            c.gi[s][e / 2] = w;
-            if (POS)
-                c.pos[s][e / 2] = wp;
+            pc.gi[s][e / 2] = g;
+            if (PM == kPairPos)
+                pc.pos[s][e / 2] = wp;
         }
-        tails += max(0, n - kMax);
+        if (PM == kRunPos)
+            pc.pos[s][0] = (uint32_t)(n > 0 ? t0 - lo : 0);
     }
-    int base = block_scan<T>(tails, part);
+    lds_barrier();
+    return total <= cap;
+}
+
+// True when slot s of this wave holds at least one piece.
+template <int SLP, int PM> __device__ __forceinline__ bool wave_active(const Pieces<SLP, PM> &pc, int s)
+{
+    return s * kT + (int)(threadIdx.x & ~63u) < pc.n;
+}
+
+// Visits the kP entries of piece slot s: f(gathered, p0, position, real).
+// Padding entries have real == false, P0 = 0, gathered index 0 and position
+// 0: they add exact zeros to sums, and f must not store for them.
+template <int SLP, int PM, class F>
+__device__ __forceinline__ void pvisit(const Pieces<SLP, PM> &pc, int s, F f)
+{
+    const int run = PM == kRunPos ? (int)opaque(pc.pos[s][0]) : 0;
 #pragma unroll
-    for (int s = 0; s < SL; ++s) {
-        c.toff[s] = base;
-        for (int e = kMax; e < c.len[s]; ++e, ++base)
-            if (base < kTailCap) {
-                const int t = c.start[s] + e;
-                tl.gp[base] = (uint32_t)o.gather[t] | (((uint32_t)(POS ? o.perm[t] - lo : t - lo) & 0xFFFFu) << 16);
-                tl.p0[base] = o.val[t];
-            }
+    for (int e = 0; e < kP; ++e) {
+        const uint32_t g = opaque(pc.gi[s][e / 2]);
+        const float p0 = opaque(pc.p0[s][e]);
+        const int pos = PM == kPairPos ? half16(opaque(pc.pos[s][e / 2]), e) : run + e;
+        f(gidx(g, e), p0, pos, greal(g, e));
     }
 }
 
-// Number of slot s's pairs beyond kMax that sit in the LDS tail; the rest of
-// them are read from global memory.
-template <int SL, bool POS> __device__ __forceinline__ int tail_in_lds(const LCache<SL, POS> &c, int s)
+// Sum of the partials of owner slot s, in piece order. The first four are
+// loaded together.
+__device__ __forceinline__ double owner_sum(const Owners &ow, int s, const double *part)
 {
-    return max(0, min(c.len[s] - kMax, kTailCap - c.toff[s]));
-}
-
-// Visits the pairs of slot s in order: f(gathered, p0, row-major position,
-// real). The kMax cached entries are visited unconditionally: padding entries
-// (real == false) carry P0 = 0, gathered index 0 and position 0, all valid, so
-// they add exact zeros to sums; f must skip stores for them.
-template <int SL, bool POS, class F>
-__device__ __forceinline__ void leach(const LCache<SL, POS> &c, const LOrder &o, int lo, Tail tl, int s, F f)
-{
-    // The cached words pass through opaque() at each use: values derived from
-    // them (widened P0, unpacked indices, positions) are loop invariants of
-    // the sweep loop, and hoisting them would multiply the registers held.
-    const int st = opaque(c.start[s] - lo), n = opaque(c.len[s]);
+    const int first = (int)(ow.pp[s] & 0xFFFFu), cnt = (int)(ow.pp[s] >> 16);
+    double v[4];
 #pragma unroll
-    for (int e = 0; e < kMax; ++e) {
-        if (e < c.wmax[s]) { // wave-uniform
-            const float p0 = opaque(c.p0[s][e]);
-            const bool real = e < n;
-            const int pos = POS ? h16(opaque(c.pos[s][e / 2]), e) : (real ? st + e : 0);
-            f(h16(opaque(c.gi[s][e / 2]), e), p0, pos, real);
-        }
-    }
-    const int nl = tail_in_lds(c, s);
-    for (int k = c.toff[s]; k < c.toff[s] + nl; ++k) {
-        const uint32_t w = tl.gp[k];
-        f((int)(w & 0xFFFFu), tl.p0[k], (int)(w >> 16), true);
-    }
-    for (int t = c.start[s] + kMax + nl; t < c.start[s] + c.len[s]; ++t)
-        f(o.gather[t], o.val[t], POS ? o.perm[t] - lo : t - lo, true);
-}
-
-// Sum over the pairs of slot s, in order, of f(gathered, p0, row-major position).
-template <int SL, bool POS, class F>
-__device__ __forceinline__ double lsum(const LCache<SL, POS> &c, const LOrder &o, int lo, Tail tl, int s, F f)
-{
-    double acc = 0.0;
-    leach(c, o, lo, tl, s, [&](int g, float p0, int pos, bool) { acc += f(g, p0, pos); });
+    for (int k = 0; k < 4; ++k)
+        v[k] = k < cnt ? part[first + k] : 0.0;
+    double acc = ((v[0] + v[1]) + v[2]) + v[3];
+    for (int k = first + 4; k < first + cnt; ++k)
+        acc += part[k];
     return acc;
 }
 
-// LDS: va [kCover], vb [kCover], part [2 kMaxWaves ints], row tail, column
-// tail, then a region that holds the loader's scratch during set-up and
-// afterwards (reverse, adjoint in LDS) the plan adjoint.
-struct LShared {
-    double *va, *vb, *adj;
-    int *part;
-    Tail tr, tc;
-    __device__ explicit LShared(double *lds)
-    {
-        va = lds;
-        vb = va + kCover;
-        part = reinterpret_cast<int *>(vb + kCover);
-        tr.gp = reinterpret_cast<uint32_t *>(part + 2 * kMaxWaves);
-        tr.p0 = reinterpret_cast<float *>(tr.gp + kTailCap);
-        tc.gp = reinterpret_cast<uint32_t *>(tr.p0 + kTailCap);
-        tc.p0 = reinterpret_cast<float *>(tc.gp + kTailCap);
-        adj = reinterpret_cast<double *>(tc.p0 + kTailCap);
-        scratch = reinterpret_cast<int *>(adj);
-    }
-    int *scratch;
-};
-constexpr size_t kLSharedBytes = 8 * 2 * (size_t)kCover + 8 * kMaxWaves + 4 * 4 * (size_t)kTailCap;
-constexpr size_t kLoadScratchBytes = 4 * (size_t)(kCover + kBuckets);
+// Most pieces an order of a sample with n_own owners and at most max_pairs
+// pairs can have: sum over owners of ceil(len / kP).
+inline int64_t max_pieces(int n_own, int64_t max_pairs) { return (max_pairs + (int64_t)(kP - 1) * n_own) / kP; }
 
-__global__ __launch_bounds__(kFwdT) void k_sinkhorn_fwd(DevPlan d, double eps)
+constexpr size_t fwd_lds_bytes() { return 8 * (2 * (size_t)kCover + (size_t)kFwdSLP * kT) + 4 * (kT / 64); }
+constexpr size_t bwd_lds_bytes() { return 8 * (6 * (size_t)kCover + (size_t)kBwdSLP * kT) + 4 * (kT / 64); }
+
+__global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
 {
-    constexpr int T = kFwdT, SL = kCover / kFwdT;
+    constexpr int SLP = kFwdSLP;
     extern __shared__ double lds[];
-    LShared sh(lds);
+    double *va = lds, *vb = va + kCover, *part = vb + kCover;
+    int *scan = reinterpret_cast<int *>(part + SLP * kT);
+    uint32_t *owner_of = reinterpret_cast<uint32_t *>(part); // set-up only
     const int b = blockIdx.x, tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
-    const LOrder orow{d.row_ptr + (size_t)b * N, d.csr_col, d.p0r, nullptr, N};
-    const LOrder ocol{d.col_ptr + (size_t)b * M, d.csc_row, d.p0c, nullptr, M};
     const int lo = d.row_ptr[(size_t)b * N], hi = d.row_ptr[(size_t)(b + 1) * N];
-    LCache<SL, false> cr, cc;
-    lload<T>(cr, orow, lo, sh.tr, sh.part, sh.scratch);
-    lload<T>(cc, ocol, lo, sh.tc, sh.part, sh.scratch);
-    for (int k = tid; k < N; k += T) {
-        sh.va[k] = 1.0;
+    const POrder orow{d.row_ptr + (size_t)b * N, d.csr_col, d.p0r, nullptr, N};
+    const POrder ocol{d.col_ptr + (size_t)b * M, d.csc_row, d.p0c, nullptr, M};
+    Pieces<SLP, kNoPos> pr, pc;
+    Owners owr, owc;
+    bool ok = pload(pr, owr, orow, lo, scan, owner_of);
+    ok = pload(pc, owc, ocol, lo, scan, owner_of) && ok;
+    if (!ok) { // excluded by the host's capacity check; fail loudly if reached
+        if (tid == 0)
+            d.loss[b] = __builtin_nanf("");
+        return;
+    }
+    for (int k = tid; k < N; k += kT) {
+        va[k] = 1.0;
         d.alpha[(size_t)b * N + k] = 1.0;
     }
-    for (int k = tid; k < M; k += T) {
-        sh.vb[k] = 1.0;
+    for (int k = tid; k < M; k += kT) {
+        vb[k] = 1.0;
         d.beta[(size_t)b * M + k] = 1.0;
     }
     lds_barrier();
@@ -286,14 +259,22 @@ __global__ __launch_bounds__(kFwdT) void k_sinkhorn_fwd(DevPlan d, double eps)
     for (int l = 1; l <= L; ++l) {
         // column scaling (Eq. 3): beta_j /= beta_j sum_i alpha_i P0_ij + eps
 #pragma unroll
-        for (int s = 0; s < SL; ++s) {
-            const int j = cc.own[s];
-            if (j >= 0) {
-                const double S = lsum(cc, ocol, lo, sh.tc, s, [&](int i, float p0, int) { return (double)p0 * sh.va[i]; });
-                const double o = sh.vb[j];
+        for (int s = 0; s < SLP; ++s)
+            if (wave_active(pc, s)) {
+                double acc = 0.0;
+                pvisit(pc, s, [&](int i, float p0, int, bool) { acc += (double)p0 * va[i]; });
+                part[s * kT + tid] = acc;
+            }
+        lds_barrier();
+#pragma unroll
+        for (int s = 0; s < kSL; ++s) {
+            const int j = kSL * tid + s;
+            if (j < M) {
+                const double S = owner_sum(owc, s, part);
+                const double o = vb[j];
                 const double den = o * S + eps;
                 const double v = o / den;
-                sh.vb[j] = v;
+                vb[j] = v;
                 d.beta[l * BM + (size_t)b * M + j] = v;
                 d.sden[(l - 1) * BM + (size_t)b * M + j] = den;
             }
@@ -301,14 +282,22 @@ __global__ __launch_bounds__(kFwdT) void k_sinkhorn_fwd(DevPlan d, double eps)
         lds_barrier();
         // row scaling (Eq. 4): alpha_i /= alpha_i sum_j P0_ij beta_j + eps
 #pragma unroll
-        for (int s = 0; s < SL; ++s) {
-            const int i = cr.own[s];
-            if (i >= 0) {
-                const double R = lsum(cr, orow, lo, sh.tr, s, [&](int j, float p0, int) { return (double)p0 * sh.vb[j]; });
-                const double o = sh.va[i];
+        for (int s = 0; s < SLP; ++s)
+            if (wave_active(pr, s)) {
+                double acc = 0.0;
+                pvisit(pr, s, [&](int j, float p0, int, bool) { acc += (double)p0 * vb[j]; });
+                part[s * kT + tid] = acc;
+            }
+        lds_barrier();
+#pragma unroll
+        for (int s = 0; s < kSL; ++s) {
+            const int i = kSL * tid + s;
+            if (i < N) {
+                const double R = owner_sum(owr, s, part);
+                const double o = va[i];
                 const double den = o * R + eps;
                 const double v = o / den;
-                sh.va[i] = v;
+                va[i] = v;
                 d.alpha[l * BN + (size_t)b * N + i] = v;
                 d.rden[(l - 1) * BN + (size_t)b * N + i] = den;
             }
@@ -318,117 +307,158 @@ __global__ __launch_bounds__(kFwdT) void k_sinkhorn_fwd(DevPlan d, double eps)
 
     // loss = sum_t v_t C_t (Sec. III-D), over the sample's pairs in row-major order
     double acc = 0.0;
-    for (int t = lo + tid; t < hi; t += T)
-        acc += sh.va[d.csr_row[t] - b * N] * (double)d.p0r[t] * sh.vb[d.csr_col[t]] * d.cost[t];
+    for (int t = lo + tid; t < hi; t += kT)
+        acc += va[d.csr_row[t] - b * N] * (double)d.p0r[t] * vb[d.csr_col[t]] * d.cost[t];
     acc = wave_sum(acc);
-    double *part = reinterpret_cast<double *>(sh.tc.p0); // the tails are no longer read
     if (lane_id() == 0)
         part[tid >> 6] = acc;
     lds_barrier();
     if (tid == 0) {
         double s = 0.0;
-        for (int w = 0; w < T / 64; ++w)
+        for (int w = 0; w < kT / 64; ++w)
             s += part[w];
         d.loss[b] = (float)s;
     }
 }
 
 // Reverse sweeps, last iteration first. The plan adjoint starts as
-// grad_loss * C (loss = sum v C) and ends as dLoss/dP0 in d.adj. ADJ_LDS keeps
-// it in LDS (indexed by row-major position within the sample).
-template <bool ADJ_LDS> __global__ __launch_bounds__(kBwdT) void k_sinkhorn_bwd(DevPlan d)
+// grad_loss * C (loss = sum v C) and ends as dLoss/dP0 in d.adj (row-major).
+__global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
 {
-    constexpr int T = kBwdT, SL = kCover / kBwdT;
+    constexpr int SLP = kBwdSLP;
     extern __shared__ double lds[];
-    LShared sh(lds);
+    // row side: alpha^(l-1), 1/(R + eps), q; column side: beta^l, 1/(S + eps), q
+    double *va = lds, *ri = va + kCover, *qr = ri + kCover;
+    double *vb = qr + kCover, *si = vb + kCover, *qc = si + kCover;
+    double *part = qc + kCover;
+    int *scan = reinterpret_cast<int *>(part + SLP * kT);
+    uint32_t *owner_of = reinterpret_cast<uint32_t *>(part); // set-up only
     const int b = blockIdx.x, tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
     const int lo = d.row_ptr[(size_t)b * N], hi = d.row_ptr[(size_t)(b + 1) * N];
-    const LOrder orow{d.row_ptr + (size_t)b * N, d.csr_col, d.p0r, nullptr, N};
-    const LOrder ocol{d.col_ptr + (size_t)b * M, d.csc_row, d.p0c, d.csc_perm, M};
-    LCache<SL, false> cr;
-    LCache<SL, true> cc;
-    lload<T>(cr, orow, lo, sh.tr, sh.part, sh.scratch);
-    lload<T>(cc, ocol, lo, sh.tc, sh.part, sh.scratch);
-    double *adj = ADJ_LDS ? sh.adj : d.adj + lo; // indexed by position within the sample
-    const double gl = d.grad_loss[b];
-    for (int t = lo + tid; t < hi; t += T)
-        adj[t - lo] = gl * d.cost[t];
-    // own scalings, loaded one phase ahead
-    double a_own[SL], b_own[SL];
-#pragma unroll
-    for (int s = 0; s < SL; ++s) {
-        const int i = cr.own[s], j = cc.own[s];
-        a_own[s] = i >= 0 ? d.alpha[L * BN + (size_t)b * N + i] : 0.0;
-        b_own[s] = j >= 0 ? d.beta[L * BM + (size_t)b * M + j] : 0.0;
+    const POrder orow{d.row_ptr + (size_t)b * N, d.csr_col, d.p0r, nullptr, N};
+    const POrder ocol{d.col_ptr + (size_t)b * M, d.csc_row, d.p0c, d.csc_perm, M};
+    Pieces<SLP, kRunPos> pr;
+    Pieces<SLP, kPairPos> pc;
+    Owners owr, owc;
+    bool ok = pload(pr, owr, orow, lo, scan, owner_of);
+    ok = pload(pc, owc, ocol, lo, scan, owner_of) && ok;
+    double *adj = d.adj + lo; // indexed by row-major position within the sample
+    if (!ok) { // excluded by the host's capacity check; fail loudly if reached
+        for (int t = lo + tid; t < hi; t += kT)
+            adj[t - lo] = __builtin_nan("");
+        return;
     }
+    const double gl = d.grad_loss[b];
+    for (int t = lo + tid; t < hi; t += kT)
+        adj[t - lo] = gl * d.cost[t];
+    double a_own[kSL], b_own[kSL];
+#pragma unroll
+    for (int s = 0; s < kSL; ++s) {
+        const int i = kSL * tid + s, j = kSL * tid + s;
+        a_own[s] = i < N ? d.alpha[L * BN + (size_t)b * N + i] : 0.0;
+        b_own[s] = j < M ? d.beta[L * BM + (size_t)b * M + j] : 0.0;
+        if (j < M) { // no pending column update before the last iteration
+            vb[j] = b_own[s];
+            si[j] = 1.0;
+            qc[j] = 0.0;
+        }
+    }
+    __syncthreads();
 
     for (int l = L; l >= 1; --l) {
-        double a_prev[SL], r_own[SL], s_own[SL];
+        // saved values of this iteration, loaded ahead of their use
+        double rden[kSL], a_prev[kSL], sden[kSL], b_prev[kSL];
 #pragma unroll
-        for (int s = 0; s < SL; ++s) {
-            const int i = cr.own[s], j = cc.own[s];
-            r_own[s] = i >= 0 ? d.rden[(l - 1) * BN + (size_t)b * N + i] : 1.0;
-            a_prev[s] = i >= 0 ? d.alpha[(l - 1) * BN + (size_t)b * N + i] : 0.0;
-            s_own[s] = j >= 0 ? d.sden[(l - 1) * BM + (size_t)b * M + j] : 1.0;
-            if (j >= 0)
-                sh.vb[j] = b_own[s];
+        for (int s = 0; s < kSL; ++s) {
+            const int k = kSL * tid + s;
+            rden[s] = k < N ? d.rden[(l - 1) * BN + (size_t)b * N + k] : 1.0;
+            a_prev[s] = k < N ? d.alpha[(l - 1) * BN + (size_t)b * N + k] : 0.0;
+            sden[s] = k < M ? d.sden[(l - 1) * BM + (size_t)b * M + k] : 1.0;
+            b_prev[s] = (k < M && l > 1) ? d.beta[(l - 1) * BM + (size_t)b * M + k] : 0.0;
         }
-        // orders the previous column step's adjoint updates (or the initial
-        // adjoint) before this row step, and publishes vb = beta^l
-        wg_barrier<ADJ_LDS>();
-        // adjoint of the row scaling: d_i = sum_row ubar alpha^l_i P0 beta^l_j;
-        // ubar <- (ubar - d_i) / (R_i + eps) on the row's pairs
+        // row pieces: apply the pending column update, then partial sums of
+        // ubar * P0 * beta^l over each piece
+        // (all adjoint loads of the phase are issued before its first store)
+        double m[SLP][kP];
 #pragma unroll
-        for (int s = 0; s < SL; ++s) {
-            if (cr.own[s] >= 0) {
-                const double ai = a_own[s];
-                const double dsum =
-                    lsum(cr, orow, lo, sh.tr, s, [&](int j, float p0, int p) { return adj[p] * (ai * (double)p0 * sh.vb[j]); });
-                const double ri = 1.0 / r_own[s], q = dsum * ri;
-                leach(cr, orow, lo, sh.tr, s, [&](int, float, int p, bool real) {
+        for (int s = 0; s < SLP; ++s)
+            if (wave_active(pr, s)) {
+                int e = 0;
+                pvisit(pr, s, [&](int, float, int p, bool real) { m[s][e++] = real ? adj[p] : 0.0; });
+            }
+#pragma unroll
+        for (int s = 0; s < SLP; ++s)
+            if (wave_active(pr, s)) {
+                double acc = 0.0;
+                int e = 0;
+                pvisit(pr, s, [&](int j, float p0, int p, bool real) {
+                    const double a = m[s][e++] * si[j] - qc[j];
                     if (real)
-                        adj[p] = adj[p] * ri - q;
+                        adj[p] = a;
+                    acc += a * ((double)p0 * vb[j]);
                 });
+                part[s * kT + tid] = acc;
+            }
+        __syncthreads();
+        // row owners (adjoint of Eq. 4): d_i = alpha^l_i * sum; publish
+        // 1/(R + eps) and q = d_i/(R + eps), and alpha^(l-1) for the columns
+#pragma unroll
+        for (int s = 0; s < kSL; ++s) {
+            const int i = kSL * tid + s;
+            if (i < N) {
+                const double dsum = a_own[s] * owner_sum(owr, s, part);
+                const double r = 1.0 / rden[s];
+                ri[i] = r;
+                qr[i] = dsum * r;
+                va[i] = a_prev[s];
             }
         }
-#pragma unroll
-        for (int s = 0; s < SL; ++s) {
-            const int i = cr.own[s];
-            if (i >= 0)
-                sh.va[i] = a_prev[s];
-        }
-        wg_barrier<ADJ_LDS>();
-        // adjoint of the column scaling: e_j = sum_col wbar alpha^(l-1)_i P0 beta^l_j
-#pragma unroll
-        for (int s = 0; s < SL; ++s) {
-            if (cc.own[s] >= 0) {
-                const double bj = b_own[s];
-                const double esum =
-                    lsum(cc, ocol, lo, sh.tc, s, [&](int i, float p0, int p) { return adj[p] * (sh.va[i] * (double)p0 * bj); });
-                const double ri = 1.0 / s_own[s], q = esum * ri;
-                leach(cc, ocol, lo, sh.tc, s, [&](int, float, int p, bool real) {
-                    if (real)
-                        adj[p] = adj[p] * ri - q;
-                });
-            }
-        }
-        // the next iteration's own values; vb is rewritten at the top of the
-        // next iteration, after every lane has passed this iteration's second
-        // barrier, the last point where it was read
-#pragma unroll
-        for (int s = 0; s < SL; ++s) {
-            const int j = cc.own[s];
-            a_own[s] = a_prev[s];
-            if (l > 1)
-                b_own[s] = j >= 0 ? d.beta[(l - 1) * BM + (size_t)b * M + j] : 0.0;
-        }
-    }
-    if (ADJ_LDS) {
         lds_barrier();
-        for (int t = lo + tid; t < hi; t += T)
-            d.adj[t] = adj[t - lo];
+        // column pieces: apply the row update, then partial sums of
+        // wbar * alpha^(l-1) * P0 over each piece
+#pragma unroll
+        for (int s = 0; s < SLP; ++s)
+            if (wave_active(pc, s)) {
+                int e = 0;
+                pvisit(pc, s, [&](int, float, int p, bool real) { m[s][e++] = real ? adj[p] : 0.0; });
+            }
+#pragma unroll
+        for (int s = 0; s < SLP; ++s)
+            if (wave_active(pc, s)) {
+                double acc = 0.0;
+                int e = 0;
+                pvisit(pc, s, [&](int i, float p0, int p, bool real) {
+                    const double a = m[s][e++] * ri[i] - qr[i];
+                    if (real)
+                        adj[p] = a;
+                    acc += a * (va[i] * (double)p0);
+                });
+                part[s * kT + tid] = acc;
+            }
+        __syncthreads();
+        // column owners (adjoint of Eq. 3): e_j = beta^l_j * sum; publish
+        // 1/(S + eps), q = e_j/(S + eps), and beta^(l-1) for the next rows
+#pragma unroll
+        for (int s = 0; s < kSL; ++s) {
+            const int j = kSL * tid + s;
+            if (j < M) {
+                const double esum = b_own[s] * owner_sum(owc, s, part);
+                const double r = 1.0 / sden[s];
+                si[j] = r;
+                qc[j] = esum * r;
+                vb[j] = b_prev[s];
+            }
+            a_own[s] = a_prev[s];
+            b_own[s] = b_prev[s];
+        }
+        lds_barrier();
+    }
+    // the last column update
+    for (int t = lo + tid; t < hi; t += kT) {
+        const int j = d.csr_col[t];
+        adj[t - lo] = adj[t - lo] * si[j] - qc[j];
     }
 }
 
@@ -555,38 +585,36 @@ __global__ __launch_bounds__(kBlock) void k_bwd_sink_col(DevPlan d, int l)
 
 } // namespace
 
-bool sinkhorn_per_sample_ok(int N, int M) { return N <= kCover && M <= kCover; }
+bool sinkhorn_per_sample_ok(int N, int M, int64_t max_pairs)
+{
+    return N <= kCover && M <= kCover && max_pieces(std::max(N, M), max_pairs) <= (int64_t)kFwdSLP * kT;
+}
 
 bool sinkhorn_bwd_per_sample_ok(int N, int M, int64_t max_pairs)
 {
-    return sinkhorn_per_sample_ok(N, M) && max_pairs <= 65536; // positions are packed in 16 bits
+    return N <= kCover && M <= kCover && max_pieces(std::max(N, M), max_pairs) <= (int64_t)kBwdSLP * kT &&
+           max_pairs <= 65536; // positions within a sample are packed in 16 bits
 }
 
 hipError_t launch_sinkhorn_fwd(const DevPlan &d, double eps, hipStream_t s)
 {
-    const size_t bytes = kLSharedBytes + kLoadScratchBytes;
+    const size_t bytes = fwd_lds_bytes();
     hipError_t e = hipFuncSetAttribute((const void *)k_sinkhorn_fwd,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(k_sinkhorn_fwd, dim3(d.B), dim3(kFwdT), bytes, s, d, eps);
+    hipLaunchKernelGGL(k_sinkhorn_fwd, dim3(d.B), dim3(kT), bytes, s, d, eps);
     return hipGetLastError();
 }
 
-hipError_t launch_sinkhorn_bwd(const DevPlan &d, int64_t max_pairs, hipStream_t s)
+hipError_t launch_sinkhorn_bwd(const DevPlan &d, hipStream_t s)
 {
-    const size_t budget = 160 * 1024;
-    const size_t adj_bytes = 8 * (size_t)max_pairs;
-    const bool adj_lds = kLSharedBytes + std::max(adj_bytes, kLoadScratchBytes) <= budget;
-    const size_t bytes = kLSharedBytes + (adj_lds ? std::max(adj_bytes, kLoadScratchBytes) : kLoadScratchBytes);
-    const void *k = adj_lds ? (const void *)k_sinkhorn_bwd<true> : (const void *)k_sinkhorn_bwd<false>;
-    hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    const size_t bytes = bwd_lds_bytes();
+    hipError_t e = hipFuncSetAttribute((const void *)k_sinkhorn_bwd,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess)
         return e;
-    if (adj_lds)
-        hipLaunchKernelGGL(k_sinkhorn_bwd<true>, dim3(d.B), dim3(kBwdT), bytes, s, d);
-    else
-        hipLaunchKernelGGL(k_sinkhorn_bwd<false>, dim3(d.B), dim3(kBwdT), bytes, s, d);
+    hipLaunchKernelGGL(k_sinkhorn_bwd, dim3(d.B), dim3(kT), bytes, s, d);
     return hipGetLastError();
 }
 
