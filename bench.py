@@ -35,6 +35,74 @@ HBM_PEAK = 8.0e12
 OPS_PER_PAIR_DIR = 8
 
 
+# Algorithmic work of each phase of one step, per launch (the library records
+# one HIP event pair per phase on its stream). Dense phases count VALU
+# operations per point pair; sparse phases count bytes per stored entry of the
+# support (nnz after symmetrization), as the method must move them at least
+# once: emission 16 B, CSR/CSC build 32 B, softmaxes 24 B, Sinkhorn 8 B per
+# entry and half-step forward (+8 B for the loss) and 16 B per entry and
+# half-step in reverse, softmax/temperature adjoint 24 B + distance gradient
+# 8 B.
+def _ops(per_pair):
+    return lambda w, pairs, nnz: per_pair * pairs
+
+
+def _bytes(per_entry_fn):
+    return lambda w, pairs, nnz: per_entry_fn(w) * nnz
+
+
+PHASE_MODEL = {
+    "stats": ("alu", _ops(2 * OPS_PER_PAIR_DIR), "VALU ops",
+              "k_top2: minimum and second minimum of every row and column"),
+    "support": ("alu", _ops(OPS_PER_PAIR_DIR), "VALU ops",
+                "k_emit: radius test of every pair, emission of the candidate support"),
+    "build": ("hbm", _bytes(lambda w: 16 + 32), "bytes", "CSR fill + CSC build"),
+    "softmax": ("hbm", _bytes(lambda w: 24), "bytes", "k_row_softmax + k_col_softmax (Eq. 1, Eq. 2, P0)"),
+    "sinkhorn": ("hbm", _bytes(lambda w: 2 * w.n_iter * 8 + 8), "bytes",
+                 "k_sinkhorn_fwd: L Sinkhorn iterations (Eq. 3, Eq. 4) and the loss"),
+    "bwd_sinkhorn": ("hbm", _bytes(lambda w: 2 * w.n_iter * 16), "bytes",
+                     "k_sinkhorn_bwd: reverse Sinkhorn sweeps"),
+    "bwd_softmax": ("hbm", _bytes(lambda w: 24 + 8), "bytes",
+                    "softmax and temperature adjoints, distance gradient (Eq. 5)"),
+}
+
+# HBM bytes per launch measured with rocprofv3 counters (FETCH_SIZE and
+# WRITE_SIZE, KiB per dispatch, each scaled by the same counter's reading for
+# a plain device copy of known size). Each entry names the source file it was
+# measured on and that file's SHA-256: once the file changes, traffic is
+# reported as null until measured again.
+TRAFFIC = {
+    "stats": {"source": "paper_2512_19743_amd/csrc/dense.hip", "sha256": "f399107bed24cfcc2ea41a6d8214c225236a4b4d616063b962cbfcd3d9a07386",
+              "kernels": ["k_top2"], "bytes_per_launch": 27850447},
+    "support": {"source": "paper_2512_19743_amd/csrc/dense.hip", "sha256": "f399107bed24cfcc2ea41a6d8214c225236a4b4d616063b962cbfcd3d9a07386",
+              "kernels": ["k_emit"], "bytes_per_launch": 24107499},
+    "build": {"source": "paper_2512_19743_amd/csrc/build.hip", "sha256": "0d4b8abe202b425f1450e3ba02cf243d36f99f55e84e53020b40c004ae146fa6",
+              "kernels": ["k_csr_fill", "k_ovf_fill", "k_col_hist", "k_scan_reduce", "k_scan_tiles", "k_scan_apply", "k_csc_fill", "k_csc_sort"], "bytes_per_launch": 78878543},
+    "softmax": {"source": "paper_2512_19743_amd/csrc/softmax.hip", "sha256": "b01efbbd9d54d1f5d88cb80f906e1e04475b4fe6c2354ea28c5d5324ce972d0c",
+              "kernels": ["k_row_softmax", "k_col_softmax"], "bytes_per_launch": 120298708},
+    "sinkhorn": {"source": "paper_2512_19743_amd/csrc/sinkhorn.hip", "sha256": "ed5c3a1a8c923176204281003249261a8e143f981b9e9d6237e83a943749bb9d",
+              "kernels": ["k_sinkhorn_fwd"], "bytes_per_launch": 41521939},
+    "bwd_sinkhorn": {"source": "paper_2512_19743_amd/csrc/sinkhorn.hip", "sha256": "ed5c3a1a8c923176204281003249261a8e143f981b9e9d6237e83a943749bb9d",
+              "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 60778166},
+    "bwd_softmax": {"source": "paper_2512_19743_amd/csrc/softmax.hip", "sha256": "b01efbbd9d54d1f5d88cb80f906e1e04475b4fe6c2354ea28c5d5324ce972d0c",
+              "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 109464758},
+}
+
+
+def _sha(path):
+    import hashlib
+
+    with open(os.path.join(ROOT, path), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def traffic_for(phase, d):
+    t = TRAFFIC.get(phase)
+    if not t or _sha(t["source"]) != t["sha256"]:
+        return None
+    return t["bytes_per_launch"]
+
+
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -43,6 +111,7 @@ def parse():
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--cpu-baseline", choices=["on", "off"], default="on")
     ap.add_argument("--cpu-repeats", type=int, default=3)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (5 times), to scale HBM byte counters")
     return ap.parse_args()
@@ -106,8 +175,7 @@ def main():
     stored = plan.info().stored_pairs
     plan.close()
 
-    apml.apml_profile_reset()
-    apml.apml_profile_enable(True)
+    # timed region: K steps, library profiling off
     apml.apml_reset_peak_memory()
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
@@ -119,20 +187,43 @@ def main():
     e1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    apml.apml_profile_enable(False)
     ms = e0.elapsed_time(e1) / args.steps
-    phases = apml.apml_profile_read()
     mem = apml.apml_get_memory_stats()
+
+    # per-phase split: the same K steps again with HIP events recorded by the
+    # library on its stream around each phase
+    apml.apml_profile_reset()
+    apml.apml_profile_enable(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    apml.apml_profile_enable(False)
+    phases = apml.apml_profile_read()
 
     pairs = w.B * w.N * w.M
     value = pairs / (ms * 1e-3)
-    # dominant kernel: the statistics scan (one launch per step, both directions)
-    stats_ms, stats_n = phases["stats"]
-    stats_avg = stats_ms / max(stats_n, 1)
-    ops = 2 * pairs * OPS_PER_PAIR_DIR
-    achieved = ops / (stats_avg * 1e-3)
-    support_ms, support_n = phases["support"]
-    support_avg = support_ms / max(support_n, 1)
+    nnz_total = int(nnz.sum())
+    kernels = {}
+    for name, (tot_ms, n) in phases.items():
+        if n == 0 or name not in PHASE_MODEL:
+            continue
+        bound, per, unit_kind, what = PHASE_MODEL[name]
+        avg = tot_ms / n
+        work = per(w, pairs, nnz_total)
+        achieved = work / (avg * 1e-3)
+        peak = VALU_PEAK_OPS if bound == "alu" else HBM_PEAK
+        kernels[name] = {"kernel": what, "bound": bound, "avg_launch_ms": avg, "launches_per_step": n / args.steps,
+                         "work_per_launch": work, "work_unit": unit_kind,
+                         "achieved": achieved / (1e12 if bound == "alu" else 1e9),
+                         "unit": "TOP/s" if bound == "alu" else "GB/s", "frac": achieved / peak,
+                         "traffic": traffic_for(name, None)}
+    dom = max(kernels, key=lambda k: kernels[k]["avg_launch_ms"] * kernels[k]["launches_per_step"])
+    d = kernels[dom]
+    roofline = {"bound": d["bound"], "achieved": d["achieved"],
+                "peak": VALU_PEAK_OPS / 1e12 if d["bound"] == "alu" else HBM_PEAK / 1e9,
+                "unit": d["unit"], "frac": d["frac"], "traffic": traffic_for(dom, d),
+                "kernel": d["kernel"], "phase": dom, "avg_launch_ms": d["avg_launch_ms"],
+                "work_per_launch": d["work_per_launch"], "work_unit": d["work_unit"]}
 
     line = {
         "metric": METRIC,
@@ -150,23 +241,12 @@ def main():
         "config": {"workload": f"config {w.cfg} ({w.name}): B={w.B} N={w.N} M={w.M} L={w.n_iter}, "
                                f"{w.reference} reference, {w.prediction} prediction sigma={w.sigma}",
                    "B": w.B, "N": w.N, "M": w.M, "n_iter": w.n_iter, "tau": 1e-8, "p_min": 0.8},
-        "roofline": {
-            "kernel": "k_top2 (minimum / second minimum scan, rows and columns)",
-            "bound": "alu",
-            "achieved": achieved / 1e12,
-            "peak": VALU_PEAK_OPS / 1e12,
-            "unit": "TOP/s",
-            "frac": achieved / VALU_PEAK_OPS,
-            "traffic": None,
-            "avg_launch_ms": stats_avg,
-            "ops_per_launch": ops,
-        },
+        "roofline": roofline,
         "peak_hbm_mb": mem["peak_in_use"] / 1e6,
-        "support": {"nnz_total": int(nnz.sum()), "nnz_per_row": float(nnz.sum()) / (w.B * w.N),
+        "support": {"nnz_total": nnz_total, "nnz_per_row": nnz_total / (w.B * w.N),
                     "stored_pairs": int(stored)},
         "phases_ms_per_step": {k: v[0] / args.steps for k, v in phases.items()},
-        "support_scan": {"avg_launch_ms": support_avg,
-                         "frac_valu": pairs * OPS_PER_PAIR_DIR / (support_avg * 1e-3) / VALU_PEAK_OPS},
+        "kernels": kernels,
         "wall_ms_per_step": wall * 1e3 / args.steps,
     }
 
@@ -181,7 +261,9 @@ def main():
             idx = [0]
             sample = "sample 0 of the workload, forward + backward"
         times = []
-        for _ in range(max(1, args.cpu_repeats)):
+        t_start = time.perf_counter()
+        # at least cpu_repeats runs and about ten seconds of CPU work
+        while len(times) < max(1, args.cpu_repeats) or time.perf_counter() - t_start < args.cpu_seconds:
             t = time.perf_counter()
             oracle.run_batch(X[idx], Y[idx], op, grad=True)
             times.append(time.perf_counter() - t)
