@@ -260,6 +260,8 @@ struct apml_plan {
     hipStream_t stream = nullptr;
     int64_t stored = 0;     // stored pairs
     int64_t max_sample = 0; // stored pairs of the largest sample
+    bool sink_fwd = false;  // per-sample Sinkhorn kernels take this plan (forward)
+    bool sink_bwd = false;  // and the reverse sweeps
     Arena keep;         // everything backward and export need
     DevPlan dv{};       // device arrays (x, y and the backward fields are set per call)
 };
@@ -471,18 +473,22 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     ea.ovf_cap = (unsigned)std::max<int64_t>(65536, 2 * (int64_t)(BN + BM));
     ea.ovf = tmp.get<OverflowEntry>(ea.ovf_cap);
     ea.ctr = dv.ctr;
+    ea.col_cnt = ba.col_cnt; // cleared by the finalize kernel
     const int tile = scan_tile_items();
     ScanArray sr{ea.cnt, BN, ea.S, dv.row_ptr, tmp.get<int32_t>(ceil_div(BN, tile)), ceil_div(BN, tile)};
     if (tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (support)");
     int32_t *offsets_dev = tmp.get<int32_t>((size_t)B + 1);
-    std::vector<int32_t> offsets((size_t)B + 1);
+    int32_t *pieces_dev = tmp.get<int32_t>(3 * (size_t)B);
+    std::vector<int32_t> offsets((size_t)B + 1), pieces(3 * (size_t)B);
     if (tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (support)");
     Counters hc{};
     for (int attempt = 0; attempt < 2; ++attempt) {
-        if (attempt > 0)
+        if (attempt > 0) {
             HIP_TRY(hipMemsetAsync(dv.ctr, 0, sizeof(Counters), s));
+            HIP_TRY(hipMemsetAsync(ba.col_cnt, 0, sizeof(int32_t) * (size_t)BM, s));
+        }
         {
             PhaseTimer pt(PH_SUPPORT, s);
             launch_emit(ea, s);
@@ -491,8 +497,10 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         }
         launch_scan(sr, s); // row offsets, while the host waits for the count
         launch_sample_offsets(dv.row_ptr, B, N, offsets_dev, s);
+        launch_piece_counts(dv.row_ptr, ba.col_cnt, B, N, M, pieces_dev, s);
         HIP_TRY(hipMemcpyAsync(&hc, dv.ctr, sizeof(Counters), hipMemcpyDeviceToHost, s));
         HIP_TRY(hipMemcpyAsync(offsets.data(), offsets_dev, sizeof(int32_t) * (B + 1), hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipMemcpyAsync(pieces.data(), pieces_dev, sizeof(int32_t) * 3 * B, hipMemcpyDeviceToHost, s));
         HIP_TRY(hipStreamSynchronize(s));
         if (hc.overflow <= ea.ovf_cap)
             break;
@@ -513,6 +521,8 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     for (int b = 0; b < B; ++b)
         plan->max_sample = std::max<int64_t>(plan->max_sample, offsets[b + 1] - offsets[b]);
     dv.nnz = nnz;
+    plan->sink_fwd = sinkhorn_fwd_fits(N, M, pieces.data(), B);
+    plan->sink_bwd = plan->sink_fwd && sinkhorn_bwd_fits(N, M, pieces.data(), B, plan->max_sample);
 
     // ---- sparse structure -------------------------------------------------
     PhaseTimer pt_build(PH_BUILD, s);
@@ -560,6 +570,16 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     dv.sden = keep.get<double>((size_t)std::max(L, 1) * BM);
     dv.dvec = keep.get<double>(BN);
     dv.evec = keep.get<double>(BM);
+    if (plan->sink_fwd) {
+        const size_t w = packed_order_words(B);
+        for (PackedOrder *pk : {&dv.pk_row, &dv.pk_col}) {
+            pk->p0 = keep.get<float>(w);
+            pk->gi = keep.get<uint32_t>(w / 2);
+            pk->info = keep.get<uint32_t>(w / kSinkPiece);
+            pk->pos = pk == &dv.pk_col ? keep.get<uint32_t>(w / 2) : nullptr;
+            pk->n_pos = keep.get<int32_t>(B);
+        }
+    }
     if (keep.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (plan)");
     {
@@ -572,7 +592,11 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     // ---- Sinkhorn (Eq. 3, Eq. 4) and the loss ------------------------------
     {
         PhaseTimer pt(PH_SINKHORN, s);
-        if (sinkhorn_per_sample_ok(N, M, plan->max_sample)) {
+        if (plan->sink_fwd) {
+            int32_t *place = tmp.get<int32_t>((size_t)B * 2 * kSinkOwners);
+            if (tmp.failed)
+                return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (pieces)");
+            launch_pack(dv, place, s);
             HIP_TRY(launch_sinkhorn_fwd(dv, prm.eps_stab, s));
         } else {
             launch_sinkhorn_fwd_steps(dv, prm.eps_stab, s);
@@ -610,8 +634,8 @@ apml_status apml_backward(apml_plan *plan, const float *x, const float *y, const
     {
         PhaseTimer pt(PH_BWD_SINK, s);
         if (dv.L > 0) {
-            if (sinkhorn_bwd_per_sample_ok(dv.N, dv.M, plan->max_sample)) {
-                HIP_TRY(launch_sinkhorn_bwd(dv, s));
+            if (plan->sink_bwd) {
+                HIP_TRY(launch_sinkhorn_bwd(dv, plan->max_sample, s));
             } else {
                 launch_sinkhorn_bwd_steps(dv, s);
                 HIP_TRY(hipGetLastError());

@@ -77,6 +77,7 @@ struct EmitArgs {
     OverflowEntry *ovf;
     unsigned ovf_cap;
     Counters *ctr;
+    int32_t *col_cnt;    // [B*M] stored pairs per column, counted during emission
 };
 void launch_emit(const EmitArgs &a, hipStream_t s);
 
@@ -95,6 +96,28 @@ struct ScanArray {
 };
 int scan_tile_items();
 void launch_scan(const ScanArray &a, hipStream_t s);
+
+// Pieces of the per-sample Sinkhorn kernels. Each row's (column's) pairs are
+// cut into pieces of kSinkPiece consecutive pairs; an owner with n pieces
+// takes a group of 2^ceil(log2 n) consecutive positions (padding pieces are
+// empty), groups are ordered by size, largest first, so every group is
+// aligned to its size. Position p belongs to lane p % kSinkLanes, slot
+// p / kSinkLanes. Arrays are plane-major so that the lanes of a wave read
+// consecutive words: word w of lane l, slot s, sample b sits at
+// ((b * kSinkSlots + s) * words + w) * kSinkLanes + l.
+constexpr int kSinkLanes = 1024; // threads of a per-sample Sinkhorn workgroup
+constexpr int kSinkSlots = 5;    // positions per lane and order
+constexpr int kSinkPiece = 4;    // pairs per piece
+constexpr int kSinkOwners = 2048; // rows or columns a workgroup covers
+constexpr int kSinkMaxGroup = 64; // largest group (pieces of one owner)
+
+struct PackedOrder {
+    float *p0;      // [B][slots][kSinkPiece][lanes]: P0 (0 for padding)
+    uint32_t *gi;   // [B][slots][kSinkPiece/2][lanes]: gathered index | real << 15, two per word
+    uint32_t *info; // [B][slots][lanes]: owner | log2(group) << 11 | head << 14 | valid << 15 | first position << 16 (rows)
+    uint32_t *pos;  // [B][slots][kSinkPiece/2][lanes]: row-major positions within the sample (columns only)
+    int32_t *n_pos; // [B]: positions used
+};
 
 // Device view of a plan, passed by value to the sparse kernels.
 struct DevPlan {
@@ -123,6 +146,7 @@ struct DevPlan {
     float *grad_x, *grad_y;
     double *adj, *cbar;           // [nnz] row-major
     double *dvec, *evec;          // [B*N], [B*M] scratch when the scalings do not fit in LDS
+    PackedOrder pk_row, pk_col;   // per-sample Sinkhorn pieces (when that path is taken)
 };
 
 struct BuildArgs {
@@ -141,13 +165,23 @@ void launch_softmax(const DevPlan &d, const Params &p, hipStream_t s);
 void launch_bwd_softmax(const DevPlan &d, const Params &p, hipStream_t s);
 
 // Sinkhorn. The per-sample kernels run all iterations in one workgroup per
-// sample with the sample's pairs in registers (N, M <= 2048 and a bounded
-// number of pairs per sample, max_pairs); the per-iteration kernels are the
-// general fallback.
-bool sinkhorn_per_sample_ok(int N, int M, int64_t max_pairs);
-bool sinkhorn_bwd_per_sample_ok(int N, int M, int64_t max_pairs);
+// sample with the sample's pairs in registers; the per-iteration kernels are
+// the general fallback.
+//
+// Per sample b, out[3b..3b+2] = positions needed by the rows, by the columns,
+// and the most pieces of any row or column (row lengths from row_ptr, column
+// lengths from col_cnt).
+void launch_piece_counts(const int32_t *row_ptr, const int32_t *col_cnt, int B, int N, int M, int32_t *out,
+                         hipStream_t s);
+// Whether the per-sample kernels take a batch: counts are the host copy of the
+// piece counts above, max_pairs the largest sample's stored pairs.
+bool sinkhorn_fwd_fits(int N, int M, const int32_t *counts, int B);
+bool sinkhorn_bwd_fits(int N, int M, const int32_t *counts, int B, int64_t max_pairs);
+size_t packed_order_words(int B); // 32-bit words of one PackedOrder's p0 array
+// Lays out the pieces of both orders; place: [B][2][2048] int32 scratch.
+void launch_pack(const DevPlan &d, int32_t *place, hipStream_t s);
 hipError_t launch_sinkhorn_fwd(const DevPlan &d, double eps, hipStream_t s);
-hipError_t launch_sinkhorn_bwd(const DevPlan &d, hipStream_t s);
+hipError_t launch_sinkhorn_bwd(const DevPlan &d, int64_t max_pairs, hipStream_t s);
 void launch_sinkhorn_fwd_steps(const DevPlan &d, double eps, hipStream_t s);
 void launch_sinkhorn_bwd_steps(const DevPlan &d, hipStream_t s);
 

@@ -138,15 +138,6 @@ __global__ __launch_bounds__(kBlock) void k_ovf_fill(DevPlan d, BuildArgs a)
 // column-major permutation
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(kBlock) void k_col_hist(DevPlan d, BuildArgs a)
-{
-    const int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (t >= d.nnz)
-        return;
-    const int b = d.csr_row[t] / d.N;
-    atomicAdd(&a.col_cnt[(size_t)b * d.M + d.csr_col[t]], 1);
-}
-
 // Places every pair in its column segment; the order inside a segment
 // depends on the atomics and is fixed by k_csc_sort.
 __global__ __launch_bounds__(kBlock) void k_csc_fill(DevPlan d, BuildArgs a)
@@ -237,8 +228,8 @@ void launch_csr_fill(const DevPlan &d, const BuildArgs &a, hipStream_t s)
 
 void launch_csc_build(const DevPlan &d, const BuildArgs &a, hipStream_t s)
 {
+    // a.col_cnt holds the stored pairs per column, counted during emission
     const unsigned g = blocks_for(d.nnz, kBlock);
-    hipLaunchKernelGGL(k_col_hist, dim3(g), dim3(kBlock), 0, s, d, a);
     const int n = d.B * d.M;
     ScanArray sc{a.col_cnt, n, 1, d.col_ptr, a.col_tiles, (n + kScanTile - 1) / kScanTile};
     launch_scan(sc, s);

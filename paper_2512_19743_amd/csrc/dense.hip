@@ -14,8 +14,8 @@
 //              column's threshold. Per pair 6 VALU ops for the distance and two
 //              compares whose wave masks are combined on the scalar unit. Each
 //              lane appends its row's pairs, in column order, to a private slot
-//              group; the exact test s >= tau is applied later in double
-//              precision on this candidate set.
+//              group and counts it in its column; the exact test s >= tau is
+//              applied later in double precision on this candidate set.
 #include "apml_internal.h"
 #include "device_common.h"
 
@@ -116,10 +116,12 @@ __global__ __launch_bounds__(kBlock) void k_finalize(FinalizeArgs args)
     }
 }
 
-// Appends pair (row, j) to the lane's slot group, or to the overflow list.
-__device__ __forceinline__ void emit_pair(const EmitArgs &a, int32_t *slot, int row, int ch, int j,
-                                          int &cnt)
+// Appends pair (row, j) to the lane's slot group, or to the overflow list,
+// and counts it in its column.
+__device__ __forceinline__ void emit_pair(const EmitArgs &a, int32_t *slot, int32_t *col_cnt, int row, int ch,
+                                          int j, int &cnt)
 {
+    atomicAdd(&col_cnt[j], 1);
     if (cnt < a.K) {
         slot[cnt] = j;
     } else {
@@ -148,6 +150,7 @@ __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs a)
     const int j0 = ch * a.chunk;
     const int j1 = min(a.M, j0 + a.chunk);
     int32_t *slot = a.slots + ((size_t)row * a.S + ch) * a.K;
+    int32_t *col_cnt = a.col_cnt + (size_t)b * a.M;
     const int lane = lane_id();
     int cnt = 0;
     int j = j0;
@@ -166,7 +169,7 @@ __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs a)
 #pragma unroll
             for (int u = 0; u < 4; ++u)
                 if ((mk[u] >> lane) & 1ull)
-                    emit_pair(a, slot, row, ch, j + u, cnt);
+                    emit_pair(a, slot, col_cnt, row, ch, j + u, cnt);
         }
     }
     for (; j < j1; ++j) {
@@ -175,7 +178,7 @@ __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs a)
         const unsigned long long m =
             (__builtin_amdgcn_ballot_w64(s <= E) | __builtin_amdgcn_ballot_w64(s <= yv.w)) & valid_mask;
         if ((m >> lane) & 1ull)
-            emit_pair(a, slot, row, ch, j, cnt);
+            emit_pair(a, slot, col_cnt, row, ch, j, cnt);
     }
     if (valid)
         a.cnt[(size_t)row * a.S + ch] = cnt;

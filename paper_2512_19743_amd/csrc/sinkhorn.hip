@@ -9,26 +9,27 @@
 // which is Eq. 3 / Eq. 4 exactly, including eps. A sweep reads P0 and the
 // indices once and writes no per-pair values.
 //
-// Per-sample kernels (N, M <= kCover): one workgroup per sample runs all 2L
-// sweeps with the sample's pairs held in registers. Each row's (column's)
-// pairs are cut into pieces of kP consecutive pairs; piece k sits in lane
-// k mod kT, slot k / kT, for the whole kernel. A sweep is two phases:
-//   piece phase  each lane forms the partial sum of each of its pieces
-//                (gathering the other side's scalings from LDS) and stores it
-//                in LDS;
-//   owner phase  the lane owning a row (column) adds its pieces' partials in
-//                piece order and applies the scaling.
-// Every sum has a fixed order, so the result is bitwise reproducible, and no
-// lane walks a long row alone.
+// Per-sample kernels: one 1024-lane workgroup per sample runs all 2L sweeps
+// with the sample's pairs in registers. k_place and k_pack_pairs cut every
+// row's (column's) pairs into pieces of kP and lay them out so that an
+// owner's pieces are consecutive lanes of one wave (see PackedOrder). A sweep has two phases:
+//   piece phase  each lane sums its pieces (gathering the other side's
+//                scalings from LDS); the pieces of one owner are added by a
+//                butterfly inside their aligned lane group, in a fixed order,
+//                and the group's first lane stores the owner's sum in LDS;
+//   owner phase  lane t owns rows (columns) 2t and 2t+1: it reads the sum and
+//                applies the scaling.
+// Sums have a fixed association, so results are bitwise reproducible.
 //
 // Reverse sweeps: for u = w/(R + eps) with R = sum over the row of w,
 //   wbar = (ubar - sum_row ubar*u) / (R + eps),
-// and likewise for the columns. The per-pair adjoint lives in global memory
-// (it stays in L2). An update is applied lazily: the owner phase of a row step
-// only publishes 1/(R + eps) and q = (sum_row ubar*u)/(R + eps) per row, and
-// the next piece phase, which visits the pairs in column order, applies
-// wbar = ubar/(R + eps) - q to each pair it reads and writes the result back.
-// So each pair's adjoint is read and written once per sweep.
+// and likewise for the columns. The per-pair adjoint lives in LDS (indexed
+// by row-major position within the sample). An update is applied lazily: the
+// owner phase of a row step only publishes 1/(R + eps) and
+// q = (sum_row ubar*u)/(R + eps) per row, and the next piece phase, which
+// visits the pairs in column order, applies wbar = ubar/(R + eps) - q to each
+// pair it reads and writes the result back. Each pair's adjoint is read and
+// written once per sweep.
 #include <algorithm>
 
 #include "apml_internal.h"
@@ -37,44 +38,192 @@
 namespace apml {
 namespace {
 
-constexpr int kT = 1024;            // threads of a per-sample workgroup
-constexpr int kSL = 2;              // owners per lane: owner o sits in lane o / kSL
-constexpr int kCover = kT * kSL;    // rows or columns a workgroup covers
-constexpr int kP = 4;               // pairs per piece
-constexpr int kFwdSLP = 6;          // piece slots per lane and order, forward
-constexpr int kBwdSLP = 5;          // and reverse
+constexpr int kT = kSinkLanes;
+constexpr int kSLP = kSinkSlots;
+constexpr int kP = kSinkPiece;
+constexpr int kSL = kSinkOwners / kSinkLanes; // owners per lane in the owner phase
+constexpr int kCap = kT * kSLP;               // positions per sample and order
 
-// One order of a sample's pairs: owners are rows (row-major) or columns
-// (column-major).
-struct POrder {
-    const int32_t *ptr;    // [n_own + 1]: global positions of the owners' segments
-    const int32_t *gather; // per pair: index of the other side, within the sample
-    const float *val;      // per pair: P0
-    const int32_t *perm;   // per pair: row-major position (column-major order) or nullptr
-    int n_own;
+__device__ __forceinline__ int pieces_of(int len) { return max(1, (len + kP - 1) / kP); }
+__device__ __forceinline__ int log2_group(int np) { return np <= 1 ? 0 : 32 - __clz(np - 1); }
+
+// Word w of position p in a plane-major packed array with `words` words per
+// position.
+__device__ __forceinline__ size_t pk_index(int b, int p, int w, int words)
+{
+    return (((size_t)b * kSLP + p / kT) * words + w) * kT + p % kT;
+}
+
+__global__ __launch_bounds__(kT) void k_piece_counts(const int32_t *row_ptr, const int32_t *col_cnt, int N, int M,
+                                                     int32_t *out)
+{
+    __shared__ int red[3][kT / 64];
+    const int b = blockIdx.x, tid = threadIdx.x;
+    int pr = 0, pc = 0, mx = 0;
+    for (int i = tid; i < N; i += kT) {
+        const int np = pieces_of(row_ptr[(size_t)b * N + i + 1] - row_ptr[(size_t)b * N + i]);
+        pr += 1 << min(log2_group(np), 30);
+        mx = max(mx, np);
+    }
+    for (int j = tid; j < M; j += kT) {
+        const int np = pieces_of(col_cnt[(size_t)b * M + j]);
+        pc += 1 << min(log2_group(np), 30);
+        mx = max(mx, np);
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+        pr += __shfl_xor(pr, o);
+        pc += __shfl_xor(pc, o);
+        mx = max(mx, __shfl_xor(mx, o));
+    }
+    if (lane_id() == 0) {
+        red[0][tid >> 6] = pr;
+        red[1][tid >> 6] = pc;
+        red[2][tid >> 6] = mx;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int a = 0, c = 0, m = 0;
+        for (int w = 0; w < kT / 64; ++w) {
+            a += red[0][w];
+            c += red[1][w];
+            m = max(m, red[2][w]);
+        }
+        out[3 * b] = a;
+        out[3 * b + 1] = c;
+        out[3 * b + 2] = m;
+    }
+}
+
+// Placement of the pieces of one order (blockIdx.y: 0 rows, 1 columns) of
+// sample blockIdx.x: every owner gets the first position of its group
+// (first | log2(group) << 16 in place[]), the info word of every position is
+// written, and the P0 / index / position words are cleared (k_pack_pairs
+// fills in the real pairs). The host has checked that the positions fit
+// (kCap) and that no owner has more than kSinkMaxGroup pieces.
+__global__ __launch_bounds__(kT) void k_place(DevPlan d, int32_t *place)
+{
+    __shared__ int hist[8], base[8];
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const bool rows = blockIdx.y == 0;
+    const int n_own = rows ? d.N : d.M;
+    const int32_t *ptr = rows ? d.row_ptr + (size_t)b * d.N : d.col_ptr + (size_t)b * d.M;
+    const PackedOrder pk = rows ? d.pk_row : d.pk_col;
+    const int lo = d.row_ptr[(size_t)b * d.N];
+    // clear this sample's words (contiguous blocks of the plane-major arrays)
+    {
+        const size_t np0 = (size_t)kSLP * kP * kT, ngi = np0 / 2;
+        for (size_t k = tid; k < np0; k += kT)
+            pk.p0[(size_t)b * np0 + k] = 0.0f;
+        for (size_t k = tid; k < ngi; k += kT) {
+            pk.gi[(size_t)b * ngi + k] = 0u;
+            if (!rows)
+                pk.pos[(size_t)b * ngi + k] = 0u;
+        }
+    }
+    if (tid < 8)
+        hist[tid] = 0;
+    __syncthreads();
+    int lg[kSL], rk[kSL], st[kSL], len[kSL];
+#pragma unroll
+    for (int s = 0; s < kSL; ++s) {
+        const int k = kSL * tid + s;
+        lg[s] = -1;
+        if (k < n_own) {
+            st[s] = ptr[k];
+            len[s] = ptr[k + 1] - st[s];
+            lg[s] = log2_group(pieces_of(len[s]));
+            rk[s] = atomicAdd(&hist[lg[s]], 1);
+        }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int run = 0;
+        for (int c = 6; c >= 0; --c) { // largest groups first: every group is aligned to its size
+            base[c] = run;
+            run += hist[c] << c;
+        }
+        base[7] = run;
+        pk.n_pos[b] = run;
+    }
+    __syncthreads();
+    for (int p = base[7] + tid; p < kCap; p += kT) // unused positions: invalid
+        pk.info[pk_index(b, p, 0, 1)] = 0u;
+#pragma unroll
+    for (int s = 0; s < kSL; ++s) {
+        if (lg[s] < 0)
+            continue;
+        const int k = kSL * tid + s, c = 1 << lg[s];
+        const int first = base[lg[s]] + (rk[s] << lg[s]);
+        place[((size_t)b * 2 + blockIdx.y) * kSinkOwners + k] = first | (lg[s] << 16);
+        for (int q = 0; q < c; ++q) {
+            uint32_t info = (uint32_t)k | ((uint32_t)lg[s] << 11) | ((q == 0 ? 1u : 0u) << 14) | 0x8000u;
+            if (rows && q * kP < len[s])
+                info |= ((uint32_t)(st[s] + q * kP - lo) & 0xFFFFu) << 16;
+            pk.info[pk_index(b, first + q, 0, 1)] = info;
+        }
+    }
+}
+
+// Writes every stored pair into its piece, one thread per pair and order:
+// P0, the gathered index with its 'real' bit and (columns) the row-major
+// position within the sample.
+__global__ __launch_bounds__(kBlock) void k_pack_pairs(DevPlan d, const int32_t *place)
+{
+    const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const bool rows = g < d.nnz;
+    const int64_t t = rows ? g : g - d.nnz;
+    if (t >= d.nnz)
+        return;
+    const int own_g = rows ? d.csr_row[t] : d.csc_col[t]; // global row or column
+    const int n_own = rows ? d.N : d.M;
+    const int b = own_g / n_own, k = own_g - b * n_own;
+    const int off = (int)(t - (rows ? d.row_ptr[own_g] : d.col_ptr[own_g]));
+    const int q = off / kP, e = off % kP;
+    const int p = (place[((size_t)b * 2 + (rows ? 0 : 1)) * kSinkOwners + k] & 0xFFFF) + q;
+    const PackedOrder &pk = rows ? d.pk_row : d.pk_col;
+    pk.p0[pk_index(b, p, e, kP)] = rows ? d.p0r[t] : d.p0c[t];
+    const int other = rows ? d.csr_col[t] : d.csc_row[t];
+    uint16_t *gi = reinterpret_cast<uint16_t *>(pk.gi + pk_index(b, p, e / 2, kP / 2));
+    gi[e & 1] = (uint16_t)((other & 0x7FFF) | 0x8000);
+    if (!rows) {
+        const int lo = d.row_ptr[(size_t)b * d.N];
+        uint16_t *ps = reinterpret_cast<uint16_t *>(pk.pos + pk_index(b, p, e / 2, kP / 2));
+        ps[e & 1] = (uint16_t)((d.csc_perm[t] - lo) & 0xFFFF);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// per-sample kernels
+// ---------------------------------------------------------------------------
+
+// A lane's positions of one order, in registers for the whole kernel.
+template <bool POS> struct Pieces {
+    float p0[kSLP][kP];
+    uint32_t gi[kSLP][kP / 2];
+    uint32_t pos[POS ? kSLP : 1][POS ? kP / 2 : 1];
+    uint32_t info[kSLP];
+    int n; // positions used (wave-uniform)
 };
 
-enum PosMode { kNoPos, kRunPos, kPairPos };
-
-// A lane's pieces of one order. Per pair: P0, and the gathered index with a
-// 'real' bit (bit 15), two per word; padding entries have P0 = 0, index 0.
-// kRunPos: the first pair's row-major position within the sample (the pairs of
-// a row piece are consecutive); kPairPos: each pair's position, two per word.
-template <int SLP, int PM> struct Pieces {
-    float p0[SLP][kP];
-    uint32_t gi[SLP][kP / 2];
-    uint32_t pos[SLP][PM == kPairPos ? kP / 2 : 1];
-    int n; // number of pieces of the order in this sample (wave-uniform)
-};
-
-// A lane's owners: first piece | piece count << 16.
-struct Owners {
-    uint32_t pp[kSL];
-};
-
-__device__ __forceinline__ int half16(uint32_t w, int e) { return (int)((w >> (16 * (e & 1))) & 0xFFFFu); }
-__device__ __forceinline__ int gidx(uint32_t w, int e) { return half16(w, e) & 0x7FFF; }
-__device__ __forceinline__ bool greal(uint32_t w, int e) { return (half16(w, e) >> 15) != 0; }
+template <bool POS> __device__ void load_pieces(Pieces<POS> &pc, const PackedOrder &pk, int b)
+{
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int s = 0; s < kSLP; ++s) {
+        const int p = s * kT + tid;
+#pragma unroll
+        for (int e = 0; e < kP; ++e)
+            pc.p0[s][e] = pk.p0[pk_index(b, p, e, kP)];
+#pragma unroll
+        for (int w = 0; w < kP / 2; ++w) {
+            pc.gi[s][w] = pk.gi[pk_index(b, p, w, kP / 2)];
+            if (POS)
+                pc.pos[s][w] = pk.pos[pk_index(b, p, w, kP / 2)];
+        }
+        pc.info[s] = pk.info[pk_index(b, p, 0, 1)];
+    }
+    pc.n = __builtin_amdgcn_readfirstlane(pk.n_pos[b]);
+}
 
 // A copy of v that the compiler cannot see through: keeps values derived from
 // the cached words (widened P0, unpacked indices) from being hoisted out of
@@ -85,195 +234,125 @@ template <typename V> __device__ __forceinline__ V opaque(V v)
     return v;
 }
 
-// Workgroup-wide exclusive scan of one int per thread; also returns the total.
-// part: kT/64 ints of LDS.
-__device__ int block_scan(int v, int *part, int &total)
-{
-    const int lane = lane_id(), wave = threadIdx.x >> 6;
-    int inc = v;
-    for (int off = 1; off < 64; off <<= 1) {
-        const int n = __shfl_up(inc, off);
-        if (lane >= off)
-            inc += n;
-    }
-    if (lane == 63)
-        part[wave] = inc;
-    lds_barrier();
-    int base = 0, tot = 0;
-    for (int w = 0; w < kT / 64; ++w) {
-        const int p = part[w];
-        base += w < wave ? p : 0;
-        tot += p;
-    }
-    lds_barrier();
-    total = tot;
-    return base + inc - v;
-}
+__device__ __forceinline__ int half16(uint32_t w, int e) { return (int)((w >> (16 * (e & 1))) & 0xFFFFu); }
 
-// Cuts one order into pieces and loads the lane's pieces into registers.
-// owner_of: SLP*kT words of LDS scratch (free again on return). Returns false
-// when the sample has more pieces than the workgroup holds.
-template <int SLP, int PM>
-__device__ bool pload(Pieces<SLP, PM> &pc, Owners &ow, const POrder &o, int lo, int *part, uint32_t *owner_of)
-{
-    const int tid = threadIdx.x;
-    constexpr int cap = SLP * kT;
-    int np[kSL], local = 0;
-#pragma unroll
-    for (int s = 0; s < kSL; ++s) {
-        const int own = kSL * tid + s;
-        const int n = own < o.n_own ? o.ptr[own + 1] - o.ptr[own] : 0;
-        np[s] = (n + kP - 1) / kP;
-        local += np[s];
-    }
-    int total;
-    int base = block_scan(local, part, total);
-#pragma unroll
-    for (int s = 0; s < kSL; ++s) {
-        ow.pp[s] = (uint32_t)base | ((uint32_t)np[s] << 16);
-        for (int q = 0; q < np[s]; ++q)
-            if (base + q < cap)
-                owner_of[base + q] = (uint32_t)(kSL * tid + s) | ((uint32_t)q << 16);
-        base += np[s];
-    }
-    lds_barrier();
-    pc.n = __builtin_amdgcn_readfirstlane(total);
-    // all slots' loads are independent: no branches between them
-    int t0s[SLP], ns[SLP];
-#pragma unroll
-    for (int s = 0; s < SLP; ++s) {
-        const int k = s * kT + tid;
-        const bool v = k < min(total, cap);
-        const uint32_t w = owner_of[v ? k : 0];
-        const int own = v ? (int)(w & 0xFFFFu) : 0, q = (int)(w >> 16);
-        const int a = o.ptr[own], e = o.ptr[own + 1];
-        t0s[s] = v ? a + q * kP : 0;
-        ns[s] = v ? min(kP, e - (a + q * kP)) : 0;
-    }
-#pragma unroll
-    for (int s = 0; s < SLP; ++s) {
-        const int t0 = t0s[s], n = ns[s];
-#pragma unroll
-        for (int e = 0; e < kP; e += 2) {
-            uint32_t g = 0, wp = 0;
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const bool v = e + h < n;
-                const int t = v ? t0 + e + h : lo; // position lo always exists
-                const uint32_t gv = (uint32_t)o.gather[t];
-                const float pv = o.val[t];
-                g |= (v ? gv | 0x8000u : 0u) << (16 * h);
-                pc.p0[s][e + h] = v ? pv : 0.0f;
-                if (PM == kPairPos) {
-                    const int pp = o.perm[t] - lo;
-                    wp |= ((uint32_t)(v ? pp : 0) & 0xFFFFu) << (16 * h);
-                }
-            }
-            pc.gi[s][e / 2] = g;
-            if (PM == kPairPos)
-                pc.pos[s][e / 2] = wp;
-        }
-        if (PM == kRunPos)
-            pc.pos[s][0] = (uint32_t)(n > 0 ? t0 - lo : 0);
-    }
-    lds_barrier();
-    return total <= cap;
-}
-
-// True when slot s of this wave holds at least one piece.
-template <int SLP, int PM> __device__ __forceinline__ bool wave_active(const Pieces<SLP, PM> &pc, int s)
+// Slot s of this wave holds at least one used position.
+template <bool POS> __device__ __forceinline__ bool wave_active(const Pieces<POS> &pc, int s)
 {
     return s * kT + (int)(threadIdx.x & ~63u) < pc.n;
 }
 
-// Visits the kP entries of piece slot s: f(gathered, p0, position, real).
-// Padding entries have real == false, P0 = 0, gathered index 0 and position
-// 0: they add exact zeros to sums, and f must not store for them.
-template <int SLP, int PM, class F>
-__device__ __forceinline__ void pvisit(const Pieces<SLP, PM> &pc, int s, F f)
+// Visits the kP pairs of slot s: f(e, gathered, p0, real).
+template <bool POS, class F> __device__ __forceinline__ void pvisit(const Pieces<POS> &pc, int s, F f)
 {
-    const int run = PM == kRunPos ? (int)opaque(pc.pos[s][0]) : 0;
 #pragma unroll
     for (int e = 0; e < kP; ++e) {
-        const uint32_t g = opaque(pc.gi[s][e / 2]);
-        const float p0 = opaque(pc.p0[s][e]);
-        const int pos = PM == kPairPos ? half16(opaque(pc.pos[s][e / 2]), e) : run + e;
-        f(gidx(g, e), p0, pos, greal(g, e));
+        const int h = half16(opaque(pc.gi[s][e / 2]), e);
+        f(e, h & 0x7FFF, opaque(pc.p0[s][e]), (h & 0x8000) != 0);
     }
 }
 
-// Sum of the partials of owner slot s, in piece order. The first four are
-// loaded together.
-__device__ __forceinline__ double owner_sum(const Owners &ow, int s, const double *part)
+// v from the lane D positions away (lane ^ D).
+template <int D> __device__ __forceinline__ double xor_lane(double v)
 {
-    const int first = (int)(ow.pp[s] & 0xFFFFu), cnt = (int)(ow.pp[s] >> 16);
-    double v[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-        v[k] = k < cnt ? part[first + k] : 0.0;
-    double acc = ((v[0] + v[1]) + v[2]) + v[3];
-    for (int k = first + 4; k < first + cnt; ++k)
-        acc += part[k];
+    int2 w = __builtin_bit_cast(int2, v);
+    if constexpr (D == 1) {
+        w.x = __builtin_amdgcn_update_dpp(0, w.x, 0xB1, 0xF, 0xF, true); // quad_perm [1,0,3,2]
+        w.y = __builtin_amdgcn_update_dpp(0, w.y, 0xB1, 0xF, 0xF, true);
+    } else if constexpr (D == 2) {
+        w.x = __builtin_amdgcn_update_dpp(0, w.x, 0x4E, 0xF, 0xF, true); // quad_perm [2,3,0,1]
+        w.y = __builtin_amdgcn_update_dpp(0, w.y, 0x4E, 0xF, 0xF, true);
+    } else if constexpr (D < 32) {
+        w.x = __builtin_amdgcn_ds_swizzle(w.x, 0x1F | (D << 10)); // bitmask mode: lane ^ D within 32
+        w.y = __builtin_amdgcn_ds_swizzle(w.y, 0x1F | (D << 10));
+    } else {
+        w.x = __shfl_xor(w.x, D);
+        w.y = __shfl_xor(w.y, D);
+    }
+    return __builtin_bit_cast(double, w);
+}
+
+template <int K> __device__ __forceinline__ void bfly_step(double &acc, int lg, int lgmax)
+{
+    if (K < lgmax) { // wave-uniform
+        const double y = xor_lane<(1 << K)>(acc);
+        if (K < lg)
+            acc += y;
+    }
+}
+
+// Adds the partial sums of each aligned group of 2^lg lanes (lg from info);
+// every lane of a group ends with the same bits. Groups are sorted by size,
+// so the wave's first lane has the largest.
+__device__ __forceinline__ double group_reduce(double acc, uint32_t info)
+{
+    const int lg = (int)((info >> 11) & 7u);
+    const int lgmax = __builtin_amdgcn_readfirstlane(lg);
+    bfly_step<0>(acc, lg, lgmax);
+    bfly_step<1>(acc, lg, lgmax);
+    bfly_step<2>(acc, lg, lgmax);
+    bfly_step<3>(acc, lg, lgmax);
+    bfly_step<4>(acc, lg, lgmax);
+    bfly_step<5>(acc, lg, lgmax);
     return acc;
 }
 
-// Most pieces an order of a sample with n_own owners and at most max_pairs
-// pairs can have: sum over owners of ceil(len / kP).
-inline int64_t max_pieces(int n_own, int64_t max_pairs) { return (max_pairs + (int64_t)(kP - 1) * n_own) / kP; }
+// Stores a group's sum at its owner (first lane of the group).
+__device__ __forceinline__ void store_sum(double acc, uint32_t info, double *sums)
+{
+    if ((info & 0xC000u) == 0xC000u) // valid and head
+        sums[info & 0x7FFu] = acc;
+}
 
-constexpr size_t fwd_lds_bytes() { return 8 * (2 * (size_t)kCover + (size_t)kFwdSLP * kT) + 4 * (kT / 64); }
-constexpr size_t bwd_lds_bytes() { return 8 * (6 * (size_t)kCover + (size_t)kBwdSLP * kT) + 4 * (kT / 64); }
+constexpr size_t fwd_lds_bytes() { return 8 * 3 * (size_t)kSinkOwners; }
+constexpr size_t bwd_fixed_lds_bytes() { return 8 * 4 * (size_t)kSinkOwners; }
 
 __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
 {
-    constexpr int SLP = kFwdSLP;
     extern __shared__ double lds[];
-    double *va = lds, *vb = va + kCover, *part = vb + kCover;
-    int *scan = reinterpret_cast<int *>(part + SLP * kT);
-    uint32_t *owner_of = reinterpret_cast<uint32_t *>(part); // set-up only
+    double *va = lds, *vb = va + kSinkOwners, *sums = vb + kSinkOwners;
     const int b = blockIdx.x, tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
     const int lo = d.row_ptr[(size_t)b * N], hi = d.row_ptr[(size_t)(b + 1) * N];
-    const POrder orow{d.row_ptr + (size_t)b * N, d.csr_col, d.p0r, nullptr, N};
-    const POrder ocol{d.col_ptr + (size_t)b * M, d.csc_row, d.p0c, nullptr, M};
-    Pieces<SLP, kNoPos> pr, pc;
-    Owners owr, owc;
-    bool ok = pload(pr, owr, orow, lo, scan, owner_of);
-    ok = pload(pc, owc, ocol, lo, scan, owner_of) && ok;
-    if (!ok) { // excluded by the host's capacity check; fail loudly if reached
-        if (tid == 0)
-            d.loss[b] = __builtin_nanf("");
-        return;
-    }
-    for (int k = tid; k < N; k += kT) {
-        va[k] = 1.0;
-        d.alpha[(size_t)b * N + k] = 1.0;
-    }
-    for (int k = tid; k < M; k += kT) {
-        vb[k] = 1.0;
-        d.beta[(size_t)b * M + k] = 1.0;
+    Pieces<false> pr, pc;
+    load_pieces(pr, d.pk_row, b);
+    load_pieces(pc, d.pk_col, b);
+    double am[kSL], bm[kSL]; // the lane's own scalings
+#pragma unroll
+    for (int s = 0; s < kSL; ++s) {
+        const int k = kSL * tid + s;
+        am[s] = 1.0;
+        bm[s] = 1.0;
+        if (k < N) {
+            va[k] = 1.0;
+            d.alpha[(size_t)b * N + k] = 1.0;
+        }
+        if (k < M) {
+            vb[k] = 1.0;
+            d.beta[(size_t)b * M + k] = 1.0;
+        }
     }
     lds_barrier();
 
     for (int l = 1; l <= L; ++l) {
         // column scaling (Eq. 3): beta_j /= beta_j sum_i alpha_i P0_ij + eps
 #pragma unroll
-        for (int s = 0; s < SLP; ++s)
+        for (int s = 0; s < kSLP; ++s)
             if (wave_active(pc, s)) {
                 double acc = 0.0;
-                pvisit(pc, s, [&](int i, float p0, int, bool) { acc += (double)p0 * va[i]; });
-                part[s * kT + tid] = acc;
+                pvisit(pc, s, [&](int, int i, float p0, bool) { acc += (double)p0 * va[i]; });
+                store_sum(group_reduce(acc, pc.info[s]), pc.info[s], sums);
             }
         lds_barrier();
 #pragma unroll
         for (int s = 0; s < kSL; ++s) {
             const int j = kSL * tid + s;
+            const double S = sums[min(j, M - 1)];
+            const double den = bm[s] * S + eps;
+            const double v = bm[s] / den;
             if (j < M) {
-                const double S = owner_sum(owc, s, part);
-                const double o = vb[j];
-                const double den = o * S + eps;
-                const double v = o / den;
+                bm[s] = v;
                 vb[j] = v;
                 d.beta[l * BM + (size_t)b * M + j] = v;
                 d.sden[(l - 1) * BM + (size_t)b * M + j] = den;
@@ -282,21 +361,21 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
         lds_barrier();
         // row scaling (Eq. 4): alpha_i /= alpha_i sum_j P0_ij beta_j + eps
 #pragma unroll
-        for (int s = 0; s < SLP; ++s)
+        for (int s = 0; s < kSLP; ++s)
             if (wave_active(pr, s)) {
                 double acc = 0.0;
-                pvisit(pr, s, [&](int j, float p0, int, bool) { acc += (double)p0 * vb[j]; });
-                part[s * kT + tid] = acc;
+                pvisit(pr, s, [&](int, int j, float p0, bool) { acc += (double)p0 * vb[j]; });
+                store_sum(group_reduce(acc, pr.info[s]), pr.info[s], sums);
             }
         lds_barrier();
 #pragma unroll
         for (int s = 0; s < kSL; ++s) {
             const int i = kSL * tid + s;
+            const double R = sums[min(i, N - 1)];
+            const double den = am[s] * R + eps;
+            const double v = am[s] / den;
             if (i < N) {
-                const double R = owner_sum(owr, s, part);
-                const double o = va[i];
-                const double den = o * R + eps;
-                const double v = o / den;
+                am[s] = v;
                 va[i] = v;
                 d.alpha[l * BN + (size_t)b * N + i] = v;
                 d.rden[(l - 1) * BN + (size_t)b * N + i] = den;
@@ -305,18 +384,34 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
         lds_barrier();
     }
 
-    // loss = sum_t v_t C_t (Sec. III-D), over the sample's pairs in row-major order
+    // loss = sum_t v_t C_t (Sec. III-D), over the sample's pairs in row-major
+    // order, four pairs per lane in flight
     double acc = 0.0;
-    for (int t = lo + tid; t < hi; t += kT)
-        acc += va[d.csr_row[t] - b * N] * (double)d.p0r[t] * vb[d.csr_col[t]] * d.cost[t];
+    for (int t0 = lo + tid; t0 < hi; t0 += 4 * kT) {
+        int r[4], c[4];
+        float p[4];
+        double C[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int t = t0 + u * kT < hi ? t0 + u * kT : lo;
+            r[u] = d.csr_row[t] - b * N;
+            c[u] = d.csr_col[t];
+            p[u] = d.p0r[t];
+            C[u] = d.cost[t];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (t0 + u * kT < hi)
+                acc += va[r[u]] * (double)p[u] * vb[c[u]] * C[u];
+    }
     acc = wave_sum(acc);
     if (lane_id() == 0)
-        part[tid >> 6] = acc;
+        sums[tid >> 6] = acc;
     lds_barrier();
     if (tid == 0) {
         double s = 0.0;
         for (int w = 0; w < kT / 64; ++w)
-            s += part[w];
+            s += sums[w];
         d.loss[b] = (float)s;
     }
 }
@@ -325,47 +420,35 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
 // grad_loss * C (loss = sum v C) and ends as dLoss/dP0 in d.adj (row-major).
 __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
 {
-    constexpr int SLP = kBwdSLP;
     extern __shared__ double lds[];
-    // row side: alpha^(l-1), 1/(R + eps), q; column side: beta^l, 1/(S + eps), q
-    double *va = lds, *ri = va + kCover, *qr = ri + kCover;
-    double *vb = qr + kCover, *si = vb + kCover, *qc = si + kCover;
-    double *part = qc + kCover;
-    int *scan = reinterpret_cast<int *>(part + SLP * kT);
-    uint32_t *owner_of = reinterpret_cast<uint32_t *>(part); // set-up only
+    // one side's values at a time: rows (alpha^(l-1), 1/(R + eps), q) after a
+    // row owner phase, columns (beta^l, 1/(S + eps), q) after a column owner phase
+    double *s0 = lds, *s1 = s0 + kSinkOwners, *s2 = s1 + kSinkOwners;
+    double *sums = s2 + kSinkOwners, *adj = sums + kSinkOwners;
     const int b = blockIdx.x, tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
     const int lo = d.row_ptr[(size_t)b * N], hi = d.row_ptr[(size_t)(b + 1) * N];
-    const POrder orow{d.row_ptr + (size_t)b * N, d.csr_col, d.p0r, nullptr, N};
-    const POrder ocol{d.col_ptr + (size_t)b * M, d.csc_row, d.p0c, d.csc_perm, M};
-    Pieces<SLP, kRunPos> pr;
-    Pieces<SLP, kPairPos> pc;
-    Owners owr, owc;
-    bool ok = pload(pr, owr, orow, lo, scan, owner_of);
-    ok = pload(pc, owc, ocol, lo, scan, owner_of) && ok;
-    double *adj = d.adj + lo; // indexed by row-major position within the sample
-    if (!ok) { // excluded by the host's capacity check; fail loudly if reached
-        for (int t = lo + tid; t < hi; t += kT)
-            adj[t - lo] = __builtin_nan("");
-        return;
-    }
+    Pieces<false> pr;
+    Pieces<true> pc;
+    load_pieces(pr, d.pk_row, b);
+    load_pieces(pc, d.pk_col, b);
     const double gl = d.grad_loss[b];
     for (int t = lo + tid; t < hi; t += kT)
         adj[t - lo] = gl * d.cost[t];
     double a_own[kSL], b_own[kSL];
 #pragma unroll
     for (int s = 0; s < kSL; ++s) {
-        const int i = kSL * tid + s, j = kSL * tid + s;
-        a_own[s] = i < N ? d.alpha[L * BN + (size_t)b * N + i] : 0.0;
-        b_own[s] = j < M ? d.beta[L * BM + (size_t)b * M + j] : 0.0;
-        if (j < M) { // no pending column update before the last iteration
-            vb[j] = b_own[s];
-            si[j] = 1.0;
-            qc[j] = 0.0;
+        const int k = kSL * tid + s;
+        a_own[s] = k < N ? d.alpha[L * BN + (size_t)b * N + k] : 0.0;
+        b_own[s] = k < M ? d.beta[L * BM + (size_t)b * M + k] : 0.0;
+        if (k < M) { // no pending column update before the last iteration
+            s0[k] = b_own[s];
+            s1[k] = 1.0;
+            s2[k] = 0.0;
         }
     }
-    __syncthreads();
+    lds_barrier();
 
     for (int l = L; l >= 1; --l) {
         // saved values of this iteration, loaded ahead of their use
@@ -378,87 +461,78 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
             sden[s] = k < M ? d.sden[(l - 1) * BM + (size_t)b * M + k] : 1.0;
             b_prev[s] = (k < M && l > 1) ? d.beta[(l - 1) * BM + (size_t)b * M + k] : 0.0;
         }
-        // row pieces: apply the pending column update, then partial sums of
-        // ubar * P0 * beta^l over each piece
-        // (all adjoint loads of the phase are issued before its first store)
-        double m[SLP][kP];
+        // row pieces: apply the pending column update, then sum
+        // ubar * P0 * beta^l over each row
 #pragma unroll
-        for (int s = 0; s < SLP; ++s)
+        for (int s = 0; s < kSLP; ++s)
             if (wave_active(pr, s)) {
-                int e = 0;
-                pvisit(pr, s, [&](int, float, int p, bool real) { m[s][e++] = real ? adj[p] : 0.0; });
-            }
-#pragma unroll
-        for (int s = 0; s < SLP; ++s)
-            if (wave_active(pr, s)) {
+                const int run = (int)(pr.info[s] >> 16);
+                double m[kP];
+                pvisit(pr, s, [&](int e, int, float, bool real) { m[e] = real ? adj[run + e] : 0.0; });
                 double acc = 0.0;
-                int e = 0;
-                pvisit(pr, s, [&](int j, float p0, int p, bool real) {
-                    const double a = m[s][e++] * si[j] - qc[j];
+                pvisit(pr, s, [&](int e, int j, float p0, bool real) {
+                    const double a = m[e] * s1[j] - s2[j];
                     if (real)
-                        adj[p] = a;
-                    acc += a * ((double)p0 * vb[j]);
+                        adj[run + e] = a;
+                    acc += a * ((double)p0 * s0[j]);
                 });
-                part[s * kT + tid] = acc;
+                store_sum(group_reduce(acc, pr.info[s]), pr.info[s], sums);
             }
-        __syncthreads();
+        lds_barrier();
         // row owners (adjoint of Eq. 4): d_i = alpha^l_i * sum; publish
-        // 1/(R + eps) and q = d_i/(R + eps), and alpha^(l-1) for the columns
+        // alpha^(l-1), 1/(R + eps) and q = d_i/(R + eps)
 #pragma unroll
         for (int s = 0; s < kSL; ++s) {
             const int i = kSL * tid + s;
+            const double dsum = a_own[s] * sums[min(i, N - 1)];
+            const double r = 1.0 / rden[s];
             if (i < N) {
-                const double dsum = a_own[s] * owner_sum(owr, s, part);
-                const double r = 1.0 / rden[s];
-                ri[i] = r;
-                qr[i] = dsum * r;
-                va[i] = a_prev[s];
+                s0[i] = a_prev[s];
+                s1[i] = r;
+                s2[i] = dsum * r;
             }
         }
         lds_barrier();
-        // column pieces: apply the row update, then partial sums of
-        // wbar * alpha^(l-1) * P0 over each piece
+        // column pieces: apply the row update, then sum
+        // wbar * alpha^(l-1) * P0 over each column
 #pragma unroll
-        for (int s = 0; s < SLP; ++s)
+        for (int s = 0; s < kSLP; ++s)
             if (wave_active(pc, s)) {
-                int e = 0;
-                pvisit(pc, s, [&](int, float, int p, bool real) { m[s][e++] = real ? adj[p] : 0.0; });
-            }
-#pragma unroll
-        for (int s = 0; s < SLP; ++s)
-            if (wave_active(pc, s)) {
-                double acc = 0.0;
-                int e = 0;
-                pvisit(pc, s, [&](int i, float p0, int p, bool real) {
-                    const double a = m[s][e++] * ri[i] - qr[i];
-                    if (real)
-                        adj[p] = a;
-                    acc += a * (va[i] * (double)p0);
+                double m[kP];
+                pvisit(pc, s, [&](int e, int, float, bool real) {
+                    m[e] = real ? adj[half16(opaque(pc.pos[s][e / 2]), e)] : 0.0;
                 });
-                part[s * kT + tid] = acc;
+                double acc = 0.0;
+                pvisit(pc, s, [&](int e, int i, float p0, bool real) {
+                    const double a = m[e] * s1[i] - s2[i];
+                    if (real)
+                        adj[half16(opaque(pc.pos[s][e / 2]), e)] = a;
+                    acc += a * (s0[i] * (double)p0);
+                });
+                store_sum(group_reduce(acc, pc.info[s]), pc.info[s], sums);
             }
-        __syncthreads();
+        lds_barrier();
         // column owners (adjoint of Eq. 3): e_j = beta^l_j * sum; publish
-        // 1/(S + eps), q = e_j/(S + eps), and beta^(l-1) for the next rows
+        // beta^(l-1), 1/(S + eps) and q = e_j/(S + eps)
 #pragma unroll
         for (int s = 0; s < kSL; ++s) {
             const int j = kSL * tid + s;
+            const double esum = b_own[s] * sums[min(j, M - 1)];
+            const double r = 1.0 / sden[s];
             if (j < M) {
-                const double esum = b_own[s] * owner_sum(owc, s, part);
-                const double r = 1.0 / sden[s];
-                si[j] = r;
-                qc[j] = esum * r;
-                vb[j] = b_prev[s];
+                s0[j] = b_prev[s];
+                s1[j] = r;
+                s2[j] = esum * r;
             }
             a_own[s] = a_prev[s];
             b_own[s] = b_prev[s];
         }
         lds_barrier();
     }
-    // the last column update
+    // the last column update, written out in row-major order
     for (int t = lo + tid; t < hi; t += kT) {
         const int j = d.csr_col[t];
-        adj[t - lo] = adj[t - lo] * si[j] - qc[j];
+        d.adj[t] = adj[t - lo] * s1[j] - s2[j];
     }
 }
 
@@ -585,15 +659,37 @@ __global__ __launch_bounds__(kBlock) void k_bwd_sink_col(DevPlan d, int l)
 
 } // namespace
 
-bool sinkhorn_per_sample_ok(int N, int M, int64_t max_pairs)
+void launch_piece_counts(const int32_t *row_ptr, const int32_t *col_cnt, int B, int N, int M, int32_t *out,
+                         hipStream_t s)
 {
-    return N <= kCover && M <= kCover && max_pieces(std::max(N, M), max_pairs) <= (int64_t)kFwdSLP * kT;
+    hipLaunchKernelGGL(k_piece_counts, dim3(B), dim3(kT), 0, s, row_ptr, col_cnt, N, M, out);
 }
 
-bool sinkhorn_bwd_per_sample_ok(int N, int M, int64_t max_pairs)
+bool sinkhorn_fwd_fits(int N, int M, const int32_t *counts, int B)
 {
-    return N <= kCover && M <= kCover && max_pieces(std::max(N, M), max_pairs) <= (int64_t)kBwdSLP * kT &&
-           max_pairs <= 65536; // positions within a sample are packed in 16 bits
+    if (N > kSinkOwners || M > kSinkOwners)
+        return false;
+    for (int b = 0; b < B; ++b)
+        if (counts[3 * b] > kCap || counts[3 * b + 1] > kCap || counts[3 * b + 2] > kSinkMaxGroup)
+            return false;
+    return true;
+}
+
+constexpr size_t kLdsBudget = 160 * 1024;
+
+bool sinkhorn_bwd_fits(int N, int M, const int32_t *counts, int B, int64_t max_pairs)
+{
+    // the adjoint of every pair of a sample in LDS; positions are 16-bit
+    return sinkhorn_fwd_fits(N, M, counts, B) && max_pairs <= 65536 &&
+           bwd_fixed_lds_bytes() + 8 * (size_t)max_pairs <= kLdsBudget;
+}
+
+size_t packed_order_words(int B) { return (size_t)B * kSLP * kP * kT; }
+
+void launch_pack(const DevPlan &d, int32_t *place, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_place, dim3(d.B, 2), dim3(kT), 0, s, d, place);
+    hipLaunchKernelGGL(k_pack_pairs, dim3(blocks_for(2 * d.nnz, kBlock)), dim3(kBlock), 0, s, d, (const int32_t *)place);
 }
 
 hipError_t launch_sinkhorn_fwd(const DevPlan &d, double eps, hipStream_t s)
@@ -607,9 +703,9 @@ hipError_t launch_sinkhorn_fwd(const DevPlan &d, double eps, hipStream_t s)
     return hipGetLastError();
 }
 
-hipError_t launch_sinkhorn_bwd(const DevPlan &d, hipStream_t s)
+hipError_t launch_sinkhorn_bwd(const DevPlan &d, int64_t max_pairs, hipStream_t s)
 {
-    const size_t bytes = bwd_lds_bytes();
+    const size_t bytes = bwd_fixed_lds_bytes() + 8 * (size_t)max_pairs;
     hipError_t e = hipFuncSetAttribute((const void *)k_sinkhorn_bwd,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess)
