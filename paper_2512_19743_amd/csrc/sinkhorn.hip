@@ -305,7 +305,7 @@ __device__ __forceinline__ void store_sum(double acc, uint32_t info, double *sum
 }
 
 constexpr size_t fwd_lds_bytes() { return 8 * 3 * (size_t)kSinkOwners; }
-constexpr size_t bwd_fixed_lds_bytes() { return 8 * 4 * (size_t)kSinkOwners; }
+constexpr size_t bwd_fixed_lds_bytes() { return (8 + 3 * 4) * (size_t)kSinkOwners; }
 
 __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
 {
@@ -423,8 +423,9 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
     extern __shared__ double lds[];
     // one side's values at a time: rows (alpha^(l-1), 1/(R + eps), q) after a
     // row owner phase, columns (beta^l, 1/(S + eps), q) after a column owner phase
-    double *s0 = lds, *s1 = s0 + kSinkOwners, *s2 = s1 + kSinkOwners;
-    double *sums = s2 + kSinkOwners, *adj = sums + kSinkOwners;
+    double *sums = lds;
+    float *s0 = reinterpret_cast<float *>(sums + kSinkOwners), *s1 = s0 + kSinkOwners, *s2 = s1 + kSinkOwners;
+    double *adj = reinterpret_cast<double *>(s2 + kSinkOwners);
     const int b = blockIdx.x, tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
@@ -443,9 +444,9 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
         a_own[s] = k < N ? d.alpha[L * BN + (size_t)b * N + k] : 0.0;
         b_own[s] = k < M ? d.beta[L * BM + (size_t)b * M + k] : 0.0;
         if (k < M) { // no pending column update before the last iteration
-            s0[k] = b_own[s];
-            s1[k] = 1.0;
-            s2[k] = 0.0;
+            s0[k] = (float)b_own[s];
+            s1[k] = 1.0f;
+            s2[k] = 0.0f;
         }
     }
     lds_barrier();
@@ -471,10 +472,10 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
                 pvisit(pr, s, [&](int e, int, float, bool real) { m[e] = real ? adj[run + e] : 0.0; });
                 double acc = 0.0;
                 pvisit(pr, s, [&](int e, int j, float p0, bool real) {
-                    const double a = m[e] * s1[j] - s2[j];
+                    const double a = m[e] * (double)s1[j] - (double)s2[j];
                     if (real)
                         adj[run + e] = a;
-                    acc += a * ((double)p0 * s0[j]);
+                    acc += a * ((double)p0 * (double)s0[j]);
                 });
                 store_sum(group_reduce(acc, pr.info[s]), pr.info[s], sums);
             }
@@ -487,9 +488,9 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
             const double dsum = a_own[s] * sums[min(i, N - 1)];
             const double r = 1.0 / rden[s];
             if (i < N) {
-                s0[i] = a_prev[s];
-                s1[i] = r;
-                s2[i] = dsum * r;
+                s0[i] = (float)a_prev[s];
+                s1[i] = (float)r;
+                s2[i] = (float)(dsum * r);
             }
         }
         lds_barrier();
@@ -504,10 +505,10 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
                 });
                 double acc = 0.0;
                 pvisit(pc, s, [&](int e, int i, float p0, bool real) {
-                    const double a = m[e] * s1[i] - s2[i];
+                    const double a = m[e] * (double)s1[i] - (double)s2[i];
                     if (real)
                         adj[half16(opaque(pc.pos[s][e / 2]), e)] = a;
-                    acc += a * (s0[i] * (double)p0);
+                    acc += a * ((double)s0[i] * (double)p0);
                 });
                 store_sum(group_reduce(acc, pc.info[s]), pc.info[s], sums);
             }
@@ -520,9 +521,9 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
             const double esum = b_own[s] * sums[min(j, M - 1)];
             const double r = 1.0 / sden[s];
             if (j < M) {
-                s0[j] = b_prev[s];
-                s1[j] = r;
-                s2[j] = esum * r;
+                s0[j] = (float)b_prev[s];
+                s1[j] = (float)r;
+                s2[j] = (float)(esum * r);
             }
             a_own[s] = a_prev[s];
             b_own[s] = b_prev[s];
@@ -532,7 +533,7 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
     // the last column update, written out in row-major order
     for (int t = lo + tid; t < hi; t += kT) {
         const int j = d.csr_col[t];
-        d.adj[t] = adj[t - lo] * s1[j] - s2[j];
+        d.adj[t] = adj[t - lo] * (double)s1[j] - (double)s2[j];
     }
 }
 

@@ -67,12 +67,14 @@ def compare_sample(g: dict, b: int, x: np.ndarray, y: np.ndarray, ref: oracle.Sa
     N, M = x.shape[0], y.shape[0]
     plan: apml.Plan = g["plan"]
     # loss and gradients
-    assert abs(g["loss"][b] - ref.loss) <= LOSS_RTOL * abs(ref.loss), (b, g["loss"][b], ref.loss)
-    e = rel_norm(g["gx"][b], ref.grad_x)
-    assert e <= GRAD_RTOL, (b, "grad_x", e)
+    loss_rel = abs(g["loss"][b] - ref.loss) / abs(ref.loss)
+    assert loss_rel <= LOSS_RTOL, (b, g["loss"][b], ref.loss)
+    gx_rel = rel_norm(g["gx"][b], ref.grad_x)
+    assert gx_rel <= GRAD_RTOL, (b, "grad_x", gx_rel)
+    gy_rel = 0.0
     if check_grad_y and g["gy"] is not None:
-        e = rel_norm(g["gy"][b], ref.grad_y)
-        assert e <= GRAD_RTOL, (b, "grad_y", e)
+        gy_rel = rel_norm(g["gy"][b], ref.grad_y)
+        assert gy_rel <= GRAD_RTOL, (b, "grad_y", gy_rel)
     # statistics: argmins bit-exact, temperatures to double precision
     st = plan.export_stats(b)
     np.testing.assert_array_equal(st["j1"], ref.row["k1"])
@@ -122,4 +124,5 @@ def compare_sample(g: dict, b: int, x: np.ndarray, y: np.ndarray, ref: oracle.Sa
         assert not bad.any(), (b, name, int(bad.sum()), float(np.max(np.abs(a - r) / np.maximum(np.abs(r), 1e-300))))
     v_err = rel_norm(ex["v"][gi].astype(np.float64), ref.v[oi])
     assert v_err <= 1e-5, (b, "v", v_err)
-    return dict(nnz_gpu=len(gk), nnz_ref=ref.nnz, flips=flips)
+    return dict(nnz_gpu=len(gk), nnz_ref=ref.nnz, flips=flips, loss_rel=loss_rel, gx_rel=gx_rel, gy_rel=gy_rel,
+                v_rel=v_err)

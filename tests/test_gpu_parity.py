@@ -28,6 +28,8 @@ def _check_batch(X, Y, label, samples=None, check_grad_y=True, **prm):
     for b in (range(X.shape[0]) if samples is None else samples):
         ref = oracle.run_sample(X[b], Y[b], oracle_params(**prm), grad=True)
         out.append(compare_sample(g, b, X[b], Y[b], ref, tau, check_grad_y=check_grad_y))
+    worst = {k: max(r[k] for r in out) for k in ("loss_rel", "gx_rel", "gy_rel", "v_rel")}
+    note(f"{label}: worst relative errors " + ", ".join(f"{k} {v:.2e}" for k, v in worst.items()))
     return g, out
 
 
