@@ -478,11 +478,13 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     ScanArray sr{ea.cnt, BN, ea.S, dv.row_ptr, tmp.get<int32_t>(ceil_div(BN, tile)), ceil_div(BN, tile)};
     if (tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (support)");
-    int32_t *offsets_dev = tmp.get<int32_t>((size_t)B + 1);
-    int32_t *pieces_dev = tmp.get<int32_t>(3 * (size_t)B);
-    std::vector<int32_t> offsets((size_t)B + 1), pieces(3 * (size_t)B);
+    Readback *rb_dev = (Readback *)tmp.get<uint8_t>(readback_bytes(B));
+    ba.col_tiles = tmp.get<int32_t>(ceil_div(BM, tile));
+    std::vector<uint8_t> rb_host(readback_bytes(B));
     if (tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (support)");
+    const Readback *rb = (const Readback *)rb_host.data();
+    const int32_t *offsets = rb->data, *pieces = rb->data + B + 1;
     Counters hc{};
     for (int attempt = 0; attempt < 2; ++attempt) {
         if (attempt > 0) {
@@ -495,13 +497,13 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
             HIP_TRY(hipGetLastError());
             pt.stop();
         }
-        launch_scan(sr, s); // row offsets, while the host waits for the count
-        launch_sample_offsets(dv.row_ptr, B, N, offsets_dev, s);
-        launch_piece_counts(dv.row_ptr, ba.col_cnt, B, N, M, pieces_dev, s);
-        HIP_TRY(hipMemcpyAsync(&hc, dv.ctr, sizeof(Counters), hipMemcpyDeviceToHost, s));
-        HIP_TRY(hipMemcpyAsync(offsets.data(), offsets_dev, sizeof(int32_t) * (B + 1), hipMemcpyDeviceToHost, s));
-        HIP_TRY(hipMemcpyAsync(pieces.data(), pieces_dev, sizeof(int32_t) * 3 * B, hipMemcpyDeviceToHost, s));
+        // row and column offsets, and what the host needs, in one copy
+        launch_scan(sr, s);
+        launch_col_scan(ba.col_cnt, BM, dv.col_ptr, ba.col_tiles, s);
+        launch_readback(dv.row_ptr, ba.col_cnt, dv.ctr, B, N, M, rb_dev, s);
+        HIP_TRY(hipMemcpyAsync(rb_host.data(), rb_dev, readback_bytes(B), hipMemcpyDeviceToHost, s));
         HIP_TRY(hipStreamSynchronize(s));
+        hc = rb->ctr;
         if (hc.overflow <= ea.ovf_cap)
             break;
         // more overflow pairs than room: enlarge the list and scan again
@@ -521,8 +523,8 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     for (int b = 0; b < B; ++b)
         plan->max_sample = std::max<int64_t>(plan->max_sample, offsets[b + 1] - offsets[b]);
     dv.nnz = nnz;
-    plan->sink_fwd = sinkhorn_fwd_fits(N, M, pieces.data(), B);
-    plan->sink_bwd = plan->sink_fwd && sinkhorn_bwd_fits(N, M, pieces.data(), B, plan->max_sample);
+    plan->sink_fwd = sinkhorn_fwd_fits(N, M, pieces, B);
+    plan->sink_bwd = plan->sink_fwd && sinkhorn_bwd_fits(N, M, pieces, B, plan->max_sample);
 
     // ---- sparse structure -------------------------------------------------
     PhaseTimer pt_build(PH_BUILD, s);
@@ -543,7 +545,6 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     ba.cnt = ea.cnt;
     ba.ovf = ea.ovf;
     ba.n_ovf = (int)hc.overflow;
-    ba.col_tiles = tmp.get<int32_t>(ceil_div(BM, tile));
     ba.tmp_row = tmp.get<int32_t>(nnz);
     ba.tmp_src = tmp.get<int32_t>(nnz);
     if (tmp.failed || keep.failed)

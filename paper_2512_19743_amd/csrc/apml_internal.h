@@ -159,6 +159,8 @@ struct BuildArgs {
     int32_t *tmp_row, *tmp_src;  // column-major staging [nnz]
 };
 void launch_csr_fill(const DevPlan &d, const BuildArgs &a, hipStream_t s);
+// col_ptr = exclusive scan of the column counts (n = B*M columns).
+void launch_col_scan(const int32_t *col_cnt, int n, int32_t *col_ptr, int32_t *tiles, hipStream_t s);
 void launch_csc_build(const DevPlan &d, const BuildArgs &a, hipStream_t s);
 
 void launch_softmax(const DevPlan &d, const Params &p, hipStream_t s);
@@ -168,11 +170,18 @@ void launch_bwd_softmax(const DevPlan &d, const Params &p, hipStream_t s);
 // sample with the sample's pairs in registers; the per-iteration kernels are
 // the general fallback.
 //
-// Per sample b, out[3b..3b+2] = positions needed by the rows, by the columns,
-// and the most pieces of any row or column (row lengths from row_ptr, column
-// lengths from col_cnt).
-void launch_piece_counts(const int32_t *row_ptr, const int32_t *col_cnt, int B, int N, int M, int32_t *out,
-                         hipStream_t s);
+// What the host reads back after the support scan, in one copy: the
+// counters, the pair offsets of the samples (row_ptr[b*N], b = 0..B) and per
+// sample the positions needed by its rows, by its columns, and the most
+// pieces of any row or column (row lengths from row_ptr, column lengths from
+// col_cnt).
+struct Readback {
+    Counters ctr;
+    int32_t data[1]; // [B + 1] offsets, then [3B] piece counts
+};
+inline size_t readback_bytes(int B) { return sizeof(Readback) + sizeof(int32_t) * (4 * (size_t)B); }
+void launch_readback(const int32_t *row_ptr, const int32_t *col_cnt, const Counters *ctr, int B, int N, int M,
+                     Readback *out, hipStream_t s);
 // Whether the per-sample kernels take a batch: counts are the host copy of the
 // piece counts above, max_pairs the largest sample's stored pairs.
 bool sinkhorn_fwd_fits(int N, int M, const int32_t *counts, int B);
@@ -184,9 +193,6 @@ hipError_t launch_sinkhorn_fwd(const DevPlan &d, double eps, hipStream_t s);
 hipError_t launch_sinkhorn_bwd(const DevPlan &d, int64_t max_pairs, hipStream_t s);
 void launch_sinkhorn_fwd_steps(const DevPlan &d, double eps, hipStream_t s);
 void launch_sinkhorn_bwd_steps(const DevPlan &d, hipStream_t s);
-
-// out[b] = row_ptr[b*N] for b = 0..B (pair offsets of the samples).
-void launch_sample_offsets(const int32_t *row_ptr, int B, int N, int32_t *out, hipStream_t s);
 
 void launch_count_support(const int32_t *row_ptr, const uint8_t *flags, int B, int N,
                           unsigned long long *out, hipStream_t s);

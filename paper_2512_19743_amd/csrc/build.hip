@@ -194,23 +194,9 @@ __global__ __launch_bounds__(kBlock) void k_count_support(const int32_t *row_ptr
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_sample_offsets(const int32_t *row_ptr, int B, int N,
-                                                           int32_t *out)
-{
-    const int b = blockIdx.x * kBlock + threadIdx.x;
-    if (b <= B)
-        out[b] = row_ptr[(size_t)b * N];
-}
-
 } // namespace
 
 int scan_tile_items() { return kScanTile; }
-
-void launch_sample_offsets(const int32_t *row_ptr, int B, int N, int32_t *out, hipStream_t s)
-{
-    hipLaunchKernelGGL(k_sample_offsets, dim3(blocks_for(B + 1, kBlock)), dim3(kBlock), 0, s, row_ptr, B, N,
-                       out);
-}
 
 void launch_scan(const ScanArray &a, hipStream_t s)
 {
@@ -226,13 +212,16 @@ void launch_csr_fill(const DevPlan &d, const BuildArgs &a, hipStream_t s)
         hipLaunchKernelGGL(k_ovf_fill, dim3(blocks_for(a.n_ovf, kBlock)), dim3(kBlock), 0, s, d, a);
 }
 
+void launch_col_scan(const int32_t *col_cnt, int n, int32_t *col_ptr, int32_t *tiles, hipStream_t s)
+{
+    ScanArray sc{col_cnt, n, 1, col_ptr, tiles, (n + kScanTile - 1) / kScanTile};
+    launch_scan(sc, s);
+}
+
 void launch_csc_build(const DevPlan &d, const BuildArgs &a, hipStream_t s)
 {
-    // a.col_cnt holds the stored pairs per column, counted during emission
+    // d.col_ptr holds the scan of the column counts (launch_col_scan)
     const unsigned g = blocks_for(d.nnz, kBlock);
-    const int n = d.B * d.M;
-    ScanArray sc{a.col_cnt, n, 1, d.col_ptr, a.col_tiles, (n + kScanTile - 1) / kScanTile};
-    launch_scan(sc, s);
     hipLaunchKernelGGL(k_csc_fill, dim3(g), dim3(kBlock), 0, s, d, a);
     hipLaunchKernelGGL(k_csc_sort, dim3(g), dim3(kBlock), 0, s, d, a);
 }

@@ -54,11 +54,19 @@ __device__ __forceinline__ size_t pk_index(int b, int p, int w, int words)
     return (((size_t)b * kSLP + p / kT) * words + w) * kT + p % kT;
 }
 
-__global__ __launch_bounds__(kT) void k_piece_counts(const int32_t *row_ptr, const int32_t *col_cnt, int N, int M,
-                                                     int32_t *out)
+__global__ __launch_bounds__(kT) void k_readback(const int32_t *row_ptr, const int32_t *col_cnt,
+                                                 const Counters *ctr, int N, int M, Readback *rb)
 {
     __shared__ int red[3][kT / 64];
-    const int b = blockIdx.x, tid = threadIdx.x;
+    const int b = blockIdx.x, tid = threadIdx.x, B = gridDim.x;
+    int32_t *offsets = rb->data, *out = rb->data + B + 1;
+    if (tid == 0) {
+        offsets[b] = row_ptr[(size_t)b * N];
+        if (b == B - 1)
+            offsets[B] = row_ptr[(size_t)B * N];
+        if (b == 0)
+            rb->ctr = *ctr;
+    }
     int pr = 0, pc = 0, mx = 0;
     for (int i = tid; i < N; i += kT) {
         const int np = pieces_of(row_ptr[(size_t)b * N + i + 1] - row_ptr[(size_t)b * N + i]);
@@ -660,10 +668,10 @@ __global__ __launch_bounds__(kBlock) void k_bwd_sink_col(DevPlan d, int l)
 
 } // namespace
 
-void launch_piece_counts(const int32_t *row_ptr, const int32_t *col_cnt, int B, int N, int M, int32_t *out,
-                         hipStream_t s)
+void launch_readback(const int32_t *row_ptr, const int32_t *col_cnt, const Counters *ctr, int B, int N, int M,
+                     Readback *out, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_piece_counts, dim3(B), dim3(kT), 0, s, row_ptr, col_cnt, N, M, out);
+    hipLaunchKernelGGL(k_readback, dim3(B), dim3(kT), 0, s, row_ptr, col_cnt, ctr, N, M, out);
 }
 
 bool sinkhorn_fwd_fits(int N, int M, const int32_t *counts, int B)
