@@ -483,8 +483,9 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     std::vector<uint8_t> rb_host(readback_bytes(B));
     if (tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (support)");
-    const Readback *rb = (const Readback *)rb_host.data();
-    const int32_t *offsets = rb->data, *pieces = rb->data + B + 1;
+    Readback *rb = (Readback *)rb_host.data();
+    const int64_t *totals = readback_totals(rb);
+    const int32_t *offsets = readback_offsets(rb, B), *pieces = readback_pieces(rb, B);
     Counters hc{};
     for (int attempt = 0; attempt < 2; ++attempt) {
         if (attempt > 0) {
@@ -514,9 +515,11 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     }
     if (hc.overflow > ea.ovf_cap)
         return fail(APML_ERR_INTERNAL, "overflow count changed between identical scans");
-    if (hc.stored > (unsigned long long)(INT32_MAX - 1))
+    int64_t nnz = 0;
+    for (int b = 0; b < B; ++b)
+        nnz += totals[b];
+    if (nnz > (int64_t)INT32_MAX - 1)
         return fail(APML_ERR_UNSUPPORTED, "more than 2^31 stored pairs: raise tau or lower N*M");
-    const int64_t nnz = (int64_t)hc.stored;
     plan->stored = nnz;
     if (offsets[B] != nnz)
         return fail(APML_ERR_INTERNAL, "row offsets disagree with the emitted pair count");

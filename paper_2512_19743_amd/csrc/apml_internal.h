@@ -15,9 +15,8 @@ constexpr int kGroup = 4;         // lanes per row / column in the sparse kernel
 
 // Device-side counters of one forward call.
 struct Counters {
-    unsigned long long stored; // pairs emitted by the support scan
-    unsigned int overflow;     // emitted pairs that did not fit their slot group
-    unsigned int error;        // bit 0: a row's minima not found among its pairs; bit 1: a column's
+    unsigned int overflow; // emitted pairs that did not fit their slot group
+    unsigned int error;    // bit 0: a row's minima not found among its pairs; bit 1: a column's
 };
 
 // A pair that did not fit its (row, chunk) slot group.
@@ -171,15 +170,19 @@ void launch_bwd_softmax(const DevPlan &d, const Params &p, hipStream_t s);
 // the general fallback.
 //
 // What the host reads back after the support scan, in one copy: the
-// counters, the pair offsets of the samples (row_ptr[b*N], b = 0..B) and per
-// sample the positions needed by its rows, by its columns, and the most
-// pieces of any row or column (row lengths from row_ptr, column lengths from
-// col_cnt).
+// counters, the stored pairs of each sample counted in 64 bits, the pair
+// offsets of the samples (row_ptr[b*N], b = 0..B) and per sample the
+// positions needed by its rows, by its columns, and the most pieces of any
+// row or column (row lengths from row_ptr, column lengths from col_cnt).
 struct Readback {
     Counters ctr;
-    int32_t data[1]; // [B + 1] offsets, then [3B] piece counts
 };
-inline size_t readback_bytes(int B) { return sizeof(Readback) + sizeof(int32_t) * (4 * (size_t)B); }
+// After the Readback header: int64 stored pairs per sample [B] (from the
+// column counts, in 64 bits), int32 offsets [B + 1], int32 piece counts [3B].
+inline size_t readback_bytes(int B) { return sizeof(Readback) + 8 * (size_t)B + 4 * (4 * (size_t)B + 1); }
+__host__ __device__ inline int64_t *readback_totals(Readback *r) { return reinterpret_cast<int64_t *>(r + 1); }
+__host__ __device__ inline int32_t *readback_offsets(Readback *r, int B) { return reinterpret_cast<int32_t *>(readback_totals(r) + B); }
+__host__ __device__ inline int32_t *readback_pieces(Readback *r, int B) { return readback_offsets(r, B) + B + 1; }
 void launch_readback(const int32_t *row_ptr, const int32_t *col_cnt, const Counters *ctr, int B, int N, int M,
                      Readback *out, hipStream_t s);
 // Whether the per-sample kernels take a batch: counts are the host copy of the

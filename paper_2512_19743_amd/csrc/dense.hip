@@ -11,9 +11,10 @@
 //              C <= C1 + log(1/tau)/T (Sec. III-B, Eq. 1), widened by a small
 //              relative margin and never below the second minimum.
 //   k_emit     the candidate support: every pair inside its row's or its
-//              column's threshold. Per pair 6 VALU ops for the distance and two
-//              compares whose wave masks are combined on the scalar unit. Each
-//              lane appends its row's pairs, in column order, to a private slot
+//              column's threshold. Per pair 6 VALU ops for the distance, a max
+//              of the two radii, a compare and an add-with-carry that records
+//              the hit in a per-lane bitmask of 32 columns. Each lane then
+//              appends its row's pairs, in column order, to a private slot
 //              group and counts it in its column; the exact test s >= tau is
 //              applied later in double precision on this candidate set.
 #include "apml_internal.h"
@@ -77,7 +78,7 @@ __global__ __launch_bounds__(kBlock) void k_finalize(FinalizeArgs args)
 {
     int k = blockIdx.x * kBlock + threadIdx.x;
     if (k == 0)
-        *args.ctr = Counters{0, 0, 0};
+        *args.ctr = Counters{0, 0};
     const int which = k < args.rows ? 0 : 1;
     if (which)
         k -= args.rows;
@@ -116,20 +117,69 @@ __global__ __launch_bounds__(kBlock) void k_finalize(FinalizeArgs args)
     }
 }
 
-// Appends pair (row, j) to the lane's slot group, or to the overflow list,
-// and counts it in its column.
-__device__ __forceinline__ void emit_pair(const EmitArgs &a, int32_t *slot, int32_t *col_cnt, int row, int ch,
-                                          int j, int &cnt)
+// Appends pair (row, j) to the lane's slot group when it has room, and
+// counts it in its column. Pairs beyond the slot group go to the overflow
+// list in a second pass (emit_overflow), so that the scan loop issues no
+// atomic whose result it must wait for.
+__device__ __forceinline__ void emit_pair(const EmitArgs &a, int32_t *slot, int32_t *col_cnt, int j, int &cnt)
 {
     atomicAdd(&col_cnt[j], 1);
-    if (cnt < a.K) {
+    if (cnt < a.K)
         slot[cnt] = j;
-    } else {
-        const unsigned o = atomicAdd(&a.ctr->overflow, 1u);
-        if (o < a.ovf_cap)
-            a.ovf[o] = OverflowEntry{row, ch, cnt, j};
-    }
     ++cnt;
+}
+
+// Radius test of one pair (inside the row's ball E or the column's ball w),
+// shifted into bits: bits = 2*bits + hit. Three VALU instructions; the
+// compiler's own max would first canonicalize the scalar operand, and its
+// bit insertion takes two more.
+__device__ __forceinline__ uint32_t shift_in_hit(uint32_t bits, float ax, float ay, float az, float E,
+                                                 f32x4 yv)
+{
+    const float s = sqdist_f32(ax, ay, az, yv.x, yv.y, yv.z);
+    float m;
+    asm("v_max_f32 %1, %3, %4\n\t"
+        "v_cmp_le_f32 vcc, %2, %1\n\t"
+        "v_addc_co_u32 %0, vcc, %0, %0, vcc"
+        : "+v"(bits), "=&v"(m)
+        : "v"(s), "s"(yv.w), "v"(E)
+        : "vcc");
+    return bits;
+}
+
+// Calls f(j) for every column j in [j0, j1) whose pair with this lane's row
+// passes the radius test, in increasing j. Blocks of 32 columns: one bit per
+// column is shifted in as the columns pass (first column in the top bit),
+// then the lane visits its hits. keep masks out lanes that have no row.
+template <class F>
+__device__ __forceinline__ void for_each_hit(float ax, float ay, float az, float E, const_ptr<f32x4> q, int j0,
+                                             int j1, uint32_t keep, F f)
+{
+    int j = j0;
+    for (; j + 32 <= j1; j += 32) {
+        uint32_t bits = 0;
+#pragma unroll
+        for (int u = 0; u < 32; ++u)
+            bits = shift_in_hit(bits, ax, ay, az, E, q[j + u]);
+        bits &= keep;
+        while (bits) {
+            const int u = __clz(bits);
+            f(j + u);
+            bits &= ~(0x80000000u >> u);
+        }
+    }
+    if (j < j1) {
+        uint32_t bits = 0;
+        const int n = j1 - j;
+        for (int u = 0; u < n; ++u)
+            bits = shift_in_hit(bits, ax, ay, az, E, q[j + u]);
+        bits = (bits << (32 - n)) & keep;
+        while (bits) {
+            const int u = __clz(bits);
+            f(j + u);
+            bits &= ~(0x80000000u >> u);
+        }
+    }
 }
 
 __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs a)
@@ -141,52 +191,34 @@ __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs a)
     const int b = rest / a.S;
     const int i = ob * kBlock + threadIdx.x;
     const bool valid = i < a.N;
-    const unsigned long long valid_mask = __builtin_amdgcn_ballot_w64(valid);
     const int row = b * a.N + (valid ? i : a.N - 1);
     const float *p = a.x + (size_t)row * 3;
     const float ax = p[0], ay = p[1], az = p[2];
-    const float E = a.E_row[row];
+    const float E = valid ? a.E_row[row] : -kInf;
     const_ptr<f32x4> q = as_const(reinterpret_cast<const f32x4 *>(a.ypack + (size_t)b * a.M));
     const int j0 = ch * a.chunk;
     const int j1 = min(a.M, j0 + a.chunk);
     int32_t *slot = a.slots + ((size_t)row * a.S + ch) * a.K;
     int32_t *col_cnt = a.col_cnt + (size_t)b * a.M;
-    const int lane = lane_id();
+    const uint32_t keep = valid ? ~0u : 0u; // a lane without a row ignores the columns' balls too
     int cnt = 0;
-    int j = j0;
-    // Common path: per column the distance and two compares whose wave masks
-    // are OR'ed on the scalar unit; one branch per 4 columns.
-    for (; j + 4 <= j1; j += 4) {
-        unsigned long long mk[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const f32x4 yv = q[j + u];
-            const float s = sqdist_f32(ax, ay, az, yv.x, yv.y, yv.z);
-            mk[u] = (__builtin_amdgcn_ballot_w64(s <= E) | __builtin_amdgcn_ballot_w64(s <= yv.w)) &
-                    valid_mask;
-        }
-        if (mk[0] | mk[1] | mk[2] | mk[3]) {
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-                if ((mk[u] >> lane) & 1ull)
-                    emit_pair(a, slot, col_cnt, row, ch, j + u, cnt);
-        }
-    }
-    for (; j < j1; ++j) {
-        const f32x4 yv = q[j];
-        const float s = sqdist_f32(ax, ay, az, yv.x, yv.y, yv.z);
-        const unsigned long long m =
-            (__builtin_amdgcn_ballot_w64(s <= E) | __builtin_amdgcn_ballot_w64(s <= yv.w)) & valid_mask;
-        if ((m >> lane) & 1ull)
-            emit_pair(a, slot, col_cnt, row, ch, j, cnt);
+    for_each_hit(ax, ay, az, E, q, j0, j1, keep, [&](int j) { emit_pair(a, slot, col_cnt, j, cnt); });
+    // rare: lanes with more hits than slots scan their columns again and
+    // append the hits of rank >= K to the overflow list
+    if (__builtin_amdgcn_ballot_w64(cnt > a.K)) {
+        int r = 0;
+        const uint32_t over = cnt > a.K ? ~0u : 0u;
+        for_each_hit(ax, ay, az, E, q, j0, j1, over, [&](int j) {
+            if (r >= a.K) {
+                const unsigned o = atomicAdd(&a.ctr->overflow, 1u);
+                if (o < a.ovf_cap)
+                    a.ovf[o] = OverflowEntry{row, ch, r, j};
+            }
+            ++r;
+        });
     }
     if (valid)
         a.cnt[(size_t)row * a.S + ch] = cnt;
-    int w = cnt;
-    for (int off = 32; off > 0; off >>= 1)
-        w += __shfl_xor(w, off);
-    if (lane == 0 && w)
-        atomicAdd(&a.ctr->stored, (unsigned long long)w);
 }
 
 } // namespace

@@ -58,8 +58,9 @@ __global__ __launch_bounds__(kT) void k_readback(const int32_t *row_ptr, const i
                                                  const Counters *ctr, int N, int M, Readback *rb)
 {
     __shared__ int red[3][kT / 64];
+    __shared__ long long tot[kT / 64];
     const int b = blockIdx.x, tid = threadIdx.x, B = gridDim.x;
-    int32_t *offsets = rb->data, *out = rb->data + B + 1;
+    int32_t *offsets = readback_offsets(rb, B), *out = readback_pieces(rb, B);
     if (tid == 0) {
         offsets[b] = row_ptr[(size_t)b * N];
         if (b == B - 1)
@@ -73,8 +74,11 @@ __global__ __launch_bounds__(kT) void k_readback(const int32_t *row_ptr, const i
         pr += 1 << min(log2_group(np), 30);
         mx = max(mx, np);
     }
+    long long pairs = 0;
     for (int j = tid; j < M; j += kT) {
-        const int np = pieces_of(col_cnt[(size_t)b * M + j]);
+        const int n = col_cnt[(size_t)b * M + j];
+        const int np = pieces_of(n);
+        pairs += n;
         pc += 1 << min(log2_group(np), 30);
         mx = max(mx, np);
     }
@@ -82,20 +86,25 @@ __global__ __launch_bounds__(kT) void k_readback(const int32_t *row_ptr, const i
         pr += __shfl_xor(pr, o);
         pc += __shfl_xor(pc, o);
         mx = max(mx, __shfl_xor(mx, o));
+        pairs += __shfl_xor(pairs, o);
     }
     if (lane_id() == 0) {
         red[0][tid >> 6] = pr;
         red[1][tid >> 6] = pc;
         red[2][tid >> 6] = mx;
+        tot[tid >> 6] = pairs;
     }
     __syncthreads();
     if (tid == 0) {
         int a = 0, c = 0, m = 0;
+        long long t = 0;
         for (int w = 0; w < kT / 64; ++w) {
             a += red[0][w];
             c += red[1][w];
             m = max(m, red[2][w]);
+            t += tot[w];
         }
+        readback_totals(rb)[b] = t;
         out[3 * b] = a;
         out[3 * b + 1] = c;
         out[3 * b + 2] = m;
