@@ -301,12 +301,12 @@ int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
 // Chunks of the broadcast range so that a dense scan has about 8 waves per
 // SIMD on 256 CUs, each chunk at least 512 points long.
-void choose_chunks(int B, int n_own, int n_bc, int *S, int *chunk)
+void choose_chunks(int B, int n_own, int n_bc, int *S, int *chunk, int min_chunk = 512)
 {
     const int64_t waves = (int64_t)B * ceil_div(n_own, 64);
     const int64_t target = 8192;
     int s = (int)std::max<int64_t>(1, (target + waves - 1) / waves);
-    s = std::min(s, std::max(1, n_bc / 512));
+    s = std::min(s, std::max(1, n_bc / min_chunk));
     int len = ceil_div(n_bc, s);
     len = ceil_div(len, kUnroll) * kUnroll;
     *chunk = len;
@@ -433,7 +433,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     float4 *ypack = tmp.get<float4>(BM);
     dv.ctr = keep.get<Counters>(1);
     BuildArgs ba{};
-    ba.col_cnt = tmp.get<int32_t>(BM);
+    int32_t *col_cnt = tmp.get<int32_t>(BM); // stored pairs per column, counted by the emission
     ba.col_fill = tmp.get<int32_t>(BM);
     dv.row_ptr = keep.get<int32_t>((size_t)BN + 1);
     dv.col_ptr = keep.get<int32_t>((size_t)BM + 1);
@@ -447,7 +447,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         pt.stop();
     }
     FinalizeDir fr{rows.partial, x, dv.m12_row, E_row, nullptr, nullptr, nullptr, N, rows.S, kp.lk_row};
-    FinalizeDir fc{cols.partial, y, dv.m12_col, nullptr, ypack, ba.col_cnt, ba.col_fill, M, cols.S, kp.lk_col};
+    FinalizeDir fc{cols.partial, y, dv.m12_col, nullptr, ypack, col_cnt, ba.col_fill, M, cols.S, kp.lk_col};
     launch_finalize(fr, fc, B, kp, dv.ctr, s); // also clears the counters
     HIP_TRY(hipGetLastError());
 
@@ -459,25 +459,12 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     ea.B = B;
     ea.N = N;
     ea.M = M;
-    ea.S = rows.S;
-    ea.chunk = rows.chunk;
     ea.owner_blocks = rows.owner_blocks;
-    {
-        const double per_row = 12.0 * (1.0 + (double)M / N);
-        int K = (int)std::ceil(per_row / ea.S);
-        K = std::max(4, std::min(64, (K + 3) / 4 * 4));
-        ea.K = K;
-    }
-    ea.slots = tmp.get<int32_t>((size_t)BN * ea.S * ea.K);
+    choose_chunks(B, N, M, &ea.S, &ea.chunk, 256);
     ea.cnt = tmp.get<int32_t>((size_t)BN * ea.S);
-    ea.ovf_cap = (unsigned)std::max<int64_t>(65536, 2 * (int64_t)(BN + BM));
-    ea.ovf = tmp.get<OverflowEntry>(ea.ovf_cap);
-    ea.ctr = dv.ctr;
-    ea.col_cnt = ba.col_cnt; // cleared by the finalize kernel
+    ea.col_cnt = col_cnt; // cleared by the finalize kernel
     const int tile = scan_tile_items();
     ScanArray sr{ea.cnt, BN, ea.S, dv.row_ptr, tmp.get<int32_t>(ceil_div(BN, tile)), ceil_div(BN, tile)};
-    if (tmp.failed)
-        return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (support)");
     Readback *rb_dev = (Readback *)tmp.get<uint8_t>(readback_bytes(B));
     ba.col_tiles = tmp.get<int32_t>(ceil_div(BM, tile));
     std::vector<uint8_t> rb_host(readback_bytes(B));
@@ -486,35 +473,18 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     Readback *rb = (Readback *)rb_host.data();
     const int64_t *totals = readback_totals(rb);
     const int32_t *offsets = readback_offsets(rb, B), *pieces = readback_pieces(rb, B);
-    Counters hc{};
-    for (int attempt = 0; attempt < 2; ++attempt) {
-        if (attempt > 0) {
-            HIP_TRY(hipMemsetAsync(dv.ctr, 0, sizeof(Counters), s));
-            HIP_TRY(hipMemsetAsync(ba.col_cnt, 0, sizeof(int32_t) * (size_t)BM, s));
-        }
-        {
-            PhaseTimer pt(PH_SUPPORT, s);
-            launch_emit(ea, s);
-            HIP_TRY(hipGetLastError());
-            pt.stop();
-        }
-        // row and column offsets, and what the host needs, in one copy
-        launch_scan(sr, s);
-        launch_col_scan(ba.col_cnt, BM, dv.col_ptr, ba.col_tiles, s);
-        launch_readback(dv.row_ptr, ba.col_cnt, dv.ctr, B, N, M, rb_dev, s);
-        HIP_TRY(hipMemcpyAsync(rb_host.data(), rb_dev, readback_bytes(B), hipMemcpyDeviceToHost, s));
-        HIP_TRY(hipStreamSynchronize(s));
-        hc = rb->ctr;
-        if (hc.overflow <= ea.ovf_cap)
-            break;
-        // more overflow pairs than room: enlarge the list and scan again
-        ea.ovf_cap = hc.overflow;
-        ea.ovf = tmp.get<OverflowEntry>(ea.ovf_cap);
-        if (tmp.failed)
-            return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (overflow)");
+    {
+        PhaseTimer pt(PH_SUPPORT, s);
+        launch_emit_count(ea, s);
+        HIP_TRY(hipGetLastError());
+        pt.stop();
     }
-    if (hc.overflow > ea.ovf_cap)
-        return fail(APML_ERR_INTERNAL, "overflow count changed between identical scans");
+    // row and column offsets, and what the host needs, in one copy
+    launch_scan(sr, s);
+    launch_col_scan(col_cnt, BM, dv.col_ptr, ba.col_tiles, s);
+    launch_readback(dv.row_ptr, col_cnt, dv.ctr, B, N, M, rb_dev, s);
+    HIP_TRY(hipMemcpyAsync(rb_host.data(), rb_dev, readback_bytes(B), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
     int64_t nnz = 0;
     for (int b = 0; b < B; ++b)
         nnz += totals[b];
@@ -522,7 +492,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         return fail(APML_ERR_UNSUPPORTED, "more than 2^31 stored pairs: raise tau or lower N*M");
     plan->stored = nnz;
     if (offsets[B] != nnz)
-        return fail(APML_ERR_INTERNAL, "row offsets disagree with the emitted pair count");
+        return fail(APML_ERR_INTERNAL, "row offsets disagree with the column counts");
     for (int b = 0; b < B; ++b)
         plan->max_sample = std::max<int64_t>(plan->max_sample, offsets[b + 1] - offsets[b]);
     dv.nnz = nnz;
@@ -530,7 +500,6 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     plan->sink_bwd = plan->sink_fwd && sinkhorn_bwd_fits(N, M, pieces, B, plan->max_sample);
 
     // ---- sparse structure -------------------------------------------------
-    PhaseTimer pt_build(PH_BUILD, s);
     dv.csr_col = keep.get<int32_t>(nnz);
     dv.csr_row = keep.get<int32_t>(nnz);
     dv.csc_row = keep.get<int32_t>(nnz);
@@ -542,20 +511,20 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     dv.p0r = keep.get<float>(nnz);
     dv.p0c = keep.get<float>(nnz);
     dv.cost = keep.get<double>(nnz);
-    ba.S = ea.S;
-    ba.K = ea.K;
-    ba.slots = ea.slots;
-    ba.cnt = ea.cnt;
-    ba.ovf = ea.ovf;
-    ba.n_ovf = (int)hc.overflow;
     ba.tmp_row = tmp.get<int32_t>(nnz);
     ba.tmp_src = tmp.get<int32_t>(nnz);
     if (tmp.failed || keep.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (sparse arrays)");
-    launch_csr_fill(dv, ba, s);
-    launch_csc_build(dv, ba, s);
-    HIP_TRY(hipGetLastError());
-    pt_build.stop();
+    {
+        PhaseTimer pt(PH_BUILD, s);
+        ea.row_ptr = dv.row_ptr;
+        ea.csr_col = dv.csr_col;
+        ea.csr_row = dv.csr_row;
+        launch_emit_write(ea, s);
+        launch_csc_build(dv, ba, s);
+        HIP_TRY(hipGetLastError());
+        pt.stop();
+    }
 
     // ---- temperatures, softmaxes, P0 ---------------------------------------
     dv.T_row = keep.get<double>(BN);

@@ -15,16 +15,7 @@ constexpr int kGroup = 4;         // lanes per row / column in the sparse kernel
 
 // Device-side counters of one forward call.
 struct Counters {
-    unsigned int overflow; // emitted pairs that did not fit their slot group
-    unsigned int error;    // bit 0: a row's minima not found among its pairs; bit 1: a column's
-};
-
-// A pair that did not fit its (row, chunk) slot group.
-struct OverflowEntry {
-    int32_t row;   // global row b*N + i
-    int32_t chunk; // column chunk that emitted it
-    int32_t rank;  // position among the pairs of this (row, chunk)
-    int32_t col;   // column j within the sample
+    unsigned int error; // bit 0: a row's minima not found among its pairs; bit 1: a column's
 };
 
 struct Params {
@@ -70,15 +61,17 @@ struct EmitArgs {
     const float *x;      // [B, N, 3]
     const float4 *ypack; // [B, M]: y and its column threshold
     const float *E_row;  // [B*N]
-    int B, N, M, S, chunk, K, owner_blocks;
-    int32_t *slots;      // [B*N][S][K]
-    int32_t *cnt;        // [B*N][S]
-    OverflowEntry *ovf;
-    unsigned ovf_cap;
-    Counters *ctr;
-    int32_t *col_cnt;    // [B*M] stored pairs per column, counted during emission
+    int B, N, M, S, chunk, owner_blocks;
+    int32_t *cnt;        // [B*N][S] stored pairs per (row, column chunk)
+    int32_t *col_cnt;    // [B*M] stored pairs per column
+    // second pass
+    const int32_t *row_ptr; // [B*N+1]
+    int32_t *csr_col, *csr_row;
 };
-void launch_emit(const EmitArgs &a, hipStream_t s);
+// Pass 1 counts the candidate support per (row, chunk) and per column; pass 2
+// (after the offsets are known) writes it into the CSR arrays.
+void launch_emit_count(const EmitArgs &a, hipStream_t s);
+void launch_emit_write(const EmitArgs &a, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // sparse structure
@@ -149,15 +142,10 @@ struct DevPlan {
 };
 
 struct BuildArgs {
-    int S, K;
-    const int32_t *slots, *cnt;
-    const OverflowEntry *ovf;
-    int n_ovf;
-    int32_t *col_cnt, *col_fill; // [B*M], cleared by the finalize kernel
-    int32_t *col_tiles;          // tile sums of the column-count scan
-    int32_t *tmp_row, *tmp_src;  // column-major staging [nnz]
+    int32_t *col_fill;          // [B*M], cleared by the finalize kernel
+    int32_t *col_tiles;         // tile sums of the column-count scan
+    int32_t *tmp_row, *tmp_src; // column-major staging [nnz]
 };
-void launch_csr_fill(const DevPlan &d, const BuildArgs &a, hipStream_t s);
 // col_ptr = exclusive scan of the column counts (n = B*M columns).
 void launch_col_scan(const int32_t *col_cnt, int n, int32_t *col_ptr, int32_t *tiles, hipStream_t s);
 void launch_csc_build(const DevPlan &d, const BuildArgs &a, hipStream_t s);

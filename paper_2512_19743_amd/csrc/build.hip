@@ -1,5 +1,5 @@
 // Sparse structure of the stored pairs: row-major order (CSR; each row's
-// pairs in increasing column, as the support scan emitted them) and a
+// pairs in increasing column, written by the support scan) and a
 // column-major permutation (CSC; each column's pairs in increasing row).
 // The paper symmetrizes by concatenating the two COO streams and sorting
 // 64-bit keys (Sec. III-C); here every pair is emitted once, with both
@@ -99,42 +99,6 @@ __global__ __launch_bounds__(kBlock) void k_scan_apply(ScanArray a)
 }
 
 // ---------------------------------------------------------------------------
-// row-major fill
-// ---------------------------------------------------------------------------
-
-__global__ __launch_bounds__(kBlock) void k_csr_fill(DevPlan d, BuildArgs a)
-{
-    const int r = blockIdx.x * kBlock + threadIdx.x;
-    if (r >= d.B * d.N)
-        return;
-    int pos = d.row_ptr[r];
-    for (int c = 0; c < a.S; ++c) {
-        const int n = a.cnt[(size_t)r * a.S + c];
-        const int m = min(n, a.K);
-        const int32_t *sl = a.slots + ((size_t)r * a.S + c) * a.K;
-        for (int k = 0; k < m; ++k) {
-            d.csr_col[pos + k] = sl[k];
-            d.csr_row[pos + k] = r;
-        }
-        for (int k = m; k < n; ++k) // filled by k_ovf_fill
-            d.csr_row[pos + k] = r;
-        pos += n;
-    }
-}
-
-__global__ __launch_bounds__(kBlock) void k_ovf_fill(DevPlan d, BuildArgs a)
-{
-    const int o = blockIdx.x * kBlock + threadIdx.x;
-    if (o >= a.n_ovf)
-        return;
-    const OverflowEntry e = a.ovf[o];
-    int pos = d.row_ptr[e.row];
-    for (int c = 0; c < e.chunk; ++c)
-        pos += a.cnt[(size_t)e.row * a.S + c];
-    d.csr_col[pos + e.rank] = e.col;
-}
-
-// ---------------------------------------------------------------------------
 // column-major permutation
 // ---------------------------------------------------------------------------
 
@@ -205,12 +169,6 @@ void launch_scan(const ScanArray &a, hipStream_t s)
     hipLaunchKernelGGL(k_scan_apply, dim3(a.tiles), dim3(kBlock), 0, s, a);
 }
 
-void launch_csr_fill(const DevPlan &d, const BuildArgs &a, hipStream_t s)
-{
-    hipLaunchKernelGGL(k_csr_fill, dim3(blocks_for((int64_t)d.B * d.N, kBlock)), dim3(kBlock), 0, s, d, a);
-    if (a.n_ovf > 0)
-        hipLaunchKernelGGL(k_ovf_fill, dim3(blocks_for(a.n_ovf, kBlock)), dim3(kBlock), 0, s, d, a);
-}
 
 void launch_col_scan(const int32_t *col_cnt, int n, int32_t *col_ptr, int32_t *tiles, hipStream_t s)
 {

@@ -13,10 +13,12 @@
 //   k_emit     the candidate support: every pair inside its row's or its
 //              column's threshold. Per pair 6 VALU ops for the distance, a max
 //              of the two radii, a compare and an add-with-carry that records
-//              the hit in a per-lane bitmask of 32 columns. Each lane then
-//              appends its row's pairs, in column order, to a private slot
-//              group and counts it in its column; the exact test s >= tau is
-//              applied later in double precision on this candidate set.
+//              the hit in a per-lane bitmask of 32 columns. A first pass counts
+//              the hits per (row, column chunk) and per column; once the
+//              offsets are known, a second pass writes each row's pairs, in
+//              column order, straight into the CSR arrays. The exact test
+//              s >= tau is applied later in double precision on this
+//              candidate set.
 #include "apml_internal.h"
 #include "device_common.h"
 
@@ -78,7 +80,7 @@ __global__ __launch_bounds__(kBlock) void k_finalize(FinalizeArgs args)
 {
     int k = blockIdx.x * kBlock + threadIdx.x;
     if (k == 0)
-        *args.ctr = Counters{0, 0};
+        *args.ctr = Counters{0};
     const int which = k < args.rows ? 0 : 1;
     if (which)
         k -= args.rows;
@@ -115,18 +117,6 @@ __global__ __launch_bounds__(kBlock) void k_finalize(FinalizeArgs args)
         d.zero_a[k] = 0;
         d.zero_b[k] = 0;
     }
-}
-
-// Appends pair (row, j) to the lane's slot group when it has room, and
-// counts it in its column. Pairs beyond the slot group go to the overflow
-// list in a second pass (emit_overflow), so that the scan loop issues no
-// atomic whose result it must wait for.
-__device__ __forceinline__ void emit_pair(const EmitArgs &a, int32_t *slot, int32_t *col_cnt, int j, int &cnt)
-{
-    atomicAdd(&col_cnt[j], 1);
-    if (cnt < a.K)
-        slot[cnt] = j;
-    ++cnt;
 }
 
 // Radius test of one pair (inside the row's ball E or the column's ball w),
@@ -182,7 +172,11 @@ __device__ __forceinline__ void for_each_hit(float ax, float ay, float az, float
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_emit(EmitArgs a)
+// Pass 1 (WRITE = false) counts the hits of each (row, chunk) and of each
+// column; pass 2 writes them, in increasing column, at the row's CSR offset
+// plus the counts of the row's earlier chunks. Both passes take bitwise the
+// same decisions.
+template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs a)
 {
     const int t = blockIdx.x;
     const int ob = t % a.owner_blocks;
@@ -198,27 +192,26 @@ __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs a)
     const_ptr<f32x4> q = as_const(reinterpret_cast<const f32x4 *>(a.ypack + (size_t)b * a.M));
     const int j0 = ch * a.chunk;
     const int j1 = min(a.M, j0 + a.chunk);
-    int32_t *slot = a.slots + ((size_t)row * a.S + ch) * a.K;
-    int32_t *col_cnt = a.col_cnt + (size_t)b * a.M;
     const uint32_t keep = valid ? ~0u : 0u; // a lane without a row ignores the columns' balls too
-    int cnt = 0;
-    for_each_hit(ax, ay, az, E, q, j0, j1, keep, [&](int j) { emit_pair(a, slot, col_cnt, j, cnt); });
-    // rare: lanes with more hits than slots scan their columns again and
-    // append the hits of rank >= K to the overflow list
-    if (__builtin_amdgcn_ballot_w64(cnt > a.K)) {
-        int r = 0;
-        const uint32_t over = cnt > a.K ? ~0u : 0u;
-        for_each_hit(ax, ay, az, E, q, j0, j1, over, [&](int j) {
-            if (r >= a.K) {
-                const unsigned o = atomicAdd(&a.ctr->overflow, 1u);
-                if (o < a.ovf_cap)
-                    a.ovf[o] = OverflowEntry{row, ch, r, j};
-            }
-            ++r;
+    if (!WRITE) {
+        int32_t *col_cnt = a.col_cnt + (size_t)b * a.M;
+        int cnt = 0;
+        for_each_hit(ax, ay, az, E, q, j0, j1, keep, [&](int j) {
+            atomicAdd(&col_cnt[j], 1);
+            ++cnt;
+        });
+        if (valid)
+            a.cnt[(size_t)row * a.S + ch] = cnt;
+    } else {
+        int pos = a.row_ptr[row];
+        for (int c = 0; c < ch; ++c)
+            pos += a.cnt[(size_t)row * a.S + c];
+        for_each_hit(ax, ay, az, E, q, j0, j1, keep, [&](int j) {
+            a.csr_col[pos] = j;
+            a.csr_row[pos] = row;
+            ++pos;
         });
     }
-    if (valid)
-        a.cnt[(size_t)row * a.S + ch] = cnt;
 }
 
 } // namespace
@@ -237,9 +230,14 @@ void launch_finalize(const FinalizeDir &rows, const FinalizeDir &cols, int B, co
                        dim3(kBlock), 0, s, a);
 }
 
-void launch_emit(const EmitArgs &a, hipStream_t s)
+void launch_emit_count(const EmitArgs &a, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_emit, dim3(a.B * a.S * a.owner_blocks), dim3(kBlock), 0, s, a);
+    hipLaunchKernelGGL(k_emit<false>, dim3(a.B * a.S * a.owner_blocks), dim3(kBlock), 0, s, a);
+}
+
+void launch_emit_write(const EmitArgs &a, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_emit<true>, dim3(a.B * a.S * a.owner_blocks), dim3(kBlock), 0, s, a);
 }
 
 } // namespace apml
