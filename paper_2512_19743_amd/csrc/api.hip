@@ -301,6 +301,17 @@ int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
 // Chunks of the broadcast range so that a dense scan has about 8 waves per
 // SIMD on 256 CUs, each chunk at least 512 points long.
+// Waits for the stream by polling: the forward's one synchronisation sits
+// on the critical path, and a blocking wait adds the wake-up latency.
+hipError_t wait_for(hipStream_t s)
+{
+    for (;;) {
+        const hipError_t e = hipStreamQuery(s);
+        if (e != hipErrorNotReady)
+            return e;
+    }
+}
+
 void choose_chunks(int B, int n_own, int n_bc, int *S, int *chunk, int min_chunk = 512)
 {
     const int64_t waves = (int64_t)B * ceil_div(n_own, 64);
@@ -463,10 +474,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     choose_chunks(B, N, M, &ea.S, &ea.chunk, 256);
     ea.cnt = tmp.get<int32_t>((size_t)BN * ea.S);
     ea.col_cnt = col_cnt; // cleared by the finalize kernel
-    const int tile = scan_tile_items();
-    ScanArray sr{ea.cnt, BN, ea.S, dv.row_ptr, tmp.get<int32_t>(ceil_div(BN, tile)), ceil_div(BN, tile)};
     Readback *rb_dev = (Readback *)tmp.get<uint8_t>(readback_bytes(B));
-    ba.col_tiles = tmp.get<int32_t>(ceil_div(BM, tile));
     std::vector<uint8_t> rb_host(readback_bytes(B));
     if (tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (support)");
@@ -480,14 +488,15 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         pt.stop();
     }
     // row and column offsets, and what the host needs, in one copy
-    launch_scan(sr, s);
-    launch_col_scan(col_cnt, BM, dv.col_ptr, ba.col_tiles, s);
-    launch_readback(dv.row_ptr, col_cnt, dv.ctr, B, N, M, rb_dev, s);
+    launch_offsets(ea.cnt, ea.S, col_cnt, dv.ctr, B, N, M, dv.row_ptr, dv.col_ptr, rb_dev, s);
     HIP_TRY(hipMemcpyAsync(rb_host.data(), rb_dev, readback_bytes(B), hipMemcpyDeviceToHost, s));
-    HIP_TRY(hipStreamSynchronize(s));
+    HIP_TRY(wait_for(s));
     int64_t nnz = 0;
-    for (int b = 0; b < B; ++b)
+    for (int b = 0; b < B; ++b) {
+        if (totals[b] != totals[B + b])
+            return fail(APML_ERR_INTERNAL, "row and column counts of the support disagree");
         nnz += totals[b];
+    }
     if (nnz > (int64_t)INT32_MAX - 1)
         return fail(APML_ERR_UNSUPPORTED, "more than 2^31 stored pairs: raise tau or lower N*M");
     plan->stored = nnz;

@@ -77,17 +77,6 @@ void launch_emit_write(const EmitArgs &a, hipStream_t s);
 // sparse structure
 // ---------------------------------------------------------------------------
 
-// Exclusive prefix sum: element k is the sum of in[k*S .. k*S+S-1]; out has
-// n+1 entries (out[n] = total).
-struct ScanArray {
-    const int32_t *in;
-    int n, S;
-    int32_t *out;
-    int32_t *tile_sums;
-    int tiles;
-};
-int scan_tile_items();
-void launch_scan(const ScanArray &a, hipStream_t s);
 
 // Pieces of the per-sample Sinkhorn kernels. Each row's (column's) pairs are
 // cut into pieces of kSinkPiece consecutive pairs; an owner with n pieces
@@ -143,11 +132,9 @@ struct DevPlan {
 
 struct BuildArgs {
     int32_t *col_fill;          // [B*M], cleared by the finalize kernel
-    int32_t *col_tiles;         // tile sums of the column-count scan
     int32_t *tmp_row, *tmp_src; // column-major staging [nnz]
 };
-// col_ptr = exclusive scan of the column counts (n = B*M columns).
-void launch_col_scan(const int32_t *col_cnt, int n, int32_t *col_ptr, int32_t *tiles, hipStream_t s);
+
 void launch_csc_build(const DevPlan &d, const BuildArgs &a, hipStream_t s);
 
 void launch_softmax(const DevPlan &d, const Params &p, hipStream_t s);
@@ -157,24 +144,32 @@ void launch_bwd_softmax(const DevPlan &d, const Params &p, hipStream_t s);
 // sample with the sample's pairs in registers; the per-iteration kernels are
 // the general fallback.
 //
+// Pieces of a row or column with len pairs, and log2 of its group size.
+__device__ __forceinline__ int sink_pieces(int len) { return len < kSinkPiece ? 1 : (len + kSinkPiece - 1) / kSinkPiece; }
+__device__ __forceinline__ int sink_log2_group(int np) { return np <= 1 ? 0 : 32 - __clz(np - 1); }
+
 // What the host reads back after the support scan, in one copy: the
-// counters, the stored pairs of each sample counted in 64 bits, the pair
-// offsets of the samples (row_ptr[b*N], b = 0..B) and per sample the
-// positions needed by its rows, by its columns, and the most pieces of any
-// row or column (row lengths from row_ptr, column lengths from col_cnt).
+// counters, then per sample the stored pairs counted over rows and over
+// columns (int64 [2][B]), the pair offsets of the samples (int32 [B + 1],
+// row_ptr[b*N]) and the piece counts (int32 [B][4]: positions needed by the
+// rows, by the columns, most pieces of a row, of a column).
 struct Readback {
     Counters ctr;
+    unsigned int pad;
 };
-// After the Readback header: int64 stored pairs per sample [B] (from the
-// column counts, in 64 bits), int32 offsets [B + 1], int32 piece counts [3B].
-inline size_t readback_bytes(int B) { return sizeof(Readback) + 8 * (size_t)B + 4 * (4 * (size_t)B + 1); }
+inline size_t readback_bytes(int B) { return sizeof(Readback) + 16 * (size_t)B + 4 * (5 * (size_t)B + 1); }
 __host__ __device__ inline int64_t *readback_totals(Readback *r) { return reinterpret_cast<int64_t *>(r + 1); }
-__host__ __device__ inline int32_t *readback_offsets(Readback *r, int B) { return reinterpret_cast<int32_t *>(readback_totals(r) + B); }
+__host__ __device__ inline int32_t *readback_offsets(Readback *r, int B) { return reinterpret_cast<int32_t *>(readback_totals(r) + 2 * B); }
 __host__ __device__ inline int32_t *readback_pieces(Readback *r, int B) { return readback_offsets(r, B) + B + 1; }
-void launch_readback(const int32_t *row_ptr, const int32_t *col_cnt, const Counters *ctr, int B, int N, int M,
-                     Readback *out, hipStream_t s);
+
+// Row and column offsets of all samples (row_ptr [B*N+1] from the per-(row,
+// chunk) counts cnt [B*N][S], col_ptr [B*M+1] from col_cnt) and the read-back
+// block, in two launches.
+void launch_offsets(const int32_t *cnt, int S, const int32_t *col_cnt, const Counters *ctr, int B, int N, int M,
+                    int32_t *row_ptr, int32_t *col_ptr, Readback *rb, hipStream_t s);
 // Whether the per-sample kernels take a batch: counts are the host copy of the
-// piece counts above, max_pairs the largest sample's stored pairs.
+// piece counts of the read-back block, max_pairs the largest sample's stored
+// pairs.
 bool sinkhorn_fwd_fits(int N, int M, const int32_t *counts, int B);
 bool sinkhorn_bwd_fits(int N, int M, const int32_t *counts, int B, int64_t max_pairs);
 size_t packed_order_words(int B); // 32-bit words of one PackedOrder's p0 array

@@ -11,91 +11,108 @@ namespace apml {
 namespace {
 
 // ---------------------------------------------------------------------------
-// exclusive prefix sums (three phases: tile sums, scan of tile sums, apply)
+// per-sample offsets
 // ---------------------------------------------------------------------------
 
-constexpr int kScanItems = 8;
-constexpr int kScanTile = kBlock * kScanItems;
+constexpr int kOffT = 1024;
 
-__device__ __forceinline__ int scan_load(const ScanArray &a, int k)
+// Per sample (blockIdx.x) and direction (blockIdx.y: 0 rows, 1 columns): the
+// sample-local exclusive scan of the owners' pair counts into row_ptr /
+// col_ptr, the sample's total and its piece counts.
+__global__ __launch_bounds__(kOffT) void k_sample_scan(const int32_t *cnt, int S, const int32_t *col_cnt, int N,
+                                                       int M, int32_t *row_ptr, int32_t *col_ptr, Readback *rb)
 {
-    if (k >= a.n)
-        return 0;
-    int s = 0;
-    for (int c = 0; c < a.S; ++c)
-        s += a.in[(size_t)k * a.S + c];
-    return s;
-}
-
-// Exclusive scan of one value per thread over the block; *total gets the sum.
-__device__ int block_exclusive_scan(int v, int *total)
-{
-    __shared__ int wave_sums[kBlock / 64];
-    const int lane = lane_id(), wave = threadIdx.x >> 6;
-    int inc = v;
-    for (int off = 1; off < 64; off <<= 1) {
-        const int n = __shfl_up(inc, off);
-        if (lane >= off)
-            inc += n;
+    __shared__ int wsum[kOffT / 64];
+    __shared__ int red[2][kOffT / 64];
+    const int b = blockIdx.x, rows = blockIdx.y == 0, tid = threadIdx.x, B = gridDim.x;
+    const int lane = lane_id(), wave = tid >> 6;
+    const int n = rows ? N : M;
+    int32_t *out = rows ? row_ptr + (size_t)b * N : col_ptr + (size_t)b * M;
+    int carry = 0, pos = 0, mx = 0;
+    for (int base = 0; base < n; base += kOffT) {
+        const int k = base + tid;
+        int len = 0;
+        if (k < n) {
+            if (rows)
+                for (int c = 0; c < S; ++c)
+                    len += cnt[((size_t)b * N + k) * S + c];
+            else
+                len = col_cnt[(size_t)b * M + k];
+            const int np = sink_pieces(len);
+            pos += 1 << min(sink_log2_group(np), 30);
+            mx = max(mx, np);
+        }
+        int inc = len;
+        for (int off = 1; off < 64; off <<= 1) {
+            const int v = __shfl_up(inc, off);
+            if (lane >= off)
+                inc += v;
+        }
+        if (lane == 63)
+            wsum[wave] = inc;
+        __syncthreads();
+        int before = 0, all = 0;
+        for (int w = 0; w < kOffT / 64; ++w) {
+            before += w < wave ? wsum[w] : 0;
+            all += wsum[w];
+        }
+        __syncthreads();
+        if (k < n)
+            out[k] = carry + before + inc - len;
+        carry += all;
     }
-    if (lane == 63)
-        wave_sums[wave] = inc;
+    for (int off = 32; off > 0; off >>= 1) {
+        pos += __shfl_xor(pos, off);
+        mx = max(mx, __shfl_xor(mx, off));
+    }
+    if (lane == 0) {
+        red[0][wave] = pos;
+        red[1][wave] = mx;
+    }
     __syncthreads();
-    int base = 0, all = 0;
-    for (int w = 0; w < kBlock / 64; ++w) {
-        if (w < wave)
-            base += wave_sums[w];
-        all += wave_sums[w];
+    if (tid == 0) {
+        int a = 0, m = 0;
+        for (int w = 0; w < kOffT / 64; ++w) {
+            a += red[0][w];
+            m = max(m, red[1][w]);
+        }
+        readback_totals(rb)[(rows ? 0 : B) + b] = carry;
+        int32_t *pc = readback_pieces(rb, B) + 4 * b;
+        pc[rows ? 0 : 1] = a;
+        pc[rows ? 2 : 3] = m;
+    }
+}
+
+// Adds each sample's base (pairs of the earlier samples) to its local
+// offsets, closes row_ptr / col_ptr with the total and fills the read-back
+// offsets and counters.
+__global__ __launch_bounds__(kOffT) void k_sample_base(const Counters *ctr, int N, int M, int32_t *row_ptr,
+                                                       int32_t *col_ptr, Readback *rb)
+{
+    __shared__ int base_s;
+    const int b = blockIdx.x, rows = blockIdx.y == 0, tid = threadIdx.x, B = gridDim.x;
+    const int64_t *tot = readback_totals(rb) + (rows ? 0 : B);
+    if (tid == 0) {
+        int64_t base = 0;
+        for (int k = 0; k < b; ++k)
+            base += tot[k];
+        base_s = (int)base; // the host rejects totals beyond int32 before using any offset
+        if (rows)
+            readback_offsets(rb, B)[b] = (int)base;
+        if (b == B - 1) {
+            const int end = (int)(base + tot[b]);
+            (rows ? row_ptr[(size_t)B * N] : col_ptr[(size_t)B * M]) = end;
+            if (rows)
+                readback_offsets(rb, B)[B] = end;
+        }
+        if (b == 0 && rows)
+            rb->ctr = *ctr;
     }
     __syncthreads();
-    *total = all;
-    return base + inc - v;
-}
-
-__global__ __launch_bounds__(kBlock) void k_scan_reduce(ScanArray a)
-{
-    const int k0 = blockIdx.x * kScanTile + threadIdx.x * kScanItems;
-    int s = 0;
-    for (int u = 0; u < kScanItems; ++u)
-        s += scan_load(a, k0 + u);
-    int total;
-    block_exclusive_scan(s, &total);
-    if (threadIdx.x == 0)
-        a.tile_sums[blockIdx.x] = total;
-}
-
-__global__ __launch_bounds__(kBlock) void k_scan_tiles(ScanArray a)
-{
-    int carry = 0;
-    for (int base = 0; base < a.tiles; base += kBlock) {
-        const int k = base + threadIdx.x;
-        const int v = k < a.tiles ? a.tile_sums[k] : 0;
-        int total;
-        const int ex = block_exclusive_scan(v, &total);
-        if (k < a.tiles)
-            a.tile_sums[k] = carry + ex;
-        carry += total;
-    }
-    if (threadIdx.x == 0)
-        a.out[a.n] = carry;
-}
-
-__global__ __launch_bounds__(kBlock) void k_scan_apply(ScanArray a)
-{
-    const int k0 = blockIdx.x * kScanTile + threadIdx.x * kScanItems;
-    int v[kScanItems];
-    int s = 0;
-    for (int u = 0; u < kScanItems; ++u) {
-        v[u] = scan_load(a, k0 + u);
-        s += v[u];
-    }
-    int total;
-    int run = block_exclusive_scan(s, &total) + a.tile_sums[blockIdx.x];
-    for (int u = 0; u < kScanItems; ++u) {
-        if (k0 + u < a.n)
-            a.out[k0 + u] = run;
-        run += v[u];
-    }
+    const int n = rows ? N : M;
+    int32_t *out = rows ? row_ptr + (size_t)b * N : col_ptr + (size_t)b * M;
+    for (int k = tid; k < n; k += kOffT)
+        out[k] += base_s;
 }
 
 // ---------------------------------------------------------------------------
@@ -160,20 +177,11 @@ __global__ __launch_bounds__(kBlock) void k_count_support(const int32_t *row_ptr
 
 } // namespace
 
-int scan_tile_items() { return kScanTile; }
-
-void launch_scan(const ScanArray &a, hipStream_t s)
+void launch_offsets(const int32_t *cnt, int S, const int32_t *col_cnt, const Counters *ctr, int B, int N, int M,
+                    int32_t *row_ptr, int32_t *col_ptr, Readback *rb, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_scan_reduce, dim3(a.tiles), dim3(kBlock), 0, s, a);
-    hipLaunchKernelGGL(k_scan_tiles, dim3(1), dim3(kBlock), 0, s, a);
-    hipLaunchKernelGGL(k_scan_apply, dim3(a.tiles), dim3(kBlock), 0, s, a);
-}
-
-
-void launch_col_scan(const int32_t *col_cnt, int n, int32_t *col_ptr, int32_t *tiles, hipStream_t s)
-{
-    ScanArray sc{col_cnt, n, 1, col_ptr, tiles, (n + kScanTile - 1) / kScanTile};
-    launch_scan(sc, s);
+    hipLaunchKernelGGL(k_sample_scan, dim3(B, 2), dim3(kOffT), 0, s, cnt, S, col_cnt, N, M, row_ptr, col_ptr, rb);
+    hipLaunchKernelGGL(k_sample_base, dim3(B, 2), dim3(kOffT), 0, s, ctr, N, M, row_ptr, col_ptr, rb);
 }
 
 void launch_csc_build(const DevPlan &d, const BuildArgs &a, hipStream_t s)

@@ -44,71 +44,14 @@ constexpr int kP = kSinkPiece;
 constexpr int kSL = kSinkOwners / kSinkLanes; // owners per lane in the owner phase
 constexpr int kCap = kT * kSLP;               // positions per sample and order
 
-__device__ __forceinline__ int pieces_of(int len) { return max(1, (len + kP - 1) / kP); }
-__device__ __forceinline__ int log2_group(int np) { return np <= 1 ? 0 : 32 - __clz(np - 1); }
+__device__ __forceinline__ int pieces_of(int len) { return sink_pieces(len); }
+__device__ __forceinline__ int log2_group(int np) { return sink_log2_group(np); }
 
 // Word w of position p in a plane-major packed array with `words` words per
 // position.
 __device__ __forceinline__ size_t pk_index(int b, int p, int w, int words)
 {
     return (((size_t)b * kSLP + p / kT) * words + w) * kT + p % kT;
-}
-
-__global__ __launch_bounds__(kT) void k_readback(const int32_t *row_ptr, const int32_t *col_cnt,
-                                                 const Counters *ctr, int N, int M, Readback *rb)
-{
-    __shared__ int red[3][kT / 64];
-    __shared__ long long tot[kT / 64];
-    const int b = blockIdx.x, tid = threadIdx.x, B = gridDim.x;
-    int32_t *offsets = readback_offsets(rb, B), *out = readback_pieces(rb, B);
-    if (tid == 0) {
-        offsets[b] = row_ptr[(size_t)b * N];
-        if (b == B - 1)
-            offsets[B] = row_ptr[(size_t)B * N];
-        if (b == 0)
-            rb->ctr = *ctr;
-    }
-    int pr = 0, pc = 0, mx = 0;
-    for (int i = tid; i < N; i += kT) {
-        const int np = pieces_of(row_ptr[(size_t)b * N + i + 1] - row_ptr[(size_t)b * N + i]);
-        pr += 1 << min(log2_group(np), 30);
-        mx = max(mx, np);
-    }
-    long long pairs = 0;
-    for (int j = tid; j < M; j += kT) {
-        const int n = col_cnt[(size_t)b * M + j];
-        const int np = pieces_of(n);
-        pairs += n;
-        pc += 1 << min(log2_group(np), 30);
-        mx = max(mx, np);
-    }
-    for (int o = 32; o > 0; o >>= 1) {
-        pr += __shfl_xor(pr, o);
-        pc += __shfl_xor(pc, o);
-        mx = max(mx, __shfl_xor(mx, o));
-        pairs += __shfl_xor(pairs, o);
-    }
-    if (lane_id() == 0) {
-        red[0][tid >> 6] = pr;
-        red[1][tid >> 6] = pc;
-        red[2][tid >> 6] = mx;
-        tot[tid >> 6] = pairs;
-    }
-    __syncthreads();
-    if (tid == 0) {
-        int a = 0, c = 0, m = 0;
-        long long t = 0;
-        for (int w = 0; w < kT / 64; ++w) {
-            a += red[0][w];
-            c += red[1][w];
-            m = max(m, red[2][w]);
-            t += tot[w];
-        }
-        readback_totals(rb)[b] = t;
-        out[3 * b] = a;
-        out[3 * b + 1] = c;
-        out[3 * b + 2] = m;
-    }
 }
 
 // Placement of the pieces of one order (blockIdx.y: 0 rows, 1 columns) of
@@ -677,18 +620,13 @@ __global__ __launch_bounds__(kBlock) void k_bwd_sink_col(DevPlan d, int l)
 
 } // namespace
 
-void launch_readback(const int32_t *row_ptr, const int32_t *col_cnt, const Counters *ctr, int B, int N, int M,
-                     Readback *out, hipStream_t s)
-{
-    hipLaunchKernelGGL(k_readback, dim3(B), dim3(kT), 0, s, row_ptr, col_cnt, ctr, N, M, out);
-}
-
 bool sinkhorn_fwd_fits(int N, int M, const int32_t *counts, int B)
 {
     if (N > kSinkOwners || M > kSinkOwners)
         return false;
     for (int b = 0; b < B; ++b)
-        if (counts[3 * b] > kCap || counts[3 * b + 1] > kCap || counts[3 * b + 2] > kSinkMaxGroup)
+        if (counts[4 * b] > kCap || counts[4 * b + 1] > kCap || counts[4 * b + 2] > kSinkMaxGroup ||
+            counts[4 * b + 3] > kSinkMaxGroup)
             return false;
     return true;
 }
