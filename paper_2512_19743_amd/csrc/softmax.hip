@@ -116,6 +116,12 @@ __global__ __launch_bounds__(kBlock) void k_row_softmax(DevPlan d, Params p)
     }
 }
 
+// Columns of at most G * kColCache pairs keep their pairs in registers (one
+// pass over the column's data instead of three); the cost of a pair is
+// recomputed from the coordinates, bitwise as the row kernel computed it,
+// instead of being gathered from the row-major array.
+constexpr int kColCache = 4;
+
 __global__ __launch_bounds__(kBlock) void k_col_softmax(DevPlan d, Params p)
 {
     const int gid = blockIdx.x * kBlock + threadIdx.x;
@@ -128,10 +134,28 @@ __global__ __launch_bounds__(kBlock) void k_col_softmax(DevPlan d, Params p)
     const float *xb = d.x + (size_t)b * d.N * 3;
     const float2 m = d.m12_col[gc];
     const int s0 = d.col_ptr[gc], s1 = d.col_ptr[gc + 1];
+    const bool cached = s1 - s0 <= G * kColCache; // the same for the whole group
     Argmins am;
-    for (int q = s0 + lg; q < s1; q += G) {
-        const float *xi = xb + 3 * (size_t)d.csc_row[q];
-        am.see(q, sqdist_f32(y0, y1, y2, xi[0], xi[1], xi[2]), m);
+    int tq[kColCache];
+    double cq[kColCache];
+    if (cached) {
+#pragma unroll
+        for (int k = 0; k < kColCache; ++k) {
+            const int q = s0 + lg + G * k;
+            tq[k] = -1;
+            cq[k] = 0.0;
+            if (q < s1) {
+                const float *xi = xb + 3 * (size_t)d.csc_row[q];
+                am.see(q, sqdist_f32(y0, y1, y2, xi[0], xi[1], xi[2]), m);
+                cq[k] = dist_f64(xi, yc);
+                tq[k] = d.csc_perm[q];
+            }
+        }
+    } else {
+        for (int q = s0 + lg; q < s1; q += G) {
+            const float *xi = xb + 3 * (size_t)d.csc_row[q];
+            am.see(q, sqdist_f32(y0, y1, y2, xi[0], xi[1], xi[2]), m);
+        }
     }
     int q1, q2;
     am.resolve(&q1, &q2);
@@ -151,22 +175,44 @@ __global__ __launch_bounds__(kBlock) void k_col_softmax(DevPlan d, Params p)
         }
         return;
     }
-    const double c1 = d.cost[d.csc_perm[q1]];
-    const double c2 = d.cost[d.csc_perm[q2]];
+    double c1, c2;
+    if (cached) {
+        double a1 = 0.0, a2 = 0.0;
+#pragma unroll
+        for (int k = 0; k < kColCache; ++k) {
+            const int q = s0 + lg + G * k;
+            a1 += q == q1 ? cq[k] : 0.0;
+            a2 += q == q2 ? cq[k] : 0.0;
+        }
+        c1 = group_sum<G>(a1); // one lane holds it, the others add zeros
+        c2 = group_sum<G>(a2);
+    } else {
+        c1 = d.cost[d.csc_perm[q1]];
+        c2 = d.cost[d.csc_perm[q2]];
+    }
     const double gap = (c2 - c1) + p.delta;
     const bool clamped = gap < p.eps_gap;
     const double g = clamped ? p.eps_gap : gap;
     const double T = p.lk_col / g;
     double z = 0.0;
-    for (int q = s0 + lg; q < s1; q += G) {
-        const double s = exp(-T * (d.cost[d.csc_perm[q]] - c1));
-        if (s >= p.tau)
-            z += s;
+    if (cached) {
+#pragma unroll
+        for (int k = 0; k < kColCache; ++k)
+            if (tq[k] >= 0) {
+                const double s = exp(-T * (cq[k] - c1));
+                if (s >= p.tau)
+                    z += s;
+            }
+    } else {
+        for (int q = s0 + lg; q < s1; q += G) {
+            const double s = exp(-T * (d.cost[d.csc_perm[q]] - c1));
+            if (s >= p.tau)
+                z += s;
+        }
     }
     z = group_sum<G>(z);
-    for (int q = s0 + lg; q < s1; q += G) {
-        const int t = d.csc_perm[q];
-        const double s = exp(-T * (d.cost[t] - c1));
+    auto write = [&](int q, int t, double c) {
+        const double s = exp(-T * (c - c1));
         const bool keep = s >= p.tau;
         const double pc = keep ? s / z : 0.0;
         d.flags[t] = (uint8_t)(d.flags[t] | (keep ? 2 : 0));
@@ -174,6 +220,17 @@ __global__ __launch_bounds__(kBlock) void k_col_softmax(DevPlan d, Params p)
         d.p_col[q] = (float)pc;
         d.p0c[q] = p0;
         d.p0r[t] = p0;
+    };
+    if (cached) {
+#pragma unroll
+        for (int k = 0; k < kColCache; ++k)
+            if (tq[k] >= 0)
+                write(s0 + lg + G * k, tq[k], cq[k]);
+    } else {
+        for (int q = s0 + lg; q < s1; q += G) {
+            const int t = d.csc_perm[q];
+            write(q, t, d.cost[t]);
+        }
     }
     if (lg == 0) {
         d.T_col[gc] = T;
@@ -201,6 +258,53 @@ __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(DevPlan d, Params p)
     const int b = gc / d.M;
     const double gl = d.grad_loss[b];
     const int s0 = d.col_ptr[gc], s1 = d.col_ptr[gc + 1];
+    const double T = d.T_col[gc], c1 = d.C1_col[gc];
+    const double gapbar_scale = d.clamp_col[gc] ? 0.0 : -T / d.g_col[gc];
+    const int q1 = d.pos_col[2 * (size_t)gc], q2 = d.pos_col[2 * (size_t)gc + 1];
+    if (s1 - s0 <= G * kColCache) {
+        // one pass over the column's data: kept pairs' P_col, dL/dP0 and cost in registers
+        const float *yc = d.y + (size_t)gc * 3;
+        const float *xb = d.x + (size_t)b * d.N * 3;
+        int tq[kColCache];
+        double pq[kColCache], aq[kColCache], cq[kColCache];
+        double sigma = 0.0;
+#pragma unroll
+        for (int k = 0; k < kColCache; ++k) {
+            const int q = s0 + lg + G * k;
+            tq[k] = -1;
+            pq[k] = aq[k] = cq[k] = 0.0;
+            if (q < s1) {
+                const int t = d.csc_perm[q];
+                tq[k] = t;
+                if (d.flags[t] & 2) {
+                    pq[k] = (double)d.p_col[q];
+                    aq[k] = 0.5 * p0bar(d, t, gl);
+                    cq[k] = dist_f64(xb + 3 * (size_t)d.csc_row[q], yc);
+                    sigma += pq[k] * aq[k];
+                }
+            }
+        }
+        sigma = group_sum<G>(sigma);
+        double tbar = 0.0;
+#pragma unroll
+        for (int k = 0; k < kColCache; ++k)
+            tbar -= pq[k] * (aq[k] - sigma) * (cq[k] - c1); // zero for pairs not kept
+        tbar = group_sum<G>(tbar);
+        const double gapbar = gapbar_scale * tbar;
+#pragma unroll
+        for (int k = 0; k < kColCache; ++k) {
+            const int q = s0 + lg + G * k;
+            if (tq[k] >= 0) {
+                double cb = -T * pq[k] * (aq[k] - sigma);
+                if (q == q2)
+                    cb += gapbar;
+                if (q == q1)
+                    cb -= gapbar;
+                d.cbar[tq[k]] = cb;
+            }
+        }
+        return;
+    }
     double sigma = 0.0;
     for (int q = s0 + lg; q < s1; q += G) {
         const int t = d.csc_perm[q];
@@ -208,7 +312,6 @@ __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(DevPlan d, Params p)
             sigma += (double)d.p_col[q] * 0.5 * p0bar(d, t, gl);
     }
     sigma = group_sum<G>(sigma);
-    const double T = d.T_col[gc], c1 = d.C1_col[gc];
     double tbar = 0.0;
     for (int q = s0 + lg; q < s1; q += G) {
         const int t = d.csc_perm[q];
@@ -218,8 +321,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(DevPlan d, Params p)
         }
     }
     tbar = group_sum<G>(tbar);
-    const double gapbar = d.clamp_col[gc] ? 0.0 : -tbar * T / d.g_col[gc];
-    const int q1 = d.pos_col[2 * (size_t)gc], q2 = d.pos_col[2 * (size_t)gc + 1];
+    const double gapbar = gapbar_scale * tbar;
     for (int q = s0 + lg; q < s1; q += G) {
         const int t = d.csc_perm[q];
         double cb = 0.0;
