@@ -68,24 +68,24 @@ PHASE_MODEL = {
 
 # HBM bytes per launch measured with rocprofv3 counters (FETCH_SIZE and
 # WRITE_SIZE, KiB per dispatch, each scaled by the same counter's reading for
-# a plain device copy of known size). Each entry names the source file it was
-# measured on and that file's SHA-256: once the file changes, traffic is
-# reported as null until measured again.
+# a plain device copy of known size), summed over the phase's kernels. Each
+# entry names the source files it was measured on with their SHA-256: once a
+# file changes, traffic is reported as null until measured again.
 TRAFFIC = {
-    "stats": {"source": "paper_2512_19743_amd/csrc/dense.hip", "sha256": "f399107bed24cfcc2ea41a6d8214c225236a4b4d616063b962cbfcd3d9a07386",
-              "kernels": ["k_top2"], "bytes_per_launch": 27850447},
-    "support": {"source": "paper_2512_19743_amd/csrc/dense.hip", "sha256": "f399107bed24cfcc2ea41a6d8214c225236a4b4d616063b962cbfcd3d9a07386",
-              "kernels": ["k_emit"], "bytes_per_launch": 24107499},
-    "build": {"source": "paper_2512_19743_amd/csrc/build.hip", "sha256": "0d4b8abe202b425f1450e3ba02cf243d36f99f55e84e53020b40c004ae146fa6",
-              "kernels": ["k_csr_fill", "k_ovf_fill", "k_col_hist", "k_scan_reduce", "k_scan_tiles", "k_scan_apply", "k_csc_fill", "k_csc_sort"], "bytes_per_launch": 78878543},
-    "softmax": {"source": "paper_2512_19743_amd/csrc/softmax.hip", "sha256": "b01efbbd9d54d1f5d88cb80f906e1e04475b4fe6c2354ea28c5d5324ce972d0c",
-              "kernels": ["k_row_softmax", "k_col_softmax"], "bytes_per_launch": 120298708},
-    "sinkhorn": {"source": "paper_2512_19743_amd/csrc/sinkhorn.hip", "sha256": "ed5c3a1a8c923176204281003249261a8e143f981b9e9d6237e83a943749bb9d",
-              "kernels": ["k_sinkhorn_fwd"], "bytes_per_launch": 41521939},
-    "bwd_sinkhorn": {"source": "paper_2512_19743_amd/csrc/sinkhorn.hip", "sha256": "ed5c3a1a8c923176204281003249261a8e143f981b9e9d6237e83a943749bb9d",
-              "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 60778166},
-    "bwd_softmax": {"source": "paper_2512_19743_amd/csrc/softmax.hip", "sha256": "b01efbbd9d54d1f5d88cb80f906e1e04475b4fe6c2354ea28c5d5324ce972d0c",
-              "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 109464758},
+    "stats": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "01860daa9c746654d974da689bd7408f0cb3934d74685c6b20970025f8c23b0f"},
+              "kernels": ["k_top2"], "bytes_per_launch": 27840037},
+    "support": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "01860daa9c746654d974da689bd7408f0cb3934d74685c6b20970025f8c23b0f"},
+              "kernels": ["k_emit"], "bytes_per_launch": 25438631},
+    "build": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "01860daa9c746654d974da689bd7408f0cb3934d74685c6b20970025f8c23b0f", "paper_2512_19743_amd/csrc/build.hip": "6723dba8905fa6f817b70685fbcc8ca8ac2a9ccb306df467aa05524ef4d4a134"},
+              "kernels": ["k_emit", "k_csc_fill", "k_csc_sort"], "bytes_per_launch": 77945908},
+    "softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "3609b543c9dc952699450f88633f27542562abd386bcd7f0474fa6ab4cd999a4"},
+              "kernels": ["k_row_softmax", "k_col_softmax"], "bytes_per_launch": 69352898},
+    "sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "0e84d29e1b824a91e75f0334a7d28a1b38c78d9f96e8ccff872df1bc31edffe3"},
+              "kernels": ["k_place", "k_pack_pairs", "k_sinkhorn_fwd"], "bytes_per_launch": 71988287},
+    "bwd_sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "0e84d29e1b824a91e75f0334a7d28a1b38c78d9f96e8ccff872df1bc31edffe3"},
+              "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 44354585},
+    "bwd_softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "3609b543c9dc952699450f88633f27542562abd386bcd7f0474fa6ab4cd999a4"},
+              "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 79758875},
 }
 
 
@@ -98,7 +98,7 @@ def _sha(path):
 
 def traffic_for(phase, d):
     t = TRAFFIC.get(phase)
-    if not t or _sha(t["source"]) != t["sha256"]:
+    if not t or any(_sha(src) != h for src, h in t["sources"].items()):
         return None
     return t["bytes_per_launch"]
 
