@@ -265,7 +265,7 @@ __device__ __forceinline__ void store_sum(double acc, uint32_t info, double *sum
 }
 
 constexpr size_t fwd_lds_bytes() { return 8 * 3 * (size_t)kSinkOwners; }
-constexpr size_t bwd_fixed_lds_bytes() { return (8 + 3 * 4) * (size_t)kSinkOwners; }
+constexpr size_t bwd_fixed_lds_bytes() { return (8 + 8 + 4 + 4) * (size_t)kSinkOwners; }
 
 __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
 {
@@ -378,14 +378,27 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
 
 // Reverse sweeps, last iteration first. The plan adjoint starts as
 // grad_loss * C (loss = sum v C) and ends as dLoss/dP0 in d.adj (row-major).
+//
+// Scaled representation. With the lazy updates above a row piece would need
+// three per-column values (the pending 1/(S + eps), q and beta) and a column
+// piece three per-row values. Storing instead z = adjoint * alpha^l_i before
+// a row phase and z = adjoint * beta^l_j before a column phase, each phase
+// needs two values of the other side, X and Y, and one value of its own
+// owner, 1/alpha or 1/beta:
+//   row phase l:    z' = (z / alpha^l_i) X_j - Y_j,  X_j = beta^l_j / (S_j + eps),
+//                   Y_j = beta^l_j e_j / (S_j + eps)     (pending column update)
+//   column phase l: z' = (z / beta^l_j) X_i - Y_i,   X_i = alpha^(l-1)_i / (R_i + eps),
+//                   Y_i = alpha^(l-1)_i d_i / (R_i + eps)
+// and the row sum d_i / alpha^l_i (column sum e_j / beta^l_j) is just the sum
+// of z' P0 over the row's (column's) pairs. X, Y and the reciprocals are kept
+// in single precision, the adjoint and all sums in double.
 __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
 {
     extern __shared__ double lds[];
-    // one side's values at a time: rows (alpha^(l-1), 1/(R + eps), q) after a
-    // row owner phase, columns (beta^l, 1/(S + eps), q) after a column owner phase
     double *sums = lds;
-    float *s0 = reinterpret_cast<float *>(sums + kSinkOwners), *s1 = s0 + kSinkOwners, *s2 = s1 + kSinkOwners;
-    double *adj = reinterpret_cast<double *>(s2 + kSinkOwners);
+    float2 *xy = reinterpret_cast<float2 *>(sums + kSinkOwners); // one side at a time
+    float *inv_a = reinterpret_cast<float *>(xy + kSinkOwners), *inv_b = inv_a + kSinkOwners;
+    double *adj = reinterpret_cast<double *>(inv_b + kSinkOwners);
     const int b = blockIdx.x, tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
@@ -395,18 +408,20 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
     load_pieces(pr, d.pk_row, b);
     load_pieces(pc, d.pk_col, b);
     const double gl = d.grad_loss[b];
+    const double *alpha_L = d.alpha + L * BN;
     for (int t = lo + tid; t < hi; t += kT)
-        adj[t - lo] = gl * d.cost[t];
+        adj[t - lo] = gl * d.cost[t] * alpha_L[d.csr_row[t]];
     double a_own[kSL], b_own[kSL];
 #pragma unroll
     for (int s = 0; s < kSL; ++s) {
         const int k = kSL * tid + s;
-        a_own[s] = k < N ? d.alpha[L * BN + (size_t)b * N + k] : 0.0;
-        b_own[s] = k < M ? d.beta[L * BM + (size_t)b * M + k] : 0.0;
+        a_own[s] = k < N ? alpha_L[(size_t)b * N + k] : 1.0;
+        b_own[s] = k < M ? d.beta[L * BM + (size_t)b * M + k] : 1.0;
+        if (k < N)
+            inv_a[k] = (float)(1.0 / a_own[s]);
         if (k < M) { // no pending column update before the last iteration
-            s0[k] = (float)b_own[s];
-            s1[k] = 1.0f;
-            s2[k] = 0.0f;
+            xy[k] = make_float2((float)b_own[s], 0.0f);
+            inv_b[k] = (float)(1.0 / b_own[s]);
         }
     }
     lds_barrier();
@@ -418,82 +433,80 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
         for (int s = 0; s < kSL; ++s) {
             const int k = kSL * tid + s;
             rden[s] = k < N ? d.rden[(l - 1) * BN + (size_t)b * N + k] : 1.0;
-            a_prev[s] = k < N ? d.alpha[(l - 1) * BN + (size_t)b * N + k] : 0.0;
+            a_prev[s] = k < N ? d.alpha[(l - 1) * BN + (size_t)b * N + k] : 1.0;
             sden[s] = k < M ? d.sden[(l - 1) * BM + (size_t)b * M + k] : 1.0;
-            b_prev[s] = (k < M && l > 1) ? d.beta[(l - 1) * BM + (size_t)b * M + k] : 0.0;
+            b_prev[s] = k < M ? d.beta[(l - 1) * BM + (size_t)b * M + k] : 1.0;
         }
-        // row pieces: apply the pending column update, then sum
-        // ubar * P0 * beta^l over each row
+        // row phase
 #pragma unroll
         for (int s = 0; s < kSLP; ++s)
             if (wave_active(pr, s)) {
                 const int run = (int)(pr.info[s] >> 16);
+                const double inv = (double)inv_a[pr.info[s] & 0x7FFu];
                 double m[kP];
                 pvisit(pr, s, [&](int e, int, float, bool real) { m[e] = real ? adj[run + e] : 0.0; });
                 double acc = 0.0;
                 pvisit(pr, s, [&](int e, int j, float p0, bool real) {
-                    const double a = m[e] * (double)s1[j] - (double)s2[j];
+                    const float2 w = xy[j];
+                    const double z = (m[e] * inv) * (double)w.x - (double)w.y;
                     if (real)
-                        adj[run + e] = a;
-                    acc += a * ((double)p0 * (double)s0[j]);
+                        adj[run + e] = z;
+                    acc += z * (double)p0;
                 });
                 store_sum(group_reduce(acc, pr.info[s]), pr.info[s], sums);
             }
         lds_barrier();
-        // row owners (adjoint of Eq. 4): d_i = alpha^l_i * sum; publish
-        // alpha^(l-1), 1/(R + eps) and q = d_i/(R + eps)
+        // row owners (adjoint of Eq. 4): d_i = alpha^l_i * sum
 #pragma unroll
         for (int s = 0; s < kSL; ++s) {
             const int i = kSL * tid + s;
             const double dsum = a_own[s] * sums[min(i, N - 1)];
             const double r = 1.0 / rden[s];
             if (i < N) {
-                s0[i] = (float)a_prev[s];
-                s1[i] = (float)r;
-                s2[i] = (float)(dsum * r);
+                xy[i] = make_float2((float)(r * a_prev[s]), (float)(dsum * r * a_prev[s]));
+                inv_a[i] = (float)(1.0 / a_prev[s]);
             }
         }
         lds_barrier();
-        // column pieces: apply the row update, then sum
-        // wbar * alpha^(l-1) * P0 over each column
+        // column phase
 #pragma unroll
         for (int s = 0; s < kSLP; ++s)
             if (wave_active(pc, s)) {
+                const double inv = (double)inv_b[pc.info[s] & 0x7FFu];
                 double m[kP];
                 pvisit(pc, s, [&](int e, int, float, bool real) {
                     m[e] = real ? adj[half16(opaque(pc.pos[s][e / 2]), e)] : 0.0;
                 });
                 double acc = 0.0;
                 pvisit(pc, s, [&](int e, int i, float p0, bool real) {
-                    const double a = m[e] * (double)s1[i] - (double)s2[i];
+                    const float2 w = xy[i];
+                    const double z = (m[e] * inv) * (double)w.x - (double)w.y;
                     if (real)
-                        adj[half16(opaque(pc.pos[s][e / 2]), e)] = a;
-                    acc += a * ((double)s0[i] * (double)p0);
+                        adj[half16(opaque(pc.pos[s][e / 2]), e)] = z;
+                    acc += z * (double)p0;
                 });
                 store_sum(group_reduce(acc, pc.info[s]), pc.info[s], sums);
             }
         lds_barrier();
-        // column owners (adjoint of Eq. 3): e_j = beta^l_j * sum; publish
-        // beta^(l-1), 1/(S + eps) and q = e_j/(S + eps)
+        // column owners (adjoint of Eq. 3): e_j = beta^l_j * sum
 #pragma unroll
         for (int s = 0; s < kSL; ++s) {
             const int j = kSL * tid + s;
             const double esum = b_own[s] * sums[min(j, M - 1)];
             const double r = 1.0 / sden[s];
             if (j < M) {
-                s0[j] = (float)b_prev[s];
-                s1[j] = (float)r;
-                s2[j] = (float)(esum * r);
+                xy[j] = make_float2((float)(r * b_prev[s]), (float)(esum * r * b_prev[s]));
+                inv_b[j] = (float)(1.0 / b_prev[s]);
             }
             a_own[s] = a_prev[s];
             b_own[s] = b_prev[s];
         }
         lds_barrier();
     }
-    // the last column update, written out in row-major order
+    // the last column update (alpha^0 = beta^0 = 1), written out in row-major order
     for (int t = lo + tid; t < hi; t += kT) {
-        const int j = d.csr_col[t];
-        d.adj[t] = adj[t - lo] * (double)s1[j] - (double)s2[j];
+        const float2 w = xy[d.csr_col[t]];
+        d.adj[t] = adj[t - lo] * (double)w.x - (double)w.y;
     }
 }
 
