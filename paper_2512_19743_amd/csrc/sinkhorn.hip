@@ -212,22 +212,30 @@ template <bool POS, class F> __device__ __forceinline__ void pvisit(const Pieces
     }
 }
 
-// v from the lane D positions away (lane ^ D).
-template <int D> __device__ __forceinline__ double xor_lane(double v)
+// v from the partner lane of butterfly step K. Steps 0 and 1 pair lane i with
+// i ^ 1 and i ^ 2 (quad_perm); from step 2 on, all lanes of an aligned block
+// of 2^K lanes already hold the same value, so any lane of the neighbouring
+// block will do: step 2 uses row_half_mirror (i -> 7 - i within 8), step 3
+// row_mirror (i -> 15 - i within 16), both DPP moves; steps 4 and 5 use lane
+// permutes across rows.
+template <int K> __device__ __forceinline__ double partner(double v)
 {
     int2 w = __builtin_bit_cast(int2, v);
-    if constexpr (D == 1) {
+    if constexpr (K == 0) {
         w.x = __builtin_amdgcn_update_dpp(0, w.x, 0xB1, 0xF, 0xF, true); // quad_perm [1,0,3,2]
         w.y = __builtin_amdgcn_update_dpp(0, w.y, 0xB1, 0xF, 0xF, true);
-    } else if constexpr (D == 2) {
+    } else if constexpr (K == 1) {
         w.x = __builtin_amdgcn_update_dpp(0, w.x, 0x4E, 0xF, 0xF, true); // quad_perm [2,3,0,1]
         w.y = __builtin_amdgcn_update_dpp(0, w.y, 0x4E, 0xF, 0xF, true);
-    } else if constexpr (D < 32) {
-        w.x = __builtin_amdgcn_ds_swizzle(w.x, 0x1F | (D << 10)); // bitmask mode: lane ^ D within 32
-        w.y = __builtin_amdgcn_ds_swizzle(w.y, 0x1F | (D << 10));
+    } else if constexpr (K == 2) {
+        w.x = __builtin_amdgcn_update_dpp(0, w.x, 0x141, 0xF, 0xF, true); // row_half_mirror
+        w.y = __builtin_amdgcn_update_dpp(0, w.y, 0x141, 0xF, 0xF, true);
+    } else if constexpr (K == 3) {
+        w.x = __builtin_amdgcn_update_dpp(0, w.x, 0x140, 0xF, 0xF, true); // row_mirror
+        w.y = __builtin_amdgcn_update_dpp(0, w.y, 0x140, 0xF, 0xF, true);
     } else {
-        w.x = __shfl_xor(w.x, D);
-        w.y = __shfl_xor(w.y, D);
+        w.x = __shfl_xor(w.x, 1 << K);
+        w.y = __shfl_xor(w.y, 1 << K);
     }
     return __builtin_bit_cast(double, w);
 }
@@ -235,15 +243,16 @@ template <int D> __device__ __forceinline__ double xor_lane(double v)
 template <int K> __device__ __forceinline__ void bfly_step(double &acc, int lg, int lgmax)
 {
     if (K < lgmax) { // wave-uniform
-        const double y = xor_lane<(1 << K)>(acc);
+        const double y = partner<K>(acc);
         if (K < lg)
             acc += y;
     }
 }
 
 // Adds the partial sums of each aligned group of 2^lg lanes (lg from info);
-// every lane of a group ends with the same bits. Groups are sorted by size,
-// so the wave's first lane has the largest.
+// every lane of a group ends with the same bits (each step adds two values
+// that are the same on both sides, and addition commutes). Groups are sorted
+// by size, so the wave's first lane has the largest.
 __device__ __forceinline__ double group_reduce(double acc, uint32_t info)
 {
     const int lg = (int)((info >> 11) & 7u);
