@@ -112,6 +112,9 @@ def parse():
     ap.add_argument("--cpu-baseline", choices=["on", "off"], default="on")
     ap.add_argument("--cpu-repeats", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--memory-sweep", action="store_true",
+                    help="only measure peak library memory and time of one forward+backward at B=1, "
+                         "N=M in 1k..64k (shape-completion generator), one JSON line per size")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (5 times), to scale HBM byte counters")
     return ap.parse_args()
@@ -130,6 +133,58 @@ def copy_calibration(mib: int):
     print(json.dumps({"copy_calibration_bytes": n * 4, "launches": 5}), flush=True)
 
 
+def memory_sweep():
+    """Peak device memory held by the library (plan + scratch) and time of one
+    forward+backward at B = 1 as N = M grows; a least-squares line in N + M
+    gives the bytes per point."""
+    import numpy as np
+    import torch
+
+    import paper_2512_19743_amd as apml
+    from workloads import custom
+
+    apml.load()
+    sizes = [1024, 2048, 4096, 8192, 16384, 32768, 65536]
+    pts, peaks = [], []
+    for n in sizes:
+        X, Y = custom(n, 1, n, n, reference="primitives", prediction="perm_noise", sigma=0.05)
+        x = torch.from_numpy(X).cuda()
+        y = torch.from_numpy(Y).cuda()
+        gl = torch.ones(1, device="cuda")
+        prm = apml.apml_params_default(n_iter=10)
+
+        def step():
+            loss, plan = apml.apml_forward(x, y, prm)
+            apml.apml_backward(plan, x, y, gl)
+            nnz = int(plan.nnz().sum())
+            plan.close()
+            return nnz
+
+        step()
+        torch.cuda.synchronize()
+        apml.apml_reset_peak_memory()
+        times = []
+        for _ in range(3):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            loss, plan = apml.apml_forward(x, y, prm)
+            apml.apml_backward(plan, x, y, gl)
+            e1.record()
+            torch.cuda.synchronize()
+            nnz = int(plan.nnz().sum())
+            plan.close()
+            times.append(e0.elapsed_time(e1))
+        peak = apml.apml_get_memory_stats()["peak_in_use"]
+        pts.append(2 * n)
+        peaks.append(peak)
+        print(json.dumps({"N": n, "M": n, "B": 1, "nnz": nnz, "peak_library_mb": peak / 1e6,
+                          "bytes_per_point": peak / (2 * n), "ms_fwd_bwd": statistics.median(times)}), flush=True)
+    A = np.vstack([np.asarray(pts, float), np.ones(len(pts))]).T
+    slope, icpt = np.linalg.lstsq(A, np.asarray(peaks, float), rcond=None)[0]
+    print(json.dumps({"fit": "peak_bytes = a * (N + M) + b", "a_bytes_per_point": slope, "b_bytes": icpt}), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -141,6 +196,9 @@ def main():
 
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
+        return
+    if args.memory_sweep:
+        memory_sweep()
         return
 
     import numpy as np
