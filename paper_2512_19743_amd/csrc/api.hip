@@ -505,8 +505,9 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     for (int b = 0; b < B; ++b)
         plan->max_sample = std::max<int64_t>(plan->max_sample, offsets[b + 1] - offsets[b]);
     dv.nnz = nnz;
-    plan->sink_fwd = sinkhorn_fwd_fits(N, M, pieces, B);
-    plan->sink_bwd = plan->sink_fwd && sinkhorn_bwd_fits(N, M, pieces, B, plan->max_sample);
+    const int slots = sinkhorn_slots(N, M, pieces, B);
+    plan->sink_fwd = slots > 0;
+    plan->sink_bwd = sinkhorn_bwd_fits(slots, plan->max_sample);
 
     // ---- sparse structure -------------------------------------------------
     dv.csr_col = keep.get<int32_t>(nnz);
@@ -553,8 +554,9 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     dv.dvec = keep.get<double>(BN);
     dv.evec = keep.get<double>(BM);
     if (plan->sink_fwd) {
-        const size_t w = packed_order_words(B);
+        const size_t w = packed_order_words(B, slots);
         for (PackedOrder *pk : {&dv.pk_row, &dv.pk_col}) {
+            pk->slots = slots;
             pk->p0 = keep.get<float>(w);
             pk->gi = keep.get<uint32_t>(w / 2);
             pk->info = keep.get<uint32_t>(w / kSinkPiece);

@@ -85,9 +85,10 @@ void launch_emit_write(const EmitArgs &a, hipStream_t s);
 // aligned to its size. Position p belongs to lane p % kSinkLanes, slot
 // p / kSinkLanes. Arrays are plane-major so that the lanes of a wave read
 // consecutive words: word w of lane l, slot s, sample b sits at
-// ((b * kSinkSlots + s) * words + w) * kSinkLanes + l.
+// ((b * slots + s) * words + w) * kSinkLanes + l, where slots (1..kSinkMaxSlots)
+// is the smallest count that holds the batch's largest sample.
 constexpr int kSinkLanes = 1024; // threads of a per-sample Sinkhorn workgroup
-constexpr int kSinkSlots = 5;    // positions per lane and order
+constexpr int kSinkMaxSlots = 6; // most positions per lane and order (the layout of a plan uses 1..6)
 constexpr int kSinkPiece = 4;    // pairs per piece
 constexpr int kSinkOwners = 2048; // rows or columns a workgroup covers
 constexpr int kSinkMaxGroup = 64; // largest group (pieces of one owner)
@@ -98,6 +99,7 @@ struct PackedOrder {
     uint32_t *info; // [B][slots][lanes]: owner | log2(group) << 11 | head << 14 | valid << 15 | first position << 16 (rows)
     uint32_t *pos;  // [B][slots][kSinkPiece/2][lanes]: row-major positions within the sample (columns only)
     int32_t *n_pos; // [B]: positions used
+    int slots;      // positions per lane of this layout
 };
 
 // Device view of a plan, passed by value to the sparse kernels.
@@ -170,9 +172,11 @@ void launch_offsets(const int32_t *cnt, int S, const int32_t *col_cnt, const Cou
 // Whether the per-sample kernels take a batch: counts are the host copy of the
 // piece counts of the read-back block, max_pairs the largest sample's stored
 // pairs.
-bool sinkhorn_fwd_fits(int N, int M, const int32_t *counts, int B);
-bool sinkhorn_bwd_fits(int N, int M, const int32_t *counts, int B, int64_t max_pairs);
-size_t packed_order_words(int B); // 32-bit words of one PackedOrder's p0 array
+// Positions per lane the per-sample kernels need for a batch (1..kSinkMaxSlots),
+// 0 when it does not fit them.
+int sinkhorn_slots(int N, int M, const int32_t *counts, int B);
+bool sinkhorn_bwd_fits(int slots, int64_t max_pairs);
+size_t packed_order_words(int B, int slots); // 32-bit words of one PackedOrder's p0 array
 // Lays out the pieces of both orders; place: [B][2][2048] int32 scratch.
 void launch_pack(const DevPlan &d, int32_t *place, hipStream_t s);
 hipError_t launch_sinkhorn_fwd(const DevPlan &d, double eps, hipStream_t s);

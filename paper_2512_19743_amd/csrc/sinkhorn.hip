@@ -39,19 +39,17 @@ namespace apml {
 namespace {
 
 constexpr int kT = kSinkLanes;
-constexpr int kSLP = kSinkSlots;
 constexpr int kP = kSinkPiece;
 constexpr int kSL = kSinkOwners / kSinkLanes; // owners per lane in the owner phase
-constexpr int kCap = kT * kSLP;               // positions per sample and order
 
 __device__ __forceinline__ int pieces_of(int len) { return sink_pieces(len); }
 __device__ __forceinline__ int log2_group(int np) { return sink_log2_group(np); }
 
 // Word w of position p in a plane-major packed array with `words` words per
 // position.
-__device__ __forceinline__ size_t pk_index(int b, int p, int w, int words)
+__device__ __forceinline__ size_t pk_index(int b, int p, int w, int words, int slots)
 {
-    return (((size_t)b * kSLP + p / kT) * words + w) * kT + p % kT;
+    return (((size_t)b * slots + p / kT) * words + w) * kT + p % kT;
 }
 
 // Placement of the pieces of one order (blockIdx.y: 0 rows, 1 columns) of
@@ -59,7 +57,7 @@ __device__ __forceinline__ size_t pk_index(int b, int p, int w, int words)
 // (first | log2(group) << 16 in place[]), the info word of every position is
 // written, and the P0 / index / position words are cleared (k_pack_pairs
 // fills in the real pairs). The host has checked that the positions fit
-// (kCap) and that no owner has more than kSinkMaxGroup pieces.
+// (slots * kT) and that no owner has more than kSinkMaxGroup pieces.
 __global__ __launch_bounds__(kT) void k_place(DevPlan d, int32_t *place)
 {
     __shared__ int hist[8], base[8];
@@ -68,10 +66,11 @@ __global__ __launch_bounds__(kT) void k_place(DevPlan d, int32_t *place)
     const int n_own = rows ? d.N : d.M;
     const int32_t *ptr = rows ? d.row_ptr + (size_t)b * d.N : d.col_ptr + (size_t)b * d.M;
     const PackedOrder pk = rows ? d.pk_row : d.pk_col;
+    const int slots = pk.slots, cap = slots * kT;
     const int lo = d.row_ptr[(size_t)b * d.N];
     // clear this sample's words (contiguous blocks of the plane-major arrays)
     {
-        const size_t np0 = (size_t)kSLP * kP * kT, ngi = np0 / 2;
+        const size_t np0 = (size_t)slots * kP * kT, ngi = np0 / 2;
         for (size_t k = tid; k < np0; k += kT)
             pk.p0[(size_t)b * np0 + k] = 0.0f;
         for (size_t k = tid; k < ngi; k += kT) {
@@ -106,8 +105,8 @@ __global__ __launch_bounds__(kT) void k_place(DevPlan d, int32_t *place)
         pk.n_pos[b] = run;
     }
     __syncthreads();
-    for (int p = base[7] + tid; p < kCap; p += kT) // unused positions: invalid
-        pk.info[pk_index(b, p, 0, 1)] = 0u;
+    for (int p = base[7] + tid; p < cap; p += kT) // unused positions: invalid
+        pk.info[pk_index(b, p, 0, 1, slots)] = 0u;
 #pragma unroll
     for (int s = 0; s < kSL; ++s) {
         if (lg[s] < 0)
@@ -119,7 +118,7 @@ __global__ __launch_bounds__(kT) void k_place(DevPlan d, int32_t *place)
             uint32_t info = (uint32_t)k | ((uint32_t)lg[s] << 11) | ((q == 0 ? 1u : 0u) << 14) | 0x8000u;
             if (rows && q * kP < len[s])
                 info |= ((uint32_t)(st[s] + q * kP - lo) & 0xFFFFu) << 16;
-            pk.info[pk_index(b, first + q, 0, 1)] = info;
+            pk.info[pk_index(b, first + q, 0, 1, slots)] = info;
         }
     }
 }
@@ -141,13 +140,14 @@ __global__ __launch_bounds__(kBlock) void k_pack_pairs(DevPlan d, const int32_t 
     const int q = off / kP, e = off % kP;
     const int p = (place[((size_t)b * 2 + (rows ? 0 : 1)) * kSinkOwners + k] & 0xFFFF) + q;
     const PackedOrder &pk = rows ? d.pk_row : d.pk_col;
-    pk.p0[pk_index(b, p, e, kP)] = rows ? d.p0r[t] : d.p0c[t];
+    const int slots = pk.slots;
+    pk.p0[pk_index(b, p, e, kP, slots)] = rows ? d.p0r[t] : d.p0c[t];
     const int other = rows ? d.csr_col[t] : d.csc_row[t];
-    uint16_t *gi = reinterpret_cast<uint16_t *>(pk.gi + pk_index(b, p, e / 2, kP / 2));
-    gi[e & 1] = (uint16_t)((other & 0x7FFF) | 0x8000);
+    uint16_t *gi = reinterpret_cast<uint16_t *>(pk.gi + pk_index(b, p, e / 2, kP / 2, slots));
+    gi[e & 1] = (uint16_t)(other << 3); // byte offset of an 8-byte entry
     if (!rows) {
         const int lo = d.row_ptr[(size_t)b * d.N];
-        uint16_t *ps = reinterpret_cast<uint16_t *>(pk.pos + pk_index(b, p, e / 2, kP / 2));
+        uint16_t *ps = reinterpret_cast<uint16_t *>(pk.pos + pk_index(b, p, e / 2, kP / 2, slots));
         ps[e & 1] = (uint16_t)((d.csc_perm[t] - lo) & 0xFFFF);
     }
 }
@@ -157,59 +157,95 @@ __global__ __launch_bounds__(kBlock) void k_pack_pairs(DevPlan d, const int32_t 
 // ---------------------------------------------------------------------------
 
 // A lane's positions of one order, in registers for the whole kernel.
-template <bool POS> struct Pieces {
-    float p0[kSLP][kP];
-    uint32_t gi[kSLP][kP / 2];
-    uint32_t pos[POS ? kSLP : 1][POS ? kP / 2 : 1];
-    uint32_t info[kSLP];
+template <bool POS, int SLP> struct Pieces {
+    float p0[SLP][kP];
+    uint32_t gi[SLP][kP / 2];
+    uint32_t pos[POS ? SLP : 1][POS ? kP / 2 : 1];
+    uint32_t info[SLP];
     int n; // positions used (wave-uniform)
 };
 
-template <bool POS> __device__ void load_pieces(Pieces<POS> &pc, const PackedOrder &pk, int b)
+template <bool POS, int SLP> __device__ void load_pieces(Pieces<POS, SLP> &pc, const PackedOrder &pk, int b)
 {
     const int tid = threadIdx.x;
 #pragma unroll
-    for (int s = 0; s < kSLP; ++s) {
+    for (int s = 0; s < SLP; ++s) {
         const int p = s * kT + tid;
 #pragma unroll
         for (int e = 0; e < kP; ++e)
-            pc.p0[s][e] = pk.p0[pk_index(b, p, e, kP)];
+            pc.p0[s][e] = pk.p0[pk_index(b, p, e, kP, SLP)];
 #pragma unroll
         for (int w = 0; w < kP / 2; ++w) {
-            pc.gi[s][w] = pk.gi[pk_index(b, p, w, kP / 2)];
+            pc.gi[s][w] = pk.gi[pk_index(b, p, w, kP / 2, SLP)];
             if (POS)
-                pc.pos[s][w] = pk.pos[pk_index(b, p, w, kP / 2)];
+                pc.pos[s][w] = pk.pos[pk_index(b, p, w, kP / 2, SLP)];
         }
-        pc.info[s] = pk.info[pk_index(b, p, 0, 1)];
+        pc.info[s] = pk.info[pk_index(b, p, 0, 1, SLP)];
     }
     pc.n = __builtin_amdgcn_readfirstlane(pk.n_pos[b]);
 }
 
-// A copy of v that the compiler cannot see through: keeps values derived from
-// the cached words (widened P0, unpacked indices) from being hoisted out of
-// the sweep loop, which would multiply the registers held.
-template <typename V> __device__ __forceinline__ V opaque(V v)
+// Unpacking of the cached words. Each 16-bit half of a gi word holds the byte
+// offset of the gathered 8-byte value, each half of a pos word a row-major
+// position; an info word is owner (bits 0-10) | log2 group (11-13) | head (14)
+// | valid (15) | first row-major position of a row piece (16-31). Bit fields
+// are extracted at a base offset the compiler cannot see through (Unpack,
+// renewed every sweep), so the unpacked values and the masks derived from
+// them are recomputed inside the sweep loop instead of being hoisted out of
+// it, which would multiply the registers held; P0 is widened to double by an
+// instruction of its own for the same reason. The loads of a slot are issued
+// before any of its arithmetic. Padding pairs carry P0 = 0 and offset or
+// position 0: they gather and read real data, add nothing and write nothing.
+struct Unpack {
+    uint32_t lo; // 0
+
+    __device__ __forceinline__ static Unpack make()
+    {
+        Unpack u{0u};
+        asm volatile("" : "+s"(u.lo));
+        return u;
+    }
+    __device__ __forceinline__ uint32_t bits(uint32_t w, uint32_t pos, uint32_t width) const
+    {
+        return __builtin_amdgcn_ubfe(w, lo + pos, width);
+    }
+    __device__ __forceinline__ uint32_t half(uint32_t w, int e) const { return bits(w, (e & 1) ? 16u : 0u, 16u); }
+    __device__ __forceinline__ int owner(uint32_t info) const { return (int)bits(info, 0, 11); }
+    __device__ __forceinline__ int run(uint32_t info) const { return (int)bits(info, 16, 16); }
+};
+
+__device__ __forceinline__ double widen(float f)
 {
-    asm volatile("" : "+v"(v));
-    return v;
+    double d;
+    asm volatile("v_cvt_f64_f32 %0, %1" : "=v"(d) : "v"(f));
+    return d;
 }
 
-__device__ __forceinline__ int half16(uint32_t w, int e) { return (int)((w >> (16 * (e & 1))) & 0xFFFFu); }
+template <typename T> __device__ __forceinline__ T lds_at(const void *base, uint32_t byte_off)
+{
+    return *reinterpret_cast<const T *>(reinterpret_cast<const char *>(base) + byte_off);
+}
 
 // Slot s of this wave holds at least one used position.
-template <bool POS> __device__ __forceinline__ bool wave_active(const Pieces<POS> &pc, int s)
+template <bool POS, int SLP> __device__ __forceinline__ bool wave_active(const Pieces<POS, SLP> &pc, int s)
 {
     return s * kT + (int)(threadIdx.x & ~63u) < pc.n;
 }
 
-// Visits the kP pairs of slot s: f(e, gathered, p0, real).
-template <bool POS, class F> __device__ __forceinline__ void pvisit(const Pieces<POS> &pc, int s, F f)
+// Sum over the pairs of slot s of P0 times the gathered value (doubles at
+// vals + byte offset), in pair order.
+template <bool POS, int SLP>
+__device__ __forceinline__ double slot_dot(const Pieces<POS, SLP> &pc, int s, const double *vals, const Unpack &u)
 {
+    double g[kP];
 #pragma unroll
-    for (int e = 0; e < kP; ++e) {
-        const int h = half16(opaque(pc.gi[s][e / 2]), e);
-        f(e, h & 0x7FFF, opaque(pc.p0[s][e]), (h & 0x8000) != 0);
-    }
+    for (int e = 0; e < kP; ++e)
+        g[e] = lds_at<double>(vals, u.half(pc.gi[s][e / 2], e));
+    double acc = widen(pc.p0[s][0]) * g[0];
+#pragma unroll
+    for (int e = 1; e < kP; ++e)
+        acc = __builtin_fma(widen(pc.p0[s][e]), g[e], acc);
+    return acc;
 }
 
 // v from the partner lane of butterfly step K. Steps 0 and 1 pair lane i with
@@ -253,9 +289,9 @@ template <int K> __device__ __forceinline__ void bfly_step(double &acc, int lg, 
 // every lane of a group ends with the same bits (each step adds two values
 // that are the same on both sides, and addition commutes). Groups are sorted
 // by size, so the wave's first lane has the largest.
-__device__ __forceinline__ double group_reduce(double acc, uint32_t info)
+__device__ __forceinline__ double group_reduce(double acc, uint32_t info, const Unpack &u)
 {
-    const int lg = (int)((info >> 11) & 7u);
+    const int lg = (int)u.bits(info, 11, 3);
     const int lgmax = __builtin_amdgcn_readfirstlane(lg);
     bfly_step<0>(acc, lg, lgmax);
     bfly_step<1>(acc, lg, lgmax);
@@ -267,16 +303,17 @@ __device__ __forceinline__ double group_reduce(double acc, uint32_t info)
 }
 
 // Stores a group's sum at its owner (first lane of the group).
-__device__ __forceinline__ void store_sum(double acc, uint32_t info, double *sums)
+__device__ __forceinline__ void store_sum(double acc, uint32_t info, double *sums, const Unpack &u)
 {
-    if ((info & 0xC000u) == 0xC000u) // valid and head
-        sums[info & 0x7FFu] = acc;
+    if (u.bits(info, 14, 2) == 3u) // head and valid
+        sums[u.owner(info)] = acc;
 }
 
 constexpr size_t fwd_lds_bytes() { return 8 * 3 * (size_t)kSinkOwners; }
 constexpr size_t bwd_fixed_lds_bytes() { return (8 + 8 + 4 + 4) * (size_t)kSinkOwners; }
+constexpr int kAdjPad = kP; // adjoint entries after a sample's pairs
 
-__global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
+template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
 {
     extern __shared__ double lds[];
     double *va = lds, *vb = va + kSinkOwners, *sums = vb + kSinkOwners;
@@ -284,7 +321,7 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
     const int lo = d.row_ptr[(size_t)b * N], hi = d.row_ptr[(size_t)(b + 1) * N];
-    Pieces<false> pr, pc;
+    Pieces<false, SLP> pr, pc;
     load_pieces(pr, d.pk_row, b);
     load_pieces(pc, d.pk_col, b);
     double am[kSL], bm[kSL]; // the lane's own scalings
@@ -305,13 +342,13 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
     lds_barrier();
 
     for (int l = 1; l <= L; ++l) {
+        const Unpack u = Unpack::make();
         // column scaling (Eq. 3): beta_j /= beta_j sum_i alpha_i P0_ij + eps
 #pragma unroll
-        for (int s = 0; s < kSLP; ++s)
+        for (int s = 0; s < SLP; ++s)
             if (wave_active(pc, s)) {
-                double acc = 0.0;
-                pvisit(pc, s, [&](int, int i, float p0, bool) { acc += (double)p0 * va[i]; });
-                store_sum(group_reduce(acc, pc.info[s]), pc.info[s], sums);
+                const double acc = slot_dot(pc, s, va, u);
+                store_sum(group_reduce(acc, pc.info[s], u), pc.info[s], sums, u);
             }
         lds_barrier();
 #pragma unroll
@@ -330,11 +367,10 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
         lds_barrier();
         // row scaling (Eq. 4): alpha_i /= alpha_i sum_j P0_ij beta_j + eps
 #pragma unroll
-        for (int s = 0; s < kSLP; ++s)
+        for (int s = 0; s < SLP; ++s)
             if (wave_active(pr, s)) {
-                double acc = 0.0;
-                pvisit(pr, s, [&](int, int j, float p0, bool) { acc += (double)p0 * vb[j]; });
-                store_sum(group_reduce(acc, pr.info[s]), pr.info[s], sums);
+                const double acc = slot_dot(pr, s, vb, u);
+                store_sum(group_reduce(acc, pr.info[s], u), pr.info[s], sums, u);
             }
         lds_barrier();
 #pragma unroll
@@ -401,7 +437,7 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
 // and the row sum d_i / alpha^l_i (column sum e_j / beta^l_j) is just the sum
 // of z' P0 over the row's (column's) pairs. X, Y and the reciprocals are kept
 // in single precision, the adjoint and all sums in double.
-__global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
+template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
 {
     extern __shared__ double lds[];
     double *sums = lds;
@@ -412,14 +448,16 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
     const int lo = d.row_ptr[(size_t)b * N], hi = d.row_ptr[(size_t)(b + 1) * N];
-    Pieces<false> pr;
-    Pieces<true> pc;
+    Pieces<false, SLP> pr;
+    Pieces<true, SLP> pc;
     load_pieces(pr, d.pk_row, b);
     load_pieces(pc, d.pk_col, b);
     const double gl = d.grad_loss[b];
     const double *alpha_L = d.alpha + L * BN;
     for (int t = lo + tid; t < hi; t += kT)
         adj[t - lo] = gl * d.cost[t] * alpha_L[d.csr_row[t]];
+    if (tid < kAdjPad) // read (never written) by padding pairs of the sample's last pieces
+        adj[hi - lo + tid] = 0.0;
     double a_own[kSL], b_own[kSL];
 #pragma unroll
     for (int s = 0; s < kSL; ++s) {
@@ -436,78 +474,96 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
     lds_barrier();
 
     for (int l = L; l >= 1; --l) {
-        // saved values of this iteration, loaded ahead of their use
-        double rden[kSL], a_prev[kSL], sden[kSL], b_prev[kSL];
+        // scalings of the previous iteration for the row owners, loaded ahead
+        // of their use (those of the column owners after the row owners)
+        double a_prev[kSL], b_prev[kSL];
 #pragma unroll
         for (int s = 0; s < kSL; ++s) {
             const int k = kSL * tid + s;
-            rden[s] = k < N ? d.rden[(l - 1) * BN + (size_t)b * N + k] : 1.0;
             a_prev[s] = k < N ? d.alpha[(l - 1) * BN + (size_t)b * N + k] : 1.0;
-            sden[s] = k < M ? d.sden[(l - 1) * BM + (size_t)b * M + k] : 1.0;
-            b_prev[s] = k < M ? d.beta[(l - 1) * BM + (size_t)b * M + k] : 1.0;
         }
         // row phase
+        const Unpack u = Unpack::make();
 #pragma unroll
-        for (int s = 0; s < kSLP; ++s)
+        for (int s = 0; s < SLP; ++s)
             if (wave_active(pr, s)) {
-                const int run = (int)(pr.info[s] >> 16);
-                const double inv = (double)inv_a[pr.info[s] & 0x7FFu];
+                const int run = u.run(pr.info[s]);
+                const double inv = (double)inv_a[u.owner(pr.info[s])];
                 double m[kP];
-                pvisit(pr, s, [&](int e, int, float, bool real) { m[e] = real ? adj[run + e] : 0.0; });
+                float2 w[kP];
+#pragma unroll
+                for (int e = 0; e < kP; ++e) {
+                    m[e] = adj[run + e];
+                    w[e] = lds_at<float2>(xy, u.half(pr.gi[s][e / 2], e));
+                }
                 double acc = 0.0;
-                pvisit(pr, s, [&](int e, int j, float p0, bool real) {
-                    const float2 w = xy[j];
-                    const double z = (m[e] * inv) * (double)w.x - (double)w.y;
-                    if (real)
+#pragma unroll
+                for (int e = 0; e < kP; ++e) {
+                    const double z = __builtin_fma(m[e] * inv, (double)w[e].x, -(double)w[e].y);
+                    const double p0 = widen(pr.p0[s][e]);
+                    if (p0 != 0.0)
                         adj[run + e] = z;
-                    acc += z * (double)p0;
-                });
-                store_sum(group_reduce(acc, pr.info[s]), pr.info[s], sums);
+                    acc = e == 0 ? z * p0 : __builtin_fma(z, p0, acc);
+                }
+                store_sum(group_reduce(acc, pr.info[s], u), pr.info[s], sums, u);
             }
         lds_barrier();
-        // row owners (adjoint of Eq. 4): d_i = alpha^l_i * sum
+        // row owners (adjoint of Eq. 4): d_i = alpha^l_i * sum; the pending
+        // factor alpha^(l-1)_i / (R_i + eps) is alpha^l_i itself
 #pragma unroll
         for (int s = 0; s < kSL; ++s) {
             const int i = kSL * tid + s;
-            const double dsum = a_own[s] * sums[min(i, N - 1)];
-            const double r = 1.0 / rden[s];
+            const double al = a_own[s];
+            const double dsum = al * sums[min(i, N - 1)];
             if (i < N) {
-                xy[i] = make_float2((float)(r * a_prev[s]), (float)(dsum * r * a_prev[s]));
+                xy[i] = make_float2((float)al, (float)(dsum * al));
                 inv_a[i] = (float)(1.0 / a_prev[s]);
             }
+            a_own[s] = a_prev[s];
+        }
+#pragma unroll
+        for (int s = 0; s < kSL; ++s) {
+            const int k = kSL * tid + s;
+            b_prev[s] = k < M ? d.beta[(l - 1) * BM + (size_t)b * M + k] : 1.0;
         }
         lds_barrier();
         // column phase
 #pragma unroll
-        for (int s = 0; s < kSLP; ++s)
+        for (int s = 0; s < SLP; ++s)
             if (wave_active(pc, s)) {
-                const double inv = (double)inv_b[pc.info[s] & 0x7FFu];
+                const double inv = (double)inv_b[u.owner(pc.info[s])];
+                uint32_t ps[kP];
                 double m[kP];
-                pvisit(pc, s, [&](int e, int, float, bool real) {
-                    m[e] = real ? adj[half16(opaque(pc.pos[s][e / 2]), e)] : 0.0;
-                });
+                float2 w[kP];
+#pragma unroll
+                for (int e = 0; e < kP; ++e) {
+                    ps[e] = u.half(pc.pos[s][e / 2], e);
+                    m[e] = adj[ps[e]];
+                    w[e] = lds_at<float2>(xy, u.half(pc.gi[s][e / 2], e));
+                }
                 double acc = 0.0;
-                pvisit(pc, s, [&](int e, int i, float p0, bool real) {
-                    const float2 w = xy[i];
-                    const double z = (m[e] * inv) * (double)w.x - (double)w.y;
-                    if (real)
-                        adj[half16(opaque(pc.pos[s][e / 2]), e)] = z;
-                    acc += z * (double)p0;
-                });
-                store_sum(group_reduce(acc, pc.info[s]), pc.info[s], sums);
+#pragma unroll
+                for (int e = 0; e < kP; ++e) {
+                    const double z = __builtin_fma(m[e] * inv, (double)w[e].x, -(double)w[e].y);
+                    const double p0 = widen(pc.p0[s][e]);
+                    if (p0 != 0.0)
+                        adj[ps[e]] = z;
+                    acc = e == 0 ? z * p0 : __builtin_fma(z, p0, acc);
+                }
+                store_sum(group_reduce(acc, pc.info[s], u), pc.info[s], sums, u);
             }
         lds_barrier();
-        // column owners (adjoint of Eq. 3): e_j = beta^l_j * sum
+        // column owners (adjoint of Eq. 3): e_j = beta^l_j * sum; the pending
+        // factor beta^(l-1)_j / (S_j + eps) is beta^l_j
 #pragma unroll
         for (int s = 0; s < kSL; ++s) {
             const int j = kSL * tid + s;
-            const double esum = b_own[s] * sums[min(j, M - 1)];
-            const double r = 1.0 / sden[s];
+            const double bl = b_own[s];
+            const double esum = bl * sums[min(j, M - 1)];
             if (j < M) {
-                xy[j] = make_float2((float)(r * b_prev[s]), (float)(esum * r * b_prev[s]));
+                xy[j] = make_float2((float)bl, (float)(esum * bl));
                 inv_b[j] = (float)(1.0 / b_prev[s]);
             }
-            a_own[s] = a_prev[s];
             b_own[s] = b_prev[s];
         }
         lds_barrier();
@@ -642,27 +698,29 @@ __global__ __launch_bounds__(kBlock) void k_bwd_sink_col(DevPlan d, int l)
 
 } // namespace
 
-bool sinkhorn_fwd_fits(int N, int M, const int32_t *counts, int B)
+int sinkhorn_slots(int N, int M, const int32_t *counts, int B)
 {
     if (N > kSinkOwners || M > kSinkOwners)
-        return false;
-    for (int b = 0; b < B; ++b)
-        if (counts[4 * b] > kCap || counts[4 * b + 1] > kCap || counts[4 * b + 2] > kSinkMaxGroup ||
-            counts[4 * b + 3] > kSinkMaxGroup)
-            return false;
-    return true;
+        return 0;
+    int most = 1;
+    for (int b = 0; b < B; ++b) {
+        if (counts[4 * b + 2] > kSinkMaxGroup || counts[4 * b + 3] > kSinkMaxGroup)
+            return 0;
+        most = std::max({most, counts[4 * b], counts[4 * b + 1]});
+    }
+    const int slots = (most + kT - 1) / kT;
+    return slots <= kSinkMaxSlots ? slots : 0;
 }
 
 constexpr size_t kLdsBudget = 160 * 1024;
 
-bool sinkhorn_bwd_fits(int N, int M, const int32_t *counts, int B, int64_t max_pairs)
+bool sinkhorn_bwd_fits(int slots, int64_t max_pairs)
 {
     // the adjoint of every pair of a sample in LDS; positions are 16-bit
-    return sinkhorn_fwd_fits(N, M, counts, B) && max_pairs <= 65536 &&
-           bwd_fixed_lds_bytes() + 8 * (size_t)max_pairs <= kLdsBudget;
+    return slots > 0 && max_pairs <= 65536 && bwd_fixed_lds_bytes() + 8 * (size_t)(max_pairs + kAdjPad) <= kLdsBudget;
 }
 
-size_t packed_order_words(int B) { return (size_t)B * kSLP * kP * kT; }
+size_t packed_order_words(int B, int slots) { return (size_t)B * slots * kP * kT; }
 
 void launch_pack(const DevPlan &d, int32_t *place, hipStream_t s)
 {
@@ -670,25 +728,40 @@ void launch_pack(const DevPlan &d, int32_t *place, hipStream_t s)
     hipLaunchKernelGGL(k_pack_pairs, dim3(blocks_for(2 * d.nnz, kBlock)), dim3(kBlock), 0, s, d, (const int32_t *)place);
 }
 
+// The kernel instance for the plan's slot count.
+template <template <int> class K> static auto for_slots(int slots) -> decltype(K<1>::fn)
+{
+    switch (slots) {
+    case 1: return K<1>::fn;
+    case 2: return K<2>::fn;
+    case 3: return K<3>::fn;
+    case 4: return K<4>::fn;
+    case 5: return K<5>::fn;
+    default: return K<6>::fn;
+    }
+}
+template <int S> struct FwdK { static constexpr auto fn = k_sinkhorn_fwd<S>; };
+template <int S> struct BwdK { static constexpr auto fn = k_sinkhorn_bwd<S>; };
+
 hipError_t launch_sinkhorn_fwd(const DevPlan &d, double eps, hipStream_t s)
 {
     const size_t bytes = fwd_lds_bytes();
-    hipError_t e = hipFuncSetAttribute((const void *)k_sinkhorn_fwd,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    const auto k = for_slots<FwdK>(d.pk_row.slots);
+    hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(k_sinkhorn_fwd, dim3(d.B), dim3(kT), bytes, s, d, eps);
+    hipLaunchKernelGGL(k, dim3(d.B), dim3(kT), bytes, s, d, eps);
     return hipGetLastError();
 }
 
 hipError_t launch_sinkhorn_bwd(const DevPlan &d, int64_t max_pairs, hipStream_t s)
 {
-    const size_t bytes = bwd_fixed_lds_bytes() + 8 * (size_t)max_pairs;
-    hipError_t e = hipFuncSetAttribute((const void *)k_sinkhorn_bwd,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    const size_t bytes = bwd_fixed_lds_bytes() + 8 * (size_t)(max_pairs + kAdjPad);
+    const auto k = for_slots<BwdK>(d.pk_row.slots);
+    hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(k_sinkhorn_bwd, dim3(d.B), dim3(kT), bytes, s, d);
+    hipLaunchKernelGGL(k, dim3(d.B), dim3(kT), bytes, s, d);
     return hipGetLastError();
 }
 
