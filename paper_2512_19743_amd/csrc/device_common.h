@@ -90,6 +90,30 @@ template <bool LDS_ONLY> __device__ __forceinline__ void wg_barrier()
         __syncthreads();
 }
 
+// Finds, among the pairs of one segment, the first position whose
+// single-precision squared distance equals m1 and the first other position
+// whose distance equals m2 (the second order statistic): the minimum and the
+// second minimum with ties to the smaller index.
+template <int G> struct Argmins {
+    int f1 = INT_MAX, g1 = INT_MAX, g2 = INT_MAX;
+    __device__ void see(int t, float s, float2 m)
+    {
+        if (s == m.x && f1 == INT_MAX)
+            f1 = t;
+        if (s == m.y) {
+            if (g1 == INT_MAX)
+                g1 = t;
+            else if (g2 == INT_MAX)
+                g2 = t;
+        }
+    }
+    __device__ void resolve(int *q1, int *q2) const
+    {
+        *q1 = group_min<G>(f1);
+        *q2 = group_min<G>(g1 != *q1 ? g1 : g2);
+    }
+};
+
 inline unsigned blocks_for(int64_t n, int per_block) { return (unsigned)((n + per_block - 1) / per_block); }
 
 } // namespace apml

@@ -234,17 +234,42 @@ template <bool POS, int SLP> __device__ __forceinline__ bool wave_active(const P
 
 // Sum over the pairs of slot s of P0 times the gathered value (doubles at
 // vals + byte offset), in pair order.
-template <bool POS, int SLP>
-__device__ __forceinline__ double slot_dot(const Pieces<POS, SLP> &pc, int s, const double *vals, const Unpack &u)
+// P0 of slot s in double: widened once per kernel when the registers allow
+// (WIDE), else widened at each use.
+template <bool POS, int SLP, bool WIDE> struct P0Cache {
+    double v[WIDE ? SLP : 1][WIDE ? kP : 1];
+
+    __device__ __forceinline__ void init(const Pieces<POS, SLP> &pc)
+    {
+        if constexpr (WIDE) {
+#pragma unroll
+            for (int s = 0; s < SLP; ++s)
+#pragma unroll
+                for (int e = 0; e < kP; ++e)
+                    v[s][e] = (double)pc.p0[s][e];
+        }
+    }
+    __device__ __forceinline__ double get(const Pieces<POS, SLP> &pc, int s, int e) const
+    {
+        if constexpr (WIDE)
+            return v[s][e];
+        else
+            return widen(pc.p0[s][e]);
+    }
+};
+
+template <bool POS, int SLP, bool WIDE>
+__device__ __forceinline__ double slot_dot(const Pieces<POS, SLP> &pc, const P0Cache<POS, SLP, WIDE> &p0, int s,
+                                           const double *vals, const Unpack &u)
 {
     double g[kP];
 #pragma unroll
     for (int e = 0; e < kP; ++e)
         g[e] = lds_at<double>(vals, u.half(pc.gi[s][e / 2], e));
-    double acc = widen(pc.p0[s][0]) * g[0];
+    double acc = p0.get(pc, s, 0) * g[0];
 #pragma unroll
     for (int e = 1; e < kP; ++e)
-        acc = __builtin_fma(widen(pc.p0[s][e]), g[e], acc);
+        acc = __builtin_fma(p0.get(pc, s, e), g[e], acc);
     return acc;
 }
 
@@ -309,14 +334,28 @@ __device__ __forceinline__ void store_sum(double acc, uint32_t info, double *sum
         sums[u.owner(info)] = acc;
 }
 
-constexpr size_t fwd_lds_bytes() { return 8 * 3 * (size_t)kSinkOwners; }
 constexpr size_t bwd_fixed_lds_bytes() { return (8 + 8 + 4 + 4) * (size_t)kSinkOwners; }
 constexpr int kAdjPad = kP; // adjoint entries after a sample's pairs
 
+// a / b for positive normal a, b: the hardware reciprocal refined by two
+// Newton steps, then one correction of the quotient (within an ulp of the
+// correctly rounded quotient; no scaling for denormals or overflow).
+__device__ __forceinline__ double quotient(double a, double b)
+{
+    double r = __builtin_amdgcn_rcp(b);
+    r = __builtin_fma(r, __builtin_fma(-b, r, 1.0), r);
+    r = __builtin_fma(r, __builtin_fma(-b, r, 1.0), r);
+    const double q = a * r;
+    return __builtin_fma(r, __builtin_fma(-b, q, a), q);
+}
+
+// Up to this many slots the forward kernel keeps P0 in double in registers.
+constexpr int kFwdWideSlots = 4;
+
 template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
 {
-    extern __shared__ double lds[];
-    double *va = lds, *vb = va + kSinkOwners, *sums = vb + kSinkOwners;
+    // static arrays: their addresses are constants folded into the LDS instructions
+    __shared__ double va[kSinkOwners], vb[kSinkOwners], sums[kSinkOwners];
     const int b = blockIdx.x, tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
@@ -324,6 +363,10 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan 
     Pieces<false, SLP> pr, pc;
     load_pieces(pr, d.pk_row, b);
     load_pieces(pc, d.pk_col, b);
+    constexpr bool kWide = SLP <= kFwdWideSlots;
+    P0Cache<false, SLP, kWide> prw, pcw;
+    prw.init(pr);
+    pcw.init(pc);
     double am[kSL], bm[kSL]; // the lane's own scalings
 #pragma unroll
     for (int s = 0; s < kSL; ++s) {
@@ -347,7 +390,7 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan 
 #pragma unroll
         for (int s = 0; s < SLP; ++s)
             if (wave_active(pc, s)) {
-                const double acc = slot_dot(pc, s, va, u);
+                const double acc = slot_dot(pc, pcw, s, va, u);
                 store_sum(group_reduce(acc, pc.info[s], u), pc.info[s], sums, u);
             }
         lds_barrier();
@@ -356,7 +399,7 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan 
             const int j = kSL * tid + s;
             const double S = sums[min(j, M - 1)];
             const double den = bm[s] * S + eps;
-            const double v = bm[s] / den;
+            const double v = quotient(bm[s], den);
             if (j < M) {
                 bm[s] = v;
                 vb[j] = v;
@@ -369,7 +412,7 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan 
 #pragma unroll
         for (int s = 0; s < SLP; ++s)
             if (wave_active(pr, s)) {
-                const double acc = slot_dot(pr, s, vb, u);
+                const double acc = slot_dot(pr, prw, s, vb, u);
                 store_sum(group_reduce(acc, pr.info[s], u), pr.info[s], sums, u);
             }
         lds_barrier();
@@ -378,7 +421,7 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan 
             const int i = kSL * tid + s;
             const double R = sums[min(i, N - 1)];
             const double den = am[s] * R + eps;
-            const double v = am[s] / den;
+            const double v = quotient(am[s], den);
             if (i < N) {
                 am[s] = v;
                 va[i] = v;
@@ -439,11 +482,11 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan 
 // in single precision, the adjoint and all sums in double.
 template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
 {
-    extern __shared__ double lds[];
-    double *sums = lds;
-    float2 *xy = reinterpret_cast<float2 *>(sums + kSinkOwners); // one side at a time
-    float *inv_a = reinterpret_cast<float *>(xy + kSinkOwners), *inv_b = inv_a + kSinkOwners;
-    double *adj = reinterpret_cast<double *>(inv_b + kSinkOwners);
+    // fixed arrays static (constant addresses), the adjoints dynamic
+    __shared__ double sums[kSinkOwners];
+    __shared__ float2 xy[kSinkOwners]; // one side at a time
+    __shared__ float inv_a[kSinkOwners], inv_b[kSinkOwners];
+    extern __shared__ double adj[];
     const int b = blockIdx.x, tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
@@ -517,7 +560,7 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan 
             const double dsum = al * sums[min(i, N - 1)];
             if (i < N) {
                 xy[i] = make_float2((float)al, (float)(dsum * al));
-                inv_a[i] = (float)(1.0 / a_prev[s]);
+                inv_a[i] = __builtin_amdgcn_rcpf((float)a_prev[s]);
             }
             a_own[s] = a_prev[s];
         }
@@ -562,7 +605,7 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan 
             const double esum = bl * sums[min(j, M - 1)];
             if (j < M) {
                 xy[j] = make_float2((float)bl, (float)(esum * bl));
-                inv_b[j] = (float)(1.0 / b_prev[s]);
+                inv_b[j] = __builtin_amdgcn_rcpf((float)b_prev[s]);
             }
             b_own[s] = b_prev[s];
         }
@@ -745,18 +788,14 @@ template <int S> struct BwdK { static constexpr auto fn = k_sinkhorn_bwd<S>; };
 
 hipError_t launch_sinkhorn_fwd(const DevPlan &d, double eps, hipStream_t s)
 {
-    const size_t bytes = fwd_lds_bytes();
     const auto k = for_slots<FwdK>(d.pk_row.slots);
-    hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-    if (e != hipSuccess)
-        return e;
-    hipLaunchKernelGGL(k, dim3(d.B), dim3(kT), bytes, s, d, eps);
+    hipLaunchKernelGGL(k, dim3(d.B), dim3(kT), 0, s, d, eps);
     return hipGetLastError();
 }
 
 hipError_t launch_sinkhorn_bwd(const DevPlan &d, int64_t max_pairs, hipStream_t s)
 {
-    const size_t bytes = bwd_fixed_lds_bytes() + 8 * (size_t)(max_pairs + kAdjPad);
+    const size_t bytes = 8 * (size_t)(max_pairs + kAdjPad); // beyond the static arrays
     const auto k = for_slots<BwdK>(d.pk_row.slots);
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess)

@@ -26,30 +26,6 @@ namespace {
 
 constexpr int G = kGroup;
 
-// Finds, among the pairs of one segment, the first position whose
-// single-precision squared distance equals m1 and the first other position
-// whose distance equals m2 (the second order statistic): the minimum and the
-// second minimum with ties to the smaller index.
-struct Argmins {
-    int f1 = INT_MAX, g1 = INT_MAX, g2 = INT_MAX;
-    __device__ void see(int t, float s, float2 m)
-    {
-        if (s == m.x && f1 == INT_MAX)
-            f1 = t;
-        if (s == m.y) {
-            if (g1 == INT_MAX)
-                g1 = t;
-            else if (g2 == INT_MAX)
-                g2 = t;
-        }
-    }
-    __device__ void resolve(int *q1, int *q2) const
-    {
-        *q1 = group_min<G>(f1);
-        *q2 = group_min<G>(g1 != *q1 ? g1 : g2);
-    }
-};
-
 __global__ __launch_bounds__(kBlock) void k_row_softmax(DevPlan d, Params p)
 {
     const int gid = blockIdx.x * kBlock + threadIdx.x;
@@ -62,7 +38,7 @@ __global__ __launch_bounds__(kBlock) void k_row_softmax(DevPlan d, Params p)
     const float *yb = d.y + (size_t)b * d.M * 3;
     const float2 m = d.m12_row[r];
     const int t0 = d.row_ptr[r], t1 = d.row_ptr[r + 1];
-    Argmins am;
+    Argmins<G> am;
     for (int t = t0 + lg; t < t1; t += G) {
         const float *yj = yb + 3 * (size_t)d.csr_col[t];
         am.see(t, sqdist_f32(x0, x1, x2, yj[0], yj[1], yj[2]), m);
@@ -135,7 +111,7 @@ __global__ __launch_bounds__(kBlock) void k_col_softmax(DevPlan d, Params p)
     const float2 m = d.m12_col[gc];
     const int s0 = d.col_ptr[gc], s1 = d.col_ptr[gc + 1];
     const bool cached = s1 - s0 <= G * kColCache; // the same for the whole group
-    Argmins am;
+    Argmins<G> am;
     int tq[kColCache];
     double cq[kColCache];
     if (cached) {
