@@ -408,8 +408,9 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     kp.n_iter = L;
 
     const int BN = B * N, BM = B * M;
-    Arena tmp;
+    Arena tmp, dense_tmp; // dense_tmp: scratch of the dense scans, released once the CSR is written
     tmp.stream = s;
+    dense_tmp.stream = s;
     Arena &keep = plan->keep;
     DevPlan &dv = plan->dv;
     dv.B = B;
@@ -436,19 +437,19 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     choose_chunks(B, M, N, &cols.S, &cols.chunk);
     cols.owner_blocks = ceil_div(M, kBlock);
     cols.tiles = B * cols.S * cols.owner_blocks;
-    rows.partial = tmp.get<float2>((size_t)rows.S * BN);
-    cols.partial = tmp.get<float2>((size_t)cols.S * BM);
+    rows.partial = dense_tmp.get<float2>((size_t)rows.S * BN);
+    cols.partial = dense_tmp.get<float2>((size_t)cols.S * BM);
     dv.m12_row = keep.get<float2>(BN);
     dv.m12_col = keep.get<float2>(BM);
-    float *E_row = tmp.get<float>(BN);
-    float4 *ypack = tmp.get<float4>(BM);
+    float *E_row = dense_tmp.get<float>(BN);
+    float4 *ypack = dense_tmp.get<float4>(BM);
     dv.ctr = keep.get<Counters>(1);
     BuildArgs ba{};
     int32_t *col_cnt = tmp.get<int32_t>(BM); // stored pairs per column, counted by the emission
     ba.col_fill = tmp.get<int32_t>(BM);
     dv.row_ptr = keep.get<int32_t>((size_t)BN + 1);
     dv.col_ptr = keep.get<int32_t>((size_t)BM + 1);
-    if (tmp.failed || keep.failed)
+    if (tmp.failed || dense_tmp.failed || keep.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (statistics)");
 
     {
@@ -472,11 +473,20 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     ea.M = M;
     ea.owner_blocks = rows.owner_blocks;
     choose_chunks(B, N, M, &ea.S, &ea.chunk, 256);
-    ea.cnt = tmp.get<int32_t>((size_t)BN * ea.S);
+    ea.cnt = dense_tmp.get<int32_t>((size_t)BN * ea.S);
     ea.col_cnt = col_cnt; // cleared by the finalize kernel
+    ea.ctr = dv.ctr;
+    // the counting pass keeps the first hits of every (row, chunk); offsets
+    // within a chunk are 16-bit
+    if (ea.chunk <= 65536) {
+        ea.stage = dense_tmp.get<uint16_t>((size_t)BN * ea.S * kStage);
+        const size_t tiles = (size_t)B * ea.S * ea.owner_blocks;
+        ea.spill = dense_tmp.get<uint32_t>(tiles * kTileSpill);
+        ea.spill_n = dense_tmp.get<int32_t>(tiles);
+    }
     Readback *rb_dev = (Readback *)tmp.get<uint8_t>(readback_bytes(B));
     std::vector<uint8_t> rb_host(readback_bytes(B));
-    if (tmp.failed)
+    if (tmp.failed || dense_tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (support)");
     Readback *rb = (Readback *)rb_host.data();
     const int64_t *totals = readback_totals(rb);
@@ -530,11 +540,15 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         ea.row_ptr = dv.row_ptr;
         ea.csr_col = dv.csr_col;
         ea.csr_row = dv.csr_row;
-        launch_emit_write(ea, s);
+        if (ea.stage)
+            launch_emit_compact(ea, rb->ctr.overflow != 0, s);
+        else
+            launch_emit_write(ea, s);
         launch_csc_build(dv, ba, s);
         HIP_TRY(hipGetLastError());
         pt.stop();
     }
+    dense_tmp.release();
 
     // ---- temperatures, softmaxes, P0 ---------------------------------------
     dv.T_row = keep.get<double>(BN);

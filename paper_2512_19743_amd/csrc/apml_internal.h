@@ -15,7 +15,8 @@ constexpr int kGroup = 4;         // lanes per row / column in the sparse kernel
 
 // Device-side counters of one forward call.
 struct Counters {
-    unsigned int error; // bit 0: a row's minima not found among its pairs; bit 1: a column's
+    unsigned int error;    // bit 0: a row's minima not found among its pairs; bit 1: a column's
+    unsigned int overflow; // a (row, chunk) of the support scan had more hits than its staging slots
 };
 
 struct Params {
@@ -57,6 +58,13 @@ void launch_top2(const ScanDir &rows, const ScanDir &cols, int B, hipStream_t s)
 void launch_finalize(const FinalizeDir &rows, const FinalizeDir &cols, int B, const Params &p,
                      Counters *ctr, hipStream_t s);
 
+// The counting pass of the support scan keeps the first kStage hits of every
+// (row, chunk) and the further hits of a tile (kBlock rows, one chunk) in a
+// tile list of kTileSpill entries; only when a tile list overflows does the
+// writing pass scan that tile again.
+constexpr int kStage = 16;
+constexpr int kTileSpill = 512;
+
 struct EmitArgs {
     const float *x;      // [B, N, 3]
     const float4 *ypack; // [B, M]: y and its column threshold
@@ -64,7 +72,11 @@ struct EmitArgs {
     int B, N, M, S, chunk, owner_blocks;
     int32_t *cnt;        // [B*N][S] stored pairs per (row, column chunk)
     int32_t *col_cnt;    // [B*M] stored pairs per column
-    // second pass
+    uint16_t *stage;     // [B*N][S][kStage] column offsets within the chunk of the first hits, or NULL
+    uint32_t *spill;     // [tiles][kTileSpill]: further hits, row within the tile << 16 | offset in the chunk
+    int32_t *spill_n;    // [tiles]: entries of the tile list (more than kTileSpill: overflowed)
+    Counters *ctr;
+    // second pass (or compaction of the staged hits)
     const int32_t *row_ptr; // [B*N+1]
     int32_t *csr_col, *csr_row;
 };
@@ -72,6 +84,10 @@ struct EmitArgs {
 // (after the offsets are known) writes it into the CSR arrays.
 void launch_emit_count(const EmitArgs &a, hipStream_t s);
 void launch_emit_write(const EmitArgs &a, hipStream_t s);
+// Writes the CSR from the staged hits of every tile whose list did not
+// overflow; with overflow set, the writing pass then rescans only the tiles
+// whose list overflowed.
+void launch_emit_compact(const EmitArgs &a, bool overflow, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // sparse structure
@@ -157,7 +173,6 @@ __device__ __forceinline__ int sink_log2_group(int np) { return np <= 1 ? 0 : 32
 // rows, by the columns, most pieces of a row, of a column).
 struct Readback {
     Counters ctr;
-    unsigned int pad;
 };
 inline size_t readback_bytes(int B) { return sizeof(Readback) + 16 * (size_t)B + 4 * (5 * (size_t)B + 1); }
 __host__ __device__ inline int64_t *readback_totals(Readback *r) { return reinterpret_cast<int64_t *>(r + 1); }

@@ -80,7 +80,7 @@ __global__ __launch_bounds__(kBlock) void k_finalize(FinalizeArgs args)
 {
     int k = blockIdx.x * kBlock + threadIdx.x;
     if (k == 0)
-        *args.ctr = Counters{0};
+        *args.ctr = Counters{0, 0};
     const int which = k < args.rows ? 0 : 1;
     if (which)
         k -= args.rows;
@@ -178,6 +178,7 @@ __device__ __forceinline__ void for_each_hit(float ax, float ay, float az, float
 // same decisions.
 template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs a)
 {
+    __shared__ int n_spill;
     const int t = blockIdx.x;
     const int ob = t % a.owner_blocks;
     const int rest = t / a.owner_blocks;
@@ -195,14 +196,38 @@ template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs 
     const uint32_t keep = valid ? ~0u : 0u; // a lane without a row ignores the columns' balls too
     if (!WRITE) {
         int32_t *col_cnt = a.col_cnt + (size_t)b * a.M;
+        uint16_t *stage = a.stage ? a.stage + ((size_t)row * a.S + ch) * kStage : nullptr;
+        uint32_t *spill = a.stage ? a.spill + (size_t)t * kTileSpill : nullptr;
+        if (threadIdx.x == 0)
+            n_spill = 0;
+        __syncthreads();
         int cnt = 0;
         for_each_hit(ax, ay, az, E, q, j0, j1, keep, [&](int j) {
             atomicAdd(&col_cnt[j], 1);
+            if (stage) {
+                if (cnt < kStage) {
+                    stage[cnt] = (uint16_t)(j - j0);
+                } else { // in increasing j for each row
+                    const int k = atomicAdd(&n_spill, 1);
+                    if (k < kTileSpill)
+                        spill[k] = (uint32_t)threadIdx.x << 16 | (uint32_t)(j - j0);
+                }
+            }
             ++cnt;
         });
         if (valid)
             a.cnt[(size_t)row * a.S + ch] = cnt;
+        if (stage) {
+            __syncthreads();
+            if (threadIdx.x == 0) {
+                a.spill_n[t] = n_spill;
+                if (n_spill > kTileSpill)
+                    atomicOr(&a.ctr->overflow, 1u);
+            }
+        }
     } else {
+        if (a.stage && a.spill_n[t] <= kTileSpill) // rescan only the tiles whose list overflowed
+            return;
         int pos = a.row_ptr[row];
         for (int c = 0; c < ch; ++c)
             pos += a.cnt[(size_t)row * a.S + c];
@@ -211,6 +236,45 @@ template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs 
             a.csr_row[pos] = row;
             ++pos;
         });
+    }
+}
+
+// CSR from the staged hits: one thread per (row, chunk) writes its hits at
+// the row's offset plus the hits of the row's earlier chunks; hits beyond
+// kStage come from the tile list, in list order (increasing column).
+__global__ __launch_bounds__(kBlock) void k_emit_compact(EmitArgs a)
+{
+    const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (g >= (int64_t)a.B * a.N * a.S)
+        return;
+    const int row = (int)(g / a.S), ch = (int)(g % a.S);
+    const int b = row / a.N, i = row - b * a.N;
+    const int t = (b * a.S + ch) * a.owner_blocks + i / kBlock; // the tile of the counting pass
+    const int32_t *cnt = a.cnt + (size_t)row * a.S;
+    int pos = a.row_ptr[row];
+    for (int c = 0; c < ch; ++c)
+        pos += cnt[c];
+    const int n = cnt[ch];
+    const int n_spill = a.spill_n[t];
+    if (n_spill > kTileSpill) // the writing pass rescans this tile
+        return;
+    const uint16_t *st = a.stage + (size_t)g * kStage;
+    const int j0 = ch * a.chunk;
+    const int ns = min(n, kStage);
+    for (int k = 0; k < ns; ++k) {
+        a.csr_col[pos + k] = j0 + st[k];
+        a.csr_row[pos + k] = row;
+    }
+    if (n > kStage) {
+        const uint32_t *sp = a.spill + (size_t)t * kTileSpill;
+        const uint32_t me = (uint32_t)(i % kBlock);
+        int k = kStage;
+        for (int u = 0; u < n_spill; ++u)
+            if (sp[u] >> 16 == me) {
+                a.csr_col[pos + k] = j0 + (int)(sp[u] & 0xFFFFu);
+                a.csr_row[pos + k] = row;
+                ++k;
+            }
     }
 }
 
@@ -238,6 +302,13 @@ void launch_emit_count(const EmitArgs &a, hipStream_t s)
 void launch_emit_write(const EmitArgs &a, hipStream_t s)
 {
     hipLaunchKernelGGL(k_emit<true>, dim3(a.B * a.S * a.owner_blocks), dim3(kBlock), 0, s, a);
+}
+
+void launch_emit_compact(const EmitArgs &a, bool overflow, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_emit_compact, dim3(blocks_for((int64_t)a.B * a.N * a.S, kBlock)), dim3(kBlock), 0, s, a);
+    if (overflow)
+        hipLaunchKernelGGL(k_emit<true>, dim3(a.B * a.S * a.owner_blocks), dim3(kBlock), 0, s, a);
 }
 
 } // namespace apml
