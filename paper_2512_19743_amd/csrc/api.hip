@@ -540,11 +540,20 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         ea.row_ptr = dv.row_ptr;
         ea.csr_col = dv.csr_col;
         ea.csr_row = dv.csr_row;
+        ea.col_ptr = dv.col_ptr;
+        ea.col_fill = ba.col_fill;
+        ea.tmp_row = ba.tmp_row;
+        ea.tmp_src = ba.tmp_src;
+        ea.csc_col = dv.csc_col;
+        const bool placed = ea.stage && !rb->ctr.overflow;
         if (ea.stage)
             launch_emit_compact(ea, rb->ctr.overflow != 0, s);
         else
             launch_emit_write(ea, s);
-        launch_csc_build(dv, ba, s);
+        if (placed)
+            launch_csc_sort(dv, ba, s);
+        else
+            launch_csc_build(dv, ba, s);
         HIP_TRY(hipGetLastError());
         pt.stop();
     }

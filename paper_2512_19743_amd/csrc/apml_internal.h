@@ -79,6 +79,10 @@ struct EmitArgs {
     // second pass (or compaction of the staged hits)
     const int32_t *row_ptr; // [B*N+1]
     int32_t *csr_col, *csr_row;
+    // column-major placement done by the compaction (when no tile is rescanned)
+    const int32_t *col_ptr; // [B*M+1]
+    int32_t *col_fill;      // [B*M], zero
+    int32_t *tmp_row, *tmp_src, *csc_col;
 };
 // Pass 1 counts the candidate support per (row, chunk) and per column; pass 2
 // (after the offsets are known) writes it into the CSR arrays.
@@ -154,6 +158,9 @@ struct BuildArgs {
 };
 
 void launch_csc_build(const DevPlan &d, const BuildArgs &a, hipStream_t s);
+// With the column slots taken by the compaction, only the canonical order of
+// each column remains.
+void launch_csc_sort(const DevPlan &d, const BuildArgs &a, hipStream_t s);
 
 void launch_softmax(const DevPlan &d, const Params &p, hipStream_t s);
 void launch_bwd_softmax(const DevPlan &d, const Params &p, hipStream_t s);

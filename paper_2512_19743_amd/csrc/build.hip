@@ -192,6 +192,11 @@ void launch_csc_build(const DevPlan &d, const BuildArgs &a, hipStream_t s)
     hipLaunchKernelGGL(k_csc_sort, dim3(g), dim3(kBlock), 0, s, d, a);
 }
 
+void launch_csc_sort(const DevPlan &d, const BuildArgs &a, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_csc_sort, dim3(blocks_for(d.nnz, kBlock)), dim3(kBlock), 0, s, d, a);
+}
+
 void launch_count_support(const int32_t *row_ptr, const uint8_t *flags, int B, int N,
                           unsigned long long *out, hipStream_t s)
 {

@@ -241,8 +241,23 @@ template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs 
 
 // CSR from the staged hits: one thread per (row, chunk) writes its hits at
 // the row's offset plus the hits of the row's earlier chunks; hits beyond
-// kStage come from the tile list, in list order (increasing column).
-__global__ __launch_bounds__(kBlock) void k_emit_compact(EmitArgs a)
+// kStage come from the tile list, in list order (increasing column). With
+// PLACE, each pair also takes a slot in its column segment (k_csc_sort then
+// fixes the order inside the segment).
+template <bool PLACE>
+__device__ __forceinline__ void emit_pair(const EmitArgs &a, int pos, int row, int i, int gc, int j)
+{
+    a.csr_col[pos] = j;
+    a.csr_row[pos] = row;
+    if (PLACE) {
+        const int p = a.col_ptr[gc] + atomicAdd(&a.col_fill[gc], 1);
+        a.tmp_row[p] = i;
+        a.tmp_src[p] = pos;
+        a.csc_col[p] = gc;
+    }
+}
+
+template <bool PLACE> __global__ __launch_bounds__(kBlock) void k_emit_compact(EmitArgs a)
 {
     const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (g >= (int64_t)a.B * a.N * a.S)
@@ -259,20 +274,20 @@ __global__ __launch_bounds__(kBlock) void k_emit_compact(EmitArgs a)
     if (n_spill > kTileSpill) // the writing pass rescans this tile
         return;
     const uint16_t *st = a.stage + (size_t)g * kStage;
-    const int j0 = ch * a.chunk;
+    const int j0 = ch * a.chunk, gc0 = b * a.M + j0;
     const int ns = min(n, kStage);
-    for (int k = 0; k < ns; ++k) {
-        a.csr_col[pos + k] = j0 + st[k];
-        a.csr_row[pos + k] = row;
-    }
+#pragma unroll
+    for (int k = 0; k < kStage; ++k) // fixed trip count: the pairs' loads and atomics overlap
+        if (k < ns)
+            emit_pair<PLACE>(a, pos + k, row, i, gc0 + st[k], j0 + st[k]);
     if (n > kStage) {
         const uint32_t *sp = a.spill + (size_t)t * kTileSpill;
         const uint32_t me = (uint32_t)(i % kBlock);
         int k = kStage;
         for (int u = 0; u < n_spill; ++u)
             if (sp[u] >> 16 == me) {
-                a.csr_col[pos + k] = j0 + (int)(sp[u] & 0xFFFFu);
-                a.csr_row[pos + k] = row;
+                const int jj = (int)(sp[u] & 0xFFFFu);
+                emit_pair<PLACE>(a, pos + k, row, i, gc0 + jj, j0 + jj);
                 ++k;
             }
     }
@@ -306,7 +321,11 @@ void launch_emit_write(const EmitArgs &a, hipStream_t s)
 
 void launch_emit_compact(const EmitArgs &a, bool overflow, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_emit_compact, dim3(blocks_for((int64_t)a.B * a.N * a.S, kBlock)), dim3(kBlock), 0, s, a);
+    const dim3 g(blocks_for((int64_t)a.B * a.N * a.S, kBlock));
+    if (overflow) // the rescanned tiles are placed by k_csc_fill afterwards
+        hipLaunchKernelGGL(k_emit_compact<false>, g, dim3(kBlock), 0, s, a);
+    else
+        hipLaunchKernelGGL(k_emit_compact<true>, g, dim3(kBlock), 0, s, a);
     if (overflow)
         hipLaunchKernelGGL(k_emit<true>, dim3(a.B * a.S * a.owner_blocks), dim3(kBlock), 0, s, a);
 }
