@@ -545,15 +545,21 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         ea.tmp_row = ba.tmp_row;
         ea.tmp_src = ba.tmp_src;
         ea.csc_col = dv.csc_col;
-        const bool placed = ea.stage && !rb->ctr.overflow;
+        // column-major view: per sample in LDS when it fits, else slots taken
+        // by global counters (in the compaction when no tile is rescanned)
+        const bool csc_lds = csc_sample_fits(N, M, plan->max_sample);
+        const bool placed = !csc_lds && ea.stage && !rb->ctr.overflow;
         if (ea.stage)
-            launch_emit_compact(ea, rb->ctr.overflow != 0, s);
+            launch_emit_compact(ea, rb->ctr.overflow != 0, placed, s);
         else
             launch_emit_write(ea, s);
-        if (placed)
+        if (csc_lds) {
+            HIP_TRY(launch_csc_sample(dv, plan->max_sample, s));
+        } else if (placed) {
             launch_csc_sort(dv, ba, s);
-        else
+        } else {
             launch_csc_build(dv, ba, s);
+        }
         HIP_TRY(hipGetLastError());
         pt.stop();
     }

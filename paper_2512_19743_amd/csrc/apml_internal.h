@@ -91,7 +91,7 @@ void launch_emit_write(const EmitArgs &a, hipStream_t s);
 // Writes the CSR from the staged hits of every tile whose list did not
 // overflow; with overflow set, the writing pass then rescans only the tiles
 // whose list overflowed.
-void launch_emit_compact(const EmitArgs &a, bool overflow, hipStream_t s);
+void launch_emit_compact(const EmitArgs &a, bool overflow, bool place, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // sparse structure
@@ -161,6 +161,10 @@ void launch_csc_build(const DevPlan &d, const BuildArgs &a, hipStream_t s);
 // With the column slots taken by the compaction, only the canonical order of
 // each column remains.
 void launch_csc_sort(const DevPlan &d, const BuildArgs &a, hipStream_t s);
+// The column-major view of each sample in one workgroup (LDS counters), when
+// the sample's column offsets and pairs fit in LDS.
+bool csc_sample_fits(int N, int M, int64_t max_pairs);
+hipError_t launch_csc_sample(const DevPlan &d, int64_t max_pairs, hipStream_t s);
 
 void launch_softmax(const DevPlan &d, const Params &p, hipStream_t s);
 void launch_bwd_softmax(const DevPlan &d, const Params &p, hipStream_t s);

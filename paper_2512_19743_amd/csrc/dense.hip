@@ -319,10 +319,10 @@ void launch_emit_write(const EmitArgs &a, hipStream_t s)
     hipLaunchKernelGGL(k_emit<true>, dim3(a.B * a.S * a.owner_blocks), dim3(kBlock), 0, s, a);
 }
 
-void launch_emit_compact(const EmitArgs &a, bool overflow, hipStream_t s)
+void launch_emit_compact(const EmitArgs &a, bool overflow, bool place, hipStream_t s)
 {
     const dim3 g(blocks_for((int64_t)a.B * a.N * a.S, kBlock));
-    if (overflow) // the rescanned tiles are placed by k_csc_fill afterwards
+    if (overflow || !place) // the rescanned tiles are placed by k_csc_fill afterwards
         hipLaunchKernelGGL(k_emit_compact<false>, g, dim3(kBlock), 0, s, a);
     else
         hipLaunchKernelGGL(k_emit_compact<true>, g, dim3(kBlock), 0, s, a);
