@@ -26,197 +26,203 @@ namespace {
 
 constexpr int G = kGroup;
 
-__global__ __launch_bounds__(kBlock) void k_row_softmax(DevPlan d, Params p)
+// The forward softmax of one owner (a row, or a column) by its group of G
+// lanes. Lane lg sees pairs k = lg, lg + G, ... of the owner's segment; the
+// first kSmCache of them are loaded up front (index, the other point's
+// coordinates and, for columns, P_row and the flags of the pair) and their
+// distances and similarities kept in registers, so the segment is read once.
+// Longer segments read the rest again in each step.
+constexpr int kSmCache = 8;
+
+__device__ __forceinline__ double dist3(float ax, float ay, float az, float bx, float by, float bz)
 {
-    const int gid = blockIdx.x * kBlock + threadIdx.x;
-    const int r = gid / G, lg = gid % G;
-    if (r >= d.B * d.N)
-        return;
-    const int b = r / d.N;
-    const float *xr = d.x + (size_t)r * 3;
-    const float x0 = xr[0], x1 = xr[1], x2 = xr[2];
-    const float *yb = d.y + (size_t)b * d.M * 3;
-    const float2 m = d.m12_row[r];
-    const int t0 = d.row_ptr[r], t1 = d.row_ptr[r + 1];
+    const double dx = (double)ax - (double)bx;
+    const double dy = (double)ay - (double)by;
+    const double dz = (double)az - (double)bz;
+    return sqrt(dx * dx + dy * dy + dz * dz);
+}
+
+// ROWS: owner r = b*N + i over row-major pairs t (the other index is the
+// column j); else owner gc = b*M + j over column-major entries q (the other
+// index is the row i, the row-major position t = csc_perm[q]).
+template <bool ROWS> __device__ __forceinline__ void owner_softmax(const DevPlan &d, const Params &p, int o, int lg)
+{
+    const int n_own = ROWS ? d.N : d.M, n_oth = ROWS ? d.M : d.N;
+    const int b = o / n_own;
+    const float *own = (ROWS ? d.x : d.y) + (size_t)o * 3;
+    const float *oth = (ROWS ? d.y : d.x) + (size_t)b * n_oth * 3;
+    const int32_t *ptr = ROWS ? d.row_ptr : d.col_ptr;
+    const int32_t *idx = ROWS ? d.csr_col : d.csc_row;
+    const int s0 = ptr[o], n = ptr[o + 1] - s0;
+    const float a0 = own[0], a1 = own[1], a2 = own[2];
+    const float2 m = ROWS ? d.m12_row[o] : d.m12_col[o];
+    const double lk = ROWS ? p.lk_row : p.lk_col;
+
+    int oi[kSmCache], tt[kSmCache];
+    float ox[kSmCache], oy[kSmCache], oz[kSmCache], prow[kSmCache];
+    uint8_t fl[kSmCache];
+#pragma unroll
+    for (int c = 0; c < kSmCache; ++c) {
+        const int k = lg + G * c;
+        oi[c] = k < n ? idx[s0 + k] : 0;
+        tt[c] = ROWS ? s0 + k : (k < n ? d.csc_perm[s0 + k] : 0);
+    }
+#pragma unroll
+    for (int c = 0; c < kSmCache; ++c) {
+        const int k = lg + G * c;
+        const float *q = oth + 3 * (size_t)oi[c];
+        ox[c] = q[0];
+        oy[c] = q[1];
+        oz[c] = q[2];
+        if (!ROWS) {
+            prow[c] = k < n ? d.p_row[tt[c]] : 0.0f;
+            fl[c] = k < n ? d.flags[tt[c]] : 0;
+        }
+    }
+    auto other = [&](int k, float &x, float &y, float &z) {
+        const float *q = oth + 3 * (size_t)idx[s0 + k];
+        x = q[0];
+        y = q[1];
+        z = q[2];
+    };
+
+    // minimum and second minimum among the stored pairs (single precision)
     Argmins<G> am;
-    for (int t = t0 + lg; t < t1; t += G) {
-        const float *yj = yb + 3 * (size_t)d.csr_col[t];
-        am.see(t, sqdist_f32(x0, x1, x2, yj[0], yj[1], yj[2]), m);
+#pragma unroll
+    for (int c = 0; c < kSmCache; ++c)
+        if (lg + G * c < n)
+            am.see(s0 + lg + G * c, sqdist_f32(a0, a1, a2, ox[c], oy[c], oz[c]), m);
+    for (int k = lg + G * kSmCache; k < n; k += G) {
+        float x, y, z;
+        other(k, x, y, z);
+        am.see(s0 + k, sqdist_f32(a0, a1, a2, x, y, z), m);
     }
     int q1, q2;
     am.resolve(&q1, &q2);
     if (q1 == INT_MAX || q2 == INT_MAX) { // cannot happen: both minima are always emitted
         if (lg == 0) {
-            atomicOr(&d.ctr->error, 1u);
-            d.T_row[r] = 0.0;
-            d.C1_row[r] = 0.0;
-            d.g_row[r] = 1.0;
-            d.pos_row[2 * (size_t)r] = d.pos_row[2 * (size_t)r + 1] = -1;
-            d.clamp_row[r] = 1;
+            atomicOr(&d.ctr->error, ROWS ? 1u : 2u);
+            (ROWS ? d.T_row : d.T_col)[o] = 0.0;
+            (ROWS ? d.C1_row : d.C1_col)[o] = 0.0;
+            (ROWS ? d.g_row : d.g_col)[o] = 1.0;
+            (ROWS ? d.pos_row : d.pos_col)[2 * (size_t)o] = -1;
+            (ROWS ? d.pos_row : d.pos_col)[2 * (size_t)o + 1] = -1;
+            (ROWS ? d.clamp_row : d.clamp_col)[o] = 1;
         }
-        for (int t = t0 + lg; t < t1; t += G) {
-            d.cost[t] = 0.0;
-            d.p_row[t] = 0.0f;
-            d.flags[t] = 0;
+        for (int k = lg; k < n; k += G) {
+            if (ROWS) {
+                d.cost[s0 + k] = 0.0;
+                d.p_row[s0 + k] = 0.0f;
+                d.flags[s0 + k] = 0;
+            } else {
+                const int t = d.csc_perm[s0 + k];
+                d.p_col[s0 + k] = 0.0f;
+                d.p0c[s0 + k] = d.p0r[t] = 0.5f * d.p_row[t];
+            }
         }
         return;
     }
-    const double c1 = dist_f64(xr, yb + 3 * (size_t)d.csr_col[q1]);
-    const double c2 = dist_f64(xr, yb + 3 * (size_t)d.csr_col[q2]);
+    double dc[kSmCache];
+#pragma unroll
+    for (int c = 0; c < kSmCache; ++c) // only where the lane holds a pair: slots past the segment cost nothing
+        dc[c] = lg + G * c < n ? dist3(a0, a1, a2, ox[c], oy[c], oz[c]) : 0.0;
+    auto dist_at = [&](int q) { // distance of the pair at position q of the segment array
+        const int k = q - s0;
+        if (k < G * kSmCache) { // held by one lane of the group
+            double v = 0.0;
+#pragma unroll
+            for (int c = 0; c < kSmCache; ++c)
+                v += lg + G * c == k ? dc[c] : 0.0;
+            return group_sum<G>(v);
+        }
+        float x, y, z;
+        other(k, x, y, z);
+        return dist3(a0, a1, a2, x, y, z);
+    };
+    const double c1 = dist_at(q1), c2 = dist_at(q2);
     const double gap = (c2 - c1) + p.delta;
     const bool clamped = gap < p.eps_gap;
     const double g = clamped ? p.eps_gap : gap;
-    const double T = p.lk_row / g;
-    double z = 0.0;
-    for (int t = t0 + lg; t < t1; t += G) {
-        const double c = dist_f64(xr, yb + 3 * (size_t)d.csr_col[t]);
-        d.cost[t] = c;
-        const double s = exp(-T * (c - c1));
-        if (s >= p.tau)
-            z += s;
+    const double T = lk / g;
+
+    // kept similarities and their sum
+    double sv[kSmCache], zsum = 0.0;
+#pragma unroll
+    for (int c = 0; c < kSmCache; ++c) {
+        sv[c] = 0.0;
+        if (lg + G * c < n) {
+            const double s = exp(-T * (dc[c] - c1));
+            sv[c] = s;
+            if (s >= p.tau)
+                zsum += s;
+        }
     }
-    z = group_sum<G>(z);
-    for (int t = t0 + lg; t < t1; t += G) {
-        const double s = exp(-T * (d.cost[t] - c1));
+    for (int k = lg + G * kSmCache; k < n; k += G) {
+        float x, y, z;
+        other(k, x, y, z);
+        const double s = exp(-T * (dist3(a0, a1, a2, x, y, z) - c1));
+        if (s >= p.tau)
+            zsum += s;
+    }
+    zsum = group_sum<G>(zsum);
+
+    // P = s / Z on the kept pairs; rows store C, columns P0 = (P_row + P_col)/2
+    auto write = [&](int k, int t, double c, double s, float pr, uint8_t f) {
         const bool keep = s >= p.tau;
-        d.p_row[t] = keep ? (float)(s / z) : 0.0f;
-        d.flags[t] = keep ? 1 : 0;
+        const double pk = keep ? s / zsum : 0.0;
+        if (ROWS) {
+            d.cost[t] = c;
+            d.p_row[t] = (float)pk;
+            d.flags[t] = keep ? 1 : 0;
+        } else {
+            const int q = s0 + k;
+            d.flags[t] = (uint8_t)(f | (keep ? 2 : 0));
+            const float p0 = (float)(0.5 * ((double)pr + pk));
+            d.p_col[q] = (float)pk;
+            d.p0c[q] = p0;
+            d.p0r[t] = p0;
+        }
+    };
+#pragma unroll
+    for (int c = 0; c < kSmCache; ++c)
+        if (lg + G * c < n)
+            write(lg + G * c, tt[c], dc[c], sv[c], prow[c], fl[c]);
+    for (int k = lg + G * kSmCache; k < n; k += G) {
+        float x, y, z;
+        other(k, x, y, z);
+        const double c = dist3(a0, a1, a2, x, y, z);
+        const int t = ROWS ? s0 + k : d.csc_perm[s0 + k];
+        write(k, t, c, exp(-T * (c - c1)), ROWS ? 0.0f : d.p_row[t], ROWS ? 0 : d.flags[t]);
     }
     if (lg == 0) {
-        d.T_row[r] = T;
-        d.C1_row[r] = c1;
-        d.g_row[r] = g;
-        d.pos_row[2 * (size_t)r] = q1;
-        d.pos_row[2 * (size_t)r + 1] = q2;
-        d.clamp_row[r] = clamped;
+        (ROWS ? d.T_row : d.T_col)[o] = T;
+        (ROWS ? d.C1_row : d.C1_col)[o] = c1;
+        (ROWS ? d.g_row : d.g_col)[o] = g;
+        (ROWS ? d.pos_row : d.pos_col)[2 * (size_t)o] = q1;
+        (ROWS ? d.pos_row : d.pos_col)[2 * (size_t)o + 1] = q2;
+        (ROWS ? d.clamp_row : d.clamp_col)[o] = clamped;
     }
 }
 
-// Columns of at most G * kColCache pairs keep their pairs in registers (one
-// pass over the column's data instead of three); the cost of a pair is
-// recomputed from the coordinates, bitwise as the row kernel computed it,
-// instead of being gathered from the row-major array.
-constexpr int kColCache = 4;
+__global__ __launch_bounds__(kBlock) void k_row_softmax(DevPlan d, Params p)
+{
+    const int gid = blockIdx.x * kBlock + threadIdx.x;
+    const int r = gid / G;
+    if (r < d.B * d.N)
+        owner_softmax<true>(d, p, r, gid % G);
+}
 
 __global__ __launch_bounds__(kBlock) void k_col_softmax(DevPlan d, Params p)
 {
     const int gid = blockIdx.x * kBlock + threadIdx.x;
-    const int gc = gid / G, lg = gid % G;
-    if (gc >= d.B * d.M)
-        return;
-    const int b = gc / d.M;
-    const float *yc = d.y + (size_t)gc * 3;
-    const float y0 = yc[0], y1 = yc[1], y2 = yc[2];
-    const float *xb = d.x + (size_t)b * d.N * 3;
-    const float2 m = d.m12_col[gc];
-    const int s0 = d.col_ptr[gc], s1 = d.col_ptr[gc + 1];
-    const bool cached = s1 - s0 <= G * kColCache; // the same for the whole group
-    Argmins<G> am;
-    int tq[kColCache];
-    double cq[kColCache];
-    if (cached) {
-#pragma unroll
-        for (int k = 0; k < kColCache; ++k) {
-            const int q = s0 + lg + G * k;
-            tq[k] = -1;
-            cq[k] = 0.0;
-            if (q < s1) {
-                const float *xi = xb + 3 * (size_t)d.csc_row[q];
-                am.see(q, sqdist_f32(y0, y1, y2, xi[0], xi[1], xi[2]), m);
-                cq[k] = dist_f64(xi, yc);
-                tq[k] = d.csc_perm[q];
-            }
-        }
-    } else {
-        for (int q = s0 + lg; q < s1; q += G) {
-            const float *xi = xb + 3 * (size_t)d.csc_row[q];
-            am.see(q, sqdist_f32(y0, y1, y2, xi[0], xi[1], xi[2]), m);
-        }
-    }
-    int q1, q2;
-    am.resolve(&q1, &q2);
-    if (q1 == INT_MAX || q2 == INT_MAX) {
-        if (lg == 0) {
-            atomicOr(&d.ctr->error, 2u);
-            d.T_col[gc] = 0.0;
-            d.C1_col[gc] = 0.0;
-            d.g_col[gc] = 1.0;
-            d.pos_col[2 * (size_t)gc] = d.pos_col[2 * (size_t)gc + 1] = -1;
-            d.clamp_col[gc] = 1;
-        }
-        for (int q = s0 + lg; q < s1; q += G) {
-            const int t = d.csc_perm[q];
-            d.p_col[q] = 0.0f;
-            d.p0c[q] = d.p0r[t] = 0.5f * d.p_row[t];
-        }
-        return;
-    }
-    double c1, c2;
-    if (cached) {
-        double a1 = 0.0, a2 = 0.0;
-#pragma unroll
-        for (int k = 0; k < kColCache; ++k) {
-            const int q = s0 + lg + G * k;
-            a1 += q == q1 ? cq[k] : 0.0;
-            a2 += q == q2 ? cq[k] : 0.0;
-        }
-        c1 = group_sum<G>(a1); // one lane holds it, the others add zeros
-        c2 = group_sum<G>(a2);
-    } else {
-        c1 = d.cost[d.csc_perm[q1]];
-        c2 = d.cost[d.csc_perm[q2]];
-    }
-    const double gap = (c2 - c1) + p.delta;
-    const bool clamped = gap < p.eps_gap;
-    const double g = clamped ? p.eps_gap : gap;
-    const double T = p.lk_col / g;
-    double z = 0.0;
-    if (cached) {
-#pragma unroll
-        for (int k = 0; k < kColCache; ++k)
-            if (tq[k] >= 0) {
-                const double s = exp(-T * (cq[k] - c1));
-                if (s >= p.tau)
-                    z += s;
-            }
-    } else {
-        for (int q = s0 + lg; q < s1; q += G) {
-            const double s = exp(-T * (d.cost[d.csc_perm[q]] - c1));
-            if (s >= p.tau)
-                z += s;
-        }
-    }
-    z = group_sum<G>(z);
-    auto write = [&](int q, int t, double c) {
-        const double s = exp(-T * (c - c1));
-        const bool keep = s >= p.tau;
-        const double pc = keep ? s / z : 0.0;
-        d.flags[t] = (uint8_t)(d.flags[t] | (keep ? 2 : 0));
-        const float p0 = (float)(0.5 * ((double)d.p_row[t] + pc));
-        d.p_col[q] = (float)pc;
-        d.p0c[q] = p0;
-        d.p0r[t] = p0;
-    };
-    if (cached) {
-#pragma unroll
-        for (int k = 0; k < kColCache; ++k)
-            if (tq[k] >= 0)
-                write(s0 + lg + G * k, tq[k], cq[k]);
-    } else {
-        for (int q = s0 + lg; q < s1; q += G) {
-            const int t = d.csc_perm[q];
-            write(q, t, d.cost[t]);
-        }
-    }
-    if (lg == 0) {
-        d.T_col[gc] = T;
-        d.C1_col[gc] = c1;
-        d.g_col[gc] = g;
-        d.pos_col[2 * (size_t)gc] = q1;
-        d.pos_col[2 * (size_t)gc + 1] = q2;
-        d.clamp_col[gc] = clamped;
-    }
+    const int gc = gid / G;
+    if (gc < d.B * d.M)
+        owner_softmax<false>(d, p, gc, gid % G);
 }
+
+// Columns of at most G * kColCache pairs keep their pairs in registers in the
+// backward (one pass over the column's data instead of three).
+constexpr int kColCache = 4;
 
 // dLoss/dP0 of stored pair t: the Sinkhorn adjoint, or grad_loss * C when
 // there are no Sinkhorn iterations.
