@@ -52,6 +52,13 @@ __device__ __forceinline__ size_t pk_index(int b, int p, int w, int words, int s
     return (((size_t)b * slots + p / kT) * words + w) * kT + p % kT;
 }
 
+// The reverse kernel keeps the adjoint of every pair in LDS at the place of
+// the pair in the row pieces: slot s, pair e, lane l at (s * kP + e) * kT + l,
+// so that the row phase reads and writes consecutive words; a spare entry
+// after them takes the reads and writes of the column pieces' padding.
+__host__ __device__ constexpr int adj_slots(int slots) { return slots * kP * kT; }
+__device__ __forceinline__ int adj_slot(int p, int e) { return ((p / kT) * kP + e) * kT + p % kT; }
+
 // Placement of the pieces of one order (blockIdx.y: 0 rows, 1 columns) of
 // sample blockIdx.x: every owner gets the first position of its group
 // (first | log2(group) << 16 in place[]), the info word of every position is
@@ -71,12 +78,13 @@ __global__ __launch_bounds__(kT) void k_place(DevPlan d, int32_t *place)
     // clear this sample's words (contiguous blocks of the plane-major arrays)
     {
         const size_t np0 = (size_t)slots * kP * kT, ngi = np0 / 2;
+        const uint32_t dummy = (uint32_t)adj_slots(slots); // the reverse kernel's spare adjoint
         for (size_t k = tid; k < np0; k += kT)
             pk.p0[(size_t)b * np0 + k] = 0.0f;
         for (size_t k = tid; k < ngi; k += kT) {
             pk.gi[(size_t)b * ngi + k] = 0u;
             if (!rows)
-                pk.pos[(size_t)b * ngi + k] = 0u;
+                pk.pos[(size_t)b * ngi + k] = dummy | dummy << 16;
         }
     }
     if (tid < 8)
@@ -145,10 +153,12 @@ __global__ __launch_bounds__(kBlock) void k_pack_pairs(DevPlan d, const int32_t 
     const int other = rows ? d.csr_col[t] : d.csc_row[t];
     uint16_t *gi = reinterpret_cast<uint16_t *>(pk.gi + pk_index(b, p, e / 2, kP / 2, slots));
     gi[e & 1] = (uint16_t)(other << 3); // byte offset of an 8-byte entry
-    if (!rows) {
-        const int lo = d.row_ptr[(size_t)b * d.N];
+    if (!rows) { // where the reverse kernel keeps this pair's adjoint: its row piece
+        const int i = d.csc_row[t], gr = b * d.N + i;
+        const int roff = d.csc_perm[t] - d.row_ptr[gr];
+        const int rp = (place[((size_t)b * 2) * kSinkOwners + i] & 0xFFFF) + roff / kP;
         uint16_t *ps = reinterpret_cast<uint16_t *>(pk.pos + pk_index(b, p, e / 2, kP / 2, slots));
-        ps[e & 1] = (uint16_t)((d.csc_perm[t] - lo) & 0xFFFF);
+        ps[e & 1] = (uint16_t)adj_slot(rp, roff % kP);
     }
 }
 
@@ -335,7 +345,7 @@ __device__ __forceinline__ void store_sum(double acc, uint32_t info, double *sum
 }
 
 constexpr size_t bwd_fixed_lds_bytes() { return (8 + 8 + 4 + 4) * (size_t)kSinkOwners; }
-constexpr int kAdjPad = kP; // adjoint entries after a sample's pairs
+
 
 // a / b for positive normal a, b: the hardware reciprocal refined by two
 // Newton steps, then one correction of the quotient (within an ulp of the
@@ -480,27 +490,51 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan 
 // and the row sum d_i / alpha^l_i (column sum e_j / beta^l_j) is just the sum
 // of z' P0 over the row's (column's) pairs. X, Y and the reciprocals are kept
 // in single precision, the adjoint and all sums in double.
+// A row piece that holds pairs: valid and either the row's first piece or one
+// with a position (a padding piece of a group has neither; a later real
+// piece starts at least kP pairs into its row).
+__device__ __forceinline__ bool real_piece(uint32_t info, const Unpack &u)
+{
+    return (info & 0x8000u) != 0 && (u.bits(info, 14, 1) != 0 || u.run(info) != 0);
+}
+
 template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan d)
 {
-    // fixed arrays static (constant addresses), the adjoints dynamic
+    // fixed arrays static (constant addresses), the adjoints (single
+    // precision, row-piece layout) dynamic
     __shared__ double sums[kSinkOwners];
     __shared__ float2 xy[kSinkOwners]; // one side at a time
     __shared__ float inv_a[kSinkOwners], inv_b[kSinkOwners];
-    extern __shared__ double adj[];
+    extern __shared__ float adj[];
     const int b = blockIdx.x, tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
-    const int lo = d.row_ptr[(size_t)b * N], hi = d.row_ptr[(size_t)(b + 1) * N];
+    const int lo = d.row_ptr[(size_t)b * N];
     Pieces<false, SLP> pr;
     Pieces<true, SLP> pc;
     load_pieces(pr, d.pk_row, b);
     load_pieces(pc, d.pk_col, b);
     const double gl = d.grad_loss[b];
     const double *alpha_L = d.alpha + L * BN;
-    for (int t = lo + tid; t < hi; t += kT)
-        adj[t - lo] = gl * d.cost[t] * alpha_L[d.csr_row[t]];
-    if (tid < kAdjPad) // read (never written) by padding pairs of the sample's last pieces
-        adj[hi - lo + tid] = 0.0;
+    {
+        const Unpack u = Unpack::make();
+        // the plan adjoint starts as grad_loss * C, held as adjoint * alpha^L_i
+#pragma unroll
+        for (int s = 0; s < SLP; ++s) {
+            const int i = u.owner(pr.info[s]), run = u.run(pr.info[s]);
+            const bool piece = real_piece(pr.info[s], u);
+            const int rend = piece ? d.row_ptr[(size_t)b * N + i + 1] - lo : 0;
+            const double al = piece ? alpha_L[(size_t)b * N + i] : 0.0;
+#pragma unroll
+            for (int e = 0; e < kP; ++e) {
+                const bool real = piece && run + e < rend;
+                const bool mass = pr.p0[s][e] != 0.0f; // only pairs with mass carry an adjoint
+                adj[adj_slot(s * kT + tid, e)] = real && mass ? (float)(gl * d.cost[lo + run + e] * al) : 0.0f;
+            }
+        }
+        if (tid == 0)
+            adj[adj_slots(SLP)] = 0.0f;
+    }
     double a_own[kSL], b_own[kSL];
 #pragma unroll
     for (int s = 0; s < kSL; ++s) {
@@ -525,27 +559,26 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan 
             const int k = kSL * tid + s;
             a_prev[s] = k < N ? d.alpha[(l - 1) * BN + (size_t)b * N + k] : 1.0;
         }
-        // row phase
+        // row phase: the lane's own adjoint words, consecutive across lanes
         const Unpack u = Unpack::make();
 #pragma unroll
         for (int s = 0; s < SLP; ++s)
             if (wave_active(pr, s)) {
-                const int run = u.run(pr.info[s]);
                 const double inv = (double)inv_a[u.owner(pr.info[s])];
-                double m[kP];
+                float m[kP];
                 float2 w[kP];
 #pragma unroll
                 for (int e = 0; e < kP; ++e) {
-                    m[e] = adj[run + e];
+                    m[e] = adj[adj_slot(s * kT + tid, e)];
                     w[e] = lds_at<float2>(xy, u.half(pr.gi[s][e / 2], e));
                 }
                 double acc = 0.0;
 #pragma unroll
                 for (int e = 0; e < kP; ++e) {
-                    const double z = __builtin_fma(m[e] * inv, (double)w[e].x, -(double)w[e].y);
+                    const double z = __builtin_fma((double)m[e] * inv, (double)w[e].x, -(double)w[e].y);
                     const double p0 = widen(pr.p0[s][e]);
-                    if (p0 != 0.0)
-                        adj[run + e] = z;
+                    // pairs without mass (padding) keep 0, so their values stay bounded
+                    adj[adj_slot(s * kT + tid, e)] = p0 != 0.0 ? (float)z : 0.0f;
                     acc = e == 0 ? z * p0 : __builtin_fma(z, p0, acc);
                 }
                 store_sum(group_reduce(acc, pr.info[s], u), pr.info[s], sums, u);
@@ -570,13 +603,14 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan 
             b_prev[s] = k < M ? d.beta[(l - 1) * BM + (size_t)b * M + k] : 1.0;
         }
         lds_barrier();
-        // column phase
+        // column phase: the adjoints of the column's pairs at their row-piece
+        // places (padding at the spare entry)
 #pragma unroll
         for (int s = 0; s < SLP; ++s)
             if (wave_active(pc, s)) {
                 const double inv = (double)inv_b[u.owner(pc.info[s])];
                 uint32_t ps[kP];
-                double m[kP];
+                float m[kP];
                 float2 w[kP];
 #pragma unroll
                 for (int e = 0; e < kP; ++e) {
@@ -587,10 +621,10 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan 
                 double acc = 0.0;
 #pragma unroll
                 for (int e = 0; e < kP; ++e) {
-                    const double z = __builtin_fma(m[e] * inv, (double)w[e].x, -(double)w[e].y);
+                    const double z = __builtin_fma((double)m[e] * inv, (double)w[e].x, -(double)w[e].y);
                     const double p0 = widen(pc.p0[s][e]);
-                    if (p0 != 0.0)
-                        adj[ps[e]] = z;
+                    if (p0 != 0.0) // padding leaves the spare entry at 0
+                        adj[ps[e]] = (float)z;
                     acc = e == 0 ? z * p0 : __builtin_fma(z, p0, acc);
                 }
                 store_sum(group_reduce(acc, pc.info[s], u), pc.info[s], sums, u);
@@ -612,9 +646,20 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan 
         lds_barrier();
     }
     // the last column update (alpha^0 = beta^0 = 1), written out in row-major order
-    for (int t = lo + tid; t < hi; t += kT) {
-        const float2 w = xy[d.csr_col[t]];
-        d.adj[t] = adj[t - lo] * (double)w.x - (double)w.y;
+    {
+        const Unpack u = Unpack::make();
+#pragma unroll
+        for (int s = 0; s < SLP; ++s) {
+            const int i = u.owner(pr.info[s]), run = u.run(pr.info[s]);
+            const bool piece = real_piece(pr.info[s], u);
+            const int rend = piece ? d.row_ptr[(size_t)b * N + i + 1] - lo : 0;
+#pragma unroll
+            for (int e = 0; e < kP; ++e)
+                if (piece && run + e < rend) {
+                    const float2 w = lds_at<float2>(xy, u.half(pr.gi[s][e / 2], e));
+                    d.adj[lo + run + e] = (double)adj[adj_slot(s * kT + tid, e)] * (double)w.x - (double)w.y;
+                }
+        }
     }
 }
 
@@ -759,8 +804,9 @@ constexpr size_t kLdsBudget = 160 * 1024;
 
 bool sinkhorn_bwd_fits(int slots, int64_t max_pairs)
 {
-    // the adjoint of every pair of a sample in LDS; positions are 16-bit
-    return slots > 0 && max_pairs <= 65536 && bwd_fixed_lds_bytes() + 8 * (size_t)(max_pairs + kAdjPad) <= kLdsBudget;
+    // the adjoint of every pair of a sample in LDS, at its row piece
+    (void)max_pairs;
+    return slots > 0 && bwd_fixed_lds_bytes() + 4 * (size_t)(adj_slots(slots) + 1) <= kLdsBudget;
 }
 
 size_t packed_order_words(int B, int slots) { return (size_t)B * slots * kP * kT; }
@@ -795,7 +841,8 @@ hipError_t launch_sinkhorn_fwd(const DevPlan &d, double eps, hipStream_t s)
 
 hipError_t launch_sinkhorn_bwd(const DevPlan &d, int64_t max_pairs, hipStream_t s)
 {
-    const size_t bytes = 8 * (size_t)(max_pairs + kAdjPad); // beyond the static arrays
+    (void)max_pairs;
+    const size_t bytes = 4 * (size_t)(adj_slots(d.pk_row.slots) + 1); // beyond the static arrays
     const auto k = for_slots<BwdK>(d.pk_row.slots);
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess)
