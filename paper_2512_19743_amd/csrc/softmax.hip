@@ -220,10 +220,6 @@ __global__ __launch_bounds__(kBlock) void k_col_softmax(DevPlan d, Params p)
         owner_softmax<false>(d, p, gc, gid % G);
 }
 
-// Columns of at most G * kColCache pairs keep their pairs in registers in the
-// backward (one pass over the column's data instead of three).
-constexpr int kColCache = 4;
-
 // dLoss/dP0 of stored pair t: the Sinkhorn adjoint, or grad_loss * C when
 // there are no Sinkhorn iterations.
 __device__ __forceinline__ double p0bar(const DevPlan &d, int t, double gl)
@@ -231,6 +227,12 @@ __device__ __forceinline__ double p0bar(const DevPlan &d, int t, double gl)
     return d.L == 0 ? gl * d.cost[t] : d.adj[t];
 }
 
+// Backward of one owner's softmax by its group of G lanes, with the first
+// kSmCache pairs of each lane loaded up front (as in the forward).
+//   columns: cbar_t = -T P_col (Pbar_t - sigma) on kept pairs, plus the gap
+//            term at the two argmins; written per pair (cbar).
+//   rows:    the same for P_row, plus cbar from the columns and the direct
+//            term grad_loss * v; then Eq. 5 turns cbar into grad_x.
 __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(DevPlan d, Params p)
 {
     const int gid = blockIdx.x * kBlock + threadIdx.x;
@@ -239,81 +241,71 @@ __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(DevPlan d, Params p)
         return;
     const int b = gc / d.M;
     const double gl = d.grad_loss[b];
-    const int s0 = d.col_ptr[gc], s1 = d.col_ptr[gc + 1];
+    const int s0 = d.col_ptr[gc], n = d.col_ptr[gc + 1] - s0;
     const double T = d.T_col[gc], c1 = d.C1_col[gc];
     const double gapbar_scale = d.clamp_col[gc] ? 0.0 : -T / d.g_col[gc];
     const int q1 = d.pos_col[2 * (size_t)gc], q2 = d.pos_col[2 * (size_t)gc + 1];
-    if (s1 - s0 <= G * kColCache) {
-        // one pass over the column's data: kept pairs' P_col, dL/dP0 and cost in registers
-        const float *yc = d.y + (size_t)gc * 3;
-        const float *xb = d.x + (size_t)b * d.N * 3;
-        int tq[kColCache];
-        double pq[kColCache], aq[kColCache], cq[kColCache];
-        double sigma = 0.0;
+    const float *yc = d.y + (size_t)gc * 3;
+    const float y0 = yc[0], y1 = yc[1], y2 = yc[2];
+    const float *xb = d.x + (size_t)b * d.N * 3;
+
+    int tq[kSmCache], iq[kSmCache];
+    float pq[kSmCache];
 #pragma unroll
-        for (int k = 0; k < kColCache; ++k) {
-            const int q = s0 + lg + G * k;
-            tq[k] = -1;
-            pq[k] = aq[k] = cq[k] = 0.0;
-            if (q < s1) {
-                const int t = d.csc_perm[q];
-                tq[k] = t;
-                if (d.flags[t] & 2) {
-                    pq[k] = (double)d.p_col[q];
-                    aq[k] = 0.5 * p0bar(d, t, gl);
-                    cq[k] = dist_f64(xb + 3 * (size_t)d.csc_row[q], yc);
-                    sigma += pq[k] * aq[k];
-                }
-            }
-        }
-        sigma = group_sum<G>(sigma);
-        double tbar = 0.0;
+    for (int c = 0; c < kSmCache; ++c) {
+        const int k = lg + G * c;
+        tq[c] = k < n ? d.csc_perm[s0 + k] : 0;
+        iq[c] = k < n ? d.csc_row[s0 + k] : 0;
+        pq[c] = k < n ? d.p_col[s0 + k] : 0.0f;
+    }
+    double aq[kSmCache], cq[kSmCache];
+    bool kq[kSmCache];
 #pragma unroll
-        for (int k = 0; k < kColCache; ++k)
-            tbar -= pq[k] * (aq[k] - sigma) * (cq[k] - c1); // zero for pairs not kept
-        tbar = group_sum<G>(tbar);
-        const double gapbar = gapbar_scale * tbar;
-#pragma unroll
-        for (int k = 0; k < kColCache; ++k) {
-            const int q = s0 + lg + G * k;
-            if (tq[k] >= 0) {
-                double cb = -T * pq[k] * (aq[k] - sigma);
-                if (q == q2)
-                    cb += gapbar;
-                if (q == q1)
-                    cb -= gapbar;
-                d.cbar[tq[k]] = cb;
-            }
-        }
-        return;
+    for (int c = 0; c < kSmCache; ++c) {
+        const int k = lg + G * c;
+        kq[c] = k < n && (d.flags[tq[c]] & 2) != 0;
+        aq[c] = kq[c] ? 0.5 * p0bar(d, tq[c], gl) : 0.0;
+        const float *xi = xb + 3 * (size_t)iq[c];
+        cq[c] = kq[c] ? dist3(xi[0], xi[1], xi[2], y0, y1, y2) : 0.0;
     }
     double sigma = 0.0;
-    for (int q = s0 + lg; q < s1; q += G) {
-        const int t = d.csc_perm[q];
+#pragma unroll
+    for (int c = 0; c < kSmCache; ++c)
+        sigma += kq[c] ? (double)pq[c] * aq[c] : 0.0;
+    for (int k = lg + G * kSmCache; k < n; k += G) {
+        const int t = d.csc_perm[s0 + k];
         if (d.flags[t] & 2)
-            sigma += (double)d.p_col[q] * 0.5 * p0bar(d, t, gl);
+            sigma += (double)d.p_col[s0 + k] * (0.5 * p0bar(d, t, gl));
     }
     sigma = group_sum<G>(sigma);
     double tbar = 0.0;
-    for (int q = s0 + lg; q < s1; q += G) {
-        const int t = d.csc_perm[q];
-        if (d.flags[t] & 2) {
-            const double ab = (double)d.p_col[q] * (0.5 * p0bar(d, t, gl) - sigma);
-            tbar -= ab * (d.cost[t] - c1);
-        }
+#pragma unroll
+    for (int c = 0; c < kSmCache; ++c)
+        tbar -= kq[c] ? (double)pq[c] * (aq[c] - sigma) * (cq[c] - c1) : 0.0;
+    for (int k = lg + G * kSmCache; k < n; k += G) {
+        const int t = d.csc_perm[s0 + k];
+        if (d.flags[t] & 2)
+            tbar -= (double)d.p_col[s0 + k] * (0.5 * p0bar(d, t, gl) - sigma) * (d.cost[t] - c1);
     }
     tbar = group_sum<G>(tbar);
     const double gapbar = gapbar_scale * tbar;
-    for (int q = s0 + lg; q < s1; q += G) {
-        const int t = d.csc_perm[q];
-        double cb = 0.0;
-        if (d.flags[t] & 2)
-            cb = -T * (double)d.p_col[q] * (0.5 * p0bar(d, t, gl) - sigma);
+    auto gap_terms = [&](int q, double cb) {
         if (q == q2)
             cb += gapbar;
         if (q == q1)
             cb -= gapbar;
-        d.cbar[t] = cb;
+        return cb;
+    };
+#pragma unroll
+    for (int c = 0; c < kSmCache; ++c) {
+        const int k = lg + G * c;
+        if (k < n)
+            d.cbar[tq[c]] = gap_terms(s0 + k, kq[c] ? -T * (double)pq[c] * (aq[c] - sigma) : 0.0);
+    }
+    for (int k = lg + G * kSmCache; k < n; k += G) {
+        const int t = d.csc_perm[s0 + k];
+        const double cb = (d.flags[t] & 2) ? -T * (double)d.p_col[s0 + k] * (0.5 * p0bar(d, t, gl) - sigma) : 0.0;
+        d.cbar[t] = gap_terms(s0 + k, cb);
     }
 }
 
@@ -326,44 +318,80 @@ __global__ __launch_bounds__(kBlock) void k_bwd_row_softmax(DevPlan d, Params p,
     const int b = r / d.N;
     const size_t BN = (size_t)d.B * d.N, BM = (size_t)d.B * d.M;
     const float *xr = d.x + (size_t)r * 3;
+    const float x0 = xr[0], x1 = xr[1], x2 = xr[2];
     const float *yb = d.y + (size_t)b * d.M * 3;
     const double gl = d.grad_loss[b];
-    const int t0 = d.row_ptr[r], t1 = d.row_ptr[r + 1];
-    double sigma = 0.0;
-    for (int t = t0 + lg; t < t1; t += G)
-        if (d.flags[t] & 1)
-            sigma += (double)d.p_row[t] * 0.5 * p0bar(d, t, gl);
-    sigma = group_sum<G>(sigma);
+    const int t0 = d.row_ptr[r], n = d.row_ptr[r + 1] - t0;
     const double T = d.T_row[r], c1 = d.C1_row[r];
-    double tbar = 0.0;
-    for (int t = t0 + lg; t < t1; t += G)
-        if (d.flags[t] & 1) {
-            const double ab = (double)d.p_row[t] * (0.5 * p0bar(d, t, gl) - sigma);
-            tbar -= ab * (d.cost[t] - c1);
-        }
-    tbar = group_sum<G>(tbar);
-    const double gapbar = d.clamp_row[r] ? 0.0 : -tbar * T / d.g_row[r];
+    const double gscale = d.clamp_row[r] ? 0.0 : -T / d.g_row[r];
     const int q1 = d.pos_row[2 * (size_t)r], q2 = d.pos_row[2 * (size_t)r + 1];
     const double al = d.alpha[(size_t)d.L * BN + r];
     const double *bl = d.beta + (size_t)d.L * BM + (size_t)b * d.M;
-    double gx = 0.0, gy = 0.0, gz = 0.0;
-    for (int t = t0 + lg; t < t1; t += G) {
-        const int j = d.csr_col[t];
-        const float *yj = yb + 3 * (size_t)j;
-        const double c = d.cost[t];
-        double cb = d.cbar[t] + gl * (al * (double)d.p0r[t] * bl[j]);
+
+    int jq[kSmCache];
+    bool kq[kSmCache];
+    float pq[kSmCache], p0q[kSmCache];
+    double aq[kSmCache], cq[kSmCache], cbq[kSmCache];
+#pragma unroll
+    for (int c = 0; c < kSmCache; ++c) {
+        const int k = lg + G * c, t = t0 + k;
+        const bool in = k < n;
+        jq[c] = in ? d.csr_col[t] : 0;
+        kq[c] = in && (d.flags[t] & 1) != 0;
+        pq[c] = in ? d.p_row[t] : 0.0f;
+        p0q[c] = in ? d.p0r[t] : 0.0f;
+        aq[c] = in ? 0.5 * p0bar(d, t, gl) : 0.0;
+        cq[c] = in ? d.cost[t] : 1.0;
+        cbq[c] = in ? d.cbar[t] : 0.0;
+    }
+    double sigma = 0.0;
+#pragma unroll
+    for (int c = 0; c < kSmCache; ++c)
+        sigma += kq[c] ? (double)pq[c] * aq[c] : 0.0;
+    for (int k = lg + G * kSmCache; k < n; k += G) {
+        const int t = t0 + k;
         if (d.flags[t] & 1)
-            cb -= T * (double)d.p_row[t] * (0.5 * p0bar(d, t, gl) - sigma);
+            sigma += (double)d.p_row[t] * (0.5 * p0bar(d, t, gl));
+    }
+    sigma = group_sum<G>(sigma);
+    double tbar = 0.0;
+#pragma unroll
+    for (int c = 0; c < kSmCache; ++c)
+        tbar -= kq[c] ? (double)pq[c] * (aq[c] - sigma) * (cq[c] - c1) : 0.0;
+    for (int k = lg + G * kSmCache; k < n; k += G) {
+        const int t = t0 + k;
+        if (d.flags[t] & 1)
+            tbar -= (double)d.p_row[t] * (0.5 * p0bar(d, t, gl) - sigma) * (d.cost[t] - c1);
+    }
+    tbar = group_sum<G>(tbar);
+    const double gapbar = gscale * tbar;
+    double gx = 0.0, gy = 0.0, gz = 0.0;
+    // cbar of pair t (column part cb0, P_row, dL/dP0, cost, P0, column j) into grad_x (Eq. 5)
+    auto add = [&](int t, int j, double cb0, bool kept, float prow, double a, double c, float p0) {
+        double cb = cb0 + gl * (al * (double)p0 * bl[j]);
+        if (kept)
+            cb -= T * (double)prow * (a - sigma);
         if (t == q2)
             cb += gapbar;
         if (t == q1)
             cb -= gapbar;
+        const float *yj = yb + 3 * (size_t)j;
         const double w = cb / (c + p.eps_dist); // Eq. 5
-        gx += w * ((double)xr[0] - (double)yj[0]);
-        gy += w * ((double)xr[1] - (double)yj[1]);
-        gz += w * ((double)xr[2] - (double)yj[2]);
+        gx += w * ((double)x0 - (double)yj[0]);
+        gy += w * ((double)x1 - (double)yj[1]);
+        gz += w * ((double)x2 - (double)yj[2]);
         if (keep_cbar)
             d.cbar[t] = cb;
+    };
+#pragma unroll
+    for (int c = 0; c < kSmCache; ++c) {
+        const int k = lg + G * c;
+        if (k < n)
+            add(t0 + k, jq[c], cbq[c], kq[c], pq[c], aq[c], cq[c], p0q[c]);
+    }
+    for (int k = lg + G * kSmCache; k < n; k += G) {
+        const int t = t0 + k;
+        add(t, d.csr_col[t], d.cbar[t], (d.flags[t] & 1) != 0, d.p_row[t], 0.5 * p0bar(d, t, gl), d.cost[t], d.p0r[t]);
     }
     gx = group_sum<G>(gx);
     gy = group_sum<G>(gy);
