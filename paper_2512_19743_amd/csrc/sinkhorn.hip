@@ -34,6 +34,7 @@
 
 #include "apml_internal.h"
 #include "device_common.h"
+#include "pieces.h"
 
 namespace apml {
 namespace {
@@ -41,99 +42,20 @@ namespace {
 constexpr int kT = kSinkLanes;
 constexpr int kP = kSinkPiece;
 constexpr int kSL = kSinkOwners / kSinkLanes; // owners per lane in the owner phase
+using pieces::adj_slot;
+using pieces::adj_slots;
+using pieces::pack_col_pair;
+using pieces::pack_row_pair;
+using pieces::pk_index;
+using pieces::place_order;
 
-__device__ __forceinline__ int pieces_of(int len) { return sink_pieces(len); }
-__device__ __forceinline__ int log2_group(int np) { return sink_log2_group(np); }
-
-// Word w of position p in a plane-major packed array with `words` words per
-// position.
-__device__ __forceinline__ size_t pk_index(int b, int p, int w, int words, int slots)
-{
-    return (((size_t)b * slots + p / kT) * words + w) * kT + p % kT;
-}
-
-// The reverse kernel keeps the adjoint of every pair in LDS at the place of
-// the pair in the row pieces: slot s, pair e, lane l at (s * kP + e) * kT + l,
-// so that the row phase reads and writes consecutive words; a spare entry
-// after them takes the reads and writes of the column pieces' padding.
-__host__ __device__ constexpr int adj_slots(int slots) { return slots * kP * kT; }
-__device__ __forceinline__ int adj_slot(int p, int e) { return ((p / kT) * kP + e) * kT + p % kT; }
-
-// Placement of the pieces of one order (blockIdx.y: 0 rows, 1 columns) of
-// sample blockIdx.x: every owner gets the first position of its group
-// (first | log2(group) << 16 in place[]), the info word of every position is
-// written, and the P0 / index / position words are cleared (k_pack_pairs
-// fills in the real pairs). The host has checked that the positions fit
-// (slots * kT) and that no owner has more than kSinkMaxGroup pieces.
 __global__ __launch_bounds__(kT) void k_place(DevPlan d, int32_t *place)
 {
     __shared__ int hist[8], base[8];
-    const int b = blockIdx.x, tid = threadIdx.x;
-    const bool rows = blockIdx.y == 0;
-    const int n_own = rows ? d.N : d.M;
-    const int32_t *ptr = rows ? d.row_ptr + (size_t)b * d.N : d.col_ptr + (size_t)b * d.M;
-    const PackedOrder pk = rows ? d.pk_row : d.pk_col;
-    const int slots = pk.slots, cap = slots * kT;
-    const int lo = d.row_ptr[(size_t)b * d.N];
-    // clear this sample's words (contiguous blocks of the plane-major arrays)
-    {
-        const size_t np0 = (size_t)slots * kP * kT, ngi = np0 / 2;
-        const uint32_t dummy = (uint32_t)adj_slots(slots); // the reverse kernel's spare adjoint
-        for (size_t k = tid; k < np0; k += kT)
-            pk.p0[(size_t)b * np0 + k] = 0.0f;
-        for (size_t k = tid; k < ngi; k += kT) {
-            pk.gi[(size_t)b * ngi + k] = 0u;
-            if (!rows)
-                pk.pos[(size_t)b * ngi + k] = dummy | dummy << 16;
-        }
-    }
-    if (tid < 8)
-        hist[tid] = 0;
-    __syncthreads();
-    int lg[kSL], rk[kSL], st[kSL], len[kSL];
-#pragma unroll
-    for (int s = 0; s < kSL; ++s) {
-        const int k = kSL * tid + s;
-        lg[s] = -1;
-        if (k < n_own) {
-            st[s] = ptr[k];
-            len[s] = ptr[k + 1] - st[s];
-            lg[s] = log2_group(pieces_of(len[s]));
-            rk[s] = atomicAdd(&hist[lg[s]], 1);
-        }
-    }
-    __syncthreads();
-    if (tid == 0) {
-        int run = 0;
-        for (int c = 6; c >= 0; --c) { // largest groups first: every group is aligned to its size
-            base[c] = run;
-            run += hist[c] << c;
-        }
-        base[7] = run;
-        pk.n_pos[b] = run;
-    }
-    __syncthreads();
-    for (int p = base[7] + tid; p < cap; p += kT) // unused positions: invalid
-        pk.info[pk_index(b, p, 0, 1, slots)] = 0u;
-#pragma unroll
-    for (int s = 0; s < kSL; ++s) {
-        if (lg[s] < 0)
-            continue;
-        const int k = kSL * tid + s, c = 1 << lg[s];
-        const int first = base[lg[s]] + (rk[s] << lg[s]);
-        place[((size_t)b * 2 + blockIdx.y) * kSinkOwners + k] = first | (lg[s] << 16);
-        for (int q = 0; q < c; ++q) {
-            uint32_t info = (uint32_t)k | ((uint32_t)lg[s] << 11) | ((q == 0 ? 1u : 0u) << 14) | 0x8000u;
-            if (rows && q * kP < len[s])
-                info |= ((uint32_t)(st[s] + q * kP - lo) & 0xFFFFu) << 16;
-            pk.info[pk_index(b, first + q, 0, 1, slots)] = info;
-        }
-    }
+    place_order(d, place, blockIdx.x, blockIdx.y == 0, hist, base);
 }
 
-// Writes every stored pair into its piece, one thread per pair and order:
-// P0, the gathered index with its 'real' bit and (columns) the row-major
-// position within the sample.
+// Writes every stored pair into its piece, one thread per pair and order.
 __global__ __launch_bounds__(kBlock) void k_pack_pairs(DevPlan d, const int32_t *place)
 {
     const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
@@ -141,24 +63,13 @@ __global__ __launch_bounds__(kBlock) void k_pack_pairs(DevPlan d, const int32_t 
     const int64_t t = rows ? g : g - d.nnz;
     if (t >= d.nnz)
         return;
-    const int own_g = rows ? d.csr_row[t] : d.csc_col[t]; // global row or column
-    const int n_own = rows ? d.N : d.M;
-    const int b = own_g / n_own, k = own_g - b * n_own;
-    const int off = (int)(t - (rows ? d.row_ptr[own_g] : d.col_ptr[own_g]));
-    const int q = off / kP, e = off % kP;
-    const int p = (place[((size_t)b * 2 + (rows ? 0 : 1)) * kSinkOwners + k] & 0xFFFF) + q;
-    const PackedOrder &pk = rows ? d.pk_row : d.pk_col;
-    const int slots = pk.slots;
-    pk.p0[pk_index(b, p, e, kP, slots)] = rows ? d.p0r[t] : d.p0c[t];
-    const int other = rows ? d.csr_col[t] : d.csc_row[t];
-    uint16_t *gi = reinterpret_cast<uint16_t *>(pk.gi + pk_index(b, p, e / 2, kP / 2, slots));
-    gi[e & 1] = (uint16_t)(other << 3); // byte offset of an 8-byte entry
-    if (!rows) { // where the reverse kernel keeps this pair's adjoint: its row piece
-        const int i = d.csc_row[t], gr = b * d.N + i;
-        const int roff = d.csc_perm[t] - d.row_ptr[gr];
-        const int rp = (place[((size_t)b * 2) * kSinkOwners + i] & 0xFFFF) + roff / kP;
-        uint16_t *ps = reinterpret_cast<uint16_t *>(pk.pos + pk_index(b, p, e / 2, kP / 2, slots));
-        ps[e & 1] = (uint16_t)adj_slot(rp, roff % kP);
+    if (rows) {
+        const int r = d.csr_row[t], b = r / d.N;
+        pack_row_pair(d, place, b, r - b * d.N, (int)(t - d.row_ptr[r]), d.csr_col[t], d.p0r[t]);
+    } else {
+        const int gc = d.csc_col[t], b = gc / d.M, i = d.csc_row[t];
+        const int roff = d.csc_perm[t] - d.row_ptr[(size_t)b * d.N + i];
+        pack_col_pair(d, place, b, gc - b * d.M, (int)(t - d.col_ptr[gc]), i, roff, d.p0c[t]);
     }
 }
 
