@@ -531,8 +531,31 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     dv.p0r = keep.get<float>(nnz);
     dv.p0c = keep.get<float>(nnz);
     dv.cost = keep.get<double>(nnz);
-    ba.tmp_row = tmp.get<int32_t>(nnz);
-    ba.tmp_src = tmp.get<int32_t>(nnz);
+    // column-major view: per sample in LDS when it fits (with the row
+    // softmax), else slots taken by global counters (in the compaction when
+    // no tile is rescanned)
+    const bool csc_lds = csc_sample_fits(N, M, plan->max_sample);
+    const bool placed = !csc_lds && ea.stage && !rb->ctr.overflow;
+    if (!csc_lds) {
+        ba.tmp_row = tmp.get<int32_t>(nnz);
+        ba.tmp_src = tmp.get<int32_t>(nnz);
+    }
+    // pieces of the per-sample Sinkhorn kernels; with staged hits their
+    // placement runs in the compaction's launch
+    int32_t *place = nullptr;
+    if (plan->sink_fwd) {
+        const size_t w = packed_order_words(B, slots);
+        for (PackedOrder *pk : {&dv.pk_row, &dv.pk_col}) {
+            pk->slots = slots;
+            pk->p0 = keep.get<float>(w);
+            pk->gi = keep.get<uint32_t>(w / 2);
+            pk->info = keep.get<uint32_t>(w / kSinkPiece);
+            pk->pos = pk == &dv.pk_col ? keep.get<uint32_t>(w / 2) : nullptr;
+            pk->n_pos = keep.get<int32_t>(B);
+        }
+        place = tmp.get<int32_t>((size_t)B * 2 * kSinkOwners);
+    }
+    const bool pieces_placed = place && ea.stage && !placed;
     if (tmp.failed || keep.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (sparse arrays)");
     {
@@ -545,16 +568,12 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         ea.tmp_row = ba.tmp_row;
         ea.tmp_src = ba.tmp_src;
         ea.csc_col = dv.csc_col;
-        // column-major view: per sample in LDS when it fits, else slots taken
-        // by global counters (in the compaction when no tile is rescanned)
-        const bool csc_lds = csc_sample_fits(N, M, plan->max_sample);
-        const bool placed = !csc_lds && ea.stage && !rb->ctr.overflow;
         if (ea.stage)
-            launch_emit_compact(ea, rb->ctr.overflow != 0, placed, s);
+            launch_emit_compact(ea, rb->ctr.overflow != 0, placed, &dv, pieces_placed ? place : nullptr, s);
         else
             launch_emit_write(ea, s);
         if (csc_lds) {
-            HIP_TRY(launch_csc_sample(dv, plan->max_sample, s));
+            // built with the row softmax below
         } else if (placed) {
             launch_csc_sort(dv, ba, s);
         } else {
@@ -582,23 +601,16 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     dv.sden = keep.get<double>((size_t)std::max(L, 1) * BM);
     dv.dvec = keep.get<double>(BN);
     dv.evec = keep.get<double>(BM);
-    if (plan->sink_fwd) {
-        const size_t w = packed_order_words(B, slots);
-        for (PackedOrder *pk : {&dv.pk_row, &dv.pk_col}) {
-            pk->slots = slots;
-            pk->p0 = keep.get<float>(w);
-            pk->gi = keep.get<uint32_t>(w / 2);
-            pk->info = keep.get<uint32_t>(w / kSinkPiece);
-            pk->pos = pk == &dv.pk_col ? keep.get<uint32_t>(w / 2) : nullptr;
-            pk->n_pos = keep.get<int32_t>(B);
-        }
-    }
     if (keep.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (plan)");
     {
         PhaseTimer pt(PH_SOFTMAX, s);
-        launch_softmax(dv, kp, s);
-        HIP_TRY(hipGetLastError());
+        if (csc_lds) {
+            HIP_TRY(launch_csc_and_softmax(dv, kp, plan->max_sample, s));
+        } else {
+            launch_softmax(dv, kp, s);
+            HIP_TRY(hipGetLastError());
+        }
         pt.stop();
     }
 
@@ -606,10 +618,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     {
         PhaseTimer pt(PH_SINKHORN, s);
         if (plan->sink_fwd) {
-            int32_t *place = tmp.get<int32_t>((size_t)B * 2 * kSinkOwners);
-            if (tmp.failed)
-                return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (pieces)");
-            launch_pack(dv, place, s);
+            launch_pack(dv, place, pieces_placed, s);
             HIP_TRY(launch_sinkhorn_fwd(dv, prm.eps_stab, s));
         } else {
             launch_sinkhorn_fwd_steps(dv, prm.eps_stab, s);

@@ -91,7 +91,12 @@ void launch_emit_write(const EmitArgs &a, hipStream_t s);
 // Writes the CSR from the staged hits of every tile whose list did not
 // overflow; with overflow set, the writing pass then rescans only the tiles
 // whose list overflowed.
-void launch_emit_compact(const EmitArgs &a, bool overflow, bool place, hipStream_t s);
+struct DevPlan;
+// place: the compaction also takes each pair's column slot. pieces_place
+// (non-NULL, with place false): the same launch also places the pieces of the
+// per-sample Sinkhorn kernels (place_order) for plan d.
+void launch_emit_compact(const EmitArgs &a, bool overflow, bool place, const DevPlan *d, int32_t *pieces_place,
+                         hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // sparse structure
@@ -162,9 +167,10 @@ void launch_csc_build(const DevPlan &d, const BuildArgs &a, hipStream_t s);
 // each column remains.
 void launch_csc_sort(const DevPlan &d, const BuildArgs &a, hipStream_t s);
 // The column-major view of each sample in one workgroup (LDS counters), when
-// the sample's column offsets and pairs fit in LDS.
+// the sample's column offsets and pairs fit in LDS: launched together with
+// the row softmax, then the column softmax.
 bool csc_sample_fits(int N, int M, int64_t max_pairs);
-hipError_t launch_csc_sample(const DevPlan &d, int64_t max_pairs, hipStream_t s);
+hipError_t launch_csc_and_softmax(const DevPlan &d, const Params &p, int64_t max_pairs, hipStream_t s);
 
 void launch_softmax(const DevPlan &d, const Params &p, hipStream_t s);
 void launch_bwd_softmax(const DevPlan &d, const Params &p, hipStream_t s);
@@ -204,7 +210,8 @@ int sinkhorn_slots(int N, int M, const int32_t *counts, int B);
 bool sinkhorn_bwd_fits(int slots, int64_t max_pairs);
 size_t packed_order_words(int B, int slots); // 32-bit words of one PackedOrder's p0 array
 // Lays out the pieces of both orders; place: [B][2][2048] int32 scratch.
-void launch_pack(const DevPlan &d, int32_t *place, hipStream_t s);
+// placed: place[] and the info words are already written (with the compaction).
+void launch_pack(const DevPlan &d, int32_t *place, bool placed, hipStream_t s);
 hipError_t launch_sinkhorn_fwd(const DevPlan &d, double eps, hipStream_t s);
 hipError_t launch_sinkhorn_bwd(const DevPlan &d, int64_t max_pairs, hipStream_t s);
 void launch_sinkhorn_fwd_steps(const DevPlan &d, double eps, hipStream_t s);

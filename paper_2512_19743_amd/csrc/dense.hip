@@ -21,6 +21,7 @@
 //              candidate set.
 #include "apml_internal.h"
 #include "device_common.h"
+#include "pieces.h"
 
 namespace apml {
 namespace {
@@ -257,9 +258,8 @@ __device__ __forceinline__ void emit_pair(const EmitArgs &a, int pos, int row, i
     }
 }
 
-template <bool PLACE> __global__ __launch_bounds__(kBlock) void k_emit_compact(EmitArgs a)
+template <bool PLACE> __device__ __forceinline__ void emit_compact_thread(const EmitArgs &a, int64_t g)
 {
-    const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (g >= (int64_t)a.B * a.N * a.S)
         return;
     const int row = (int)(g / a.S), ch = (int)(g % a.S);
@@ -293,6 +293,29 @@ template <bool PLACE> __global__ __launch_bounds__(kBlock) void k_emit_compact(E
     }
 }
 
+template <bool PLACE> __global__ __launch_bounds__(kBlock) void k_emit_compact(EmitArgs a)
+{
+    emit_compact_thread<PLACE>(a, (int64_t)blockIdx.x * kBlock + threadIdx.x);
+}
+
+// The compaction (first n_compact blocks) and, in the remaining blocks, the
+// placement of the per-sample Sinkhorn pieces (block k: sample k / 2, order
+// k % 2): independent work in one launch, so the placement runs on the CUs
+// the compaction leaves free.
+constexpr int kFusedT = kSinkLanes;
+
+__global__ __launch_bounds__(kFusedT) void k_emit_compact_place(EmitArgs a, DevPlan d, int32_t *place,
+                                                                 int n_compact)
+{
+    __shared__ int hist[8], base[8];
+    if ((int)blockIdx.x < n_compact) {
+        emit_compact_thread<false>(a, (int64_t)blockIdx.x * kFusedT + threadIdx.x);
+        return;
+    }
+    const int k = blockIdx.x - n_compact;
+    pieces::place_order(d, place, k / 2, k % 2 == 0, hist, base);
+}
+
 } // namespace
 
 void launch_top2(const ScanDir &rows, const ScanDir &cols, int B, hipStream_t s)
@@ -319,13 +342,19 @@ void launch_emit_write(const EmitArgs &a, hipStream_t s)
     hipLaunchKernelGGL(k_emit<true>, dim3(a.B * a.S * a.owner_blocks), dim3(kBlock), 0, s, a);
 }
 
-void launch_emit_compact(const EmitArgs &a, bool overflow, bool place, hipStream_t s)
+void launch_emit_compact(const EmitArgs &a, bool overflow, bool place, const DevPlan *d, int32_t *pieces_place,
+                         hipStream_t s)
 {
-    const dim3 g(blocks_for((int64_t)a.B * a.N * a.S, kBlock));
-    if (overflow || !place) // the rescanned tiles are placed by k_csc_fill afterwards
-        hipLaunchKernelGGL(k_emit_compact<false>, g, dim3(kBlock), 0, s, a);
-    else
-        hipLaunchKernelGGL(k_emit_compact<true>, g, dim3(kBlock), 0, s, a);
+    if (pieces_place && !place) { // with the placement of the Sinkhorn pieces in the same launch
+        const int nc = (int)blocks_for((int64_t)a.B * a.N * a.S, kFusedT);
+        hipLaunchKernelGGL(k_emit_compact_place, dim3(nc + 2 * a.B), dim3(kFusedT), 0, s, a, *d, pieces_place, nc);
+    } else if (overflow || !place) { // the rescanned tiles are placed by k_csc_fill afterwards
+        hipLaunchKernelGGL(k_emit_compact<false>, dim3(blocks_for((int64_t)a.B * a.N * a.S, kBlock)), dim3(kBlock), 0,
+                           s, a);
+    } else {
+        hipLaunchKernelGGL(k_emit_compact<true>, dim3(blocks_for((int64_t)a.B * a.N * a.S, kBlock)), dim3(kBlock), 0,
+                           s, a);
+    }
     if (overflow)
         hipLaunchKernelGGL(k_emit<true>, dim3(a.B * a.S * a.owner_blocks), dim3(kBlock), 0, s, a);
 }

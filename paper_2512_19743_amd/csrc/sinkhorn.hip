@@ -722,9 +722,10 @@ bool sinkhorn_bwd_fits(int slots, int64_t max_pairs)
 
 size_t packed_order_words(int B, int slots) { return (size_t)B * slots * kP * kT; }
 
-void launch_pack(const DevPlan &d, int32_t *place, hipStream_t s)
+void launch_pack(const DevPlan &d, int32_t *place, bool placed, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_place, dim3(d.B, 2), dim3(kT), 0, s, d, place);
+    if (!placed)
+        hipLaunchKernelGGL(k_place, dim3(d.B, 2), dim3(kT), 0, s, d, place);
     hipLaunchKernelGGL(k_pack_pairs, dim3(blocks_for(2 * d.nnz, kBlock)), dim3(kBlock), 0, s, d, (const int32_t *)place);
 }
 

@@ -220,6 +220,78 @@ __global__ __launch_bounds__(kBlock) void k_col_softmax(DevPlan d, Params p)
         owner_softmax<false>(d, p, gc, gid % G);
 }
 
+// Column-major view of one sample (blockIdx.x) in one workgroup: every pair
+// takes a slot of its column segment through an LDS counter; the final place
+// of an entry in its segment is its rank by row among the segment's entries
+// (one thread per entry, so long segments do not serialize a lane). Entries
+// are row << 16 | position of the pair in the sample.
+constexpr int kCscT = kSinkLanes;
+
+__device__ __forceinline__ void csc_sample(const DevPlan &d, int b, uint32_t *lds_csc)
+{
+    const int tid = threadIdx.x, N = d.N, M = d.M;
+    int *cp = reinterpret_cast<int *>(lds_csc), *fill = cp + (M + 1);
+    const int lo = d.row_ptr[(size_t)b * N], n = d.row_ptr[(size_t)(b + 1) * N] - lo;
+    uint32_t *ent = reinterpret_cast<uint32_t *>(fill + M);
+    uint16_t *colof = reinterpret_cast<uint16_t *>(ent + n); // column of each slot
+    for (int k = tid; k <= M; k += kCscT)
+        cp[k] = d.col_ptr[(size_t)b * M + k] - lo; // the sample starts at lo in both orders
+    for (int k = tid; k < M; k += kCscT)
+        fill[k] = 0;
+    __syncthreads();
+    constexpr int kBatch = 8; // pairs per thread whose loads are in flight together
+    for (int t0 = 0; t0 < n; t0 += kBatch * kCscT) {
+        int j[kBatch], i[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int t = t0 + u * kCscT + tid;
+            j[u] = t < n ? d.csr_col[lo + t] : 0;
+            i[u] = t < n ? d.csr_row[lo + t] - b * N : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int t = t0 + u * kCscT + tid;
+            if (t < n) {
+                const int q = cp[j[u]] + atomicAdd(&fill[j[u]], 1);
+                ent[q] = (uint32_t)i[u] << 16 | (uint32_t)t;
+                colof[q] = (uint16_t)j[u];
+            }
+        }
+    }
+    __syncthreads();
+    for (int q = tid; q < n; q += kCscT) {
+        const uint32_t e = ent[q];
+        const int j = colof[q], s0 = cp[j], s1 = cp[j + 1];
+        int rank = 0;
+        for (int u = s0; u < s1; ++u)
+            rank += ent[u] < e;
+        d.csc_row[lo + s0 + rank] = (int)(e >> 16);
+        d.csc_perm[lo + s0 + rank] = lo + (int)(e & 0xFFFFu);
+        d.csc_col[lo + s0 + rank] = b * M + j;
+    }
+}
+
+// The column-major view of each sample (first B blocks) and the row softmax
+// (the other blocks, kCscT / G rows each): independent work in one launch, so
+// the row softmax runs on the CUs the per-sample blocks leave free.
+__global__ __launch_bounds__(kCscT) void k_csc_rows(DevPlan d, Params p)
+{
+    extern __shared__ uint32_t lds_csc[];
+    if ((int)blockIdx.x < d.B) {
+        csc_sample(d, blockIdx.x, lds_csc);
+        return;
+    }
+    const int gid = (blockIdx.x - d.B) * kCscT + threadIdx.x;
+    const int r = gid / G;
+    if (r < d.B * d.N)
+        owner_softmax<true>(d, p, r, gid % G);
+}
+
+__host__ inline size_t csc_sample_lds(int M, int64_t max_pairs)
+{
+    return 4 * (2 * (size_t)M + 1) + 6 * (size_t)max_pairs + 16;
+}
+
 // dLoss/dP0 of stored pair t: the Sinkhorn adjoint, or grad_loss * C when
 // there are no Sinkhorn iterations.
 __device__ __forceinline__ double p0bar(const DevPlan &d, int t, double gl)
@@ -434,6 +506,24 @@ __global__ __launch_bounds__(kBlock) void k_bwd_grad_y(DevPlan d, Params p)
 }
 
 } // namespace
+
+bool csc_sample_fits(int N, int M, int64_t max_pairs)
+{
+    return N <= 65536 && max_pairs <= 65536 && csc_sample_lds(M, max_pairs) <= 160 * 1024;
+}
+
+hipError_t launch_csc_and_softmax(const DevPlan &d, const Params &p, int64_t max_pairs, hipStream_t s)
+{
+    const size_t bytes = csc_sample_lds(d.M, max_pairs);
+    hipError_t e = hipFuncSetAttribute((const void *)k_csc_rows, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)bytes);
+    if (e != hipSuccess)
+        return e;
+    const unsigned rows = blocks_for((int64_t)d.B * d.N * G, kCscT);
+    hipLaunchKernelGGL(k_csc_rows, dim3(d.B + rows), dim3(kCscT), bytes, s, d, p);
+    hipLaunchKernelGGL(k_col_softmax, dim3(blocks_for((int64_t)d.B * d.M * G, kBlock)), dim3(kBlock), 0, s, d, p);
+    return hipGetLastError();
+}
 
 void launch_softmax(const DevPlan &d, const Params &p, hipStream_t s)
 {
