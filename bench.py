@@ -39,10 +39,10 @@ OPS_PER_PAIR_DIR = 8
 # one HIP event pair per phase on its stream). Dense phases count VALU
 # operations per point pair; sparse phases count bytes per stored entry of the
 # support (nnz after symmetrization), as the method must move them at least
-# once: emission 16 B, CSR/CSC build 32 B, softmaxes 24 B, Sinkhorn 8 B per
-# entry and half-step forward (+8 B for the loss) and 16 B per entry and
-# half-step in reverse, softmax/temperature adjoint 24 B + distance gradient
-# 8 B.
+# once: emission of the row-major structure 16 B, column-major view 32 B,
+# softmaxes 24 B, Sinkhorn 8 B per entry and half-step forward (+8 B for the
+# loss) and 16 B per entry and half-step in reverse, softmax/temperature
+# adjoint 24 B + distance gradient 8 B.
 def _ops(per_pair):
     return lambda w, pairs, nnz: per_pair * pairs
 
@@ -55,11 +55,13 @@ PHASE_MODEL = {
     "stats": ("alu", _ops(2 * OPS_PER_PAIR_DIR), "VALU ops",
               "k_top2: minimum and second minimum of every row and column"),
     "support": ("alu", _ops(OPS_PER_PAIR_DIR), "VALU ops",
-                "k_emit: radius test of every pair, emission of the candidate support"),
-    "build": ("hbm", _bytes(lambda w: 16 + 32), "bytes", "CSR fill + CSC build"),
-    "softmax": ("hbm", _bytes(lambda w: 24), "bytes", "k_row_softmax + k_col_softmax (Eq. 1, Eq. 2, P0)"),
+                "k_emit: radius test of every pair, counts and staged hits of the candidate support"),
+    "build": ("hbm", _bytes(lambda w: 16), "bytes",
+              "k_emit_compact_place: row-major structure from the staged hits, placement of the Sinkhorn pieces"),
+    "softmax": ("hbm", _bytes(lambda w: 32 + 24), "bytes",
+                "k_csc_rows + k_col_softmax: column-major view, Eq. 1, Eq. 2, P0"),
     "sinkhorn": ("hbm", _bytes(lambda w: 2 * w.n_iter * 8 + 8), "bytes",
-                 "k_sinkhorn_fwd: L Sinkhorn iterations (Eq. 3, Eq. 4) and the loss"),
+                 "k_pack_pairs + k_sinkhorn_fwd: L Sinkhorn iterations (Eq. 3, Eq. 4) and the loss"),
     "bwd_sinkhorn": ("hbm", _bytes(lambda w: 2 * w.n_iter * 16), "bytes",
                      "k_sinkhorn_bwd: reverse Sinkhorn sweeps"),
     "bwd_softmax": ("hbm", _bytes(lambda w: 24 + 8), "bytes",
@@ -72,20 +74,13 @@ PHASE_MODEL = {
 # entry names the source files it was measured on with their SHA-256: once a
 # file changes, traffic is reported as null until measured again.
 TRAFFIC = {
-    "stats": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "01860daa9c746654d974da689bd7408f0cb3934d74685c6b20970025f8c23b0f"},
-              "kernels": ["k_top2"], "bytes_per_launch": 27840037},
-    "support": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "01860daa9c746654d974da689bd7408f0cb3934d74685c6b20970025f8c23b0f"},
-              "kernels": ["k_emit"], "bytes_per_launch": 25438631},
-    "build": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "01860daa9c746654d974da689bd7408f0cb3934d74685c6b20970025f8c23b0f", "paper_2512_19743_amd/csrc/build.hip": "6723dba8905fa6f817b70685fbcc8ca8ac2a9ccb306df467aa05524ef4d4a134"},
-              "kernels": ["k_emit", "k_csc_fill", "k_csc_sort"], "bytes_per_launch": 77945908},
-    "softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "3609b543c9dc952699450f88633f27542562abd386bcd7f0474fa6ab4cd999a4"},
-              "kernels": ["k_row_softmax", "k_col_softmax"], "bytes_per_launch": 69352898},
-    "sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "0e84d29e1b824a91e75f0334a7d28a1b38c78d9f96e8ccff872df1bc31edffe3"},
-              "kernels": ["k_place", "k_pack_pairs", "k_sinkhorn_fwd"], "bytes_per_launch": 71988287},
-    "bwd_sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "0e84d29e1b824a91e75f0334a7d28a1b38c78d9f96e8ccff872df1bc31edffe3"},
-              "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 44354585},
-    "bwd_softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "3609b543c9dc952699450f88633f27542562abd386bcd7f0474fa6ab4cd999a4"},
-              "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 79758875},
+    "stats": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "5eab9277f4b592a91254b4c43afbb9172273f72b15ca77df8a7f3aabf67eb7a2", "paper_2512_19743_amd/csrc/apml_internal.h": "868a1d412a1555396b8735dd5c8effaab8c62b5b739bffc96108f4bbc6dce3cf", "paper_2512_19743_amd/csrc/device_common.h": "ae2b3955e6043d486d001b8a23e72dd6da741ba032fae3475c8169f16e724b13"}, "kernels": ["k_top2"], "bytes_per_launch": 27845861},
+    "support": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "5eab9277f4b592a91254b4c43afbb9172273f72b15ca77df8a7f3aabf67eb7a2", "paper_2512_19743_amd/csrc/apml_internal.h": "868a1d412a1555396b8735dd5c8effaab8c62b5b739bffc96108f4bbc6dce3cf", "paper_2512_19743_amd/csrc/device_common.h": "ae2b3955e6043d486d001b8a23e72dd6da741ba032fae3475c8169f16e724b13"}, "kernels": ["k_emit"], "bytes_per_launch": 37327081},
+    "build": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "5eab9277f4b592a91254b4c43afbb9172273f72b15ca77df8a7f3aabf67eb7a2", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "868a1d412a1555396b8735dd5c8effaab8c62b5b739bffc96108f4bbc6dce3cf", "paper_2512_19743_amd/csrc/device_common.h": "ae2b3955e6043d486d001b8a23e72dd6da741ba032fae3475c8169f16e724b13"}, "kernels": ["k_emit_compact_place"], "bytes_per_launch": 27805105},
+    "softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "1eddfab1e8f062399c35ef907eec6dc7f8222bd4bf2bd5fddbe10d06826aff3b", "paper_2512_19743_amd/csrc/apml_internal.h": "868a1d412a1555396b8735dd5c8effaab8c62b5b739bffc96108f4bbc6dce3cf", "paper_2512_19743_amd/csrc/device_common.h": "ae2b3955e6043d486d001b8a23e72dd6da741ba032fae3475c8169f16e724b13"}, "kernels": ["k_csc_rows", "k_col_softmax"], "bytes_per_launch": 63826073},
+    "sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "419ee3423b65e4e29970514e8a3218dfd2664aa2c81aff2130635c5366aa2317", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "868a1d412a1555396b8735dd5c8effaab8c62b5b739bffc96108f4bbc6dce3cf", "paper_2512_19743_amd/csrc/device_common.h": "ae2b3955e6043d486d001b8a23e72dd6da741ba032fae3475c8169f16e724b13"}, "kernels": ["k_pack_pairs", "k_sinkhorn_fwd"], "bytes_per_launch": 61792421},
+    "bwd_sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "419ee3423b65e4e29970514e8a3218dfd2664aa2c81aff2130635c5366aa2317", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "868a1d412a1555396b8735dd5c8effaab8c62b5b739bffc96108f4bbc6dce3cf", "paper_2512_19743_amd/csrc/device_common.h": "ae2b3955e6043d486d001b8a23e72dd6da741ba032fae3475c8169f16e724b13"}, "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 26050889},
+    "bwd_softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "1eddfab1e8f062399c35ef907eec6dc7f8222bd4bf2bd5fddbe10d06826aff3b", "paper_2512_19743_amd/csrc/apml_internal.h": "868a1d412a1555396b8735dd5c8effaab8c62b5b739bffc96108f4bbc6dce3cf", "paper_2512_19743_amd/csrc/device_common.h": "ae2b3955e6043d486d001b8a23e72dd6da741ba032fae3475c8169f16e724b13"}, "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 73459591},
 }
 
 

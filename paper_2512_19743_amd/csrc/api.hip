@@ -479,7 +479,8 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     // the counting pass keeps the first hits of every (row, chunk); offsets
     // within a chunk are 16-bit
     if (ea.chunk <= 65536) {
-        ea.stage = dense_tmp.get<uint16_t>((size_t)BN * ea.S * kStage);
+        ea.kst = stage_slots(ea.S);
+        ea.stage = dense_tmp.get<uint16_t>((size_t)BN * ea.S * ea.kst);
         const size_t tiles = (size_t)B * ea.S * ea.owner_blocks;
         ea.spill = dense_tmp.get<uint32_t>(tiles * kTileSpill);
         ea.spill_n = dense_tmp.get<int32_t>(tiles);

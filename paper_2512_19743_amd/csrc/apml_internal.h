@@ -58,12 +58,15 @@ void launch_top2(const ScanDir &rows, const ScanDir &cols, int B, hipStream_t s)
 void launch_finalize(const FinalizeDir &rows, const FinalizeDir &cols, int B, const Params &p,
                      Counters *ctr, hipStream_t s);
 
-// The counting pass of the support scan keeps the first kStage hits of every
-// (row, chunk) and the further hits of a tile (kBlock rows, one chunk) in a
-// tile list of kTileSpill entries; only when a tile list overflows does the
-// writing pass scan that tile again.
+// The counting pass of the support scan keeps the first kst hits of every
+// (row, chunk) (kst = stage_slots(S), at most kStage: fewer when the columns
+// are cut into many chunks, each of which then holds few of a row's hits) and
+// the further hits of a tile (kBlock rows, one chunk) in a tile list of
+// kTileSpill entries; only when a tile list overflows does the writing pass
+// scan that tile again.
 constexpr int kStage = 16;
 constexpr int kTileSpill = 512;
+inline int stage_slots(int S) { return S >= 32 ? 2 : S >= 16 ? 4 : S >= 8 ? 8 : kStage; }
 
 struct EmitArgs {
     const float *x;      // [B, N, 3]
@@ -72,7 +75,8 @@ struct EmitArgs {
     int B, N, M, S, chunk, owner_blocks;
     int32_t *cnt;        // [B*N][S] stored pairs per (row, column chunk)
     int32_t *col_cnt;    // [B*M] stored pairs per column
-    uint16_t *stage;     // [B*N][S][kStage] column offsets within the chunk of the first hits, or NULL
+    uint16_t *stage;     // [B*N][S][kst] column offsets within the chunk of the first hits, or NULL
+    int kst;             // staged hits per (row, chunk)
     uint32_t *spill;     // [tiles][kTileSpill]: further hits, row within the tile << 16 | offset in the chunk
     int32_t *spill_n;    // [tiles]: entries of the tile list (more than kTileSpill: overflowed)
     Counters *ctr;

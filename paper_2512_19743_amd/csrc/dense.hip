@@ -197,7 +197,7 @@ template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs 
     const uint32_t keep = valid ? ~0u : 0u; // a lane without a row ignores the columns' balls too
     if (!WRITE) {
         int32_t *col_cnt = a.col_cnt + (size_t)b * a.M;
-        uint16_t *stage = a.stage ? a.stage + ((size_t)row * a.S + ch) * kStage : nullptr;
+        uint16_t *stage = a.stage ? a.stage + ((size_t)row * a.S + ch) * a.kst : nullptr;
         uint32_t *spill = a.stage ? a.spill + (size_t)t * kTileSpill : nullptr;
         if (threadIdx.x == 0)
             n_spill = 0;
@@ -206,7 +206,7 @@ template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs 
         for_each_hit(ax, ay, az, E, q, j0, j1, keep, [&](int j) {
             atomicAdd(&col_cnt[j], 1);
             if (stage) {
-                if (cnt < kStage) {
+                if (cnt < a.kst) {
                     stage[cnt] = (uint16_t)(j - j0);
                 } else { // in increasing j for each row
                     const int k = atomicAdd(&n_spill, 1);
@@ -242,7 +242,7 @@ template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs 
 
 // CSR from the staged hits: one thread per (row, chunk) writes its hits at
 // the row's offset plus the hits of the row's earlier chunks; hits beyond
-// kStage come from the tile list, in list order (increasing column). With
+// kst come from the tile list, in list order (increasing column). With
 // PLACE, each pair also takes a slot in its column segment (k_csc_sort then
 // fixes the order inside the segment).
 template <bool PLACE>
@@ -273,17 +273,17 @@ template <bool PLACE> __device__ __forceinline__ void emit_compact_thread(const 
     const int n_spill = a.spill_n[t];
     if (n_spill > kTileSpill) // the writing pass rescans this tile
         return;
-    const uint16_t *st = a.stage + (size_t)g * kStage;
+    const uint16_t *st = a.stage + (size_t)g * a.kst;
     const int j0 = ch * a.chunk, gc0 = b * a.M + j0;
-    const int ns = min(n, kStage);
+    const int ns = min(n, a.kst);
 #pragma unroll
     for (int k = 0; k < kStage; ++k) // fixed trip count: the pairs' loads and atomics overlap
         if (k < ns)
             emit_pair<PLACE>(a, pos + k, row, i, gc0 + st[k], j0 + st[k]);
-    if (n > kStage) {
+    if (n > a.kst) {
         const uint32_t *sp = a.spill + (size_t)t * kTileSpill;
         const uint32_t me = (uint32_t)(i % kBlock);
-        int k = kStage;
+        int k = a.kst;
         for (int u = 0; u < n_spill; ++u)
             if (sp[u] >> 16 == me) {
                 const int jj = (int)(sp[u] & 0xFFFFu);
