@@ -652,6 +652,10 @@ apml_status apml_backward(apml_plan *plan, const float *x, const float *y, const
     dv.grad_y = grad_y;
     dv.adj = tmp.get<double>(plan->stored);
     dv.cbar = tmp.get<double>(plan->stored);
+    if (dv.L > 0 && !plan->sink_bwd) {
+        dv.rz = tmp.get<double>(plan->stored);
+        dv.kz = tmp.get<double>(plan->stored);
+    }
     if (tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (backward)");
     {

@@ -574,8 +574,14 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan 
     }
 }
 
-// per-iteration fallback (any N, M): one launch per sweep
+// per-iteration kernels (any N, M): one launch per sweep
 // ---------------------------------------------------------------------------
+//
+// kSG lanes per owner (row or column); each lane issues the loads of kSB of
+// its pairs together before using them. Sums are per lane in pair order,
+// then a butterfly over the group, so results do not depend on scheduling.
+constexpr int kSG = 4;
+constexpr int kSB = 8;
 
 __global__ __launch_bounds__(kBlock) void k_fill_ones(double *a, int n)
 {
@@ -584,52 +590,91 @@ __global__ __launch_bounds__(kBlock) void k_fill_ones(double *a, int n)
         a[k] = 1.0;
 }
 
-__global__ __launch_bounds__(kBlock) void k_sink_col(DevPlan d, int l, double eps)
+// Sum over owner o's pairs k = lg, lg + kSG, ... of f(k, position) with the
+// loads of kSB pairs in flight at once.
+template <class Load, class Use>
+__device__ __forceinline__ double owner_sum(int n, int lg, Load load, Use use)
 {
-    const int gc = blockIdx.x * kBlock + threadIdx.x;
-    if (gc >= d.B * d.M)
-        return;
-    const int b = gc / d.M;
-    const size_t BN = (size_t)d.B * d.N, BM = (size_t)d.B * d.M;
-    const double *alpha_prev = d.alpha + (size_t)(l - 1) * BN + (size_t)b * d.N;
     double acc = 0.0;
-    for (int q = d.col_ptr[gc]; q < d.col_ptr[gc + 1]; ++q)
-        acc += (double)d.p0c[q] * alpha_prev[d.csc_row[q]];
-    const double bprev = d.beta[(size_t)(l - 1) * BM + gc];
-    const double den = bprev * acc + eps;
-    d.beta[(size_t)l * BM + gc] = bprev / den;
-    d.sden[(size_t)(l - 1) * BM + gc] = den;
+    for (int k0 = lg; k0 < n; k0 += kSG * kSB) {
+        decltype(load(0)) v[kSB];
+#pragma unroll
+        for (int u = 0; u < kSB; ++u)
+            v[u] = load(k0 + kSG * u < n ? k0 + kSG * u : -1);
+#pragma unroll
+        for (int u = 0; u < kSB; ++u)
+            if (k0 + kSG * u < n)
+                acc += use(v[u]);
+    }
+    return group_sum<kSG>(acc);
 }
 
-__global__ __launch_bounds__(kBlock) void k_sink_row(DevPlan d, int l, double eps)
+// Column step (Eq. 3, COL) or row step (Eq. 4) of iteration l for all owners.
+template <bool COL> __global__ __launch_bounds__(kBlock) void k_sink_step(DevPlan d, int l, double eps)
 {
-    const int r = blockIdx.x * kBlock + threadIdx.x;
-    if (r >= d.B * d.N)
+    const int gid = blockIdx.x * kBlock + threadIdx.x;
+    const int o = gid / kSG, lg = gid % kSG;
+    const int n_own = COL ? d.M : d.N, n_oth = COL ? d.N : d.M;
+    if (o >= d.B * n_own)
         return;
-    const int b = r / d.N;
+    const int b = o / n_own;
     const size_t BN = (size_t)d.B * d.N, BM = (size_t)d.B * d.M;
-    const double *beta_cur = d.beta + (size_t)l * BM + (size_t)b * d.M;
-    double acc = 0.0;
-    for (int t = d.row_ptr[r]; t < d.row_ptr[r + 1]; ++t)
-        acc += (double)d.p0r[t] * beta_cur[d.csr_col[t]];
-    const double aprev = d.alpha[(size_t)(l - 1) * BN + r];
-    const double den = aprev * acc + eps;
-    d.alpha[(size_t)l * BN + r] = aprev / den;
-    d.rden[(size_t)(l - 1) * BN + r] = den;
+    const int32_t *ptr = COL ? d.col_ptr : d.row_ptr;
+    const int32_t *idx = COL ? d.csc_row : d.csr_col;
+    const float *p0 = COL ? d.p0c : d.p0r;
+    // the other side's scalings: alpha^(l-1) for columns, beta^l for rows
+    const double *oth = (COL ? d.alpha + (size_t)(l - 1) * BN : d.beta + (size_t)l * BM) + (size_t)b * n_oth;
+    const int s0 = ptr[o], n = ptr[o + 1] - s0;
+    struct V {
+        float p;
+        double x;
+    };
+    const double acc = owner_sum(n, lg,
+                                 [&](int k) {
+                                     V v{0.0f, 0.0};
+                                     if (k >= 0) {
+                                         v.p = p0[s0 + k];
+                                         v.x = oth[idx[s0 + k]];
+                                     }
+                                     return v;
+                                 },
+                                 [&](const V &v) { return (double)v.p * v.x; });
+    if (lg == 0) {
+        double *cur = COL ? d.beta : d.alpha, *den_out = COL ? d.sden : d.rden;
+        const size_t BO = COL ? BM : BN;
+        const double prev = cur[(size_t)(l - 1) * BO + o];
+        const double den = prev * acc + eps;
+        cur[(size_t)l * BO + o] = prev / den;
+        den_out[(size_t)(l - 1) * BO + o] = den;
+    }
 }
 
 __global__ __launch_bounds__(kBlock) void k_loss_rows(DevPlan d, double *loss_rows)
 {
-    const int r = blockIdx.x * kBlock + threadIdx.x;
+    const int gid = blockIdx.x * kBlock + threadIdx.x;
+    const int r = gid / kSG, lg = gid % kSG;
     if (r >= d.B * d.N)
         return;
     const int b = r / d.N;
     const size_t BN = (size_t)d.B * d.N, BM = (size_t)d.B * d.M;
     const double *beta = d.beta + (size_t)d.L * BM + (size_t)b * d.M;
-    double acc = 0.0;
-    for (int t = d.row_ptr[r]; t < d.row_ptr[r + 1]; ++t)
-        acc += (double)d.p0r[t] * beta[d.csr_col[t]] * d.cost[t];
-    loss_rows[r] = d.alpha[(size_t)d.L * BN + r] * acc;
+    const int t0 = d.row_ptr[r], n = d.row_ptr[r + 1] - t0;
+    struct V {
+        float p;
+        double bc;
+    };
+    const double acc = owner_sum(n, lg,
+                                 [&](int k) {
+                                     V v{0.0f, 0.0};
+                                     if (k >= 0) {
+                                         v.p = d.p0r[t0 + k];
+                                         v.bc = beta[d.csr_col[t0 + k]] * d.cost[t0 + k];
+                                     }
+                                     return v;
+                                 },
+                                 [&](const V &v) { return (double)v.p * v.bc; });
+    if (lg == 0)
+        loss_rows[r] = d.alpha[(size_t)d.L * BN + r] * acc;
 }
 
 __global__ __launch_bounds__(kBlock) void k_loss_reduce(DevPlan d, const double *loss_rows)
@@ -651,48 +696,147 @@ __global__ __launch_bounds__(kBlock) void k_loss_reduce(DevPlan d, const double 
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_bwd_sink_row(DevPlan d, int l)
+// Reverse sweeps, one launch per half-step. The adjoint is kept twice in
+// double precision, in row order (rz) and in column order (kz), in the
+// scaled form of the per-sample kernel (adjoint * alpha^l before a row
+// phase, * beta^l before a column phase), and each copy is brought up to
+// date in its own order, so no launch reads or writes pairs out of order:
+//   row launch l:    rz <- column update of iteration l+1 (l < L), then the
+//                    row update of iteration l; row sums; row values
+//                    X_i = alpha^l_i, Y_i = d_i alpha^l_i into xyr
+//   column launch l: kz <- row update of iteration l, then the column update
+//                    of iteration l; column sums; column values into xyc
+// where the row update of iteration l is z' = (z / alpha^l_i) X_j - Y_j with
+// the column values published last, and the column update z' = (z / beta^l_j)
+// X_i - Y_i with the row values of iteration l.
+__device__ __forceinline__ float rinv(double v) { return __builtin_amdgcn_rcpf((float)v); }
+
+__global__ __launch_bounds__(kBlock) void k_bwd_init(DevPlan d)
 {
-    const int r = blockIdx.x * kBlock + threadIdx.x;
+    const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const size_t BN = (size_t)d.B * d.N, BM = (size_t)d.B * d.M;
+    if (g < d.nnz) { // row order: grad_loss * C, times alpha^L_i
+        const int r = d.csr_row[g], b = r / d.N;
+        d.rz[g] = d.grad_loss[b] * d.cost[g] * d.alpha[(size_t)d.L * BN + r];
+        // column order: the same pair through the permutation
+        const int t = d.csc_perm[g], rr = d.csr_row[t], bb = rr / d.N;
+        d.kz[g] = d.grad_loss[bb] * d.cost[t] * d.alpha[(size_t)d.L * BN + rr];
+    }
+    if (g < (int64_t)BM) { // no pending column update before the last iteration
+        float2 *xyc = reinterpret_cast<float2 *>(d.evec);
+        xyc[g] = make_float2((float)d.beta[(size_t)d.L * BM + g], 0.0f);
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void k_bwd_rows(DevPlan d, int l)
+{
+    const int gid = blockIdx.x * kBlock + threadIdx.x;
+    const int r = gid / kSG, lg = gid % kSG;
     if (r >= d.B * d.N)
         return;
     const int b = r / d.N;
     const size_t BN = (size_t)d.B * d.N, BM = (size_t)d.B * d.M;
+    float2 *xyr = reinterpret_cast<float2 *>(d.dvec);
+    const float2 *xyc = reinterpret_cast<const float2 *>(d.evec) + (size_t)b * d.M;
+    const double *beta_next = d.beta + (size_t)(l + 1) * BM + (size_t)b * d.M; // iteration l+1 (l < L)
+    const bool pending = l < d.L;
+    const float2 mine = pending ? xyr[r] : make_float2(0.0f, 0.0f); // row values of iteration l+1
     const double al = d.alpha[(size_t)l * BN + r];
-    const double *bl = d.beta + (size_t)l * BM + (size_t)b * d.M;
-    const bool last = l == d.L;
-    const double gl = d.grad_loss[b];
-    const int t0 = d.row_ptr[r], t1 = d.row_ptr[r + 1];
-    double dsum = 0.0;
-    for (int t = t0; t < t1; ++t) {
-        const double ub = last ? gl * d.cost[t] : d.adj[t];
-        dsum += ub * (al * (double)d.p0r[t] * bl[d.csr_col[t]]);
-    }
-    const double den = d.rden[(size_t)(l - 1) * BN + r];
-    for (int t = t0; t < t1; ++t) {
-        const double ub = last ? gl * d.cost[t] : d.adj[t];
-        d.adj[t] = (ub - dsum) / den;
+    const double inv_a = (double)rinv(al);
+    const int t0 = d.row_ptr[r], n = d.row_ptr[r + 1] - t0;
+    struct V {
+        double z;
+        float p;
+        int k;
+        float ib;
+        float2 c;
+    };
+    const double acc = owner_sum(n, lg,
+                                 [&](int k) {
+                                     V v{0.0, 0.0f, k, 1.0f, make_float2(0.0f, 0.0f)};
+                                     if (k >= 0) {
+                                         const int j = d.csr_col[t0 + k];
+                                         v.z = d.rz[t0 + k];
+                                         v.p = d.p0r[t0 + k];
+                                         v.ib = pending ? rinv(beta_next[j]) : 1.0f;
+                                         v.c = xyc[j];
+                                     }
+                                     return v;
+                                 },
+                                 [&](const V &v) {
+                                     double z = v.z;
+                                     if (pending)
+                                         z = __builtin_fma(z * (double)v.ib, (double)mine.x, -(double)mine.y);
+                                     z = __builtin_fma(z * inv_a, (double)v.c.x, -(double)v.c.y);
+                                     d.rz[t0 + v.k] = z;
+                                     return z * (double)v.p;
+                                 });
+    if (lg == 0) { // adjoint of Eq. 4: d_i = alpha^l_i * sum
+        const double dsum = al * acc;
+        xyr[r] = make_float2((float)al, (float)(dsum * al));
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_bwd_sink_col(DevPlan d, int l)
+__global__ __launch_bounds__(kBlock) void k_bwd_cols(DevPlan d, int l)
 {
-    const int gc = blockIdx.x * kBlock + threadIdx.x;
+    const int gid = blockIdx.x * kBlock + threadIdx.x;
+    const int gc = gid / kSG, lg = gid % kSG;
     if (gc >= d.B * d.M)
         return;
     const int b = gc / d.M;
     const size_t BN = (size_t)d.B * d.N, BM = (size_t)d.B * d.M;
-    const double *ap = d.alpha + (size_t)(l - 1) * BN + (size_t)b * d.N;
+    const float2 *xyr = reinterpret_cast<const float2 *>(d.dvec) + (size_t)b * d.N;
+    float2 *xyc = reinterpret_cast<float2 *>(d.evec);
+    const double *alpha_l = d.alpha + (size_t)l * BN + (size_t)b * d.N;
+    const float2 mine = xyc[gc]; // column values published last
     const double bl = d.beta[(size_t)l * BM + gc];
-    const int s0 = d.col_ptr[gc], s1 = d.col_ptr[gc + 1];
-    double e = 0.0;
-    for (int q = s0; q < s1; ++q)
-        e += d.adj[d.csc_perm[q]] * (ap[d.csc_row[q]] * (double)d.p0c[q] * bl);
-    const double den = d.sden[(size_t)(l - 1) * BM + gc];
-    for (int q = s0; q < s1; ++q) {
-        const int t = d.csc_perm[q];
-        d.adj[t] = (d.adj[t] - e) / den;
+    const double inv_b = (double)rinv(bl);
+    const int s0 = d.col_ptr[gc], n = d.col_ptr[gc + 1] - s0;
+    struct V {
+        double z;
+        float p;
+        int k;
+        float ia;
+        float2 rw;
+    };
+    const double acc = owner_sum(n, lg,
+                                 [&](int k) {
+                                     V v{0.0, 0.0f, k, 1.0f, make_float2(0.0f, 0.0f)};
+                                     if (k >= 0) {
+                                         const int i = d.csc_row[s0 + k];
+                                         v.z = d.kz[s0 + k];
+                                         v.p = d.p0c[s0 + k];
+                                         v.ia = rinv(alpha_l[i]);
+                                         v.rw = xyr[i];
+                                     }
+                                     return v;
+                                 },
+                                 [&](const V &v) {
+                                     double z = __builtin_fma(v.z * (double)v.ia, (double)mine.x, -(double)mine.y);
+                                     z = __builtin_fma(z * inv_b, (double)v.rw.x, -(double)v.rw.y);
+                                     d.kz[s0 + v.k] = z;
+                                     return z * (double)v.p;
+                                 });
+    if (lg == 0) { // adjoint of Eq. 3: e_j = beta^l_j * sum
+        const double esum = bl * acc;
+        xyc[gc] = make_float2((float)bl, (float)(esum * bl));
     }
+}
+
+// dLoss/dP0 in row order: the column update of iteration 1, then the row
+// update of iteration 0 (alpha^0 = 1).
+__global__ __launch_bounds__(kBlock) void k_bwd_final(DevPlan d)
+{
+    const int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (t >= d.nnz)
+        return;
+    const size_t BM = (size_t)d.B * d.M;
+    const int r = d.csr_row[t], b = r / d.N, j = d.csr_col[t];
+    const float2 rw = reinterpret_cast<const float2 *>(d.dvec)[r];
+    const float2 c = reinterpret_cast<const float2 *>(d.evec)[(size_t)b * d.M + j];
+    double z = __builtin_fma(d.rz[t] * (double)rinv(d.beta[BM + (size_t)b * d.M + j]), (double)rw.x,
+                             -(double)rw.y);
+    d.adj[t] = z * (double)c.x - (double)c.y;
 }
 
 } // namespace
@@ -769,21 +913,25 @@ void launch_sinkhorn_fwd_steps(const DevPlan &d, double eps, hipStream_t s)
     hipLaunchKernelGGL(k_fill_ones, dim3(blocks_for(BN, kBlock)), dim3(kBlock), 0, s, d.alpha, BN);
     hipLaunchKernelGGL(k_fill_ones, dim3(blocks_for(BM, kBlock)), dim3(kBlock), 0, s, d.beta, BM);
     for (int l = 1; l <= d.L; ++l) {
-        hipLaunchKernelGGL(k_sink_col, dim3(blocks_for(BM, kBlock)), dim3(kBlock), 0, s, d, l, eps);
-        hipLaunchKernelGGL(k_sink_row, dim3(blocks_for(BN, kBlock)), dim3(kBlock), 0, s, d, l, eps);
+        hipLaunchKernelGGL(k_sink_step<true>, dim3(blocks_for((int64_t)BM * kSG, kBlock)), dim3(kBlock), 0, s, d, l,
+                           eps);
+        hipLaunchKernelGGL(k_sink_step<false>, dim3(blocks_for((int64_t)BN * kSG, kBlock)), dim3(kBlock), 0, s, d, l,
+                           eps);
     }
     // the backward scratch is free during the forward pass: use it for the row losses
-    hipLaunchKernelGGL(k_loss_rows, dim3(blocks_for(BN, kBlock)), dim3(kBlock), 0, s, d, d.dvec);
+    hipLaunchKernelGGL(k_loss_rows, dim3(blocks_for((int64_t)BN * kSG, kBlock)), dim3(kBlock), 0, s, d, d.dvec);
     hipLaunchKernelGGL(k_loss_reduce, dim3(d.B), dim3(kBlock), 0, s, d, (const double *)d.dvec);
 }
 
 void launch_sinkhorn_bwd_steps(const DevPlan &d, hipStream_t s)
 {
     const int BN = d.B * d.N, BM = d.B * d.M;
+    hipLaunchKernelGGL(k_bwd_init, dim3(blocks_for(std::max<int64_t>(d.nnz, BM), kBlock)), dim3(kBlock), 0, s, d);
     for (int l = d.L; l >= 1; --l) {
-        hipLaunchKernelGGL(k_bwd_sink_row, dim3(blocks_for(BN, kBlock)), dim3(kBlock), 0, s, d, l);
-        hipLaunchKernelGGL(k_bwd_sink_col, dim3(blocks_for(BM, kBlock)), dim3(kBlock), 0, s, d, l);
+        hipLaunchKernelGGL(k_bwd_rows, dim3(blocks_for((int64_t)BN * kSG, kBlock)), dim3(kBlock), 0, s, d, l);
+        hipLaunchKernelGGL(k_bwd_cols, dim3(blocks_for((int64_t)BM * kSG, kBlock)), dim3(kBlock), 0, s, d, l);
     }
+    hipLaunchKernelGGL(k_bwd_final, dim3(blocks_for(d.nnz, kBlock)), dim3(kBlock), 0, s, d);
 }
 
 } // namespace apml
