@@ -225,7 +225,9 @@ def main():
     # support size of this workload (diagnostic, outside the timed region)
     loss, plan = apml.apml_forward(x, y, prm)
     nnz = plan.nnz()
-    stored = plan.info().stored_pairs
+    info = plan.info()
+    stored = info.stored_pairs
+    scanned = (int(info.scanned_min), int(info.scanned_support))
     plan.close()
 
     # timed region: K steps, library profiling off
@@ -297,7 +299,9 @@ def main():
         "roofline": roofline,
         "peak_hbm_mb": mem["peak_in_use"] / 1e6,
         "support": {"nnz_total": nnz_total, "nnz_per_row": nnz_total / (w.B * w.N),
-                    "stored_pairs": int(stored)},
+                    "stored_pairs": int(stored),
+                    "scanned_fraction_min": scanned[0] / (2 * w.B * w.N * w.M),
+                    "scanned_fraction_support": scanned[1] / (w.B * w.N * w.M)},
         "phases_ms_per_step": {k: v[0] / args.steps for k, v in phases.items()},
         "kernels": kernels,
         "wall_ms_per_step": wall * 1e3 / args.steps,

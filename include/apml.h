@@ -60,6 +60,15 @@ typedef void *apml_stream;
  * tau = 1e-8, L_iter = 10, eps_stab = 1e-8 (Sec. III-E, Sec. IV-C) and, where
  * the paper gives no value, p_min = 0.8, delta = 1e-8, eps_gap = 1e-6,
  * eps_dist = 1e-12. */
+/* How the dense scans (the minimum and second minimum of every row and
+ * column, Sec. III-A; the candidate support, Sec. III-B) visit the pairs.
+ * Both modes give identical results. FULL evaluates every pair. SKIP sorts
+ * both clouds along a space-filling curve and skips every run of 32 points
+ * whose bounding box is provably beyond the distance that can still matter
+ * to the owners being scanned; it pays off for large samples. AUTO takes SKIP
+ * when N*M >= 2^24. */
+typedef enum { APML_SCAN_AUTO = 0, APML_SCAN_FULL = 1, APML_SCAN_SKIP = 2 } apml_scan_mode;
+
 typedef struct apml_params {
     uint32_t struct_size; /* sizeof(apml_params), for forward compatibility */
     int32_t n_iter;       /* L_iter >= 0: Sinkhorn iterations (Alg. 1) */
@@ -69,6 +78,8 @@ typedef struct apml_params {
     double delta;         /* >= 0, gap offset g = c2 + delta (Sec. III-A) */
     double eps_gap;       /* > 0, gap clamp max(gap, eps_gap) (Sec. III-D) */
     double eps_dist;      /* >= 0, added to ||x - y|| in the gradient only (Eq. 5) */
+    int32_t dense_scan;   /* apml_scan_mode: how the two dense scans visit the pairs */
+    int32_t reserved;     /* 0 */
 } apml_params;
 
 /* Fills *p with the defaults above (p must not be NULL). */
@@ -117,11 +128,16 @@ apml_status apml_plan_destroy(apml_plan *plan);
 
 /* Sizes of a plan. stored_pairs counts every stored pair, including pairs kept
  * only as the minimum or second minimum of a row or column (they carry zero
- * mass). bytes is the device memory the plan holds. */
+ * mass). bytes is the device memory the plan holds. scanned_min and
+ * scanned_support count the pairs whose distance the two dense scans of the
+ * forward evaluated (the minimum scan over both directions, the support scan
+ * over rows); the scans skip pairs that provably cannot matter, so these stay
+ * below 2*B*N*M and B*N*M. */
 typedef struct apml_plan_info {
     int32_t B, N, M, n_iter;
     int64_t stored_pairs;
     int64_t bytes;
+    int64_t scanned_min, scanned_support;
 } apml_plan_info;
 apml_status apml_plan_get_info(const apml_plan *plan, apml_plan_info *info);
 

@@ -40,12 +40,15 @@ class apml_params(ctypes.Structure):
         ("delta", ctypes.c_double),
         ("eps_gap", ctypes.c_double),
         ("eps_dist", ctypes.c_double),
+        ("dense_scan", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
     ]
 
 
 class apml_plan_info(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("N", ctypes.c_int32), ("M", ctypes.c_int32),
-                ("n_iter", ctypes.c_int32), ("stored_pairs", ctypes.c_int64), ("bytes", ctypes.c_int64)]
+                ("n_iter", ctypes.c_int32), ("stored_pairs", ctypes.c_int64), ("bytes", ctypes.c_int64),
+                ("scanned_min", ctypes.c_int64), ("scanned_support", ctypes.c_int64)]
 
 
 class apml_memory_stats(ctypes.Structure):

@@ -259,6 +259,8 @@ struct apml_plan {
     int device = 0;
     hipStream_t stream = nullptr;
     int64_t stored = 0;     // stored pairs
+    int64_t scanned[2] = {0, 0}; // pairs evaluated by the two dense scans
+    bool skipping = false;  // the dense scans skipped pairs (large samples)
     int64_t max_sample = 0; // stored pairs of the largest sample
     bool sink_fwd = false;  // per-sample Sinkhorn kernels take this plan (forward)
     bool sink_bwd = false;  // and the reverse sweeps
@@ -291,6 +293,8 @@ apml_status validate(const float *x, const float *y, int32_t B, int32_t N, int32
         !std::isfinite(p.delta) || !std::isfinite(p.eps_gap) || !std::isfinite(p.eps_stab) ||
         !std::isfinite(p.eps_dist))
         return fail(APML_ERR_INVALID_ARG, "need delta >= 0, eps_gap > 0, eps_stab >= 0, eps_dist >= 0, all finite");
+    if (p.dense_scan < APML_SCAN_AUTO || p.dense_scan > APML_SCAN_SKIP)
+        return fail(APML_ERR_INVALID_ARG, "dense_scan must be APML_SCAN_AUTO, APML_SCAN_FULL or APML_SCAN_SKIP");
     return APML_OK;
 }
 
@@ -299,8 +303,6 @@ double log_ratio(int K, double p) { return -std::log((1.0 - p) / ((double)(K - 1
 
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
-// Chunks of the broadcast range so that a dense scan has about 8 waves per
-// SIMD on 256 CUs, each chunk at least 512 points long.
 // Waits for the stream by polling: the forward's one synchronisation sits
 // on the critical path, and a blocking wait adds the wake-up latency.
 hipError_t wait_for(hipStream_t s)
@@ -312,6 +314,8 @@ hipError_t wait_for(hipStream_t s)
     }
 }
 
+// Chunks of the broadcast range so that a full dense scan has about 8 waves
+// per SIMD on 256 CUs, each chunk at least 512 points long.
 void choose_chunks(int B, int n_own, int n_bc, int *S, int *chunk, int min_chunk = 512)
 {
     const int64_t waves = (int64_t)B * ceil_div(n_own, 64);
@@ -322,6 +326,19 @@ void choose_chunks(int B, int n_own, int n_bc, int *S, int *chunk, int min_chunk
     len = ceil_div(len, kUnroll) * kUnroll;
     *chunk = len;
     *S = ceil_div(n_bc, len);
+}
+
+// The skipping scans pay off once a sample has many pairs per stored pair;
+// below about 2^24 pairs per sample the full scans are faster.
+constexpr int64_t kSkipMinPairs = int64_t(1) << 24;
+
+bool use_skipping_scans(const apml_params &p, int N, int M)
+{
+    if (p.dense_scan == APML_SCAN_FULL)
+        return false;
+    if (p.dense_scan == APML_SCAN_SKIP)
+        return true;
+    return (int64_t)N * M >= kSkipMinPairs;
 }
 
 } // namespace
@@ -340,6 +357,8 @@ void apml_params_default(apml_params *p)
     p->delta = 1e-8;
     p->eps_gap = 1e-6;
     p->eps_dist = 1e-12;
+    p->dense_scan = APML_SCAN_AUTO;
+    p->reserved = 0;
 }
 
 apml_status apml_plan_destroy(apml_plan *plan)
@@ -422,68 +441,156 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     dv.loss = loss;
 
     // ---- dense scan 1: minima -------------------------------------------
-    ScanDir rows{}, cols{};
-    rows.own = x;
-    rows.bcast = y;
-    rows.n_own = N;
-    rows.n_bc = M;
-    choose_chunks(B, N, M, &rows.S, &rows.chunk);
-    rows.owner_blocks = ceil_div(N, kBlock);
-    rows.tiles = B * rows.S * rows.owner_blocks;
-    cols.own = y;
-    cols.bcast = x;
-    cols.n_own = M;
-    cols.n_bc = N;
-    choose_chunks(B, M, N, &cols.S, &cols.chunk);
-    cols.owner_blocks = ceil_div(M, kBlock);
-    cols.tiles = B * cols.S * cols.owner_blocks;
-    rows.partial = dense_tmp.get<float2>((size_t)rows.S * BN);
-    cols.partial = dense_tmp.get<float2>((size_t)cols.S * BM);
+    // Large samples take the skipping scans over spatially sorted clouds
+    // (cull.hip), small ones the full scans (dense.hip).
+    const bool skip = use_skipping_scans(prm, N, M);
+    plan->skipping = skip;
     dv.m12_row = keep.get<float2>(BN);
     dv.m12_col = keep.get<float2>(BM);
-    float *E_row = dense_tmp.get<float>(BN);
-    float4 *ypack = dense_tmp.get<float4>(BM);
     dv.ctr = keep.get<Counters>(1);
     BuildArgs ba{};
     int32_t *col_cnt = tmp.get<int32_t>(BM); // stored pairs per column, counted by the emission
     ba.col_fill = tmp.get<int32_t>(BM);
     dv.row_ptr = keep.get<int32_t>((size_t)BN + 1);
     dv.col_ptr = keep.get<int32_t>((size_t)BM + 1);
-    if (tmp.failed || dense_tmp.failed || keep.failed)
-        return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (statistics)");
-
-    {
-        PhaseTimer pt(PH_STATS, s);
-        launch_top2(rows, cols, B, s);
-        HIP_TRY(hipGetLastError());
-        pt.stop();
-    }
-    FinalizeDir fr{rows.partial, x, dv.m12_row, E_row, nullptr, nullptr, nullptr, N, rows.S, kp.lk_row};
-    FinalizeDir fc{cols.partial, y, dv.m12_col, nullptr, ypack, col_cnt, ba.col_fill, M, cols.S, kp.lk_col};
-    launch_finalize(fr, fc, B, kp, dv.ctr, s); // also clears the counters
-    HIP_TRY(hipGetLastError());
-
-    // ---- dense scan 2: candidate support ---------------------------------
+    // full scans
+    ScanDir rows{}, cols{};
     EmitArgs ea{};
-    ea.x = x;
-    ea.ypack = ypack;
-    ea.E_row = E_row;
-    ea.B = B;
-    ea.N = N;
-    ea.M = M;
-    ea.owner_blocks = rows.owner_blocks;
-    choose_chunks(B, N, M, &ea.S, &ea.chunk, 256);
-    ea.cnt = dense_tmp.get<int32_t>((size_t)BN * ea.S);
-    ea.col_cnt = col_cnt; // cleared by the finalize kernel
-    ea.ctr = dv.ctr;
-    // the counting pass keeps the first hits of every (row, chunk); offsets
-    // within a chunk are 16-bit
-    if (ea.chunk <= 65536) {
-        ea.kst = stage_slots(ea.S);
-        ea.stage = dense_tmp.get<uint16_t>((size_t)BN * ea.S * ea.kst);
-        const size_t tiles = (size_t)B * ea.S * ea.owner_blocks;
-        ea.spill = dense_tmp.get<uint32_t>(tiles * kTileSpill);
-        ea.spill_n = dense_tmp.get<int32_t>(tiles);
+    // skipping scans
+    SpatialArgs sa{};
+    CullDir crows{}, ccols{};
+    CullEmitArgs ca{};
+    int32_t *cnt = nullptr; // stored pairs per row (per (row, chunk) for the full scan)
+    int cnt_chunks = 1;
+    if (!skip) {
+        rows.own = x;
+        rows.bcast = y;
+        rows.n_own = N;
+        rows.n_bc = M;
+        choose_chunks(B, N, M, &rows.S, &rows.chunk);
+        rows.owner_blocks = ceil_div(N, kBlock);
+        rows.tiles = B * rows.S * rows.owner_blocks;
+        cols.own = y;
+        cols.bcast = x;
+        cols.n_own = M;
+        cols.n_bc = N;
+        choose_chunks(B, M, N, &cols.S, &cols.chunk);
+        cols.owner_blocks = ceil_div(M, kBlock);
+        cols.tiles = B * cols.S * cols.owner_blocks;
+        rows.partial = dense_tmp.get<float2>((size_t)rows.S * BN);
+        cols.partial = dense_tmp.get<float2>((size_t)cols.S * BM);
+        float *E_row = dense_tmp.get<float>(BN);
+        float4 *ypack = dense_tmp.get<float4>(BM);
+        if (tmp.failed || dense_tmp.failed || keep.failed)
+            return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (statistics)");
+        {
+            PhaseTimer pt(PH_STATS, s);
+            launch_top2(rows, cols, B, s);
+            HIP_TRY(hipGetLastError());
+            pt.stop();
+        }
+        FinalizeDir fr{rows.partial, x, dv.m12_row, E_row, nullptr, nullptr, nullptr, N, rows.S, kp.lk_row};
+        FinalizeDir fc{cols.partial, y, dv.m12_col, nullptr, ypack, col_cnt, ba.col_fill, M, cols.S, kp.lk_col};
+        launch_finalize(fr, fc, B, kp, dv.ctr, s); // also clears the counters
+        HIP_TRY(hipGetLastError());
+
+        // ---- dense scan 2: candidate support -----------------------------
+        ea.x = x;
+        ea.ypack = ypack;
+        ea.E_row = E_row;
+        ea.B = B;
+        ea.N = N;
+        ea.M = M;
+        ea.owner_blocks = rows.owner_blocks;
+        choose_chunks(B, N, M, &ea.S, &ea.chunk, 256);
+        ea.cnt = dense_tmp.get<int32_t>((size_t)BN * ea.S);
+        ea.col_cnt = col_cnt; // cleared by the finalize kernel
+        ea.ctr = dv.ctr;
+        // the counting pass keeps the first hits of every (row, chunk);
+        // offsets within a chunk are 16-bit
+        if (ea.chunk <= 65536) {
+            ea.kst = stage_slots(ea.S);
+            ea.stage = dense_tmp.get<uint16_t>((size_t)BN * ea.S * ea.kst);
+            const size_t tiles = (size_t)B * ea.S * ea.owner_blocks;
+            ea.spill = dense_tmp.get<uint32_t>(tiles * kTileSpill);
+            ea.spill_n = dense_tmp.get<int32_t>(tiles);
+        }
+        cnt = ea.cnt;
+        cnt_chunks = ea.S;
+    } else {
+        const int pad_x = pad64(N), pad_y = pad64(M);
+        sa.x = x;
+        sa.y = y;
+        sa.B = B;
+        sa.N = N;
+        sa.M = M;
+        sa.pad_x = pad_x;
+        sa.pad_y = pad_y;
+        const size_t n_sort = (size_t)B * pad_x + (size_t)B * pad_y;
+        for (int k = 0; k < 2; ++k) {
+            sa.key[k] = dense_tmp.get<uint32_t>(n_sort);
+            sa.val[k] = dense_tmp.get<uint32_t>(n_sort);
+        }
+        sa.sx = dense_tmp.get<float4>((size_t)B * pad_x);
+        sa.sy = dense_tmp.get<float4>((size_t)B * pad_y);
+        sa.box_x = dense_tmp.get<Box>((size_t)B * pad_x / kRun);
+        sa.box_y = dense_tmp.get<Box>((size_t)B * pad_y / kRun);
+        sa.ctr = dv.ctr;
+        crows.own = sa.sx;
+        crows.bc = sa.sy;
+        crows.own_box = sa.box_x;
+        crows.bc_box = sa.box_y;
+        crows.n_own = N;
+        crows.n_bc = M;
+        crows.pad_own = pad_x;
+        crows.pad_bc = pad_y;
+        crows.waves = ceil_div(N, kScanRows);
+        ccols.own = sa.sy;
+        ccols.bc = sa.sx;
+        ccols.own_box = sa.box_y;
+        ccols.bc_box = sa.box_x;
+        ccols.n_own = M;
+        ccols.n_bc = N;
+        ccols.pad_own = pad_y;
+        ccols.pad_bc = pad_x;
+        ccols.waves = ceil_div(M, kScanRows);
+        crows.m12s = dense_tmp.get<float2>((size_t)B * pad_x);
+        ccols.m12s = dense_tmp.get<float2>((size_t)B * pad_y);
+        float *E_row = dense_tmp.get<float>((size_t)B * pad_x);
+        float4 *ypack = dense_tmp.get<float4>((size_t)B * pad_y);
+        if (tmp.failed || dense_tmp.failed || keep.failed)
+            return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (statistics)");
+        {
+            PhaseTimer pt(PH_STATS, s);
+            HIP_TRY(launch_spatial_sort(sa, s)); // also clears the counters
+            launch_cull_top2(crows, ccols, B, dv.ctr, s);
+            HIP_TRY(hipGetLastError());
+            pt.stop();
+        }
+        CullFinalizeDir fr{crows.m12s, sa.sx, dv.m12_row, E_row, nullptr, nullptr, nullptr, nullptr, N, pad_x,
+                           kp.lk_row};
+        CullFinalizeDir fc{ccols.m12s, sa.sy, dv.m12_col, nullptr, ypack, sa.box_y, col_cnt, ba.col_fill, M, pad_y,
+                           kp.lk_col};
+        launch_cull_finalize(fr, fc, B, kp, s);
+        HIP_TRY(hipGetLastError());
+
+        // ---- dense scan 2: candidate support -----------------------------
+        ca.sx = sa.sx;
+        ca.E = E_row;
+        ca.yp = ypack;
+        ca.sy = sa.sy;
+        ca.box_x = sa.box_x;
+        ca.box_y = sa.box_y;
+        ca.B = B;
+        ca.N = N;
+        ca.M = M;
+        ca.pad_x = pad_x;
+        ca.pad_y = pad_y;
+        ca.waves = crows.waves;
+        ca.cnt = dense_tmp.get<int32_t>(BN);
+        ca.col_cnt = col_cnt; // cleared by the finalize kernel
+        ca.ctr = dv.ctr;
+        cnt = ca.cnt;
     }
     Readback *rb_dev = (Readback *)tmp.get<uint8_t>(readback_bytes(B));
     std::vector<uint8_t> rb_host(readback_bytes(B));
@@ -494,12 +601,15 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     const int32_t *offsets = readback_offsets(rb, B), *pieces = readback_pieces(rb, B);
     {
         PhaseTimer pt(PH_SUPPORT, s);
-        launch_emit_count(ea, s);
+        if (skip)
+            launch_cull_emit_count(ca, s);
+        else
+            launch_emit_count(ea, s);
         HIP_TRY(hipGetLastError());
         pt.stop();
     }
     // row and column offsets, and what the host needs, in one copy
-    launch_offsets(ea.cnt, ea.S, col_cnt, dv.ctr, B, N, M, dv.row_ptr, dv.col_ptr, rb_dev, s);
+    launch_offsets(cnt, cnt_chunks, col_cnt, dv.ctr, B, N, M, dv.row_ptr, dv.col_ptr, rb_dev, s);
     HIP_TRY(hipMemcpyAsync(rb_host.data(), rb_dev, readback_bytes(B), hipMemcpyDeviceToHost, s));
     HIP_TRY(wait_for(s));
     int64_t nnz = 0;
@@ -511,6 +621,8 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     if (nnz > (int64_t)INT32_MAX - 1)
         return fail(APML_ERR_UNSUPPORTED, "more than 2^31 stored pairs: raise tau or lower N*M");
     plan->stored = nnz;
+    plan->scanned[0] = skip ? (int64_t)rb->ctr.scanned[0] : 2 * (int64_t)B * N * M;
+    plan->scanned[1] = skip ? (int64_t)rb->ctr.scanned[1] : (int64_t)B * N * M;
     if (offsets[B] != nnz)
         return fail(APML_ERR_INTERNAL, "row offsets disagree with the column counts");
     for (int b = 0; b < B; ++b)
@@ -533,16 +645,19 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     dv.p0c = keep.get<float>(nnz);
     dv.cost = keep.get<double>(nnz);
     // column-major view: per sample in LDS when it fits (with the row
-    // softmax), else slots taken by global counters (in the compaction when
-    // no tile is rescanned)
+    // softmax), else slots taken by global counters (in the full scan's
+    // compaction when no tile is rescanned)
     const bool csc_lds = csc_sample_fits(N, M, plan->max_sample);
-    const bool placed = !csc_lds && ea.stage && !rb->ctr.overflow;
+    const bool placed = !skip && !csc_lds && ea.stage && !rb->ctr.overflow;
     if (!csc_lds) {
         ba.tmp_row = tmp.get<int32_t>(nnz);
         ba.tmp_src = tmp.get<int32_t>(nnz);
     }
-    // pieces of the per-sample Sinkhorn kernels; with staged hits their
-    // placement runs in the compaction's launch
+    if (skip)
+        ca.tmp_col = dense_tmp.get<int32_t>(nnz);
+    // pieces of the per-sample Sinkhorn kernels; with staged hits (or the
+    // skipping scans) their placement runs in the compaction's (ranking's)
+    // launch
     int32_t *place = nullptr;
     if (plan->sink_fwd) {
         const size_t w = packed_order_words(B, slots);
@@ -556,23 +671,32 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         }
         place = tmp.get<int32_t>((size_t)B * 2 * kSinkOwners);
     }
-    const bool pieces_placed = place && ea.stage && !placed;
-    if (tmp.failed || keep.failed)
+    const bool pieces_placed = place && (skip || (ea.stage && !placed));
+    if (tmp.failed || keep.failed || dense_tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (sparse arrays)");
     {
         PhaseTimer pt(PH_BUILD, s);
-        ea.row_ptr = dv.row_ptr;
-        ea.csr_col = dv.csr_col;
-        ea.csr_row = dv.csr_row;
-        ea.col_ptr = dv.col_ptr;
-        ea.col_fill = ba.col_fill;
-        ea.tmp_row = ba.tmp_row;
-        ea.tmp_src = ba.tmp_src;
-        ea.csc_col = dv.csc_col;
-        if (ea.stage)
-            launch_emit_compact(ea, rb->ctr.overflow != 0, placed, &dv, pieces_placed ? place : nullptr, s);
-        else
-            launch_emit_write(ea, s);
+        if (skip) {
+            ca.row_ptr = dv.row_ptr;
+            ca.csr_col = dv.csr_col;
+            ca.csr_row = dv.csr_row;
+            ca.nnz = nnz;
+            launch_cull_emit_write(ca, s);
+            launch_cull_emit_rank(ca, &dv, place, s);
+        } else {
+            ea.row_ptr = dv.row_ptr;
+            ea.csr_col = dv.csr_col;
+            ea.csr_row = dv.csr_row;
+            ea.col_ptr = dv.col_ptr;
+            ea.col_fill = ba.col_fill;
+            ea.tmp_row = ba.tmp_row;
+            ea.tmp_src = ba.tmp_src;
+            ea.csc_col = dv.csc_col;
+            if (ea.stage)
+                launch_emit_compact(ea, rb->ctr.overflow != 0, placed, &dv, pieces_placed ? place : nullptr, s);
+            else
+                launch_emit_write(ea, s);
+        }
         if (csc_lds) {
             // built with the row softmax below
         } else if (placed) {
@@ -690,6 +814,8 @@ apml_status apml_plan_get_info(const apml_plan *plan, apml_plan_info *info)
     info->n_iter = plan->L;
     info->stored_pairs = plan->stored;
     info->bytes = plan->keep.bytes;
+    info->scanned_min = plan->scanned[0];
+    info->scanned_support = plan->scanned[1];
     return APML_OK;
 }
 

@@ -13,10 +13,12 @@ constexpr int kBlock = 256;       // threads per workgroup of the grid-wide kern
 constexpr int kUnroll = 8;        // broadcast points per inner step of the dense scans
 constexpr int kGroup = 4;         // lanes per row / column in the sparse kernels
 
-// Device-side counters of one forward call.
+// Device-side counters of one forward call (cleared by the first kernel that
+// runs after them: the full scan's finalize kernel or the spatial sort).
 struct Counters {
-    unsigned int error;    // bit 0: a row's minima not found among its pairs; bit 1: a column's
-    unsigned int overflow; // a (row, chunk) of the support scan had more hits than its staging slots
+    unsigned int error;            // bit 0: a row's minima not found among its pairs; bit 1: a column's
+    unsigned int overflow;         // a (row, chunk) of the full support scan had more hits than its staging slots
+    unsigned long long scanned[2]; // pairs evaluated by the skipping scans: minimum scan, support scan
 };
 
 struct Params {
@@ -101,6 +103,83 @@ struct DevPlan;
 // per-sample Sinkhorn kernels (place_order) for plan d.
 void launch_emit_compact(const EmitArgs &a, bool overflow, bool place, const DevPlan *d, int32_t *pieces_place,
                          hipStream_t s);
+
+// The skipping scans (cull.hip), for large samples. Both clouds are sorted
+// along a Morton curve per sample (spatial.hip). A sorted cloud is [B][pad]
+// float4 (x, y, z, original index as bits), pad = the point count rounded up
+// to a multiple of 64, with the bounding box of every run of kRun consecutive
+// points ([B][pad / kRun]). The scans skip every run whose box is provably
+// too far from the box of their rows.
+constexpr int kRun = 32;      // points per box
+constexpr int kScanRows = 64; // owners per wave of the dense scans (one per lane)
+inline int pad64(int n) { return (n + 63) / 64 * 64; }
+
+struct Box {
+    float4 lo, hi; // hi.w: (columns, after the finalize kernel) the largest emission threshold of the run
+};
+
+struct SpatialArgs {
+    const float *x, *y; // [B, N, 3], [B, M, 3]
+    int B, N, M, pad_x, pad_y;
+    uint32_t *key[2], *val[2]; // scratch: [B * pad_x + B * pad_y] each
+    float4 *sx, *sy;           // out: sorted clouds
+    Box *box_x, *box_y;        // out: boxes of the runs
+    Counters *ctr;             // cleared here
+};
+size_t spatial_sort_lds();
+hipError_t launch_spatial_sort(const SpatialArgs &a, hipStream_t s);
+
+// One direction of the minimum / second-minimum scan: owners (X for rows, Y
+// for columns) against every point of the other cloud.
+struct CullDir {
+    const float4 *own, *bc; // sorted owners [B][pad_own] and other cloud [B][pad_bc]
+    const Box *own_box;     // [B][pad_own / kRun]
+    const Box *bc_box;      // [B][pad_bc / kRun]
+    float2 *m12s;           // out [B][pad_own]: (min, second min) of the squared distance, sorted position
+    int n_own, n_bc, pad_own, pad_bc;
+    int waves;              // per sample: ceil(n_own / kScanRows)
+};
+
+struct CullFinalizeDir {
+    const float2 *m12s;       // [B][pad]
+    const float4 *own;        // sorted owners [B][pad]
+    float2 *m12;              // out: (m1, m2) per owner, original order [B * n_own]
+    float *E;                 // out (rows): emission threshold on the squared distance, sorted [B][pad]
+    float4 *packed;           // out (columns): (x, y, z, emission threshold), sorted [B][pad]
+    Box *box;                 // (columns) hi.w of every run: its largest threshold
+    int32_t *zero_a, *zero_b; // (columns) per-owner counters cleared here, original order
+    int n_own, pad;
+    double log_ratio;         // -log((1-p)/((K-1)p)), K = length of the other set
+};
+
+void launch_cull_top2(const CullDir &rows, const CullDir &cols, int B, Counters *ctr, hipStream_t s);
+void launch_cull_finalize(const CullFinalizeDir &rows, const CullFinalizeDir &cols, int B, const Params &p,
+                          hipStream_t s);
+
+struct CullEmitArgs {
+    const float4 *sx;    // sorted rows [B][pad_x]
+    const float *E;      // their thresholds [B][pad_x]
+    const float4 *yp;    // sorted columns with their thresholds [B][pad_y]
+    const float4 *sy;    // sorted columns with their original index [B][pad_y]
+    const Box *box_x;    // [B][pad_x / kRun]
+    const Box *box_y;    // [B][pad_y / kRun]
+    int B, N, M, pad_x, pad_y, waves;
+    int32_t *cnt;        // [B*N] stored pairs per row
+    int32_t *col_cnt;    // [B*M] stored pairs per column
+    Counters *ctr;
+    // writing pass and ranking
+    const int32_t *row_ptr; // [B*N+1]
+    int32_t *tmp_col;       // [nnz] each row's columns in scan order
+    int32_t *csr_col, *csr_row;
+    int64_t nnz;
+};
+// Pass 1 counts the candidate support per row and per column; pass 2 (after
+// the offsets are known) writes each row's columns in scan order; the ranking
+// puts them in increasing column order and (pieces_place non-NULL) places the
+// pieces of the per-sample Sinkhorn kernels (place_order) in the same launch.
+void launch_cull_emit_count(const CullEmitArgs &a, hipStream_t s);
+void launch_cull_emit_write(const CullEmitArgs &a, hipStream_t s);
+void launch_cull_emit_rank(const CullEmitArgs &a, const DevPlan *d, int32_t *pieces_place, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // sparse structure

@@ -81,7 +81,7 @@ __global__ __launch_bounds__(kBlock) void k_finalize(FinalizeArgs args)
 {
     int k = blockIdx.x * kBlock + threadIdx.x;
     if (k == 0)
-        *args.ctr = Counters{0, 0};
+        *args.ctr = Counters{};
     const int which = k < args.rows ? 0 : 1;
     if (which)
         k -= args.rows;

@@ -114,6 +114,17 @@ template <int G> struct Argmins {
     }
 };
 
+// Workgroups are dealt to the 8 XCDs round robin (workgroup i to XCD i % 8),
+// and each XCD has its own L2. This maps the hardware index to a logical one
+// under which every XCD receives one contiguous range of the grid, so that
+// workgroups sharing data (one sample) share an L2.
+constexpr int kXcds = 8;
+__device__ __forceinline__ int xcd_contiguous(int bid, int grid)
+{
+    const int q = grid / kXcds, r = grid % kXcds, x = bid % kXcds;
+    return x * q + min(x, r) + bid / kXcds;
+}
+
 inline unsigned blocks_for(int64_t n, int per_block) { return (unsigned)((n + per_block - 1) / per_block); }
 
 } // namespace apml

@@ -1,0 +1,254 @@
+// Spatial order of the two clouds for the dense scans.
+//
+// Every pair whose distance can matter to a row or a column lies within a
+// small radius (the kept ball of Sec. III-B, Eq. 1, or the second minimum of
+// Sec. III-A). With each cloud sorted along a Morton curve, a run of 32
+// consecutive points occupies a small box, and the dense scans skip every
+// run whose box is provably beyond that radius from the box of their rows
+// (dense.hip). The order only decides which work is skipped: results do not
+// depend on it.
+//
+//   k_spatial_sort  one workgroup per (sample, cloud). The frame is the
+//                   bounding cube of both clouds of the sample, quantized to
+//                   10 bits per axis; the 30-bit Morton keys are sorted by a
+//                   least-significant-digit radix sort (three 10-bit digits,
+//                   stable: ranks within a wave from ballots, across waves
+//                   from per-wave digit counts in LDS). The sorted points are
+//                   written as (x, y, z, original index), with the bounding
+//                   box of every run of 32.
+#include "apml_internal.h"
+#include "device_common.h"
+
+namespace apml {
+namespace {
+
+constexpr int kSortT = 1024;
+constexpr int kSortWaves = kSortT / 64;
+constexpr int kDigitBits = 10;
+constexpr int kBins = 1 << kDigitBits; // == kSortT: one bin per thread in the scans
+constexpr int kPasses = 3;
+constexpr int kSuper = 8; // keys per thread held in registers between global round trips
+static_assert(kBins == kSortT, "one bin per thread");
+
+// Spreads the low 10 bits of v to every third bit (bit k goes to bit 3k).
+__device__ __forceinline__ uint32_t spread3(uint32_t v)
+{
+    v &= 0x3FFu;
+    v = (v | (v << 16)) & 0x030000FFu;
+    v = (v | (v << 8)) & 0x0300F00Fu;
+    v = (v | (v << 4)) & 0x030C30C3u;
+    v = (v | (v << 2)) & 0x09249249u;
+    return v;
+}
+
+__device__ __forceinline__ uint32_t quantize(float v, float lo, float scale)
+{
+    const float t = (v - lo) * scale;
+    return (uint32_t)fminf(fmaxf(t, 0.0f), 1023.0f);
+}
+
+// LDS of k_spatial_sort (dynamic; about 140 KB).
+struct SortLds {
+    int whist[kSortWaves][kBins]; // digit counts of each wave in the current tile (zero outside a tile)
+    int woff[kSortWaves][kBins];  // their exclusive prefix over the waves
+    int base[kPasses][kBins];     // next output position of every digit, per pass
+    float frame[kSortWaves][6];
+    int wsum[kSortWaves];
+};
+
+__device__ __forceinline__ uint64_t lanes_below() { return (1ull << lane_id()) - 1ull; }
+
+// One stable pass: the n keys and values of src, in order of digit pass p.
+__device__ void radix_pass(SortLds &s, int p, int n, const uint32_t *sk, const uint32_t *sv, uint32_t *dk,
+                           uint32_t *dv)
+{
+    const int tid = threadIdx.x, wave = tid >> 6;
+    const int shift = p * kDigitBits;
+    for (int t0 = 0; t0 < n; t0 += kSuper * kSortT) {
+        uint32_t key[kSuper], val[kSuper];
+#pragma unroll
+        for (int u = 0; u < kSuper; ++u) { // one global round trip for kSuper tiles
+            const int k = t0 + u * kSortT + tid;
+            key[u] = k < n ? sk[k] : 0u;
+            val[u] = k < n ? sv[k] : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < kSuper; ++u) {
+            const int k0 = t0 + u * kSortT;
+            if (k0 >= n) // uniform over the workgroup
+                break;
+            const bool valid = k0 + tid < n;
+            const uint32_t dg = (key[u] >> shift) & (kBins - 1);
+            uint64_t peers = __ballot(valid);
+#pragma unroll
+            for (int i = 0; i < kDigitBits; ++i) {
+                const uint64_t bal = __ballot((dg >> i) & 1u);
+                peers &= ((dg >> i) & 1u) ? bal : ~bal;
+            }
+            const uint64_t lower = peers & lanes_below();
+            const int rank = __popcll(lower);
+            const bool leader = valid && lower == 0;
+            if (leader)
+                s.whist[wave][dg] = __popcll(peers);
+            lds_barrier();
+            int run = 0;
+#pragma unroll
+            for (int w = 0; w < kSortWaves; ++w) {
+                const int c = s.whist[w][tid];
+                s.woff[w][tid] = run;
+                run += c;
+            }
+            lds_barrier();
+            const int pos = s.base[p][dg] + s.woff[wave][dg] + rank;
+            if (valid && pos < n) { // always below n: every pass sees the digits the histograms counted
+                dk[pos] = key[u];
+                dv[pos] = val[u];
+            }
+            lds_barrier();
+            s.base[p][tid] += run;
+            if (leader) // this wave's next tile writes its counts after these clears (same wave, in order)
+                s.whist[wave][dg] = 0;
+        }
+    }
+}
+
+__global__ __launch_bounds__(kSortT) void k_spatial_sort(SpatialArgs a)
+{
+    extern __shared__ int4 lds_raw[];
+    SortLds &s = *reinterpret_cast<SortLds *>(lds_raw);
+    const int b = blockIdx.x >> 1, cloud = blockIdx.x & 1;
+    const int tid = threadIdx.x, lane = lane_id(), wave = tid >> 6;
+    if (blockIdx.x == 0 && tid == 0)
+        *a.ctr = Counters{};
+    const int n = cloud ? a.M : a.N;
+    const int pad = cloud ? a.pad_y : a.pad_x;
+    const float *pts = (cloud ? a.y : a.x) + (size_t)b * n * 3;
+    const size_t seg = cloud ? (size_t)a.B * a.pad_x + (size_t)b * a.pad_y : (size_t)b * a.pad_x;
+    uint32_t *k0 = a.key[0] + seg, *v0 = a.val[0] + seg, *k1 = a.key[1] + seg, *v1 = a.val[1] + seg;
+
+    // frame: bounding cube of both clouds of the sample
+    float f[6] = {kInf, kInf, kInf, -kInf, -kInf, -kInf};
+    {
+        const float *xs = a.x + (size_t)b * a.N * 3, *ys = a.y + (size_t)b * a.M * 3;
+        for (int k = tid; k < a.N + a.M; k += kSortT) {
+            const float *p = k < a.N ? xs + 3 * (size_t)k : ys + 3 * (size_t)(k - a.N);
+#pragma unroll
+            for (int c = 0; c < 3; ++c) {
+                f[c] = fminf(f[c], p[c]);
+                f[3 + c] = fmaxf(f[3 + c], p[c]);
+            }
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1)
+#pragma unroll
+            for (int c = 0; c < 3; ++c) {
+                f[c] = fminf(f[c], __shfl_xor(f[c], o));
+                f[3 + c] = fmaxf(f[3 + c], __shfl_xor(f[3 + c], o));
+            }
+        if (lane == 0)
+#pragma unroll
+            for (int c = 0; c < 6; ++c)
+                s.frame[wave][c] = f[c];
+    }
+    for (int i = tid; i < kPasses * kBins; i += kSortT)
+        (&s.base[0][0])[i] = 0;
+    for (int i = tid; i < kSortWaves * kBins; i += kSortT)
+        (&s.whist[0][0])[i] = 0;
+    lds_barrier();
+#pragma unroll
+    for (int w = 0; w < kSortWaves; ++w)
+#pragma unroll
+        for (int c = 0; c < 3; ++c) {
+            f[c] = fminf(f[c], s.frame[w][c]);
+            f[3 + c] = fmaxf(f[3 + c], s.frame[w][3 + c]);
+        }
+    const float ext = fmaxf(fmaxf(f[3] - f[0], f[4] - f[1]), f[5] - f[2]);
+    const float scale = ext > 0.0f ? 1024.0f / ext : 0.0f;
+
+    // keys and the digit histograms of all passes (independent of the order)
+    for (int k = tid; k < n; k += kSortT) {
+        const float *p = pts + 3 * (size_t)k;
+        const uint32_t key = spread3(quantize(p[0], f[0], scale)) | spread3(quantize(p[1], f[1], scale)) << 1 |
+                             spread3(quantize(p[2], f[2], scale)) << 2;
+        k0[k] = key;
+        v0[k] = (uint32_t)k;
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q)
+            atomicAdd(&s.base[q][(key >> (q * kDigitBits)) & (kBins - 1)], 1);
+    }
+    __syncthreads(); // the keys written above are read back by other threads
+    // exclusive scans of the histograms: bin tid of every pass
+#pragma unroll
+    for (int q = 0; q < kPasses; ++q) {
+        const int c = s.base[q][tid];
+        int inc = c;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int v = __shfl_up(inc, o);
+            if (lane >= o)
+                inc += v;
+        }
+        if (lane == 63)
+            s.wsum[wave] = inc;
+        lds_barrier();
+        int before = 0;
+#pragma unroll
+        for (int w = 0; w < kSortWaves; ++w)
+            before += w < wave ? s.wsum[w] : 0;
+        lds_barrier();
+        s.base[q][tid] = before + inc - c;
+    }
+    lds_barrier();
+    radix_pass(s, 0, n, k0, v0, k1, v1);
+    __syncthreads();
+    radix_pass(s, 1, n, k1, v1, k0, v0);
+    __syncthreads();
+    radix_pass(s, 2, n, k0, v0, k1, v1);
+    __syncthreads();
+
+    // sorted points and the boxes of the runs of 32 (padding: empty boxes)
+    float4 *out = (cloud ? a.sy : a.sx) + (size_t)b * pad;
+    Box *box = (cloud ? a.box_y : a.box_x) + (size_t)b * (pad / kRun);
+    for (int k = tid; k < pad; k += kSortT) { // pad is a multiple of 64: whole waves
+        float4 v = make_float4(0.0f, 0.0f, 0.0f, __int_as_float(-1));
+        float lo[3] = {kInf, kInf, kInf}, hi[3] = {-kInf, -kInf, -kInf};
+        if (k < n) {
+            const uint32_t i = v1[k];
+            const float *p = pts + 3 * (size_t)i;
+            v = make_float4(p[0], p[1], p[2], __uint_as_float(i));
+            lo[0] = hi[0] = p[0];
+            lo[1] = hi[1] = p[1];
+            lo[2] = hi[2] = p[2];
+        }
+        out[k] = v;
+#pragma unroll
+        for (int o = 1; o < kRun; o <<= 1)
+#pragma unroll
+            for (int c = 0; c < 3; ++c) {
+                lo[c] = fminf(lo[c], __shfl_xor(lo[c], o));
+                hi[c] = fmaxf(hi[c], __shfl_xor(hi[c], o));
+            }
+        if ((lane & (kRun - 1)) == 0)
+            box[k / kRun] = Box{make_float4(lo[0], lo[1], lo[2], 0.0f), make_float4(hi[0], hi[1], hi[2], 0.0f)};
+    }
+}
+
+} // namespace
+
+size_t spatial_sort_lds() { return sizeof(SortLds); }
+
+hipError_t launch_spatial_sort(const SpatialArgs &a, hipStream_t s)
+{
+    static bool attr = false;
+    if (!attr) {
+        const hipError_t e = hipFuncSetAttribute((const void *)k_spatial_sort,
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(SortLds));
+        if (e != hipSuccess)
+            return e;
+        attr = true;
+    }
+    hipLaunchKernelGGL(k_spatial_sort, dim3(2 * a.B), dim3(kSortT), sizeof(SortLds), s, a);
+    return hipGetLastError();
+}
+
+} // namespace apml

@@ -38,7 +38,7 @@ def test_every_declared_symbol_is_exported():
 
 def test_defaults_are_the_papers():
     p = _lib.apml_params_default()
-    assert p.struct_size == ctypes.sizeof(_lib.apml_params) == 56
+    assert p.struct_size == ctypes.sizeof(_lib.apml_params) == 64
     assert (p.tau, p.n_iter, p.eps_stab) == (1e-8, 10, 1e-8)  # Sec. III-E, Sec. IV-C
     assert (p.p_min, p.delta, p.eps_gap, p.eps_dist) == (0.8, 1e-8, 1e-6, 1e-12)
 

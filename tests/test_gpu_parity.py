@@ -20,9 +20,14 @@ def _gpu():
     apml.load()
 
 
-def _check_batch(X, Y, label, samples=None, check_grad_y=True, **prm):
-    note(f"{label}: B={X.shape[0]} N={X.shape[1]} M={Y.shape[1]} {prm}")
-    g = run_gpu(X, Y, **prm)
+# the two ways the dense scans visit the pairs (identical results): every
+# pair, or skipping runs of the spatially sorted clouds that cannot matter
+SCANS = {"full": 1, "skip": 2}
+
+
+def _check_batch(X, Y, label, samples=None, check_grad_y=True, scan=None, **prm):
+    note(f"{label}: B={X.shape[0]} N={X.shape[1]} M={Y.shape[1]} {prm} scan={scan or 'auto'}")
+    g = run_gpu(X, Y, **prm, **({} if scan is None else {"dense_scan": SCANS[scan]}))
     tau = prm.get("tau", 1e-8)
     out = []
     for b in (range(X.shape[0]) if samples is None else samples):
@@ -33,32 +38,37 @@ def _check_batch(X, Y, label, samples=None, check_grad_y=True, **prm):
     return g, out
 
 
-def test_tiny_config_full():
+@pytest.mark.parametrize("scan", ["full", "skip"])
+def test_tiny_config_full(scan):
     w = config(1)
     X, Y = batch(w)
-    _, res = _check_batch(X, Y, "config 1", n_iter=w.n_iter)
+    _, res = _check_batch(X, Y, "config 1", n_iter=w.n_iter, scan=scan)
     assert all(r["flips"] == 0 for r in res), res
 
 
-def test_ragged_unequal_sizes():
+@pytest.mark.parametrize("scan", ["full", "skip"])
+def test_ragged_unequal_sizes(scan):
     # sizes that are not multiples of the wave, the workgroup or the chunk
     X, Y = custom(21, 3, 300, 517, reference="sphere", prediction="uniform_cube")
-    _check_batch(X, Y, "ragged", n_iter=7)
+    _check_batch(X, Y, "ragged", n_iter=7, scan=scan)
 
 
-def test_unequal_cardinality_primitives():
+@pytest.mark.parametrize("scan", ["full", "skip"])
+def test_unequal_cardinality_primitives(scan):
     X, Y = custom(22, 2, 700, 2100, reference="primitives", prediction="uniform_cube")
-    _check_batch(X, Y, "unequal", n_iter=10)
+    _check_batch(X, Y, "unequal", n_iter=10, scan=scan)
 
 
-def test_minimum_size():
+@pytest.mark.parametrize("scan", ["full", "skip"])
+def test_minimum_size(scan):
     X, Y = custom(23, 4, 2, 2, sigma=0.1)
-    _check_batch(X, Y, "N=M=2", n_iter=10)
+    _check_batch(X, Y, "N=M=2", n_iter=10, scan=scan)
 
 
-def test_single_sample_odd_shapes():
+@pytest.mark.parametrize("scan", ["full", "skip"])
+def test_single_sample_odd_shapes(scan):
     X, Y = custom(24, 1, 65, 3, reference="sphere", prediction="uniform_cube")
-    _check_batch(X, Y, "N=65 M=3", n_iter=3)
+    _check_batch(X, Y, "N=65 M=3", n_iter=3, scan=scan)
 
 
 @pytest.mark.parametrize("L", [0, 1, 20])
@@ -67,17 +77,19 @@ def test_iteration_counts(L):
     _check_batch(X, Y, f"L={L}", n_iter=L)
 
 
-def test_dense_threshold_zero_with_overflow():
-    # tau = 0 keeps every pair: every row overflows its slots and the overflow
-    # list itself has to grow once (retry path)
+@pytest.mark.parametrize("scan", ["full", "skip"])
+def test_dense_threshold_zero_full_support(scan):
+    # tau = 0 keeps every pair: no run of the support scan can be skipped and
+    # every row holds all M columns
     X, Y = custom(26, 1, 400, 400, sigma=0.05)
-    g, res = _check_batch(X, Y, "tau=0", tau=0.0, n_iter=5)
+    g, res = _check_batch(X, Y, "tau=0", tau=0.0, n_iter=5, scan=scan)
     assert res[0]["nnz_gpu"] == 400 * 400
 
 
-def test_threshold_one_is_half_chamfer():
+@pytest.mark.parametrize("scan", ["full", "skip"])
+def test_threshold_one_is_half_chamfer(scan):
     X, Y = custom(27, 2, 150, 170, sigma=0.05)
-    g, _ = _check_batch(X, Y, "tau=1", tau=1.0, n_iter=0)
+    g, _ = _check_batch(X, Y, "tau=1", tau=1.0, n_iter=0, scan=scan)
     for b in range(2):
         D = np.linalg.norm(X[b].astype(np.float64)[:, None] - Y[b].astype(np.float64)[None], axis=-1)
         assert g["loss"][b] == pytest.approx(0.5 * (D.min(1).sum() + D.min(0).sum()), rel=1e-5)
@@ -89,18 +101,20 @@ def test_other_p_min(p_min):
     _check_batch(X, Y, f"p_min={p_min}", p_min=p_min)
 
 
-def test_duplicates_ties_and_clamps():
+@pytest.mark.parametrize("scan", ["full", "skip"])
+def test_duplicates_ties_and_clamps(scan):
     X, Y = custom(29, 2, 128, 100, sigma=0.05)
     Y = np.ascontiguousarray(np.concatenate([Y, Y[:, :30]], axis=1))  # exact ties
     X = np.ascontiguousarray(np.concatenate([X, X[:, :10]], axis=1))
-    g, _ = _check_batch(X, Y, "ties")
+    g, _ = _check_batch(X, Y, "ties", scan=scan)
     st = g["plan"].export_stats(0)
     assert st["clamp_row"].any() and st["clamp_col"].any()
 
 
-def test_identical_clouds():
+@pytest.mark.parametrize("scan", ["full", "skip"])
+def test_identical_clouds(scan):
     _, Y = custom(30, 2, 300, 300, sigma=0.05)
-    _check_batch(Y.copy(), Y, "x == y")
+    _check_batch(Y.copy(), Y, "x == y", scan=scan)
 
 
 def test_upstream_gradient_scaling():
@@ -116,11 +130,12 @@ def test_upstream_gradient_scaling():
             assert rel_norm(g["gx"][b], ref.grad_x) <= 1e-4
 
 
-def test_deterministic_bitwise():
+@pytest.mark.parametrize("scan", ["full", "skip"])
+def test_deterministic_bitwise(scan):
     X, Y = batch(config(1))
-    note("determinism")
-    a = run_gpu(X, Y)
-    b = run_gpu(X, Y)
+    note(f"determinism scan={scan}")
+    a = run_gpu(X, Y, dense_scan=SCANS[scan])
+    b = run_gpu(X, Y, dense_scan=SCANS[scan])
     assert np.array_equal(a["loss"], b["loss"])
     assert np.array_equal(a["gx"], b["gx"]) and np.array_equal(a["gy"], b["gy"])
 
@@ -162,19 +177,20 @@ def test_plan_reports_and_memory_returns():
 # full-size configurations, in the launch configuration the benchmark times
 # ---------------------------------------------------------------------------
 
-def test_config2_full_batch():
+@pytest.mark.parametrize("scan", ["full", "skip"])
+def test_config2_full_batch(scan):
     w = config(2)
     X, Y = batch(w)
-    _, res = _check_batch(X, Y, "config 2", n_iter=w.n_iter)
+    _, res = _check_batch(X, Y, "config 2", n_iter=w.n_iter, scan=scan)
     note(f"config 2 nnz per sample: {[r['nnz_gpu'] for r in res[:4]]} flips {sum(r['flips'] for r in res)}")
 
 
-@pytest.mark.parametrize("cfg", [3, 4])
-def test_large_configs_one_sample_exact(cfg):
+@pytest.mark.parametrize("cfg,scan", [(3, None), (4, None), (4, "full")])
+def test_large_configs_one_sample_exact(cfg, scan):
     # the whole batch runs on the GPU; sample 0 is checked against a full oracle run
     w = config(cfg)
     X, Y = batch(w)
-    _check_batch(X, Y, f"config {cfg}", samples=[0], n_iter=w.n_iter)
+    _check_batch(X, Y, f"config {cfg}", samples=[0], n_iter=w.n_iter, scan=scan)
 
 
 def test_config5_sampled_owners_and_invariants():
