@@ -104,6 +104,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--scan", choices=["auto", "full", "skip"], default="auto",
+                    help="how the dense scans visit the pairs (identical results)")
     ap.add_argument("--cpu-baseline", choices=["on", "off"], default="on")
     ap.add_argument("--cpu-repeats", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -211,7 +213,7 @@ def main():
     x = torch.from_numpy(X).cuda()
     y = torch.from_numpy(Y).cuda()
     gl = torch.ones(w.B, device="cuda")
-    prm = apml.apml_params_default(n_iter=w.n_iter)
+    prm = apml.apml_params_default(n_iter=w.n_iter, dense_scan={"auto": 0, "full": 1, "skip": 2}[args.scan])
 
     def step():
         loss, plan = apml.apml_forward(x, y, prm)

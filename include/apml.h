@@ -66,7 +66,7 @@ typedef void *apml_stream;
  * both clouds along a space-filling curve and skips every run of 32 points
  * whose bounding box is provably beyond the distance that can still matter
  * to the owners being scanned; it pays off for large samples. AUTO takes SKIP
- * when N*M >= 2^24. */
+ * when min(N, M) >= 8192. */
 typedef enum { APML_SCAN_AUTO = 0, APML_SCAN_FULL = 1, APML_SCAN_SKIP = 2 } apml_scan_mode;
 
 typedef struct apml_params {

@@ -328,9 +328,11 @@ void choose_chunks(int B, int n_own, int n_bc, int *S, int *chunk, int min_chunk
     *S = ceil_div(n_bc, len);
 }
 
-// The skipping scans pay off once a sample has many pairs per stored pair;
-// below about 2^24 pairs per sample the full scans are faster.
-constexpr int64_t kSkipMinPairs = int64_t(1) << 24;
+// The skipping scans pay off when both clouds are large: their sort and
+// run selection cost about as much as the full scans of 2048 x 2048 or
+// 4096 x 16384 points per sample (measured), and far less than those of two
+// clouds of 8192 points or more.
+constexpr int kSkipMinPoints = 8192;
 
 bool use_skipping_scans(const apml_params &p, int N, int M)
 {
@@ -338,7 +340,7 @@ bool use_skipping_scans(const apml_params &p, int N, int M)
         return false;
     if (p.dense_scan == APML_SCAN_SKIP)
         return true;
-    return (int64_t)N * M >= kSkipMinPairs;
+    return std::min(N, M) >= kSkipMinPoints;
 }
 
 } // namespace
@@ -621,8 +623,12 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     if (nnz > (int64_t)INT32_MAX - 1)
         return fail(APML_ERR_UNSUPPORTED, "more than 2^31 stored pairs: raise tau or lower N*M");
     plan->stored = nnz;
-    plan->scanned[0] = skip ? (int64_t)rb->ctr.scanned[0] : 2 * (int64_t)B * N * M;
-    plan->scanned[1] = skip ? (int64_t)rb->ctr.scanned[1] : (int64_t)B * N * M;
+    plan->scanned[0] = skip ? 0 : 2 * (int64_t)B * N * M;
+    plan->scanned[1] = skip ? 0 : (int64_t)B * N * M;
+    for (int k = 0; skip && k < kScanSlots; ++k) {
+        plan->scanned[0] += (int64_t)rb->ctr.scanned[0][k];
+        plan->scanned[1] += (int64_t)rb->ctr.scanned[1][k];
+    }
     if (offsets[B] != nnz)
         return fail(APML_ERR_INTERNAL, "row offsets disagree with the column counts");
     for (int b = 0; b < B; ++b)

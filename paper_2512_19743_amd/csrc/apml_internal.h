@@ -13,12 +13,17 @@ constexpr int kBlock = 256;       // threads per workgroup of the grid-wide kern
 constexpr int kUnroll = 8;        // broadcast points per inner step of the dense scans
 constexpr int kGroup = 4;         // lanes per row / column in the sparse kernels
 
+constexpr int kScanSlots = 64;
+
 // Device-side counters of one forward call (cleared by the first kernel that
 // runs after them: the full scan's finalize kernel or the spatial sort).
 struct Counters {
     unsigned int error;            // bit 0: a row's minima not found among its pairs; bit 1: a column's
     unsigned int overflow;         // a (row, chunk) of the full support scan had more hits than its staging slots
-    unsigned long long scanned[2]; // pairs evaluated by the skipping scans: minimum scan, support scan
+    // pairs evaluated by the skipping scans (minimum scan, support scan), in
+    // kScanSlots partial sums: workgroup w adds to slot w % kScanSlots, so
+    // that no single address takes every workgroup's atomic
+    unsigned long long scanned[2][kScanSlots];
 };
 
 struct Params {
@@ -105,7 +110,7 @@ void launch_emit_compact(const EmitArgs &a, bool overflow, bool place, const Dev
                          hipStream_t s);
 
 // The skipping scans (cull.hip), for large samples. Both clouds are sorted
-// along a Morton curve per sample (spatial.hip). A sorted cloud is [B][pad]
+// along a Hilbert curve per sample (spatial.hip). A sorted cloud is [B][pad]
 // float4 (x, y, z, original index as bits), pad = the point count rounded up
 // to a multiple of 64, with the bounding box of every run of kRun consecutive
 // points ([B][pad / kRun]). The scans skip every run whose box is provably

@@ -259,7 +259,8 @@ __global__ __launch_bounds__(kBlock) void k_cull_top2(Top2Args args)
             d.m12s[(size_t)b * d.pad_own + k] = make_float2(m1, m2);
     }
     if (lane == 0)
-        atomicAdd(&args.ctr->scanned[0], (unsigned long long)cols * min(kScanRows, d.n_own - g * kScanRows));
+        atomicAdd(&args.ctr->scanned[0][blockIdx.x % kScanSlots],
+                  (unsigned long long)cols * min(kScanRows, d.n_own - g * kScanRows));
 }
 
 struct FinalizeArgs {
@@ -416,7 +417,8 @@ template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_cull_emit(Cull
         if (wv == 0 && valid)
             a.cnt[row] = acc[0][lane] + acc[1][lane] + acc[2][lane] + acc[3][lane];
         if (lane == 0)
-            atomicAdd(&a.ctr->scanned[1], (unsigned long long)cols * min(kScanRows, a.N - g * kScanRows));
+            atomicAdd(&a.ctr->scanned[1][blockIdx.x % kScanSlots],
+                      (unsigned long long)cols * min(kScanRows, a.N - g * kScanRows));
     }
 }
 

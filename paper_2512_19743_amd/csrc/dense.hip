@@ -80,8 +80,10 @@ struct FinalizeArgs {
 __global__ __launch_bounds__(kBlock) void k_finalize(FinalizeArgs args)
 {
     int k = blockIdx.x * kBlock + threadIdx.x;
-    if (k == 0)
-        *args.ctr = Counters{};
+    if (k == 0) { // the full scans leave the skipping scans' counts unused
+        args.ctr->error = 0;
+        args.ctr->overflow = 0;
+    }
     const int which = k < args.rows ? 0 : 1;
     if (which)
         k -= args.rows;

@@ -2,7 +2,7 @@
 //
 // Every pair whose distance can matter to a row or a column lies within a
 // small radius (the kept ball of Sec. III-B, Eq. 1, or the second minimum of
-// Sec. III-A). With each cloud sorted along a Morton curve, a run of 32
+// Sec. III-A). With each cloud sorted along a Hilbert curve, a run of 32
 // consecutive points occupies a small box, and the dense scans skip every
 // run whose box is provably beyond that radius from the box of their rows
 // (dense.hip). The order only decides which work is skipped: results do not
@@ -10,7 +10,7 @@
 //
 //   k_spatial_sort  one workgroup per (sample, cloud). The frame is the
 //                   bounding cube of both clouds of the sample, quantized to
-//                   10 bits per axis; the 30-bit Morton keys are sorted by a
+//                   10 bits per axis; the 30-bit Hilbert keys are sorted by a
 //                   least-significant-digit radix sort (three 10-bit digits,
 //                   stable: ranks within a wave from ballots, across waves
 //                   from per-wave digit counts in LDS). The sorted points are
@@ -39,6 +39,41 @@ __device__ __forceinline__ uint32_t spread3(uint32_t v)
     v = (v | (v << 4)) & 0x030C30C3u;
     v = (v | (v << 2)) & 0x09249249u;
     return v;
+}
+
+// Position along the Hilbert curve of the cell (x, y, z), 10 bits per axis,
+// by Skilling's transposition ("Programming the Hilbert curve", 2004): the
+// axes are turned into the transposed Hilbert index, whose bits interleaved
+// give the 30-bit key. Consecutive keys are adjacent cells, so a run of
+// consecutive points stays compact (a Morton order jumps across the space).
+__device__ __forceinline__ uint32_t hilbert_key(uint32_t x, uint32_t y, uint32_t z)
+{
+    uint32_t X[3] = {x, y, z};
+#pragma unroll
+    for (uint32_t Q = 1u << 9; Q > 1; Q >>= 1) {
+        const uint32_t P = Q - 1;
+#pragma unroll
+        for (int i = 0; i < 3; ++i) {
+            if (X[i] & Q) {
+                X[0] ^= P; // invert the low bits of the first axis
+            } else {       // exchange the low bits of the first axis and axis i
+                const uint32_t t = (X[0] ^ X[i]) & P;
+                X[0] ^= t;
+                X[i] ^= t;
+            }
+        }
+    }
+    X[1] ^= X[0]; // Gray encode
+    X[2] ^= X[1];
+    uint32_t t = 0;
+#pragma unroll
+    for (uint32_t Q = 1u << 9; Q > 1; Q >>= 1)
+        if (X[2] & Q)
+            t ^= Q - 1;
+    X[0] ^= t;
+    X[1] ^= t;
+    X[2] ^= t;
+    return spread3(X[2]) | spread3(X[1]) << 1 | spread3(X[0]) << 2;
 }
 
 __device__ __forceinline__ uint32_t quantize(float v, float lo, float scale)
@@ -118,8 +153,13 @@ __global__ __launch_bounds__(kSortT) void k_spatial_sort(SpatialArgs a)
     SortLds &s = *reinterpret_cast<SortLds *>(lds_raw);
     const int b = blockIdx.x >> 1, cloud = blockIdx.x & 1;
     const int tid = threadIdx.x, lane = lane_id(), wave = tid >> 6;
-    if (blockIdx.x == 0 && tid == 0)
-        *a.ctr = Counters{};
+    if (blockIdx.x == 0 && tid < 2 * kScanSlots) {
+        (&a.ctr->scanned[0][0])[tid] = 0;
+        if (tid == 0) {
+            a.ctr->error = 0;
+            a.ctr->overflow = 0;
+        }
+    }
     const int n = cloud ? a.M : a.N;
     const int pad = cloud ? a.pad_y : a.pad_x;
     const float *pts = (cloud ? a.y : a.x) + (size_t)b * n * 3;
@@ -168,8 +208,8 @@ __global__ __launch_bounds__(kSortT) void k_spatial_sort(SpatialArgs a)
     // keys and the digit histograms of all passes (independent of the order)
     for (int k = tid; k < n; k += kSortT) {
         const float *p = pts + 3 * (size_t)k;
-        const uint32_t key = spread3(quantize(p[0], f[0], scale)) | spread3(quantize(p[1], f[1], scale)) << 1 |
-                             spread3(quantize(p[2], f[2], scale)) << 2;
+        const uint32_t key =
+            hilbert_key(quantize(p[0], f[0], scale), quantize(p[1], f[1], scale), quantize(p[2], f[2], scale));
         k0[k] = key;
         v0[k] = (uint32_t)k;
 #pragma unroll
