@@ -591,6 +591,8 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         ca.waves = crows.waves;
         ca.cnt = dense_tmp.get<int32_t>(BN);
         ca.col_cnt = col_cnt; // cleared by the finalize kernel
+        ca.stage = dense_tmp.get<int32_t>((size_t)BN * kCullStage);
+        ca.wg_over = dense_tmp.get<uint8_t>((size_t)B * ca.waves);
         ca.ctr = dv.ctr;
         cnt = ca.cnt;
     }
@@ -659,7 +661,8 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         ba.tmp_row = tmp.get<int32_t>(nnz);
         ba.tmp_src = tmp.get<int32_t>(nnz);
     }
-    if (skip)
+    const bool cull_over = skip && rb->ctr.overflow; // a row beyond the staging: written by a second pass
+    if (cull_over)
         ca.tmp_col = dense_tmp.get<int32_t>(nnz);
     // pieces of the per-sample Sinkhorn kernels; with staged hits (or the
     // skipping scans) their placement runs in the compaction's (ranking's)
@@ -687,8 +690,11 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
             ca.csr_col = dv.csr_col;
             ca.csr_row = dv.csr_row;
             ca.nnz = nnz;
-            launch_cull_emit_write(ca, s);
-            launch_cull_emit_rank(ca, &dv, place, s);
+            if (cull_over)
+                launch_cull_emit_write(ca, s);
+            launch_cull_emit_order(ca, &dv, place, s);
+            if (cull_over)
+                launch_cull_emit_rank(ca, s);
         } else {
             ea.row_ptr = dv.row_ptr;
             ea.csr_col = dv.csr_col;

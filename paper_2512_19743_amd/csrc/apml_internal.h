@@ -171,20 +171,26 @@ struct CullEmitArgs {
     int B, N, M, pad_x, pad_y, waves;
     int32_t *cnt;        // [B*N] stored pairs per row
     int32_t *col_cnt;    // [B*M] stored pairs per column
-    Counters *ctr;
-    // writing pass and ranking
+    int32_t *stage;      // [B*N][kCullStage] the first columns of each row, in scan order
+    uint8_t *wg_over;    // [B * waves] a row of this workgroup has more than kCullStage pairs
+    Counters *ctr;       // overflow: some row has more than kCullStage pairs
+    // writing pass (rows beyond the staging only) and ordering
     const int32_t *row_ptr; // [B*N+1]
-    int32_t *tmp_col;       // [nnz] each row's columns in scan order
+    int32_t *tmp_col;       // [nnz] the columns of those rows in scan order
     int32_t *csr_col, *csr_row;
     int64_t nnz;
 };
-// Pass 1 counts the candidate support per row and per column; pass 2 (after
-// the offsets are known) writes each row's columns in scan order; the ranking
-// puts them in increasing column order and (pieces_place non-NULL) places the
-// pieces of the per-sample Sinkhorn kernels (place_order) in the same launch.
+constexpr int kCullStage = 16;
+// Pass 1 counts the candidate support per row and per column and keeps each
+// row's first kCullStage columns; the ordering writes every row that fits
+// there in increasing column order and (pieces_place non-NULL) places the
+// pieces of the per-sample Sinkhorn kernels (place_order) in the same
+// launch. Only when a row overflowed does pass 2 (after the offsets are known)
+// write the columns of the overflowing rows, which a ranking then orders.
 void launch_cull_emit_count(const CullEmitArgs &a, hipStream_t s);
 void launch_cull_emit_write(const CullEmitArgs &a, hipStream_t s);
-void launch_cull_emit_rank(const CullEmitArgs &a, const DevPlan *d, int32_t *pieces_place, hipStream_t s);
+void launch_cull_emit_order(const CullEmitArgs &a, const DevPlan *d, int32_t *pieces_place, hipStream_t s);
+void launch_cull_emit_rank(const CullEmitArgs &a, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // sparse structure

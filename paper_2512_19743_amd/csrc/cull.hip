@@ -356,14 +356,16 @@ template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_cull_emit(Cull
     const float4 *sy = a.sy + (size_t)b * a.pad_y;
     const Box *boxes = a.box_y + (size_t)b * (a.pad_y / kRun);
     const int nb = (a.M + kRun - 1) / kRun;
-    const uint32_t keep = valid ? ~0u : 0u; // a lane without a row ignores the columns' balls too
-    int cnt = 0, cols = 0;
+    int cols = 0;
     const int pos0 = valid && WRITE ? a.row_ptr[row] : 0;
-    if (WRITE) {
-        if (wv == 0)
-            acc[0][lane] = 0;
-        __syncthreads();
-    }
+    // pass 2 writes only the rows beyond the staging, in workgroups that have one
+    if (WRITE && !a.wg_over[grp])
+        return;
+    const bool mine = WRITE ? valid && a.row_ptr[row + 1] - pos0 > kCullStage : valid;
+    const uint32_t keep = mine ? ~0u : 0u; // a lane without a row ignores the columns' balls too
+    if (wv == 0)
+        acc[0][lane] = 0;
+    __syncthreads();
     for (int base = 0; base < nb; base += 64) {
         const int r = base + lane;
         bool take = false;
@@ -400,36 +402,49 @@ template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_cull_emit(Cull
                 const int u = __clz(bits);
                 bits &= ~(0x80000000u >> u);
                 const int j = __float_as_int(sy[j0 + u].w);
+                const int slot = atomicAdd(&acc[0][lane], 1); // this row's hits over the waves
                 if (WRITE) {
-                    const int p = pos0 + atomicAdd(&acc[0][lane], 1);
-                    a.tmp_col[p] = j;
-                    a.csr_row[p] = row;
+                    a.tmp_col[pos0 + slot] = j;
+                    a.csr_row[pos0 + slot] = row;
                 } else {
-                    ++cnt;
+                    if (slot < kCullStage)
+                        a.stage[(size_t)row * kCullStage + slot] = j;
                     atomicAdd(&a.col_cnt[(size_t)b * a.M + j], 1);
                 }
             }
         }
     }
     if (!WRITE) {
-        acc[wv][lane] = cnt;
         __syncthreads();
-        if (wv == 0 && valid)
-            a.cnt[row] = acc[0][lane] + acc[1][lane] + acc[2][lane] + acc[3][lane];
+        if (wv == 0) {
+            const int n = acc[0][lane];
+            if (valid)
+                a.cnt[row] = n;
+            if (__ballot(valid && n > kCullStage)) { // rare: pass 2 writes this workgroup's long rows
+                if (lane == 0) {
+                    a.wg_over[grp] = 1;
+                    atomicOr(&a.ctr->overflow, 1u);
+                }
+            } else if (lane == 0) {
+                a.wg_over[grp] = 0;
+            }
+        }
         if (lane == 0)
             atomicAdd(&a.ctr->scanned[1][blockIdx.x % kScanSlots],
                       (unsigned long long)cols * min(kScanRows, a.N - g * kScanRows));
     }
 }
 
-// Increasing column order inside each row: the rank of an entry is the
-// number of entries of its row with a smaller column.
+// Increasing column order inside a row that overflowed the staging: the
+// rank of an entry is the number of entries of its row with a smaller column.
 __device__ __forceinline__ void rank_entry(const CullEmitArgs &a, int64_t e)
 {
     if (e >= a.nnz)
         return;
     const int r = a.csr_row[e];
     const int s0 = a.row_ptr[r], s1 = a.row_ptr[r + 1];
+    if (s1 - s0 <= kCullStage) // ordered from the staging
+        return;
     const int j = a.tmp_col[e];
     int rank = 0;
     for (int t = s0; t < s1; ++t)
@@ -442,21 +457,52 @@ __global__ __launch_bounds__(kBlock) void k_cull_rank(CullEmitArgs a)
     rank_entry(a, (int64_t)blockIdx.x * kBlock + threadIdx.x);
 }
 
-// The ranking (first n_rank blocks) and, in the remaining blocks, the
+// Row r (global) from its staged columns, when they are all there: each goes
+// to the position given by its rank among them.
+__device__ __forceinline__ void order_row(const CullEmitArgs &a, int64_t r)
+{
+    if (r >= (int64_t)a.B * a.N)
+        return;
+    const int s0 = a.row_ptr[r], n = a.row_ptr[r + 1] - s0;
+    if (n > kCullStage) // written and ranked by the overflow passes
+        return;
+    int j[kCullStage];
+#pragma unroll
+    for (int k = 0; k < kCullStage; ++k)
+        j[k] = k < n ? a.stage[r * kCullStage + k] : INT_MAX;
+#pragma unroll
+    for (int k = 0; k < kCullStage; ++k) {
+        int rank = 0;
+#pragma unroll
+        for (int q = 0; q < kCullStage; ++q)
+            rank += j[q] < j[k];
+        if (k < n) {
+            a.csr_col[s0 + rank] = j[k];
+            a.csr_row[s0 + k] = (int)r;
+        }
+    }
+}
+
+// The ordering (first n_rows blocks) and, in the remaining blocks, the
 // placement of the per-sample Sinkhorn pieces (block k: sample k / 2, order
 // k % 2): independent work in one launch, so the placement runs on the CUs
-// the ranking leaves free.
+// the ordering leaves free.
 constexpr int kFusedT = kSinkLanes;
 
-__global__ __launch_bounds__(kFusedT) void k_cull_rank_place(CullEmitArgs a, DevPlan d, int32_t *place, int n_rank)
+__global__ __launch_bounds__(kFusedT) void k_cull_order_place(CullEmitArgs a, DevPlan d, int32_t *place, int n_rows)
 {
     __shared__ int hist[8], base[8];
-    if ((int)blockIdx.x < n_rank) {
-        rank_entry(a, (int64_t)blockIdx.x * kFusedT + threadIdx.x);
+    if ((int)blockIdx.x < n_rows) {
+        order_row(a, (int64_t)blockIdx.x * kFusedT + threadIdx.x);
         return;
     }
-    const int k = blockIdx.x - n_rank;
+    const int k = blockIdx.x - n_rows;
     pieces::place_order(d, place, k / 2, k % 2 == 0, hist, base);
+}
+
+__global__ __launch_bounds__(kBlock) void k_cull_order(CullEmitArgs a)
+{
+    order_row(a, (int64_t)blockIdx.x * kBlock + threadIdx.x);
 }
 
 } // namespace
@@ -485,14 +531,20 @@ void launch_cull_emit_write(const CullEmitArgs &a, hipStream_t s)
     hipLaunchKernelGGL(k_cull_emit<true>, dim3(a.B * a.waves), dim3(kBlock), 0, s, a);
 }
 
-void launch_cull_emit_rank(const CullEmitArgs &a, const DevPlan *d, int32_t *pieces_place, hipStream_t s)
+void launch_cull_emit_order(const CullEmitArgs &a, const DevPlan *d, int32_t *pieces_place, hipStream_t s)
 {
+    const int64_t rows = (int64_t)a.B * a.N;
     if (pieces_place) {
-        const int nr = (int)blocks_for(a.nnz, kFusedT);
-        hipLaunchKernelGGL(k_cull_rank_place, dim3(nr + 2 * a.B), dim3(kFusedT), 0, s, a, *d, pieces_place, nr);
+        const int nr = (int)blocks_for(rows, kFusedT);
+        hipLaunchKernelGGL(k_cull_order_place, dim3(nr + 2 * a.B), dim3(kFusedT), 0, s, a, *d, pieces_place, nr);
     } else {
-        hipLaunchKernelGGL(k_cull_rank, dim3(blocks_for(a.nnz, kBlock)), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL(k_cull_order, dim3(blocks_for(rows, kBlock)), dim3(kBlock), 0, s, a);
     }
+}
+
+void launch_cull_emit_rank(const CullEmitArgs &a, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_cull_rank, dim3(blocks_for(a.nnz, kBlock)), dim3(kBlock), 0, s, a);
 }
 
 } // namespace apml
