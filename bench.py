@@ -25,9 +25,12 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "APML fwd+bwd point-pairs/s (B=32, N=M=2048 fp32); peak HBM MB"
-# MI355X: 256 CUs x 4 SIMD x 16 lanes at 2.4 GHz, one 32-bit VALU operation per
-# lane per clock (packed FP32 not used).
-VALU_PEAK_OPS = 256 * 64 * 2.4e9
+# MI355X FP32 vector peak, 157.3 TFLOP/s, in 32-bit VALU lane operations: 128
+# lanes per CU per clock (256 CUs, 2.4 GHz; an FMA counts two flops). The
+# library does not use packed FP32, so one instruction stream reaches half of
+# it (64 lanes per CU per clock, measured); v_min co-issues with other VALU
+# work, so a mix such as the statistics scan's goes above that half.
+VALU_PEAK_OPS = 157.3e12 / 2
 HBM_PEAK = 8.0e12
 # Algorithmic VALU operations per pair and direction of the statistics scan:
 # 3 subtractions, 1 multiply, 2 fused multiply-adds (squared distance) and
@@ -43,21 +46,27 @@ OPS_PER_PAIR_DIR = 8
 # softmaxes 24 B, Sinkhorn 8 B per entry and half-step forward (+8 B for the
 # loss) and 16 B per entry and half-step in reverse, softmax/temperature
 # adjoint 24 B + distance gradient 8 B.
-def _ops(per_pair):
-    return lambda w, pairs, nnz: per_pair * pairs
+# The dense phases count the pairs their scans evaluate (every pair in the
+# full scans; the skipping scans of large samples skip pairs that cannot
+# matter and report how many they evaluated).
+def _ops(per_pair, which):
+    return lambda w, scanned, nnz: per_pair * scanned[which]
 
 
 def _bytes(per_entry_fn):
-    return lambda w, pairs, nnz: per_entry_fn(w) * nnz
+    return lambda w, scanned, nnz: per_entry_fn(w) * nnz
 
 
 PHASE_MODEL = {
-    "stats": ("alu", _ops(2 * OPS_PER_PAIR_DIR), "VALU ops",
-              "k_top2: minimum and second minimum of every row and column"),
-    "support": ("alu", _ops(OPS_PER_PAIR_DIR), "VALU ops",
-                "k_emit: radius test of every pair, counts and staged hits of the candidate support"),
+    "stats": ("alu", _ops(OPS_PER_PAIR_DIR, 0), "VALU ops",
+              {"full": "k_top2: minimum and second minimum of every row and column",
+               "skip": "k_spatial_sort + k_cull_top2: curve order, then the minima over the runs that can matter"}),
+    "support": ("alu", _ops(OPS_PER_PAIR_DIR, 1), "VALU ops",
+                {"full": "k_emit: radius test of every pair, counts and staged hits of the candidate support",
+                 "skip": "k_cull_emit: radius test over the runs that can matter, counts and staged hits"}),
     "build": ("hbm", _bytes(lambda w: 16), "bytes",
-              "k_emit_compact_place: row-major structure from the staged hits, placement of the Sinkhorn pieces"),
+              {"full": "k_emit_compact_place: row-major structure from the staged hits, placement of the Sinkhorn pieces",
+               "skip": "k_cull_order_place: row-major structure from the staged hits, placement of the Sinkhorn pieces"}),
     "softmax": ("hbm", _bytes(lambda w: 32 + 24), "bytes",
                 "k_csc_rows + k_col_softmax: column-major view, Eq. 1, Eq. 2, P0"),
     "sinkhorn": ("hbm", _bytes(lambda w: 2 * w.n_iter * 8 + 8), "bytes",
@@ -259,14 +268,17 @@ def main():
 
     pairs = w.B * w.N * w.M
     value = pairs / (ms * 1e-3)
+    scan_mode = "skip" if scanned[0] < 2 * pairs else "full"
     nnz_total = int(nnz.sum())
     kernels = {}
     for name, (tot_ms, n) in phases.items():
         if n == 0 or name not in PHASE_MODEL:
             continue
         bound, per, unit_kind, what = PHASE_MODEL[name]
+        if isinstance(what, dict):
+            what = what[scan_mode]
         avg = tot_ms / n
-        work = per(w, pairs, nnz_total)
+        work = per(w, scanned, nnz_total)
         achieved = work / (avg * 1e-3)
         peak = VALU_PEAK_OPS if bound == "alu" else HBM_PEAK
         kernels[name] = {"kernel": what, "bound": bound, "avg_launch_ms": avg, "launches_per_step": n / args.steps,
@@ -297,7 +309,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"config {w.cfg} ({w.name}): B={w.B} N={w.N} M={w.M} L={w.n_iter}, "
                                f"{w.reference} reference, {w.prediction} prediction sigma={w.sigma}",
-                   "B": w.B, "N": w.N, "M": w.M, "n_iter": w.n_iter, "tau": 1e-8, "p_min": 0.8},
+                   "B": w.B, "N": w.N, "M": w.M, "n_iter": w.n_iter, "tau": 1e-8, "p_min": 0.8,
+                   "dense_scan": scan_mode},
         "roofline": roofline,
         "peak_hbm_mb": mem["peak_in_use"] / 1e6,
         "support": {"nnz_total": nnz_total, "nnz_per_row": nnz_total / (w.B * w.N),
