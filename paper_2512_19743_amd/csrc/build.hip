@@ -33,11 +33,19 @@ __global__ __launch_bounds__(kOffT) void k_sample_scan(const int32_t *cnt, int S
         const int k = base + tid;
         int len = 0;
         if (k < n) {
-            if (rows)
-                for (int c = 0; c < S; ++c)
-                    len += cnt[((size_t)b * N + k) * S + c];
-            else
+            if (rows) {
+                const int32_t *rc = cnt + ((size_t)b * N + k) * S;
+                int c = 0;
+                if (S % 4 == 0) // the row's chunk counts in 16-byte loads, all in flight together
+                    for (; c < S; c += 4) {
+                        const int4 v = *reinterpret_cast<const int4 *>(rc + c);
+                        len += v.x + v.y + v.z + v.w;
+                    }
+                for (; c < S; ++c)
+                    len += rc[c];
+            } else {
                 len = col_cnt[(size_t)b * M + k];
+            }
             const int np = sink_pieces(len);
             pos += 1 << min(sink_log2_group(np), 30);
             mx = max(mx, np);
