@@ -55,6 +55,43 @@ struct Memory {
     int live_plans = 0;
 };
 
+// Mapped pinned host memory for the forward's read-back block, one buffer per
+// device, grown on demand; callers hold mu from the launch that writes it to
+// the copy that reads it.
+struct Pinned {
+    std::mutex mu;
+    void *host[64] = {};
+    void *dev[64] = {};
+    size_t bytes[64] = {};
+    void *get(int device, size_t n)
+    {
+        if (device < 0 || device >= 64)
+            return nullptr;
+        if (bytes[device] < n) {
+            if (host[device])
+                (void)hipHostFree(host[device]);
+            host[device] = dev[device] = nullptr;
+            bytes[device] = 0;
+            const size_t want = std::max<size_t>(n, 4096);
+            if (hipHostMalloc(&host[device], want, hipHostMallocMapped | hipHostMallocPortable) != hipSuccess)
+                return host[device] = nullptr;
+            if (hipHostGetDevicePointer(&dev[device], host[device], 0) != hipSuccess) {
+                (void)hipHostFree(host[device]);
+                return host[device] = nullptr;
+            }
+            bytes[device] = want;
+        }
+        return host[device];
+    }
+    void *device_ptr(int device) const { return dev[device]; }
+};
+
+Pinned &pinned()
+{
+    static Pinned *p = new Pinned(); // never destroyed: outlives every plan
+    return *p;
+}
+
 Memory &mem()
 {
     static Memory m;
@@ -602,6 +639,12 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     std::vector<uint8_t> rb_host(readback_bytes(B));
     if (tmp.failed || dense_tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (support)");
+    // the kernels write the read-back block straight into pinned host memory
+    // (no copy launch); the buffer is shared, so it is held until copied out
+    std::unique_lock<std::mutex> pin_lock(pinned().mu);
+    Readback *rb_pin = (Readback *)pinned().get(plan->device, readback_bytes(B));
+    if (!rb_pin)
+        return fail(APML_ERR_OUT_OF_MEMORY, "pinned host allocation failed (read-back)");
     Readback *rb = (Readback *)rb_host.data();
     const int64_t *totals = readback_totals(rb);
     const int32_t *offsets = readback_offsets(rb, B), *pieces = readback_pieces(rb, B);
@@ -615,9 +658,12 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         pt.stop();
     }
     // row and column offsets, and what the host needs, in one copy
-    launch_offsets(cnt, cnt_chunks, col_cnt, dv.ctr, B, N, M, dv.row_ptr, dv.col_ptr, rb_dev, s);
-    HIP_TRY(hipMemcpyAsync(rb_host.data(), rb_dev, readback_bytes(B), hipMemcpyDeviceToHost, s));
+    launch_offsets(cnt, cnt_chunks, col_cnt, dv.ctr, B, N, M, dv.row_ptr, dv.col_ptr, rb_dev,
+                   (Readback *)pinned().device_ptr(plan->device), s);
+    HIP_TRY(hipGetLastError());
     HIP_TRY(wait_for(s));
+    std::memcpy(rb_host.data(), rb_pin, readback_bytes(B));
+    pin_lock.unlock();
     int64_t nnz = 0;
     for (int b = 0; b < B; ++b) {
         if (totals[b] != totals[B + b])

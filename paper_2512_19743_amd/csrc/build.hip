@@ -20,7 +20,8 @@ constexpr int kOffT = 1024;
 // sample-local exclusive scan of the owners' pair counts into row_ptr /
 // col_ptr, the sample's total and its piece counts.
 __global__ __launch_bounds__(kOffT) void k_sample_scan(const int32_t *cnt, int S, const int32_t *col_cnt, int N,
-                                                       int M, int32_t *row_ptr, int32_t *col_ptr, Readback *rb)
+                                                       int M, int32_t *row_ptr, int32_t *col_ptr, Readback *rb,
+                                                       Readback *rb_host)
 {
     __shared__ int wsum[kOffT / 64];
     __shared__ int red[2][kOffT / 64];
@@ -85,7 +86,8 @@ __global__ __launch_bounds__(kOffT) void k_sample_scan(const int32_t *cnt, int S
             m = max(m, red[1][w]);
         }
         readback_totals(rb)[(rows ? 0 : B) + b] = carry;
-        int32_t *pc = readback_pieces(rb, B) + 4 * b;
+        readback_totals(rb_host)[(rows ? 0 : B) + b] = carry;
+        int32_t *pc = readback_pieces(rb_host, B) + 4 * b;
         pc[rows ? 0 : 1] = a;
         pc[rows ? 2 : 3] = m;
     }
@@ -95,27 +97,28 @@ __global__ __launch_bounds__(kOffT) void k_sample_scan(const int32_t *cnt, int S
 // offsets, closes row_ptr / col_ptr with the total and fills the read-back
 // offsets and counters.
 __global__ __launch_bounds__(kOffT) void k_sample_base(const Counters *ctr, int N, int M, int32_t *row_ptr,
-                                                       int32_t *col_ptr, Readback *rb)
+                                                       int32_t *col_ptr, const Readback *rb, Readback *rb_host)
 {
     __shared__ int base_s;
     const int b = blockIdx.x, rows = blockIdx.y == 0, tid = threadIdx.x, B = gridDim.x;
-    const int64_t *tot = readback_totals(rb) + (rows ? 0 : B);
+    const int64_t *tot = readback_totals(const_cast<Readback *>(rb)) + (rows ? 0 : B);
     if (tid == 0) {
         int64_t base = 0;
         for (int k = 0; k < b; ++k)
             base += tot[k];
         base_s = (int)base; // the host rejects totals beyond int32 before using any offset
         if (rows)
-            readback_offsets(rb, B)[b] = (int)base;
+            readback_offsets(rb_host, B)[b] = (int)base;
         if (b == B - 1) {
             const int end = (int)(base + tot[b]);
             (rows ? row_ptr[(size_t)B * N] : col_ptr[(size_t)B * M]) = end;
             if (rows)
-                readback_offsets(rb, B)[B] = end;
+                readback_offsets(rb_host, B)[B] = end;
         }
-        if (b == 0 && rows)
-            rb->ctr = *ctr;
     }
+    if (b == 0 && rows) // the counters, word by word over the workgroup
+        for (int i = tid; i < (int)(sizeof(Counters) / 4); i += kOffT)
+            reinterpret_cast<uint32_t *>(&rb_host->ctr)[i] = reinterpret_cast<const uint32_t *>(ctr)[i];
     __syncthreads();
     const int n = rows ? N : M;
     int32_t *out = rows ? row_ptr + (size_t)b * N : col_ptr + (size_t)b * M;
@@ -186,10 +189,11 @@ __global__ __launch_bounds__(kBlock) void k_count_support(const int32_t *row_ptr
 } // namespace
 
 void launch_offsets(const int32_t *cnt, int S, const int32_t *col_cnt, const Counters *ctr, int B, int N, int M,
-                    int32_t *row_ptr, int32_t *col_ptr, Readback *rb, hipStream_t s)
+                    int32_t *row_ptr, int32_t *col_ptr, Readback *rb, Readback *rb_host, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_sample_scan, dim3(B, 2), dim3(kOffT), 0, s, cnt, S, col_cnt, N, M, row_ptr, col_ptr, rb);
-    hipLaunchKernelGGL(k_sample_base, dim3(B, 2), dim3(kOffT), 0, s, ctr, N, M, row_ptr, col_ptr, rb);
+    hipLaunchKernelGGL(k_sample_scan, dim3(B, 2), dim3(kOffT), 0, s, cnt, S, col_cnt, N, M, row_ptr, col_ptr, rb,
+                       rb_host);
+    hipLaunchKernelGGL(k_sample_base, dim3(B, 2), dim3(kOffT), 0, s, ctr, N, M, row_ptr, col_ptr, rb, rb_host);
 }
 
 void launch_csc_build(const DevPlan &d, const BuildArgs &a, hipStream_t s)
