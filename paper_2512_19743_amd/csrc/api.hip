@@ -577,6 +577,10 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         sa.box_x = dense_tmp.get<Box>((size_t)B * pad_x / kRun);
         sa.box_y = dense_tmp.get<Box>((size_t)B * pad_y / kRun);
         sa.ctr = dv.ctr;
+        if (std::max(N, M) > kSortChunkPoints) { // chunked sort: the frame from partial boxes
+            sa.frame_slices = ceil_div((int64_t)N + M, 16384);
+            sa.frame_part = dense_tmp.get<float>((size_t)B * sa.frame_slices * 6);
+        }
         crows.own = sa.sx;
         crows.bc = sa.sy;
         crows.own_box = sa.box_x;

@@ -127,11 +127,16 @@ struct SpatialArgs {
     const float *x, *y; // [B, N, 3], [B, M, 3]
     int B, N, M, pad_x, pad_y;
     uint32_t *key[2], *val[2]; // scratch: [B * pad_x + B * pad_y] each
+    float *frame_part;         // scratch [B][frame_slices][6] when a cloud exceeds one sort chunk, else NULL
+    int frame_slices;
     float4 *sx, *sy;           // out: sorted clouds
     Box *box_x, *box_y;        // out: boxes of the runs
     Counters *ctr;             // cleared here
 };
 size_t spatial_sort_lds();
+// Points one workgroup of the spatial sort takes; larger clouds are sorted in
+// chunks, then merged.
+constexpr int kSortChunkPoints = 8192;
 hipError_t launch_spatial_sort(const SpatialArgs &a, hipStream_t s);
 
 // One direction of the minimum / second-minimum scan: owners (X for rows, Y

@@ -185,7 +185,7 @@ def test_config2_full_batch(scan):
     note(f"config 2 nnz per sample: {[r['nnz_gpu'] for r in res[:4]]} flips {sum(r['flips'] for r in res)}")
 
 
-@pytest.mark.parametrize("cfg,scan", [(3, None), (4, None), (4, "full")])
+@pytest.mark.parametrize("cfg,scan", [(3, None), (4, None), (4, "full"), (4, "skip")])
 def test_large_configs_one_sample_exact(cfg, scan):
     # the whole batch runs on the GPU; sample 0 is checked against a full oracle run
     w = config(cfg)
