@@ -599,6 +599,10 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         ccols.pad_own = pad_y;
         ccols.pad_bc = pad_x;
         ccols.waves = ceil_div(M, kScanRows);
+        Box *batch_x = dense_tmp.get<Box>((size_t)B * batches(pad_x));
+        Box *batch_y = dense_tmp.get<Box>((size_t)B * batches(pad_y));
+        crows.bc_batch = batch_y;
+        ccols.bc_batch = batch_x;
         crows.m12s = dense_tmp.get<float2>((size_t)B * pad_x);
         ccols.m12s = dense_tmp.get<float2>((size_t)B * pad_y);
         float *E_row = dense_tmp.get<float>((size_t)B * pad_x);
@@ -608,6 +612,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         {
             PhaseTimer pt(PH_STATS, s);
             HIP_TRY(launch_spatial_sort(sa, s)); // also clears the counters
+            launch_batch_boxes(sa.box_x, sa.box_y, batch_x, batch_y, B, pad_x, pad_y, false, s);
             launch_cull_top2(crows, ccols, B, dv.ctr, s);
             HIP_TRY(hipGetLastError());
             pt.stop();
@@ -617,6 +622,8 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         CullFinalizeDir fc{ccols.m12s, sa.sy, dv.m12_col, nullptr, ypack, sa.box_y, col_cnt, ba.col_fill, M, pad_y,
                            kp.lk_col};
         launch_cull_finalize(fr, fc, B, kp, s);
+        // the column batches again, now with their largest emission threshold
+        launch_batch_boxes(sa.box_x, sa.box_y, batch_x, batch_y, B, pad_x, pad_y, true, s);
         HIP_TRY(hipGetLastError());
 
         // ---- dense scan 2: candidate support -----------------------------
@@ -626,6 +633,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         ca.sy = sa.sy;
         ca.box_x = sa.box_x;
         ca.box_y = sa.box_y;
+        ca.batch_y = batch_y;
         ca.B = B;
         ca.N = N;
         ca.M = M;

@@ -133,6 +133,13 @@ struct SpatialArgs {
     Box *box_x, *box_y;        // out: boxes of the runs
     Counters *ctr;             // cleared here
 };
+// Batches of 64 runs (2048 sorted points): the scans test a batch's box
+// before its runs'.
+__host__ __device__ inline int batches(int pad) { return (pad / kRun + 63) / 64; }
+// The box of every batch of runs of both sorted clouds (columns_only: of the
+// columns, hi.w the largest of the runs' hi.w).
+void launch_batch_boxes(const Box *box_x, const Box *box_y, Box *batch_x, Box *batch_y, int B, int pad_x, int pad_y,
+                        bool columns_only, hipStream_t s);
 size_t spatial_sort_lds();
 // Points one workgroup of the spatial sort takes; larger clouds are sorted in
 // chunks, then merged.
@@ -145,6 +152,7 @@ struct CullDir {
     const float4 *own, *bc; // sorted owners [B][pad_own] and other cloud [B][pad_bc]
     const Box *own_box;     // [B][pad_own / kRun]
     const Box *bc_box;      // [B][pad_bc / kRun]
+    const Box *bc_batch;    // [B][batches(pad_bc)]: union of the boxes of 64 consecutive runs
     float2 *m12s;           // out [B][pad_own]: (min, second min) of the squared distance, sorted position
     int n_own, n_bc, pad_own, pad_bc;
     int waves;              // per sample: ceil(n_own / kScanRows)
@@ -173,6 +181,7 @@ struct CullEmitArgs {
     const float4 *sy;    // sorted columns with their original index [B][pad_y]
     const Box *box_x;    // [B][pad_x / kRun]
     const Box *box_y;    // [B][pad_y / kRun]
+    const Box *batch_y;  // [B][batches(pad_y)]: union of 64 runs' boxes, hi.w their largest column threshold
     int B, N, M, pad_x, pad_y, waves;
     int32_t *cnt;        // [B*N] stored pairs per row
     int32_t *col_cnt;    // [B*M] stored pairs per column

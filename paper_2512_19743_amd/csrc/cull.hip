@@ -216,7 +216,16 @@ __global__ __launch_bounds__(kBlock) void k_cull_top2(Top2Args args)
         scan_run(home);
     const int nbatch = (nb + 63) / 64;
     int base = home / 64 * 64;
-    for (int t = 0; t < nbatch; ++t) {
+    const_ptr<f32x4> batch = as_const(reinterpret_cast<const f32x4 *>(d.bc_batch + (size_t)b * batches(d.pad_bc)));
+    for (int t = 0; t < nbatch; ++t, base = base + 64 >= nbatch * 64 ? 0 : base + 64) {
+        // the whole batch first: its box against the largest current bound
+        {
+            const f32x4 lo = batch[2 * (base / 64)], hi = batch[2 * (base / 64) + 1];
+            const float g2 = box_gap2(wb, make_float4(lo.x, lo.y, lo.z, 0.0f), make_float4(hi.x, hi.y, hi.z, 0.0f));
+            const float lb = bound();
+            if (g2 > wave_max_nonneg(valid ? lb : 0.0f))
+                continue;
+        }
         const int r = base + lane;
         bool live = r < nb && r != home && r % kWaves == wv;
         float4 blo = make_float4(0.0f, 0.0f, 0.0f, 0.0f), bhi = blo;
@@ -244,9 +253,6 @@ __global__ __launch_bounds__(kBlock) void k_cull_top2(Top2Args args)
             if (__ballot(valid && !(pg > lb)))
                 scan_run(base + i);
         }
-        base += 64;
-        if (base >= nbatch * 64)
-            base = 0;
     }
     __syncthreads();
     if (wv == 0) {
@@ -366,7 +372,14 @@ template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_cull_emit(Cull
     if (wv == 0)
         acc[0][lane] = 0;
     __syncthreads();
+    const_ptr<f32x4> batch = as_const(reinterpret_cast<const f32x4 *>(a.batch_y + (size_t)b * batches(a.pad_y)));
     for (int base = 0; base < nb; base += 64) {
+        { // the whole batch first
+            const f32x4 lo = batch[2 * (base / 64)], hi = batch[2 * (base / 64) + 1];
+            const float g2 = box_gap2(wb, make_float4(lo.x, lo.y, lo.z, 0.0f), make_float4(hi.x, hi.y, hi.z, 0.0f));
+            if (g2 > fmaxf(wave_E, hi.w))
+                continue;
+        }
         const int r = base + lane;
         bool take = false;
         float4 blo = make_float4(0.0f, 0.0f, 0.0f, 0.0f), bhi = blo;
