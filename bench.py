@@ -120,7 +120,7 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--memory-sweep", action="store_true",
                     help="only measure peak library memory and time of one forward+backward at B=1, "
-                         "N=M in 1k..64k (shape-completion generator), one JSON line per size")
+                         "N=M in 1k..256k (shape-completion generator), one JSON line per size")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (5 times), to scale HBM byte counters")
     return ap.parse_args()
@@ -150,7 +150,7 @@ def memory_sweep():
     from workloads import custom
 
     apml.load()
-    sizes = [1024, 2048, 4096, 8192, 16384, 32768, 65536]
+    sizes = [1024, 2048, 4096, 8192, 16384, 32768, 65536, 131072, 262144]
     pts, peaks = [], []
     for n in sizes:
         X, Y = custom(n, 1, n, n, reference="primitives", prediction="perm_noise", sigma=0.05)
@@ -184,8 +184,11 @@ def memory_sweep():
         peak = apml.apml_get_memory_stats()["peak_in_use"]
         pts.append(2 * n)
         peaks.append(peak)
+        # one dense fp32 N x M matrix, the least a dense formulation holds
         print(json.dumps({"N": n, "M": n, "B": 1, "nnz": nnz, "peak_library_mb": peak / 1e6,
-                          "bytes_per_point": peak / (2 * n), "ms_fwd_bwd": statistics.median(times)}), flush=True)
+                          "bytes_per_point": peak / (2 * n), "dense_matrix_mb": 4.0 * n * n / 1e6,
+                          "ms_fwd_bwd": statistics.median(times)}), flush=True)
+        del x, y
     A = np.vstack([np.asarray(pts, float), np.ones(len(pts))]).T
     slope, icpt = np.linalg.lstsq(A, np.asarray(peaks, float), rcond=None)[0]
     print(json.dumps({"fit": "peak_bytes = a * (N + M) + b", "a_bytes_per_point": slope, "b_bytes": icpt}), flush=True)

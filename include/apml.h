@@ -69,6 +69,22 @@ typedef void *apml_stream;
  * when min(N, M) >= 8192. */
 typedef enum { APML_SCAN_AUTO = 0, APML_SCAN_FULL = 1, APML_SCAN_SKIP = 2 } apml_scan_mode;
 
+/* Readings of the paper where it offers two (for ablation; the defaults are
+ * the first of each).
+ * gap_mode  CLAMP: g = max(C2 - C1 + delta, eps_gap) (Sec. III-D).
+ *           UNIFORM_FALLBACK: an owner whose gap C2 - C1 is below eps_gap
+ *           gets P = 1/K on all K pairs (Sec. III-A, Sec. III-C); all of its
+ *           pairs are stored and no gradient flows through that softmax.
+ * sym_mode  HALF_SUM: P0 = (P_row + P_col)/2 with an absent side 0 (the
+ *           dense initial plan of Sec. III-A on the union support).
+ *           MEAN_DUP: duplicates averaged (Sec. III-C, Alg. 1 step 3) and a
+ *           pair kept by one direction only keeps that direction's value.
+ * tgrad_mode FULL: the gradient reaches the costs through the temperatures
+ *           (Eq. 1); DETACHED: the temperatures are constants in backward. */
+typedef enum { APML_GAP_CLAMP = 0, APML_GAP_UNIFORM_FALLBACK = 1 } apml_gap_mode;
+typedef enum { APML_SYM_HALF_SUM = 0, APML_SYM_MEAN_DUP = 1 } apml_sym_mode;
+typedef enum { APML_TGRAD_FULL = 0, APML_TGRAD_DETACHED = 1 } apml_tgrad_mode;
+
 typedef struct apml_params {
     uint32_t struct_size; /* sizeof(apml_params), for forward compatibility */
     int32_t n_iter;       /* L_iter >= 0: Sinkhorn iterations (Alg. 1) */
@@ -79,7 +95,9 @@ typedef struct apml_params {
     double eps_gap;       /* > 0, gap clamp max(gap, eps_gap) (Sec. III-D) */
     double eps_dist;      /* >= 0, added to ||x - y|| in the gradient only (Eq. 5) */
     int32_t dense_scan;   /* apml_scan_mode: how the two dense scans visit the pairs */
-    int32_t reserved;     /* 0 */
+    int32_t gap_mode;     /* apml_gap_mode (default CLAMP) */
+    int32_t sym_mode;     /* apml_sym_mode (default HALF_SUM) */
+    int32_t tgrad_mode;   /* apml_tgrad_mode (default FULL) */
 } apml_params;
 
 /* Fills *p with the defaults above (p must not be NULL). */

@@ -47,18 +47,21 @@ class Params(ctypes.Structure):
         ("eps_gap", ctypes.c_double),
         ("eps_dist", ctypes.c_double),
         ("n_iter", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("gap_mode", ctypes.c_int32),    # 0 clamp, 1 uniform fallback
+        ("sym_mode", ctypes.c_int32),    # 0 half sum, 1 mean of the present sides
+        ("tgrad_mode", ctypes.c_int32),  # 0 full, 1 temperature detached
     ]
 
 
-DEFAULTS = dict(p_min=0.8, tau=1e-8, eps_stab=1e-8, delta=1e-8, eps_gap=1e-6, eps_dist=1e-12, n_iter=10)
+DEFAULTS = dict(p_min=0.8, tau=1e-8, eps_stab=1e-8, delta=1e-8, eps_gap=1e-6, eps_dist=1e-12, n_iter=10,
+                gap_mode=0, sym_mode=0, tgrad_mode=0)
 
 
 def params(**kw) -> Params:
     d = dict(DEFAULTS)
     d.update(kw)
     return Params(d["p_min"], d["tau"], d["eps_stab"], d["delta"], d["eps_gap"], d["eps_dist"],
-                  int(d["n_iter"]), 0)
+                  int(d["n_iter"]), int(d["gap_mode"]), int(d["sym_mode"]), int(d["tgrad_mode"]))
 
 
 def _load():

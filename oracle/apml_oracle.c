@@ -44,6 +44,16 @@
  *   R8  eps_dist appears only in the gradient (Eq. 5), not in the forward cost.
  *   R9  No gradient flows through the choice of the support or of the argmins.
  *
+ * Variants (selected by orc_params, for ablation):
+ *   gap_mode = 1     uniform fallback instead of the clamp: an owner whose gap
+ *                    C2 - C1 is below eps_g gets P = 1/K on all K entries
+ *                    (Sec. III-A; the kernel of Sec. III-C writes it), which is
+ *                    the softmax at T = 0; no gradient flows through it.
+ *   sym_mode = 1     duplicates averaged literally (Sec. III-C, Alg. 1 step 3):
+ *                    P0 = (P_row + P_col)/2 where both directions keep the
+ *                    pair, the one present value elsewhere.
+ *   tgrad_mode = 1   the temperature is a constant in the backward pass.
+ *
  * Build: gcc -O2 -fopenmp -ffp-contract=off -fPIC -shared (fmaf is the
  * correctly rounded C library fused multiply-add).
  */
@@ -63,8 +73,14 @@ typedef struct {
     double eps_gap;  /* gap clamp (Sec. III-D) */
     double eps_dist; /* distance-gradient guard (Eq. 5) */
     int32_t n_iter;  /* L_iter */
-    int32_t reserved;
+    int32_t gap_mode;   /* 0: clamp (Sec. III-D); 1: uniform fallback (Sec. III-A, III-C) */
+    int32_t sym_mode;   /* 0: P0 = (P_row + P_col)/2, absent side 0; 1: mean of the present sides */
+    int32_t tgrad_mode; /* 0: full gradient; 1: temperature treated as a constant */
 } orc_params;
+
+enum { ORC_GAP_CLAMP = 0, ORC_GAP_FALLBACK = 1 };
+enum { ORC_SYM_HALF_SUM = 0, ORC_SYM_MEAN_DUP = 1 };
+enum { ORC_TGRAD_FULL = 0, ORC_TGRAD_DETACHED = 1 };
 
 enum { ORC_ROW = 1, ORC_COL = 2 };
 enum { ORC_OK = 0, ORC_BAD_ARG = 1, ORC_NO_MEMORY = 2 };
@@ -100,12 +116,12 @@ static double cost(const double *a, const double *b)
 /* Per-owner statistics of one direction. "Owner" is a row (a point of X) in
  * the row direction and a column (a point of Y) in the column direction. */
 typedef struct {
-    double T;      /* temperature, Eq. 1 */
+    double T;      /* temperature, Eq. 1 (0 for a uniform fallback) */
     double c1;     /* minimum cost of the owner */
     double g;      /* clamped gap */
     int32_t k1;    /* index of the minimum */
     int32_t k2;    /* index of the second minimum */
-    uint8_t clamped;
+    uint8_t clamped; /* the gap was clamped, or the fallback taken: no temperature gradient */
 } owner_stats;
 
 /* Minimum, second minimum, gap and temperature of the cost vector between
@@ -136,6 +152,12 @@ static void owner_statistics(const double *p, const double *Q, int K, const orc_
     st->g = st->clamped ? prm->eps_gap : gap;
     /* Eq. 1: T = -log((1 - p_min) / ((K - 1) p_min)) / g */
     st->T = -log((1.0 - prm->p_min) / ((double)(K - 1) * prm->p_min)) / st->g;
+    if (prm->gap_mode == ORC_GAP_FALLBACK && c2 - st->c1 < prm->eps_gap) {
+        /* uniform fallback: s = 1 for every entry, all kept, P = 1/K */
+        st->T = 0.0;
+        st->g = gap;
+        st->clamped = 1;
+    }
 }
 
 /* Unnormalised similarity s = exp(-T (C - C_min)) (Sec. III-B). */
@@ -277,6 +299,8 @@ static int valid(int N, int M, const orc_params *p)
         return 0;
     if (!(p->delta >= 0.0) || !(p->eps_gap > 0.0) || !(p->eps_stab >= 0.0) || !(p->eps_dist >= 0.0))
         return 0;
+    if ((unsigned)p->gap_mode > 1u || (unsigned)p->sym_mode > 1u || (unsigned)p->tgrad_mode > 1u)
+        return 0;
     return 1;
 }
 
@@ -371,7 +395,10 @@ int orc_run(const double *x, const double *y, int N, int M, const orc_params *pr
             r->p_col[e] = items[t].val;
     }
     for (int64_t t = 0; t < nnz; ++t) {
-        r->p0[t] = 0.5 * (r->p_row[t] + r->p_col[t]); /* initial plan P0 = (P_row + P_col)/2 */
+        if (prm->sym_mode == ORC_SYM_MEAN_DUP && r->ef[t] != (ORC_ROW | ORC_COL))
+            r->p0[t] = r->p_row[t] + r->p_col[t]; /* one side present: its value */
+        else
+            r->p0[t] = 0.5 * (r->p_row[t] + r->p_col[t]); /* initial plan P0 = (P_row + P_col)/2 */
         r->C[t] = cost(x + 3 * (size_t)r->ei[t], y + 3 * (size_t)r->ej[t]);
     }
     free(items);
@@ -447,17 +474,24 @@ int orc_run(const double *x, const double *y, int N, int M, const orc_params *pr
             for (int64_t t = 0; t < nnz; ++t) /* adjoint of Eq. 3 */
                 vbar[t] = (vbar[t] - colacc[r->ej[t]]) / (S[r->ej[t]] + eps);
         }
-        /* vbar is now dLoss/dP0. P0 = (P_row + P_col)/2 on the union support. */
+        /* vbar is now dLoss/dP0. P0 = (P_row + P_col)/2 on the union support
+         * (or, averaging duplicates literally, the one present value where only
+         * one direction keeps the pair): dP0/dP_row = wgt. */
+        for (int64_t t = 0; t < nnz; ++t) {
+            const double wgt = prm->sym_mode == ORC_SYM_MEAN_DUP && r->ef[t] != (ORC_ROW | ORC_COL) ? 1.0 : 0.5;
+            vbar[t] *= wgt; /* from here on: the adjoint of P_row (and of P_col) */
+        }
         /* Row softmax adjoint: P_row = s / Z over the kept set, s = exp(-T (C - C1)).
-         * abar = P (Pbar - sum P Pbar); Cbar += -T abar; Tbar += -abar (C - C1). */
+         * abar = P (Pbar - sum P Pbar); Cbar += -T abar; Tbar += -abar (C - C1).
+         * A uniform fallback (T = 0) is a constant: nothing flows through it. */
         memset(rowacc, 0, (size_t)N * sizeof(double));
         for (int64_t t = 0; t < nnz; ++t)
             if (r->ef[t] & ORC_ROW)
-                rowacc[r->ei[t]] += r->p_row[t] * 0.5 * vbar[t];
+                rowacc[r->ei[t]] += r->p_row[t] * vbar[t];
         for (int64_t t = 0; t < nnz; ++t)
-            if (r->ef[t] & ORC_ROW) {
+            if ((r->ef[t] & ORC_ROW) && r->row[r->ei[t]].T != 0.0) {
                 const int i = r->ei[t];
-                const double a = r->p_row[t] * (0.5 * vbar[t] - rowacc[i]);
+                const double a = r->p_row[t] * (vbar[t] - rowacc[i]);
                 cbar[t] += -r->row[i].T * a;
                 Tbar_r[i] += -a * (r->C[t] - r->row[i].c1);
             }
@@ -465,11 +499,11 @@ int orc_run(const double *x, const double *y, int N, int M, const orc_params *pr
         memset(colacc, 0, (size_t)M * sizeof(double));
         for (int64_t t = 0; t < nnz; ++t)
             if (r->ef[t] & ORC_COL)
-                colacc[r->ej[t]] += r->p_col[t] * 0.5 * vbar[t];
+                colacc[r->ej[t]] += r->p_col[t] * vbar[t];
         for (int64_t t = 0; t < nnz; ++t)
-            if (r->ef[t] & ORC_COL) {
+            if ((r->ef[t] & ORC_COL) && r->col[r->ej[t]].T != 0.0) {
                 const int j = r->ej[t];
-                const double a = r->p_col[t] * (0.5 * vbar[t] - colacc[j]);
+                const double a = r->p_col[t] * (vbar[t] - colacc[j]);
                 cbar[t] += -r->col[j].T * a;
                 Tbar_c[j] += -a * (r->C[t] - r->col[j].c1);
             }
@@ -480,9 +514,10 @@ int orc_run(const double *x, const double *y, int N, int M, const orc_params *pr
         /* Temperature adjoint: T = L_K / g, g = C2 - C1 + delta unless clamped.
          * gbar = Tbar dT/dg = -Tbar T / g; it reaches the costs of the minimum
          * (with sign -) and of the second minimum (with sign +). */
+        const int detached = prm->tgrad_mode == ORC_TGRAD_DETACHED;
         for (int i = 0; i < N; ++i) {
             const owner_stats *s = &r->row[i];
-            if (s->clamped)
+            if (s->clamped || detached)
                 continue;
             const double gb = -Tbar_r[i] * s->T / s->g;
             push_cost_gradient(x + 3 * (size_t)i, y + 3 * (size_t)s->k2, gb, prm->eps_dist,
@@ -492,7 +527,7 @@ int orc_run(const double *x, const double *y, int N, int M, const orc_params *pr
         }
         for (int j = 0; j < M; ++j) {
             const owner_stats *s = &r->col[j];
-            if (s->clamped)
+            if (s->clamped || detached)
                 continue;
             const double gb = -Tbar_c[j] * s->T / s->g;
             push_cost_gradient(x + 3 * (size_t)s->k2, y + 3 * (size_t)j, gb, prm->eps_dist,

@@ -25,8 +25,13 @@ def _two_smallest(C: torch.Tensor, dim: int) -> Tuple[torch.Tensor, torch.Tensor
 
 def dense_apml(x: torch.Tensor, y: torch.Tensor, *, p_min=0.8, tau=1e-8, n_iter=10, eps_stab=1e-8,
                delta=1e-8, eps_gap=1e-6, row_argmins: Optional[Tuple] = None,
-               col_argmins: Optional[Tuple] = None):
-    """Loss and intermediate matrices for x (N,3), y (M,3) float64 tensors."""
+               col_argmins: Optional[Tuple] = None, gap_mode=0, sym_mode=0, tgrad_mode=0):
+    """Loss and intermediate matrices for x (N,3), y (M,3) float64 tensors.
+
+    gap_mode 1: an owner whose gap C2 - C1 is below eps_gap gets the uniform
+    distribution 1/K over all K entries (a constant). sym_mode 1: P0 is the
+    mean of the directions that keep a pair. tgrad_mode 1: the temperatures
+    are constants (detached)."""
     N, M = x.shape[0], y.shape[0]
     C = torch.sqrt(((x[:, None, :] - y[None, :, :]) ** 2).sum(-1))  # Sec. III-A
     rN, rM = torch.arange(N), torch.arange(M)
@@ -38,7 +43,13 @@ def dense_apml(x: torch.Tensor, y: torch.Tensor, *, p_min=0.8, tau=1e-8, n_iter=
     def temperature(c1, c2, K):
         gap = c2 - c1 + delta
         g = torch.where(gap < eps_gap, torch.full_like(gap, eps_gap), gap)  # Sec. III-D clamp
-        return math.log((K - 1) * p_min / (1 - p_min)) / g  # Eq. 1
+        T = math.log((K - 1) * p_min / (1 - p_min)) / g  # Eq. 1
+        return T.detach() if tgrad_mode == 1 else T
+
+    def fallback(c1, c2):  # uniform fallback (Sec. III-A) where the raw gap is below eps_gap
+        if gap_mode != 1:
+            return torch.zeros_like(c1, dtype=torch.bool)
+        return ((c2 - c1) < eps_gap).detach()
 
     c1r = C[rN, j1]
     Tr = temperature(c1r, C[rN, j2], M)
@@ -46,6 +57,9 @@ def dense_apml(x: torch.Tensor, y: torch.Tensor, *, p_min=0.8, tau=1e-8, n_iter=
     keep_r = (s_row >= tau).detach()
     kr = torch.where(keep_r, s_row, torch.zeros_like(s_row))
     P_row = kr / kr.sum(1, keepdim=True)  # kept-sum normalisation (Sec. III-C)
+    fb_r = fallback(c1r, C[rN, j2])
+    P_row = torch.where(fb_r[:, None], torch.full_like(P_row, 1.0 / M), P_row)
+    keep_r = keep_r | fb_r[:, None]
 
     c1c = C[i1, rM]
     Tc = temperature(c1c, C[i2, rM], N)
@@ -53,8 +67,14 @@ def dense_apml(x: torch.Tensor, y: torch.Tensor, *, p_min=0.8, tau=1e-8, n_iter=
     keep_c = (s_col >= tau).detach()
     kc = torch.where(keep_c, s_col, torch.zeros_like(s_col))
     P_col = kc / kc.sum(0, keepdim=True)
+    fb_c = fallback(c1c, C[i2, rM])
+    P_col = torch.where(fb_c[None, :], torch.full_like(P_col, 1.0 / N), P_col)
+    keep_c = keep_c | fb_c[None, :]
 
-    P0 = 0.5 * (P_row + P_col)  # initial plan on the union support
+    if sym_mode == 1:  # duplicates averaged, a single value kept as is
+        P0 = torch.where(keep_r & keep_c, 0.5 * (P_row + P_col), P_row + P_col)
+    else:
+        P0 = 0.5 * (P_row + P_col)  # initial plan on the union support
     P = P0
     for _ in range(n_iter):  # Eq. 3 then Eq. 4
         P = P / (P.sum(0, keepdim=True) + eps_stab)

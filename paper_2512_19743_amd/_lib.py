@@ -41,7 +41,9 @@ class apml_params(ctypes.Structure):
         ("eps_gap", ctypes.c_double),
         ("eps_dist", ctypes.c_double),
         ("dense_scan", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("gap_mode", ctypes.c_int32),
+        ("sym_mode", ctypes.c_int32),
+        ("tgrad_mode", ctypes.c_int32),
     ]
 
 

@@ -332,6 +332,12 @@ apml_status validate(const float *x, const float *y, int32_t B, int32_t N, int32
         return fail(APML_ERR_INVALID_ARG, "need delta >= 0, eps_gap > 0, eps_stab >= 0, eps_dist >= 0, all finite");
     if (p.dense_scan < APML_SCAN_AUTO || p.dense_scan > APML_SCAN_SKIP)
         return fail(APML_ERR_INVALID_ARG, "dense_scan must be APML_SCAN_AUTO, APML_SCAN_FULL or APML_SCAN_SKIP");
+    if (p.gap_mode != APML_GAP_CLAMP && p.gap_mode != APML_GAP_UNIFORM_FALLBACK)
+        return fail(APML_ERR_INVALID_ARG, "gap_mode must be APML_GAP_CLAMP or APML_GAP_UNIFORM_FALLBACK");
+    if (p.sym_mode != APML_SYM_HALF_SUM && p.sym_mode != APML_SYM_MEAN_DUP)
+        return fail(APML_ERR_INVALID_ARG, "sym_mode must be APML_SYM_HALF_SUM or APML_SYM_MEAN_DUP");
+    if (p.tgrad_mode != APML_TGRAD_FULL && p.tgrad_mode != APML_TGRAD_DETACHED)
+        return fail(APML_ERR_INVALID_ARG, "tgrad_mode must be APML_TGRAD_FULL or APML_TGRAD_DETACHED");
     return APML_OK;
 }
 
@@ -399,7 +405,9 @@ void apml_params_default(apml_params *p)
     p->eps_gap = 1e-6;
     p->eps_dist = 1e-12;
     p->dense_scan = APML_SCAN_AUTO;
-    p->reserved = 0;
+    p->gap_mode = APML_GAP_CLAMP;
+    p->sym_mode = APML_SYM_HALF_SUM;
+    p->tgrad_mode = APML_TGRAD_FULL;
 }
 
 apml_status apml_plan_destroy(apml_plan *plan)
@@ -466,6 +474,9 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     kp.lk_row = log_ratio(M, prm.p_min);
     kp.lk_col = log_ratio(N, prm.p_min);
     kp.n_iter = L;
+    kp.gap_mode = prm.gap_mode;
+    kp.sym_mode = prm.sym_mode;
+    kp.tgrad_mode = prm.tgrad_mode;
 
     const int BN = B * N, BM = B * M;
     Arena tmp, dense_tmp; // dense_tmp: scratch of the dense scans, released once the CSR is written

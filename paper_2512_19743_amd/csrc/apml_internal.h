@@ -31,7 +31,35 @@ struct Params {
     double log_inv_tau;    // log(1/tau); +inf when tau == 0
     double lk_row, lk_col; // -log((1-p) / ((K-1) p)) for rows (K = M) and columns (K = N)
     int n_iter;
+    int gap_mode, sym_mode, tgrad_mode; // apml_gap_mode, apml_sym_mode, apml_tgrad_mode
 };
+
+constexpr int kGapFallback = 1;  // APML_GAP_UNIFORM_FALLBACK
+constexpr int kSymMeanDup = 1;   // APML_SYM_MEAN_DUP
+constexpr int kTgradDetached = 1; // APML_TGRAD_DETACHED
+
+// Squared radius of an owner's emission ball from its single-precision
+// minimum and second minimum m1 <= m2 (log_ratio: Eq. 1's numerator for the
+// owner's direction). The kept set s >= tau is the ball C <= C1 + log(1/tau)/T
+// (Sec. III-B, Eq. 1); the margin covers the rounding of this estimate
+// (relative ~1e-7 (1 + 2 kappa)) and of the single-precision distance; the
+// second minimum is always inside. An owner that may take the uniform
+// fallback (its gap within rounding of eps_gap: the fp32 costs differ from
+// the double ones by ~1.2e-7 relative) gets an infinite radius: every pair is
+// a candidate, and the softmax decides in double precision.
+__device__ inline double emission_radius2(float m1, float m2, double log_ratio, const Params &p)
+{
+    const double c1 = sqrt((double)m1), c2 = sqrt((double)m2);
+    if (p.gap_mode == kGapFallback && (c2 - c1) < p.eps_gap + 1e-5 * (c1 + c2))
+        return HUGE_VAL;
+    const double gap = (c2 - c1) + p.delta;
+    const double g = gap < p.eps_gap ? p.eps_gap : gap;
+    const double kappa = p.log_inv_tau / log_ratio; // log(1/tau) / (T g)
+    const double radius = c1 + g * kappa;
+    const double margin = 1e-5 * (1.0 + kappa);
+    const double e = radius * radius * (1.0 + margin);
+    return fmax(e, (double)m2);
+}
 
 // ---------------------------------------------------------------------------
 // dense phase

@@ -292,18 +292,7 @@ __global__ __launch_bounds__(kBlock) void k_cull_finalize(FinalizeArgs args)
         const int i = __float_as_int(o.w);
         const float2 m = d.m12s[t];
         d.m12[(size_t)b * d.n_own + i] = m;
-        // Radius of the kept ball from the single-precision minima. The margin
-        // covers the rounding of this estimate (relative ~1e-7 (1 + 2 kappa)) and
-        // of the single-precision distance.
-        const Params &p = args.p;
-        const double c1 = sqrt((double)m.x), c2 = sqrt((double)m.y);
-        const double gap = (c2 - c1) + p.delta;
-        const double g = gap < p.eps_gap ? p.eps_gap : gap;
-        const double kappa = p.log_inv_tau / d.log_ratio; // log(1/tau) / (T g)
-        const double radius = c1 + g * kappa;
-        const double margin = 1e-5 * (1.0 + kappa);
-        double e = radius * radius * (1.0 + margin);
-        e = fmax(e, (double)m.y); // the second minimum is always emitted
+        const double e = emission_radius2(m.x, m.y, d.log_ratio, args.p);
         E = isinf(e) ? kInf : __double2float_ru(e);
         if (which == 0) {
             d.E[t] = E;

@@ -99,18 +99,7 @@ __global__ __launch_bounds__(kBlock) void k_finalize(FinalizeArgs args)
         m1 = fminf(m1, v.x);
     }
     d.m12[k] = make_float2(m1, m2);
-    // Radius of the kept ball from the single-precision minima. The margin
-    // covers the rounding of this estimate (relative ~1e-7 (1 + 2 kappa)) and
-    // of the single-precision distance.
-    const Params &p = args.p;
-    const double c1 = sqrt((double)m1), c2 = sqrt((double)m2);
-    const double gap = (c2 - c1) + p.delta;
-    const double g = gap < p.eps_gap ? p.eps_gap : gap;
-    const double kappa = p.log_inv_tau / d.log_ratio; // log(1/tau) / (T g)
-    const double radius = c1 + g * kappa;
-    const double margin = 1e-5 * (1.0 + kappa);
-    double e = radius * radius * (1.0 + margin);
-    e = fmax(e, (double)m2); // the second minimum is always emitted
+    const double e = emission_radius2(m1, m2, d.log_ratio, args.p);
     const float E = isinf(e) ? kInf : __double2float_ru(e);
     if (which == 0) {
         d.E[k] = E;

@@ -34,6 +34,15 @@ constexpr int G = kGroup;
 // Longer segments read the rest again in each step.
 constexpr int kSmCache = 8;
 
+// dP0/dP_row and dP0/dP_col of a pair with these flags (bit 0: the row
+// softmax keeps it, bit 1: the column softmax): P0 = (P_row + P_col)/2 with
+// an absent side 0 (Sec. III-A), or, averaging duplicates literally
+// (Sec. III-C), the one present value where only one direction keeps it.
+__device__ __forceinline__ double sym_weight(const Params &p, uint8_t flags)
+{
+    return p.sym_mode == kSymMeanDup && flags != 3 ? 1.0 : 0.5;
+}
+
 __device__ __forceinline__ double dist3(float ax, float ay, float az, float bx, float by, float bz)
 {
     const double dx = (double)ax - (double)bx;
@@ -117,7 +126,7 @@ template <bool ROWS> __device__ __forceinline__ void owner_softmax(const DevPlan
             } else {
                 const int t = d.csc_perm[s0 + k];
                 d.p_col[s0 + k] = 0.0f;
-                d.p0c[s0 + k] = d.p0r[t] = 0.5f * d.p_row[t];
+                d.p0c[s0 + k] = d.p0r[t] = (float)(sym_weight(p, d.flags[t]) * d.p_row[t]);
             }
         }
         return;
@@ -141,9 +150,13 @@ template <bool ROWS> __device__ __forceinline__ void owner_softmax(const DevPlan
     };
     const double c1 = dist_at(q1), c2 = dist_at(q2);
     const double gap = (c2 - c1) + p.delta;
-    const bool clamped = gap < p.eps_gap;
-    const double g = clamped ? p.eps_gap : gap;
-    const double T = lk / g;
+    // uniform fallback (Sec. III-A): T = 0 makes s = 1 on every pair, all
+    // kept, P = 1/K (the emission stored all K pairs of such an owner); like
+    // a clamped gap it carries no temperature gradient
+    const bool fallback = p.gap_mode == kGapFallback && (c2 - c1) < p.eps_gap;
+    const bool clamped = gap < p.eps_gap || fallback;
+    const double g = !fallback && clamped ? p.eps_gap : gap;
+    const double T = fallback ? 0.0 : lk / g;
 
     // kept similarities and their sum
     double sv[kSmCache], zsum = 0.0;
@@ -177,7 +190,7 @@ template <bool ROWS> __device__ __forceinline__ void owner_softmax(const DevPlan
         } else {
             const int q = s0 + k;
             d.flags[t] = (uint8_t)(f | (keep ? 2 : 0));
-            const float p0 = (float)(0.5 * ((double)pr + pk));
+            const float p0 = (float)(sym_weight(p, (uint8_t)(f | (keep ? 2 : 0))) * ((double)pr + pk));
             d.p_col[q] = (float)pk;
             d.p0c[q] = p0;
             d.p0r[t] = p0;
@@ -315,7 +328,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(DevPlan d, Params p)
     const double gl = d.grad_loss[b];
     const int s0 = d.col_ptr[gc], n = d.col_ptr[gc + 1] - s0;
     const double T = d.T_col[gc], c1 = d.C1_col[gc];
-    const double gapbar_scale = d.clamp_col[gc] ? 0.0 : -T / d.g_col[gc];
+    const double gapbar_scale = d.clamp_col[gc] || p.tgrad_mode == kTgradDetached ? 0.0 : -T / d.g_col[gc];
     const int q1 = d.pos_col[2 * (size_t)gc], q2 = d.pos_col[2 * (size_t)gc + 1];
     const float *yc = d.y + (size_t)gc * 3;
     const float y0 = yc[0], y1 = yc[1], y2 = yc[2];
@@ -335,8 +348,9 @@ __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(DevPlan d, Params p)
 #pragma unroll
     for (int c = 0; c < kSmCache; ++c) {
         const int k = lg + G * c;
-        kq[c] = k < n && (d.flags[tq[c]] & 2) != 0;
-        aq[c] = kq[c] ? 0.5 * p0bar(d, tq[c], gl) : 0.0;
+        const uint8_t f = k < n ? d.flags[tq[c]] : 0;
+        kq[c] = (f & 2) != 0;
+        aq[c] = kq[c] ? sym_weight(p, f) * p0bar(d, tq[c], gl) : 0.0;
         const float *xi = xb + 3 * (size_t)iq[c];
         cq[c] = kq[c] ? dist3(xi[0], xi[1], xi[2], y0, y1, y2) : 0.0;
     }
@@ -346,8 +360,9 @@ __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(DevPlan d, Params p)
         sigma += kq[c] ? (double)pq[c] * aq[c] : 0.0;
     for (int k = lg + G * kSmCache; k < n; k += G) {
         const int t = d.csc_perm[s0 + k];
-        if (d.flags[t] & 2)
-            sigma += (double)d.p_col[s0 + k] * (0.5 * p0bar(d, t, gl));
+        const uint8_t f = d.flags[t];
+        if (f & 2)
+            sigma += (double)d.p_col[s0 + k] * (sym_weight(p, f) * p0bar(d, t, gl));
     }
     sigma = group_sum<G>(sigma);
     double tbar = 0.0;
@@ -356,8 +371,9 @@ __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(DevPlan d, Params p)
         tbar -= kq[c] ? (double)pq[c] * (aq[c] - sigma) * (cq[c] - c1) : 0.0;
     for (int k = lg + G * kSmCache; k < n; k += G) {
         const int t = d.csc_perm[s0 + k];
-        if (d.flags[t] & 2)
-            tbar -= (double)d.p_col[s0 + k] * (0.5 * p0bar(d, t, gl) - sigma) * (d.cost[t] - c1);
+        const uint8_t f = d.flags[t];
+        if (f & 2)
+            tbar -= (double)d.p_col[s0 + k] * (sym_weight(p, f) * p0bar(d, t, gl) - sigma) * (d.cost[t] - c1);
     }
     tbar = group_sum<G>(tbar);
     const double gapbar = gapbar_scale * tbar;
@@ -376,7 +392,8 @@ __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(DevPlan d, Params p)
     }
     for (int k = lg + G * kSmCache; k < n; k += G) {
         const int t = d.csc_perm[s0 + k];
-        const double cb = (d.flags[t] & 2) ? -T * (double)d.p_col[s0 + k] * (0.5 * p0bar(d, t, gl) - sigma) : 0.0;
+        const uint8_t f = d.flags[t];
+        const double cb = (f & 2) ? -T * (double)d.p_col[s0 + k] * (sym_weight(p, f) * p0bar(d, t, gl) - sigma) : 0.0;
         d.cbar[t] = gap_terms(s0 + k, cb);
     }
 }
@@ -395,7 +412,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_row_softmax(DevPlan d, Params p,
     const double gl = d.grad_loss[b];
     const int t0 = d.row_ptr[r], n = d.row_ptr[r + 1] - t0;
     const double T = d.T_row[r], c1 = d.C1_row[r];
-    const double gscale = d.clamp_row[r] ? 0.0 : -T / d.g_row[r];
+    const double gscale = d.clamp_row[r] || p.tgrad_mode == kTgradDetached ? 0.0 : -T / d.g_row[r];
     const int q1 = d.pos_row[2 * (size_t)r], q2 = d.pos_row[2 * (size_t)r + 1];
     const double al = d.alpha[(size_t)d.L * BN + r];
     const double *bl = d.beta + (size_t)d.L * BM + (size_t)b * d.M;
@@ -409,10 +426,11 @@ __global__ __launch_bounds__(kBlock) void k_bwd_row_softmax(DevPlan d, Params p,
         const int k = lg + G * c, t = t0 + k;
         const bool in = k < n;
         jq[c] = in ? d.csr_col[t] : 0;
-        kq[c] = in && (d.flags[t] & 1) != 0;
+        const uint8_t f = in ? d.flags[t] : 0;
+        kq[c] = (f & 1) != 0;
         pq[c] = in ? d.p_row[t] : 0.0f;
         p0q[c] = in ? d.p0r[t] : 0.0f;
-        aq[c] = in ? 0.5 * p0bar(d, t, gl) : 0.0;
+        aq[c] = in ? sym_weight(p, f) * p0bar(d, t, gl) : 0.0;
         cq[c] = in ? d.cost[t] : 1.0;
         cbq[c] = in ? d.cbar[t] : 0.0;
     }
@@ -422,8 +440,9 @@ __global__ __launch_bounds__(kBlock) void k_bwd_row_softmax(DevPlan d, Params p,
         sigma += kq[c] ? (double)pq[c] * aq[c] : 0.0;
     for (int k = lg + G * kSmCache; k < n; k += G) {
         const int t = t0 + k;
-        if (d.flags[t] & 1)
-            sigma += (double)d.p_row[t] * (0.5 * p0bar(d, t, gl));
+        const uint8_t f = d.flags[t];
+        if (f & 1)
+            sigma += (double)d.p_row[t] * (sym_weight(p, f) * p0bar(d, t, gl));
     }
     sigma = group_sum<G>(sigma);
     double tbar = 0.0;
@@ -432,8 +451,9 @@ __global__ __launch_bounds__(kBlock) void k_bwd_row_softmax(DevPlan d, Params p,
         tbar -= kq[c] ? (double)pq[c] * (aq[c] - sigma) * (cq[c] - c1) : 0.0;
     for (int k = lg + G * kSmCache; k < n; k += G) {
         const int t = t0 + k;
-        if (d.flags[t] & 1)
-            tbar -= (double)d.p_row[t] * (0.5 * p0bar(d, t, gl) - sigma) * (d.cost[t] - c1);
+        const uint8_t f = d.flags[t];
+        if (f & 1)
+            tbar -= (double)d.p_row[t] * (sym_weight(p, f) * p0bar(d, t, gl) - sigma) * (d.cost[t] - c1);
     }
     tbar = group_sum<G>(tbar);
     const double gapbar = gscale * tbar;
@@ -463,7 +483,9 @@ __global__ __launch_bounds__(kBlock) void k_bwd_row_softmax(DevPlan d, Params p,
     }
     for (int k = lg + G * kSmCache; k < n; k += G) {
         const int t = t0 + k;
-        add(t, d.csr_col[t], d.cbar[t], (d.flags[t] & 1) != 0, d.p_row[t], 0.5 * p0bar(d, t, gl), d.cost[t], d.p0r[t]);
+        const uint8_t f = d.flags[t];
+        add(t, d.csr_col[t], d.cbar[t], (f & 1) != 0, d.p_row[t], sym_weight(p, f) * p0bar(d, t, gl), d.cost[t],
+            d.p0r[t]);
     }
     gx = group_sum<G>(gx);
     gy = group_sum<G>(gy);

@@ -38,9 +38,11 @@ def test_every_declared_symbol_is_exported():
 
 def test_defaults_are_the_papers():
     p = _lib.apml_params_default()
-    assert p.struct_size == ctypes.sizeof(_lib.apml_params) == 64
+    assert p.struct_size == ctypes.sizeof(_lib.apml_params) == 72
     assert (p.tau, p.n_iter, p.eps_stab) == (1e-8, 10, 1e-8)  # Sec. III-E, Sec. IV-C
     assert (p.p_min, p.delta, p.eps_gap, p.eps_dist) == (0.8, 1e-8, 1e-6, 1e-12)
+    # clamp, half sum, full gradient
+    assert (p.dense_scan, p.gap_mode, p.sym_mode, p.tgrad_mode) == (0, 0, 0, 0)
 
 
 def _forward(B=2, N=8, M=8, d=3, params=None, x=FAKE, y=FAKE, loss=FAKE):
@@ -66,6 +68,7 @@ def test_forward_rejects_bad_shapes(kw, status):
 @pytest.mark.parametrize("field,value", [
     ("p_min", 1.0), ("p_min", 0.0), ("p_min", 0.1), ("tau", -1e-3), ("tau", 1.5), ("n_iter", -1),
     ("delta", -1.0), ("eps_gap", 0.0), ("eps_stab", -1.0), ("eps_dist", -1.0), ("eps_gap", float("inf")),
+    ("dense_scan", 3), ("gap_mode", 2), ("sym_mode", -1), ("tgrad_mode", 2),
 ])
 def test_forward_rejects_bad_params(field, value):
     prm = _lib.apml_params_default(**{field: value})

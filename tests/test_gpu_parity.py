@@ -111,6 +111,39 @@ def test_duplicates_ties_and_clamps(scan):
     assert st["clamp_row"].any() and st["clamp_col"].any()
 
 
+# readings of the paper where it offers two (the defaults are clamp, half sum,
+# full gradient)
+VARIANTS = {"fallback": dict(gap_mode=1), "mean_dup": dict(sym_mode=1), "detached": dict(tgrad_mode=1),
+            "all": dict(gap_mode=1, sym_mode=1, tgrad_mode=1)}
+
+
+@pytest.mark.parametrize("scan", ["full", "skip"])
+@pytest.mark.parametrize("variant", list(VARIANTS))
+def test_reading_variants_with_ties(variant, scan):
+    # duplicated points: their rows and columns tie, so the uniform fallback
+    # takes whole rows and columns into the support
+    X, Y = custom(34, 2, 128, 100, sigma=0.05)
+    Y = np.ascontiguousarray(np.concatenate([Y, Y[:, :30]], axis=1))
+    X = np.ascontiguousarray(np.concatenate([X, X[:, :10]], axis=1))
+    g, _ = _check_batch(X, Y, f"variant {variant}", scan=scan, **VARIANTS[variant])
+    if VARIANTS[variant].get("gap_mode") == 1:
+        st = g["plan"].export_stats(0)
+        ex = g["plan"].export(0)
+        rows = np.flatnonzero(st["T_row"] == 0)
+        assert rows.size > 0
+        per_row = np.bincount(ex["i"], minlength=X.shape[1])
+        assert (per_row[rows] == Y.shape[1]).all()
+        sel = np.isin(ex["i"], rows)
+        np.testing.assert_allclose(ex["p_row"][sel], 1.0 / Y.shape[1], rtol=1e-6)
+
+
+@pytest.mark.parametrize("variant", ["mean_dup", "detached"])
+def test_reading_variants_config1(variant):
+    w = config(1)
+    X, Y = batch(w)
+    _check_batch(X, Y, f"config 1 {variant}", n_iter=w.n_iter, **VARIANTS[variant])
+
+
 @pytest.mark.parametrize("scan", ["full", "skip"])
 def test_identical_clouds(scan):
     _, Y = custom(30, 2, 300, 300, sigma=0.05)

@@ -379,6 +379,116 @@ def test_ties_clamp_and_index_order():
     np.testing.assert_allclose(r.grad_x.sum(0) + r.grad_y.sum(0), 0.0, atol=1e-11 * scale)
 
 
+# ---------------------------------------------------------------------------
+# Reading variants: uniform fallback, literal duplicate averaging, detached
+# temperature. Each is pinned by a closed form and by autograd of the dense
+# formulation.
+# ---------------------------------------------------------------------------
+
+def _nn_pairs(D):
+    """Union of the row and column argmin pairs (brute force), as a set."""
+    rows = {(i, int(j)) for i, j in enumerate(D.argmin(1))}
+    cols = {(int(i), j) for j, i in enumerate(D.argmin(0))}
+    return rows, cols
+
+
+def test_mean_dup_tau_one_closed_form():
+    # tau = 1 keeps only argmin entries with probability 1 in their direction:
+    # averaging duplicates literally gives P0 = 1 on the union of the argmin
+    # pairs, so with L = 0 the loss is the sum of C over that union
+    x, y = _cloud(18, 40, 33)
+    D = np.linalg.norm(x.astype(np.float64)[:, None] - y.astype(np.float64)[None], axis=-1)
+    rows, cols = _nn_pairs(D)
+    union = rows | cols
+    want = sum(D[i, j] for i, j in union)
+    r = oracle.run_sample(x, y, oracle.params(tau=1.0, n_iter=0, sym_mode=1), grad=False)
+    assert r.nnz == len(union)
+    assert r.loss == pytest.approx(want, rel=1e-13)
+    np.testing.assert_allclose(r.p0, 1.0, rtol=0)
+    # the half sum differs exactly on the pairs one direction keeps alone
+    h = oracle.run_sample(x, y, oracle.params(tau=1.0, n_iter=0), grad=False)
+    single = sum(D[i, j] for i, j in union - (rows & cols))
+    assert r.loss - h.loss == pytest.approx(0.5 * single, rel=1e-12)
+
+
+def test_mean_dup_full_support_equals_half_sum():
+    # tau = 0 keeps every pair in both directions: nothing is a singleton
+    x, y = _cloud(19, 17, 21)
+    a = oracle.run_sample(x, y, oracle.params(tau=0.0, sym_mode=1), grad=True)
+    b = oracle.run_sample(x, y, oracle.params(tau=0.0), grad=True)
+    assert a.loss == b.loss
+    np.testing.assert_array_equal(a.grad_x, b.grad_x)
+
+
+def _tie_cloud(seed):
+    # every reference point doubled: each row's two smallest costs tie
+    x, y = _cloud(seed, 12, 10, sigma=0.1)
+    return x, np.concatenate([y, y])
+
+
+def test_fallback_tau_one_closed_form():
+    # with all references doubled, every row falls back to 1/M over all M
+    # entries; columns (distinct x) keep their argmin. tau = 1, L = 0:
+    # loss = (sum_i mean_j C_ij + sum_j min_i C_ij) / 2
+    x, y = _tie_cloud(20)
+    N, M = x.shape[0], y.shape[0]
+    D = np.linalg.norm(x.astype(np.float64)[:, None] - y.astype(np.float64)[None], axis=-1)
+    r = oracle.run_sample(x, y, oracle.params(tau=1.0, n_iter=0, gap_mode=1), grad=True)
+    assert (r.row["T"] == 0).all() and r.row["clamped"].all()
+    assert r.nnz == N * M
+    want = 0.5 * (D.mean(1).sum() + D.min(0).sum())
+    assert r.loss == pytest.approx(want, rel=1e-13)
+    np.testing.assert_allclose(r.p_row, 1.0 / M, rtol=1e-15)
+    # the fallback is a constant: only the column softmaxes and the costs carry gradient,
+    # and at tau = 1 the column direction is a plain nearest neighbour
+    gx = np.zeros_like(D[:, :1].repeat(3, 1))
+    diff = x.astype(np.float64)[:, None] - y.astype(np.float64)[None]
+    gx += 0.5 * (diff / D[..., None]).sum(1) / M
+    i1 = D.argmin(0)
+    for j in range(M):
+        gx[i1[j]] += 0.5 * diff[i1[j], j] / D[i1[j], j]
+    np.testing.assert_allclose(r.grad_x, gx, rtol=1e-10, atol=1e-14)
+
+
+def test_fallback_only_below_eps_gap():
+    # generic data: no gap is below eps_g, so the fallback changes nothing
+    x, y = _cloud(21, 30, 30)
+    a = oracle.run_sample(x, y, oracle.params(gap_mode=1), grad=True)
+    b = oracle.run_sample(x, y, oracle.params(), grad=True)
+    assert a.loss == b.loss and a.nnz == b.nnz
+    np.testing.assert_array_equal(a.grad_x, b.grad_x)
+
+
+def test_detached_temperature_drops_gap_term():
+    # with the temperature a constant, the gradient is the full one minus the
+    # gap term; finite differences of a loss at fixed T are not available from
+    # the oracle, so the dense formulation's autograd (T detached) pins it
+    x, y = _cloud(22, 19, 23, sigma=0.1)
+    kw = dict(p_min=0.8, tau=1e-2, n_iter=6, eps_stab=1e-8, delta=1e-8, eps_gap=1e-6)
+    r = oracle.run_sample(x, y, oracle.params(tgrad_mode=1, **kw), grad=True)
+    full = oracle.run_sample(x, y, oracle.params(**kw), grad=True)
+    assert r.loss == full.loss
+    assert np.abs(r.grad_x - full.grad_x).max() > 1e-3 * np.abs(full.grad_x).max()
+    loss, gx, gy, _ = _dense_from_oracle(x, y, r, tgrad_mode=1, **kw)
+    assert r.loss == pytest.approx(loss, rel=1e-12)
+    np.testing.assert_allclose(r.grad_x, gx, rtol=1e-9, atol=1e-12 * np.abs(gx).max())
+    np.testing.assert_allclose(r.grad_y, gy, rtol=1e-9, atol=1e-12 * np.abs(gy).max())
+
+
+@pytest.mark.parametrize("mode", [dict(sym_mode=1), dict(gap_mode=1), dict(gap_mode=1, sym_mode=1, tgrad_mode=1)])
+def test_variants_match_dense_formulation(mode):
+    x, y = _tie_cloud(23) if mode.get("gap_mode") else _cloud(23, 21, 26, sigma=0.1)
+    kw = dict(p_min=0.8, tau=1e-3, n_iter=5, eps_stab=1e-8, delta=1e-8, eps_gap=1e-6)
+    r = oracle.run_sample(x, y, oracle.params(**kw, **mode), grad=True)
+    loss, gx, gy, mats = _dense_from_oracle(x, y, r, **kw, **mode)
+    assert r.loss == pytest.approx(loss, rel=1e-12)
+    np.testing.assert_allclose(r.grad_x, gx, rtol=1e-9, atol=1e-12 * np.abs(gx).max())
+    np.testing.assert_allclose(r.grad_y, gy, rtol=1e-9, atol=1e-12 * np.abs(gy).max())
+    np.testing.assert_allclose(r.p0, mats["P0"].detach().numpy()[r.i, r.j], rtol=1e-12)
+    union = (mats["keep_row"] | mats["keep_col"]).numpy()
+    assert r.nnz == union.sum()
+
+
 def test_owner_sampling_matches_full_run():
     x, y = _cloud(16, 70, 90)
     prm = oracle.params()
@@ -397,7 +507,8 @@ def test_owner_sampling_matches_full_run():
 
 def test_rejects_invalid_arguments():
     x, y = _cloud(17, 8, 8)
-    for bad in (dict(p_min=1.0), dict(p_min=0.1), dict(tau=2.0), dict(n_iter=-1), dict(eps_gap=0.0)):
+    for bad in (dict(p_min=1.0), dict(p_min=0.1), dict(tau=2.0), dict(n_iter=-1), dict(eps_gap=0.0),
+                dict(gap_mode=2), dict(sym_mode=-1), dict(tgrad_mode=3)):
         with pytest.raises(ValueError):
             oracle.run_sample(x, y, oracle.params(**bad))
     with pytest.raises(ValueError):
