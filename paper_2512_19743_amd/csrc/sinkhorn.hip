@@ -612,7 +612,9 @@ __device__ __forceinline__ double owner_sum(int n, int lg, Load load, Use use)
 // Column step (Eq. 3, COL) or row step (Eq. 4) of iteration l for all owners.
 template <bool COL> __global__ __launch_bounds__(kBlock) void k_sink_step(DevPlan d, int l, double eps)
 {
-    const int gid = blockIdx.x * kBlock + threadIdx.x;
+    // each XCD takes a contiguous range of owners: its L2 holds only the
+    // other side's scalings of those owners' samples
+    const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x;
     const int o = gid / kSG, lg = gid % kSG;
     const int n_own = COL ? d.M : d.N, n_oth = COL ? d.N : d.M;
     if (o >= d.B * n_own)
@@ -651,7 +653,7 @@ template <bool COL> __global__ __launch_bounds__(kBlock) void k_sink_step(DevPla
 
 __global__ __launch_bounds__(kBlock) void k_loss_rows(DevPlan d, double *loss_rows)
 {
-    const int gid = blockIdx.x * kBlock + threadIdx.x;
+    const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // as in k_sink_step
     const int r = gid / kSG, lg = gid % kSG;
     if (r >= d.B * d.N)
         return;
@@ -730,7 +732,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_init(DevPlan d)
 
 __global__ __launch_bounds__(kBlock) void k_bwd_rows(DevPlan d, int l)
 {
-    const int gid = blockIdx.x * kBlock + threadIdx.x;
+    const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // as in k_sink_step
     const int r = gid / kSG, lg = gid % kSG;
     if (r >= d.B * d.N)
         return;
@@ -779,7 +781,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(DevPlan d, int l)
 
 __global__ __launch_bounds__(kBlock) void k_bwd_cols(DevPlan d, int l)
 {
-    const int gid = blockIdx.x * kBlock + threadIdx.x;
+    const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // as in k_sink_step
     const int gc = gid / kSG, lg = gid % kSG;
     if (gc >= d.B * d.M)
         return;

@@ -219,7 +219,7 @@ template <bool ROWS> __device__ __forceinline__ void owner_softmax(const DevPlan
 
 __global__ __launch_bounds__(kBlock) void k_row_softmax(DevPlan d, Params p)
 {
-    const int gid = blockIdx.x * kBlock + threadIdx.x;
+    const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // a sample's owners share an L2
     const int r = gid / G;
     if (r < d.B * d.N)
         owner_softmax<true>(d, p, r, gid % G);
@@ -227,7 +227,7 @@ __global__ __launch_bounds__(kBlock) void k_row_softmax(DevPlan d, Params p)
 
 __global__ __launch_bounds__(kBlock) void k_col_softmax(DevPlan d, Params p)
 {
-    const int gid = blockIdx.x * kBlock + threadIdx.x;
+    const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // a sample's owners share an L2
     const int gc = gid / G;
     if (gc < d.B * d.M)
         owner_softmax<false>(d, p, gc, gid % G);
@@ -320,7 +320,7 @@ __device__ __forceinline__ double p0bar(const DevPlan &d, int t, double gl)
 //            term grad_loss * v; then Eq. 5 turns cbar into grad_x.
 __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(DevPlan d, Params p)
 {
-    const int gid = blockIdx.x * kBlock + threadIdx.x;
+    const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // a sample's owners share an L2
     const int gc = gid / G, lg = gid % G;
     if (gc >= d.B * d.M)
         return;
@@ -400,7 +400,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(DevPlan d, Params p)
 
 __global__ __launch_bounds__(kBlock) void k_bwd_row_softmax(DevPlan d, Params p, int keep_cbar)
 {
-    const int gid = blockIdx.x * kBlock + threadIdx.x;
+    const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // a sample's owners share an L2
     const int r = gid / G, lg = gid % G;
     if (r >= d.B * d.N)
         return;
@@ -500,7 +500,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_row_softmax(DevPlan d, Params p,
 
 __global__ __launch_bounds__(kBlock) void k_bwd_grad_y(DevPlan d, Params p)
 {
-    const int gid = blockIdx.x * kBlock + threadIdx.x;
+    const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // a sample's owners share an L2
     const int gc = gid / G, lg = gid % G;
     if (gc >= d.B * d.M)
         return;
