@@ -658,7 +658,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         ca.ctr = dv.ctr;
         cnt = ca.cnt;
     }
-    Readback *rb_dev = (Readback *)tmp.get<uint8_t>(readback_bytes(B));
+    int32_t *off_tiles = tmp.get<int32_t>(offsets_scratch_ints(B, N, M));
     std::vector<uint8_t> rb_host(readback_bytes(B));
     if (tmp.failed || dense_tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (support)");
@@ -681,7 +681,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         pt.stop();
     }
     // row and column offsets, and what the host needs, in one copy
-    launch_offsets(cnt, cnt_chunks, col_cnt, dv.ctr, B, N, M, dv.row_ptr, dv.col_ptr, rb_dev,
+    launch_offsets(cnt, cnt_chunks, col_cnt, dv.ctr, B, N, M, dv.row_ptr, dv.col_ptr, off_tiles,
                    (Readback *)pinned().device_ptr(plan->device), s);
     HIP_TRY(hipGetLastError());
     HIP_TRY(wait_for(s));

@@ -336,10 +336,12 @@ __host__ __device__ inline int32_t *readback_pieces(Readback *r, int B) { return
 
 // Row and column offsets of all samples (row_ptr [B*N+1] from the per-(row,
 // chunk) counts cnt [B*N][S], col_ptr [B*M+1] from col_cnt) and the read-back
-// block, in two launches. rb is device scratch (the totals); rb_host, mapped
-// pinned host memory, receives the whole block, written by the kernels.
+// block, in two launches. tiles is device scratch of offsets_scratch_ints
+// ints (per-tile totals); rb_host, mapped pinned host memory, receives the
+// whole block, written by the kernels.
+size_t offsets_scratch_ints(int B, int N, int M);
 void launch_offsets(const int32_t *cnt, int S, const int32_t *col_cnt, const Counters *ctr, int B, int N, int M,
-                    int32_t *row_ptr, int32_t *col_ptr, Readback *rb, Readback *rb_host, hipStream_t s);
+                    int32_t *row_ptr, int32_t *col_ptr, int32_t *tiles, Readback *rb_host, hipStream_t s);
 // Whether the per-sample kernels take a batch: counts are the host copy of the
 // piece counts of the read-back block, max_pairs the largest sample's stored
 // pairs.

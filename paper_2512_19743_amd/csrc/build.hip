@@ -4,6 +4,8 @@
 // The paper symmetrizes by concatenating the two COO streams and sorting
 // 64-bit keys (Sec. III-C); here every pair is emitted once, with both
 // memberships decided later, so only the column-major view needs building.
+#include <algorithm>
+
 #include "apml_internal.h"
 #include "device_common.h"
 
@@ -16,42 +18,159 @@ namespace {
 
 constexpr int kOffT = 1024;
 
-// Per sample (blockIdx.x) and direction (blockIdx.y: 0 rows, 1 columns): the
-// sample-local exclusive scan of the owners' pair counts into row_ptr /
-// col_ptr, the sample's total and its piece counts.
-__global__ __launch_bounds__(kOffT) void k_sample_scan(const int32_t *cnt, int S, const int32_t *col_cnt, int N,
-                                                       int M, int32_t *row_ptr, int32_t *col_ptr, Readback *rb,
-                                                       Readback *rb_host)
+// Pair count of owner k of sample b: the sum of a row's chunk counts (in
+// 16-byte loads when the count is a multiple of 4), or a column's count.
+__device__ __forceinline__ int owner_len(bool rows, const int32_t *cnt, int S, const int32_t *col_cnt, int b, int N,
+                                         int M, int k)
 {
-    __shared__ int wsum[kOffT / 64];
-    __shared__ int red[2][kOffT / 64];
-    const int b = blockIdx.x, rows = blockIdx.y == 0, tid = threadIdx.x, B = gridDim.x;
-    const int lane = lane_id(), wave = tid >> 6;
+    if (!rows)
+        return col_cnt[(size_t)b * M + k];
+    const int32_t *rc = cnt + ((size_t)b * N + k) * S;
+    int len = 0, c = 0;
+    if (S % 4 == 0)
+        for (; c < S; c += 4) {
+            const int4 v = *reinterpret_cast<const int4 *>(rc + c);
+            len += v.x + v.y + v.z + v.w;
+        }
+    for (; c < S; ++c)
+        len += rc[c];
+    return len;
+}
+
+// Owners are cut into tiles of kOffTile; a workgroup of kOffT threads takes
+// one tile of one sample and direction (grid: tiles x B x 2, blockIdx.z 0 for
+// rows, 1 for columns), thread t owners tile * kOffTile + u * kOffT + t.
+constexpr int kOffPer = 8;
+constexpr int kOffTile = kOffT * kOffPer;
+
+// Per tile: the pair total, the lane positions of its owners' piece groups and
+// the largest piece count, into tiles[((dir * B + b) * T + tile) * 3 + 0..2].
+__global__ __launch_bounds__(kOffT) void k_sample_scan(const int32_t *cnt, int S, const int32_t *col_cnt, int N,
+                                                       int M, int32_t *tiles, int T)
+{
+    __shared__ int red[3][kOffT / 64];
+    const int tile = blockIdx.x, b = blockIdx.y, B = gridDim.y, tid = threadIdx.x;
+    const bool rows = blockIdx.z == 0;
     const int n = rows ? N : M;
-    int32_t *out = rows ? row_ptr + (size_t)b * N : col_ptr + (size_t)b * M;
-    int carry = 0, pos = 0, mx = 0;
-    for (int base = 0; base < n; base += kOffT) {
-        const int k = base + tid;
-        int len = 0;
-        if (k < n) {
-            if (rows) {
-                const int32_t *rc = cnt + ((size_t)b * N + k) * S;
-                int c = 0;
-                if (S % 4 == 0) // the row's chunk counts in 16-byte loads, all in flight together
-                    for (; c < S; c += 4) {
-                        const int4 v = *reinterpret_cast<const int4 *>(rc + c);
-                        len += v.x + v.y + v.z + v.w;
-                    }
-                for (; c < S; ++c)
-                    len += rc[c];
-            } else {
-                len = col_cnt[(size_t)b * M + k];
-            }
-            const int np = sink_pieces(len);
+    if (tile * kOffTile >= n) // the whole workgroup
+        return;
+    const int lane = lane_id(), wave = tid >> 6;
+    int len[kOffPer];
+#pragma unroll
+    for (int u = 0; u < kOffPer; ++u) {
+        const int k = tile * kOffTile + u * kOffT + tid;
+        len[u] = k < n ? owner_len(rows, cnt, S, col_cnt, b, N, M, k) : -1;
+    }
+    int sum = 0, pos = 0, mx = 0;
+#pragma unroll
+    for (int u = 0; u < kOffPer; ++u)
+        if (len[u] >= 0) {
+            const int np = sink_pieces(len[u]);
+            sum += len[u];
             pos += 1 << min(sink_log2_group(np), 30);
             mx = max(mx, np);
         }
-        int inc = len;
+    for (int off = 32; off > 0; off >>= 1) {
+        sum += __shfl_xor(sum, off);
+        pos += __shfl_xor(pos, off);
+        mx = max(mx, __shfl_xor(mx, off));
+    }
+    if (lane == 0) {
+        red[0][wave] = sum;
+        red[1][wave] = pos;
+        red[2][wave] = mx;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int t = 0, a = 0, m = 0;
+        for (int w = 0; w < kOffT / 64; ++w) {
+            t += red[0][w];
+            a += red[1][w];
+            m = max(m, red[2][w]);
+        }
+        int32_t *o = tiles + (((size_t)(rows ? 0 : 1) * B + b) * T + tile) * 3;
+        o[0] = t;
+        o[1] = a;
+        o[2] = m;
+    }
+}
+
+// The offsets of one tile: the base of its sample (pairs of the earlier
+// samples) and of its tile within the sample, plus the exclusive scan of its
+// owners' counts (one workgroup scan per round u). The first tile of each
+// sample also closes row_ptr / col_ptr and fills the read-back block (totals,
+// offsets, piece counts; the counters from sample 0's row tile).
+__global__ __launch_bounds__(kOffT) void k_sample_base(const int32_t *cnt, int S, const int32_t *col_cnt,
+                                                       const Counters *ctr, int N, int M, int32_t *row_ptr,
+                                                       int32_t *col_ptr, const int32_t *tiles, int T,
+                                                       Readback *rb_host)
+{
+    __shared__ int wsum[kOffT / 64];
+    __shared__ int base_s;
+    const int tile = blockIdx.x, b = blockIdx.y, B = gridDim.y, tid = threadIdx.x;
+    const bool rows = blockIdx.z == 0;
+    const int n = rows ? N : M;
+    if (tile * kOffTile >= n)
+        return;
+    const int lane = lane_id(), wave = tid >> 6;
+    const int32_t *tl = tiles + (size_t)(rows ? 0 : 1) * B * T * 3;
+    if (wave == 0) {
+        // pairs before this tile: all tiles of the earlier samples, then the
+        // earlier tiles of this one (tile entries of a direction are in
+        // sample-major order)
+        const int before = b * T + tile, nt = (n + kOffTile - 1) / kOffTile;
+        int64_t base = 0;
+        for (int e = lane; e < before; e += 64)
+            if (e % T < nt) // this direction's tiles (the grid covers the longer one)
+                base += tl[3 * e];
+        for (int off = 32; off > 0; off >>= 1)
+            base += __shfl_xor(base, off);
+        if (lane == 0)
+            base_s = (int)base; // the host rejects totals beyond int32 before using any offset
+        if (tile == 0) {
+            int64_t tot = 0;
+            int a = 0, m = 0;
+            for (int e = lane; e < nt; e += 64) {
+                tot += tl[3 * ((size_t)b * T + e)];
+                a += tl[3 * ((size_t)b * T + e) + 1];
+                m = max(m, tl[3 * ((size_t)b * T + e) + 2]);
+            }
+            for (int off = 32; off > 0; off >>= 1) {
+                tot += __shfl_xor(tot, off);
+                a += __shfl_xor(a, off);
+                m = max(m, __shfl_xor(m, off));
+            }
+            if (lane == 0) {
+                readback_totals(rb_host)[(rows ? 0 : B) + b] = tot;
+                int32_t *pc = readback_pieces(rb_host, B) + 4 * b;
+                pc[rows ? 0 : 1] = a;
+                pc[rows ? 2 : 3] = m;
+                if (rows)
+                    readback_offsets(rb_host, B)[b] = (int)base;
+                if (b == B - 1) {
+                    const int end = (int)(base + tot);
+                    (rows ? row_ptr[(size_t)B * N] : col_ptr[(size_t)B * M]) = end;
+                    if (rows)
+                        readback_offsets(rb_host, B)[B] = end;
+                }
+            }
+        }
+    }
+    if (tile == 0 && b == 0 && rows) // the counters, word by word over the workgroup
+        for (int i = tid; i < (int)(sizeof(Counters) / 4); i += kOffT)
+            reinterpret_cast<uint32_t *>(&rb_host->ctr)[i] = reinterpret_cast<const uint32_t *>(ctr)[i];
+    int len[kOffPer];
+#pragma unroll
+    for (int u = 0; u < kOffPer; ++u) {
+        const int k = tile * kOffTile + u * kOffT + tid;
+        len[u] = k < n ? owner_len(rows, cnt, S, col_cnt, b, N, M, k) : 0;
+    }
+    __syncthreads(); // base_s
+    int carry = base_s;
+    int32_t *out = rows ? row_ptr + (size_t)b * N : col_ptr + (size_t)b * M;
+#pragma unroll
+    for (int u = 0; u < kOffPer; ++u) {
+        int inc = len[u];
         for (int off = 1; off < 64; off <<= 1) {
             const int v = __shfl_up(inc, off);
             if (lane >= off)
@@ -66,65 +185,22 @@ __global__ __launch_bounds__(kOffT) void k_sample_scan(const int32_t *cnt, int S
             all += wsum[w];
         }
         __syncthreads();
+        const int k = tile * kOffTile + u * kOffT + tid;
         if (k < n)
-            out[k] = carry + before + inc - len;
+            out[k] = carry + before + inc - len[u];
         carry += all;
-    }
-    for (int off = 32; off > 0; off >>= 1) {
-        pos += __shfl_xor(pos, off);
-        mx = max(mx, __shfl_xor(mx, off));
-    }
-    if (lane == 0) {
-        red[0][wave] = pos;
-        red[1][wave] = mx;
-    }
-    __syncthreads();
-    if (tid == 0) {
-        int a = 0, m = 0;
-        for (int w = 0; w < kOffT / 64; ++w) {
-            a += red[0][w];
-            m = max(m, red[1][w]);
-        }
-        readback_totals(rb)[(rows ? 0 : B) + b] = carry;
-        readback_totals(rb_host)[(rows ? 0 : B) + b] = carry;
-        int32_t *pc = readback_pieces(rb_host, B) + 4 * b;
-        pc[rows ? 0 : 1] = a;
-        pc[rows ? 2 : 3] = m;
     }
 }
 
-// Adds each sample's base (pairs of the earlier samples) to its local
-// offsets, closes row_ptr / col_ptr with the total and fills the read-back
-// offsets and counters.
-__global__ __launch_bounds__(kOffT) void k_sample_base(const Counters *ctr, int N, int M, int32_t *row_ptr,
-                                                       int32_t *col_ptr, const Readback *rb, Readback *rb_host)
+} // namespace
+
+size_t offsets_scratch_ints(int B, int N, int M)
 {
-    __shared__ int base_s;
-    const int b = blockIdx.x, rows = blockIdx.y == 0, tid = threadIdx.x, B = gridDim.x;
-    const int64_t *tot = readback_totals(const_cast<Readback *>(rb)) + (rows ? 0 : B);
-    if (tid == 0) {
-        int64_t base = 0;
-        for (int k = 0; k < b; ++k)
-            base += tot[k];
-        base_s = (int)base; // the host rejects totals beyond int32 before using any offset
-        if (rows)
-            readback_offsets(rb_host, B)[b] = (int)base;
-        if (b == B - 1) {
-            const int end = (int)(base + tot[b]);
-            (rows ? row_ptr[(size_t)B * N] : col_ptr[(size_t)B * M]) = end;
-            if (rows)
-                readback_offsets(rb_host, B)[B] = end;
-        }
-    }
-    if (b == 0 && rows) // the counters, word by word over the workgroup
-        for (int i = tid; i < (int)(sizeof(Counters) / 4); i += kOffT)
-            reinterpret_cast<uint32_t *>(&rb_host->ctr)[i] = reinterpret_cast<const uint32_t *>(ctr)[i];
-    __syncthreads();
-    const int n = rows ? N : M;
-    int32_t *out = rows ? row_ptr + (size_t)b * N : col_ptr + (size_t)b * M;
-    for (int k = tid; k < n; k += kOffT)
-        out[k] += base_s;
+    const int T = (std::max(N, M) + kOffTile - 1) / kOffTile;
+    return 3 * 2 * (size_t)B * T;
 }
+
+namespace {
 
 // ---------------------------------------------------------------------------
 // column-major permutation
@@ -189,11 +265,12 @@ __global__ __launch_bounds__(kBlock) void k_count_support(const int32_t *row_ptr
 } // namespace
 
 void launch_offsets(const int32_t *cnt, int S, const int32_t *col_cnt, const Counters *ctr, int B, int N, int M,
-                    int32_t *row_ptr, int32_t *col_ptr, Readback *rb, Readback *rb_host, hipStream_t s)
+                    int32_t *row_ptr, int32_t *col_ptr, int32_t *tiles, Readback *rb_host, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_sample_scan, dim3(B, 2), dim3(kOffT), 0, s, cnt, S, col_cnt, N, M, row_ptr, col_ptr, rb,
-                       rb_host);
-    hipLaunchKernelGGL(k_sample_base, dim3(B, 2), dim3(kOffT), 0, s, ctr, N, M, row_ptr, col_ptr, rb, rb_host);
+    const int T = (std::max(N, M) + kOffTile - 1) / kOffTile;
+    hipLaunchKernelGGL(k_sample_scan, dim3(T, B, 2), dim3(kOffT), 0, s, cnt, S, col_cnt, N, M, tiles, T);
+    hipLaunchKernelGGL(k_sample_base, dim3(T, B, 2), dim3(kOffT), 0, s, cnt, S, col_cnt, ctr, N, M, row_ptr, col_ptr,
+                       (const int32_t *)tiles, T, rb_host);
 }
 
 void launch_csc_build(const DevPlan &d, const BuildArgs &a, hipStream_t s)
