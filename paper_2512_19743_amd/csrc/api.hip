@@ -808,7 +808,6 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     dv.rden = keep.get<double>((size_t)std::max(L, 1) * BN);
     dv.sden = keep.get<double>((size_t)std::max(L, 1) * BM);
     dv.dvec = keep.get<double>(BN);
-    dv.evec = keep.get<double>(BM);
     if (keep.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (plan)");
     {
@@ -862,6 +861,8 @@ apml_status apml_backward(apml_plan *plan, const float *x, const float *y, const
     if (dv.L > 0 && !plan->sink_bwd) {
         dv.rz = tmp.get<double>(plan->stored);
         dv.kz = tmp.get<double>(plan->stored);
+        dv.xyr = tmp.get<float4>((size_t)plan->B * plan->N);
+        dv.xyc = tmp.get<float4>((size_t)plan->B * plan->M);
     }
     if (tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (backward)");

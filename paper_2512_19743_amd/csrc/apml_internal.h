@@ -289,8 +289,9 @@ struct DevPlan {
     const float *grad_loss;
     float *grad_x, *grad_y;
     double *adj, *cbar;           // [nnz] row-major
-    double *dvec, *evec;          // [B*N], [B*M] scratch of the per-iteration kernels (row losses; row and
-                                  // column values of the reverse sweeps as float2)
+    double *dvec;                 // [B*N] row losses of the per-iteration forward kernels
+    float4 *xyr, *xyc;            // [B*N], [B*M] per-owner values of the per-iteration reverse sweeps: X, Y and
+                                  // the reciprocal of the owner's scaling
     double *rz, *kz;              // [nnz] reverse-sweep adjoints in row and in column order (per-iteration kernels)
     PackedOrder pk_row, pk_col;   // per-sample Sinkhorn pieces (when that path is taken)
 };

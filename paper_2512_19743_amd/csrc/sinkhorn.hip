@@ -713,12 +713,14 @@ __global__ __launch_bounds__(kLossT) void k_loss_reduce(DevPlan d, const double 
 // date in its own order, so no launch reads or writes pairs out of order:
 //   row launch l:    rz <- column update of iteration l+1 (l < L), then the
 //                    row update of iteration l; row sums; row values
-//                    X_i = alpha^l_i, Y_i = d_i alpha^l_i into xyr
+//                    X_i = alpha^l_i, Y_i = d_i alpha^l_i and 1/alpha^l_i into xyr
 //   column launch l: kz <- row update of iteration l, then the column update
-//                    of iteration l; column sums; column values into xyc
+//                    of iteration l; column sums; column values X_j =
+//                    beta^l_j, Y_j = e_j beta^l_j and 1/beta^l_j into xyc
 // where the row update of iteration l is z' = (z / alpha^l_i) X_j - Y_j with
 // the column values published last, and the column update z' = (z / beta^l_j)
-// X_i - Y_i with the row values of iteration l.
+// X_i - Y_i with the row values of iteration l. The other side's values of a
+// pair arrive in one 16-byte gather; sums and updates are double.
 __device__ __forceinline__ float rinv(double v) { return __builtin_amdgcn_rcpf((float)v); }
 
 __global__ __launch_bounds__(kBlock) void k_bwd_init(DevPlan d)
@@ -733,8 +735,8 @@ __global__ __launch_bounds__(kBlock) void k_bwd_init(DevPlan d)
         d.kz[g] = d.grad_loss[bb] * d.cost[t] * d.alpha[(size_t)d.L * BN + rr];
     }
     if (g < (int64_t)BM) { // no pending column update before the last iteration
-        float2 *xyc = reinterpret_cast<float2 *>(d.evec);
-        xyc[g] = make_float2((float)d.beta[(size_t)d.L * BM + g], 0.0f);
+        const double bl = d.beta[(size_t)d.L * BM + g];
+        d.xyc[g] = make_float4((float)bl, 0.0f, rinv(bl), 0.0f);
     }
 }
 
@@ -745,12 +747,10 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(DevPlan d, int l)
     if (r >= d.B * d.N)
         return;
     const int b = r / d.N;
-    const size_t BN = (size_t)d.B * d.N, BM = (size_t)d.B * d.M;
-    float2 *xyr = reinterpret_cast<float2 *>(d.dvec);
-    const float2 *xyc = reinterpret_cast<const float2 *>(d.evec) + (size_t)b * d.M;
-    const double *beta_next = d.beta + (size_t)(l + 1) * BM + (size_t)b * d.M; // iteration l+1 (l < L)
+    const size_t BN = (size_t)d.B * d.N;
+    const float4 *xyc = d.xyc + (size_t)b * d.M;
     const bool pending = l < d.L;
-    const float2 mine = pending ? xyr[r] : make_float2(0.0f, 0.0f); // row values of iteration l+1
+    const float4 mine = pending ? d.xyr[r] : make_float4(0.0f, 0.0f, 0.0f, 0.0f); // row values of iteration l+1
     const double al = d.alpha[(size_t)l * BN + r];
     const double inv_a = (double)rinv(al);
     const int t0 = d.row_ptr[r], n = d.row_ptr[r + 1] - t0;
@@ -758,32 +758,30 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(DevPlan d, int l)
         double z;
         float p;
         int k;
-        float ib;
-        float2 c;
+        float4 c;
     };
     const double acc = owner_sum(n, lg,
                                  [&](int k) {
-                                     V v{0.0, 0.0f, k, 1.0f, make_float2(0.0f, 0.0f)};
+                                     V v{0.0, 0.0f, k, make_float4(0.0f, 0.0f, 1.0f, 0.0f)};
                                      if (k >= 0) {
                                          const int j = d.csr_col[t0 + k];
                                          v.z = d.rz[t0 + k];
                                          v.p = d.p0r[t0 + k];
-                                         v.ib = pending ? rinv(beta_next[j]) : 1.0f;
                                          v.c = xyc[j];
                                      }
                                      return v;
                                  },
                                  [&](const V &v) {
                                      double z = v.z;
-                                     if (pending)
-                                         z = __builtin_fma(z * (double)v.ib, (double)mine.x, -(double)mine.y);
+                                     if (pending) // 1/beta^(l+1)_j
+                                         z = __builtin_fma(z * (double)v.c.z, (double)mine.x, -(double)mine.y);
                                      z = __builtin_fma(z * inv_a, (double)v.c.x, -(double)v.c.y);
                                      d.rz[t0 + v.k] = z;
                                      return z * (double)v.p;
                                  });
     if (lg == 0) { // adjoint of Eq. 4: d_i = alpha^l_i * sum
         const double dsum = al * acc;
-        xyr[r] = make_float2((float)al, (float)(dsum * al));
+        d.xyr[r] = make_float4((float)al, (float)(dsum * al), (float)inv_a, 0.0f);
     }
 }
 
@@ -794,11 +792,9 @@ __global__ __launch_bounds__(kBlock) void k_bwd_cols(DevPlan d, int l)
     if (gc >= d.B * d.M)
         return;
     const int b = gc / d.M;
-    const size_t BN = (size_t)d.B * d.N, BM = (size_t)d.B * d.M;
-    const float2 *xyr = reinterpret_cast<const float2 *>(d.dvec) + (size_t)b * d.N;
-    float2 *xyc = reinterpret_cast<float2 *>(d.evec);
-    const double *alpha_l = d.alpha + (size_t)l * BN + (size_t)b * d.N;
-    const float2 mine = xyc[gc]; // column values published last
+    const size_t BM = (size_t)d.B * d.M;
+    const float4 *xyr = d.xyr + (size_t)b * d.N;
+    const float4 mine = d.xyc[gc]; // column values published last
     const double bl = d.beta[(size_t)l * BM + gc];
     const double inv_b = (double)rinv(bl);
     const int s0 = d.col_ptr[gc], n = d.col_ptr[gc + 1] - s0;
@@ -806,30 +802,29 @@ __global__ __launch_bounds__(kBlock) void k_bwd_cols(DevPlan d, int l)
         double z;
         float p;
         int k;
-        float ia;
-        float2 rw;
+        float4 rw;
     };
     const double acc = owner_sum(n, lg,
                                  [&](int k) {
-                                     V v{0.0, 0.0f, k, 1.0f, make_float2(0.0f, 0.0f)};
+                                     V v{0.0, 0.0f, k, make_float4(0.0f, 0.0f, 1.0f, 0.0f)};
                                      if (k >= 0) {
                                          const int i = d.csc_row[s0 + k];
                                          v.z = d.kz[s0 + k];
                                          v.p = d.p0c[s0 + k];
-                                         v.ia = rinv(alpha_l[i]);
                                          v.rw = xyr[i];
                                      }
                                      return v;
                                  },
-                                 [&](const V &v) {
-                                     double z = __builtin_fma(v.z * (double)v.ia, (double)mine.x, -(double)mine.y);
+                                 [&](const V &v) { // v.rw.z = 1/alpha^l_i
+                                     double z = __builtin_fma(v.z * (double)v.rw.z, (double)mine.x,
+                                                              -(double)mine.y);
                                      z = __builtin_fma(z * inv_b, (double)v.rw.x, -(double)v.rw.y);
                                      d.kz[s0 + v.k] = z;
                                      return z * (double)v.p;
                                  });
     if (lg == 0) { // adjoint of Eq. 3: e_j = beta^l_j * sum
         const double esum = bl * acc;
-        xyc[gc] = make_float2((float)bl, (float)(esum * bl));
+        d.xyc[gc] = make_float4((float)bl, (float)(esum * bl), (float)inv_b, 0.0f);
     }
 }
 
@@ -840,12 +835,10 @@ __global__ __launch_bounds__(kBlock) void k_bwd_final(DevPlan d)
     const int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (t >= d.nnz)
         return;
-    const size_t BM = (size_t)d.B * d.M;
     const int r = d.csr_row[t], b = r / d.N, j = d.csr_col[t];
-    const float2 rw = reinterpret_cast<const float2 *>(d.dvec)[r];
-    const float2 c = reinterpret_cast<const float2 *>(d.evec)[(size_t)b * d.M + j];
-    double z = __builtin_fma(d.rz[t] * (double)rinv(d.beta[BM + (size_t)b * d.M + j]), (double)rw.x,
-                             -(double)rw.y);
+    const float4 rw = d.xyr[r];
+    const float4 c = d.xyc[(size_t)b * d.M + j]; // c.z = 1/beta^1_j
+    double z = __builtin_fma(d.rz[t] * (double)c.z, (double)rw.x, -(double)rw.y);
     d.adj[t] = z * (double)c.x - (double)c.y;
 }
 
