@@ -626,6 +626,9 @@ template <bool COL> __global__ __launch_bounds__(kBlock) void k_sink_step(DevPla
     const float *p0 = COL ? d.p0c : d.p0r;
     // the other side's scalings: alpha^(l-1) for columns, beta^l for rows
     const double *oth = (COL ? d.alpha + (size_t)(l - 1) * BN : d.beta + (size_t)l * BM) + (size_t)b * n_oth;
+    double *cur = COL ? d.beta : d.alpha, *den_out = COL ? d.sden : d.rden;
+    const size_t BO = COL ? BM : BN;
+    const double prev = cur[(size_t)(l - 1) * BO + o]; // loaded with the segment bounds
     const int s0 = ptr[o], n = ptr[o + 1] - s0;
     struct V {
         float p;
@@ -642,9 +645,6 @@ template <bool COL> __global__ __launch_bounds__(kBlock) void k_sink_step(DevPla
                                  },
                                  [&](const V &v) { return (double)v.p * v.x; });
     if (lg == 0) {
-        double *cur = COL ? d.beta : d.alpha, *den_out = COL ? d.sden : d.rden;
-        const size_t BO = COL ? BM : BN;
-        const double prev = cur[(size_t)(l - 1) * BO + o];
         const double den = prev * acc + eps;
         cur[(size_t)l * BO + o] = prev / den;
         den_out[(size_t)(l - 1) * BO + o] = den;
