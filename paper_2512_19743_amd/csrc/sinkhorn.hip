@@ -12,13 +12,13 @@
 // Per-sample kernels: one 1024-lane workgroup per sample runs all 2L sweeps
 // with the sample's pairs in registers. k_place and k_pack_pairs cut every
 // row's (column's) pairs into pieces of kP and lay them out so that an
-// owner's pieces are consecutive lanes of one wave (see PackedOrder). A sweep has two phases:
-//   piece phase  each lane sums its pieces (gathering the other side's
-//                scalings from LDS); the pieces of one owner are added by a
-//                butterfly inside their aligned lane group, in a fixed order,
-//                and the group's first lane stores the owner's sum in LDS;
-//   owner phase  lane t owns rows (columns) 2t and 2t+1: it reads the sum and
-//                applies the scaling.
+// owner's pieces are consecutive lanes of one wave (see PackedOrder). In a
+// sweep each lane sums its pieces (gathering the other side's values from
+// LDS) and the pieces of one owner are added by a butterfly inside their
+// aligned lane group, in a fixed order. In the forward kernel the group's
+// first lane then applies its owner's scaling at once (one barrier per
+// sweep); in the reverse kernel it stores the sum in LDS for an owner phase
+// in which lane t owns rows (columns) 2t and 2t+1.
 // Sums have a fixed association, so results are bitwise reproducible.
 //
 // Reverse sweeps: for u = w/(R + eps) with R = sum over the row of w,
@@ -273,10 +273,28 @@ __device__ __forceinline__ double quotient(double a, double b)
 // Up to this many slots the forward kernel keeps P0 in double in registers.
 constexpr int kFwdWideSlots = 4;
 
+// The head lane of an owner's group applies the owner's scaling as soon as
+// the group has its sum: v = cur / (cur * sum + eps) (Eq. 3 or Eq. 4), into
+// the owner's side array in LDS (which the phase does not gather from) and
+// into the saved scalings and denominators.
+__device__ __forceinline__ void apply_scaling(double acc, uint32_t info, double *own, double eps, double *g_val,
+                                              double *g_den, const Unpack &u)
+{
+    if (u.bits(info, 14, 2) == 3u) { // head and valid
+        const int o = u.owner(info);
+        const double cur = own[o];
+        const double den = cur * acc + eps;
+        const double v = quotient(cur, den);
+        own[o] = v;
+        g_val[o] = v;
+        g_den[o] = den;
+    }
+}
+
 template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
 {
     // static arrays: their addresses are constants folded into the LDS instructions
-    __shared__ double va[kSinkOwners], vb[kSinkOwners], sums[kSinkOwners];
+    __shared__ double va[kSinkOwners], vb[kSinkOwners], part[kT / 64];
     const int b = blockIdx.x, tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
@@ -288,12 +306,9 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan 
     P0Cache<false, SLP, kWide> prw, pcw;
     prw.init(pr);
     pcw.init(pc);
-    double am[kSL], bm[kSL]; // the lane's own scalings
 #pragma unroll
     for (int s = 0; s < kSL; ++s) {
         const int k = kSL * tid + s;
-        am[s] = 1.0;
-        bm[s] = 1.0;
         if (k < N) {
             va[k] = 1.0;
             d.alpha[(size_t)b * N + k] = 1.0;
@@ -308,48 +323,22 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan 
     for (int l = 1; l <= L; ++l) {
         const Unpack u = Unpack::make();
         // column scaling (Eq. 3): beta_j /= beta_j sum_i alpha_i P0_ij + eps
+        double *gb = d.beta + l * BM + (size_t)b * M, *gs = d.sden + (l - 1) * BM + (size_t)b * M;
 #pragma unroll
         for (int s = 0; s < SLP; ++s)
             if (wave_active(pc, s)) {
                 const double acc = slot_dot(pc, pcw, s, va, u);
-                store_sum(group_reduce(acc, pc.info[s], u), pc.info[s], sums, u);
+                apply_scaling(group_reduce(acc, pc.info[s], u), pc.info[s], vb, eps, gb, gs, u);
             }
-        lds_barrier();
-#pragma unroll
-        for (int s = 0; s < kSL; ++s) {
-            const int j = kSL * tid + s;
-            const double S = sums[min(j, M - 1)];
-            const double den = bm[s] * S + eps;
-            const double v = quotient(bm[s], den);
-            if (j < M) {
-                bm[s] = v;
-                vb[j] = v;
-                d.beta[l * BM + (size_t)b * M + j] = v;
-                d.sden[(l - 1) * BM + (size_t)b * M + j] = den;
-            }
-        }
         lds_barrier();
         // row scaling (Eq. 4): alpha_i /= alpha_i sum_j P0_ij beta_j + eps
+        double *ga = d.alpha + l * BN + (size_t)b * N, *gr = d.rden + (l - 1) * BN + (size_t)b * N;
 #pragma unroll
         for (int s = 0; s < SLP; ++s)
             if (wave_active(pr, s)) {
                 const double acc = slot_dot(pr, prw, s, vb, u);
-                store_sum(group_reduce(acc, pr.info[s], u), pr.info[s], sums, u);
+                apply_scaling(group_reduce(acc, pr.info[s], u), pr.info[s], va, eps, ga, gr, u);
             }
-        lds_barrier();
-#pragma unroll
-        for (int s = 0; s < kSL; ++s) {
-            const int i = kSL * tid + s;
-            const double R = sums[min(i, N - 1)];
-            const double den = am[s] * R + eps;
-            const double v = quotient(am[s], den);
-            if (i < N) {
-                am[s] = v;
-                va[i] = v;
-                d.alpha[l * BN + (size_t)b * N + i] = v;
-                d.rden[(l - 1) * BN + (size_t)b * N + i] = den;
-            }
-        }
         lds_barrier();
     }
 
@@ -375,12 +364,12 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan 
     }
     acc = wave_sum(acc);
     if (lane_id() == 0)
-        sums[tid >> 6] = acc;
+        part[tid >> 6] = acc;
     lds_barrier();
     if (tid == 0) {
         double s = 0.0;
         for (int w = 0; w < kT / 64; ++w)
-            s += sums[w];
+            s += part[w];
         d.loss[b] = (float)s;
     }
 }
