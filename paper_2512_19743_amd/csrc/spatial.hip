@@ -413,28 +413,39 @@ __global__ __launch_bounds__(kBlock) void k_sort_gather(SpatialArgs a, int src)
             Box{make_float4(lo[0], lo[1], lo[2], 0.0f), make_float4(hi[0], hi[1], hi[2], 0.0f)};
 }
 
-// Box of each batch of 64 runs: one thread per (cloud, sample, batch).
+// Box of each batch of 64 runs: one wave per (cloud, sample, batch), one lane
+// per run (coalesced loads), then wave-wide min / max.
 __global__ __launch_bounds__(kBlock) void k_batch_boxes(const Box *box_x, const Box *box_y, Box *batch_x,
                                                         Box *batch_y, int B, int pad_x, int pad_y, bool columns_only)
 {
-    const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const int64_t g = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
+    const int lane = lane_id();
     const int nbx = batches(pad_x), nby = batches(pad_y);
     const int64_t nx = columns_only ? 0 : (int64_t)B * nbx;
     const int cloud = g < nx ? 0 : 1;
     const int64_t h = cloud ? g - nx : g;
     const int nbt = cloud ? nby : nbx, pad = cloud ? pad_y : pad_x;
-    if (h >= (int64_t)B * nbt)
+    if (h >= (int64_t)B * nbt) // the whole wave
         return;
     const int b = (int)(h / nbt), t = (int)(h - (int64_t)b * nbt);
-    const int runs = pad / kRun;
+    const int runs = pad / kRun, r = t * 64 + lane;
     const Box *rb = (cloud ? box_y : box_x) + (size_t)b * runs;
-    float4 lo = make_float4(kInf, kInf, kInf, -kInf), hi = make_float4(-kInf, -kInf, -kInf, -kInf);
-    for (int r = t * 64; r < min(runs, t * 64 + 64); ++r) {
-        const Box x = rb[r];
-        lo = make_float4(fminf(lo.x, x.lo.x), fminf(lo.y, x.lo.y), fminf(lo.z, x.lo.z), 0.0f);
-        hi = make_float4(fmaxf(hi.x, x.hi.x), fmaxf(hi.y, x.hi.y), fmaxf(hi.z, x.hi.z), fmaxf(hi.w, x.hi.w));
+    float4 lo = make_float4(kInf, kInf, kInf, 0.0f), hi = make_float4(-kInf, -kInf, -kInf, -kInf);
+    if (r < runs) {
+        lo = rb[r].lo;
+        hi = rb[r].hi;
     }
-    (cloud ? batch_y : batch_x)[(size_t)b * nbt + t] = Box{lo, hi};
+    for (int off = 32; off > 0; off >>= 1) {
+        lo.x = fminf(lo.x, __shfl_xor(lo.x, off));
+        lo.y = fminf(lo.y, __shfl_xor(lo.y, off));
+        lo.z = fminf(lo.z, __shfl_xor(lo.z, off));
+        hi.x = fmaxf(hi.x, __shfl_xor(hi.x, off));
+        hi.y = fmaxf(hi.y, __shfl_xor(hi.y, off));
+        hi.z = fmaxf(hi.z, __shfl_xor(hi.z, off));
+        hi.w = fmaxf(hi.w, __shfl_xor(hi.w, off));
+    }
+    if (lane == 0)
+        (cloud ? batch_y : batch_x)[(size_t)b * nbt + t] = Box{make_float4(lo.x, lo.y, lo.z, 0.0f), hi};
 }
 
 } // namespace
@@ -445,8 +456,8 @@ void launch_batch_boxes(const Box *box_x, const Box *box_y, Box *batch_x, Box *b
                         bool columns_only, hipStream_t s)
 {
     const int64_t n = (int64_t)B * ((columns_only ? 0 : batches(pad_x)) + batches(pad_y));
-    hipLaunchKernelGGL(k_batch_boxes, dim3(blocks_for(n, kBlock)), dim3(kBlock), 0, s, box_x, box_y, batch_x, batch_y,
-                       B, pad_x, pad_y, columns_only);
+    hipLaunchKernelGGL(k_batch_boxes, dim3(blocks_for(64 * n, kBlock)), dim3(kBlock), 0, s, box_x, box_y, batch_x,
+                       batch_y, B, pad_x, pad_y, columns_only);
 }
 
 hipError_t launch_spatial_sort(const SpatialArgs &a, hipStream_t s)
