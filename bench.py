@@ -83,13 +83,13 @@ PHASE_MODEL = {
 # entry names the source files it was measured on with their SHA-256: once a
 # file changes, traffic is reported as null until measured again.
 TRAFFIC = {
-    "stats": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "5eab9277f4b592a91254b4c43afbb9172273f72b15ca77df8a7f3aabf67eb7a2", "paper_2512_19743_amd/csrc/apml_internal.h": "868a1d412a1555396b8735dd5c8effaab8c62b5b739bffc96108f4bbc6dce3cf", "paper_2512_19743_amd/csrc/device_common.h": "ae2b3955e6043d486d001b8a23e72dd6da741ba032fae3475c8169f16e724b13"}, "kernels": ["k_top2"], "bytes_per_launch": 27845861},
-    "support": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "5eab9277f4b592a91254b4c43afbb9172273f72b15ca77df8a7f3aabf67eb7a2", "paper_2512_19743_amd/csrc/apml_internal.h": "868a1d412a1555396b8735dd5c8effaab8c62b5b739bffc96108f4bbc6dce3cf", "paper_2512_19743_amd/csrc/device_common.h": "ae2b3955e6043d486d001b8a23e72dd6da741ba032fae3475c8169f16e724b13"}, "kernels": ["k_emit"], "bytes_per_launch": 37327081},
-    "build": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "5eab9277f4b592a91254b4c43afbb9172273f72b15ca77df8a7f3aabf67eb7a2", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "868a1d412a1555396b8735dd5c8effaab8c62b5b739bffc96108f4bbc6dce3cf", "paper_2512_19743_amd/csrc/device_common.h": "ae2b3955e6043d486d001b8a23e72dd6da741ba032fae3475c8169f16e724b13"}, "kernels": ["k_emit_compact_place"], "bytes_per_launch": 27805105},
-    "softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "1eddfab1e8f062399c35ef907eec6dc7f8222bd4bf2bd5fddbe10d06826aff3b", "paper_2512_19743_amd/csrc/apml_internal.h": "868a1d412a1555396b8735dd5c8effaab8c62b5b739bffc96108f4bbc6dce3cf", "paper_2512_19743_amd/csrc/device_common.h": "ae2b3955e6043d486d001b8a23e72dd6da741ba032fae3475c8169f16e724b13"}, "kernels": ["k_csc_rows", "k_col_softmax"], "bytes_per_launch": 63826073},
-    "sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "419ee3423b65e4e29970514e8a3218dfd2664aa2c81aff2130635c5366aa2317", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "868a1d412a1555396b8735dd5c8effaab8c62b5b739bffc96108f4bbc6dce3cf", "paper_2512_19743_amd/csrc/device_common.h": "ae2b3955e6043d486d001b8a23e72dd6da741ba032fae3475c8169f16e724b13"}, "kernels": ["k_pack_pairs", "k_sinkhorn_fwd"], "bytes_per_launch": 61792421},
-    "bwd_sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "419ee3423b65e4e29970514e8a3218dfd2664aa2c81aff2130635c5366aa2317", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "868a1d412a1555396b8735dd5c8effaab8c62b5b739bffc96108f4bbc6dce3cf", "paper_2512_19743_amd/csrc/device_common.h": "ae2b3955e6043d486d001b8a23e72dd6da741ba032fae3475c8169f16e724b13"}, "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 26050889},
-    "bwd_softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "1eddfab1e8f062399c35ef907eec6dc7f8222bd4bf2bd5fddbe10d06826aff3b", "paper_2512_19743_amd/csrc/apml_internal.h": "868a1d412a1555396b8735dd5c8effaab8c62b5b739bffc96108f4bbc6dce3cf", "paper_2512_19743_amd/csrc/device_common.h": "ae2b3955e6043d486d001b8a23e72dd6da741ba032fae3475c8169f16e724b13"}, "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 73459591},
+    "stats": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/apml_internal.h": "da32312abd3cd19a70cdb14534b3b870b84eba4c168bd6a6563a07af9e5ce3e7", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_top2"], "bytes_per_launch": 32794787},
+    "support": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/apml_internal.h": "da32312abd3cd19a70cdb14534b3b870b84eba4c168bd6a6563a07af9e5ce3e7", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit"], "bytes_per_launch": 32859673},
+    "build": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "da32312abd3cd19a70cdb14534b3b870b84eba4c168bd6a6563a07af9e5ce3e7", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit_compact_place"], "bytes_per_launch": 23189572},
+    "softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "15992d8f233b535129ec9269c76a7b4de90a87f394d8ae57d683e1107e43c6b5", "paper_2512_19743_amd/csrc/apml_internal.h": "da32312abd3cd19a70cdb14534b3b870b84eba4c168bd6a6563a07af9e5ce3e7", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_csc_rows", "k_col_softmax"], "bytes_per_launch": 37358082},
+    "sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "e3e3f1daa114d42861dd0aad1d7f2d3d7e9d311de669a904b3129ad5948e63e0", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "da32312abd3cd19a70cdb14534b3b870b84eba4c168bd6a6563a07af9e5ce3e7", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_pack_pairs", "k_sinkhorn_fwd"], "bytes_per_launch": 61792837},
+    "bwd_sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "e3e3f1daa114d42861dd0aad1d7f2d3d7e9d311de669a904b3129ad5948e63e0", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "da32312abd3cd19a70cdb14534b3b870b84eba4c168bd6a6563a07af9e5ce3e7", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 26057928},
+    "bwd_softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "15992d8f233b535129ec9269c76a7b4de90a87f394d8ae57d683e1107e43c6b5", "paper_2512_19743_amd/csrc/apml_internal.h": "da32312abd3cd19a70cdb14534b3b870b84eba4c168bd6a6563a07af9e5ce3e7", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 33366348},
 }
 
 
