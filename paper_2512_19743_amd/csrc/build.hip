@@ -168,8 +168,11 @@ __global__ __launch_bounds__(kOffT) void k_sample_base(const int32_t *cnt, int S
     __syncthreads(); // base_s
     int carry = base_s;
     int32_t *out = rows ? row_ptr + (size_t)b * N : col_ptr + (size_t)b * M;
+    const int rounds = min(kOffPer, (n - tile * kOffTile + kOffT - 1) / kOffT); // rounds holding owners
 #pragma unroll
     for (int u = 0; u < kOffPer; ++u) {
+        if (u >= rounds) // the same for the whole workgroup
+            break;
         int inc = len[u];
         for (int off = 1; off < 64; off <<= 1) {
             const int v = __shfl_up(inc, off);
