@@ -120,7 +120,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--memory-sweep", action="store_true",
                     help="only measure peak library memory and time of one forward+backward at B=1, "
-                         "N=M in 1k..256k (shape-completion generator), one JSON line per size")
+                         "N=M in 1k..256k (shape-completion generator), one JSON line per size, with the "
+                         "stored pairs of 16 seeded samples per size")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (5 times), to scale HBM byte counters")
     return ap.parse_args()
@@ -151,6 +152,7 @@ def memory_sweep():
 
     apml.load()
     sizes = [1024, 2048, 4096, 8192, 16384, 32768, 65536, 131072, 262144]
+    trials = 16
     pts, peaks = [], []
     for n in sizes:
         X, Y = custom(n, 1, n, n, reference="primitives", prediction="perm_noise", sigma=0.05)
@@ -168,6 +170,9 @@ def memory_sweep():
 
         step()
         torch.cuda.synchronize()
+        apml.apml_release_cached_memory()
+        step()  # warm again with blocks sized for this N only
+        torch.cuda.synchronize()
         apml.apml_reset_peak_memory()
         times = []
         for _ in range(3):
@@ -184,11 +189,20 @@ def memory_sweep():
         peak = apml.apml_get_memory_stats()["peak_in_use"]
         pts.append(2 * n)
         peaks.append(peak)
+        # stored pairs over several seeded samples of the same size (one batched forward)
+        Xt, Yt = custom(n, trials, n, n, reference="primitives", prediction="perm_noise", sigma=0.05)
+        _, plan = apml.apml_forward(torch.from_numpy(Xt).cuda(), torch.from_numpy(Yt).cuda(), prm)
+        per = plan.nnz().astype(np.float64)
+        plan.close()
+        torch.cuda.synchronize()
+        apml.apml_release_cached_memory()  # the batch's blocks would inflate the next size's peak
         # one dense fp32 N x M matrix, the least a dense formulation holds
         print(json.dumps({"N": n, "M": n, "B": 1, "nnz": nnz, "peak_library_mb": peak / 1e6,
                           "bytes_per_point": peak / (2 * n), "dense_matrix_mb": 4.0 * n * n / 1e6,
-                          "ms_fwd_bwd": statistics.median(times)}), flush=True)
-        del x, y
+                          "ms_fwd_bwd": statistics.median(times), "trials": trials,
+                          "nnz_mean": float(per.mean()), "nnz_std": float(per.std(ddof=1)),
+                          "nnz_min": int(per.min()), "nnz_max": int(per.max())}), flush=True)
+        del x, y, Xt, Yt
     A = np.vstack([np.asarray(pts, float), np.ones(len(pts))]).T
     slope, icpt = np.linalg.lstsq(A, np.asarray(peaks, float), rcond=None)[0]
     print(json.dumps({"fit": "peak_bytes = a * (N + M) + b", "a_bytes_per_point": slope, "b_bytes": icpt}), flush=True)
