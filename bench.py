@@ -324,7 +324,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": f"config {w.cfg} ({w.name}): B={w.B} N={w.N} M={w.M} L={w.n_iter}, "
+        "config": {"workload": f"{w.name}: B={w.B} N={w.N} M={w.M} L={w.n_iter}, "
                                f"{w.reference} reference, {w.prediction} prediction sigma={w.sigma}",
                    "B": w.B, "N": w.N, "M": w.M, "n_iter": w.n_iter, "tau": 1e-8, "p_min": 0.8,
                    "dense_scan": scan_mode},

@@ -39,10 +39,10 @@ def _check_batch(X, Y, label, samples=None, check_grad_y=True, scan=None, **prm)
 
 
 @pytest.mark.parametrize("scan", ["full", "skip"])
-def test_tiny_config_full(scan):
+def test_tiny_workload_full(scan):
     w = config(1)
     X, Y = batch(w)
-    _, res = _check_batch(X, Y, "config 1", n_iter=w.n_iter, scan=scan)
+    _, res = _check_batch(X, Y, w.name, n_iter=w.n_iter, scan=scan)
     assert all(r["flips"] == 0 for r in res), res
 
 
@@ -138,10 +138,10 @@ def test_reading_variants_with_ties(variant, scan):
 
 
 @pytest.mark.parametrize("variant", ["mean_dup", "detached"])
-def test_reading_variants_config1(variant):
+def test_reading_variants_tiny(variant):
     w = config(1)
     X, Y = batch(w)
-    _check_batch(X, Y, f"config 1 {variant}", n_iter=w.n_iter, **VARIANTS[variant])
+    _check_batch(X, Y, f"{w.name} {variant}", n_iter=w.n_iter, **VARIANTS[variant])
 
 
 @pytest.mark.parametrize("scan", ["full", "skip"])
@@ -211,25 +211,25 @@ def test_plan_reports_and_memory_returns():
 # ---------------------------------------------------------------------------
 
 @pytest.mark.parametrize("scan", ["full", "skip"])
-def test_config2_full_batch(scan):
+def test_shape_completion_full_batch(scan):
     w = config(2)
     X, Y = batch(w)
-    _, res = _check_batch(X, Y, "config 2", n_iter=w.n_iter, scan=scan)
-    note(f"config 2 nnz per sample: {[r['nnz_gpu'] for r in res[:4]]} flips {sum(r['flips'] for r in res)}")
+    _, res = _check_batch(X, Y, w.name, n_iter=w.n_iter, scan=scan)
+    note(f"{w.name} nnz per sample: {[r['nnz_gpu'] for r in res[:4]]} flips {sum(r['flips'] for r in res)}")
 
 
 @pytest.mark.parametrize("cfg,scan", [(3, None), (4, None), (4, "full"), (4, "skip")])
-def test_large_configs_one_sample_exact(cfg, scan):
+def test_large_workloads_one_sample_exact(cfg, scan):
     # the whole batch runs on the GPU; sample 0 is checked against a full oracle run
     w = config(cfg)
     X, Y = batch(w)
-    _check_batch(X, Y, f"config {cfg}", samples=[0], n_iter=w.n_iter, scan=scan)
+    _check_batch(X, Y, w.name, samples=[0], n_iter=w.n_iter, scan=scan)
 
 
-def test_config5_sampled_owners_and_invariants():
+def test_large_scene_sampled_owners_and_invariants():
     w = config(5)
     X, Y = batch(w)
-    note("config 5")
+    note(w.name)
     g = run_gpu(X, Y, n_iter=w.n_iter)
     plan = g["plan"]
     nnz = plan.nnz()
