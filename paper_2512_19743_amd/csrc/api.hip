@@ -811,6 +811,13 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     dv.dvec = keep.get<double>(BN);
     if (keep.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (plan)");
+    // the per-sample Sinkhorn path: the column softmax writes each pair into
+    // its pieces (no separate packing launch)
+    if (plan->sink_fwd) {
+        if (!pieces_placed)
+            launch_place(dv, place, s);
+        dv.sink_place = place;
+    }
     {
         PhaseTimer pt(PH_SOFTMAX, s);
         if (csc_lds) {
@@ -826,7 +833,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     {
         PhaseTimer pt(PH_SINKHORN, s);
         if (plan->sink_fwd) {
-            launch_pack(dv, place, pieces_placed, s);
+            dv.sink_place = nullptr; // scratch of this call
             HIP_TRY(launch_sinkhorn_fwd(dv, prm.eps_stab, s));
         } else {
             launch_sinkhorn_fwd_steps(dv, prm.eps_stab, s);

@@ -294,6 +294,8 @@ struct DevPlan {
                                   // the reciprocal of the owner's scaling
     double *rz, *kz;              // [nnz] reverse-sweep adjoints in row and in column order (per-iteration kernels)
     PackedOrder pk_row, pk_col;   // per-sample Sinkhorn pieces (when that path is taken)
+    const int32_t *sink_place;    // during the forward softmax of that path: the pieces' placement, so that the
+                                  // column softmax writes every pair into its pieces; else NULL
 };
 
 struct BuildArgs {
@@ -354,6 +356,9 @@ size_t packed_order_words(int B, int slots); // 32-bit words of one PackedOrder'
 // Lays out the pieces of both orders; place: [B][2][2048] int32 scratch.
 // placed: place[] and the info words are already written (with the compaction).
 void launch_pack(const DevPlan &d, int32_t *place, bool placed, hipStream_t s);
+// Only the placement (place[] and the info words), when the column softmax
+// packs the pairs.
+void launch_place(const DevPlan &d, int32_t *place, hipStream_t s);
 hipError_t launch_sinkhorn_fwd(const DevPlan &d, double eps, hipStream_t s);
 hipError_t launch_sinkhorn_bwd(const DevPlan &d, int64_t max_pairs, hipStream_t s);
 void launch_sinkhorn_fwd_steps(const DevPlan &d, double eps, hipStream_t s);

@@ -858,6 +858,11 @@ bool sinkhorn_bwd_fits(int slots, int64_t max_pairs)
 
 size_t packed_order_words(int B, int slots) { return (size_t)B * slots * kP * kT; }
 
+void launch_place(const DevPlan &d, int32_t *place, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_place, dim3(d.B, 2), dim3(kT), 0, s, d, place);
+}
+
 void launch_pack(const DevPlan &d, int32_t *place, bool placed, hipStream_t s)
 {
     if (!placed)

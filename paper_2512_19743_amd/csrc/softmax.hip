@@ -20,6 +20,7 @@
 //     with Eq. 5, k_bwd_grad_y into grad_y.
 #include "apml_internal.h"
 #include "device_common.h"
+#include "pieces.h"
 
 namespace apml {
 namespace {
@@ -33,6 +34,15 @@ constexpr int G = kGroup;
 // distances and similarities kept in registers, so the segment is read once.
 // Longer segments read the rest again in each step.
 constexpr int kSmCache = 8;
+
+// Pair t (row-major position; row i, column j of sample b, the k-th entry of
+// its column) with P0 into the per-sample Sinkhorn pieces of both orders.
+__device__ __forceinline__ void pack_pair(const DevPlan &d, int b, int j, int k, int i, int t, float p0)
+{
+    const int roff = t - d.row_ptr[(size_t)b * d.N + i];
+    pieces::pack_row_pair(d, d.sink_place, b, i, roff, j, p0);
+    pieces::pack_col_pair(d, d.sink_place, b, j, k, i, roff, p0);
+}
 
 // dP0/dP_row and dP0/dP_col of a pair with these flags (bit 0: the row
 // softmax keeps it, bit 1: the column softmax): P0 = (P_row + P_col)/2 with
@@ -126,7 +136,10 @@ template <bool ROWS> __device__ __forceinline__ void owner_softmax(const DevPlan
             } else {
                 const int t = d.csc_perm[s0 + k];
                 d.p_col[s0 + k] = 0.0f;
-                d.p0c[s0 + k] = d.p0r[t] = (float)(sym_weight(p, d.flags[t]) * d.p_row[t]);
+                const float p0 = (float)(sym_weight(p, d.flags[t]) * d.p_row[t]);
+                d.p0c[s0 + k] = d.p0r[t] = p0;
+                if (d.sink_place)
+                    pack_pair(d, b, (int)(o - (int64_t)b * n_own), k, idx[s0 + k], t, p0);
             }
         }
         return;
@@ -194,6 +207,8 @@ template <bool ROWS> __device__ __forceinline__ void owner_softmax(const DevPlan
             d.p_col[q] = (float)pk;
             d.p0c[q] = p0;
             d.p0r[t] = p0;
+            if (d.sink_place)
+                pack_pair(d, b, (int)(o - (int64_t)b * n_own), k, idx[q], t, p0);
         }
     };
 #pragma unroll
