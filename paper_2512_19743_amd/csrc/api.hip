@@ -203,6 +203,20 @@ struct Arena {
     ~Arena() { release(); }
 };
 
+// Several arrays cut from one allocation (one pool call instead of one per
+// array), each starting on a 256-byte boundary. A first pass with base ==
+// nullptr only adds up the size.
+struct Carve {
+    uint8_t *base = nullptr;
+    size_t off = 0;
+    template <typename T> T *take(size_t count)
+    {
+        T *p = base ? reinterpret_cast<T *>(base + off) : nullptr;
+        off += (std::max<size_t>(count * sizeof(T), 16) + 255) & ~size_t(255);
+        return p;
+    }
+};
+
 // ---------------------------------------------------------------------------
 // per-phase event timing
 // ---------------------------------------------------------------------------
@@ -713,17 +727,38 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     plan->sink_bwd = sinkhorn_bwd_fits(slots, plan->max_sample);
 
     // ---- sparse structure -------------------------------------------------
-    dv.csr_col = keep.get<int32_t>(nnz);
-    dv.csr_row = keep.get<int32_t>(nnz);
-    dv.csc_row = keep.get<int32_t>(nnz);
-    dv.csc_col = keep.get<int32_t>(nnz);
-    dv.csc_perm = keep.get<int32_t>(nnz);
-    dv.flags = keep.get<uint8_t>(nnz);
-    dv.p_row = keep.get<float>(nnz);
-    dv.p_col = keep.get<float>(nnz);
-    dv.p0r = keep.get<float>(nnz);
-    dv.p0c = keep.get<float>(nnz);
-    dv.cost = keep.get<double>(nnz);
+    // (with the per-sample Sinkhorn pieces, in one allocation)
+    auto lay_pairs = [&](Carve &c) {
+        dv.csr_col = c.take<int32_t>(nnz);
+        dv.csr_row = c.take<int32_t>(nnz);
+        dv.csc_row = c.take<int32_t>(nnz);
+        dv.csc_col = c.take<int32_t>(nnz);
+        dv.csc_perm = c.take<int32_t>(nnz);
+        dv.flags = c.take<uint8_t>(nnz);
+        dv.p_row = c.take<float>(nnz);
+        dv.p_col = c.take<float>(nnz);
+        dv.p0r = c.take<float>(nnz);
+        dv.p0c = c.take<float>(nnz);
+        dv.cost = c.take<double>(nnz);
+        if (plan->sink_fwd) {
+            const size_t w = packed_order_words(B, slots);
+            for (PackedOrder *pk : {&dv.pk_row, &dv.pk_col}) {
+                pk->slots = slots;
+                pk->p0 = c.take<float>(w);
+                pk->gi = c.take<uint32_t>(w / 2);
+                pk->info = c.take<uint32_t>(w / kSinkPiece);
+                pk->pos = pk == &dv.pk_col ? c.take<uint32_t>(w / 2) : nullptr;
+                pk->n_pos = c.take<int32_t>(B);
+            }
+        }
+    };
+    {
+        Carve size;
+        lay_pairs(size);
+        Carve c{keep.get<uint8_t>(size.off)};
+        if (!keep.failed)
+            lay_pairs(c);
+    }
     // column-major view: per sample in LDS when it fits (with the row
     // softmax), else slots taken by global counters (in the full scan's
     // compaction when no tile is rescanned)
@@ -739,19 +774,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     // pieces of the per-sample Sinkhorn kernels; with staged hits (or the
     // skipping scans) their placement runs in the compaction's (ranking's)
     // launch
-    int32_t *place = nullptr;
-    if (plan->sink_fwd) {
-        const size_t w = packed_order_words(B, slots);
-        for (PackedOrder *pk : {&dv.pk_row, &dv.pk_col}) {
-            pk->slots = slots;
-            pk->p0 = keep.get<float>(w);
-            pk->gi = keep.get<uint32_t>(w / 2);
-            pk->info = keep.get<uint32_t>(w / kSinkPiece);
-            pk->pos = pk == &dv.pk_col ? keep.get<uint32_t>(w / 2) : nullptr;
-            pk->n_pos = keep.get<int32_t>(B);
-        }
-        place = tmp.get<int32_t>((size_t)B * 2 * kSinkOwners);
-    }
+    int32_t *place = plan->sink_fwd ? tmp.get<int32_t>((size_t)B * 2 * kSinkOwners) : nullptr;
     const bool pieces_placed = place && (skip || (ea.stage && !placed));
     if (tmp.failed || keep.failed || dense_tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (sparse arrays)");
@@ -794,23 +817,33 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     dense_tmp.release();
 
     // ---- temperatures, softmaxes, P0 ---------------------------------------
-    dv.T_row = keep.get<double>(BN);
-    dv.C1_row = keep.get<double>(BN);
-    dv.g_row = keep.get<double>(BN);
-    dv.T_col = keep.get<double>(BM);
-    dv.C1_col = keep.get<double>(BM);
-    dv.g_col = keep.get<double>(BM);
-    dv.pos_row = keep.get<int32_t>(2 * (size_t)BN);
-    dv.pos_col = keep.get<int32_t>(2 * (size_t)BM);
-    dv.clamp_row = keep.get<uint8_t>(BN);
-    dv.clamp_col = keep.get<uint8_t>(BM);
-    dv.alpha = keep.get<double>((size_t)(L + 1) * BN);
-    dv.beta = keep.get<double>((size_t)(L + 1) * BM);
-    dv.rden = keep.get<double>((size_t)std::max(L, 1) * BN);
-    dv.sden = keep.get<double>((size_t)std::max(L, 1) * BM);
-    dv.dvec = keep.get<double>(BN);
-    if (keep.failed)
-        return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (plan)");
+    // the per-point arrays of the plan (one allocation, taken once the
+    // scans' scratch is released, so that the two never coexist)
+    {
+        auto lay = [&](Carve &c) {
+            dv.T_row = c.take<double>(BN);
+            dv.C1_row = c.take<double>(BN);
+            dv.g_row = c.take<double>(BN);
+            dv.T_col = c.take<double>(BM);
+            dv.C1_col = c.take<double>(BM);
+            dv.g_col = c.take<double>(BM);
+            dv.pos_row = c.take<int32_t>(2 * (size_t)BN);
+            dv.pos_col = c.take<int32_t>(2 * (size_t)BM);
+            dv.clamp_row = c.take<uint8_t>(BN);
+            dv.clamp_col = c.take<uint8_t>(BM);
+            dv.alpha = c.take<double>((size_t)(L + 1) * BN);
+            dv.beta = c.take<double>((size_t)(L + 1) * BM);
+            dv.rden = c.take<double>((size_t)std::max(L, 1) * BN);
+            dv.sden = c.take<double>((size_t)std::max(L, 1) * BM);
+            dv.dvec = c.take<double>(BN);
+        };
+        Carve size;
+        lay(size);
+        Carve c{keep.get<uint8_t>(size.off)};
+        if (keep.failed)
+            return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (plan)");
+        lay(c);
+    }
     // the per-sample Sinkhorn path: the column softmax writes each pair into
     // its pieces (no separate packing launch)
     if (plan->sink_fwd) {
