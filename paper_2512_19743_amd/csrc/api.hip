@@ -544,10 +544,33 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         choose_chunks(B, M, N, &cols.S, &cols.chunk, 256, 16384);
         cols.owner_blocks = ceil_div(M, kBlock);
         cols.tiles = B * cols.S * cols.owner_blocks;
-        rows.partial = dense_tmp.get<float2>((size_t)rows.S * BN);
-        cols.partial = dense_tmp.get<float2>((size_t)cols.S * BM);
-        float *E_row = dense_tmp.get<float>(BN);
-        float4 *ypack = dense_tmp.get<float4>(BM);
+        choose_chunks(B, N, M, &ea.S, &ea.chunk, 256);
+        // the scratch of both scans in one allocation; the counting pass
+        // keeps the first hits of every (row, chunk), at 16-bit offsets
+        // within the chunk
+        float *E_row = nullptr;
+        float4 *ypack = nullptr;
+        auto lay = [&](Carve &c) {
+            rows.partial = c.take<float2>((size_t)rows.S * BN);
+            cols.partial = c.take<float2>((size_t)cols.S * BM);
+            E_row = c.take<float>(BN);
+            ypack = c.take<float4>(BM);
+            ea.cnt = c.take<int32_t>((size_t)BN * ea.S);
+            if (ea.chunk <= 65536) {
+                ea.kst = stage_slots(ea.S);
+                ea.stage = c.take<uint16_t>((size_t)BN * ea.S * ea.kst);
+                const size_t tiles = (size_t)B * ea.S * rows.owner_blocks;
+                ea.spill = c.take<uint32_t>(tiles * kTileSpill);
+                ea.spill_n = c.take<int32_t>(tiles);
+            }
+        };
+        {
+            Carve size;
+            lay(size);
+            Carve c{dense_tmp.get<uint8_t>(size.off)};
+            if (!dense_tmp.failed)
+                lay(c);
+        }
         if (tmp.failed || dense_tmp.failed || keep.failed)
             return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (statistics)");
         {
@@ -569,19 +592,8 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         ea.N = N;
         ea.M = M;
         ea.owner_blocks = rows.owner_blocks;
-        choose_chunks(B, N, M, &ea.S, &ea.chunk, 256);
-        ea.cnt = dense_tmp.get<int32_t>((size_t)BN * ea.S);
         ea.col_cnt = col_cnt; // cleared by the finalize kernel
         ea.ctr = dv.ctr;
-        // the counting pass keeps the first hits of every (row, chunk);
-        // offsets within a chunk are 16-bit
-        if (ea.chunk <= 65536) {
-            ea.kst = stage_slots(ea.S);
-            ea.stage = dense_tmp.get<uint16_t>((size_t)BN * ea.S * ea.kst);
-            const size_t tiles = (size_t)B * ea.S * ea.owner_blocks;
-            ea.spill = dense_tmp.get<uint32_t>(tiles * kTileSpill);
-            ea.spill_n = dense_tmp.get<int32_t>(tiles);
-        }
         cnt = ea.cnt;
         cnt_chunks = ea.S;
     } else {
@@ -897,13 +909,22 @@ apml_status apml_backward(apml_plan *plan, const float *x, const float *y, const
     dv.grad_loss = grad_loss;
     dv.grad_x = grad_x;
     dv.grad_y = grad_y;
-    dv.adj = tmp.get<double>(plan->stored);
-    dv.cbar = tmp.get<double>(plan->stored);
-    if (dv.L > 0 && !plan->sink_bwd) {
-        dv.rz = tmp.get<double>(plan->stored);
-        dv.kz = tmp.get<double>(plan->stored);
-        dv.xyr = tmp.get<float4>((size_t)plan->B * plan->N);
-        dv.xyc = tmp.get<float4>((size_t)plan->B * plan->M);
+    auto lay = [&](Carve &c) {
+        dv.adj = c.take<double>(plan->stored);
+        dv.cbar = c.take<double>(plan->stored);
+        if (dv.L > 0 && !plan->sink_bwd) {
+            dv.rz = c.take<double>(plan->stored);
+            dv.kz = c.take<double>(plan->stored);
+            dv.xyr = c.take<float4>((size_t)plan->B * plan->N);
+            dv.xyc = c.take<float4>((size_t)plan->B * plan->M);
+        }
+    };
+    {
+        Carve size;
+        lay(size);
+        Carve c{tmp.get<uint8_t>(size.off)};
+        if (!tmp.failed)
+            lay(c);
     }
     if (tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (backward)");
