@@ -606,18 +606,40 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         sa.pad_x = pad_x;
         sa.pad_y = pad_y;
         const size_t n_sort = (size_t)B * pad_x + (size_t)B * pad_y;
-        for (int k = 0; k < 2; ++k) {
-            sa.key[k] = dense_tmp.get<uint32_t>(n_sort);
-            sa.val[k] = dense_tmp.get<uint32_t>(n_sort);
-        }
-        sa.sx = dense_tmp.get<float4>((size_t)B * pad_x);
-        sa.sy = dense_tmp.get<float4>((size_t)B * pad_y);
-        sa.box_x = dense_tmp.get<Box>((size_t)B * pad_x / kRun);
-        sa.box_y = dense_tmp.get<Box>((size_t)B * pad_y / kRun);
         sa.ctr = dv.ctr;
-        if (std::max(N, M) > kSortChunkPoints) { // chunked sort: the frame from partial boxes
+        crows.waves = ceil_div(N, kScanRows);
+        if (std::max(N, M) > kSortChunkPoints) // chunked sort: the frame from partial boxes
             sa.frame_slices = ceil_div((int64_t)N + M, 16384);
-            sa.frame_part = dense_tmp.get<float>((size_t)B * sa.frame_slices * 6);
+        // the scratch of both scans in one allocation
+        Box *batch_x = nullptr, *batch_y = nullptr;
+        float *E_row = nullptr;
+        float4 *ypack = nullptr;
+        auto lay = [&](Carve &c) {
+            for (int k = 0; k < 2; ++k) {
+                sa.key[k] = c.take<uint32_t>(n_sort);
+                sa.val[k] = c.take<uint32_t>(n_sort);
+            }
+            sa.sx = c.take<float4>((size_t)B * pad_x);
+            sa.sy = c.take<float4>((size_t)B * pad_y);
+            sa.box_x = c.take<Box>((size_t)B * pad_x / kRun);
+            sa.box_y = c.take<Box>((size_t)B * pad_y / kRun);
+            sa.frame_part = sa.frame_slices ? c.take<float>((size_t)B * sa.frame_slices * 6) : nullptr;
+            batch_x = c.take<Box>((size_t)B * batches(pad_x));
+            batch_y = c.take<Box>((size_t)B * batches(pad_y));
+            crows.m12s = c.take<float2>((size_t)B * pad_x);
+            ccols.m12s = c.take<float2>((size_t)B * pad_y);
+            E_row = c.take<float>((size_t)B * pad_x);
+            ypack = c.take<float4>((size_t)B * pad_y);
+            ca.cnt = c.take<int32_t>(BN);
+            ca.stage = c.take<int32_t>((size_t)BN * kCullStage);
+            ca.wg_over = c.take<uint8_t>((size_t)B * crows.waves);
+        };
+        {
+            Carve size;
+            lay(size);
+            Carve c{dense_tmp.get<uint8_t>(size.off)};
+            if (!dense_tmp.failed)
+                lay(c);
         }
         crows.own = sa.sx;
         crows.bc = sa.sy;
@@ -627,7 +649,6 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         crows.n_bc = M;
         crows.pad_own = pad_x;
         crows.pad_bc = pad_y;
-        crows.waves = ceil_div(N, kScanRows);
         ccols.own = sa.sy;
         ccols.bc = sa.sx;
         ccols.own_box = sa.box_y;
@@ -637,14 +658,8 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         ccols.pad_own = pad_y;
         ccols.pad_bc = pad_x;
         ccols.waves = ceil_div(M, kScanRows);
-        Box *batch_x = dense_tmp.get<Box>((size_t)B * batches(pad_x));
-        Box *batch_y = dense_tmp.get<Box>((size_t)B * batches(pad_y));
         crows.bc_batch = batch_y;
         ccols.bc_batch = batch_x;
-        crows.m12s = dense_tmp.get<float2>((size_t)B * pad_x);
-        ccols.m12s = dense_tmp.get<float2>((size_t)B * pad_y);
-        float *E_row = dense_tmp.get<float>((size_t)B * pad_x);
-        float4 *ypack = dense_tmp.get<float4>((size_t)B * pad_y);
         if (tmp.failed || dense_tmp.failed || keep.failed)
             return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (statistics)");
         {
@@ -678,10 +693,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         ca.pad_x = pad_x;
         ca.pad_y = pad_y;
         ca.waves = crows.waves;
-        ca.cnt = dense_tmp.get<int32_t>(BN);
         ca.col_cnt = col_cnt; // cleared by the finalize kernel
-        ca.stage = dense_tmp.get<int32_t>((size_t)BN * kCullStage);
-        ca.wg_over = dense_tmp.get<uint8_t>((size_t)B * ca.waves);
         ca.ctr = dv.ctr;
         cnt = ca.cnt;
     }
