@@ -857,8 +857,6 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
             dv.clamp_col = c.take<uint8_t>(BM);
             dv.alpha = c.take<double>((size_t)(L + 1) * BN);
             dv.beta = c.take<double>((size_t)(L + 1) * BM);
-            dv.rden = c.take<double>((size_t)std::max(L, 1) * BN);
-            dv.sden = c.take<double>((size_t)std::max(L, 1) * BM);
             dv.dvec = c.take<double>(BN);
         };
         Carve size;

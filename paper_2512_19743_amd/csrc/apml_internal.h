@@ -282,7 +282,6 @@ struct DevPlan {
     int32_t *pos_col;             // [2*B*M] column-major positions
     uint8_t *clamp_row, *clamp_col;
     double *alpha, *beta;         // [(L+1)][B*N], [(L+1)][B*M] Sinkhorn scalings
-    double *rden, *sden;          // [L][B*N], [L][B*M]: R + eps, S + eps
     Counters *ctr;
     float *loss;                  // [B]
     // backward

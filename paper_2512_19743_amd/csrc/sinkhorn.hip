@@ -276,9 +276,9 @@ constexpr int kFwdWideSlots = 4;
 // The head lane of an owner's group applies the owner's scaling as soon as
 // the group has its sum: v = cur / (cur * sum + eps) (Eq. 3 or Eq. 4), into
 // the owner's side array in LDS (which the phase does not gather from) and
-// into the saved scalings and denominators.
+// into the saved scalings.
 __device__ __forceinline__ void apply_scaling(double acc, uint32_t info, double *own, double eps, double *g_val,
-                                              double *g_den, const Unpack &u)
+                                              const Unpack &u)
 {
     if (u.bits(info, 14, 2) == 3u) { // head and valid
         const int o = u.owner(info);
@@ -287,7 +287,6 @@ __device__ __forceinline__ void apply_scaling(double acc, uint32_t info, double 
         const double v = quotient(cur, den);
         own[o] = v;
         g_val[o] = v;
-        g_den[o] = den;
     }
 }
 
@@ -323,21 +322,21 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan 
     for (int l = 1; l <= L; ++l) {
         const Unpack u = Unpack::make();
         // column scaling (Eq. 3): beta_j /= beta_j sum_i alpha_i P0_ij + eps
-        double *gb = d.beta + l * BM + (size_t)b * M, *gs = d.sden + (l - 1) * BM + (size_t)b * M;
+        double *gb = d.beta + l * BM + (size_t)b * M;
 #pragma unroll
         for (int s = 0; s < SLP; ++s)
             if (wave_active(pc, s)) {
                 const double acc = slot_dot(pc, pcw, s, va, u);
-                apply_scaling(group_reduce(acc, pc.info[s], u), pc.info[s], vb, eps, gb, gs, u);
+                apply_scaling(group_reduce(acc, pc.info[s], u), pc.info[s], vb, eps, gb, u);
             }
         lds_barrier();
         // row scaling (Eq. 4): alpha_i /= alpha_i sum_j P0_ij beta_j + eps
-        double *ga = d.alpha + l * BN + (size_t)b * N, *gr = d.rden + (l - 1) * BN + (size_t)b * N;
+        double *ga = d.alpha + l * BN + (size_t)b * N;
 #pragma unroll
         for (int s = 0; s < SLP; ++s)
             if (wave_active(pr, s)) {
                 const double acc = slot_dot(pr, prw, s, vb, u);
-                apply_scaling(group_reduce(acc, pr.info[s], u), pr.info[s], va, eps, ga, gr, u);
+                apply_scaling(group_reduce(acc, pr.info[s], u), pr.info[s], va, eps, ga, u);
             }
         lds_barrier();
     }
@@ -615,7 +614,7 @@ template <bool COL> __global__ __launch_bounds__(kBlock) void k_sink_step(DevPla
     const float *p0 = COL ? d.p0c : d.p0r;
     // the other side's scalings: alpha^(l-1) for columns, beta^l for rows
     const double *oth = (COL ? d.alpha + (size_t)(l - 1) * BN : d.beta + (size_t)l * BM) + (size_t)b * n_oth;
-    double *cur = COL ? d.beta : d.alpha, *den_out = COL ? d.sden : d.rden;
+    double *cur = COL ? d.beta : d.alpha;
     const size_t BO = COL ? BM : BN;
     const double prev = cur[(size_t)(l - 1) * BO + o]; // loaded with the segment bounds
     const int s0 = ptr[o], n = ptr[o + 1] - s0;
@@ -636,7 +635,6 @@ template <bool COL> __global__ __launch_bounds__(kBlock) void k_sink_step(DevPla
     if (lg == 0) {
         const double den = prev * acc + eps;
         cur[(size_t)l * BO + o] = prev / den;
-        den_out[(size_t)(l - 1) * BO + o] = den;
     }
 }
 
