@@ -919,14 +919,19 @@ apml_status apml_backward(apml_plan *plan, const float *x, const float *y, const
     dv.grad_loss = grad_loss;
     dv.grad_x = grad_x;
     dv.grad_y = grad_y;
+    // On the per-iteration path the row-order sweep adjoint becomes the final
+    // adjoint in place (k_bwd_final reads and writes the same pair), and the
+    // cost adjoint reuses the column-order copy, dead once the sweeps end.
     auto lay = [&](Carve &c) {
         dv.adj = c.take<double>(plan->stored);
-        dv.cbar = c.take<double>(plan->stored);
         if (dv.L > 0 && !plan->sink_bwd) {
-            dv.rz = c.take<double>(plan->stored);
+            dv.rz = dv.adj;
             dv.kz = c.take<double>(plan->stored);
+            dv.cbar = dv.kz;
             dv.xyr = c.take<float4>((size_t)plan->B * plan->N);
             dv.xyc = c.take<float4>((size_t)plan->B * plan->M);
+        } else {
+            dv.cbar = c.take<double>(plan->stored);
         }
     };
     {

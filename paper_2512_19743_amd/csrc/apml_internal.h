@@ -291,7 +291,8 @@ struct DevPlan {
     double *dvec;                 // [B*N] row losses of the per-iteration forward kernels
     float4 *xyr, *xyc;            // [B*N], [B*M] per-owner values of the per-iteration reverse sweeps: X, Y and
                                   // the reciprocal of the owner's scaling
-    double *rz, *kz;              // [nnz] reverse-sweep adjoints in row and in column order (per-iteration kernels)
+    double *rz, *kz;              // [nnz] reverse-sweep adjoints in row and in column order (per-iteration
+                                  // kernels; rz shares adj's memory and cbar kz's)
     PackedOrder pk_row, pk_col;   // per-sample Sinkhorn pieces (when that path is taken)
     const int32_t *sink_place;    // during the forward softmax of that path: the pieces' placement, so that the
                                   // column softmax writes every pair into its pieces; else NULL
