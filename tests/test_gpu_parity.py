@@ -137,6 +137,19 @@ def test_reading_variants_with_ties(variant, scan):
         np.testing.assert_allclose(ex["p_row"][sel], 1.0 / Y.shape[1], rtol=1e-6)
 
 
+@pytest.mark.parametrize("scan", ["full", "skip"])
+def test_fallback_rows_take_the_per_iteration_path(scan):
+    # every reference point doubled: every row falls back to all 1200 columns,
+    # too many pieces for the per-sample Sinkhorn kernels, so the sweeps take
+    # one launch each
+    X, Y = custom(35, 1, 700, 600, sigma=0.05, reference="sphere", prediction="uniform_cube")
+    Y = np.ascontiguousarray(np.concatenate([Y, Y], axis=1))
+    g, res = _check_batch(X, Y, "fallback, whole rows", scan=scan, n_iter=5, **VARIANTS["all"])
+    st = g["plan"].export_stats(0)
+    assert (st["T_row"] == 0).all()
+    assert res[0]["nnz_gpu"] >= 700 * 1200
+
+
 @pytest.mark.parametrize("variant", ["mean_dup", "detached"])
 def test_reading_variants_tiny(variant):
     w = config(1)
