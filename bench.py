@@ -68,9 +68,9 @@ PHASE_MODEL = {
               {"full": "k_emit_compact_place: row-major structure from the staged hits, placement of the Sinkhorn pieces",
                "skip": "k_cull_order_place: row-major structure from the staged hits, placement of the Sinkhorn pieces"}),
     "softmax": ("hbm", _bytes(lambda w: 32 + 24), "bytes",
-                "k_csc_rows + k_col_softmax: column-major view, Eq. 1, Eq. 2, P0"),
+                "k_csc_rows + k_col_softmax: column-major view, Eq. 1, Eq. 2, P0 (written into the Sinkhorn pieces)"),
     "sinkhorn": ("hbm", _bytes(lambda w: 2 * w.n_iter * 8 + 8), "bytes",
-                 "k_pack_pairs + k_sinkhorn_fwd: L Sinkhorn iterations (Eq. 3, Eq. 4) and the loss"),
+                 "k_sinkhorn_fwd: L Sinkhorn iterations (Eq. 3, Eq. 4) and the loss"),
     "bwd_sinkhorn": ("hbm", _bytes(lambda w: 2 * w.n_iter * 16), "bytes",
                      "k_sinkhorn_bwd: reverse Sinkhorn sweeps"),
     "bwd_softmax": ("hbm", _bytes(lambda w: 24 + 8), "bytes",
@@ -83,13 +83,13 @@ PHASE_MODEL = {
 # entry names the source files it was measured on with their SHA-256: once a
 # file changes, traffic is reported as null until measured again.
 TRAFFIC = {
-    "stats": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/apml_internal.h": "da32312abd3cd19a70cdb14534b3b870b84eba4c168bd6a6563a07af9e5ce3e7", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_top2"], "bytes_per_launch": 32794787},
-    "support": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/apml_internal.h": "da32312abd3cd19a70cdb14534b3b870b84eba4c168bd6a6563a07af9e5ce3e7", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit"], "bytes_per_launch": 32859673},
-    "build": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "da32312abd3cd19a70cdb14534b3b870b84eba4c168bd6a6563a07af9e5ce3e7", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit_compact_place"], "bytes_per_launch": 23189572},
-    "softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "15992d8f233b535129ec9269c76a7b4de90a87f394d8ae57d683e1107e43c6b5", "paper_2512_19743_amd/csrc/apml_internal.h": "da32312abd3cd19a70cdb14534b3b870b84eba4c168bd6a6563a07af9e5ce3e7", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_csc_rows", "k_col_softmax"], "bytes_per_launch": 37358082},
-    "sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "e3e3f1daa114d42861dd0aad1d7f2d3d7e9d311de669a904b3129ad5948e63e0", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "da32312abd3cd19a70cdb14534b3b870b84eba4c168bd6a6563a07af9e5ce3e7", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_pack_pairs", "k_sinkhorn_fwd"], "bytes_per_launch": 61792837},
-    "bwd_sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "e3e3f1daa114d42861dd0aad1d7f2d3d7e9d311de669a904b3129ad5948e63e0", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "da32312abd3cd19a70cdb14534b3b870b84eba4c168bd6a6563a07af9e5ce3e7", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 26057928},
-    "bwd_softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "15992d8f233b535129ec9269c76a7b4de90a87f394d8ae57d683e1107e43c6b5", "paper_2512_19743_amd/csrc/apml_internal.h": "da32312abd3cd19a70cdb14534b3b870b84eba4c168bd6a6563a07af9e5ce3e7", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 33366348},
+    "stats": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/apml_internal.h": "785e5aa28dc56f6554029d4693937a5ba75ea074754c60e2d7ef97cda04d2fc6", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_top2"], "bytes_per_launch": 32795363},
+    "support": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/apml_internal.h": "785e5aa28dc56f6554029d4693937a5ba75ea074754c60e2d7ef97cda04d2fc6", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit"], "bytes_per_launch": 32853033},
+    "build": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "785e5aa28dc56f6554029d4693937a5ba75ea074754c60e2d7ef97cda04d2fc6", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit_compact_place"], "bytes_per_launch": 23189044},
+    "softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "e60ae38f51b348e507d98b90395a7968f6fcf72a7bbe7e7bc61c6e8f488f9cda", "paper_2512_19743_amd/csrc/apml_internal.h": "785e5aa28dc56f6554029d4693937a5ba75ea074754c60e2d7ef97cda04d2fc6", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_csc_rows", "k_col_softmax"], "bytes_per_launch": 45110532},
+    "sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "4c802f43f25de7177c72507d1ed13422c43d16c1647567695adad8abc2a7eb9b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "785e5aa28dc56f6554029d4693937a5ba75ea074754c60e2d7ef97cda04d2fc6", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_sinkhorn_fwd"], "bytes_per_launch": 26081540},
+    "bwd_sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "4c802f43f25de7177c72507d1ed13422c43d16c1647567695adad8abc2a7eb9b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "785e5aa28dc56f6554029d4693937a5ba75ea074754c60e2d7ef97cda04d2fc6", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 26068295},
+    "bwd_softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "e60ae38f51b348e507d98b90395a7968f6fcf72a7bbe7e7bc61c6e8f488f9cda", "paper_2512_19743_amd/csrc/apml_internal.h": "785e5aa28dc56f6554029d4693937a5ba75ea074754c60e2d7ef97cda04d2fc6", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 33363148},
 }
 
 
