@@ -987,18 +987,24 @@ apml_status apml_plan_nnz(const apml_plan *plan, int64_t *nnz)
     hipStream_t s = plan->stream;
     Arena tmp;
     tmp.stream = s;
-    unsigned long long *d = tmp.get<unsigned long long>(plan->B);
+    const int chunks = count_support_chunks(plan->max_sample);
+    const size_t parts = (size_t)plan->B * chunks;
+    unsigned long long *d = tmp.get<unsigned long long>(parts);
     if (tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed");
-    launch_count_support(plan->dv.row_ptr, plan->dv.flags, plan->B, plan->N, d, s);
+    launch_count_support(plan->dv.row_ptr, plan->dv.flags, plan->B, plan->N, chunks, d, s);
     HIP_TRY(hipGetLastError());
-    std::vector<unsigned long long> h(plan->B);
+    std::vector<unsigned long long> h(parts);
     Counters hc{};
-    HIP_TRY(hipMemcpyAsync(h.data(), d, sizeof(unsigned long long) * plan->B, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(h.data(), d, sizeof(unsigned long long) * parts, hipMemcpyDeviceToHost, s));
     HIP_TRY(hipMemcpyAsync(&hc, plan->dv.ctr, sizeof(Counters), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
-    for (int b = 0; b < plan->B; ++b)
-        nnz[b] = (int64_t)h[b];
+    for (int b = 0; b < plan->B; ++b) {
+        int64_t n = 0;
+        for (int c = 0; c < chunks; ++c)
+            n += (int64_t)h[(size_t)b * chunks + c];
+        nnz[b] = n;
+    }
     if (hc.error)
         return fail(APML_ERR_INTERNAL, "a row or column minimum was not found among its stored pairs");
     return APML_OK;

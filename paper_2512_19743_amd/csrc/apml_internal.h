@@ -364,7 +364,10 @@ hipError_t launch_sinkhorn_bwd(const DevPlan &d, int64_t max_pairs, hipStream_t 
 void launch_sinkhorn_fwd_steps(const DevPlan &d, double eps, hipStream_t s);
 void launch_sinkhorn_bwd_steps(const DevPlan &d, hipStream_t s);
 
-void launch_count_support(const int32_t *row_ptr, const uint8_t *flags, int B, int N,
+// Kept pairs per sample, in count_support_chunks(largest sample) partial
+// counts per sample: out [B][chunks].
+int count_support_chunks(int64_t max_pairs);
+void launch_count_support(const int32_t *row_ptr, const uint8_t *flags, int B, int N, int chunks,
                           unsigned long long *out, hipStream_t s);
 
 } // namespace apml

@@ -242,15 +242,20 @@ __global__ __launch_bounds__(kBlock) void k_csc_sort(DevPlan d, BuildArgs a)
     d.csc_perm[s0 + rank] = a.tmp_src[p];
 }
 
+// Kept pairs of one chunk of kCountChunk stored pairs of sample blockIdx.y
+// (grid: chunks x samples), into out[sample * chunks + chunk].
+constexpr int kCountChunk = 8192;
+
 __global__ __launch_bounds__(kBlock) void k_count_support(const int32_t *row_ptr,
                                                           const uint8_t *flags, int N,
                                                           unsigned long long *out)
 {
     __shared__ unsigned long long part[kBlock / 64];
-    const int b = blockIdx.x;
+    const int b = blockIdx.y;
     const int t0 = row_ptr[(size_t)b * N], t1 = row_ptr[(size_t)(b + 1) * N];
+    const int c0 = t0 + (int)blockIdx.x * kCountChunk, c1 = min(t1, c0 + kCountChunk);
     unsigned long long n = 0;
-    for (int t = t0 + threadIdx.x; t < t1; t += kBlock)
+    for (int t = c0 + threadIdx.x; t < c1; t += kBlock)
         n += flags[t] != 0;
     for (int off = 32; off > 0; off >>= 1)
         n += __shfl_xor(n, off);
@@ -261,7 +266,7 @@ __global__ __launch_bounds__(kBlock) void k_count_support(const int32_t *row_ptr
         unsigned long long s = 0;
         for (int w = 0; w < kBlock / 64; ++w)
             s += part[w];
-        out[b] = s;
+        out[(size_t)b * gridDim.x + blockIdx.x] = s;
     }
 }
 
@@ -289,10 +294,12 @@ void launch_csc_sort(const DevPlan &d, const BuildArgs &a, hipStream_t s)
     hipLaunchKernelGGL(k_csc_sort, dim3(blocks_for(d.nnz, kBlock)), dim3(kBlock), 0, s, d, a);
 }
 
-void launch_count_support(const int32_t *row_ptr, const uint8_t *flags, int B, int N,
+int count_support_chunks(int64_t max_pairs) { return (int)std::max<int64_t>(1, (max_pairs + kCountChunk - 1) / kCountChunk); }
+
+void launch_count_support(const int32_t *row_ptr, const uint8_t *flags, int B, int N, int chunks,
                           unsigned long long *out, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_count_support, dim3(B), dim3(kBlock), 0, s, row_ptr, flags, N, out);
+    hipLaunchKernelGGL(k_count_support, dim3(chunks, B), dim3(kBlock), 0, s, row_ptr, flags, N, out);
 }
 
 } // namespace apml
