@@ -25,7 +25,14 @@
 namespace apml {
 namespace {
 
-constexpr int G = kGroup;
+// G lanes per owner: 4, or 8 where the grid of 8 stays within 2^21 lanes and
+// that of 4 would hold fewer than 2^19 + 1 (measured: 8 lanes were 45 us
+// faster on 4 x 65536 points and 100 us slower on 64 x 8192 points, where
+// they double an already full grid; on 32 x 2048 points no faster).
+__host__ inline int softmax_lanes(int64_t owners)
+{
+    return owners * 8 <= (int64_t(1) << 21) && owners * 4 > (int64_t(1) << 19) ? 8 : kGroup;
+}
 
 // The forward softmax of one owner (a row, or a column) by its group of G
 // lanes. Lane lg sees pairs k = lg, lg + G, ... of the owner's segment; the
@@ -64,7 +71,8 @@ __device__ __forceinline__ double dist3(float ax, float ay, float az, float bx, 
 // ROWS: owner r = b*N + i over row-major pairs t (the other index is the
 // column j); else owner gc = b*M + j over column-major entries q (the other
 // index is the row i, the row-major position t = csc_perm[q]).
-template <bool ROWS> __device__ __forceinline__ void owner_softmax(const DevPlan &d, const Params &p, int o, int lg)
+template <bool ROWS, int G>
+__device__ __forceinline__ void owner_softmax(const DevPlan &d, const Params &p, int o, int lg)
 {
     const int n_own = ROWS ? d.N : d.M, n_oth = ROWS ? d.M : d.N;
     const int b = o / n_own;
@@ -232,20 +240,20 @@ template <bool ROWS> __device__ __forceinline__ void owner_softmax(const DevPlan
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_row_softmax(DevPlan d, Params p)
+template <int G> __global__ __launch_bounds__(kBlock) void k_row_softmax(DevPlan d, Params p)
 {
     const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // a sample's owners share an L2
     const int r = gid / G;
     if (r < d.B * d.N)
-        owner_softmax<true>(d, p, r, gid % G);
+        owner_softmax<true, G>(d, p, r, gid % G);
 }
 
-__global__ __launch_bounds__(kBlock) void k_col_softmax(DevPlan d, Params p)
+template <int G> __global__ __launch_bounds__(kBlock) void k_col_softmax(DevPlan d, Params p)
 {
     const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // a sample's owners share an L2
     const int gc = gid / G;
     if (gc < d.B * d.M)
-        owner_softmax<false>(d, p, gc, gid % G);
+        owner_softmax<false, G>(d, p, gc, gid % G);
 }
 
 // Column-major view of one sample (blockIdx.x) in one workgroup: every pair
@@ -302,7 +310,7 @@ __device__ __forceinline__ void csc_sample(const DevPlan &d, int b, uint32_t *ld
 // The column-major view of each sample (first B blocks) and the row softmax
 // (the other blocks, kCscT / G rows each): independent work in one launch, so
 // the row softmax runs on the CUs the per-sample blocks leave free.
-__global__ __launch_bounds__(kCscT) void k_csc_rows(DevPlan d, Params p)
+template <int G> __global__ __launch_bounds__(kCscT) void k_csc_rows(DevPlan d, Params p)
 {
     extern __shared__ uint32_t lds_csc[];
     if ((int)blockIdx.x < d.B) {
@@ -312,7 +320,7 @@ __global__ __launch_bounds__(kCscT) void k_csc_rows(DevPlan d, Params p)
     const int gid = (blockIdx.x - d.B) * kCscT + threadIdx.x;
     const int r = gid / G;
     if (r < d.B * d.N)
-        owner_softmax<true>(d, p, r, gid % G);
+        owner_softmax<true, G>(d, p, r, gid % G);
 }
 
 __host__ inline size_t csc_sample_lds(int M, int64_t max_pairs)
@@ -333,7 +341,7 @@ __device__ __forceinline__ double p0bar(const DevPlan &d, int t, double gl)
 //            term at the two argmins; written per pair (cbar).
 //   rows:    the same for P_row, plus cbar from the columns and the direct
 //            term grad_loss * v; then Eq. 5 turns cbar into grad_x.
-__global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(DevPlan d, Params p)
+template <int G> __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(DevPlan d, Params p)
 {
     const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // a sample's owners share an L2
     const int gc = gid / G, lg = gid % G;
@@ -413,7 +421,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(DevPlan d, Params p)
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_bwd_row_softmax(DevPlan d, Params p, int keep_cbar)
+template <int G> __global__ __launch_bounds__(kBlock) void k_bwd_row_softmax(DevPlan d, Params p, int keep_cbar)
 {
     const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // a sample's owners share an L2
     const int r = gid / G, lg = gid % G;
@@ -513,7 +521,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_row_softmax(DevPlan d, Params p,
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_bwd_grad_y(DevPlan d, Params p)
+template <int G> __global__ __launch_bounds__(kBlock) void k_bwd_grad_y(DevPlan d, Params p)
 {
     const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // a sample's owners share an L2
     const int gc = gid / G, lg = gid % G;
@@ -549,36 +557,49 @@ bool csc_sample_fits(int N, int M, int64_t max_pairs)
     return N <= 65536 && max_pairs <= 65536 && csc_sample_lds(M, max_pairs) <= 160 * 1024;
 }
 
+// Launches kernel template K with the lanes per owner of `owners`.
+#define APML_LAUNCH_G(K, owners, per_block, shmem, s, ...)                                                          \
+    do {                                                                                                           \
+        const int g_ = softmax_lanes(owners);                                                                      \
+        const dim3 grid_(blocks_for((int64_t)(owners) * g_, per_block));                                           \
+        if (g_ == 8)                                                                                               \
+            hipLaunchKernelGGL(K<8>, grid_, dim3(per_block), shmem, s, __VA_ARGS__);                               \
+        else                                                                                                       \
+            hipLaunchKernelGGL(K<kGroup>, grid_, dim3(per_block), shmem, s, __VA_ARGS__);                          \
+    } while (0)
+
 hipError_t launch_csc_and_softmax(const DevPlan &d, const Params &p, int64_t max_pairs, hipStream_t s)
 {
     const size_t bytes = csc_sample_lds(d.M, max_pairs);
-    hipError_t e = hipFuncSetAttribute((const void *)k_csc_rows, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       (int)bytes);
+    const int64_t BN = (int64_t)d.B * d.N;
+    const int gr = softmax_lanes(BN);
+    const void *k = gr == 8 ? (const void *)k_csc_rows<8> : (const void *)k_csc_rows<kGroup>;
+    hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess)
         return e;
-    const unsigned rows = blocks_for((int64_t)d.B * d.N * G, kCscT);
-    hipLaunchKernelGGL(k_csc_rows, dim3(d.B + rows), dim3(kCscT), bytes, s, d, p);
-    hipLaunchKernelGGL(k_col_softmax, dim3(blocks_for((int64_t)d.B * d.M * G, kBlock)), dim3(kBlock), 0, s, d, p);
+    const unsigned rows = blocks_for(BN * gr, kCscT);
+    if (gr == 8)
+        hipLaunchKernelGGL(k_csc_rows<8>, dim3(d.B + rows), dim3(kCscT), bytes, s, d, p);
+    else
+        hipLaunchKernelGGL(k_csc_rows<kGroup>, dim3(d.B + rows), dim3(kCscT), bytes, s, d, p);
+    APML_LAUNCH_G(k_col_softmax, (int64_t)d.B * d.M, kBlock, 0, s, d, p);
     return hipGetLastError();
 }
 
 void launch_softmax(const DevPlan &d, const Params &p, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_row_softmax, dim3(blocks_for((int64_t)d.B * d.N * G, kBlock)), dim3(kBlock), 0, s,
-                       d, p);
-    hipLaunchKernelGGL(k_col_softmax, dim3(blocks_for((int64_t)d.B * d.M * G, kBlock)), dim3(kBlock), 0, s,
-                       d, p);
+    APML_LAUNCH_G(k_row_softmax, (int64_t)d.B * d.N, kBlock, 0, s, d, p);
+    APML_LAUNCH_G(k_col_softmax, (int64_t)d.B * d.M, kBlock, 0, s, d, p);
 }
 
 void launch_bwd_softmax(const DevPlan &d, const Params &p, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_bwd_col_softmax, dim3(blocks_for((int64_t)d.B * d.M * G, kBlock)), dim3(kBlock), 0,
-                       s, d, p);
-    hipLaunchKernelGGL(k_bwd_row_softmax, dim3(blocks_for((int64_t)d.B * d.N * G, kBlock)), dim3(kBlock), 0,
-                       s, d, p, d.grad_y != nullptr ? 1 : 0);
+    APML_LAUNCH_G(k_bwd_col_softmax, (int64_t)d.B * d.M, kBlock, 0, s, d, p);
+    APML_LAUNCH_G(k_bwd_row_softmax, (int64_t)d.B * d.N, kBlock, 0, s, d, p, d.grad_y != nullptr ? 1 : 0);
     if (d.grad_y)
-        hipLaunchKernelGGL(k_bwd_grad_y, dim3(blocks_for((int64_t)d.B * d.M * G, kBlock)), dim3(kBlock), 0, s,
-                           d, p);
+        APML_LAUNCH_G(k_bwd_grad_y, (int64_t)d.B * d.M, kBlock, 0, s, d, p);
 }
+
+#undef APML_LAUNCH_G
 
 } // namespace apml
