@@ -83,13 +83,13 @@ PHASE_MODEL = {
 # entry names the source files it was measured on with their SHA-256: once a
 # file changes, traffic is reported as null until measured again.
 TRAFFIC = {
-    "stats": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_top2"], "bytes_per_launch": 32793955},
-    "support": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit"], "bytes_per_launch": 32856345},
-    "build": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit_compact_place"], "bytes_per_launch": 23188884},
-    "softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "e60ae38f51b348e507d98b90395a7968f6fcf72a7bbe7e7bc61c6e8f488f9cda", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_csc_rows", "k_col_softmax"], "bytes_per_launch": 45108580},
+    "stats": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_top2"], "bytes_per_launch": 32794531},
+    "support": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit"], "bytes_per_launch": 32857993},
+    "build": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit_compact_place"], "bytes_per_launch": 23189412},
+    "softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "083b4fd2edd2980ac8cfd94a426dbcdb3c2e0009101b2824711be304ce307d34", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_csc_rows", "k_col_softmax"], "bytes_per_launch": 45071558},
     "sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "4c802f43f25de7177c72507d1ed13422c43d16c1647567695adad8abc2a7eb9b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_sinkhorn_fwd"], "bytes_per_launch": 26081540},
-    "bwd_sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "4c802f43f25de7177c72507d1ed13422c43d16c1647567695adad8abc2a7eb9b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 26068807},
-    "bwd_softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "e60ae38f51b348e507d98b90395a7968f6fcf72a7bbe7e7bc61c6e8f488f9cda", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 33363148},
+    "bwd_sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "4c802f43f25de7177c72507d1ed13422c43d16c1647567695adad8abc2a7eb9b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 26068935},
+    "bwd_softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "083b4fd2edd2980ac8cfd94a426dbcdb3c2e0009101b2824711be304ce307d34", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 33356621},
 }
 
 
