@@ -20,4 +20,4 @@ from ._lib import (  # noqa: F401
     apml_set_allocator_torch,
     load,
 )
-from .loss import APMLFunction, apml_loss  # noqa: F401
+from .loss import APMLFunction, apml_loss, loss_params  # noqa: F401

@@ -105,3 +105,14 @@ def test_binding_refuses_cpu_tensors():
     x = torch.zeros(1, 4, 3)
     with pytest.raises(ValueError, match="GPU"):
         _lib.apml_forward(x, x)
+
+
+def test_loss_params_by_name():
+    from paper_2512_19743_amd.loss import loss_params
+    p = loss_params(gap_mode="uniform_fallback", sym_mode="mean_dup", tgrad_mode="detached", dense_scan="skip",
+                    n_iter=3)
+    assert (p.gap_mode, p.sym_mode, p.tgrad_mode, p.dense_scan, p.n_iter) == (1, 1, 1, 2, 3)
+    d = loss_params()
+    assert (d.gap_mode, d.sym_mode, d.tgrad_mode, d.dense_scan) == (0, 0, 0, 0)
+    with pytest.raises(ValueError):
+        loss_params(sym_mode="average")

@@ -199,6 +199,18 @@ def test_autograd_wrapper_mean_reduction():
     assert rel_norm(y.grad.cpu().numpy().astype(np.float64), ref_gy / 4) <= 1e-4
 
 
+def test_autograd_wrapper_variant_by_name():
+    X, Y = custom(36, 2, 120, 110, sigma=0.05)
+    note("autograd wrapper, variants")
+    x = torch.from_numpy(X).cuda().requires_grad_(True)
+    y = torch.from_numpy(Y).cuda()
+    loss = apml.apml_loss(x, y, reduction="sum", sym_mode="mean_dup", tgrad_mode="detached", n_iter=5)
+    loss.backward()
+    ref_l, ref_gx, _ = oracle.run_batch(X, Y, oracle_params(n_iter=5, sym_mode=1, tgrad_mode=1), grad=True)
+    assert loss.item() == pytest.approx(ref_l.sum(), rel=1e-5)
+    assert rel_norm(x.grad.cpu().numpy().astype(np.float64), ref_gx) <= 1e-4
+
+
 def test_rejects_bad_input_on_gpu():
     x = torch.zeros(2, 8, 3, device="cuda")
     with pytest.raises(apml.ApmlError):
