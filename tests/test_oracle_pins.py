@@ -475,6 +475,35 @@ def test_detached_temperature_drops_gap_term():
     np.testing.assert_allclose(r.grad_y, gy, rtol=1e-9, atol=1e-12 * np.abs(gy).max())
 
 
+def test_mean_dup_finite_differences():
+    # literal duplicate averaging is still a differentiable function of the
+    # points away from support changes: its hand-written gradient against
+    # central differences of its own loss
+    x, y = _cloud(24, 13, 16, sigma=0.15)
+    prm = oracle.params(n_iter=4, sym_mode=1)
+    r = oracle.run_sample(x, y, prm, grad=True)
+    assert ((r.flags == 1) | (r.flags == 2)).any()  # singletons exist, so the variant differs
+    x64, y64 = x.astype(np.float64), y.astype(np.float64)
+    h = 1e-6
+    rng = np.random.default_rng(3)
+    checked = 0
+    for which, base, g in (("x", x64, r.grad_x), ("y", y64, r.grad_y)):
+        for _ in range(10):
+            a, k = int(rng.integers(base.shape[0])), int(rng.integers(3))
+            vals = []
+            for sgn in (1, -1):
+                pert = base.copy()
+                pert[a, k] += sgn * h
+                vals.append(oracle.run_sample(pert if which == "x" else x64, y64 if which == "x" else pert, prm,
+                                              grad=False))
+            if any(v.nnz != r.nnz or not np.array_equal(v.flags, r.flags) for v in vals):
+                continue
+            fd = (vals[0].loss - vals[1].loss) / (2 * h)
+            assert fd == pytest.approx(g[a, k], rel=2e-5, abs=2e-6 * np.abs(g).max())
+            checked += 1
+    assert checked >= 14
+
+
 @pytest.mark.parametrize("mode", [dict(sym_mode=1), dict(gap_mode=1), dict(gap_mode=1, sym_mode=1, tgrad_mode=1)])
 def test_variants_match_dense_formulation(mode):
     x, y = _tie_cloud(23) if mode.get("gap_mode") else _cloud(23, 21, 26, sigma=0.1)
