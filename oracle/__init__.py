@@ -50,18 +50,20 @@ class Params(ctypes.Structure):
         ("gap_mode", ctypes.c_int32),    # 0 clamp, 1 uniform fallback
         ("sym_mode", ctypes.c_int32),    # 0 half sum, 1 mean of the present sides
         ("tgrad_mode", ctypes.c_int32),  # 0 full, 1 temperature detached
+        ("select_mode", ctypes.c_int32),  # 0 minima decided in float32 (R2), 1 in float64
     ]
 
 
 DEFAULTS = dict(p_min=0.8, tau=1e-8, eps_stab=1e-8, delta=1e-8, eps_gap=1e-6, eps_dist=1e-12, n_iter=10,
-                gap_mode=0, sym_mode=0, tgrad_mode=0)
+                gap_mode=0, sym_mode=0, tgrad_mode=0, select_mode=0)
 
 
 def params(**kw) -> Params:
     d = dict(DEFAULTS)
     d.update(kw)
     return Params(d["p_min"], d["tau"], d["eps_stab"], d["delta"], d["eps_gap"], d["eps_dist"],
-                  int(d["n_iter"]), int(d["gap_mode"]), int(d["sym_mode"]), int(d["tgrad_mode"]))
+                  int(d["n_iter"]), int(d["gap_mode"]), int(d["sym_mode"]), int(d["tgrad_mode"]),
+                  int(d["select_mode"]))
 
 
 def _load():

@@ -53,6 +53,11 @@
  *                    P0 = (P_row + P_col)/2 where both directions keep the
  *                    pair, the one present value elsewhere.
  *   tgrad_mode = 1   the temperature is a constant in the backward pass.
+ *   select_mode = 1  the minimum and second minimum are decided on the cost
+ *                    in double precision instead of reading R2 (the paper
+ *                    defines them on C, Sec. III-A, Eq. 1; this variant
+ *                    measures how much the single-precision decision moves
+ *                    the result).
  *
  * Build: gcc -O2 -fopenmp -ffp-contract=off -fPIC -shared (fmaf is the
  * correctly rounded C library fused multiply-add).
@@ -76,6 +81,7 @@ typedef struct {
     int32_t gap_mode;   /* 0: clamp (Sec. III-D); 1: uniform fallback (Sec. III-A, III-C) */
     int32_t sym_mode;   /* 0: P0 = (P_row + P_col)/2, absent side 0; 1: mean of the present sides */
     int32_t tgrad_mode; /* 0: full gradient; 1: temperature treated as a constant */
+    int32_t select_mode; /* 0: minima decided in single precision (R2); 1: in double precision */
 } orc_params;
 
 enum { ORC_GAP_CLAMP = 0, ORC_GAP_FALLBACK = 1 };
@@ -100,6 +106,15 @@ static float sqdist_single(const double *a, const double *b)
     s = fmaf(dy, dy, s);
     s = fmaf(dz, dz, s);
     return s;
+}
+
+/* Squared distance in double precision (the select_mode = 1 variant). The
+ * order of a square root is that of its argument, so deciding on it decides
+ * on the cost itself. */
+static double sqdist_double(const double *a, const double *b)
+{
+    const double dx = a[0] - b[0], dy = a[1] - b[1], dz = a[2] - b[2];
+    return dx * dx + dy * dy + dz * dz;
 }
 
 /* Cost C = ||a - b||_2 (Sec. III-A), double precision. */
@@ -129,10 +144,11 @@ typedef struct {
 static void owner_statistics(const double *p, const double *Q, int K, const orc_params *prm,
                              owner_stats *st)
 {
-    float m1 = INFINITY, m2 = INFINITY;
+    double m1 = INFINITY, m2 = INFINITY;
     int k1 = -1, k2 = -1;
     for (int k = 0; k < K; ++k) {
-        const float d = sqdist_single(p, Q + 3 * (size_t)k);
+        const double d = prm->select_mode ? sqdist_double(p, Q + 3 * (size_t)k)
+                                          : (double)sqdist_single(p, Q + 3 * (size_t)k);
         if (d < m1) {
             m2 = m1;
             k2 = k1;
@@ -299,7 +315,8 @@ static int valid(int N, int M, const orc_params *p)
         return 0;
     if (!(p->delta >= 0.0) || !(p->eps_gap > 0.0) || !(p->eps_stab >= 0.0) || !(p->eps_dist >= 0.0))
         return 0;
-    if ((unsigned)p->gap_mode > 1u || (unsigned)p->sym_mode > 1u || (unsigned)p->tgrad_mode > 1u)
+    if ((unsigned)p->gap_mode > 1u || (unsigned)p->sym_mode > 1u || (unsigned)p->tgrad_mode > 1u ||
+        (unsigned)p->select_mode > 1u)
         return 0;
     return 1;
 }

@@ -33,7 +33,7 @@ def _check_batch(X, Y, label, samples=None, check_grad_y=True, scan=None, **prm)
     for b in (range(X.shape[0]) if samples is None else samples):
         ref = oracle.run_sample(X[b], Y[b], oracle_params(**prm), grad=True)
         out.append(compare_sample(g, b, X[b], Y[b], ref, tau, check_grad_y=check_grad_y))
-    worst = {k: max(r[k] for r in out) for k in ("loss_rel", "gx_rel", "gy_rel", "v_rel")}
+    worst = {k: max(r[k] for r in out) for k in ("loss_rel", "gx_rel", "gy_rel", "gx_row", "gy_row", "v_rel")}
     note(f"{label}: worst relative errors " + ", ".join(f"{k} {v:.2e}" for k, v in worst.items()))
     return g, out
 
@@ -249,6 +249,19 @@ def test_large_workloads_one_sample_exact(cfg, scan):
     w = config(cfg)
     X, Y = batch(w)
     _check_batch(X, Y, w.name, samples=[0], n_iter=w.n_iter, scan=scan)
+
+
+@pytest.mark.parametrize("cfg,sample", [(3, 63), (4, 15), (5, 0), (5, 3)])
+def test_large_workloads_exact_sample(cfg, sample):
+    # the whole batch on the GPU in the benchmark's launch configuration
+    # (automatic scan mode: skipping scans for the large batch and the large
+    # scene, per-iteration Sinkhorn sweeps for all three); one sample against
+    # a full oracle run: the last sample of the large batch and of the unequal
+    # workload (the largest row, column and pair offsets), the first and the
+    # last sample of the large scene
+    w = config(cfg)
+    X, Y = batch(w)
+    _check_batch(X, Y, w.name, samples=[sample], n_iter=w.n_iter)
 
 
 def test_large_scene_sampled_owners_and_invariants():
