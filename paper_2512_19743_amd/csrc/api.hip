@@ -3,12 +3,15 @@
 // and backward passes (Algorithm 1 of the paper, redesigned as described at
 // the top of kernels.hip).
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <mutex>
 #include <string>
+#include <thread>
 #include <unordered_map>
 #include <utility>
 #include <vector>
@@ -172,9 +175,20 @@ void pool_free(void *p, size_t size, hipStream_t s)
     m.free_blocks[{dev, s}].insert({size, p});
 }
 
-// A set of device blocks released together.
+// A region that arenas carve from front to back, never giving memory back
+// within a call (the static scratch of apml_forward_backward_noalloc).
+struct Bump {
+    uint8_t *base = nullptr;
+    size_t cap = 0;
+    size_t used = 0;
+    size_t need = 0; // bytes the call asked for when the region ran out
+};
+
+// A set of device blocks released together: from the pool (or the caller's
+// allocator), or carved from a bump region.
 struct Arena {
     hipStream_t stream = nullptr;
+    Bump *bump = nullptr;
     std::vector<std::pair<void *, size_t>> blocks;
     int64_t bytes = 0;
     bool failed = false;
@@ -183,8 +197,20 @@ struct Arena {
     {
         if (failed)
             return nullptr;
+        const size_t want = std::max<size_t>(count * sizeof(T), 16);
+        if (bump) {
+            const size_t at = (bump->used + 255) & ~size_t(255);
+            if (at > bump->cap || want > bump->cap - at) {
+                bump->need = std::max(bump->need, at + want);
+                failed = true;
+                return nullptr;
+            }
+            bump->used = at + want;
+            bytes += (int64_t)want;
+            return reinterpret_cast<T *>(bump->base + at);
+        }
         size_t got = 0;
-        void *p = pool_alloc(std::max<size_t>(count * sizeof(T), 16), stream, &got);
+        void *p = pool_alloc(want, stream, &got);
         if (!p) {
             failed = true;
             return nullptr;
@@ -260,8 +286,10 @@ hipEvent_t take_event()
 
 class PhaseTimer {
   public:
-    PhaseTimer(int phase, hipStream_t s) : phase_(phase), s_(s)
+    PhaseTimer(int phase, hipStream_t s, bool enabled = true) : phase_(phase), s_(s)
     {
+        if (!enabled)
+            return;
         Profiler &p = prof();
         std::lock_guard<std::mutex> lk(p.mu);
         if (!p.on)
@@ -315,6 +343,7 @@ struct apml_plan {
     int64_t max_sample = 0; // stored pairs of the largest sample
     bool sink_fwd = false;  // per-sample Sinkhorn kernels take this plan (forward)
     bool sink_bwd = false;  // and the reverse sweeps
+    bool timed = true;  // phases recorded by the profiler (off for the no-alloc entry point)
     Arena keep;         // everything backward and export need
     DevPlan dv{};       // device arrays (x, y and the backward fields are set per call)
 };
@@ -360,14 +389,43 @@ double log_ratio(int K, double p) { return -std::log((1.0 - p) / ((double)(K - 1
 
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
-// Waits for the stream by polling: the forward's one synchronisation sits
-// on the critical path, and a blocking wait adds the wake-up latency.
-hipError_t wait_for(hipStream_t s)
+// Seconds the forward waits for its read-back before it reports the device
+// as stuck: APML_WAIT_TIMEOUT_S if set (0 allowed), else 600.
+double wait_deadline_s()
 {
-    for (;;) {
+    const char *v = std::getenv("APML_WAIT_TIMEOUT_S");
+    if (v && *v) {
+        char *end = nullptr;
+        const double t = std::strtod(v, &end);
+        if (end != v && t >= 0.0)
+            return t;
+    }
+    return 600.0;
+}
+
+// Waits for the stream by polling: the forward's one synchronisation sits
+// on the critical path, and a blocking wait adds the wake-up latency. After
+// the first 2 ms the poll sleeps 50 us between queries; past the deadline the
+// call fails with APML_ERR_DEVICE instead of waiting for ever.
+apml_status wait_for(hipStream_t s)
+{
+    using clock = std::chrono::steady_clock;
+    const auto t0 = clock::now();
+    const double deadline = wait_deadline_s();
+    for (unsigned n = 0;; ++n) {
         const hipError_t e = hipStreamQuery(s);
+        if (e == hipSuccess)
+            return APML_OK;
         if (e != hipErrorNotReady)
-            return e;
+            return fail(APML_ERR_DEVICE, std::string("hipStreamQuery: ") + hipGetErrorString(e));
+        if ((n & 63) != 0)
+            continue;
+        const double waited = std::chrono::duration<double>(clock::now() - t0).count();
+        if (waited > deadline)
+            return fail(APML_ERR_DEVICE, "the stream did not reach the forward's read-back within " +
+                                             std::to_string(deadline) + " s (APML_WAIT_TIMEOUT_S)");
+        if (waited > 2e-3)
+            std::this_thread::sleep_for(std::chrono::microseconds(50));
     }
 }
 
@@ -444,31 +502,20 @@ apml_status apml_plan_destroy(apml_plan *plan)
     return APML_OK;
 }
 
-apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, int32_t M,
-                         int32_t d, const apml_params *params, float *loss, apml_plan **plan_out,
-                         apml_stream stream)
-{
-    g_last_error.clear();
-    if (plan_out)
-        *plan_out = nullptr;
-    apml_params prm;
-    apml_params_default(&prm);
-    if (params)
-        prm = *params;
-    apml_status st = validate(x, y, B, N, M, d, prm, loss);
-    if (st != APML_OK)
-        return st;
-    hipStream_t s = (hipStream_t)stream;
+} // extern "C"
 
-    apml_plan *plan = new apml_plan();
-    {
-        std::lock_guard<std::mutex> lk(mem().mu);
-        mem().live_plans++;
-    }
-    struct Guard {
-        apml_plan *p;
-        ~Guard() { apml_plan_destroy(p); }
-    } guard{plan};
+namespace {
+
+// Bytes of the read-back block the no-alloc entry point keeps in host memory
+// of its own (it bounds B there).
+constexpr size_t kStaticReadbackBytes = 64 << 10;
+
+// The forward pass (Alg. 1) into plan, whose device memory comes from
+// plan->keep: the pool (or the caller's allocator), or a bump region. The
+// arguments are validated.
+apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t B, int32_t N, int32_t M,
+                        const apml_params &prm, float *loss, hipStream_t s)
+{
     HIP_TRY(hipGetDevice(&plan->device));
     const int L = prm.n_iter;
     plan->B = B;
@@ -497,6 +544,8 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     Arena tmp, dense_tmp; // dense_tmp: scratch of the dense scans, released once the CSR is written
     tmp.stream = s;
     dense_tmp.stream = s;
+    tmp.bump = dense_tmp.bump = plan->keep.bump;
+    const bool timed = plan->timed;
     Arena &keep = plan->keep;
     DevPlan &dv = plan->dv;
     dv.B = B;
@@ -574,7 +623,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         if (tmp.failed || dense_tmp.failed || keep.failed)
             return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (statistics)");
         {
-            PhaseTimer pt(PH_STATS, s);
+            PhaseTimer pt(PH_STATS, s, timed);
             launch_top2(rows, cols, B, s);
             HIP_TRY(hipGetLastError());
             pt.stop();
@@ -663,7 +712,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         if (tmp.failed || dense_tmp.failed || keep.failed)
             return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (statistics)");
         {
-            PhaseTimer pt(PH_STATS, s);
+            PhaseTimer pt(PH_STATS, s, timed);
             HIP_TRY(launch_spatial_sort(sa, s)); // also clears the counters
             launch_batch_boxes(sa.box_x, sa.box_y, batch_x, batch_y, B, pad_x, pad_y, false, s);
             launch_cull_top2(crows, ccols, B, dv.ctr, s);
@@ -698,20 +747,29 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         cnt = ca.cnt;
     }
     int32_t *off_tiles = tmp.get<int32_t>(offsets_scratch_ints(B, N, M));
-    std::vector<uint8_t> rb_host(readback_bytes(B));
+    // the read-back block: the kernels write it straight into mapped pinned
+    // host memory (no copy launch; the buffer is shared, so it is held until
+    // copied out), or, with a bump region, into device memory copied out once
+    const bool bumped = plan->keep.bump != nullptr;
+    uint8_t *rb_dev = bumped ? tmp.get<uint8_t>(readback_bytes(B)) : nullptr;
     if (tmp.failed || dense_tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (support)");
-    // the kernels write the read-back block straight into pinned host memory
-    // (no copy launch); the buffer is shared, so it is held until copied out
-    std::unique_lock<std::mutex> pin_lock(pinned().mu);
-    Readback *rb_pin = (Readback *)pinned().get(plan->device, readback_bytes(B));
-    if (!rb_pin)
-        return fail(APML_ERR_OUT_OF_MEMORY, "pinned host allocation failed (read-back)");
-    Readback *rb = (Readback *)rb_host.data();
+    alignas(16) static thread_local uint8_t rb_static[kStaticReadbackBytes];
+    std::vector<uint8_t> rb_vec(bumped ? 0 : readback_bytes(B));
+    uint8_t *rb_host = bumped ? rb_static : rb_vec.data();
+    std::unique_lock<std::mutex> pin_lock(pinned().mu, std::defer_lock);
+    Readback *rb_pin = nullptr;
+    if (!bumped) {
+        pin_lock.lock();
+        rb_pin = (Readback *)pinned().get(plan->device, readback_bytes(B));
+        if (!rb_pin)
+            return fail(APML_ERR_OUT_OF_MEMORY, "pinned host allocation failed (read-back)");
+    }
+    Readback *rb = (Readback *)rb_host;
     const int64_t *totals = readback_totals(rb);
     const int32_t *offsets = readback_offsets(rb, B), *pieces = readback_pieces(rb, B);
     {
-        PhaseTimer pt(PH_SUPPORT, s);
+        PhaseTimer pt(PH_SUPPORT, s, timed);
         if (skip)
             launch_cull_emit_count(ca, s);
         else
@@ -719,13 +777,21 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         HIP_TRY(hipGetLastError());
         pt.stop();
     }
-    // row and column offsets, and what the host needs, in one copy
+    // row and column offsets, and what the host needs, in one block
     launch_offsets(cnt, cnt_chunks, col_cnt, dv.ctr, B, N, M, dv.row_ptr, dv.col_ptr, off_tiles,
-                   (Readback *)pinned().device_ptr(plan->device), s);
+                   bumped ? (Readback *)rb_dev : (Readback *)pinned().device_ptr(plan->device), s);
     HIP_TRY(hipGetLastError());
-    HIP_TRY(wait_for(s));
-    std::memcpy(rb_host.data(), rb_pin, readback_bytes(B));
-    pin_lock.unlock();
+    if (bumped)
+        HIP_TRY(hipMemcpyAsync(rb_host, rb_dev, readback_bytes(B), hipMemcpyDeviceToHost, s));
+    {
+        const apml_status ws = wait_for(s);
+        if (ws != APML_OK)
+            return ws;
+    }
+    if (!bumped) {
+        std::memcpy(rb_host, rb_pin, readback_bytes(B));
+        pin_lock.unlock();
+    }
     int64_t nnz = 0;
     for (int b = 0; b < B; ++b) {
         if (totals[b] != totals[B + b])
@@ -803,7 +869,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     if (tmp.failed || keep.failed || dense_tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (sparse arrays)");
     {
-        PhaseTimer pt(PH_BUILD, s);
+        PhaseTimer pt(PH_BUILD, s, timed);
         if (skip) {
             ca.row_ptr = dv.row_ptr;
             ca.csr_col = dv.csr_col;
@@ -874,7 +940,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         dv.sink_place = place;
     }
     {
-        PhaseTimer pt(PH_SOFTMAX, s);
+        PhaseTimer pt(PH_SOFTMAX, s, timed);
         if (csc_lds) {
             HIP_TRY(launch_csc_and_softmax(dv, kp, plan->max_sample, s));
         } else {
@@ -886,7 +952,7 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
 
     // ---- Sinkhorn (Eq. 3, Eq. 4) and the loss ------------------------------
     {
-        PhaseTimer pt(PH_SINKHORN, s);
+        PhaseTimer pt(PH_SINKHORN, s, timed);
         if (plan->sink_fwd) {
             dv.sink_place = nullptr; // scratch of this call
             HIP_TRY(launch_sinkhorn_fwd(dv, prm.eps_stab, s));
@@ -897,6 +963,41 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
         pt.stop();
     }
     tmp.release();
+    return APML_OK;
+}
+
+} // namespace
+
+extern "C" {
+
+apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, int32_t M,
+                         int32_t d, const apml_params *params, float *loss, apml_plan **plan_out,
+                         apml_stream stream)
+{
+    g_last_error.clear();
+    if (plan_out)
+        *plan_out = nullptr;
+    apml_params prm;
+    apml_params_default(&prm);
+    if (params)
+        prm = *params;
+    apml_status st = validate(x, y, B, N, M, d, prm, loss);
+    if (st != APML_OK)
+        return st;
+    hipStream_t s = (hipStream_t)stream;
+
+    apml_plan *plan = new apml_plan();
+    {
+        std::lock_guard<std::mutex> lk(mem().mu);
+        mem().live_plans++;
+    }
+    struct Guard {
+        apml_plan *p;
+        ~Guard() { apml_plan_destroy(p); }
+    } guard{plan};
+    st = run_forward(plan, x, y, B, N, M, prm, loss, s);
+    if (st != APML_OK)
+        return st;
     if (plan_out) {
         guard.p = nullptr;
         *plan_out = plan;
@@ -904,15 +1005,18 @@ apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, i
     return APML_OK;
 }
 
-apml_status apml_backward(apml_plan *plan, const float *x, const float *y, const float *grad_loss,
-                          float *grad_x, float *grad_y, apml_stream stream)
+} // extern "C"
+
+namespace {
+
+// The backward pass (Sec. III-D) of a plan; scratch from the pool or from the
+// plan's bump region.
+apml_status run_backward(apml_plan *plan, const float *x, const float *y, const float *grad_loss,
+                         float *grad_x, float *grad_y, hipStream_t s)
 {
-    g_last_error.clear();
-    if (!plan || !x || !y || !grad_loss || !grad_x)
-        return fail(APML_ERR_INVALID_ARG, "plan, x, y, grad_loss and grad_x must be non-NULL");
-    hipStream_t s = (hipStream_t)stream;
     Arena tmp;
     tmp.stream = s;
+    tmp.bump = plan->keep.bump;
     DevPlan dv = plan->dv;
     dv.x = x;
     dv.y = y;
@@ -944,7 +1048,7 @@ apml_status apml_backward(apml_plan *plan, const float *x, const float *y, const
     if (tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (backward)");
     {
-        PhaseTimer pt(PH_BWD_SINK, s);
+        PhaseTimer pt(PH_BWD_SINK, s, plan->timed);
         if (dv.L > 0) {
             if (plan->sink_bwd) {
                 HIP_TRY(launch_sinkhorn_bwd(dv, plan->max_sample, s));
@@ -956,13 +1060,26 @@ apml_status apml_backward(apml_plan *plan, const float *x, const float *y, const
         pt.stop();
     }
     {
-        PhaseTimer pt(PH_BWD_SOFTMAX, s);
+        PhaseTimer pt(PH_BWD_SOFTMAX, s, plan->timed);
         launch_bwd_softmax(dv, plan->kp, s);
         HIP_TRY(hipGetLastError());
         pt.stop();
     }
     tmp.release();
     return APML_OK;
+}
+
+} // namespace
+
+extern "C" {
+
+apml_status apml_backward(apml_plan *plan, const float *x, const float *y, const float *grad_loss,
+                          float *grad_x, float *grad_y, apml_stream stream)
+{
+    g_last_error.clear();
+    if (!plan || !x || !y || !grad_loss || !grad_x)
+        return fail(APML_ERR_INVALID_ARG, "plan, x, y, grad_loss and grad_x must be non-NULL");
+    return run_backward(plan, x, y, grad_loss, grad_x, grad_y, (hipStream_t)stream);
 }
 
 apml_status apml_plan_get_info(const apml_plan *plan, apml_plan_info *info)
