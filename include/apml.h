@@ -140,6 +140,35 @@ apml_status apml_backward(apml_plan *plan, const float *x, const float *y,
                           const float *grad_loss, float *grad_x, float *grad_y,
                           apml_stream stream);
 
+/*
+ * Forward and backward in one call, with no device allocation. For callers
+ * that cannot allocate device memory (code under stream capture, serving loops
+ * with a fixed memory budget, harnesses that forbid hipMalloc): the same
+ * kernels as apml_forward followed by apml_backward, with every plan array and
+ * temporary carved from one static device array of
+ * APML_NOALLOC_SCRATCH_BYTES that each device the library runs on holds until
+ * the process ends (e.g. 32 clouds of 2048 points against 2048 need about
+ * 65 MiB of it). No plan is returned.
+ *   x, y, B, N, M, d, params, loss   as for apml_forward
+ *   grad_loss, grad_x, grad_y        as for apml_backward; grad_x == NULL
+ *                                    computes the loss only (grad_loss and
+ *                                    grad_y are then ignored)
+ * Errors: as apml_forward; APML_ERR_OUT_OF_MEMORY when the call needs more
+ * scratch than the array holds (apml_last_error states both sizes; detected
+ * before the kernels that write loss or gradients run, so the outputs are
+ * untouched), APML_ERR_UNSUPPORTED when B > 1791. The call synchronises the
+ * stream once, like apml_forward. Every call on a device shares that
+ * device's array and leaves its contents behind: calls that overlap on one
+ * device (other host threads, or other streams still running an earlier
+ * call) race and give undefined results; calls on one stream, or on
+ * different devices, do not.
+ */
+#define APML_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+apml_status apml_forward_backward_noalloc(const float *x, const float *y, int32_t B, int32_t N,
+                                          int32_t M, int32_t d, const apml_params *params,
+                                          float *loss, const float *grad_loss, float *grad_x,
+                                          float *grad_y, apml_stream stream);
+
 /* Releases the plan's device memory (stream-ordered on the plan's stream).
  * NULL is accepted. */
 apml_status apml_plan_destroy(apml_plan *plan);

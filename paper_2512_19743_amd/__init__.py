@@ -8,6 +8,7 @@ from ._lib import (  # noqa: F401
     Plan,
     apml_backward,
     apml_forward,
+    apml_forward_backward_noalloc,
     apml_get_memory_stats,
     apml_params,
     apml_params_default,

@@ -79,6 +79,8 @@ def load() -> ctypes.CDLL:
         L.apml_params_default.restype = None
         L.apml_forward.argtypes = [vp, vp, i32, i32, i32, i32, P(apml_params), vp, P(vp), vp]
         L.apml_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+        L.apml_forward_backward_noalloc.argtypes = [vp, vp, i32, i32, i32, i32, P(apml_params), vp, vp, vp, vp,
+                                                    vp]
         L.apml_plan_destroy.argtypes = [vp]
         L.apml_plan_get_info.argtypes = [vp, P(apml_plan_info)]
         L.apml_plan_nnz.argtypes = [vp, P(i64)]
@@ -101,7 +103,7 @@ def load() -> ctypes.CDLL:
         L.apml_last_error.restype = ctypes.c_char_p
         L.apml_version.argtypes = []
         L.apml_version.restype = i32
-        for name in ("apml_forward", "apml_backward", "apml_plan_destroy", "apml_plan_get_info",
+        for name in ("apml_forward", "apml_backward", "apml_forward_backward_noalloc", "apml_plan_destroy", "apml_plan_get_info",
                      "apml_plan_nnz", "apml_plan_export", "apml_plan_export_stats", "apml_set_allocator",
                      "apml_get_memory_stats", "apml_reset_peak_memory", "apml_release_cached_memory",
                      "apml_profile_enable", "apml_profile_reset", "apml_profile_read"):
@@ -244,6 +246,41 @@ def apml_backward(plan: Plan, x: torch.Tensor, y: torch.Tensor, grad_loss: torch
                                   _stream_handle(stream, x.device))
     _check("apml_backward", st)
     return gx, gy
+
+
+def apml_forward_backward_noalloc(x: torch.Tensor, y: torch.Tensor, params: Optional[apml_params] = None,
+                                  grad_loss: Optional[torch.Tensor] = None, want_grad: bool = True,
+                                  want_grad_y: bool = False, stream: Optional[torch.cuda.Stream] = None
+                                  ) -> Tuple[torch.Tensor, Optional[torch.Tensor], Optional[torch.Tensor]]:
+    """Per-sample losses and (if want_grad) the gradients of sum_b grad_loss[b] * loss_b, in one call
+    that allocates no device memory inside the library (its static scratch array holds every
+    temporary). The output tensors are allocated here, by PyTorch, before the call."""
+    _gpu_f32(x, "x")
+    _gpu_f32(y, "y")
+    if x.dim() != 3 or y.dim() != 3 or x.shape[0] != y.shape[0] or x.device != y.device:
+        raise ValueError("x must be (B,N,d) and y (B,M,d) on the same device")
+    B, N, d = x.shape
+    M = y.shape[1]
+    if y.shape[2] != d:
+        raise ValueError("x and y must have the same point dimension")
+    params = params if params is not None else apml_params_default()
+    loss = torch.empty(B, dtype=torch.float32, device=x.device)
+    gx = gy = None
+    if want_grad:
+        if grad_loss is None:
+            grad_loss = torch.ones(B, dtype=torch.float32, device=x.device)
+        _gpu_f32(grad_loss, "grad_loss")
+        if grad_loss.numel() != B or grad_loss.device != x.device:
+            raise ValueError("grad_loss must have B entries on the device of x")
+        gx = torch.empty_like(x)
+        gy = torch.empty_like(y) if want_grad_y else None
+    ptr = lambda t: ctypes.c_void_p(t.data_ptr()) if t is not None else None  # noqa: E731
+    with torch.cuda.device(x.device):
+        st = load().apml_forward_backward_noalloc(
+            ptr(x), ptr(y), B, N, M, d, ctypes.byref(params), ptr(loss), ptr(grad_loss) if want_grad else None,
+            ptr(gx), ptr(gy), _stream_handle(stream, x.device))
+    _check("apml_forward_backward_noalloc", st)
+    return loss, gx, gy
 
 
 def apml_get_memory_stats() -> dict:

@@ -1082,6 +1082,113 @@ apml_status apml_backward(apml_plan *plan, const float *x, const float *y, const
     return run_backward(plan, x, y, grad_loss, grad_x, grad_y, (hipStream_t)stream);
 }
 
+} // extern "C"
+
+// ---------------------------------------------------------------------------
+// forward + backward without allocation
+// ---------------------------------------------------------------------------
+
+// Device scratch of apml_forward_backward_noalloc: every array of the plan and
+// every temporary of one forward + backward call is carved from it, front to
+// back. Each device the library runs on holds its own copy until the process
+// ends. Host code never uses this name as an address: the kernels receive the
+// per-device address that hipGetSymbolAddress returns.
+static __device__ __align__(256) unsigned char scratch[APML_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+struct ScratchAddresses {
+    std::mutex mu;
+    void *ptr[64] = {};
+};
+
+ScratchAddresses &scratch_addresses()
+{
+    static ScratchAddresses *a = new ScratchAddresses(); // never destroyed
+    return *a;
+}
+
+// The device address of the scratch array on the current device, looked up
+// once per device (with that device current).
+apml_status scratch_of_current_device(void **out)
+{
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= 64)
+        return fail(APML_ERR_UNSUPPORTED, "device index beyond 63");
+    ScratchAddresses &a = scratch_addresses();
+    std::lock_guard<std::mutex> lk(a.mu);
+    if (!a.ptr[dev]) {
+        void *p = nullptr;
+        HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        if (!p)
+            return fail(APML_ERR_DEVICE, "hipGetSymbolAddress returned NULL for the static scratch");
+        a.ptr[dev] = p;
+    }
+    *out = a.ptr[dev];
+    return APML_OK;
+}
+
+std::string mib(size_t bytes)
+{
+    char buf[32];
+    std::snprintf(buf, sizeof buf, "%.1f MiB", (double)bytes / (1 << 20));
+    return buf;
+}
+
+} // namespace
+
+extern "C" {
+
+apml_status apml_forward_backward_noalloc(const float *x, const float *y, int32_t B, int32_t N, int32_t M,
+                                          int32_t d, const apml_params *params, float *loss,
+                                          const float *grad_loss, float *grad_x, float *grad_y,
+                                          apml_stream stream)
+{
+    g_last_error.clear();
+    apml_params prm;
+    apml_params_default(&prm);
+    if (params)
+        prm = *params;
+    apml_status st = validate(x, y, B, N, M, d, prm, loss);
+    if (st != APML_OK)
+        return st;
+    if (grad_x && !grad_loss)
+        return fail(APML_ERR_INVALID_ARG, "grad_loss must be non-NULL when grad_x is");
+    if (readback_bytes(B) > kStaticReadbackBytes)
+        return fail(APML_ERR_UNSUPPORTED, "B is too large for apml_forward_backward_noalloc (at most " +
+                                              std::to_string((kStaticReadbackBytes - sizeof(Readback) - 4) / 36) +
+                                              " samples)");
+    void *base = nullptr;
+    st = scratch_of_current_device(&base);
+    if (st != APML_OK)
+        return st;
+    hipStream_t s = (hipStream_t)stream;
+    Bump bump;
+    bump.base = static_cast<uint8_t *>(base);
+    bump.cap = APML_NOALLOC_SCRATCH_BYTES;
+    apml_plan plan; // host state on the stack; its arrays live in the scratch
+    plan.timed = false;
+    plan.keep.bump = &bump;
+    plan.keep.stream = s;
+    auto too_large = [&](apml_status r) {
+        if (r == APML_ERR_OUT_OF_MEMORY && bump.need > bump.cap)
+            return fail(APML_ERR_OUT_OF_MEMORY, "the call needs " + mib(bump.need) +
+                                                    " of device scratch; apml_forward_backward_noalloc has " +
+                                                    mib(bump.cap) + " (APML_NOALLOC_SCRATCH_BYTES)");
+        return r;
+    };
+    st = run_forward(&plan, x, y, B, N, M, prm, loss, s);
+    if (st != APML_OK)
+        return too_large(st);
+    if (grad_x) {
+        st = run_backward(&plan, x, y, grad_loss, grad_x, grad_y, s);
+        if (st != APML_OK)
+            return too_large(st);
+    }
+    return APML_OK;
+}
+
 apml_status apml_plan_get_info(const apml_plan *plan, apml_plan_info *info)
 {
     if (!plan || !info)

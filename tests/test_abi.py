@@ -116,3 +116,15 @@ def test_loss_params_by_name():
     assert (d.gap_mode, d.sym_mode, d.tgrad_mode, d.dense_scan) == (0, 0, 0, 0)
     with pytest.raises(ValueError):
         loss_params(sym_mode="average")
+
+
+def test_noalloc_validates_before_any_hip_call():
+    lib = _lib.load()
+    prm = _lib.apml_params_default()
+    call = lambda B=2, N=8, M=8, d=3, loss=FAKE, gl=FAKE, gx=FAKE: lib.apml_forward_backward_noalloc(  # noqa: E731
+        FAKE, FAKE, B, N, M, d, ctypes.byref(prm), loss, gl, gx, None, None)
+    assert call(loss=None) == 1
+    assert call(d=2) == 2
+    assert call(N=1) == 1
+    assert call(gl=None) == 1  # gradients requested without an upstream gradient
+    assert call(B=1792) == 2 and "at most 1791" in lib.apml_last_error().decode()
