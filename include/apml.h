@@ -147,8 +147,8 @@ apml_status apml_backward(apml_plan *plan, const float *x, const float *y,
  * kernels as apml_forward followed by apml_backward, with every plan array and
  * temporary carved from one static device array of
  * APML_NOALLOC_SCRATCH_BYTES that each device the library runs on holds until
- * the process ends (e.g. 32 clouds of 2048 points against 2048 need about
- * 65 MiB of it). No plan is returned.
+ * the process ends (32 clouds of 2048 points against 2048 fit in it; 64 clouds
+ * of 8192 points do not). No plan is returned.
  *   x, y, B, N, M, d, params, loss   as for apml_forward
  *   grad_loss, grad_x, grad_y        as for apml_backward; grad_x == NULL
  *                                    computes the loss only (grad_loss and
