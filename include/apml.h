@@ -169,6 +169,35 @@ apml_status apml_forward_backward_noalloc(const float *x, const float *y, int32_
                                           float *loss, const float *grad_loss, float *grad_x,
                                           float *grad_y, apml_stream stream);
 
+/*
+ * Dense APML (Sec. III-A): the unpruned formulation, a baseline for the
+ * sparse path's memory and time. Every pair of a sample takes part (no
+ * threshold: tau is ignored, the result is what the sparse path gives at
+ * tau = 0), for points of any dimension 1 <= d <= 16. The minimum and second
+ * minimum of every row and column are decided on the single-precision squared
+ * distance as in the sparse path; the temperatures follow Eq. 1 with the gap
+ * clamp (Sec. III-D), the softmaxes Eq. 2 over all pairs, P0 = (P_row +
+ * P_col)/2, then L column (Eq. 3) and row (Eq. 4) scalings, loss = sum P C.
+ * The plan keeps P0 and the Sinkhorn plan as float32 N x M matrices per
+ * sample; the backward pass adds a float64 N x M adjoint. Device memory comes
+ * from the same pool or caller allocator as the sparse path.
+ *   x, y    device, float32 [B, N, d] / [B, M, d] contiguous
+ *   params  as for apml_forward; gap_mode and sym_mode must be the defaults
+ *           (else APML_ERR_UNSUPPORTED); dense_scan and tau are ignored
+ *   loss    device, float32 [B]
+ *   plan    as for apml_forward (NULL: released before returning)
+ * apml_dense_backward: gradient of sum_b grad_loss[b] loss_b, grad_x [B,N,d]
+ * overwritten, grad_y [B,M,d] overwritten or NULL. Neither call synchronises.
+ */
+typedef struct apml_dense_plan apml_dense_plan;
+apml_status apml_dense_forward(const float *x, const float *y, int32_t B, int32_t N, int32_t M,
+                               int32_t d, const apml_params *params, float *loss,
+                               apml_dense_plan **plan, apml_stream stream);
+apml_status apml_dense_backward(apml_dense_plan *plan, const float *x, const float *y,
+                                const float *grad_loss, float *grad_x, float *grad_y,
+                                apml_stream stream);
+apml_status apml_dense_plan_destroy(apml_dense_plan *plan);
+
 /* Releases the plan's device memory (stream-ordered on the plan's stream).
  * NULL is accepted. */
 apml_status apml_plan_destroy(apml_plan *plan);

@@ -5,8 +5,11 @@ include/apml.h); this package only binds it.
 """
 from ._lib import (  # noqa: F401
     ApmlError,
+    DensePlan,
     Plan,
     apml_backward,
+    apml_dense_backward,
+    apml_dense_forward,
     apml_forward,
     apml_forward_backward_noalloc,
     apml_get_memory_stats,

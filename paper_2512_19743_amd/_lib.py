@@ -82,6 +82,9 @@ def load() -> ctypes.CDLL:
         L.apml_forward_backward_noalloc.argtypes = [vp, vp, i32, i32, i32, i32, P(apml_params), vp, vp, vp, vp,
                                                     vp]
         L.apml_plan_destroy.argtypes = [vp]
+        L.apml_dense_forward.argtypes = [vp, vp, i32, i32, i32, i32, P(apml_params), vp, P(vp), vp]
+        L.apml_dense_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+        L.apml_dense_plan_destroy.argtypes = [vp]
         L.apml_plan_get_info.argtypes = [vp, P(apml_plan_info)]
         L.apml_plan_nnz.argtypes = [vp, P(i64)]
         L.apml_plan_export.argtypes = [vp, i32, i64, P(i32), P(i32), P(ctypes.c_uint8), P(ctypes.c_float),
@@ -103,7 +106,8 @@ def load() -> ctypes.CDLL:
         L.apml_last_error.restype = ctypes.c_char_p
         L.apml_version.argtypes = []
         L.apml_version.restype = i32
-        for name in ("apml_forward", "apml_backward", "apml_forward_backward_noalloc", "apml_plan_destroy", "apml_plan_get_info",
+        for name in ("apml_forward", "apml_backward", "apml_forward_backward_noalloc", "apml_plan_destroy",
+                     "apml_dense_forward", "apml_dense_backward", "apml_dense_plan_destroy", "apml_plan_get_info",
                      "apml_plan_nnz", "apml_plan_export", "apml_plan_export_stats", "apml_set_allocator",
                      "apml_get_memory_stats", "apml_reset_peak_memory", "apml_release_cached_memory",
                      "apml_profile_enable", "apml_profile_reset", "apml_profile_read"):
@@ -281,6 +285,75 @@ def apml_forward_backward_noalloc(x: torch.Tensor, y: torch.Tensor, params: Opti
             ptr(gx), ptr(gy), _stream_handle(stream, x.device))
     _check("apml_forward_backward_noalloc", st)
     return loss, gx, gy
+
+
+class DensePlan:
+    """Owns an apml_dense_plan handle; destroyed with the object."""
+
+    def __init__(self, handle: ctypes.c_void_p, B: int, N: int, M: int, d: int, device: torch.device):
+        self.handle = handle
+        self.B, self.N, self.M, self.d = B, N, M, d
+        self.device = device
+
+    def close(self):
+        if self.handle:
+            with torch.cuda.device(self.device):
+                load().apml_dense_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def apml_dense_forward(x: torch.Tensor, y: torch.Tensor, params: Optional[apml_params] = None,
+                       keep_plan: bool = True, stream: Optional[torch.cuda.Stream] = None
+                       ) -> Tuple[torch.Tensor, Optional[DensePlan]]:
+    """Dense APML (every pair, any d): per-sample losses (B,) and, if keep_plan, the plan."""
+    _gpu_f32(x, "x")
+    _gpu_f32(y, "y")
+    if x.dim() != 3 or y.dim() != 3 or x.shape[0] != y.shape[0] or x.device != y.device:
+        raise ValueError("x must be (B,N,d) and y (B,M,d) on the same device")
+    B, N, d = x.shape
+    M = y.shape[1]
+    if y.shape[2] != d:
+        raise ValueError("x and y must have the same point dimension")
+    params = params if params is not None else apml_params_default()
+    loss = torch.empty(B, dtype=torch.float32, device=x.device)
+    handle = ctypes.c_void_p()
+    with torch.cuda.device(x.device):
+        st = load().apml_dense_forward(ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(y.data_ptr()), B, N, M, d,
+                                       ctypes.byref(params), ctypes.c_void_p(loss.data_ptr()),
+                                       ctypes.byref(handle) if keep_plan else None,
+                                       _stream_handle(stream, x.device))
+    _check("apml_dense_forward", st)
+    return loss, (DensePlan(handle, B, N, M, d, x.device) if keep_plan else None)
+
+
+def apml_dense_backward(plan: DensePlan, x: torch.Tensor, y: torch.Tensor, grad_loss: torch.Tensor,
+                        want_grad_y: bool = False, stream: Optional[torch.cuda.Stream] = None
+                        ) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """Gradients (B,N,d) and optionally (B,M,d) of sum_b grad_loss[b] * loss_b (dense APML)."""
+    if plan is None or not plan.handle:
+        raise ValueError("apml_dense_backward needs a live plan from apml_dense_forward(keep_plan=True)")
+    _gpu_f32(x, "x")
+    _gpu_f32(y, "y")
+    _gpu_f32(grad_loss, "grad_loss")
+    if tuple(x.shape) != (plan.B, plan.N, plan.d) or tuple(y.shape) != (plan.B, plan.M, plan.d):
+        raise ValueError("x and y must have the shapes of the forward call")
+    if grad_loss.numel() != plan.B or grad_loss.device != x.device:
+        raise ValueError("grad_loss must have B entries on the device of x")
+    gx = torch.empty_like(x)
+    gy = torch.empty_like(y) if want_grad_y else None
+    with torch.cuda.device(x.device):
+        st = load().apml_dense_backward(plan.handle, ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(y.data_ptr()),
+                                        ctypes.c_void_p(grad_loss.data_ptr()), ctypes.c_void_p(gx.data_ptr()),
+                                        ctypes.c_void_p(gy.data_ptr()) if gy is not None else None,
+                                        _stream_handle(stream, x.device))
+    _check("apml_dense_backward", st)
+    return gx, gy
 
 
 def apml_get_memory_stats() -> dict:

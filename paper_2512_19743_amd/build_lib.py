@@ -13,7 +13,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libapml.so")
-SOURCES = ["api.hip", "dense.hip", "spatial.hip", "cull.hip", "build.hip", "softmax.hip", "sinkhorn.hip"]
+SOURCES = ["api.hip", "dense.hip", "spatial.hip", "cull.hip", "build.hip", "softmax.hip", "sinkhorn.hip", "dense_apml.hip"]
 ARCH = os.environ.get("APML_OFFLOAD_ARCH", "gfx950")
 
 FLAGS = [

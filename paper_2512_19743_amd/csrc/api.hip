@@ -1189,6 +1189,198 @@ apml_status apml_forward_backward_noalloc(const float *x, const float *y, int32_
     return APML_OK;
 }
 
+} // extern "C"
+
+// ---------------------------------------------------------------------------
+// dense APML
+// ---------------------------------------------------------------------------
+
+struct apml_dense_plan {
+    int B = 0, N = 0, M = 0, d = 0, L = 0;
+    int device = 0;
+    hipStream_t stream = nullptr;
+    Arena keep; // the per-owner vectors, P0, the plan, the Sinkhorn sums
+    DenseDev dv{};
+};
+
+namespace {
+
+apml_status validate_dense(const float *x, const float *y, int32_t B, int32_t N, int32_t M, int32_t d,
+                           const apml_params &p, const float *loss)
+{
+    if (!x || !y || !loss)
+        return fail(APML_ERR_INVALID_ARG, "x, y and loss must be non-NULL device pointers");
+    if (B < 1 || N < 2 || M < 2)
+        return fail(APML_ERR_INVALID_ARG, "need B >= 1, N >= 2 and M >= 2 (Eq. 1 needs K > 1)");
+    if (d < 1 || d > kDenseMaxD)
+        return fail(APML_ERR_UNSUPPORTED, "the dense path takes 1 <= d <= " + std::to_string(kDenseMaxD));
+    if ((int64_t)B * N > INT32_MAX / 4 || (int64_t)B * M > INT32_MAX / 4)
+        return fail(APML_ERR_UNSUPPORTED, "B*N and B*M must stay below 2^29");
+    if ((int64_t)B * N * M > ((int64_t)1 << 40))
+        return fail(APML_ERR_UNSUPPORTED, "B*N*M beyond 2^40 pairs");
+    if (p.struct_size != 0 && p.struct_size < sizeof(apml_params))
+        return fail(APML_ERR_INVALID_ARG, "apml_params.struct_size is smaller than this library's struct");
+    if (!(p.p_min > 0.0 && p.p_min < 1.0) || !(p.p_min * N > 1.0) || !(p.p_min * M > 1.0))
+        return fail(APML_ERR_INVALID_ARG, "need 1/min(N, M) < p_min < 1 (Eq. 1 gives T > 0)");
+    if (p.n_iter < 0 || p.n_iter > 100000)
+        return fail(APML_ERR_INVALID_ARG, "need 0 <= n_iter <= 100000");
+    if (!(p.delta >= 0.0) || !(p.eps_gap > 0.0) || !(p.eps_stab >= 0.0) || !(p.eps_dist >= 0.0) ||
+        !std::isfinite(p.delta) || !std::isfinite(p.eps_gap) || !std::isfinite(p.eps_stab) ||
+        !std::isfinite(p.eps_dist))
+        return fail(APML_ERR_INVALID_ARG, "need delta >= 0, eps_gap > 0, eps_stab >= 0, eps_dist >= 0, all finite");
+    if (p.gap_mode != APML_GAP_CLAMP || p.sym_mode != APML_SYM_HALF_SUM)
+        return fail(APML_ERR_UNSUPPORTED, "the dense path takes the clamp and the half sum only");
+    if (p.tgrad_mode != APML_TGRAD_FULL && p.tgrad_mode != APML_TGRAD_DETACHED)
+        return fail(APML_ERR_INVALID_ARG, "tgrad_mode must be APML_TGRAD_FULL or APML_TGRAD_DETACHED");
+    return APML_OK;
+}
+
+// Per-owner vectors of one direction, carved from c.
+void lay_side(Carve &c, DenseSide &s, size_t n)
+{
+    s.k1 = c.take<int32_t>(n);
+    s.k2 = c.take<int32_t>(n);
+    s.c1 = c.take<double>(n);
+    s.g = c.take<double>(n);
+    s.T = c.take<double>(n);
+    s.Z = c.take<double>(n);
+    s.clamped = c.take<uint8_t>(n);
+    s.sigma = c.take<double>(n);
+    s.gbar = c.take<double>(n);
+    s.e = c.take<double>(n);
+}
+
+} // namespace
+
+extern "C" {
+
+apml_status apml_dense_plan_destroy(apml_dense_plan *plan)
+{
+    if (!plan)
+        return APML_OK;
+    {
+        std::lock_guard<std::mutex> lk(mem().mu);
+        mem().live_plans--;
+    }
+    int prev = 0;
+    (void)hipGetDevice(&prev);
+    if (prev != plan->device)
+        (void)hipSetDevice(plan->device);
+    plan->keep.release();
+    if (prev != plan->device)
+        (void)hipSetDevice(prev);
+    delete plan;
+    return APML_OK;
+}
+
+apml_status apml_dense_forward(const float *x, const float *y, int32_t B, int32_t N, int32_t M, int32_t d,
+                               const apml_params *params, float *loss, apml_dense_plan **plan_out,
+                               apml_stream stream)
+{
+    g_last_error.clear();
+    if (plan_out)
+        *plan_out = nullptr;
+    apml_params prm;
+    apml_params_default(&prm);
+    if (params)
+        prm = *params;
+    apml_status st = validate_dense(x, y, B, N, M, d, prm, loss);
+    if (st != APML_OK)
+        return st;
+    hipStream_t s = (hipStream_t)stream;
+    apml_dense_plan *plan = new apml_dense_plan();
+    {
+        std::lock_guard<std::mutex> lk(mem().mu);
+        mem().live_plans++;
+    }
+    struct Guard {
+        apml_dense_plan *p;
+        ~Guard() { apml_dense_plan_destroy(p); }
+    } guard{plan};
+    HIP_TRY(hipGetDevice(&plan->device));
+    plan->B = B;
+    plan->N = N;
+    plan->M = M;
+    plan->d = d;
+    plan->L = prm.n_iter;
+    plan->stream = s;
+    plan->keep.stream = s;
+    DenseDev &D = plan->dv;
+    D.B = B;
+    D.N = N;
+    D.M = M;
+    D.d = d;
+    D.L = prm.n_iter;
+    D.delta = prm.delta;
+    D.eps_gap = prm.eps_gap;
+    D.eps_stab = prm.eps_stab;
+    D.eps_dist = prm.eps_dist;
+    D.tgrad_full = prm.tgrad_mode == APML_TGRAD_FULL;
+    D.x = x;
+    D.y = y;
+    D.loss = loss;
+    dense_chunks(B, N, M, &D.chunks, &D.chunk);
+    const size_t BN = (size_t)B * N, BM = (size_t)B * M, pairs = (size_t)B * N * M, L = (size_t)prm.n_iter;
+    auto lay = [&](Carve &c) {
+        lay_side(c, D.row, BN);
+        lay_side(c, D.col, BM);
+        D.S = c.take<double>(std::max<size_t>(L, 1) * BM);
+        D.R = c.take<double>(std::max<size_t>(L, 1) * BN);
+        D.a_cum = c.take<double>((L + 1) * BN);
+        D.c_cum = c.take<double>((L + 1) * BM);
+        D.P0 = c.take<float>(pairs);
+        D.P = c.take<float>(pairs);
+    };
+    {
+        Carve size;
+        lay(size);
+        Carve c{plan->keep.get<uint8_t>(size.off)};
+        if (plan->keep.failed)
+            return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (dense plan)");
+        lay(c);
+    }
+    Arena tmp;
+    tmp.stream = s;
+    D.part = tmp.get<double>((size_t)D.chunks * BM);
+    if (tmp.failed)
+        return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (dense scratch)");
+    launch_dense_forward(D, log_ratio(M, prm.p_min), log_ratio(N, prm.p_min), s);
+    HIP_TRY(hipGetLastError());
+    D.part = nullptr;
+    tmp.release();
+    if (plan_out) {
+        guard.p = nullptr;
+        *plan_out = plan;
+    }
+    return APML_OK;
+}
+
+apml_status apml_dense_backward(apml_dense_plan *plan, const float *x, const float *y, const float *grad_loss,
+                                float *grad_x, float *grad_y, apml_stream stream)
+{
+    g_last_error.clear();
+    if (!plan || !x || !y || !grad_loss || !grad_x)
+        return fail(APML_ERR_INVALID_ARG, "plan, x, y, grad_loss and grad_x must be non-NULL");
+    hipStream_t s = (hipStream_t)stream;
+    DenseDev D = plan->dv;
+    D.x = x;
+    D.y = y;
+    D.grad_loss = grad_loss;
+    D.grad_x = grad_x;
+    D.grad_y = grad_y;
+    const size_t BM = (size_t)plan->B * plan->M, pairs = (size_t)plan->B * plan->N * plan->M;
+    Arena tmp;
+    tmp.stream = s;
+    D.A = tmp.get<double>(pairs);
+    D.part = tmp.get<double>((size_t)D.chunks * BM * (size_t)plan->d);
+    if (tmp.failed)
+        return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (dense backward)");
+    launch_dense_backward(D, s);
+    HIP_TRY(hipGetLastError());
+    tmp.release();
+    return APML_OK;
+}
+
 apml_status apml_plan_get_info(const apml_plan *plan, apml_plan_info *info)
 {
     if (!plan || !info)

@@ -370,4 +370,39 @@ int count_support_chunks(int64_t max_pairs);
 void launch_count_support(const int32_t *row_ptr, const uint8_t *flags, int B, int N, int chunks,
                           unsigned long long *out, hipStream_t s);
 
+// ---------------------------------------------------------------------------
+// dense APML (the unpruned formulation of Sec. III-A, any dimension d)
+// ---------------------------------------------------------------------------
+
+constexpr int kDenseMaxD = 16; // largest point dimension of the dense path
+
+// Per-owner vectors of one direction (rows: [B*N], columns: [B*M]).
+struct DenseSide {
+    int32_t *k1, *k2;          // indices of the minimum and the second minimum
+    double *c1, *g, *T, *Z;    // minimum cost, clamped gap, temperature (Eq. 1), softmax normaliser (Eq. 2)
+    uint8_t *clamped;          // gap clamped: no temperature gradient
+    double *sigma, *gbar, *e;  // backward: softmax adjoint sum, gap adjoint, scratch
+};
+
+struct DenseDev {
+    int B, N, M, d, L;
+    double delta, eps_gap, eps_stab, eps_dist;
+    int tgrad_full;              // temperature differentiated (apml_tgrad_mode FULL)
+    const float *x, *y;          // [B, N, d], [B, M, d]
+    DenseSide row, col;
+    float *P0, *P;               // [B][N][M]: initial plan, plan after the Sinkhorn iterations
+    double *S, *R;               // [L][B*M], [L][B*N]: column and row sums of every iteration
+    double *a_cum, *c_cum;       // [L+1][B*N], [L+1][B*M]: cumulative row and column scalings
+    double *part;                // [chunks][B*M] (x d for the gradient): partial sums of the column passes
+    int chunks, chunk;           // row chunks of the column passes and their length
+    float *loss;                 // [B]
+    double *A;                   // [B][N][M]: plan adjoint (backward)
+    const float *grad_loss;
+    float *grad_x, *grad_y;
+};
+
+void dense_chunks(int B, int N, int M, int *chunks, int *chunk);
+void launch_dense_forward(const DenseDev &D, double lk_row, double lk_col, hipStream_t s);
+void launch_dense_backward(const DenseDev &D, hipStream_t s);
+
 } // namespace apml

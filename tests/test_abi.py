@@ -128,3 +128,19 @@ def test_noalloc_validates_before_any_hip_call():
     assert call(N=1) == 1
     assert call(gl=None) == 1  # gradients requested without an upstream gradient
     assert call(B=1792) == 2 and "at most 1791" in lib.apml_last_error().decode()
+
+
+def test_dense_validates_before_any_hip_call():
+    lib = _lib.load()
+    prm = _lib.apml_params_default()
+    plan = ctypes.c_void_p(0x1)
+    call = lambda B=2, N=8, M=8, d=3, loss=FAKE, params=prm: lib.apml_dense_forward(  # noqa: E731
+        FAKE, FAKE, B, N, M, d, ctypes.byref(params), loss, ctypes.byref(plan), None)
+    assert call(loss=None) == 1 and plan.value is None
+    assert call(N=1) == 1
+    assert call(d=0) == 2 and call(d=17) == 2
+    assert call(params=_lib.apml_params_default(gap_mode=1)) == 2
+    assert call(params=_lib.apml_params_default(sym_mode=1)) == 2
+    assert call(params=_lib.apml_params_default(p_min=1.0)) == 1
+    assert lib.apml_dense_backward(None, FAKE, FAKE, FAKE, FAKE, None, None) == 1
+    assert lib.apml_dense_plan_destroy(None) == 0
