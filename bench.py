@@ -25,32 +25,34 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "APML fwd+bwd point-pairs/s (B=32, N=M=2048 fp32); peak HBM MB"
-# MI355X FP32 vector peak, 157.3 TFLOP/s, in 32-bit VALU lane operations: 128
-# lanes per CU per clock (256 CUs, 2.4 GHz; an FMA counts two flops). The
-# library does not use packed FP32, so one instruction stream reaches half of
-# it (64 lanes per CU per clock, measured); v_min co-issues with other VALU
-# work, so a mix such as the statistics scan's goes above that half.
-VALU_PEAK_OPS = 157.3e12 / 2
+# MI355X published peaks: FP32 vector 157.3 TFLOP/s (256 CUs x 2.4 GHz x 128
+# FMA lanes x 2 flops), HBM3E 8 TB/s.
+FP32_PEAK_FLOPS = 157.3e12
 HBM_PEAK = 8.0e12
-# Algorithmic VALU operations per pair and direction of the statistics scan:
-# 3 subtractions, 1 multiply, 2 fused multiply-adds (squared distance) and
-# min + med3 (running minimum and second minimum).
-OPS_PER_PAIR_DIR = 8
+# Algorithmic floating-point work of the dense scans: one evaluation of the
+# squared distance per pair covers both directions' statistics (and, in the
+# support scan, the row's and the column's radius test): 3 subtractions,
+# 3 multiplications, 2 additions = 8 FLOPs per pair. The selects (min, med3,
+# compares) are not floating-point arithmetic and are not counted. The full
+# statistics scan evaluates every pair once per direction, so its own
+# instruction stream issues twice these FLOPs; the VALU issue rate it reaches
+# is measured with counters (VALU instructions per CU and clock), not here.
+FLOPS_PER_PAIR = 8
 
 
 # Algorithmic work of each phase of one step, per launch (the library records
-# one HIP event pair per phase on its stream). Dense phases count VALU
-# operations per point pair; sparse phases count bytes per stored entry of the
+# one HIP event pair per phase on its stream). Dense phases count FLOPs per
+# point pair evaluated; sparse phases count bytes per stored entry of the
 # support (nnz after symmetrization), as the method must move them at least
 # once: emission of the row-major structure 16 B, column-major view 32 B,
 # softmaxes 24 B, Sinkhorn 8 B per entry and half-step forward (+8 B for the
 # loss) and 16 B per entry and half-step in reverse, softmax/temperature
 # adjoint 24 B + distance gradient 8 B.
-# The dense phases count the pairs their scans evaluate (every pair in the
-# full scans; the skipping scans of large samples skip pairs that cannot
-# matter and report how many they evaluated).
-def _ops(per_pair, which):
-    return lambda w, scanned, nnz: per_pair * scanned[which]
+# The dense phases count the pairs their scans evaluate, once per pair (every
+# pair in the full scans; the skipping scans of large samples skip pairs that
+# cannot matter and report how many they evaluated per direction).
+def _flops(which, directions):
+    return lambda w, scanned, nnz: FLOPS_PER_PAIR * scanned[which] / directions
 
 
 def _bytes(per_entry_fn):
@@ -58,10 +60,10 @@ def _bytes(per_entry_fn):
 
 
 PHASE_MODEL = {
-    "stats": ("alu", _ops(OPS_PER_PAIR_DIR, 0), "VALU ops",
+    "stats": ("alu", _flops(0, 2), "FLOP",
               {"full": "k_top2: minimum and second minimum of every row and column",
                "skip": "k_spatial_sort + k_cull_top2: curve order, then the minima over the runs that can matter"}),
-    "support": ("alu", _ops(OPS_PER_PAIR_DIR, 1), "VALU ops",
+    "support": ("alu", _flops(1, 1), "FLOP",
                 {"full": "k_emit: radius test of every pair, counts and staged hits of the candidate support",
                  "skip": "k_cull_emit: radius test over the runs that can matter, counts and staged hits"}),
     "build": ("hbm", _bytes(lambda w: 16), "bytes",
@@ -119,9 +121,10 @@ def parse():
     ap.add_argument("--cpu-repeats", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--memory-sweep", action="store_true",
-                    help="only measure peak library memory and time of one forward+backward at B=1, "
-                         "N=M in 1k..256k (shape-completion generator), one JSON line per size, with the "
-                         "stored pairs of 16 seeded samples per size")
+                    help="only the scaling study: stored pairs of --trials seeded samples per size and peak "
+                         "memory and time of one forward+backward at B=1, N=M in 1k..256k (shape-completion "
+                         "generator), dense path beside it up to 64k; one JSON line per size")
+    ap.add_argument("--trials", type=int, default=500, help="samples per size of the memory sweep")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (5 times), to scale HBM byte counters")
     return ap.parse_args()
@@ -140,72 +143,223 @@ def copy_calibration(mib: int):
     print(json.dumps({"copy_calibration_bytes": n * 4, "launches": 5}), flush=True)
 
 
-def memory_sweep():
-    """Peak device memory held by the library (plan + scratch) and time of one
-    forward+backward at B = 1 as N = M grows; a least-squares line in N + M
-    gives the bytes per point."""
+SWEEP_SIZES = [1024, 2048, 4096, 8192, 16384, 32768, 65536, 131072, 262144]
+SWEEP_CHUNK = 32  # trials per batched forward
+
+
+def _sweep_inputs(job):
+    from workloads import custom
+
+    n, chunk_index, count = job
+    return custom(n * 1000 + chunk_index, count, n, n, reference="primitives", prediction="perm_noise", sigma=0.05)
+
+
+def memory_sweep(trials: int):
+    """Stored pairs and loss-side memory of the sparse path against the cloud
+    size N = M (B = 1 per sample, shape-completion generator, L = 10), with the
+    dense path beside it where its N x M matrices fit.
+
+    Per size: the stored pairs after symmetrization (nnz) of `trials` seeded
+    samples (mean, spread, range), computed in batched forwards of 32 samples;
+    for one sample, the peak device memory of one forward + backward (the
+    library's pool, and PyTorch's caching allocator route) and its time; the
+    same for the dense path up to 65536 points. A least-squares line in N + M
+    gives the sparse path's bytes per point. Inputs are generated first, in a
+    process pool, before the GPU is touched."""
+    import concurrent.futures
+    import multiprocessing
+
     import numpy as np
+
+    jobs = {n: [(n, c, min(SWEEP_CHUNK, trials - c * SWEEP_CHUNK)) for c in range((trials + SWEEP_CHUNK - 1) // SWEEP_CHUNK)]
+            for n in SWEEP_SIZES}
+    inputs = {}
+    ctx = multiprocessing.get_context("spawn")
+    with concurrent.futures.ProcessPoolExecutor(max_workers=min(16, os.cpu_count() or 1), mp_context=ctx) as ex:
+        for n in SWEEP_SIZES:
+            t = time.perf_counter()
+            inputs[n] = list(ex.map(_sweep_inputs, jobs[n]))
+            print(json.dumps({"generated": n, "trials": trials, "seconds": time.perf_counter() - t}), flush=True)
+
     import torch
 
     import paper_2512_19743_amd as apml
-    from workloads import custom
 
     apml.load()
-    sizes = [1024, 2048, 4096, 8192, 16384, 32768, 65536, 131072, 262144]
-    trials = 16
+    prm = apml.apml_params_default(n_iter=10)
     pts, peaks = [], []
-    for n in sizes:
-        X, Y = custom(n, 1, n, n, reference="primitives", prediction="perm_noise", sigma=0.05)
-        x = torch.from_numpy(X).cuda()
-        y = torch.from_numpy(Y).cuda()
+    for n in SWEEP_SIZES:
+        X, Y = inputs[n][0]
+        x = torch.from_numpy(np.ascontiguousarray(X[:1])).cuda()
+        y = torch.from_numpy(np.ascontiguousarray(Y[:1])).cuda()
         gl = torch.ones(1, device="cuda")
-        prm = apml.apml_params_default(n_iter=10)
 
         def step():
             loss, plan = apml.apml_forward(x, y, prm)
             apml.apml_backward(plan, x, y, gl)
-            nnz = int(plan.nnz().sum())
             plan.close()
-            return nnz
 
-        step()
-        torch.cuda.synchronize()
-        apml.apml_release_cached_memory()
-        step()  # warm again with blocks sized for this N only
-        torch.cuda.synchronize()
-        apml.apml_reset_peak_memory()
-        times = []
-        for _ in range(3):
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record()
-            loss, plan = apml.apml_forward(x, y, prm)
-            apml.apml_backward(plan, x, y, gl)
-            e1.record()
+        def timed(fn, reps):
+            fn()
             torch.cuda.synchronize()
-            nnz = int(plan.nnz().sum())
-            plan.close()
-            times.append(e0.elapsed_time(e1))
-        peak = apml.apml_get_memory_stats()["peak_in_use"]
+            out = []
+            for _ in range(reps):
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+                fn()
+                e1.record()
+                torch.cuda.synchronize()
+                out.append(e0.elapsed_time(e1))
+            return statistics.median(out)
+
+        def pool_peak(fn):
+            torch.cuda.synchronize()
+            apml.apml_release_cached_memory()
+            fn()  # blocks sized for this N only
+            torch.cuda.synchronize()
+            base = apml.apml_get_memory_stats()["in_use"]
+            apml.apml_reset_peak_memory()
+            fn()
+            torch.cuda.synchronize()
+            peak = apml.apml_get_memory_stats()["peak_in_use"] - base
+            apml.apml_release_cached_memory()
+            return peak
+
+        peak = pool_peak(step)
+        ms = timed(step, 3)
+        peak_torch = torch_peak_bytes(step)
         pts.append(2 * n)
         peaks.append(peak)
-        # stored pairs over several seeded samples of the same size (one batched forward)
-        Xt, Yt = custom(n, trials, n, n, reference="primitives", prediction="perm_noise", sigma=0.05)
-        _, plan = apml.apml_forward(torch.from_numpy(Xt).cuda(), torch.from_numpy(Yt).cuda(), prm)
-        per = plan.nnz().astype(np.float64)
-        plan.close()
+        # stored pairs of every trial, in batched forwards
+        nnz = []
+        for Xc, Yc in inputs[n]:
+            _, plan = apml.apml_forward(torch.from_numpy(Xc).cuda(), torch.from_numpy(Yc).cuda(), prm)
+            nnz.extend(plan.nnz().tolist())
+            plan.close()
         torch.cuda.synchronize()
-        apml.apml_release_cached_memory()  # the batch's blocks would inflate the next size's peak
-        # one dense fp32 N x M matrix, the least a dense formulation holds
-        print(json.dumps({"N": n, "M": n, "B": 1, "nnz": nnz, "peak_library_mb": peak / 1e6,
-                          "bytes_per_point": peak / (2 * n), "dense_matrix_mb": 4.0 * n * n / 1e6,
-                          "ms_fwd_bwd": statistics.median(times), "trials": trials,
-                          "nnz_mean": float(per.mean()), "nnz_std": float(per.std(ddof=1)),
-                          "nnz_min": int(per.min()), "nnz_max": int(per.max())}), flush=True)
-        del x, y, Xt, Yt
+        apml.apml_release_cached_memory()
+        per = np.asarray(nnz, dtype=np.float64)
+        rec = {"N": n, "M": n, "B": 1, "trials": len(nnz), "nnz_mean": float(per.mean()),
+               "nnz_std": float(per.std(ddof=1)), "nnz_min": int(per.min()), "nnz_max": int(per.max()),
+               "nnz_per_point": float(per.mean() / (2 * n)),
+               "peak_library_mb": peak / 1e6, "bytes_per_point": peak / (2 * n),
+               "peak_torch_mb": peak_torch / 1e6, "ms_fwd_bwd": ms,
+               "dense_model_mb": 16.0 * n * n / 1e6}
+        # the dense path (P0 and the plan in float32, the adjoint in float64:
+        # 16 bytes per pair) where it fits comfortably
+        if 16.0 * n * n < 100e9:
+            def dstep():
+                loss, plan = apml.apml_dense_forward(x, y, prm)
+                apml.apml_dense_backward(plan, x, y, gl)
+                plan.close()
+
+            dpeak = pool_peak(dstep)
+            dms = timed(dstep, 1 if n >= 32768 else 3)
+            apml.apml_release_cached_memory()
+            rec.update({"dense_peak_mb": dpeak / 1e6, "dense_ms_fwd_bwd": dms,
+                        "memory_ratio_dense_over_sparse": dpeak / peak, "time_ratio_dense_over_sparse": dms / ms})
+        print(json.dumps(rec), flush=True)
+        del x, y
+        inputs[n] = None
     A = np.vstack([np.asarray(pts, float), np.ones(len(pts))]).T
     slope, icpt = np.linalg.lstsq(A, np.asarray(peaks, float), rcond=None)[0]
     print(json.dumps({"fit": "peak_bytes = a * (N + M) + b", "a_bytes_per_point": slope, "b_bytes": icpt}), flush=True)
+
+
+def torch_peak_bytes(step) -> int:
+    """Peak device memory of one step with the library's allocations routed to
+    PyTorch's caching allocator: max_memory_allocated after a reset, minus what
+    was allocated before (inputs and outputs of the caller included only as far
+    as the step allocates them)."""
+    import gc
+
+    import torch
+
+    import paper_2512_19743_amd as apml
+
+    gc.collect()
+    torch.cuda.synchronize()
+    apml.apml_set_allocator_torch()
+    try:
+        step()  # warm the caching allocator's blocks
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats()
+        before = torch.cuda.memory_allocated()
+        step()
+        torch.cuda.synchronize()
+        return torch.cuda.max_memory_allocated() - before
+    finally:
+        gc.collect()
+        torch.cuda.synchronize()
+        apml.apml_set_allocator_default()
+
+
+def dense_baseline(x, y, gl, w, sparse_ms, sparse_peak, steps):
+    """Dense APML (every pair materialised, Sec. III-A) forward + backward on
+    the same batch: median time of a few steps and peak memory (PyTorch's
+    caching allocator route), next to the sparse path's."""
+    import torch
+
+    import paper_2512_19743_amd as apml
+
+    prm = apml.apml_params_default(n_iter=w.n_iter)
+
+    def dstep():
+        loss, plan = apml.apml_dense_forward(x, y, prm)
+        apml.apml_dense_backward(plan, x, y, gl)
+        plan.close()
+
+    dstep()
+    torch.cuda.synchronize()
+    n = max(3, min(steps, 10))
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(n):
+        dstep()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / n
+    peak = torch_peak_bytes(dstep)
+    return {"ms_per_step": ms, "peak_hbm_mb": peak / 1e6, "steps": n,
+            "time_ratio_dense_over_sparse": ms / sparse_ms, "memory_ratio_dense_over_sparse": peak / sparse_peak,
+            "what": "apml_dense_forward + apml_dense_backward: P0, the plan and its adjoint as N x M matrices"}
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def dense_oracle_tiny() -> dict:
+    """The dense float64 PyTorch formulation (oracle/dense.py) with autograd on
+    the tiny workload (2 clouds of 256 points), forward + backward."""
+    import torch
+
+    from oracle.dense import dense_apml
+    from workloads import batch, config
+
+    w = config(1)
+    X, Y = batch(w)
+    times = []
+    for _ in range(3):
+        t = time.perf_counter()
+        for b in range(w.B):
+            xb = torch.from_numpy(X[b].astype("float64")).requires_grad_(True)
+            yb = torch.from_numpy(Y[b].astype("float64")).requires_grad_(True)
+            loss, _ = dense_apml(xb, yb, n_iter=w.n_iter)
+            loss.backward()
+        times.append(time.perf_counter() - t)
+    tc = statistics.median(times)
+    return {"value": w.pairs / tc, "unit": "point-pairs/s", "threads": torch.get_num_threads(),
+            "sample": f"tiny workload (B=2, N=M=256), forward + backward with autograd; median of 3, {tc:.3f} s"}
 
 
 def main():
@@ -221,7 +375,7 @@ def main():
         copy_calibration(args.copy_calibration)
         return
     if args.memory_sweep:
-        memory_sweep()
+        memory_sweep(args.trials)
         return
 
     import numpy as np
@@ -273,6 +427,11 @@ def main():
     ms = e0.elapsed_time(e1) / args.steps
     mem = apml.apml_get_memory_stats()
 
+    # peak loss-side memory through PyTorch's caching allocator: the library
+    # routed to it, peak statistics reset, one step, max_memory_allocated
+    # above what was allocated before
+    peak_torch = torch_peak_bytes(step)
+
     # per-phase split: the same K steps again with HIP events recorded by the
     # library on its stream around each phase
     apml.apml_profile_reset()
@@ -297,16 +456,16 @@ def main():
         avg = tot_ms / n
         work = per(w, scanned, nnz_total)
         achieved = work / (avg * 1e-3)
-        peak = VALU_PEAK_OPS if bound == "alu" else HBM_PEAK
+        peak = FP32_PEAK_FLOPS if bound == "alu" else HBM_PEAK
         kernels[name] = {"kernel": what, "bound": bound, "avg_launch_ms": avg, "launches_per_step": n / args.steps,
                          "work_per_launch": work, "work_unit": unit_kind,
                          "achieved": achieved / (1e12 if bound == "alu" else 1e9),
-                         "unit": "TOP/s" if bound == "alu" else "GB/s", "frac": achieved / peak,
+                         "unit": "TFLOP/s" if bound == "alu" else "GB/s", "frac": achieved / peak,
                          "traffic": traffic_for(name, None)}
     dom = max(kernels, key=lambda k: kernels[k]["avg_launch_ms"] * kernels[k]["launches_per_step"])
     d = kernels[dom]
     roofline = {"bound": d["bound"], "achieved": d["achieved"],
-                "peak": VALU_PEAK_OPS / 1e12 if d["bound"] == "alu" else HBM_PEAK / 1e9,
+                "peak": FP32_PEAK_FLOPS / 1e12 if d["bound"] == "alu" else HBM_PEAK / 1e9,
                 "unit": d["unit"], "frac": d["frac"], "traffic": traffic_for(dom, d),
                 "kernel": d["kernel"], "phase": dom, "avg_launch_ms": d["avg_launch_ms"],
                 "work_per_launch": d["work_per_launch"], "work_unit": d["work_unit"]}
@@ -329,7 +488,8 @@ def main():
                    "B": w.B, "N": w.N, "M": w.M, "n_iter": w.n_iter, "tau": 1e-8, "p_min": 0.8,
                    "dense_scan": scan_mode},
         "roofline": roofline,
-        "peak_hbm_mb": mem["peak_in_use"] / 1e6,
+        "peak_hbm_mb": peak_torch / 1e6,
+        "peak_hbm_mb_pool": mem["peak_in_use"] / 1e6,
         "support": {"nnz_total": nnz_total, "nnz_per_row": nnz_total / (w.B * w.N),
                     "stored_pairs": int(stored),
                     "scanned_fraction_min": scanned[0] / (2 * w.B * w.N * w.M),
@@ -338,6 +498,9 @@ def main():
         "kernels": kernels,
         "wall_ms_per_step": wall * 1e3 / args.steps,
     }
+
+    # the dense formulation (Sec. III-A) on the same batch: time and peak memory
+    line["dense_baseline"] = dense_baseline(x, y, gl, w, ms, peak_torch, args.steps)
 
     if args.cpu_baseline == "on":
         import oracle
@@ -359,7 +522,9 @@ def main():
         tc = statistics.median(times)
         line["cpu_baseline"] = {"value": len(idx) * w.N * w.M / tc, "unit": "point-pairs/s",
                                 "cores": oracle.max_threads(), "kind": "oracle",
-                                "sample": f"{sample}; median of {len(times)} runs, {tc:.2f} s each"}
+                                "sample": f"{sample}; median of {len(times)} runs, {tc:.2f} s each",
+                                "cpu_model": cpu_model(), "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
+                                "dense_float64_oracle_tiny": dense_oracle_tiny()}
     print(json.dumps(line), flush=True)
 
 

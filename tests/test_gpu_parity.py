@@ -303,3 +303,40 @@ def test_large_scene_sampled_owners_and_invariants():
             sel = (ex["j"] == c) & ((ex["flags"] & 2) > 0)
             np.testing.assert_array_equal(ex["i"][sel], idx)
             np.testing.assert_allclose(ex["p_col"][sel], p, rtol=2e-6)
+
+
+def test_largest_sweep_size_sampled_owners():
+    # the memory sweep's largest clouds (N = M = 262144, shape-completion
+    # generator): sampled rows' and columns' minima, temperatures and kept
+    # supports against the oracle, owner by owner
+    n = 262144
+    X, Y = custom(7, 1, n, n, reference="primitives", prediction="perm_noise", sigma=0.05)
+    note(f"sweep size {n}")
+    g = run_gpu(X, Y, n_iter=10)
+    plan = g["plan"]
+    ex = plan.export(0)
+    st = plan.export_stats(0)
+    prm = oracle_params(n_iter=10)
+    rng = np.random.default_rng(262144)
+    assert np.isfinite(g["loss"][0]) and np.isfinite(g["gx"]).all()
+    assert ex["p0"].astype(np.float64).sum() == pytest.approx(n, rel=1e-5)  # (N + M) / 2
+    rows = rng.choice(n, 64, replace=False)
+    ref = oracle.owner_stats(X[0], Y[0], rows, prm)
+    np.testing.assert_array_equal(st["j1"][rows], ref["k1"])
+    np.testing.assert_array_equal(st["j2"][rows], ref["k2"])
+    np.testing.assert_allclose(st["T_row"][rows], ref["T"], rtol=1e-12)
+    cols = rng.choice(n, 64, replace=False)
+    refc = oracle.owner_stats(Y[0], X[0], cols, prm)
+    np.testing.assert_array_equal(st["i1"][cols], refc["k1"])
+    np.testing.assert_array_equal(st["i2"][cols], refc["k2"])
+    np.testing.assert_allclose(st["T_col"][cols], refc["T"], rtol=1e-12)
+    for r in rows[:16]:
+        idx, s, p = oracle.owner_support(X[0], Y[0], int(r), prm)
+        sel = (ex["i"] == r) & ((ex["flags"] & 1) > 0)
+        np.testing.assert_array_equal(ex["j"][sel], idx)
+        np.testing.assert_allclose(ex["p_row"][sel], p, rtol=2e-6)
+    for c in cols[:16]:
+        idx, s, p = oracle.owner_support(Y[0], X[0], int(c), prm)
+        sel = (ex["j"] == c) & ((ex["flags"] & 2) > 0)
+        np.testing.assert_array_equal(ex["i"][sel], idx)
+        np.testing.assert_allclose(ex["p_col"][sel], p, rtol=2e-6)
