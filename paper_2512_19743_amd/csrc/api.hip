@@ -343,6 +343,7 @@ struct apml_plan {
     int64_t max_sample = 0; // stored pairs of the largest sample
     bool sink_fwd = false;  // per-sample Sinkhorn kernels take this plan (forward)
     bool sink_bwd = false;  // and the reverse sweeps
+    bool sink_wide = false; // streamed per-sample Sinkhorn kernels (larger samples)
     bool timed = true;  // phases recorded by the profiler (off for the no-alloc entry point)
     Arena keep;         // everything backward and export need
     DevPlan dv{};       // device arrays (x, y and the backward fields are set per call)
@@ -815,6 +816,8 @@ apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t
     const int slots = sinkhorn_slots(N, M, pieces, B);
     plan->sink_fwd = slots > 0;
     plan->sink_bwd = sinkhorn_bwd_fits(slots, plan->max_sample);
+    const int wslots = plan->sink_fwd ? 0 : sinkhorn_slots_wide(N, M, pieces, B);
+    plan->sink_wide = wslots > 0;
 
     // ---- sparse structure -------------------------------------------------
     // (with the per-sample Sinkhorn pieces, in one allocation)
@@ -841,6 +844,16 @@ apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t
                 pk->n_pos = c.take<int32_t>(B);
             }
         }
+        if (plan->sink_wide) {
+            const size_t w = packed_order_words(B, wslots);
+            for (WideOrder *wk : {&dv.wk_row, &dv.wk_col}) {
+                wk->slots = wslots;
+                wk->p0 = c.take<float>(w);
+                wk->gi = c.take<uint32_t>(w / 2);
+                wk->info = c.take<uint32_t>(w / kSinkPiece);
+                wk->n_pos = c.take<int32_t>(B);
+            }
+        }
     };
     {
         Carve size;
@@ -865,6 +878,7 @@ apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t
     // skipping scans) their placement runs in the compaction's (ranking's)
     // launch
     int32_t *place = plan->sink_fwd ? tmp.get<int32_t>((size_t)B * 2 * kSinkOwners) : nullptr;
+    int32_t *wplace = plan->sink_wide ? tmp.get<int32_t>((size_t)B * 2 * kSinkOwnersW) : nullptr;
     const bool pieces_placed = place && (skip || (ea.stage && !placed));
     if (tmp.failed || keep.failed || dense_tmp.failed)
         return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (sparse arrays)");
@@ -956,6 +970,9 @@ apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t
         if (plan->sink_fwd) {
             dv.sink_place = nullptr; // scratch of this call
             HIP_TRY(launch_sinkhorn_fwd(dv, prm.eps_stab, s));
+        } else if (plan->sink_wide) {
+            launch_wide_pack(dv, wplace, s);
+            HIP_TRY(launch_sinkhorn_fwd_wide(dv, prm.eps_stab, s));
         } else {
             launch_sinkhorn_fwd_steps(dv, prm.eps_stab, s);
             HIP_TRY(hipGetLastError());
@@ -1028,7 +1045,12 @@ apml_status run_backward(apml_plan *plan, const float *x, const float *y, const 
     // cost adjoint reuses the column-order copy, dead once the sweeps end.
     auto lay = [&](Carve &c) {
         dv.adj = c.take<double>(plan->stored);
-        if (dv.L > 0 && !plan->sink_bwd) {
+        if (dv.L > 0 && plan->sink_wide) {
+            const size_t w = packed_order_words(plan->B, dv.wk_row.slots);
+            dv.wr = c.take<float>(w);
+            dv.wc = c.take<float>(w);
+            dv.cbar = c.take<double>(plan->stored);
+        } else if (dv.L > 0 && !plan->sink_bwd) {
             dv.rz = dv.adj;
             dv.kz = c.take<double>(plan->stored);
             dv.cbar = dv.kz;
@@ -1052,6 +1074,8 @@ apml_status run_backward(apml_plan *plan, const float *x, const float *y, const 
         if (dv.L > 0) {
             if (plan->sink_bwd) {
                 HIP_TRY(launch_sinkhorn_bwd(dv, plan->max_sample, s));
+            } else if (plan->sink_wide) {
+                HIP_TRY(launch_sinkhorn_bwd_wide(dv, s));
             } else {
                 launch_sinkhorn_bwd_steps(dv, s);
                 HIP_TRY(hipGetLastError());

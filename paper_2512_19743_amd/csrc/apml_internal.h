@@ -263,6 +263,20 @@ struct PackedOrder {
     int slots;      // positions per lane of this layout
 };
 
+// Pieces of the per-sample Sinkhorn kernels for larger samples (up to
+// kSinkOwnersW points per side): the same plane-major layout, with more slots
+// (1..kSinkMaxSlotsW), streamed from memory in every sweep instead of held in
+// registers. info: owner | log2(group) << 13 | head << 16 | valid << 17.
+constexpr int kSinkOwnersW = 8192;
+constexpr int kSinkMaxSlotsW = 32;
+struct WideOrder {
+    float *p0;      // [B][slots][kSinkPiece][lanes]
+    uint32_t *gi;   // [B][slots][kSinkPiece/2][lanes]: byte offsets of the gathered 8-byte values, two per word
+    uint32_t *info; // [B][slots][lanes]
+    int32_t *n_pos; // [B]: positions used
+    int slots;
+};
+
 // Device view of a plan, passed by value to the sparse kernels.
 struct DevPlan {
     int B, N, M, L;
@@ -294,6 +308,8 @@ struct DevPlan {
     double *rz, *kz;              // [nnz] reverse-sweep adjoints in row and in column order (per-iteration
                                   // kernels; rz shares adj's memory and cbar kz's)
     PackedOrder pk_row, pk_col;   // per-sample Sinkhorn pieces (when that path is taken)
+    WideOrder wk_row, wk_col;     // streamed per-sample pieces (larger samples)
+    float *wr, *wc;               // backward of the streamed path: the plan adjoint in row and in column pieces
     const int32_t *sink_place;    // during the forward softmax of that path: the pieces' placement, so that the
                                   // column softmax writes every pair into its pieces; else NULL
 };
@@ -351,6 +367,14 @@ void launch_offsets(const int32_t *cnt, int S, const int32_t *col_cnt, const Cou
 // Positions per lane the per-sample kernels need for a batch (1..kSinkMaxSlots),
 // 0 when it does not fit them.
 int sinkhorn_slots(int N, int M, const int32_t *counts, int B);
+// Slots of the streamed per-sample path for a batch (1..kSinkMaxSlotsW), 0
+// when it does not take it.
+int sinkhorn_slots_wide(int N, int M, const int32_t *counts, int B);
+// Places the streamed pieces (place: [B][2][kSinkOwnersW] int32 scratch)
+// and writes every pair into them (after the softmax).
+void launch_wide_pack(const DevPlan &d, int32_t *place, hipStream_t s);
+hipError_t launch_sinkhorn_fwd_wide(const DevPlan &d, double eps, hipStream_t s);
+hipError_t launch_sinkhorn_bwd_wide(const DevPlan &d, hipStream_t s);
 bool sinkhorn_bwd_fits(int slots, int64_t max_pairs);
 size_t packed_order_words(int B, int slots); // 32-bit words of one PackedOrder's p0 array
 // Lays out the pieces of both orders; place: [B][2][2048] int32 scratch.

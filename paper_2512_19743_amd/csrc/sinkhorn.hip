@@ -290,6 +290,42 @@ __device__ __forceinline__ void apply_scaling(double acc, uint32_t info, double 
     }
 }
 
+// loss = sum_t v_t C_t (Sec. III-D) of sample b, with v = alpha P0 beta from
+// the final scalings va, vb in LDS, over the sample's pairs [lo, hi) in
+// row-major order, four pairs per lane in flight; part: kT / 64 doubles of LDS.
+__device__ void sample_loss(const DevPlan &d, int b, int lo, int hi, const double *va, const double *vb, double *part)
+{
+    const int tid = threadIdx.x, N = d.N;
+    double acc = 0.0;
+    for (int t0 = lo + tid; t0 < hi; t0 += 4 * kT) {
+        int r[4], c[4];
+        float p[4];
+        double C[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int t = t0 + u * kT < hi ? t0 + u * kT : lo;
+            r[u] = d.csr_row[t] - b * N;
+            c[u] = d.csr_col[t];
+            p[u] = d.p0r[t];
+            C[u] = d.cost[t];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (t0 + u * kT < hi)
+                acc += va[r[u]] * (double)p[u] * vb[c[u]] * C[u];
+    }
+    acc = wave_sum(acc);
+    if (lane_id() == 0)
+        part[tid >> 6] = acc;
+    lds_barrier();
+    if (tid == 0) {
+        double s = 0.0;
+        for (int w = 0; w < kT / 64; ++w)
+            s += part[w];
+        d.loss[b] = (float)s;
+    }
+}
+
 template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan d, double eps)
 {
     // static arrays: their addresses are constants folded into the LDS instructions
@@ -341,36 +377,7 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd(DevPlan 
         lds_barrier();
     }
 
-    // loss = sum_t v_t C_t (Sec. III-D), over the sample's pairs in row-major
-    // order, four pairs per lane in flight
-    double acc = 0.0;
-    for (int t0 = lo + tid; t0 < hi; t0 += 4 * kT) {
-        int r[4], c[4];
-        float p[4];
-        double C[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int t = t0 + u * kT < hi ? t0 + u * kT : lo;
-            r[u] = d.csr_row[t] - b * N;
-            c[u] = d.csr_col[t];
-            p[u] = d.p0r[t];
-            C[u] = d.cost[t];
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-            if (t0 + u * kT < hi)
-                acc += va[r[u]] * (double)p[u] * vb[c[u]] * C[u];
-    }
-    acc = wave_sum(acc);
-    if (lane_id() == 0)
-        part[tid >> 6] = acc;
-    lds_barrier();
-    if (tid == 0) {
-        double s = 0.0;
-        for (int w = 0; w < kT / 64; ++w)
-            s += part[w];
-        d.loss[b] = (float)s;
-    }
+    sample_loss(d, b, lo, hi, va, vb, part);
 }
 
 // Reverse sweeps, last iteration first. The plan adjoint starts as
@@ -559,6 +566,353 @@ template <int SLP> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd(DevPlan 
                     d.adj[lo + run + e] = (double)adj[adj_slot(s * kT + tid, e)] * (double)w.x - (double)w.y;
                 }
         }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// streamed per-sample kernels (samples of up to kSinkOwnersW points per side)
+// ---------------------------------------------------------------------------
+//
+// One 1024-lane workgroup per sample runs all 2L sweeps, as above, but the
+// pieces (too many for registers) are read from memory in every sweep, a slot
+// at a time with the next slot's loads in flight. The forward kernel keeps
+// both scaling vectors in LDS in double precision (2 x 64 KB). The reverse
+// kernel keeps the plan adjoint twice, in the row pieces' and in the column
+// pieces' layout in memory (coalesced, each read and written once per phase
+// by the lane that owns the position), and exchanges two single-precision
+// factors per owner and phase through LDS. With the plan after row step l
+// equal to alpha^l_i P0 beta^l_j, after column step l to alpha^(l-1)_i P0
+// beta^l_j, and 1/(R^l_i + eps) = alpha^l_i / alpha^(l-1)_i, 1/(S^l_j + eps)
+// = beta^l_j / beta^(l-1)_j (r: row copy, c: column copy):
+//   row phase l:    rho = r - Yc_j (the adjoint after the reverse of Eq. 3
+//                   of iteration l+1, times beta^l_j); d_i = alpha^l_i
+//                   sum_j rho P0; r' = (rho - d_i beta^l_j) alpha^l_i /
+//                   alpha^(l-1)_i; publishes Yr_i = d_i alpha^l_i and
+//                   alpha^(l-1)_i
+//   column phase l: kappa = c - Yr_i; e_j = beta^l_j sum_i kappa P0;
+//                   c' = (kappa - e_j alpha^(l-1)_i) beta^l_j / beta^(l-1)_j;
+//                   publishes Yc_j = e_j beta^l_j and beta^(l-1)_j
+// from r = grad_loss C beta^L_j, c = grad_loss C alpha^L_i and Yc = 0; after
+// column phase 1 the adjoint with respect to P0 is r - Yc_j. Copies and
+// published factors are single precision, sums and updates double; pairs
+// without mass keep 0.
+constexpr int kSLW = kSinkOwnersW / kT; // owners per thread in the placement
+
+// Placement of one order of sample b (grid B x 2): as place_order, for up to
+// kSinkOwnersW owners and the wide info word.
+__global__ __launch_bounds__(kT) void k_place_w(DevPlan d, int32_t *place)
+{
+    __shared__ int hist[8], base[8];
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const bool rows = blockIdx.y == 0;
+    const int n_own = rows ? d.N : d.M;
+    const int32_t *ptr = rows ? d.row_ptr + (size_t)b * d.N : d.col_ptr + (size_t)b * d.M;
+    const WideOrder pk = rows ? d.wk_row : d.wk_col;
+    const int slots = pk.slots, cap = slots * kT;
+    {
+        const size_t np0 = (size_t)slots * kP * kT, ngi = np0 / 2;
+        for (size_t k = tid; k < np0; k += kT)
+            pk.p0[(size_t)b * np0 + k] = 0.0f;
+        for (size_t k = tid; k < ngi; k += kT)
+            pk.gi[(size_t)b * ngi + k] = 0u;
+    }
+    if (tid < 8)
+        hist[tid] = 0;
+    __syncthreads();
+    int lg[kSLW], rk[kSLW];
+#pragma unroll
+    for (int s = 0; s < kSLW; ++s) {
+        const int k = kSLW * tid + s;
+        lg[s] = -1;
+        if (k < n_own) {
+            lg[s] = sink_log2_group(sink_pieces(ptr[k + 1] - ptr[k]));
+            rk[s] = atomicAdd(&hist[lg[s]], 1);
+        }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int run = 0;
+        for (int c = 6; c >= 0; --c) { // largest groups first: every group is aligned to its size
+            base[c] = run;
+            run += hist[c] << c;
+        }
+        base[7] = run;
+        pk.n_pos[b] = run;
+    }
+    __syncthreads();
+    for (int p = base[7] + tid; p < cap; p += kT) // unused positions: invalid
+        pk.info[pk_index(b, p, 0, 1, slots)] = 0u;
+#pragma unroll
+    for (int s = 0; s < kSLW; ++s) {
+        if (lg[s] < 0)
+            continue;
+        const int k = kSLW * tid + s, first = base[lg[s]] + (rk[s] << lg[s]);
+        place[((size_t)b * 2 + (rows ? 0 : 1)) * kSinkOwnersW + k] = first;
+        for (int q = 0; q < (1 << lg[s]); ++q)
+            pk.info[pk_index(b, first + q, 0, 1, slots)] =
+                (uint32_t)k | ((uint32_t)lg[s] << 13) | ((q == 0 ? 1u : 0u) << 16) | (1u << 17);
+    }
+}
+
+// Writes every stored pair into its streamed piece, one thread per pair and order.
+__global__ __launch_bounds__(kBlock) void k_pack_w(DevPlan d, const int32_t *place)
+{
+    const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const bool rows = g < d.nnz;
+    const int64_t t = rows ? g : g - d.nnz;
+    if (t >= d.nnz)
+        return;
+    int b, owner, off, other;
+    float p0;
+    if (rows) {
+        const int r = d.csr_row[t];
+        b = r / d.N;
+        owner = r - b * d.N;
+        off = (int)(t - d.row_ptr[r]);
+        other = d.csr_col[t];
+        p0 = d.p0r[t];
+    } else {
+        const int gc = d.csc_col[t];
+        b = gc / d.M;
+        owner = gc - b * d.M;
+        off = (int)(t - d.col_ptr[gc]);
+        other = d.csc_row[t];
+        p0 = d.p0c[t];
+    }
+    const WideOrder &pk = rows ? d.wk_row : d.wk_col;
+    const int p = place[((size_t)b * 2 + (rows ? 0 : 1)) * kSinkOwnersW + owner] + off / kP, e = off % kP;
+    pk.p0[pk_index(b, p, e, kP, pk.slots)] = p0;
+    reinterpret_cast<uint16_t *>(pk.gi + pk_index(b, p, e / 2, kP / 2, pk.slots))[e & 1] = (uint16_t)(other << 3);
+}
+
+// One streamed position of a lane: P0 of its pairs, the byte offsets of the
+// gathered values, the info word.
+struct WSlot {
+    float p0[kP];
+    uint32_t gi[kP / 2];
+    uint32_t info;
+};
+
+__device__ __forceinline__ WSlot load_wslot(const WideOrder &pk, int b, int s)
+{
+    WSlot w;
+    const int p = s * kT + (int)threadIdx.x;
+#pragma unroll
+    for (int e = 0; e < kP; ++e)
+        w.p0[e] = pk.p0[pk_index(b, p, e, kP, pk.slots)];
+#pragma unroll
+    for (int q = 0; q < kP / 2; ++q)
+        w.gi[q] = pk.gi[pk_index(b, p, q, kP / 2, pk.slots)];
+    w.info = pk.info[pk_index(b, p, 0, 1, pk.slots)];
+    return w;
+}
+
+__device__ __forceinline__ double group_reduce_lg(double acc, int lg)
+{
+    const int lgmax = __builtin_amdgcn_readfirstlane(lg);
+    bfly_step<0>(acc, lg, lgmax);
+    bfly_step<1>(acc, lg, lgmax);
+    bfly_step<2>(acc, lg, lgmax);
+    bfly_step<3>(acc, lg, lgmax);
+    bfly_step<4>(acc, lg, lgmax);
+    bfly_step<5>(acc, lg, lgmax);
+    return acc;
+}
+
+// Slots of the calling wave that hold used positions (wave-uniform).
+__device__ __forceinline__ int wave_slots(int n_used)
+{
+    const int wave_base = (int)(threadIdx.x & ~63u);
+    return wave_base < n_used ? (n_used - wave_base + kT - 1) / kT : 0;
+}
+
+// Slots whose loads are issued together before any of them is used: the
+// streamed words come from the last-level cache, whose latency a single slot
+// of work does not cover.
+constexpr int kWBatch = 4;
+
+// One forward sweep: every owner's sum of P0 times the other side's scaling
+// (vals) over its pieces, then its own scaling v = cur / (cur sum + eps)
+// (Eq. 3 or Eq. 4) into own (LDS) and g_val (the saved scalings).
+__device__ void wide_sweep(const WideOrder &pk, int b, int n_used, const double *vals, double *own, double eps,
+                           double *g_val)
+{
+    const int ns = wave_slots(n_used);
+    for (int s0 = 0; s0 < ns; s0 += kWBatch) {
+        WSlot w[kWBatch];
+#pragma unroll
+        for (int k = 0; k < kWBatch; ++k)
+            if (s0 + k < ns)
+                w[k] = load_wslot(pk, b, s0 + k);
+#pragma unroll
+        for (int k = 0; k < kWBatch; ++k) {
+            if (s0 + k >= ns)
+                break;
+            const Unpack u = Unpack::make();
+            double g[kP];
+#pragma unroll
+            for (int e = 0; e < kP; ++e)
+                g[e] = lds_at<double>(vals, u.half(w[k].gi[e / 2], e));
+            double acc = (double)w[k].p0[0] * g[0];
+#pragma unroll
+            for (int e = 1; e < kP; ++e)
+                acc = __builtin_fma((double)w[k].p0[e], g[e], acc);
+            acc = group_reduce_lg(acc, (int)u.bits(w[k].info, 13, 3));
+            if (u.bits(w[k].info, 16, 2) == 3u) { // head and valid
+                const int o = (int)u.bits(w[k].info, 0, 13);
+                const double c = own[o];
+                const double v = quotient(c, c * acc + eps);
+                own[o] = v;
+                g_val[o] = v;
+            }
+        }
+    }
+}
+
+__global__ __launch_bounds__(kT) void k_sinkhorn_fwd_w(DevPlan d, double eps)
+{
+    __shared__ double va[kSinkOwnersW], vb[kSinkOwnersW], part[kT / 64];
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const int N = d.N, M = d.M, L = d.L;
+    const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
+    const int lo = d.row_ptr[(size_t)b * N], hi = d.row_ptr[(size_t)(b + 1) * N];
+    const int n_row = __builtin_amdgcn_readfirstlane(d.wk_row.n_pos[b]);
+    const int n_col = __builtin_amdgcn_readfirstlane(d.wk_col.n_pos[b]);
+    for (int k = tid; k < N; k += kT) {
+        va[k] = 1.0;
+        d.alpha[(size_t)b * N + k] = 1.0;
+    }
+    for (int k = tid; k < M; k += kT) {
+        vb[k] = 1.0;
+        d.beta[(size_t)b * M + k] = 1.0;
+    }
+    lds_barrier();
+    for (int l = 1; l <= L; ++l) {
+        // column scaling (Eq. 3), then row scaling (Eq. 4)
+        wide_sweep(d.wk_col, b, n_col, va, vb, eps, d.beta + l * BM + (size_t)b * M);
+        lds_barrier();
+        wide_sweep(d.wk_row, b, n_row, vb, va, eps, d.alpha + l * BN + (size_t)b * N);
+        lds_barrier();
+    }
+    sample_loss(d, b, lo, hi, va, vb, part);
+}
+
+// One reverse phase over the pieces of one order: copy (this order's adjoint
+// copy) is brought up to date with the other direction's pending step
+// (factors fin, gathered), the owners' sums formed, this direction's step
+// applied, and the owners' factors published in fout (see above). own:
+// the saved scalings of this direction at iteration l (own_l) and l - 1.
+__device__ void wide_reverse(const WideOrder &pk, int b, int n_used, float *copy, const float2 *fin, float2 *fout,
+                             const double *own_l, const double *own_prev)
+{
+    const int ns = wave_slots(n_used);
+    for (int s0 = 0; s0 < ns; s0 += kWBatch) {
+        WSlot w[kWBatch];
+        float cv[kWBatch][kP];
+        double al[kWBatch], alp[kWBatch];
+#pragma unroll
+        for (int k = 0; k < kWBatch; ++k)
+            if (s0 + k < ns) {
+                w[k] = load_wslot(pk, b, s0 + k);
+                const int p = (s0 + k) * kT + (int)threadIdx.x;
+#pragma unroll
+                for (int e = 0; e < kP; ++e)
+                    cv[k][e] = copy[pk_index(b, p, e, kP, pk.slots)];
+            }
+#pragma unroll
+        for (int k = 0; k < kWBatch; ++k)
+            if (s0 + k < ns) {
+                const int o = (int)(w[k].info & 0x1FFFu);
+                al[k] = own_l[o];
+                alp[k] = own_prev[o];
+            }
+#pragma unroll
+        for (int k = 0; k < kWBatch; ++k) {
+            if (s0 + k >= ns)
+                break;
+            const Unpack u = Unpack::make();
+            const int o = (int)u.bits(w[k].info, 0, 13);
+            const int p = (s0 + k) * kT + (int)threadIdx.x;
+            float2 f[kP];
+#pragma unroll
+            for (int e = 0; e < kP; ++e)
+                f[e] = lds_at<float2>(fin, u.half(w[k].gi[e / 2], e));
+            double rho[kP], acc = 0.0;
+#pragma unroll
+            for (int e = 0; e < kP; ++e) {
+                rho[e] = (double)cv[k][e] - (double)f[e].x;
+                const double p0 = (double)w[k].p0[e];
+                acc = e == 0 ? rho[e] * p0 : __builtin_fma(rho[e], p0, acc);
+            }
+            const double dsum = al[k] * group_reduce_lg(acc, (int)u.bits(w[k].info, 13, 3));
+            const double q = quotient(al[k], alp[k]);
+#pragma unroll
+            for (int e = 0; e < kP; ++e)
+                copy[pk_index(b, p, e, kP, pk.slots)] =
+                    w[k].p0[e] != 0.0f ? (float)((rho[e] - dsum * (double)f[e].y) * q) : 0.0f;
+            if (u.bits(w[k].info, 16, 2) == 3u) // head and valid
+                fout[o] = make_float2((float)(dsum * al[k]), (float)alp[k]);
+        }
+    }
+}
+
+__global__ __launch_bounds__(kT) void k_sinkhorn_bwd_w(DevPlan d)
+{
+    __shared__ float2 fr[kSinkOwnersW]; // row factors (Yr_i, alpha^(l-1)_i)
+    __shared__ float2 fc[kSinkOwnersW]; // column factors (Yc_j, beta^(l-1)_j)
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const int N = d.N, M = d.M, L = d.L;
+    const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
+    const float *xb = d.x + (size_t)b * N * 3, *yb = d.y + (size_t)b * M * 3;
+    const double *alpha = d.alpha + (size_t)b * N, *beta = d.beta + (size_t)b * M; // + l * BN, + l * BM
+    const double gl = d.grad_loss[b];
+    const int n_row = __builtin_amdgcn_readfirstlane(d.wk_row.n_pos[b]);
+    const int n_col = __builtin_amdgcn_readfirstlane(d.wk_col.n_pos[b]);
+    // the copies start as grad_loss C beta^L_j (rows) and grad_loss C alpha^L_i (columns)
+    for (int order = 0; order < 2; ++order) {
+        const WideOrder &pk = order == 0 ? d.wk_row : d.wk_col;
+        float *copy = order == 0 ? d.wr : d.wc;
+        const int ns = wave_slots(order == 0 ? n_row : n_col);
+        for (int s = 0; s < ns; ++s) {
+            const WSlot w = load_wslot(pk, b, s);
+            const Unpack u = Unpack::make();
+            const int o = (int)u.bits(w.info, 0, 13), p = s * kT + tid;
+#pragma unroll
+            for (int e = 0; e < kP; ++e) {
+                const int k = (int)(u.half(w.gi[e / 2], e) >> 3);
+                const int i = order == 0 ? o : k, j = order == 0 ? k : o;
+                const double sc = order == 0 ? beta[(size_t)L * BM + j] : alpha[(size_t)L * BN + i];
+                copy[pk_index(b, p, e, kP, pk.slots)] =
+                    w.p0[e] != 0.0f ? (float)(gl * dist_f64(xb + 3 * i, yb + 3 * j) * sc) : 0.0f;
+            }
+        }
+    }
+    for (int k = tid; k < M; k += kT) // no pending column update before row phase L
+        fc[k] = make_float2(0.0f, (float)beta[(size_t)L * BM + k]);
+    lds_barrier();
+    for (int l = L; l >= 1; --l) {
+        // reverse of Eq. 4, then of Eq. 3, of iteration l
+        wide_reverse(d.wk_row, b, n_row, d.wr, fc, fr, alpha + l * BN, alpha + (l - 1) * BN);
+        lds_barrier();
+        wide_reverse(d.wk_col, b, n_col, d.wc, fr, fc, beta + l * BM, beta + (l - 1) * BM);
+        lds_barrier();
+    }
+    // the adjoint with respect to P0, in row-major order
+    const int ns = wave_slots(n_row);
+    for (int s = 0; s < ns; ++s) {
+        const WSlot w = load_wslot(d.wk_row, b, s);
+        const Unpack u = Unpack::make();
+        if (u.bits(w.info, 17, 1) == 0u)
+            continue;
+        const int i = (int)u.bits(w.info, 0, 13), lg = (int)u.bits(w.info, 13, 3);
+        const int p = s * kT + tid, q = p & ((1 << lg) - 1); // groups are aligned to their size
+        const int r0 = d.row_ptr[(size_t)b * N + i], len = d.row_ptr[(size_t)b * N + i + 1] - r0;
+#pragma unroll
+        for (int e = 0; e < kP; ++e)
+            if (q * kP + e < len) {
+                const float2 f = lds_at<float2>(fc, u.half(w.gi[e / 2], e));
+                d.adj[r0 + q * kP + e] = (double)d.wr[pk_index(b, p, e, kP, d.wk_row.slots)] - (double)f.x;
+            }
     }
 }
 
@@ -843,6 +1197,38 @@ int sinkhorn_slots(int N, int M, const int32_t *counts, int B)
     }
     const int slots = (most + kT - 1) / kT;
     return slots <= kSinkMaxSlots ? slots : 0;
+}
+
+int sinkhorn_slots_wide(int N, int M, const int32_t *counts, int B)
+{
+    if (N > kSinkOwnersW || M > kSinkOwnersW)
+        return 0;
+    int most = 1;
+    for (int b = 0; b < B; ++b) {
+        if (counts[4 * b + 2] > kSinkMaxGroup || counts[4 * b + 3] > kSinkMaxGroup)
+            return 0;
+        most = std::max({most, counts[4 * b], counts[4 * b + 1]});
+    }
+    const int slots = (most + kT - 1) / kT;
+    return slots <= kSinkMaxSlotsW ? slots : 0;
+}
+
+void launch_wide_pack(const DevPlan &d, int32_t *place, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_place_w, dim3(d.B, 2), dim3(kT), 0, s, d, place);
+    hipLaunchKernelGGL(k_pack_w, dim3(blocks_for(2 * d.nnz, kBlock)), dim3(kBlock), 0, s, d, (const int32_t *)place);
+}
+
+hipError_t launch_sinkhorn_fwd_wide(const DevPlan &d, double eps, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_sinkhorn_fwd_w, dim3(d.B), dim3(kT), 0, s, d, eps);
+    return hipGetLastError();
+}
+
+hipError_t launch_sinkhorn_bwd_wide(const DevPlan &d, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_sinkhorn_bwd_w, dim3(d.B), dim3(kT), 0, s, d);
+    return hipGetLastError();
 }
 
 constexpr size_t kLdsBudget = 160 * 1024;

@@ -71,6 +71,14 @@ def test_single_sample_odd_shapes(scan):
     _check_batch(X, Y, "N=65 M=3", n_iter=3, scan=scan)
 
 
+@pytest.mark.parametrize("L", [1, 3, 10])
+def test_streamed_per_sample_sinkhorn(L):
+    # clouds of 2048 < N, M <= 8192 points: one workgroup per sample runs every
+    # Sinkhorn sweep with the pieces streamed from memory (ragged sizes)
+    X, Y = custom(37, 3, 3000, 5000, reference="primitives", prediction="perm_noise", sigma=0.05)
+    _check_batch(X, Y, f"streamed sweeps L={L}", n_iter=L)
+
+
 @pytest.mark.parametrize("L", [0, 1, 20])
 def test_iteration_counts(L):
     X, Y = custom(25, 2, 200, 180, sigma=0.05)
