@@ -122,7 +122,10 @@ typedef struct apml_plan apml_plan;
  * The call synchronises the stream once, after the support has been counted,
  * to size the sparse arrays (the paper's two-pass construction does the same).
  * x and y are only read. On error *plan is NULL and loss is untouched unless
- * the failure came from the device.
+ * the failure came from the device. A device-side consistency check that runs
+ * after that synchronisation (a row's or column's minimum missing from its
+ * stored pairs, which the construction rules out) is reported only by
+ * apml_plan_nnz, as APML_ERR_INTERNAL; this call returns APML_OK then.
  */
 apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, int32_t M,
                          int32_t d, const apml_params *params, float *loss, apml_plan **plan,

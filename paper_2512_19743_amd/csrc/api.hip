@@ -608,7 +608,9 @@ apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t
             ea.cnt = c.take<int32_t>((size_t)BN * ea.S);
             if (ea.chunk <= 65536) {
                 ea.kst = stage_slots(ea.S);
-                ea.stage = c.take<uint16_t>((size_t)BN * ea.S * ea.kst);
+                ea.stage_narrow = ea.chunk <= 256;
+                const size_t staged = (size_t)BN * ea.S * ea.kst;
+                ea.stage = c.take<uint16_t>(ea.stage_narrow ? (staged + 1) / 2 : staged);
                 const size_t tiles = (size_t)B * ea.S * rows.owner_blocks;
                 ea.spill = c.take<uint32_t>(tiles * kTileSpill);
                 ea.spill_n = c.take<int32_t>(tiles);

@@ -110,8 +110,10 @@ struct EmitArgs {
     int B, N, M, S, chunk, owner_blocks;
     int32_t *cnt;        // [B*N][S] stored pairs per (row, column chunk)
     int32_t *col_cnt;    // [B*M] stored pairs per column
-    uint16_t *stage;     // [B*N][S][kst] column offsets within the chunk of the first hits, or NULL
+    uint16_t *stage;     // [B*N][S][kst] column offsets within the chunk of the first hits, or NULL;
+                         // one byte each when stage_narrow (chunks of at most 256 columns)
     int kst;             // staged hits per (row, chunk)
+    int stage_narrow;
     uint32_t *spill;     // [tiles][kTileSpill]: further hits, row within the tile << 16 | offset in the chunk
     int32_t *spill_n;    // [tiles]: entries of the tile list (more than kTileSpill: overflowed)
     Counters *ctr;

@@ -164,6 +164,22 @@ __device__ __forceinline__ void for_each_hit(float ax, float ay, float az, float
     }
 }
 
+// Staged hit k of (row, chunk) slot: the column's offset within the chunk,
+// in one byte when every chunk has at most 256 columns, else in two.
+__device__ __forceinline__ void stage_put(const EmitArgs &a, size_t slot, int k, int v)
+{
+    if (a.stage_narrow)
+        reinterpret_cast<uint8_t *>(a.stage)[slot * a.kst + k] = (uint8_t)v;
+    else
+        a.stage[slot * a.kst + k] = (uint16_t)v;
+}
+
+__device__ __forceinline__ int stage_get(const EmitArgs &a, size_t slot, int k)
+{
+    return a.stage_narrow ? (int)reinterpret_cast<const uint8_t *>(a.stage)[slot * a.kst + k]
+                          : (int)a.stage[slot * a.kst + k];
+}
+
 // Pass 1 (WRITE = false) counts the hits of each (row, chunk) and of each
 // column; pass 2 writes them, in increasing column, at the row's CSR offset
 // plus the counts of the row's earlier chunks. Both passes take bitwise the
@@ -188,7 +204,8 @@ template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs 
     const uint32_t keep = valid ? ~0u : 0u; // a lane without a row ignores the columns' balls too
     if (!WRITE) {
         int32_t *col_cnt = a.col_cnt + (size_t)b * a.M;
-        uint16_t *stage = a.stage ? a.stage + ((size_t)row * a.S + ch) * a.kst : nullptr;
+        const bool stage = a.stage != nullptr;
+        const size_t slot = (size_t)row * a.S + ch;
         uint32_t *spill = a.stage ? a.spill + (size_t)t * kTileSpill : nullptr;
         if (threadIdx.x == 0)
             n_spill = 0;
@@ -198,7 +215,7 @@ template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs 
             atomicAdd(&col_cnt[j], 1);
             if (stage) {
                 if (cnt < a.kst) {
-                    stage[cnt] = (uint16_t)(j - j0);
+                    stage_put(a, slot, cnt, j - j0);
                 } else { // in increasing j for each row
                     const int k = atomicAdd(&n_spill, 1);
                     if (k < kTileSpill)
@@ -264,13 +281,14 @@ template <bool PLACE> __device__ __forceinline__ void emit_compact_thread(const 
     const int n_spill = a.spill_n[t];
     if (n_spill > kTileSpill) // the writing pass rescans this tile
         return;
-    const uint16_t *st = a.stage + (size_t)g * a.kst;
     const int j0 = ch * a.chunk, gc0 = b * a.M + j0;
     const int ns = min(n, a.kst);
 #pragma unroll
     for (int k = 0; k < kStage; ++k) // fixed trip count: the pairs' loads and atomics overlap
-        if (k < ns)
-            emit_pair<PLACE>(a, pos + k, row, i, gc0 + st[k], j0 + st[k]);
+        if (k < ns) {
+            const int jj = stage_get(a, (size_t)g, k);
+            emit_pair<PLACE>(a, pos + k, row, i, gc0 + jj, j0 + jj);
+        }
     if (n > a.kst) {
         const uint32_t *sp = a.spill + (size_t)t * kTileSpill;
         const uint32_t me = (uint32_t)(i % kBlock);

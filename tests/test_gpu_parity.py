@@ -79,6 +79,14 @@ def test_streamed_per_sample_sinkhorn(L):
     _check_batch(X, Y, f"streamed sweeps L={L}", n_iter=L)
 
 
+def test_per_iteration_sweeps_twenty_iterations():
+    # clouds beyond 8192 points: one launch per Sinkhorn half-sweep, with the
+    # per-point factors gathered in single precision; 20 iterations, as the
+    # large-batch workload
+    X, Y = custom(38, 1, 9000, 9000, reference="primitives", prediction="perm_noise", sigma=0.01)
+    _check_batch(X, Y, "per-iteration sweeps L=20", n_iter=20)
+
+
 @pytest.mark.parametrize("L", [0, 1, 20])
 def test_iteration_counts(L):
     X, Y = custom(25, 2, 200, 180, sigma=0.05)
