@@ -280,6 +280,9 @@ def torch_peak_bytes(step) -> int:
 
     gc.collect()
     torch.cuda.synchronize()
+    # blocks the library's own pool still caches would otherwise be missing
+    # from what PyTorch can allocate
+    apml.apml_release_cached_memory()
     apml.apml_set_allocator_torch()
     try:
         step()  # warm the caching allocator's blocks
@@ -295,15 +298,36 @@ def torch_peak_bytes(step) -> int:
         apml.apml_set_allocator_default()
 
 
+def dense_bytes(B, N, M, L, d=3) -> int:
+    """Device memory of one dense forward + backward: P0 and the plan (float32)
+    and the plan adjoint (float64) per pair, and an upper bound of the
+    per-point vectors (statistics, Sinkhorn sums and their products, column
+    partial sums)."""
+    return 16 * B * N * M + (96 + 16 * (L + 1) + 8 * d * 64) * B * (N + M)
+
+
 def dense_baseline(x, y, gl, w, sparse_ms, sparse_peak, steps):
     """Dense APML (every pair materialised, Sec. III-A) forward + backward on
     the same batch: median time of a few steps and peak memory (PyTorch's
-    caching allocator route), next to the sparse path's."""
+    caching allocator route), next to the sparse path's. Skipped, with the
+    reason, when its matrices do not fit in the free device memory."""
+    import gc
+
     import torch
 
     import paper_2512_19743_amd as apml
 
     prm = apml.apml_params_default(n_iter=w.n_iter)
+    need = dense_bytes(w.B, w.N, w.M, w.n_iter)
+    gc.collect()
+    torch.cuda.synchronize()
+    apml.apml_release_cached_memory()
+    torch.cuda.empty_cache()
+    free = torch.cuda.mem_get_info()[0]
+    if need > 0.8 * free:
+        return {"skipped": f"needs {need / 1e9:.1f} GB of device memory (16 B per pair), "
+                           f"{free / 1e9:.1f} GB free", "model_gb": need / 1e9,
+                "memory_ratio_dense_over_sparse_model": need / sparse_peak}
 
     def dstep():
         loss, plan = apml.apml_dense_forward(x, y, prm)
@@ -322,7 +346,8 @@ def dense_baseline(x, y, gl, w, sparse_ms, sparse_peak, steps):
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / n
     peak = torch_peak_bytes(dstep)
-    return {"ms_per_step": ms, "peak_hbm_mb": peak / 1e6, "steps": n,
+    torch.cuda.empty_cache()
+    return {"ms_per_step": ms, "peak_hbm_mb": peak / 1e6, "steps": n, "model_gb": need / 1e9,
             "time_ratio_dense_over_sparse": ms / sparse_ms, "memory_ratio_dense_over_sparse": peak / sparse_peak,
             "what": "apml_dense_forward + apml_dense_backward: P0, the plan and its adjoint as N x M matrices"}
 

@@ -256,8 +256,12 @@ apml_status apml_plan_export_stats(const apml_plan *plan, int32_t b, double *T_r
  * same stream). A caller may route every allocation through its own
  * allocator instead, e.g. a framework's caching allocator; alloc must return
  * device memory usable on `stream` (or NULL on failure), free is called with
- * the same pointer, size and stream. Passing NULLs restores the pool. Must
- * not be called while a plan is alive.
+ * the same pointer, size and stream. Every failure of alloc must come back as
+ * NULL: the library cannot tell any other pointer from device memory and its
+ * kernels will write through it (a binding whose callbacks can raise must
+ * catch and return NULL). Blocks the pool caches are not given back when the
+ * route changes: apml_release_cached_memory does that. Passing NULLs restores
+ * the pool. Must not be called while a plan is alive.
  */
 typedef void *(*apml_alloc_fn)(size_t bytes, apml_stream stream, void *user);
 typedef void (*apml_free_fn)(void *ptr, size_t bytes, apml_stream stream, void *user);

@@ -117,8 +117,13 @@ def load() -> ctypes.CDLL:
 
 
 def _check(func: str, status: int):
+    global torch_alloc_error
     if status != APML_OK:
-        raise ApmlError(func, status, load().apml_last_error().decode())
+        detail = load().apml_last_error().decode()
+        if status == 3 and torch_alloc_error is not None:
+            detail += f" (PyTorch's allocator: {type(torch_alloc_error).__name__}: {torch_alloc_error})"
+        torch_alloc_error = None
+        raise ApmlError(func, status, detail)
 
 
 def apml_params_default(**overrides) -> apml_params:
@@ -387,20 +392,38 @@ def apml_profile_read() -> dict:
 
 
 _torch_alloc_refs = None
+# the last exception raised inside the PyTorch-backed allocation callback
+torch_alloc_error: Optional[BaseException] = None
+
+
+def torch_alloc(size, stream, user):
+    """Allocation callback of the PyTorch route. A Python exception must never
+    cross into C: a ctypes callback that raises hands the caller an undefined
+    pointer instead of NULL, so every failure (PyTorch running out of memory
+    included) returns NULL, which the library reports as
+    APML_ERR_OUT_OF_MEMORY; the exception is kept in torch_alloc_error."""
+    global torch_alloc_error
+    try:
+        p = torch.cuda.caching_allocator_alloc(int(size), torch.cuda.current_device(), stream or 0)
+        return int(p) if p else None
+    except BaseException as e:  # noqa: BLE001 - nothing may propagate into C
+        torch_alloc_error = e
+        return None
+
+
+def torch_free(ptr, size, stream, user):
+    """Release callback of the PyTorch route; never raises into C."""
+    global torch_alloc_error
+    try:
+        torch.cuda.caching_allocator_delete(ptr)
+    except BaseException as e:  # noqa: BLE001
+        torch_alloc_error = e
 
 
 def apml_set_allocator_torch():
     """Routes libapml's device allocations through PyTorch's caching allocator."""
     global _torch_alloc_refs
-
-    def _alloc(size, stream, user):
-        dev = torch.cuda.current_device()
-        return torch.cuda.caching_allocator_alloc(int(size), dev, stream or 0)
-
-    def _free(ptr, size, stream, user):
-        torch.cuda.caching_allocator_delete(ptr)
-
-    a, f = ALLOC_FN(_alloc), FREE_FN(_free)
+    a, f = ALLOC_FN(torch_alloc), FREE_FN(torch_free)
     _check("apml_set_allocator", load().apml_set_allocator(a, f, None))
     _torch_alloc_refs = (a, f)
 

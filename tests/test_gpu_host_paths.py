@@ -65,26 +65,38 @@ def test_torch_caching_allocator_route():
 
 
 class _CountingAllocator:
-    """PyTorch-backed allocator that returns NULL from its n-th call on."""
+    """PyTorch-backed allocator that returns NULL from its n-th call on. Its
+    callbacks never raise into C (a ctypes callback that raises returns an
+    undefined pointer): failures are recorded in errors and checked by the
+    test."""
 
     def __init__(self, fail_from: int):
         self.fail_from = fail_from
         self.calls = 0
         self.live = {}
+        self.errors = []
         self.alloc = _lib.ALLOC_FN(self._alloc)
         self.free = _lib.FREE_FN(self._free)
 
     def _alloc(self, size, stream, user):
-        self.calls += 1
-        if self.calls >= self.fail_from:
+        try:
+            self.calls += 1
+            if self.calls >= self.fail_from:
+                return None
+            p = torch.cuda.caching_allocator_alloc(int(size), torch.cuda.current_device(), stream or 0)
+            self.live[p] = size
+            return p
+        except BaseException as e:  # noqa: BLE001
+            self.errors.append(repr(e))
             return None
-        p = torch.cuda.caching_allocator_alloc(int(size), torch.cuda.current_device(), stream or 0)
-        self.live[p] = size
-        return p
 
     def _free(self, ptr, size, stream, user):
-        assert self.live.pop(ptr) == size
-        torch.cuda.caching_allocator_delete(ptr)
+        try:
+            if self.live.pop(ptr, None) != size:
+                self.errors.append(f"free of {ptr:#x} with size {size} that was not handed out")
+            torch.cuda.caching_allocator_delete(ptr)
+        except BaseException as e:  # noqa: BLE001
+            self.errors.append(repr(e))
 
 
 def _forward_raw(lib, x, y, loss, plan):
@@ -138,6 +150,7 @@ def test_allocator_returning_null(where):
             torch.cuda.synchronize()
             assert (loss == 7.0).all()  # the loss is written by the last kernels of the forward
         torch.cuda.synchronize()
+        assert a.errors == [] and count.errors == []
         assert a.live == {}, "every block the library took must be given back"
         assert apml.apml_get_memory_stats()["in_use"] == before
     finally:
@@ -161,3 +174,43 @@ def test_forward_wait_deadline(monkeypatch):
     loss, plan = apml.apml_forward(x, y)
     torch.cuda.synchronize()
     assert np.isfinite(loss.cpu().numpy()).all()
+
+
+@pytest.mark.parametrize("fail_at", [1, 4])
+def test_torch_route_out_of_memory(monkeypatch, fail_at):
+    # PyTorch's allocator raising (as it does when the device is full) must
+    # reach the library as NULL: the call reports APML_ERR_OUT_OF_MEMORY and
+    # every block taken before is given back
+    X, Y = custom(53, 2, 300, 280, sigma=0.05)
+    x, y = torch.from_numpy(X).cuda(), torch.from_numpy(Y).cuda()
+    note(f"allocator: PyTorch route raising at call {fail_at}")
+    gc.collect()
+    torch.cuda.synchronize()
+    real = torch.cuda.caching_allocator_alloc
+    calls = [0]
+
+    def flaky(size, device=None, stream=None):
+        calls[0] += 1
+        if calls[0] >= fail_at:
+            raise torch.OutOfMemoryError("forced by the test")
+        return real(size, device, stream)
+
+    apml.apml_set_allocator_torch()
+    try:
+        base = torch.cuda.memory_allocated()
+        monkeypatch.setattr(torch.cuda, "caching_allocator_alloc", flaky)
+        with pytest.raises(apml.ApmlError) as err:
+            apml.apml_forward(x, y)
+        assert err.value.status == 3 and "forced by the test" in str(err.value)
+        monkeypatch.setattr(torch.cuda, "caching_allocator_alloc", real)
+        torch.cuda.synchronize()
+        assert torch.cuda.memory_allocated() == base
+        loss, plan = apml.apml_forward(x, y)
+        torch.cuda.synchronize()
+        assert np.isfinite(loss.cpu().numpy()).all()
+        plan.close()
+        del loss
+        torch.cuda.synchronize()
+    finally:
+        monkeypatch.setattr(torch.cuda, "caching_allocator_alloc", real)
+        apml.apml_set_allocator_default()
