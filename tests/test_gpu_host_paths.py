@@ -198,12 +198,16 @@ def test_torch_route_out_of_memory(monkeypatch, fail_at):
     apml.apml_set_allocator_torch()
     try:
         base = torch.cuda.memory_allocated()
+        before = apml.apml_get_memory_stats()["in_use"]
         monkeypatch.setattr(torch.cuda, "caching_allocator_alloc", flaky)
         with pytest.raises(apml.ApmlError) as err:
             apml.apml_forward(x, y)
         assert err.value.status == 3 and "forced by the test" in str(err.value)
         monkeypatch.setattr(torch.cuda, "caching_allocator_alloc", real)
+        del err  # its traceback holds the wrapper's output tensor
+        gc.collect()
         torch.cuda.synchronize()
+        assert apml.apml_get_memory_stats()["in_use"] == before
         assert torch.cuda.memory_allocated() == base
         loss, plan = apml.apml_forward(x, y)
         torch.cuda.synchronize()
