@@ -125,7 +125,10 @@ typedef struct apml_plan apml_plan;
  * the failure came from the device. A device-side consistency check that runs
  * after that synchronisation (a row's or column's minimum missing from its
  * stored pairs, which the construction rules out) is reported only by
- * apml_plan_nnz, as APML_ERR_INTERNAL; this call returns APML_OK then.
+ * apml_plan_nnz, as APML_ERR_INTERNAL; this call returns APML_OK then. So is
+ * a bounded wait of the Sinkhorn kernels that split a sample over several
+ * workgroups expiring (they are launched so that all of them run at once,
+ * which rules it out), as APML_ERR_DEVICE.
  */
 apml_status apml_forward(const float *x, const float *y, int32_t B, int32_t N, int32_t M,
                          int32_t d, const apml_params *params, float *loss, apml_plan **plan,
@@ -222,7 +225,8 @@ apml_status apml_plan_get_info(const apml_plan *plan, apml_plan_info *info);
 
 /* Per-sample size of the kept support Omega = Omega_row U Omega_col
  * (Sec. III-B), host int64 [B]. Synchronises the plan's stream. Returns
- * APML_ERR_INTERNAL if a device-side consistency check failed. */
+ * APML_ERR_INTERNAL if a device-side consistency check failed, and
+ * APML_ERR_DEVICE if a bounded wait of the split Sinkhorn kernels expired. */
 apml_status apml_plan_nnz(const apml_plan *plan, int64_t *nnz);
 
 /*

@@ -855,6 +855,7 @@ apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t
                 wk->info = c.take<uint32_t>(w / kSinkPiece);
                 wk->n_pos = c.take<int32_t>(B);
             }
+            dv.split_sync = c.take<uint32_t>((size_t)B * 2 * kSplitSyncStride);
         }
     };
     {
@@ -1042,6 +1043,9 @@ apml_status run_backward(apml_plan *plan, const float *x, const float *y, const 
     dv.grad_loss = grad_loss;
     dv.grad_x = grad_x;
     dv.grad_y = grad_y;
+    dv.xr2 = dv.xc2 = nullptr;
+    // the split streamed reverse kernel exchanges the owners' factors in memory
+    const bool split = dv.L > 0 && plan->sink_wide && sinkhorn_split_factor(plan->B) > 1;
     // On the per-iteration path the row-order sweep adjoint becomes the final
     // adjoint in place (k_bwd_final reads and writes the same pair), and the
     // cost adjoint reuses the column-order copy, dead once the sweeps end.
@@ -1052,6 +1056,10 @@ apml_status run_backward(apml_plan *plan, const float *x, const float *y, const 
             dv.wr = c.take<float>(w);
             dv.wc = c.take<float>(w);
             dv.cbar = c.take<double>(plan->stored);
+            if (split) {
+                dv.xr2 = c.take<float2>((size_t)plan->B * plan->N);
+                dv.xc2 = c.take<float2>((size_t)plan->B * plan->M);
+            }
         } else if (dv.L > 0 && !plan->sink_bwd) {
             dv.rz = dv.adj;
             dv.kz = c.take<double>(plan->stored);
@@ -1447,8 +1455,11 @@ apml_status apml_plan_nnz(const apml_plan *plan, int64_t *nnz)
             n += (int64_t)h[(size_t)b * chunks + c];
         nnz[b] = n;
     }
-    if (hc.error)
+    if (hc.error & 3u)
         return fail(APML_ERR_INTERNAL, "a row or column minimum was not found among its stored pairs");
+    if (hc.error & 4u)
+        return fail(APML_ERR_DEVICE, "the workgroups sharing a sample in the split Sinkhorn kernels did not all "
+                                     "arrive at a meeting (bounded wait expired)");
     return APML_OK;
 }
 

@@ -18,7 +18,8 @@ constexpr int kScanSlots = 64;
 // Device-side counters of one forward call (cleared by the first kernel that
 // runs after them: the full scan's finalize kernel or the spatial sort).
 struct Counters {
-    unsigned int error;            // bit 0: a row's minima not found among its pairs; bit 1: a column's
+    unsigned int error;            // bit 0: a row's minima not found among its pairs; bit 1: a column's;
+                                   // bit 2: a meeting of the split streamed Sinkhorn kernels timed out
     unsigned int overflow;         // a (row, chunk) of the full support scan had more hits than its staging slots
     // pairs evaluated by the skipping scans (minimum scan, support scan), in
     // kScanSlots partial sums: workgroup w adds to slot w % kScanSlots, so
@@ -312,6 +313,10 @@ struct DevPlan {
     PackedOrder pk_row, pk_col;   // per-sample Sinkhorn pieces (when that path is taken)
     WideOrder wk_row, wk_col;     // streamed per-sample pieces (larger samples)
     float *wr, *wc;               // backward of the streamed path: the plan adjoint in row and in column pieces
+    uint32_t *split_sync;         // [B][2][kSplitSyncStride]: meeting counter (word 0) and the workgroups' XCDs
+                                  // (words 1..K) of the split streamed kernels
+                                  // (forward, backward), cleared before each launch
+    float2 *xr2, *xc2;            // [2][B*N], [2][B*M]: owners' factors exchanged by the split reverse kernel
     const int32_t *sink_place;    // during the forward softmax of that path: the pieces' placement, so that the
                                   // column softmax writes every pair into its pieces; else NULL
 };
@@ -375,6 +380,15 @@ int sinkhorn_slots_wide(int N, int M, const int32_t *counts, int B);
 // Places the streamed pieces (place: [B][2][kSinkOwnersW] int32 scratch)
 // and writes every pair into them (after the softmax).
 void launch_wide_pack(const DevPlan &d, int32_t *place, hipStream_t s);
+// Workgroups per sample of the split streamed kernels for a batch of B on the
+// current device (2..kSplitMax; every workgroup of the grid must be resident
+// at once), or 1 when the one-workgroup kernels are taken (also when the
+// environment sets APML_SINKHORN_SPLIT=0).
+constexpr int kSplitMax = 8;
+constexpr int kSplitSyncStride = 32; // counters 128 bytes apart
+int sinkhorn_split_factor(int B);
+// Streamed kernels, split over sinkhorn_split_factor(B) workgroups per sample
+// when that is above 1 (the reverse kernel then needs d.xr2, d.xc2), else one.
 hipError_t launch_sinkhorn_fwd_wide(const DevPlan &d, double eps, hipStream_t s);
 hipError_t launch_sinkhorn_bwd_wide(const DevPlan &d, hipStream_t s);
 bool sinkhorn_bwd_fits(int slots, int64_t max_pairs);

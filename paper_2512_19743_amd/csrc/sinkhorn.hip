@@ -31,6 +31,8 @@
 // pair it reads and writes the result back. Each pair's adjoint is read and
 // written once per sweep.
 #include <algorithm>
+#include <atomic>
+#include <cstdlib>
 
 #include "apml_internal.h"
 #include "device_common.h"
@@ -731,22 +733,41 @@ __device__ __forceinline__ int wave_slots(int n_used)
 // of work does not cover.
 constexpr int kWBatch = 4;
 
+// Split kernels: how a sample's workgroups exchange 64-bit words. When they
+// all run on one XCD (local), through that XCD's L2: plain stores (the CU's
+// cache writes through to the L2) and loads that skip only the CU's cache
+// (sc0). Otherwise through memory: relaxed device-scope atomics, which skip
+// the per-XCD L2s. Measured with 4 workgroups exchanging 8192 words: 2.3 us
+// per meeting and exchange through the L2, 15.7 us through memory.
+__device__ __forceinline__ void publish64(void *p, uint64_t v, bool local)
+{
+    if (local)
+        *reinterpret_cast<uint64_t *>(p) = v;
+    else
+        __hip_atomic_store(reinterpret_cast<uint64_t *>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // One forward sweep: every owner's sum of P0 times the other side's scaling
 // (vals) over its pieces, then its own scaling v = cur / (cur sum + eps)
-// (Eq. 3 or Eq. 4) into own (LDS) and g_val (the saved scalings).
+// (Eq. 3 or Eq. 4) into own (LDS) and g_val (the saved scalings). With SPLIT
+// the calling workgroup takes the slots s0, s0 + step, ... of each wave, and
+// v goes to g_val only (published for the other workgroups of the sample);
+// every owner's sum is formed by the same lanes as in the one-workgroup
+// kernel, so both give the same bits.
+template <bool SPLIT>
 __device__ void wide_sweep(const WideOrder &pk, int b, int n_used, const double *vals, double *own, double eps,
-                           double *g_val)
+                           double *g_val, int s0_first = 0, int step = 1, bool local = false)
 {
     const int ns = wave_slots(n_used);
-    for (int s0 = 0; s0 < ns; s0 += kWBatch) {
+    for (int s0 = s0_first; s0 < ns; s0 += kWBatch * step) {
         WSlot w[kWBatch];
 #pragma unroll
         for (int k = 0; k < kWBatch; ++k)
-            if (s0 + k < ns)
-                w[k] = load_wslot(pk, b, s0 + k);
+            if (s0 + k * step < ns)
+                w[k] = load_wslot(pk, b, s0 + k * step);
 #pragma unroll
         for (int k = 0; k < kWBatch; ++k) {
-            if (s0 + k >= ns)
+            if (s0 + k * step >= ns)
                 break;
             const Unpack u = Unpack::make();
             double g[kP];
@@ -762,8 +783,12 @@ __device__ void wide_sweep(const WideOrder &pk, int b, int n_used, const double 
                 const int o = (int)u.bits(w[k].info, 0, 13);
                 const double c = own[o];
                 const double v = quotient(c, c * acc + eps);
-                own[o] = v;
-                g_val[o] = v;
+                if constexpr (SPLIT) {
+                    publish64(g_val + o, __builtin_bit_cast(uint64_t, v), local);
+                } else {
+                    own[o] = v;
+                    g_val[o] = v;
+                }
             }
         }
     }
@@ -789,9 +814,9 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_fwd_w(DevPlan d, double eps)
     lds_barrier();
     for (int l = 1; l <= L; ++l) {
         // column scaling (Eq. 3), then row scaling (Eq. 4)
-        wide_sweep(d.wk_col, b, n_col, va, vb, eps, d.beta + l * BM + (size_t)b * M);
+        wide_sweep<false>(d.wk_col, b, n_col, va, vb, eps, d.beta + l * BM + (size_t)b * M);
         lds_barrier();
-        wide_sweep(d.wk_row, b, n_row, vb, va, eps, d.alpha + l * BN + (size_t)b * N);
+        wide_sweep<false>(d.wk_row, b, n_row, vb, va, eps, d.alpha + l * BN + (size_t)b * N);
         lds_barrier();
     }
     sample_loss(d, b, lo, hi, va, vb, part);
@@ -802,37 +827,41 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_fwd_w(DevPlan d, double eps)
 // (factors fin, gathered), the owners' sums formed, this direction's step
 // applied, and the owners' factors published in fout (see above). own:
 // the saved scalings of this direction at iteration l (own_l) and l - 1.
+// With SPLIT the calling workgroup takes the slots s0, s0 + step, ... and
+// the factors go to fout in global memory for the sample's other workgroups.
+template <bool SPLIT>
 __device__ void wide_reverse(const WideOrder &pk, int b, int n_used, float *copy, const float2 *fin, float2 *fout,
-                             const double *own_l, const double *own_prev)
+                             const double *own_l, const double *own_prev, int s0_first = 0, int step = 1,
+                             bool local = false)
 {
     const int ns = wave_slots(n_used);
-    for (int s0 = 0; s0 < ns; s0 += kWBatch) {
+    for (int s0 = s0_first; s0 < ns; s0 += kWBatch * step) {
         WSlot w[kWBatch];
         float cv[kWBatch][kP];
         double al[kWBatch], alp[kWBatch];
 #pragma unroll
         for (int k = 0; k < kWBatch; ++k)
-            if (s0 + k < ns) {
-                w[k] = load_wslot(pk, b, s0 + k);
-                const int p = (s0 + k) * kT + (int)threadIdx.x;
+            if (s0 + k * step < ns) {
+                w[k] = load_wslot(pk, b, s0 + k * step);
+                const int p = (s0 + k * step) * kT + (int)threadIdx.x;
 #pragma unroll
                 for (int e = 0; e < kP; ++e)
                     cv[k][e] = copy[pk_index(b, p, e, kP, pk.slots)];
             }
 #pragma unroll
         for (int k = 0; k < kWBatch; ++k)
-            if (s0 + k < ns) {
+            if (s0 + k * step < ns) {
                 const int o = (int)(w[k].info & 0x1FFFu);
                 al[k] = own_l[o];
                 alp[k] = own_prev[o];
             }
 #pragma unroll
         for (int k = 0; k < kWBatch; ++k) {
-            if (s0 + k >= ns)
+            if (s0 + k * step >= ns)
                 break;
             const Unpack u = Unpack::make();
             const int o = (int)u.bits(w[k].info, 0, 13);
-            const int p = (s0 + k) * kT + (int)threadIdx.x;
+            const int p = (s0 + k * step) * kT + (int)threadIdx.x;
             float2 f[kP];
 #pragma unroll
             for (int e = 0; e < kP; ++e)
@@ -850,33 +879,34 @@ __device__ void wide_reverse(const WideOrder &pk, int b, int n_used, float *copy
             for (int e = 0; e < kP; ++e)
                 copy[pk_index(b, p, e, kP, pk.slots)] =
                     w[k].p0[e] != 0.0f ? (float)((rho[e] - dsum * (double)f[e].y) * q) : 0.0f;
-            if (u.bits(w[k].info, 16, 2) == 3u) // head and valid
-                fout[o] = make_float2((float)(dsum * al[k]), (float)alp[k]);
+            if (u.bits(w[k].info, 16, 2) == 3u) { // head and valid
+                const float2 f = make_float2((float)(dsum * al[k]), (float)alp[k]);
+                if constexpr (SPLIT)
+                    publish64(fout + o, __builtin_bit_cast(uint64_t, f), local);
+                else
+                    fout[o] = f;
+            }
         }
     }
 }
 
-__global__ __launch_bounds__(kT) void k_sinkhorn_bwd_w(DevPlan d)
+// The two adjoint copies of sample b start as grad_loss C beta^L_j (rows) and
+// grad_loss C alpha^L_i (columns), over the slots s0, s0 + step, ...
+__device__ void wide_reverse_start(const DevPlan &d, int b, int n_row, int n_col, int s0_first, int step)
 {
-    __shared__ float2 fr[kSinkOwnersW]; // row factors (Yr_i, alpha^(l-1)_i)
-    __shared__ float2 fc[kSinkOwnersW]; // column factors (Yc_j, beta^(l-1)_j)
-    const int b = blockIdx.x, tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
     const float *xb = d.x + (size_t)b * N * 3, *yb = d.y + (size_t)b * M * 3;
-    const double *alpha = d.alpha + (size_t)b * N, *beta = d.beta + (size_t)b * M; // + l * BN, + l * BM
+    const double *alpha = d.alpha + (size_t)b * N, *beta = d.beta + (size_t)b * M;
     const double gl = d.grad_loss[b];
-    const int n_row = __builtin_amdgcn_readfirstlane(d.wk_row.n_pos[b]);
-    const int n_col = __builtin_amdgcn_readfirstlane(d.wk_col.n_pos[b]);
-    // the copies start as grad_loss C beta^L_j (rows) and grad_loss C alpha^L_i (columns)
     for (int order = 0; order < 2; ++order) {
         const WideOrder &pk = order == 0 ? d.wk_row : d.wk_col;
         float *copy = order == 0 ? d.wr : d.wc;
         const int ns = wave_slots(order == 0 ? n_row : n_col);
-        for (int s = 0; s < ns; ++s) {
+        for (int s = s0_first; s < ns; s += step) {
             const WSlot w = load_wslot(pk, b, s);
             const Unpack u = Unpack::make();
-            const int o = (int)u.bits(w.info, 0, 13), p = s * kT + tid;
+            const int o = (int)u.bits(w.info, 0, 13), p = s * kT + (int)threadIdx.x;
 #pragma unroll
             for (int e = 0; e < kP; ++e) {
                 const int k = (int)(u.half(w.gi[e / 2], e) >> 3);
@@ -887,25 +917,22 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_w(DevPlan d)
             }
         }
     }
-    for (int k = tid; k < M; k += kT) // no pending column update before row phase L
-        fc[k] = make_float2(0.0f, (float)beta[(size_t)L * BM + k]);
-    lds_barrier();
-    for (int l = L; l >= 1; --l) {
-        // reverse of Eq. 4, then of Eq. 3, of iteration l
-        wide_reverse(d.wk_row, b, n_row, d.wr, fc, fr, alpha + l * BN, alpha + (l - 1) * BN);
-        lds_barrier();
-        wide_reverse(d.wk_col, b, n_col, d.wc, fr, fc, beta + l * BM, beta + (l - 1) * BM);
-        lds_barrier();
-    }
-    // the adjoint with respect to P0, in row-major order
+}
+
+// After column phase 1: the adjoint with respect to P0, r - Yc_j, written in
+// row-major order for the row slots s0, s0 + step, ... (fc: the column
+// factors of that phase).
+__device__ void wide_reverse_end(const DevPlan &d, int b, int n_row, const float2 *fc, int s0_first, int step)
+{
+    const int N = d.N;
     const int ns = wave_slots(n_row);
-    for (int s = 0; s < ns; ++s) {
+    for (int s = s0_first; s < ns; s += step) {
         const WSlot w = load_wslot(d.wk_row, b, s);
         const Unpack u = Unpack::make();
         if (u.bits(w.info, 17, 1) == 0u)
             continue;
         const int i = (int)u.bits(w.info, 0, 13), lg = (int)u.bits(w.info, 13, 3);
-        const int p = s * kT + tid, q = p & ((1 << lg) - 1); // groups are aligned to their size
+        const int p = s * kT + (int)threadIdx.x, q = p & ((1 << lg) - 1); // groups are aligned to their size
         const int r0 = d.row_ptr[(size_t)b * N + i], len = d.row_ptr[(size_t)b * N + i + 1] - r0;
 #pragma unroll
         for (int e = 0; e < kP; ++e)
@@ -914,6 +941,256 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_w(DevPlan d)
                 d.adj[r0 + q * kP + e] = (double)d.wr[pk_index(b, p, e, kP, d.wk_row.slots)] - (double)f.x;
             }
     }
+}
+
+__global__ __launch_bounds__(kT) void k_sinkhorn_bwd_w(DevPlan d)
+{
+    __shared__ float2 fr[kSinkOwnersW]; // row factors (Yr_i, alpha^(l-1)_i)
+    __shared__ float2 fc[kSinkOwnersW]; // column factors (Yc_j, beta^(l-1)_j)
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const int M = d.M, L = d.L;
+    const size_t BN = (size_t)d.B * d.N, BM = (size_t)d.B * M;
+    const double *alpha = d.alpha + (size_t)b * d.N, *beta = d.beta + (size_t)b * M; // + l * BN, + l * BM
+    const int n_row = __builtin_amdgcn_readfirstlane(d.wk_row.n_pos[b]);
+    const int n_col = __builtin_amdgcn_readfirstlane(d.wk_col.n_pos[b]);
+    wide_reverse_start(d, b, n_row, n_col, 0, 1);
+    for (int k = tid; k < M; k += kT) // no pending column update before row phase L
+        fc[k] = make_float2(0.0f, (float)beta[(size_t)L * BM + k]);
+    lds_barrier();
+    for (int l = L; l >= 1; --l) {
+        // reverse of Eq. 4, then of Eq. 3, of iteration l
+        wide_reverse<false>(d.wk_row, b, n_row, d.wr, fc, fr, alpha + l * BN, alpha + (l - 1) * BN);
+        lds_barrier();
+        wide_reverse<false>(d.wk_col, b, n_col, d.wc, fr, fc, beta + l * BM, beta + (l - 1) * BM);
+        lds_barrier();
+    }
+    wide_reverse_end(d, b, n_row, fc, 0, 1);
+}
+
+// ---------------------------------------------------------------------------
+// split streamed kernels: K workgroups per sample
+// ---------------------------------------------------------------------------
+//
+// The streamed kernels above leave most CUs idle when the batch has fewer
+// samples than the chip has CUs. Here K workgroups (one per CU) share a
+// sample: workgroup k takes the slots k, k + K, ... of every wave, so each
+// owner's sum is formed by the same lanes in the same order as in the
+// one-workgroup kernels (same bits). After each half-sweep the owners' new
+// values (the saved scalings, or the two reverse factors) are published to
+// global memory and the K workgroups meet (split_meet), then every workgroup
+// reads the whole vector into its LDS. The grid is launched cooperatively:
+// all its workgroups are resident at once, so a meeting always completes.
+
+constexpr unsigned kSplitSpinLimit = 1u << 20; // polls of one meeting (about a second) before giving up
+
+// Sample and member of workgroup g. Workgroups are dispatched to the eight
+// XCDs in turn, so when 8 divides B the K workgroups of a sample are given
+// ids on one XCD (their meetings then stay within one L2's reach).
+__device__ __forceinline__ void split_member(int g, int B, int K, int &b, int &k)
+{
+    if (B % 8 == 0) {
+        const int x = g % 8, slot = g / 8; // slot < B K / 8
+        b = x * (B / 8) + slot / K;
+        k = slot % K;
+    } else {
+        b = g / K;
+        k = g % K;
+    }
+}
+
+// Meeting t of a sample's K workgroups (t = 1, 2, ...): each waits until its
+// own stores have completed (s_waitcnt: plain stores have then reached the
+// L2, device-scope atomic stores the level every XCD reads), counts itself
+// in at the sample's counter and waits until all K have (target K t). The
+// counter is a relaxed device-scope atomic, so no cache is written back or
+// invalidated. The wait is bounded: past kSplitSpinLimit polls, or once
+// another workgroup has given up, it sets bit 2 of the error word and
+// returns false, and the caller ends.
+__device__ bool split_meet(uint32_t *cnt, uint32_t target, unsigned int *err, int *stop)
+{
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        unsigned spins = 0;
+        while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+            if (++spins > kSplitSpinLimit ||
+                ((spins & 63u) == 0 && (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 4u))) {
+                __hip_atomic_fetch_or(err, 4u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                *stop = 1;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+    }
+    __syncthreads();
+    return *stop == 0;
+}
+
+// First meeting of a sample's workgroups: each records its XCD (hardware
+// register XCC_ID) next to the counter, and all decide alike, from the same
+// K words, whether they share one (local exchange through its L2).
+__device__ bool split_begin(uint32_t *sync, int K, int k, unsigned int *err, int *stop, int *local)
+{
+    if (threadIdx.x == 0) {
+        unsigned id;
+        asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(id));
+        __hip_atomic_store(sync + 1 + k, id + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (!split_meet(sync, (uint32_t)K, err, stop))
+        return false;
+    if (threadIdx.x == 0) {
+        const unsigned first = __hip_atomic_load(sync + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        int same = 1;
+        for (int q = 1; q < K; ++q)
+            same &= __hip_atomic_load(sync + 1 + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == first;
+        *local = same;
+    }
+    __syncthreads();
+    return true;
+}
+
+// One word through the L2 only: the load skips the CU's cache (sc0). Its
+// result is not waited for here (see split_gather).
+__device__ __forceinline__ uint64_t load_l2(const void *p)
+{
+    uint64_t v;
+    asm volatile("global_load_dwordx2 %0, %1, off sc0" : "=v"(v) : "v"(p) : "memory");
+    return v;
+}
+
+// The sample's n published 64-bit words into LDS, all of a thread's loads
+// issued before the first is used.
+template <typename T> __device__ __forceinline__ void split_gather(T *lds, const T *g, int n, bool local)
+{
+    static_assert(kSinkOwnersW / kT == 8, "eight words per thread");
+    uint64_t v[8] = {};
+    if (local) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int o = u * kT + (int)threadIdx.x;
+            if (o < n)
+                v[u] = load_l2(g + o);
+        }
+        // the wait names the loaded registers, so no use is scheduled before it
+        asm volatile("s_waitcnt vmcnt(0)"
+                     : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]), "+v"(v[7])
+                     :
+                     : "memory");
+    } else {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int o = u * kT + (int)threadIdx.x;
+            if (o < n)
+                v[u] = __hip_atomic_load(reinterpret_cast<const uint64_t *>(g + o), __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int o = u * kT + (int)threadIdx.x;
+        if (o < n)
+            lds[o] = __builtin_bit_cast(T, v[u]);
+    }
+}
+
+__global__ __launch_bounds__(kT) void k_sinkhorn_fwd_ws(DevPlan d, double eps, int K)
+{
+    __shared__ double va[kSinkOwnersW], vb[kSinkOwnersW], part[kT / 64];
+    __shared__ int stop, local;
+    int b, k;
+    split_member(blockIdx.x, d.B, K, b, k);
+    const int tid = threadIdx.x;
+    const int N = d.N, M = d.M, L = d.L;
+    const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
+    uint32_t *cnt = d.split_sync + ((size_t)b * 2 + 0) * kSplitSyncStride;
+    const int n_row = __builtin_amdgcn_readfirstlane(d.wk_row.n_pos[b]);
+    const int n_col = __builtin_amdgcn_readfirstlane(d.wk_col.n_pos[b]);
+    for (int o = tid; o < N; o += kT) {
+        va[o] = 1.0;
+        if (k == 0)
+            d.alpha[(size_t)b * N + o] = 1.0;
+    }
+    for (int o = tid; o < M; o += kT) {
+        vb[o] = 1.0;
+        if (k == 0)
+            d.beta[(size_t)b * M + o] = 1.0;
+    }
+    if (tid == 0)
+        stop = 0;
+    lds_barrier();
+    if (!split_begin(cnt, K, k, &d.ctr->error, &stop, &local))
+        return;
+    const bool loc = local != 0;
+    uint32_t t = 1;
+    for (int l = 1; l <= L; ++l) {
+        // column scaling (Eq. 3) of this workgroup's owners, then all of them
+        double *gb = d.beta + l * BM + (size_t)b * M;
+        wide_sweep<true>(d.wk_col, b, n_col, va, vb, eps, gb, k, K, loc);
+        if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
+            return;
+        split_gather(vb, gb, M, loc);
+        lds_barrier();
+        // row scaling (Eq. 4)
+        double *ga = d.alpha + l * BN + (size_t)b * N;
+        wide_sweep<true>(d.wk_row, b, n_row, vb, va, eps, ga, k, K, loc);
+        if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
+            return;
+        split_gather(va, ga, N, loc);
+        lds_barrier();
+    }
+    if (k == 0) // as the one-workgroup kernel, for the same bits
+        sample_loss(d, b, d.row_ptr[(size_t)b * N], d.row_ptr[(size_t)(b + 1) * N], va, vb, part);
+}
+
+// The reverse sweeps split over K workgroups. The factors of a row phase go
+// through d.xr2, those of a column phase through d.xc2: a buffer is written
+// again only two meetings later, when every workgroup has read it.
+__global__ __launch_bounds__(kT) void k_sinkhorn_bwd_ws(DevPlan d, int K)
+{
+    __shared__ float2 fr[kSinkOwnersW]; // row factors (Yr_i, alpha^(l-1)_i)
+    __shared__ float2 fc[kSinkOwnersW]; // column factors (Yc_j, beta^(l-1)_j)
+    __shared__ int stop, local;
+    int b, k;
+    split_member(blockIdx.x, d.B, K, b, k);
+    const int tid = threadIdx.x;
+    const int N = d.N, M = d.M, L = d.L;
+    const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
+    const double *alpha = d.alpha + (size_t)b * N, *beta = d.beta + (size_t)b * M; // + l * BN, + l * BM
+    uint32_t *cnt = d.split_sync + ((size_t)b * 2 + 1) * kSplitSyncStride;
+    float2 *xr = d.xr2 + (size_t)b * N, *xc = d.xc2 + (size_t)b * M;
+    const int n_row = __builtin_amdgcn_readfirstlane(d.wk_row.n_pos[b]);
+    const int n_col = __builtin_amdgcn_readfirstlane(d.wk_col.n_pos[b]);
+    wide_reverse_start(d, b, n_row, n_col, k, K);
+    for (int o = tid; o < M; o += kT) // no pending column update before row phase L
+        fc[o] = make_float2(0.0f, (float)beta[(size_t)L * BM + o]);
+    if (tid == 0)
+        stop = 0;
+    lds_barrier();
+    if (!split_begin(cnt, K, k, &d.ctr->error, &stop, &local))
+        return;
+    const bool loc = local != 0;
+    uint32_t t = 1;
+    for (int l = L; l >= 1; --l) {
+        wide_reverse<true>(d.wk_row, b, n_row, d.wr, fc, xr, alpha + l * BN, alpha + (l - 1) * BN, k, K, loc);
+        if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
+            return;
+        split_gather(fr, xr, N, loc);
+        lds_barrier();
+        wide_reverse<true>(d.wk_col, b, n_col, d.wc, fr, xc, beta + l * BM, beta + (l - 1) * BM, k, K, loc);
+        if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
+            return;
+        split_gather(fc, xc, M, loc);
+        lds_barrier();
+    }
+    wide_reverse_end(d, b, n_row, fc, k, K);
+}
+
+__global__ __launch_bounds__(kBlock) void k_zero_u32(uint32_t *a, int n)
+{
+    const int k = blockIdx.x * kBlock + threadIdx.x;
+    if (k < n)
+        a[k] = 0u;
 }
 
 // per-iteration kernels (any N, M): one launch per sweep
@@ -1219,14 +1496,79 @@ void launch_wide_pack(const DevPlan &d, int32_t *place, hipStream_t s)
     hipLaunchKernelGGL(k_pack_w, dim3(blocks_for(2 * d.nnz, kBlock)), dim3(kBlock), 0, s, d, (const int32_t *)place);
 }
 
+int sinkhorn_split_factor(int B)
+{
+    const char *env = std::getenv("APML_SINKHORN_SPLIT");
+    if (env && env[0] == '0')
+        return 1;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64 || B < 1)
+        return 1;
+    // workgroups of the split kernels resident at once on each device, plus 1
+    // (0: not yet queried)
+    static std::atomic<int> resident[64];
+    int c = resident[dev].load(std::memory_order_relaxed);
+    if (c == 0) {
+        int cus = 0, coop = 0, f = 0, r = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&f, reinterpret_cast<const void *>(k_sinkhorn_fwd_ws), kT, 0) !=
+                hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&r, reinterpret_cast<const void *>(k_sinkhorn_bwd_ws), kT, 0) !=
+                hipSuccess) {
+            (void)hipGetLastError();
+            cus = coop = 0;
+        }
+        c = (coop ? cus * std::min(f, r) : 0) + 1;
+        resident[dev].store(c, std::memory_order_relaxed);
+    }
+    const int K = std::min(kSplitMax, (c - 1) / B);
+    return K >= 2 ? K : 1;
+}
+
+namespace {
+
+// Clears the sample's meeting counters, then launches the split kernel over
+// B K workgroups, all resident at once; false when the cooperative launch
+// is refused (the caller then takes the one-workgroup kernel).
+bool launch_split(const void *kernel, void **args, const DevPlan &d, int K, hipStream_t s)
+{
+    const int n = d.B * 2 * kSplitSyncStride;
+    hipLaunchKernelGGL(k_zero_u32, dim3(blocks_for(n, kBlock)), dim3(kBlock), 0, s, d.split_sync, n);
+    if (hipGetLastError() != hipSuccess)
+        return false;
+    if (hipLaunchCooperativeKernel(kernel, dim3(d.B * K), dim3(kT), args, 0, s) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    return true;
+}
+
+} // namespace
+
 hipError_t launch_sinkhorn_fwd_wide(const DevPlan &d, double eps, hipStream_t s)
 {
+    int K = sinkhorn_split_factor(d.B);
+    if (K > 1 && d.split_sync) {
+        DevPlan dc = d;
+        double e = eps;
+        void *args[] = {&dc, &e, &K};
+        if (launch_split(reinterpret_cast<const void *>(k_sinkhorn_fwd_ws), args, d, K, s))
+            return hipSuccess;
+    }
     hipLaunchKernelGGL(k_sinkhorn_fwd_w, dim3(d.B), dim3(kT), 0, s, d, eps);
     return hipGetLastError();
 }
 
 hipError_t launch_sinkhorn_bwd_wide(const DevPlan &d, hipStream_t s)
 {
+    int K = sinkhorn_split_factor(d.B);
+    if (K > 1 && d.split_sync && d.xr2 && d.xc2) {
+        DevPlan dc = d;
+        void *args[] = {&dc, &K};
+        if (launch_split(reinterpret_cast<const void *>(k_sinkhorn_bwd_ws), args, d, K, s))
+            return hipSuccess;
+    }
     hipLaunchKernelGGL(k_sinkhorn_bwd_w, dim3(d.B), dim3(kT), 0, s, d);
     return hipGetLastError();
 }
