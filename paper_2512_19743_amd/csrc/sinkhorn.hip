@@ -1050,42 +1050,47 @@ __device__ bool split_begin(uint32_t *sync, int K, int k, unsigned int *err, int
     return true;
 }
 
-// One word through the L2 only: the load skips the CU's cache (sc0). Its
-// result is not waited for here (see split_gather).
-__device__ __forceinline__ uint64_t load_l2(const void *p)
-{
-    uint64_t v;
-    asm volatile("global_load_dwordx2 %0, %1, off sc0" : "=v"(v) : "v"(p) : "memory");
-    return v;
-}
+// Eight published words at byte offsets off[0..7] from the sample's base
+// (uniform, in scalar registers), and the wait for them, in one asm
+// statement, so that no use of a result can be placed before the wait: through
+// the L2 only (sc0, the loads skip the CU's cache) when local, else from
+// memory past the L2s (sc1, as relaxed device-scope atomic loads).
+#define APML_LOAD8(BITS)                                                                                      \
+    asm volatile("global_load_dwordx2 %0, %8, %16 " BITS "\n\t"                                           \
+                 "global_load_dwordx2 %1, %9, %16 " BITS "\n\t"                                           \
+                 "global_load_dwordx2 %2, %10, %16 " BITS "\n\t"                                          \
+                 "global_load_dwordx2 %3, %11, %16 " BITS "\n\t"                                          \
+                 "global_load_dwordx2 %4, %12, %16 " BITS "\n\t"                                          \
+                 "global_load_dwordx2 %5, %13, %16 " BITS "\n\t"                                          \
+                 "global_load_dwordx2 %6, %14, %16 " BITS "\n\t"                                          \
+                 "global_load_dwordx2 %7, %15, %16 " BITS "\n\t"                                          \
+                 "s_waitcnt vmcnt(0)"                                                                         \
+                 : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(v[5]), "=&v"(v[6]), \
+                   "=&v"(v[7])                                                                                \
+                 : "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3]), "v"(off[4]), "v"(off[5]), "v"(off[6]),  \
+                   "v"(off[7]), "s"(base)                                                                     \
+                 : "memory")
 
-// The sample's n published 64-bit words into LDS, all of a thread's loads
-// issued before the first is used.
+// The sample's n published 64-bit words into LDS. Every lane loads eight
+// words; offsets past the n-th word are clamped to it (read, not used).
 template <typename T> __device__ __forceinline__ void split_gather(T *lds, const T *g, int n, bool local)
 {
     static_assert(kSinkOwnersW / kT == 8, "eight words per thread");
-    uint64_t v[8] = {};
-    if (local) {
+    // the base in scalar registers: each 32-bit half read from the first lane
+    // (the builtin takes 32-bit values; a 64-bit argument would be cut)
+    const uint64_t a = (uint64_t)(uintptr_t)g;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+    const void *base = reinterpret_cast<const void *>((uintptr_t)(((uint64_t)hi << 32) | lo));
+    uint32_t off[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int o = u * kT + (int)threadIdx.x;
-            if (o < n)
-                v[u] = load_l2(g + o);
-        }
-        // the wait names the loaded registers, so no use is scheduled before it
-        asm volatile("s_waitcnt vmcnt(0)"
-                     : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]), "+v"(v[7])
-                     :
-                     : "memory");
-    } else {
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int o = u * kT + (int)threadIdx.x;
-            if (o < n)
-                v[u] = __hip_atomic_load(reinterpret_cast<const uint64_t *>(g + o), __ATOMIC_RELAXED,
-                                         __HIP_MEMORY_SCOPE_AGENT);
-        }
-    }
+    for (int u = 0; u < 8; ++u)
+        off[u] = (uint32_t)min(u * kT + (int)threadIdx.x, n - 1) * 8u;
+    uint64_t v[8];
+    if (local)
+        APML_LOAD8("sc0");
+    else
+        APML_LOAD8("sc1");
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
         const int o = u * kT + (int)threadIdx.x;
@@ -1093,6 +1098,7 @@ template <typename T> __device__ __forceinline__ void split_gather(T *lds, const
             lds[o] = __builtin_bit_cast(T, v[u]);
     }
 }
+#undef APML_LOAD8
 
 __global__ __launch_bounds__(kT) void k_sinkhorn_fwd_ws(DevPlan d, double eps, int K)
 {
@@ -1184,6 +1190,251 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_ws(DevPlan d, int K)
         lds_barrier();
     }
     wide_reverse_end(d, b, n_row, fc, k, K);
+}
+
+// Register-resident split kernels: when a workgroup's share is at most SW
+// slots per lane and order, its pieces (and in the reverse kernel both
+// adjoint copies of its positions) are loaded once and kept in registers for
+// every sweep, so a half-sweep reads nothing from memory but the owners'
+// saved scalings and the exchanged vector. Same lanes, same arithmetic in the
+// same order as the streamed kernels: the same bits.
+constexpr int kSplitRegFwd = 4; // slots per lane and order held by the forward kernel
+constexpr int kSplitRegBwd = 2; // and by the reverse kernel
+
+// Slots of the calling wave that workgroup k of K takes (wave-uniform).
+__device__ __forceinline__ int split_slots(int n_used, int k, int K)
+{
+    const int ns = wave_slots(n_used);
+    return ns > k ? (ns - k + K - 1) / K : 0;
+}
+
+template <int SW> __device__ __forceinline__ void load_my_slots(WSlot (&w)[SW], const WideOrder &pk, int b, int n, int k,
+                                                              int K)
+{
+#pragma unroll
+    for (int q = 0; q < SW; ++q)
+        if (q < n)
+            w[q] = load_wslot(pk, b, k + q * K);
+}
+
+// One forward half-sweep over the slots held in registers (as wide_sweep).
+template <int SW>
+__device__ __forceinline__ void reg_sweep(const WSlot (&w)[SW], int n, const double *vals, const double *own, double eps,
+                                          double *g_val, bool local)
+{
+#pragma unroll
+    for (int q = 0; q < SW; ++q) {
+        if (q >= n)
+            break;
+        const Unpack u = Unpack::make();
+        double g[kP];
+#pragma unroll
+        for (int e = 0; e < kP; ++e)
+            g[e] = lds_at<double>(vals, u.half(w[q].gi[e / 2], e));
+        double acc = (double)w[q].p0[0] * g[0];
+#pragma unroll
+        for (int e = 1; e < kP; ++e)
+            acc = __builtin_fma((double)w[q].p0[e], g[e], acc);
+        acc = group_reduce_lg(acc, (int)u.bits(w[q].info, 13, 3));
+        if (u.bits(w[q].info, 16, 2) == 3u) { // head and valid
+            const int o = (int)u.bits(w[q].info, 0, 13);
+            const double c = own[o];
+            publish64(g_val + o, __builtin_bit_cast(uint64_t, quotient(c, c * acc + eps)), local);
+        }
+    }
+}
+
+template <int SW> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd_wr(DevPlan d, double eps, int K)
+{
+    __shared__ double va[kSinkOwnersW], vb[kSinkOwnersW], part[kT / 64];
+    __shared__ int stop, local;
+    int b, k;
+    split_member(blockIdx.x, d.B, K, b, k);
+    const int tid = threadIdx.x;
+    const int N = d.N, M = d.M, L = d.L;
+    const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
+    uint32_t *cnt = d.split_sync + ((size_t)b * 2 + 0) * kSplitSyncStride;
+    const int mr = split_slots(__builtin_amdgcn_readfirstlane(d.wk_row.n_pos[b]), k, K);
+    const int mc = split_slots(__builtin_amdgcn_readfirstlane(d.wk_col.n_pos[b]), k, K);
+    WSlot pr[SW], pc[SW];
+    load_my_slots(pr, d.wk_row, b, mr, k, K);
+    load_my_slots(pc, d.wk_col, b, mc, k, K);
+    for (int o = tid; o < N; o += kT) {
+        va[o] = 1.0;
+        if (k == 0)
+            d.alpha[(size_t)b * N + o] = 1.0;
+    }
+    for (int o = tid; o < M; o += kT) {
+        vb[o] = 1.0;
+        if (k == 0)
+            d.beta[(size_t)b * M + o] = 1.0;
+    }
+    if (tid == 0)
+        stop = 0;
+    lds_barrier();
+    if (!split_begin(cnt, K, k, &d.ctr->error, &stop, &local))
+        return;
+    const bool loc = local != 0;
+    uint32_t t = 1;
+    for (int l = 1; l <= L; ++l) {
+        double *gb = d.beta + l * BM + (size_t)b * M;
+        reg_sweep(pc, mc, va, vb, eps, gb, loc); // Eq. 3
+        if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
+            return;
+        split_gather(vb, gb, M, loc);
+        lds_barrier();
+        double *ga = d.alpha + l * BN + (size_t)b * N;
+        reg_sweep(pr, mr, vb, va, eps, ga, loc); // Eq. 4
+        if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
+            return;
+        split_gather(va, ga, N, loc);
+        lds_barrier();
+    }
+    if (k == 0)
+        sample_loss(d, b, d.row_ptr[(size_t)b * N], d.row_ptr[(size_t)(b + 1) * N], va, vb, part);
+}
+
+// One reverse half-sweep over the slots held in registers (as wide_reverse),
+// with the owners' saved scalings al (iteration l) and alp (l - 1) loaded
+// beforehand.
+template <int SW>
+__device__ __forceinline__ void reg_reverse(const WSlot (&w)[SW], float (&cp)[SW][kP], int n, const double (&al)[SW],
+                                            const double (&alp)[SW], const float2 *fin, float2 *fout, bool local)
+{
+#pragma unroll
+    for (int q = 0; q < SW; ++q) {
+        if (q >= n)
+            break;
+        const Unpack u = Unpack::make();
+        const int o = (int)u.bits(w[q].info, 0, 13);
+        float2 f[kP];
+#pragma unroll
+        for (int e = 0; e < kP; ++e)
+            f[e] = lds_at<float2>(fin, u.half(w[q].gi[e / 2], e));
+        double rho[kP], acc = 0.0;
+#pragma unroll
+        for (int e = 0; e < kP; ++e) {
+            rho[e] = (double)cp[q][e] - (double)f[e].x;
+            const double p0 = (double)w[q].p0[e];
+            acc = e == 0 ? rho[e] * p0 : __builtin_fma(rho[e], p0, acc);
+        }
+        const double dsum = al[q] * group_reduce_lg(acc, (int)u.bits(w[q].info, 13, 3));
+        const double qt = quotient(al[q], alp[q]);
+#pragma unroll
+        for (int e = 0; e < kP; ++e)
+            cp[q][e] = w[q].p0[e] != 0.0f ? (float)((rho[e] - dsum * (double)f[e].y) * qt) : 0.0f;
+        if (u.bits(w[q].info, 16, 2) == 3u) // head and valid
+            publish64(fout + o, __builtin_bit_cast(uint64_t, make_float2((float)(dsum * al[q]), (float)alp[q])), local);
+    }
+}
+
+// The owners' saved scalings of iteration l and l - 1 for the slots held.
+template <int SW>
+__device__ __forceinline__ void owner_scalings(const WSlot (&w)[SW], int n, const double *own_l, const double *own_prev,
+                                               double (&al)[SW], double (&alp)[SW])
+{
+#pragma unroll
+    for (int q = 0; q < SW; ++q)
+        if (q < n) {
+            const int o = (int)(w[q].info & 0x1FFFu);
+            al[q] = own_l[o];
+            alp[q] = own_prev[o];
+        }
+}
+
+template <int SW> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_wr(DevPlan d, int K)
+{
+    __shared__ float2 fr[kSinkOwnersW]; // row factors (Yr_i, alpha^(l-1)_i)
+    __shared__ float2 fc[kSinkOwnersW]; // column factors (Yc_j, beta^(l-1)_j)
+    __shared__ int stop, local;
+    int b, k;
+    split_member(blockIdx.x, d.B, K, b, k);
+    const int tid = threadIdx.x;
+    const int N = d.N, M = d.M, L = d.L;
+    const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
+    const double *alpha = d.alpha + (size_t)b * N, *beta = d.beta + (size_t)b * M; // + l * BN, + l * BM
+    uint32_t *cnt = d.split_sync + ((size_t)b * 2 + 1) * kSplitSyncStride;
+    float2 *xr = d.xr2 + (size_t)b * N, *xc = d.xc2 + (size_t)b * M;
+    const int mr = split_slots(__builtin_amdgcn_readfirstlane(d.wk_row.n_pos[b]), k, K);
+    const int mc = split_slots(__builtin_amdgcn_readfirstlane(d.wk_col.n_pos[b]), k, K);
+    WSlot pr[SW], pc[SW];
+    load_my_slots(pr, d.wk_row, b, mr, k, K);
+    load_my_slots(pc, d.wk_col, b, mc, k, K);
+    // the copies start as grad_loss C beta^L_j (rows) and grad_loss C alpha^L_i (columns)
+    float rr[SW][kP], rc[SW][kP];
+    {
+        const float *xb = d.x + (size_t)b * N * 3, *yb = d.y + (size_t)b * M * 3;
+        const double gl = d.grad_loss[b];
+        const Unpack u = Unpack::make();
+#pragma unroll
+        for (int q = 0; q < SW; ++q) {
+#pragma unroll
+            for (int e = 0; e < kP; ++e) {
+                rr[q][e] = 0.0f;
+                rc[q][e] = 0.0f;
+            }
+            if (q < mr) {
+                const int i = (int)u.bits(pr[q].info, 0, 13);
+#pragma unroll
+                for (int e = 0; e < kP; ++e) {
+                    const int j = (int)(u.half(pr[q].gi[e / 2], e) >> 3);
+                    if (pr[q].p0[e] != 0.0f)
+                        rr[q][e] = (float)(gl * dist_f64(xb + 3 * i, yb + 3 * j) * beta[(size_t)L * BM + j]);
+                }
+            }
+            if (q < mc) {
+                const int j = (int)u.bits(pc[q].info, 0, 13);
+#pragma unroll
+                for (int e = 0; e < kP; ++e) {
+                    const int i = (int)(u.half(pc[q].gi[e / 2], e) >> 3);
+                    if (pc[q].p0[e] != 0.0f)
+                        rc[q][e] = (float)(gl * dist_f64(xb + 3 * i, yb + 3 * j) * alpha[(size_t)L * BN + i]);
+                }
+            }
+        }
+    }
+    for (int o = tid; o < M; o += kT) // no pending column update before row phase L
+        fc[o] = make_float2(0.0f, (float)beta[(size_t)L * BM + o]);
+    if (tid == 0)
+        stop = 0;
+    lds_barrier();
+    if (!split_begin(cnt, K, k, &d.ctr->error, &stop, &local))
+        return;
+    const bool loc = local != 0;
+    uint32_t t = 1;
+    for (int l = L; l >= 1; --l) {
+        double al[SW] = {}, alp[SW] = {};
+        owner_scalings(pr, mr, alpha + l * BN, alpha + (l - 1) * BN, al, alp);
+        reg_reverse(pr, rr, mr, al, alp, fc, xr, loc); // reverse of Eq. 4
+        if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
+            return;
+        split_gather(fr, xr, N, loc);
+        lds_barrier();
+        owner_scalings(pc, mc, beta + l * BM, beta + (l - 1) * BM, al, alp);
+        reg_reverse(pc, rc, mc, al, alp, fr, xc, loc); // reverse of Eq. 3
+        if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
+            return;
+        split_gather(fc, xc, M, loc);
+        lds_barrier();
+    }
+    // the adjoint with respect to P0, r - Yc_j, in row-major order
+    {
+        const Unpack u = Unpack::make();
+#pragma unroll
+        for (int q = 0; q < SW; ++q) {
+            if (q >= mr || u.bits(pr[q].info, 17, 1) == 0u)
+                continue;
+            const int i = (int)u.bits(pr[q].info, 0, 13), lg = (int)u.bits(pr[q].info, 13, 3);
+            const int p = (k + q * K) * kT + tid, qq = p & ((1 << lg) - 1); // groups are aligned to their size
+            const int r0 = d.row_ptr[(size_t)b * N + i], len = d.row_ptr[(size_t)b * N + i + 1] - r0;
+#pragma unroll
+            for (int e = 0; e < kP; ++e)
+                if (qq * kP + e < len) {
+                    const float2 f = lds_at<float2>(fc, u.half(pr[q].gi[e / 2], e));
+                    d.adj[r0 + qq * kP + e] = (double)rr[q][e] - (double)f.x;
+                }
+        }
+    }
 }
 
 __global__ __launch_bounds__(kBlock) void k_zero_u32(uint32_t *a, int n)
@@ -1544,6 +1795,29 @@ bool launch_split(const void *kernel, void **args, const DevPlan &d, int K, hipS
     return true;
 }
 
+// The split kernel for a workgroup share of sw slots per lane and order:
+// registers up to the limit, else streamed.
+const void *split_fwd_kernel(int sw)
+{
+    switch (sw) {
+    case 1: return reinterpret_cast<const void *>(k_sinkhorn_fwd_wr<1>);
+    case 2: return reinterpret_cast<const void *>(k_sinkhorn_fwd_wr<2>);
+    case 3: return reinterpret_cast<const void *>(k_sinkhorn_fwd_wr<3>);
+    case 4: return reinterpret_cast<const void *>(k_sinkhorn_fwd_wr<4>);
+    default: return reinterpret_cast<const void *>(k_sinkhorn_fwd_ws);
+    }
+}
+
+const void *split_bwd_kernel(int sw)
+{
+    switch (sw) {
+    case 1: return reinterpret_cast<const void *>(k_sinkhorn_bwd_wr<1>);
+    case 2: return reinterpret_cast<const void *>(k_sinkhorn_bwd_wr<2>);
+    default: return reinterpret_cast<const void *>(k_sinkhorn_bwd_ws);
+    }
+}
+static_assert(kSplitRegFwd == 4 && kSplitRegBwd == 2, "instances above");
+
 } // namespace
 
 hipError_t launch_sinkhorn_fwd_wide(const DevPlan &d, double eps, hipStream_t s)
@@ -1553,7 +1827,7 @@ hipError_t launch_sinkhorn_fwd_wide(const DevPlan &d, double eps, hipStream_t s)
         DevPlan dc = d;
         double e = eps;
         void *args[] = {&dc, &e, &K};
-        if (launch_split(reinterpret_cast<const void *>(k_sinkhorn_fwd_ws), args, d, K, s))
+        if (launch_split(split_fwd_kernel((d.wk_row.slots + K - 1) / K), args, d, K, s))
             return hipSuccess;
     }
     hipLaunchKernelGGL(k_sinkhorn_fwd_w, dim3(d.B), dim3(kT), 0, s, d, eps);
@@ -1566,7 +1840,7 @@ hipError_t launch_sinkhorn_bwd_wide(const DevPlan &d, hipStream_t s)
     if (K > 1 && d.split_sync && d.xr2 && d.xc2) {
         DevPlan dc = d;
         void *args[] = {&dc, &K};
-        if (launch_split(reinterpret_cast<const void *>(k_sinkhorn_bwd_ws), args, d, K, s))
+        if (launch_split(split_bwd_kernel((d.wk_row.slots + K - 1) / K), args, d, K, s))
             return hipSuccess;
     }
     hipLaunchKernelGGL(k_sinkhorn_bwd_w, dim3(d.B), dim3(kT), 0, s, d);
