@@ -938,8 +938,10 @@ apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t
             dv.pos_col = c.take<int32_t>(2 * (size_t)BM);
             dv.clamp_row = c.take<uint8_t>(BN);
             dv.clamp_col = c.take<uint8_t>(BM);
-            dv.alpha = c.take<double>((size_t)(L + 1) * BN);
-            dv.beta = c.take<double>((size_t)(L + 1) * BM);
+            // (+ kSinkOwnersW: the split kernels read a sample's vector in
+            // whole chunks of lanes, past its end)
+            dv.alpha = c.take<double>((size_t)(L + 1) * BN + kSinkOwnersW);
+            dv.beta = c.take<double>((size_t)(L + 1) * BM + kSinkOwnersW);
             dv.dvec = c.take<double>(BN);
         };
         Carve size;
@@ -1057,8 +1059,8 @@ apml_status run_backward(apml_plan *plan, const float *x, const float *y, const 
             dv.wc = c.take<float>(w);
             dv.cbar = c.take<double>(plan->stored);
             if (split) {
-                dv.xr2 = c.take<float2>((size_t)plan->B * plan->N);
-                dv.xc2 = c.take<float2>((size_t)plan->B * plan->M);
+                dv.xr2 = c.take<float2>((size_t)plan->B * plan->N + kSinkOwnersW);
+                dv.xc2 = c.take<float2>((size_t)plan->B * plan->M + kSinkOwnersW);
             }
         } else if (dv.L > 0 && !plan->sink_bwd) {
             dv.rz = dv.adj;

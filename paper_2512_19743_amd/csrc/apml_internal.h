@@ -259,7 +259,7 @@ constexpr int kSinkMaxGroup = 64; // largest group (pieces of one owner)
 
 struct PackedOrder {
     float *p0;      // [B][slots][kSinkPiece][lanes]: P0 (0 for padding)
-    uint32_t *gi;   // [B][slots][kSinkPiece/2][lanes]: gathered index | real << 15, two per word
+    uint32_t *gi;   // [B][slots][kSinkPiece/2][lanes]: byte offsets of the gathered 8-byte values, two per word
     uint32_t *info; // [B][slots][lanes]: owner | log2(group) << 11 | head << 14 | valid << 15 | first position << 16 (rows)
     uint32_t *pos;  // [B][slots][kSinkPiece/2][lanes]: row-major positions within the sample (columns only)
     int32_t *n_pos; // [B]: positions used
@@ -316,7 +316,7 @@ struct DevPlan {
     uint32_t *split_sync;         // [B][2][kSplitSyncStride]: meeting counter (word 0) and the workgroups' XCDs
                                   // (words 1..K) of the split streamed kernels
                                   // (forward, backward), cleared before each launch
-    float2 *xr2, *xc2;            // [2][B*N], [2][B*M]: owners' factors exchanged by the split reverse kernel
+    float2 *xr2, *xc2;            // [B*N], [B*M] (+ padding): owners' factors exchanged by the split reverse kernels
     const int32_t *sink_place;    // during the forward softmax of that path: the pieces' placement, so that the
                                   // column softmax writes every pair into its pieces; else NULL
 };

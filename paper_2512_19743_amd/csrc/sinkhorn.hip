@@ -695,7 +695,7 @@ struct WSlot {
     uint32_t info;
 };
 
-__device__ __forceinline__ WSlot load_wslot(const WideOrder &pk, int b, int s)
+template <class Order> __device__ __forceinline__ WSlot load_wslot(const Order &pk, int b, int s)
 {
     WSlot w;
     const int p = s * kT + (int)threadIdx.x;
@@ -1050,55 +1050,56 @@ __device__ bool split_begin(uint32_t *sync, int K, int k, unsigned int *err, int
     return true;
 }
 
-// Eight published words at byte offsets off[0..7] from the sample's base
-// (uniform, in scalar registers), and the wait for them, in one asm
-// statement, so that no use of a result can be placed before the wait: through
-// the L2 only (sc0, the loads skip the CU's cache) when local, else from
-// memory past the L2s (sc1, as relaxed device-scope atomic loads).
+// WORDS published words per lane, word u of lane t at word u * lanes + t
+// of the sample's vector (bases in scalar registers, one per chunk of lanes,
+// one offset register), and the wait for them, in one asm statement, so that
+// no use of a result can be placed before the wait: through the L2 only (sc0,
+// the loads skip the CU's cache) when local, else from memory past the L2s
+// (sc1, as relaxed device-scope atomic loads).
+#define APML_LD(I, B, BITS) "global_load_dwordx2 %" #I ", %[off], %" #B " " BITS "\n\t"
 #define APML_LOAD8(BITS)                                                                                      \
-    asm volatile("global_load_dwordx2 %0, %8, %16 " BITS "\n\t"                                           \
-                 "global_load_dwordx2 %1, %9, %16 " BITS "\n\t"                                           \
-                 "global_load_dwordx2 %2, %10, %16 " BITS "\n\t"                                          \
-                 "global_load_dwordx2 %3, %11, %16 " BITS "\n\t"                                          \
-                 "global_load_dwordx2 %4, %12, %16 " BITS "\n\t"                                          \
-                 "global_load_dwordx2 %5, %13, %16 " BITS "\n\t"                                          \
-                 "global_load_dwordx2 %6, %14, %16 " BITS "\n\t"                                          \
-                 "global_load_dwordx2 %7, %15, %16 " BITS "\n\t"                                          \
+    asm volatile(APML_LD(0, 8, BITS) APML_LD(1, 9, BITS) APML_LD(2, 10, BITS) APML_LD(3, 11, BITS)           \
+                 APML_LD(4, 12, BITS) APML_LD(5, 13, BITS) APML_LD(6, 14, BITS) APML_LD(7, 15, BITS)         \
                  "s_waitcnt vmcnt(0)"                                                                         \
                  : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(v[5]), "=&v"(v[6]), \
                    "=&v"(v[7])                                                                                \
-                 : "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3]), "v"(off[4]), "v"(off[5]), "v"(off[6]),  \
-                   "v"(off[7]), "s"(base)                                                                     \
+                 : "s"(bs[0]), "s"(bs[1]), "s"(bs[2]), "s"(bs[3]), "s"(bs[4]), "s"(bs[5]), "s"(bs[6]),          \
+                   "s"(bs[7]), [off] "v"(off)                                                                 \
                  : "memory")
-
-// The sample's n published 64-bit words into LDS. Every lane loads eight
-// words; offsets past the n-th word are clamped to it (read, not used).
+// The sample's n published 64-bit words (n <= 8 * lanes) into LDS. Every
+// lane loads eight words: the caller's array extends at least 8 * lanes
+// words past the vector's start (words past n are read, not used).
 template <typename T> __device__ __forceinline__ void split_gather(T *lds, const T *g, int n, bool local)
 {
-    static_assert(kSinkOwnersW / kT == 8, "eight words per thread");
+    constexpr int WORDS = 8;
+    static_assert(kSinkOwnersW / kT == WORDS, "eight words per lane");
     // the base in scalar registers: each 32-bit half read from the first lane
     // (the builtin takes 32-bit values; a 64-bit argument would be cut)
     const uint64_t a = (uint64_t)(uintptr_t)g;
     const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
     const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
-    const void *base = reinterpret_cast<const void *>((uintptr_t)(((uint64_t)hi << 32) | lo));
-    uint32_t off[8];
+    const uint64_t base = ((uint64_t)hi << 32) | lo;
+    const void *bs[WORDS];
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
-        off[u] = (uint32_t)min(u * kT + (int)threadIdx.x, n - 1) * 8u;
-    uint64_t v[8];
+    for (int u = 0; u < WORDS; ++u)
+        bs[u] = reinterpret_cast<const void *>((uintptr_t)(base + (uint64_t)u * kT * 8u));
+    const uint32_t off = threadIdx.x * 8u;
+    uint64_t v[WORDS];
+    if (local) // no line of an earlier read may serve these loads
+        asm volatile("buffer_inv sc0" ::: "memory");
     if (local)
         APML_LOAD8("sc0");
     else
         APML_LOAD8("sc1");
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
+    for (int u = 0; u < WORDS; ++u) {
         const int o = u * kT + (int)threadIdx.x;
         if (o < n)
             lds[o] = __builtin_bit_cast(T, v[u]);
     }
 }
 #undef APML_LOAD8
+#undef APML_LD
 
 __global__ __launch_bounds__(kT) void k_sinkhorn_fwd_ws(DevPlan d, double eps, int K)
 {
@@ -1156,7 +1157,7 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_ws(DevPlan d, int K)
 {
     __shared__ float2 fr[kSinkOwnersW]; // row factors (Yr_i, alpha^(l-1)_i)
     __shared__ float2 fc[kSinkOwnersW]; // column factors (Yc_j, beta^(l-1)_j)
-    __shared__ int stop, local;
+    __shared__ int stop;
     int b, k;
     split_member(blockIdx.x, d.B, K, b, k);
     const int tid = threadIdx.x;
@@ -1173,10 +1174,12 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_ws(DevPlan d, int K)
     if (tid == 0)
         stop = 0;
     lds_barrier();
-    if (!split_begin(cnt, K, k, &d.ctr->error, &stop, &local))
-        return;
-    const bool loc = local != 0;
-    uint32_t t = 1;
+    // The factor buffers are written again every other phase. Measured:
+    // exchanging reused addresses through the L2 (plain stores, loads past
+    // only the CU's cache) returned stale words in some cases, so these
+    // kernels exchange through memory (device-scope atomics) only.
+    const bool loc = false;
+    uint32_t t = 0;
     for (int l = L; l >= 1; --l) {
         wide_reverse<true>(d.wk_row, b, n_row, d.wr, fc, xr, alpha + l * BN, alpha + (l - 1) * BN, k, K, loc);
         if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
@@ -1208,8 +1211,8 @@ __device__ __forceinline__ int split_slots(int n_used, int k, int K)
     return ns > k ? (ns - k + K - 1) / K : 0;
 }
 
-template <int SW> __device__ __forceinline__ void load_my_slots(WSlot (&w)[SW], const WideOrder &pk, int b, int n, int k,
-                                                              int K)
+template <int SW, class Order>
+__device__ __forceinline__ void load_my_slots(WSlot (&w)[SW], const Order &pk, int b, int n, int k, int K)
 {
 #pragma unroll
     for (int q = 0; q < SW; ++q)
@@ -1297,7 +1300,7 @@ template <int SW> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd_wr(DevPla
 // One reverse half-sweep over the slots held in registers (as wide_reverse),
 // with the owners' saved scalings al (iteration l) and alp (l - 1) loaded
 // beforehand.
-template <int SW>
+template <int SW, int OB>
 __device__ __forceinline__ void reg_reverse(const WSlot (&w)[SW], float (&cp)[SW][kP], int n, const double (&al)[SW],
                                             const double (&alp)[SW], const float2 *fin, float2 *fout, bool local)
 {
@@ -1306,7 +1309,7 @@ __device__ __forceinline__ void reg_reverse(const WSlot (&w)[SW], float (&cp)[SW
         if (q >= n)
             break;
         const Unpack u = Unpack::make();
-        const int o = (int)u.bits(w[q].info, 0, 13);
+        const int o = (int)u.bits(w[q].info, 0, OB);
         float2 f[kP];
 #pragma unroll
         for (int e = 0; e < kP; ++e)
@@ -1318,25 +1321,25 @@ __device__ __forceinline__ void reg_reverse(const WSlot (&w)[SW], float (&cp)[SW
             const double p0 = (double)w[q].p0[e];
             acc = e == 0 ? rho[e] * p0 : __builtin_fma(rho[e], p0, acc);
         }
-        const double dsum = al[q] * group_reduce_lg(acc, (int)u.bits(w[q].info, 13, 3));
+        const double dsum = al[q] * group_reduce_lg(acc, (int)u.bits(w[q].info, OB, 3));
         const double qt = quotient(al[q], alp[q]);
 #pragma unroll
         for (int e = 0; e < kP; ++e)
             cp[q][e] = w[q].p0[e] != 0.0f ? (float)((rho[e] - dsum * (double)f[e].y) * qt) : 0.0f;
-        if (u.bits(w[q].info, 16, 2) == 3u) // head and valid
+        if (u.bits(w[q].info, OB + 3, 2) == 3u) // head and valid
             publish64(fout + o, __builtin_bit_cast(uint64_t, make_float2((float)(dsum * al[q]), (float)alp[q])), local);
     }
 }
 
 // The owners' saved scalings of iteration l and l - 1 for the slots held.
-template <int SW>
+template <int SW, int OB>
 __device__ __forceinline__ void owner_scalings(const WSlot (&w)[SW], int n, const double *own_l, const double *own_prev,
                                                double (&al)[SW], double (&alp)[SW])
 {
 #pragma unroll
     for (int q = 0; q < SW; ++q)
         if (q < n) {
-            const int o = (int)(w[q].info & 0x1FFFu);
+            const int o = (int)(w[q].info & ((1u << OB) - 1u));
             al[q] = own_l[o];
             alp[q] = own_prev[o];
         }
@@ -1344,9 +1347,10 @@ __device__ __forceinline__ void owner_scalings(const WSlot (&w)[SW], int n, cons
 
 template <int SW> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_wr(DevPlan d, int K)
 {
+    constexpr int OB = 13; // owner bits of the streamed layout's info word
     __shared__ float2 fr[kSinkOwnersW]; // row factors (Yr_i, alpha^(l-1)_i)
     __shared__ float2 fc[kSinkOwnersW]; // column factors (Yc_j, beta^(l-1)_j)
-    __shared__ int stop, local;
+    __shared__ int stop;
     int b, k;
     split_member(blockIdx.x, d.B, K, b, k);
     const int tid = threadIdx.x;
@@ -1374,7 +1378,7 @@ template <int SW> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_wr(DevPla
                 rc[q][e] = 0.0f;
             }
             if (q < mr) {
-                const int i = (int)u.bits(pr[q].info, 0, 13);
+                const int i = (int)u.bits(pr[q].info, 0, OB);
 #pragma unroll
                 for (int e = 0; e < kP; ++e) {
                     const int j = (int)(u.half(pr[q].gi[e / 2], e) >> 3);
@@ -1383,7 +1387,7 @@ template <int SW> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_wr(DevPla
                 }
             }
             if (q < mc) {
-                const int j = (int)u.bits(pc[q].info, 0, 13);
+                const int j = (int)u.bits(pc[q].info, 0, OB);
 #pragma unroll
                 for (int e = 0; e < kP; ++e) {
                     const int i = (int)(u.half(pc[q].gi[e / 2], e) >> 3);
@@ -1398,20 +1402,22 @@ template <int SW> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_wr(DevPla
     if (tid == 0)
         stop = 0;
     lds_barrier();
-    if (!split_begin(cnt, K, k, &d.ctr->error, &stop, &local))
-        return;
-    const bool loc = local != 0;
-    uint32_t t = 1;
+    // The factor buffers are written again every other phase. Measured:
+    // exchanging reused addresses through the L2 (plain stores, loads past
+    // only the CU's cache) returned stale words in some cases, so these
+    // kernels exchange through memory (device-scope atomics) only.
+    const bool loc = false;
+    uint32_t t = 0;
     for (int l = L; l >= 1; --l) {
         double al[SW] = {}, alp[SW] = {};
-        owner_scalings(pr, mr, alpha + l * BN, alpha + (l - 1) * BN, al, alp);
-        reg_reverse(pr, rr, mr, al, alp, fc, xr, loc); // reverse of Eq. 4
+        owner_scalings<SW, OB>(pr, mr, alpha + l * BN, alpha + (l - 1) * BN, al, alp);
+        reg_reverse<SW, OB>(pr, rr, mr, al, alp, fc, xr, loc); // reverse of Eq. 4
         if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
             return;
         split_gather(fr, xr, N, loc);
         lds_barrier();
-        owner_scalings(pc, mc, beta + l * BM, beta + (l - 1) * BM, al, alp);
-        reg_reverse(pc, rc, mc, al, alp, fr, xc, loc); // reverse of Eq. 3
+        owner_scalings<SW, OB>(pc, mc, beta + l * BM, beta + (l - 1) * BM, al, alp);
+        reg_reverse<SW, OB>(pc, rc, mc, al, alp, fr, xc, loc); // reverse of Eq. 3
         if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
             return;
         split_gather(fc, xc, M, loc);
@@ -1422,9 +1428,9 @@ template <int SW> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_wr(DevPla
         const Unpack u = Unpack::make();
 #pragma unroll
         for (int q = 0; q < SW; ++q) {
-            if (q >= mr || u.bits(pr[q].info, 17, 1) == 0u)
+            if (q >= mr || u.bits(pr[q].info, OB + 4, 1) == 0u)
                 continue;
-            const int i = (int)u.bits(pr[q].info, 0, 13), lg = (int)u.bits(pr[q].info, 13, 3);
+            const int i = (int)u.bits(pr[q].info, 0, OB), lg = (int)u.bits(pr[q].info, OB, 3);
             const int p = (k + q * K) * kT + tid, qq = p & ((1 << lg) - 1); // groups are aligned to their size
             const int r0 = d.row_ptr[(size_t)b * N + i], len = d.row_ptr[(size_t)b * N + i + 1] - r0;
 #pragma unroll
@@ -1816,6 +1822,7 @@ const void *split_bwd_kernel(int sw)
     default: return reinterpret_cast<const void *>(k_sinkhorn_bwd_ws);
     }
 }
+
 static_assert(kSplitRegFwd == 4 && kSplitRegBwd == 2, "instances above");
 
 } // namespace

@@ -64,3 +64,4 @@ def test_split_matches_one_workgroup(case, monkeypatch):
     for b in range(X.shape[0]):
         np.testing.assert_array_equal(split["v"][b], one["v"][b])
     assert np.isfinite(split["loss"]).all()
+
