@@ -1050,56 +1050,66 @@ __device__ bool split_begin(uint32_t *sync, int K, int k, unsigned int *err, int
     return true;
 }
 
-// WORDS published words per lane, word u of lane t at word u * lanes + t
-// of the sample's vector (bases in scalar registers, one per chunk of lanes,
-// one offset register), and the wait for them, in one asm statement, so that
-// no use of a result can be placed before the wait: through the L2 only (sc0,
-// the loads skip the CU's cache) when local, else from memory past the L2s
-// (sc1, as relaxed device-scope atomic loads).
-#define APML_LD(I, B, BITS) "global_load_dwordx2 %" #I ", %[off], %" #B " " BITS "\n\t"
-#define APML_LOAD8(BITS)                                                                                      \
-    asm volatile(APML_LD(0, 8, BITS) APML_LD(1, 9, BITS) APML_LD(2, 10, BITS) APML_LD(3, 11, BITS)           \
-                 APML_LD(4, 12, BITS) APML_LD(5, 13, BITS) APML_LD(6, 14, BITS) APML_LD(7, 15, BITS)         \
-                 "s_waitcnt vmcnt(0)"                                                                         \
-                 : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(v[5]), "=&v"(v[6]), \
-                   "=&v"(v[7])                                                                                \
-                 : "s"(bs[0]), "s"(bs[1]), "s"(bs[2]), "s"(bs[3]), "s"(bs[4]), "s"(bs[5]), "s"(bs[6]),          \
-                   "s"(bs[7]), [off] "v"(off)                                                                 \
-                 : "memory")
-// The sample's n published 64-bit words (n <= 8 * lanes) into LDS. Every
-// lane loads eight words: the caller's array extends at least 8 * lanes
-// words past the vector's start (words past n are read, not used).
+// Eight published words per lane, word u of lane t at word u * lanes + t
+// of the sample's vector, and the wait for them, in one asm statement, so
+// that no use of a result can be placed before the wait.
+//  local: through the L2 only (sc0: the loads skip the CU's cache); each
+//  lane's offsets clamped to the vector's last word, so that no line outside
+//  the vector is brought into the CU's cache (see split_gather).
+//  else: from memory past the L2s (sc1, as relaxed device-scope atomic
+//  loads), one offset register and a scalar base per chunk of lanes; the
+//  caller's array extends 8 * lanes words past the vector's start.
+#define APML_LDL(I, J) "global_load_dwordx2 %" #I ", %" #J ", %[base] sc0\n\t"
+#define APML_LDM(I, B) "global_load_dwordx2 %" #I ", %[off], %" #B " sc1\n\t"
+#define APML_OUT8                                                                                             \
+    "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(v[5]), "=&v"(v[6]), "=&v"(v[7])
+
+// The sample's n published 64-bit words (n <= 8 * lanes) into LDS.
 template <typename T> __device__ __forceinline__ void split_gather(T *lds, const T *g, int n, bool local)
 {
-    constexpr int WORDS = 8;
-    static_assert(kSinkOwnersW / kT == WORDS, "eight words per lane");
+    static_assert(kSinkOwnersW / kT == 8, "eight words per lane");
     // the base in scalar registers: each 32-bit half read from the first lane
     // (the builtin takes 32-bit values; a 64-bit argument would be cut)
     const uint64_t a = (uint64_t)(uintptr_t)g;
     const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
     const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
     const uint64_t base = ((uint64_t)hi << 32) | lo;
-    const void *bs[WORDS];
+    uint64_t v[8];
+    if (local) {
+        uint32_t off[8];
 #pragma unroll
-    for (int u = 0; u < WORDS; ++u)
-        bs[u] = reinterpret_cast<const void *>((uintptr_t)(base + (uint64_t)u * kT * 8u));
-    const uint32_t off = threadIdx.x * 8u;
-    uint64_t v[WORDS];
-    if (local) // no line of an earlier read may serve these loads
-        asm volatile("buffer_inv sc0" ::: "memory");
-    if (local)
-        APML_LOAD8("sc0");
-    else
-        APML_LOAD8("sc1");
+        for (int u = 0; u < 8; ++u)
+            off[u] = (uint32_t)min(u * kT + (int)threadIdx.x, n - 1) * 8u;
+        asm volatile("buffer_inv sc0\n\t" // no line of an earlier read may serve these loads
+                     APML_LDL(0, 8) APML_LDL(1, 9) APML_LDL(2, 10) APML_LDL(3, 11) APML_LDL(4, 12) APML_LDL(5, 13)
+                     APML_LDL(6, 14) APML_LDL(7, 15) "s_waitcnt vmcnt(0)"
+                     : APML_OUT8
+                     : "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3]), "v"(off[4]), "v"(off[5]), "v"(off[6]),
+                       "v"(off[7]), [base] "s"(reinterpret_cast<const void *>((uintptr_t)base))
+                     : "memory");
+    } else {
+        const void *bs[8];
 #pragma unroll
-    for (int u = 0; u < WORDS; ++u) {
+        for (int u = 0; u < 8; ++u)
+            bs[u] = reinterpret_cast<const void *>((uintptr_t)(base + (uint64_t)u * kT * 8u));
+        const uint32_t off = threadIdx.x * 8u;
+        asm volatile(APML_LDM(0, 8) APML_LDM(1, 9) APML_LDM(2, 10) APML_LDM(3, 11) APML_LDM(4, 12)
+                         APML_LDM(5, 13) APML_LDM(6, 14) APML_LDM(7, 15) "s_waitcnt vmcnt(0)"
+                     : APML_OUT8
+                     : "s"(bs[0]), "s"(bs[1]), "s"(bs[2]), "s"(bs[3]), "s"(bs[4]), "s"(bs[5]), "s"(bs[6]),
+                       "s"(bs[7]), [off] "v"(off)
+                     : "memory");
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
         const int o = u * kT + (int)threadIdx.x;
         if (o < n)
             lds[o] = __builtin_bit_cast(T, v[u]);
     }
 }
-#undef APML_LOAD8
-#undef APML_LD
+#undef APML_OUT8
+#undef APML_LDM
+#undef APML_LDL
 
 __global__ __launch_bounds__(kT) void k_sinkhorn_fwd_ws(DevPlan d, double eps, int K)
 {
@@ -1201,7 +1211,7 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_ws(DevPlan d, int K)
 // every sweep, so a half-sweep reads nothing from memory but the owners'
 // saved scalings and the exchanged vector. Same lanes, same arithmetic in the
 // same order as the streamed kernels: the same bits.
-constexpr int kSplitRegFwd = 4; // slots per lane and order held by the forward kernel
+constexpr int kSplitRegFwd = 3; // slots per lane and order held by the forward kernel
 constexpr int kSplitRegBwd = 2; // and by the reverse kernel
 
 // Slots of the calling wave that workgroup k of K takes (wave-uniform).
@@ -1809,7 +1819,6 @@ const void *split_fwd_kernel(int sw)
     case 1: return reinterpret_cast<const void *>(k_sinkhorn_fwd_wr<1>);
     case 2: return reinterpret_cast<const void *>(k_sinkhorn_fwd_wr<2>);
     case 3: return reinterpret_cast<const void *>(k_sinkhorn_fwd_wr<3>);
-    case 4: return reinterpret_cast<const void *>(k_sinkhorn_fwd_wr<4>);
     default: return reinterpret_cast<const void *>(k_sinkhorn_fwd_ws);
     }
 }
@@ -1823,13 +1832,17 @@ const void *split_bwd_kernel(int sw)
     }
 }
 
-static_assert(kSplitRegFwd == 4 && kSplitRegBwd == 2, "instances above");
+static_assert(kSplitRegFwd == 3 && kSplitRegBwd == 2, "instances above");
 
 } // namespace
 
 hipError_t launch_sinkhorn_fwd_wide(const DevPlan &d, double eps, hipStream_t s)
 {
-    int K = sinkhorn_split_factor(d.B);
+    // a forward half-sweep over fewer slots is shorter than the meeting that
+    // splitting it needs (measured: 3000 to 4096 points per cloud, 4 to 6
+    // slots, 0.09 -> 0.13 ms; large-batch workload, 12 slots, 0.51 -> 0.35 ms)
+    constexpr int kSplitFwdMinSlots = 8;
+    int K = d.wk_row.slots >= kSplitFwdMinSlots ? sinkhorn_split_factor(d.B) : 1;
     if (K > 1 && d.split_sync) {
         DevPlan dc = d;
         double e = eps;

@@ -45,6 +45,14 @@ CASES = {
     "b16_n4096": lambda: custom(72, 16, 4096, 4096, reference="primitives", prediction="perm_noise", sigma=0.02),
     # the large-batch workload, 64 x 8192 x 8192: four per sample
     "large_batch": lambda: batch(config(3)),
+    # one sample, sizes not multiples of 16: the saved scalings of successive
+    # iterations share a cache line at every region boundary
+    "b1_n3000": lambda: custom(73, 1, 3000, 3001, reference="primitives", prediction="perm_noise", sigma=0.05),
+    # B N below 8192 words: a sample's whole-chunk reads would reach the next
+    # iteration's region
+    "b2_n3000": lambda: custom(74, 2, 3000, 2999, reference="primitives", prediction="perm_noise", sigma=0.05),
+    # one sample with enough pieces for the split forward kernel, B N < 8192
+    "b1_n8000": lambda: custom(75, 1, 8000, 7990, reference="primitives", prediction="perm_noise", sigma=0.02),
 }
 
 
@@ -64,4 +72,3 @@ def test_split_matches_one_workgroup(case, monkeypatch):
     for b in range(X.shape[0]):
         np.testing.assert_array_equal(split["v"][b], one["v"][b])
     assert np.isfinite(split["loss"]).all()
-
