@@ -72,26 +72,30 @@ PHASE_MODEL = {
     "softmax": ("hbm", _bytes(lambda w: 32 + 24), "bytes",
                 "k_csc_rows + k_col_softmax: column-major view, Eq. 1, Eq. 2, P0 (written into the Sinkhorn pieces)"),
     "sinkhorn": ("hbm", _bytes(lambda w: 2 * w.n_iter * 8 + 8), "bytes",
-                 "k_sinkhorn_fwd: L Sinkhorn iterations (Eq. 3, Eq. 4) and the loss"),
+                 "k_sinkhorn_fwd (clouds up to 2048 points; larger: the streamed or split kernels, or one launch "
+                 "per half-sweep): L Sinkhorn iterations (Eq. 3, Eq. 4) and the loss"),
     "bwd_sinkhorn": ("hbm", _bytes(lambda w: 2 * w.n_iter * 16), "bytes",
-                     "k_sinkhorn_bwd: reverse Sinkhorn sweeps"),
+                     "k_sinkhorn_bwd (clouds up to 2048 points; larger: the streamed or split kernels, or two "
+                     "launches per iteration): reverse Sinkhorn sweeps"),
     "bwd_softmax": ("hbm", _bytes(lambda w: 24 + 8), "bytes",
                     "softmax and temperature adjoints, distance gradient (Eq. 5)"),
 }
 
 # HBM bytes per launch measured with rocprofv3 counters (FETCH_SIZE and
 # WRITE_SIZE, KiB per dispatch, each scaled by the same counter's reading for
-# a plain device copy of known size), summed over the phase's kernels. Each
-# entry names the source files it was measured on with their SHA-256: once a
-# file changes, traffic is reported as null until measured again.
+# a plain device copy of known size), summed over the phase's kernels, on the
+# workload TRAFFIC_WORKLOAD. Each entry names the source files it was
+# measured on with their SHA-256: once a file changes, or on another
+# workload, traffic is reported as null.
+TRAFFIC_WORKLOAD = 2
 TRAFFIC = {
-    "stats": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_top2"], "bytes_per_launch": 32794531},
-    "support": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit"], "bytes_per_launch": 32857993},
-    "build": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "3cb072cf5cb664e8cbe1f5d54d9ee9109ac4162a21dd1abcb1c3bfe4420ac13b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit_compact_place"], "bytes_per_launch": 23189412},
-    "softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "083b4fd2edd2980ac8cfd94a426dbcdb3c2e0009101b2824711be304ce307d34", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_csc_rows", "k_col_softmax"], "bytes_per_launch": 45071558},
-    "sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "4c802f43f25de7177c72507d1ed13422c43d16c1647567695adad8abc2a7eb9b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_sinkhorn_fwd"], "bytes_per_launch": 26081540},
-    "bwd_sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "4c802f43f25de7177c72507d1ed13422c43d16c1647567695adad8abc2a7eb9b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 26068935},
-    "bwd_softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "083b4fd2edd2980ac8cfd94a426dbcdb3c2e0009101b2824711be304ce307d34", "paper_2512_19743_amd/csrc/apml_internal.h": "b3585ddee1fa29ad500cf288d62b310cc25baf2041eed550aac54c3fdf63837f", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 33356621},
+    "stats": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "16b5eb0c61d4e2da2b014f2375bb5800e4d9aa13662c4d6b1ae287703b5d6c42", "paper_2512_19743_amd/csrc/apml_internal.h": "8ab06df70588832adb6a5296337db2b3668d53f607b90efbd4d0cecf18cf475d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_top2"], "bytes_per_launch": 32794275},
+    "support": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "16b5eb0c61d4e2da2b014f2375bb5800e4d9aa13662c4d6b1ae287703b5d6c42", "paper_2512_19743_amd/csrc/apml_internal.h": "8ab06df70588832adb6a5296337db2b3668d53f607b90efbd4d0cecf18cf475d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit"], "bytes_per_launch": 31179257},
+    "build": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "16b5eb0c61d4e2da2b014f2375bb5800e4d9aa13662c4d6b1ae287703b5d6c42", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "8ab06df70588832adb6a5296337db2b3668d53f607b90efbd4d0cecf18cf475d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit_compact_place"], "bytes_per_launch": 19011715},
+    "softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "083b4fd2edd2980ac8cfd94a426dbcdb3c2e0009101b2824711be304ce307d34", "paper_2512_19743_amd/csrc/apml_internal.h": "8ab06df70588832adb6a5296337db2b3668d53f607b90efbd4d0cecf18cf475d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_csc_rows", "k_col_softmax"], "bytes_per_launch": 45065782},
+    "sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "3d83b5c2db3d28c5a08d7bb569008590d79d62e3c1e66ae2427f3b1423e0095b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "8ab06df70588832adb6a5296337db2b3668d53f607b90efbd4d0cecf18cf475d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_sinkhorn_fwd"], "bytes_per_launch": 26088451},
+    "bwd_sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "3d83b5c2db3d28c5a08d7bb569008590d79d62e3c1e66ae2427f3b1423e0095b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "8ab06df70588832adb6a5296337db2b3668d53f607b90efbd4d0cecf18cf475d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 26058696},
+    "bwd_softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "083b4fd2edd2980ac8cfd94a426dbcdb3c2e0009101b2824711be304ce307d34", "paper_2512_19743_amd/csrc/apml_internal.h": "8ab06df70588832adb6a5296337db2b3668d53f607b90efbd4d0cecf18cf475d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 33332815},
 }
 
 
@@ -102,9 +106,9 @@ def _sha(path):
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def traffic_for(phase, d):
+def traffic_for(phase, config_index):
     t = TRAFFIC.get(phase)
-    if not t or any(_sha(src) != h for src, h in t["sources"].items()):
+    if config_index != TRAFFIC_WORKLOAD or not t or any(_sha(src) != h for src, h in t["sources"].items()):
         return None
     return t["bytes_per_launch"]
 
@@ -486,12 +490,12 @@ def main():
                          "work_per_launch": work, "work_unit": unit_kind,
                          "achieved": achieved / (1e12 if bound == "alu" else 1e9),
                          "unit": "TFLOP/s" if bound == "alu" else "GB/s", "frac": achieved / peak,
-                         "traffic": traffic_for(name, None)}
+                         "traffic": traffic_for(name, args.config)}
     dom = max(kernels, key=lambda k: kernels[k]["avg_launch_ms"] * kernels[k]["launches_per_step"])
     d = kernels[dom]
     roofline = {"bound": d["bound"], "achieved": d["achieved"],
                 "peak": FP32_PEAK_FLOPS / 1e12 if d["bound"] == "alu" else HBM_PEAK / 1e9,
-                "unit": d["unit"], "frac": d["frac"], "traffic": traffic_for(dom, d),
+                "unit": d["unit"], "frac": d["frac"], "traffic": traffic_for(dom, args.config),
                 "kernel": d["kernel"], "phase": dom, "avg_launch_ms": d["avg_launch_ms"],
                 "work_per_launch": d["work_per_launch"], "work_unit": d["work_unit"]}
 
