@@ -225,6 +225,34 @@ __global__ __launch_bounds__(kBlock) void k_csc_fill(DevPlan d, BuildArgs a)
     d.csc_col[p] = gc;
 }
 
+// The same placement for the pairs of sample blockIdx.x / ranges whose column
+// lies in its range blockIdx.x % ranges of C columns (dynamic LDS: C ints):
+// each column's next free slot is kept in LDS, starting at its global offset,
+// and taken by an LDS atomic. The workgroup reads all of the sample's pairs
+// and places those of its columns.
+constexpr int kFillT = 1024;
+
+__global__ __launch_bounds__(kFillT) void k_csc_fill_lds(DevPlan d, BuildArgs a, int ranges, int C)
+{
+    extern __shared__ int next[];
+    const int b = blockIdx.x / ranges, q = blockIdx.x % ranges;
+    const int j0 = q * C, j1 = min(d.M, j0 + C);
+    const size_t gb = (size_t)b * d.M;
+    for (int j = j0 + (int)threadIdx.x; j < j1; j += kFillT)
+        next[j - j0] = d.col_ptr[gb + j];
+    __syncthreads();
+    const int lo = d.row_ptr[(size_t)b * d.N], hi = d.row_ptr[(size_t)(b + 1) * d.N];
+    for (int t = lo + (int)threadIdx.x; t < hi; t += kFillT) {
+        const int j = d.csr_col[t];
+        if (j < j0 || j >= j1)
+            continue;
+        const int p = atomicAdd(&next[j - j0], 1);
+        a.tmp_row[p] = d.csr_row[t] - b * d.N;
+        a.tmp_src[p] = t;
+        d.csc_col[p] = (int32_t)(gb + j);
+    }
+}
+
 // Canonical order inside each column (increasing row): the rank of an entry
 // is the number of entries of its column with a smaller row.
 __global__ __launch_bounds__(kBlock) void k_csc_sort(DevPlan d, BuildArgs a)
@@ -283,9 +311,19 @@ void launch_offsets(const int32_t *cnt, int S, const int32_t *col_cnt, const Cou
 
 void launch_csc_build(const DevPlan &d, const BuildArgs &a, hipStream_t s)
 {
-    // d.col_ptr holds the scan of the column counts (launch_col_scan)
+    // d.col_ptr holds the scan of the column counts (launch_col_scan). With
+    // enough samples, column ranges of each sample in LDS (each workgroup
+    // reads the sample's pairs once); else one thread per pair and a global
+    // atomic per pair (measured at 64 x 8192 x 8192: 107 us).
     const unsigned g = blocks_for(d.nnz, kBlock);
-    hipLaunchKernelGGL(k_csc_fill, dim3(g), dim3(kBlock), 0, s, d, a);
+    const int ranges = std::min(16, std::max((d.M + 16383) / 16384, (512 + d.B - 1) / d.B));
+    const int C = (d.M + ranges - 1) / ranges;
+    if (d.B * ranges >= 256 && C <= 16384) {
+        hipLaunchKernelGGL(k_csc_fill_lds, dim3(d.B * ranges), dim3(kFillT), (size_t)C * sizeof(int), s, d, a, ranges,
+                           C);
+    } else {
+        hipLaunchKernelGGL(k_csc_fill, dim3(g), dim3(kBlock), 0, s, d, a);
+    }
     hipLaunchKernelGGL(k_csc_sort, dim3(g), dim3(kBlock), 0, s, d, a);
 }
 
