@@ -1045,7 +1045,7 @@ apml_status run_backward(apml_plan *plan, const float *x, const float *y, const 
     dv.grad_loss = grad_loss;
     dv.grad_x = grad_x;
     dv.grad_y = grad_y;
-    dv.xr2 = dv.xc2 = nullptr;
+    dv.yr = dv.yc = nullptr;
     // the split streamed reverse kernel exchanges the owners' factors in memory
     const bool split = dv.L > 0 && plan->sink_wide && sinkhorn_split_factor(plan->B) > 1;
     // On the per-iteration path the row-order sweep adjoint becomes the final
@@ -1059,8 +1059,9 @@ apml_status run_backward(apml_plan *plan, const float *x, const float *y, const 
             dv.wc = c.take<float>(w);
             dv.cbar = c.take<double>(plan->stored);
             if (split) {
-                dv.xr2 = c.take<float2>((size_t)plan->B * plan->N + kSinkOwnersW);
-                dv.xc2 = c.take<float2>((size_t)plan->B * plan->M + kSinkOwnersW);
+                // one region per phase, each padded by kSinkOwnersW words
+                dv.yr = c.take<float>((size_t)dv.L * ((size_t)plan->B * plan->N + kSinkOwnersW));
+                dv.yc = c.take<float>((size_t)dv.L * ((size_t)plan->B * plan->M + kSinkOwnersW));
             }
         } else if (dv.L > 0 && !plan->sink_bwd) {
             dv.rz = dv.adj;

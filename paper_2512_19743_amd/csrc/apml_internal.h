@@ -316,7 +316,8 @@ struct DevPlan {
     uint32_t *split_sync;         // [B][2][kSplitSyncStride]: meeting counter (word 0) and the workgroups' XCDs
                                   // (words 1..K) of the split streamed kernels
                                   // (forward, backward), cleared before each launch
-    float2 *xr2, *xc2;            // [B*N], [B*M] (+ padding): owners' factors exchanged by the split reverse kernels
+    float *yr, *yc;               // [L][B*N + kSinkOwnersW], [L][B*M + kSinkOwnersW]: owners' words published by
+                                  // the split reverse kernels, one padded region per phase
     const int32_t *sink_place;    // during the forward softmax of that path: the pieces' placement, so that the
                                   // column softmax writes every pair into its pieces; else NULL
 };
@@ -387,8 +388,10 @@ void launch_wide_pack(const DevPlan &d, int32_t *place, hipStream_t s);
 constexpr int kSplitMax = 8;
 constexpr int kSplitSyncStride = 32; // counters 128 bytes apart
 int sinkhorn_split_factor(int B);
+// Workgroups of a split launch: B rounded up to a multiple of the 8 XCDs, times K.
+inline int split_grid(int B, int K) { return (B + 7) / 8 * 8 * K; }
 // Streamed kernels, split over sinkhorn_split_factor(B) workgroups per sample
-// when that is above 1 (the reverse kernel then needs d.xr2, d.xc2), else one.
+// when that is above 1 (the reverse kernel then needs d.yr, d.yc), else one.
 hipError_t launch_sinkhorn_fwd_wide(const DevPlan &d, double eps, hipStream_t s);
 hipError_t launch_sinkhorn_bwd_wide(const DevPlan &d, hipStream_t s);
 bool sinkhorn_bwd_fits(int slots, int64_t max_pairs);

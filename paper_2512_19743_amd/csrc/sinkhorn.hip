@@ -747,6 +747,16 @@ __device__ __forceinline__ void publish64(void *p, uint64_t v, bool local)
         __hip_atomic_store(reinterpret_cast<uint64_t *>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// A 32-bit word published as in publish64.
+__device__ __forceinline__ void publish32(float *p, float v, bool local)
+{
+    if (local)
+        *p = v;
+    else
+        __hip_atomic_store(reinterpret_cast<uint32_t *>(p), __builtin_bit_cast(uint32_t, v), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // One forward sweep: every owner's sum of P0 times the other side's scaling
 // (vals) over its pieces, then its own scaling v = cur / (cur sum + eps)
 // (Eq. 3 or Eq. 4) into own (LDS) and g_val (the saved scalings). With SPLIT
@@ -832,7 +842,7 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_fwd_w(DevPlan d, double eps)
 template <bool SPLIT>
 __device__ void wide_reverse(const WideOrder &pk, int b, int n_used, float *copy, const float2 *fin, float2 *fout,
                              const double *own_l, const double *own_prev, int s0_first = 0, int step = 1,
-                             bool local = false)
+                             bool local = false, float *yout = nullptr)
 {
     const int ns = wave_slots(n_used);
     for (int s0 = s0_first; s0 < ns; s0 += kWBatch * step) {
@@ -880,11 +890,10 @@ __device__ void wide_reverse(const WideOrder &pk, int b, int n_used, float *copy
                 copy[pk_index(b, p, e, kP, pk.slots)] =
                     w[k].p0[e] != 0.0f ? (float)((rho[e] - dsum * (double)f[e].y) * q) : 0.0f;
             if (u.bits(w[k].info, 16, 2) == 3u) { // head and valid
-                const float2 f = make_float2((float)(dsum * al[k]), (float)alp[k]);
-                if constexpr (SPLIT)
-                    publish64(fout + o, __builtin_bit_cast(uint64_t, f), local);
+                if constexpr (SPLIT) // the other word, alp, is a saved scaling the readers load themselves
+                    publish32(yout + o, (float)(dsum * al[k]), local);
                 else
-                    fout[o] = f;
+                    fout[o] = make_float2((float)(dsum * al[k]), (float)alp[k]);
             }
         }
     }
@@ -983,19 +992,17 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_w(DevPlan d)
 
 constexpr unsigned kSplitSpinLimit = 1u << 20; // polls of one meeting (about a second) before giving up
 
-// Sample and member of workgroup g. Workgroups are dispatched to the eight
-// XCDs in turn, so when 8 divides B the K workgroups of a sample are given
-// ids on one XCD (their meetings then stay within one L2's reach).
-__device__ __forceinline__ void split_member(int g, int B, int K, int &b, int &k)
+// Sample and member of workgroup g, or false for a workgroup without one.
+// Workgroups are dispatched to the eight XCDs in turn, so sample b takes
+// XCD b % 8 and the ids x + 8 ((b / 8) K + k) on it: a sample's K workgroups
+// share an XCD (their meetings stay within one L2's reach). The grid is
+// split_grid(B, K) workgroups; those past the last sample end at once.
+__device__ __forceinline__ bool split_member(int g, int B, int K, int &b, int &k)
 {
-    if (B % 8 == 0) {
-        const int x = g % 8, slot = g / 8; // slot < B K / 8
-        b = x * (B / 8) + slot / K;
-        k = slot % K;
-    } else {
-        b = g / K;
-        k = g % K;
-    }
+    const int x = g % 8, slot = g / 8;
+    b = (slot / K) * 8 + x;
+    k = slot % K;
+    return b < B;
 }
 
 // Meeting t of a sample's K workgroups (t = 1, 2, ...): each waits until its
@@ -1111,12 +1118,73 @@ template <typename T> __device__ __forceinline__ void split_gather(T *lds, const
 #undef APML_LDM
 #undef APML_LDL
 
+// The split reverse kernels' factors of one phase into LDS: lds[o] =
+// (Y_o, (float) own_prev[o]) for the sample's n owners. Y is the word each
+// owner's head published in this phase's region of fresh memory (32-bit
+// words: through the L2 only when local, else past the caches); own_prev is
+// the owners' saved scaling of the previous iteration, written by an earlier
+// kernel. Every lane reads eight whole chunks of lanes: each phase's region
+// is padded by kSinkOwnersW words, so a read past the sample's words stays
+// within the region of the same phase (other samples' words, which this CU
+// never uses), and the saved scalings are read only within the sample's n
+// owners. Both loads are issued together after the meeting (one latency).
+// The same float bits as the one-workgroup kernel's published pair.
+#define APML_LDY(I, B, BITS) "global_load_dword %" #I ", %[off], %" #B " " BITS "\n\t"
+#define APML_LOADY(BITS)                                                                                      \
+    asm volatile(APML_LDY(0, 8, BITS) APML_LDY(1, 9, BITS) APML_LDY(2, 10, BITS) APML_LDY(3, 11, BITS)       \
+                 APML_LDY(4, 12, BITS) APML_LDY(5, 13, BITS) APML_LDY(6, 14, BITS) APML_LDY(7, 15, BITS)     \
+                 "s_waitcnt vmcnt(0)"                                                                         \
+                 : "=&v"(y[0]), "=&v"(y[1]), "=&v"(y[2]), "=&v"(y[3]), "=&v"(y[4]), "=&v"(y[5]), "=&v"(y[6]), \
+                   "=&v"(y[7])                                                                                \
+                 : "s"(bs[0]), "s"(bs[1]), "s"(bs[2]), "s"(bs[3]), "s"(bs[4]), "s"(bs[5]), "s"(bs[6]),          \
+                   "s"(bs[7]), [off] "v"(off)                                                                 \
+                 : "memory")
+
+__device__ __forceinline__ void split_gather_factors(float2 *lds, const float *yv, const double *own_prev, int n,
+                                                     bool local)
+{
+    static_assert(kSinkOwnersW / kT == 8, "eight words per lane");
+    // the base in scalar registers: each 32-bit half read from the first lane
+    const uint64_t a = (uint64_t)(uintptr_t)yv;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+    const uint64_t base = ((uint64_t)hi << 32) | lo;
+    const void *bs[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+        bs[u] = reinterpret_cast<const void *>((uintptr_t)(base + (uint64_t)u * kT * 4u));
+    const uint32_t off = threadIdx.x * 4u;
+    float sp[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int o = u * kT + (int)threadIdx.x;
+        sp[u] = o < n ? (float)own_prev[o] : 0.0f;
+    }
+    uint32_t y[8];
+    if (local) {
+        asm volatile("buffer_inv sc0" ::: "memory"); // no line of an earlier read may serve these loads
+        APML_LOADY("sc0");
+    } else {
+        APML_LOADY("sc1");
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int o = u * kT + (int)threadIdx.x;
+        if (o < n)
+            lds[o] = make_float2(__builtin_bit_cast(float, y[u]), sp[u]);
+    }
+}
+#undef APML_LOADY
+#undef APML_LDY
+
+
 __global__ __launch_bounds__(kT) void k_sinkhorn_fwd_ws(DevPlan d, double eps, int K)
 {
     __shared__ double va[kSinkOwnersW], vb[kSinkOwnersW], part[kT / 64];
     __shared__ int stop, local;
     int b, k;
-    split_member(blockIdx.x, d.B, K, b, k);
+    if (!split_member(blockIdx.x, d.B, K, b, k))
+        return;
     const int tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
@@ -1160,22 +1228,25 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_fwd_ws(DevPlan d, double eps, i
         sample_loss(d, b, d.row_ptr[(size_t)b * N], d.row_ptr[(size_t)(b + 1) * N], va, vb, part);
 }
 
-// The reverse sweeps split over K workgroups. The factors of a row phase go
-// through d.xr2, those of a column phase through d.xc2: a buffer is written
-// again only two meetings later, when every workgroup has read it.
+// The reverse sweeps split over K workgroups. After each phase the owners'
+// heads publish one word each, Y (Yr_i = d_i alpha^l_i, Yc_j = e_j beta^l_j),
+// into a region of fresh memory for that phase (d.yr, d.yc: a word is never
+// written twice within the kernel, so the exchange may go through the L2, as
+// in the forward kernels); the pair's other factor is the owner's saved
+// scaling of the previous iteration, which every reader loads itself.
 __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_ws(DevPlan d, int K)
 {
     __shared__ float2 fr[kSinkOwnersW]; // row factors (Yr_i, alpha^(l-1)_i)
     __shared__ float2 fc[kSinkOwnersW]; // column factors (Yc_j, beta^(l-1)_j)
-    __shared__ int stop;
+    __shared__ int stop, local;
     int b, k;
-    split_member(blockIdx.x, d.B, K, b, k);
+    if (!split_member(blockIdx.x, d.B, K, b, k))
+        return;
     const int tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
     const double *alpha = d.alpha + (size_t)b * N, *beta = d.beta + (size_t)b * M; // + l * BN, + l * BM
     uint32_t *cnt = d.split_sync + ((size_t)b * 2 + 1) * kSplitSyncStride;
-    float2 *xr = d.xr2 + (size_t)b * N, *xc = d.xc2 + (size_t)b * M;
     const int n_row = __builtin_amdgcn_readfirstlane(d.wk_row.n_pos[b]);
     const int n_col = __builtin_amdgcn_readfirstlane(d.wk_col.n_pos[b]);
     wide_reverse_start(d, b, n_row, n_col, k, K);
@@ -1184,22 +1255,24 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_ws(DevPlan d, int K)
     if (tid == 0)
         stop = 0;
     lds_barrier();
-    // The factor buffers are written again every other phase. Measured:
-    // exchanging reused addresses through the L2 (plain stores, loads past
-    // only the CU's cache) returned stale words in some cases, so these
-    // kernels exchange through memory (device-scope atomics) only.
-    const bool loc = false;
-    uint32_t t = 0;
+    if (!split_begin(cnt, K, k, &d.ctr->error, &stop, &local))
+        return;
+    const bool loc = local != 0;
+    uint32_t t = 1;
     for (int l = L; l >= 1; --l) {
-        wide_reverse<true>(d.wk_row, b, n_row, d.wr, fc, xr, alpha + l * BN, alpha + (l - 1) * BN, k, K, loc);
+        float *yr = d.yr + (size_t)(L - l) * (BN + kSinkOwnersW) + (size_t)b * N;
+        wide_reverse<true>(d.wk_row, b, n_row, d.wr, fc, nullptr, alpha + l * BN, alpha + (l - 1) * BN, k, K, loc,
+                           yr);
         if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
             return;
-        split_gather(fr, xr, N, loc);
+        split_gather_factors(fr, yr, alpha + (l - 1) * BN, N, loc);
         lds_barrier();
-        wide_reverse<true>(d.wk_col, b, n_col, d.wc, fr, xc, beta + l * BM, beta + (l - 1) * BM, k, K, loc);
+        float *yc = d.yc + (size_t)(L - l) * (BM + kSinkOwnersW) + (size_t)b * M;
+        wide_reverse<true>(d.wk_col, b, n_col, d.wc, fr, nullptr, beta + l * BM, beta + (l - 1) * BM, k, K, loc,
+                           yc);
         if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
             return;
-        split_gather(fc, xc, M, loc);
+        split_gather_factors(fc, yc, beta + (l - 1) * BM, M, loc);
         lds_barrier();
     }
     wide_reverse_end(d, b, n_row, fc, k, K);
@@ -1262,7 +1335,8 @@ template <int SW> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd_wr(DevPla
     __shared__ double va[kSinkOwnersW], vb[kSinkOwnersW], part[kT / 64];
     __shared__ int stop, local;
     int b, k;
-    split_member(blockIdx.x, d.B, K, b, k);
+    if (!split_member(blockIdx.x, d.B, K, b, k))
+        return;
     const int tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
@@ -1312,7 +1386,7 @@ template <int SW> __global__ __launch_bounds__(kT) void k_sinkhorn_fwd_wr(DevPla
 // beforehand.
 template <int SW, int OB>
 __device__ __forceinline__ void reg_reverse(const WSlot (&w)[SW], float (&cp)[SW][kP], int n, const double (&al)[SW],
-                                            const double (&alp)[SW], const float2 *fin, float2 *fout, bool local)
+                                            const double (&alp)[SW], const float2 *fin, float *yout, bool local)
 {
 #pragma unroll
     for (int q = 0; q < SW; ++q) {
@@ -1324,20 +1398,24 @@ __device__ __forceinline__ void reg_reverse(const WSlot (&w)[SW], float (&cp)[SW
 #pragma unroll
         for (int e = 0; e < kP; ++e)
             f[e] = lds_at<float2>(fin, u.half(w[q].gi[e / 2], e));
-        double rho[kP], acc = 0.0;
+        // rho_e = cp_e - f_e.x is formed again in the update (the same value):
+        // keeping all of them would spill at two slots
+        double acc = 0.0;
 #pragma unroll
         for (int e = 0; e < kP; ++e) {
-            rho[e] = (double)cp[q][e] - (double)f[e].x;
+            const double rho = (double)cp[q][e] - (double)f[e].x;
             const double p0 = (double)w[q].p0[e];
-            acc = e == 0 ? rho[e] * p0 : __builtin_fma(rho[e], p0, acc);
+            acc = e == 0 ? rho * p0 : __builtin_fma(rho, p0, acc);
         }
         const double dsum = al[q] * group_reduce_lg(acc, (int)u.bits(w[q].info, OB, 3));
         const double qt = quotient(al[q], alp[q]);
 #pragma unroll
-        for (int e = 0; e < kP; ++e)
-            cp[q][e] = w[q].p0[e] != 0.0f ? (float)((rho[e] - dsum * (double)f[e].y) * qt) : 0.0f;
+        for (int e = 0; e < kP; ++e) {
+            const double rho = (double)cp[q][e] - (double)f[e].x;
+            cp[q][e] = w[q].p0[e] != 0.0f ? (float)((rho - dsum * (double)f[e].y) * qt) : 0.0f;
+        }
         if (u.bits(w[q].info, OB + 3, 2) == 3u) // head and valid
-            publish64(fout + o, __builtin_bit_cast(uint64_t, make_float2((float)(dsum * al[q]), (float)alp[q])), local);
+            publish32(yout + o, (float)(dsum * al[q]), local); // alp: read from the saved scalings
     }
 }
 
@@ -1360,15 +1438,15 @@ template <int SW> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_wr(DevPla
     constexpr int OB = 13; // owner bits of the streamed layout's info word
     __shared__ float2 fr[kSinkOwnersW]; // row factors (Yr_i, alpha^(l-1)_i)
     __shared__ float2 fc[kSinkOwnersW]; // column factors (Yc_j, beta^(l-1)_j)
-    __shared__ int stop;
+    __shared__ int stop, local;
     int b, k;
-    split_member(blockIdx.x, d.B, K, b, k);
+    if (!split_member(blockIdx.x, d.B, K, b, k))
+        return;
     const int tid = threadIdx.x;
     const int N = d.N, M = d.M, L = d.L;
     const size_t BN = (size_t)d.B * N, BM = (size_t)d.B * M;
     const double *alpha = d.alpha + (size_t)b * N, *beta = d.beta + (size_t)b * M; // + l * BN, + l * BM
     uint32_t *cnt = d.split_sync + ((size_t)b * 2 + 1) * kSplitSyncStride;
-    float2 *xr = d.xr2 + (size_t)b * N, *xc = d.xc2 + (size_t)b * M;
     const int mr = split_slots(__builtin_amdgcn_readfirstlane(d.wk_row.n_pos[b]), k, K);
     const int mc = split_slots(__builtin_amdgcn_readfirstlane(d.wk_col.n_pos[b]), k, K);
     WSlot pr[SW], pc[SW];
@@ -1412,25 +1490,26 @@ template <int SW> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_wr(DevPla
     if (tid == 0)
         stop = 0;
     lds_barrier();
-    // The factor buffers are written again every other phase. Measured:
-    // exchanging reused addresses through the L2 (plain stores, loads past
-    // only the CU's cache) returned stale words in some cases, so these
-    // kernels exchange through memory (device-scope atomics) only.
-    const bool loc = false;
-    uint32_t t = 0;
+    // the exchange as in k_sinkhorn_bwd_ws: a fresh region per phase
+    if (!split_begin(cnt, K, k, &d.ctr->error, &stop, &local))
+        return;
+    const bool loc = local != 0;
+    uint32_t t = 1;
     for (int l = L; l >= 1; --l) {
         double al[SW] = {}, alp[SW] = {};
         owner_scalings<SW, OB>(pr, mr, alpha + l * BN, alpha + (l - 1) * BN, al, alp);
-        reg_reverse<SW, OB>(pr, rr, mr, al, alp, fc, xr, loc); // reverse of Eq. 4
+        float *yr = d.yr + (size_t)(L - l) * (BN + kSinkOwnersW) + (size_t)b * N;
+        reg_reverse<SW, OB>(pr, rr, mr, al, alp, fc, yr, loc); // reverse of Eq. 4
         if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
             return;
-        split_gather(fr, xr, N, loc);
+        split_gather_factors(fr, yr, alpha + (l - 1) * BN, N, loc);
         lds_barrier();
         owner_scalings<SW, OB>(pc, mc, beta + l * BM, beta + (l - 1) * BM, al, alp);
-        reg_reverse<SW, OB>(pc, rc, mc, al, alp, fr, xc, loc); // reverse of Eq. 3
+        float *yc = d.yc + (size_t)(L - l) * (BM + kSinkOwnersW) + (size_t)b * M;
+        reg_reverse<SW, OB>(pc, rc, mc, al, alp, fr, yc, loc); // reverse of Eq. 3
         if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
             return;
-        split_gather(fc, xc, M, loc);
+        split_gather_factors(fc, yc, beta + (l - 1) * BM, M, loc);
         lds_barrier();
     }
     // the adjoint with respect to P0, r - Yc_j, in row-major order
@@ -1789,7 +1868,8 @@ int sinkhorn_split_factor(int B)
         c = (coop ? cus * std::min(f, r) : 0) + 1;
         resident[dev].store(c, std::memory_order_relaxed);
     }
-    const int K = std::min(kSplitMax, (c - 1) / B);
+    // the grid rounds B up to whole rounds of the eight XCDs
+    const int K = std::min(kSplitMax, (c - 1) / split_grid(B, 1));
     return K >= 2 ? K : 1;
 }
 
@@ -1804,7 +1884,7 @@ bool launch_split(const void *kernel, void **args, const DevPlan &d, int K, hipS
     hipLaunchKernelGGL(k_zero_u32, dim3(blocks_for(n, kBlock)), dim3(kBlock), 0, s, d.split_sync, n);
     if (hipGetLastError() != hipSuccess)
         return false;
-    if (hipLaunchCooperativeKernel(kernel, dim3(d.B * K), dim3(kT), args, 0, s) != hipSuccess) {
+    if (hipLaunchCooperativeKernel(kernel, dim3(split_grid(d.B, K)), dim3(kT), args, 0, s) != hipSuccess) {
         (void)hipGetLastError();
         return false;
     }
@@ -1857,7 +1937,7 @@ hipError_t launch_sinkhorn_fwd_wide(const DevPlan &d, double eps, hipStream_t s)
 hipError_t launch_sinkhorn_bwd_wide(const DevPlan &d, hipStream_t s)
 {
     int K = sinkhorn_split_factor(d.B);
-    if (K > 1 && d.split_sync && d.xr2 && d.xc2) {
+    if (K > 1 && d.split_sync && d.yr && d.yc) {
         DevPlan dc = d;
         void *args[] = {&dc, &K};
         if (launch_split(split_bwd_kernel((d.wk_row.slots + K - 1) / K), args, d, K, s))
