@@ -34,9 +34,9 @@ HBM_PEAK = 8.0e12
 # support scan, the row's and the column's radius test): 3 subtractions,
 # 3 multiplications, 2 additions = 8 FLOPs per pair. The selects (min, med3,
 # compares) are not floating-point arithmetic and are not counted. The full
-# statistics scan evaluates every pair once per direction, so its own
-# instruction stream issues twice these FLOPs; the VALU issue rate it reaches
-# is measured with counters (VALU instructions per CU and clock), not here.
+# statistics scan evaluates every pair once for both directions; the VALU
+# issue rate it reaches is measured with counters (VALU instructions per CU
+# and clock), not here.
 FLOPS_PER_PAIR = 8
 
 
@@ -61,7 +61,7 @@ def _bytes(per_entry_fn):
 
 PHASE_MODEL = {
     "stats": ("alu", _flops(0, 2), "FLOP",
-              {"full": "k_top2: minimum and second minimum of every row and column",
+              {"full": "k_top2_pairs: minimum and second minimum of every row and column, each pair evaluated once",
                "skip": "k_spatial_sort + k_cull_top2: curve order, then the minima over the runs that can matter"}),
     "support": ("alu", _flops(1, 1), "FLOP",
                 {"full": "k_emit: radius test of every pair, counts and staged hits of the candidate support",

@@ -211,10 +211,11 @@ apml_status apml_plan_destroy(apml_plan *plan);
 /* Sizes of a plan. stored_pairs counts every stored pair, including pairs kept
  * only as the minimum or second minimum of a row or column (they carry zero
  * mass). bytes is the device memory the plan holds. scanned_min and
- * scanned_support count the pairs whose distance the two dense scans of the
- * forward evaluated (the minimum scan over both directions, the support scan
- * over rows); the scans skip pairs that provably cannot matter, so these stay
- * below 2*B*N*M and B*N*M. */
+ * scanned_support count the pairs the two dense scans of the forward
+ * examined: the minimum scan once per direction (2*B*N*M when nothing is
+ * skipped, although the full scan evaluates each distance once for both),
+ * the support scan over rows (B*N*M); the skipping scans leave out pairs that
+ * provably cannot matter. */
 typedef struct apml_plan_info {
     int32_t B, N, M, n_iter;
     int64_t stored_pairs;

@@ -430,12 +430,9 @@ apml_status wait_for(hipStream_t s)
     }
 }
 
-// Chunks of the broadcast range so that a full dense scan has about
+// Chunks of the broadcast range so that the support scan has about
 // target / 1024 waves per SIMD on 256 CUs, each chunk at least min_chunk
-// points long. The minimum scan takes two rounds of waves (more waves hide
-// the tail of the grid better than longer loops: measured 51 us for 32
-// clouds of 2048 points against 55 us with one round and 69 us with half a
-// round).
+// points long.
 void choose_chunks(int B, int n_own, int n_bc, int *S, int *chunk, int min_chunk, int64_t target = 8192)
 {
     const int64_t waves = (int64_t)B * ceil_div(n_own, 64);
@@ -571,7 +568,7 @@ apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t
     dv.row_ptr = keep.get<int32_t>((size_t)BN + 1);
     dv.col_ptr = keep.get<int32_t>((size_t)BM + 1);
     // full scans
-    ScanDir rows{}, cols{};
+    PairScan ps{};
     EmitArgs ea{};
     // skipping scans
     SpatialArgs sa{};
@@ -580,20 +577,10 @@ apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t
     int32_t *cnt = nullptr; // stored pairs per row (per (row, chunk) for the full scan)
     int cnt_chunks = 1;
     if (!skip) {
-        rows.own = x;
-        rows.bcast = y;
-        rows.n_own = N;
-        rows.n_bc = M;
-        choose_chunks(B, N, M, &rows.S, &rows.chunk, 256, 16384);
-        rows.owner_blocks = ceil_div(N, kBlock);
-        rows.tiles = B * rows.S * rows.owner_blocks;
-        cols.own = y;
-        cols.bcast = x;
-        cols.n_own = M;
-        cols.n_bc = N;
-        choose_chunks(B, M, N, &cols.S, &cols.chunk, 256, 16384);
-        cols.owner_blocks = ceil_div(M, kBlock);
-        cols.tiles = B * cols.S * cols.owner_blocks;
+        choose_pair_scan(ps, B, N, M);
+        ps.x = x;
+        ps.y = y;
+        const int owner_blocks = ceil_div(N, kBlock);
         choose_chunks(B, N, M, &ea.S, &ea.chunk, 256);
         // the scratch of both scans in one allocation; the counting pass
         // keeps the first hits of every (row, chunk), at 16-bit offsets
@@ -601,8 +588,8 @@ apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t
         float *E_row = nullptr;
         float4 *ypack = nullptr;
         auto lay = [&](Carve &c) {
-            rows.partial = c.take<float2>((size_t)rows.S * BN);
-            cols.partial = c.take<float2>((size_t)cols.S * BM);
+            ps.row_partial = c.take<float2>((size_t)ps.S_r * BN);
+            ps.col_partial = c.take<float2>((size_t)ps.S_c * BM);
             E_row = c.take<float>(BN);
             ypack = c.take<float4>(BM);
             ea.cnt = c.take<int32_t>((size_t)BN * ea.S);
@@ -611,7 +598,7 @@ apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t
                 ea.stage_narrow = ea.chunk <= 256;
                 const size_t staged = (size_t)BN * ea.S * ea.kst;
                 ea.stage = c.take<uint16_t>(ea.stage_narrow ? (staged + 1) / 2 : staged);
-                const size_t tiles = (size_t)B * ea.S * rows.owner_blocks;
+                const size_t tiles = (size_t)B * ea.S * owner_blocks;
                 ea.spill = c.take<uint32_t>(tiles * kTileSpill);
                 ea.spill_n = c.take<int32_t>(tiles);
             }
@@ -627,12 +614,12 @@ apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t
             return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (statistics)");
         {
             PhaseTimer pt(PH_STATS, s, timed);
-            launch_top2(rows, cols, B, s);
+            launch_top2_pairs(ps, s);
             HIP_TRY(hipGetLastError());
             pt.stop();
         }
-        FinalizeDir fr{rows.partial, x, dv.m12_row, E_row, nullptr, nullptr, nullptr, N, rows.S, kp.lk_row};
-        FinalizeDir fc{cols.partial, y, dv.m12_col, nullptr, ypack, col_cnt, ba.col_fill, M, cols.S, kp.lk_col};
+        FinalizeDir fr{ps.row_partial, x, dv.m12_row, E_row, nullptr, nullptr, nullptr, N, ps.S_r, kp.lk_row};
+        FinalizeDir fc{ps.col_partial, y, dv.m12_col, nullptr, ypack, col_cnt, ba.col_fill, M, ps.S_c, kp.lk_col};
         launch_finalize(fr, fc, B, kp, dv.ctr, s); // also clears the counters
         HIP_TRY(hipGetLastError());
 
@@ -643,7 +630,7 @@ apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t
         ea.B = B;
         ea.N = N;
         ea.M = M;
-        ea.owner_blocks = rows.owner_blocks;
+        ea.owner_blocks = owner_blocks;
         ea.col_cnt = col_cnt; // cleared by the finalize kernel
         ea.ctr = dv.ctr;
         cnt = ea.cnt;

@@ -10,7 +10,6 @@
 namespace apml {
 
 constexpr int kBlock = 256;       // threads per workgroup of the grid-wide kernels
-constexpr int kUnroll = 8;        // broadcast points per inner step of the dense scans
 constexpr int kGroup = 4;         // lanes per row / column in the sparse kernels
 
 constexpr int kScanSlots = 64;
@@ -69,15 +68,8 @@ __device__ inline double emission_radius2(float m1, float m2, double log_ratio, 
 // One direction of the dense minimum / second-minimum scan. Owners are the
 // points whose statistics are computed (X for rows, Y for columns); the
 // broadcast set is scanned against every owner.
-struct ScanDir {
-    const float *own;   // [B, n_own, 3]
-    const float *bcast; // [B, n_bc, 3]
-    float2 *partial;    // [S][B * n_own]: (min, second min) of squared distance per chunk
-    int n_own, n_bc;
-    int S, chunk;       // chunks of the broadcast range and their length
-    int owner_blocks;   // workgroups per sample over the owners
-    int tiles;          // B * S * owner_blocks
-};
+// Columns of a support-scan chunk are a multiple of this.
+constexpr int kUnroll = 8;
 
 struct FinalizeDir {
     const float2 *partial; // [S][B * n_own]
@@ -90,7 +82,27 @@ struct FinalizeDir {
     double log_ratio;      // -log((1-p)/((K-1)p)), K = length of the other set
 };
 
-void launch_top2(const ScanDir &rows, const ScanDir &cols, int B, hipStream_t s);
+
+// The minimum scan with one evaluation per pair (k_top2_pairs): each wave
+// takes a block of 64 kPairR rows (x) and one chunk of columns (y); its
+// per-row partials are the row direction's chunk partials (S = S_r), its
+// per-column partials those of the column direction (S = S_c, one per row
+// block).
+constexpr int kPairR = 8;            // rows per lane
+constexpr int kPairWaves = 4;        // waves (row blocks) per workgroup
+constexpr int kPairThreads = 64 * kPairWaves;
+constexpr int kPairMaxChunk = 2048;  // columns per chunk at most
+constexpr int kPairTargetWaves = 8192;
+struct PairScan {
+    const float *x, *y;  // [B, N, 3], [B, M, 3]
+    float2 *row_partial; // [S_r][B * N]
+    float2 *col_partial; // [S_c][B * M]
+    int B, N, M;
+    int chunk, S_r;      // columns per chunk (a multiple of 8) and chunks
+    int S_c;             // row blocks of 64 kPairR rows
+};
+void choose_pair_scan(PairScan &p, int B, int N, int M);
+void launch_top2_pairs(const PairScan &p, hipStream_t s);
 void launch_finalize(const FinalizeDir &rows, const FinalizeDir &cols, int B, const Params &p,
                      Counters *ctr, hipStream_t s);
 

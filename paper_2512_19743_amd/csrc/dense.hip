@@ -1,11 +1,13 @@
 // Dense phase of the sparse APML loss: the two scans over all B*N*M pairs.
 // VALU-bound; no matrix cores (the K=3 contraction is not a GEMM).
 //
-//   k_top2     per row and per column, the minimum and second minimum of the
-//              single-precision squared distance (Sec. III-A). Each lane owns
-//              one point; the other cloud is streamed through scalar registers
-//              (wave-uniform loads), so a pair costs 6 VALU ops for the
-//              distance and 2 (min, med3) for the statistics.
+//   k_top2_pairs  per row and per column, the minimum and second minimum of
+//              the single-precision squared distance (Sec. III-A), each pair
+//              evaluated once: a lane holds eight rows, the columns stream
+//              through scalar registers (wave-uniform loads), and a pair costs
+//              6 VALU ops for the distance, 2 (min, med3) for its row's
+//              statistics and 2 for its column's, whose per-lane partials
+//              are merged across the wave once per eight columns.
 //   k_finalize merges the per-chunk statistics and derives each row's and
 //              column's emission threshold: the kept set s >= tau is the ball
 //              C <= C1 + log(1/tau)/T (Sec. III-B, Eq. 1), widened by a small
@@ -19,6 +21,9 @@
 //              column order, straight into the CSR arrays. The exact test
 //              s >= tau is applied later in double precision on this
 //              candidate set.
+#include <algorithm>
+#include <utility>
+
 #include "apml_internal.h"
 #include "device_common.h"
 #include "pieces.h"
@@ -26,47 +31,178 @@
 namespace apml {
 namespace {
 
-struct Top2Args {
-    ScanDir dir[2];
-    int B;
-};
+// ---------------------------------------------------------------------------
+// the minimum scan with one evaluation per pair
+// ---------------------------------------------------------------------------
+//
+// Each wave takes kPairR rows per lane (64 kPairR rows of a sample) and one
+// chunk of columns, which it streams through scalar registers in batches of
+// eight, as the support scan streams them. A pair costs the six operations
+// of its distance, two for its row's statistics (in the lane's registers)
+// and two for its column's statistics over the lane's rows, against 16 when
+// rows and columns are scanned separately. After each batch the eight
+// columns' statistics are merged across the 64 lanes: lane halves swap
+// columns (v_permlane32_swap, then v_permlane16_swap) so that each merge step
+// also halves the columns a lane holds, then 8-lane halves of each DPP row
+// exchange their last two columns and a butterfly finishes: about 54
+// operations per batch, under one per pair. Both statistics are
+// order-independent (minimum and second minimum of the multiset; the merge
+// of two top-2 multisets is exact), so the values are those of separate row
+// and column scans, bit for bit. Rows past N sit at +inf and columns past
+// the chunk at -inf: every pair involving one has distance +inf, which
+// changes no statistic of a real point.
 
-__global__ __launch_bounds__(kBlock) void k_top2(Top2Args args)
+// The top-2 multiset (a1 <= a2) merged with (b1 <= b2): the second smallest
+// of the four is med3(a1, b1, min(a2, b2)). Minima written out: the compiler
+// would first canonicalize operands that come from lane permutations.
+__device__ __forceinline__ void top2_merge(float &a1, float &a2, float b1, float b2)
 {
-    int t = blockIdx.x;
-    const int which = t < args.dir[0].tiles ? 0 : 1;
-    if (which)
-        t -= args.dir[0].tiles;
-    const ScanDir &d = args.dir[which];
-    const int ob = t % d.owner_blocks;
-    const int rest = t / d.owner_blocks;
-    const int ch = rest % d.S;
-    const int b = rest / d.S;
-    const int a = ob * kBlock + threadIdx.x;
-    const bool valid = a < d.n_own;
-    const float *p = d.own + ((size_t)b * d.n_own + (valid ? a : d.n_own - 1)) * 3;
-    const float ax = p[0], ay = p[1], az = p[2];
-    const float *__restrict__ q = d.bcast + (size_t)b * d.n_bc * 3;
-    const int j0 = ch * d.chunk;
-    const int j1 = min(d.n_bc, j0 + d.chunk);
-    float m1 = kInf, m2 = kInf;
-    int j = j0;
-    for (; j + kUnroll <= j1; j += kUnroll) {
-        const float *__restrict__ qq = q + 3 * (size_t)j;
+    float m;
+    asm("v_min_f32 %0, %1, %2" : "=v"(m) : "v"(a2), "v"(b2));
+    a2 = __builtin_amdgcn_fmed3f(a1, b1, m);
+    asm("v_min_f32 %0, %1, %2" : "=v"(a1) : "v"(a1), "v"(b1));
+}
+
+template <int CTRL> __device__ __forceinline__ float dpp_mov(float v)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
+}
+
+// Lane swaps between two registers, for both statistics: v_permlane32_swap
+// exchanges lanes 32-63 of the first register with lanes 0-31 of the second,
+// v_permlane16_swap the odd 16-lane rows of the first with the even rows of
+// the second. Written out: this compiler's builtins for them returned the
+// first register's new value for both results once those fed further
+// arithmetic (the merged statistics came out wrong), which inline assembly
+// avoids; the waits around them are kept by hand.
+__device__ __forceinline__ void swap32(float &a1, float &b1, float &a2, float &b2)
+{
+    asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\tv_permlane32_swap_b32 %2, %3\n\ts_nop 1"
+                 : "+v"(a1), "+v"(b1), "+v"(a2), "+v"(b2));
+}
+__device__ __forceinline__ void swap16(float &a1, float &b1, float &a2, float &b2)
+{
+    asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1\n\tv_permlane16_swap_b32 %2, %3\n\ts_nop 1"
+                 : "+v"(a1), "+v"(b1), "+v"(a2), "+v"(b2));
+}
+
+// Merges the eight columns' statistics (c1[u], c2[u]) of all 64 lanes; on
+// return lane 16 r (r = 0..3) holds column 2 r and lane 16 r + 8 column
+// 2 r + 1 of the batch.
+__device__ __forceinline__ void batch_merge(float (&c1)[8], float (&c2)[8], float &o1, float &o2)
+{
+    // lanes 0-31 keep columns 0-3, lanes 32-63 columns 4-7
+    float d1[4], d2[4];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            const float s = sqdist_f32(ax, ay, az, qq[3 * u], qq[3 * u + 1], qq[3 * u + 2]);
-            m2 = __builtin_amdgcn_fmed3f(m1, m2, s); // second order statistic of the multiset
-            m1 = fminf(m1, s);
+    for (int k = 0; k < 4; ++k) {
+        float y1 = c1[k + 4], y2 = c2[k + 4];
+        d1[k] = c1[k];
+        d2[k] = c2[k];
+        swap32(d1[k], y1, d2[k], y2);
+        top2_merge(d1[k], d2[k], y1, y2);
+    }
+    // 16-lane row r of d[k] holds column k + 4 (r / 2); after the swap of odd
+    // rows of d[k] with even rows of d[k + 2], row r holds column k + 2 r
+    float e1[2], e2[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        float y1 = d1[k + 2], y2 = d2[k + 2];
+        e1[k] = d1[k];
+        e2[k] = d2[k];
+        swap16(e1[k], y1, e2[k], y2);
+        top2_merge(e1[k], e2[k], y1, y2);
+    }
+    // lanes 0-7 of each row keep e[0] (column 2 r), lanes 8-15 e[1] (2 r + 1);
+    // each sends the other to the lane 8 places away (row_ror:8)
+    const bool hi = (threadIdx.x & 8u) != 0;
+    float k1 = hi ? e1[1] : e1[0], k2 = hi ? e2[1] : e2[0];
+    top2_merge(k1, k2, dpp_mov<0x128>(hi ? e1[0] : e1[1]), dpp_mov<0x128>(hi ? e2[0] : e2[1]));
+    // butterfly over the eight lanes: xor 1, xor 2 (quad_perm), then the
+    // mirror within 8 (every lane of a quad then holds the same values)
+    top2_merge(k1, k2, dpp_mov<0xB1>(k1), dpp_mov<0xB1>(k2));
+    top2_merge(k1, k2, dpp_mov<0x4E>(k1), dpp_mov<0x4E>(k2));
+    top2_merge(k1, k2, dpp_mov<0x141>(k1), dpp_mov<0x141>(k2));
+    o1 = k1;
+    o2 = k2;
+}
+
+// One batch of eight columns from j (scalar loads) against the lane's rows:
+// the rows' statistics, and the columns' statistics merged over the wave
+// and stored by lanes 16 r and 16 r + 8. TAIL: columns from cend on are
+// placed at -inf (not loaded).
+template <bool TAIL>
+__device__ __forceinline__ void pair_batch(const float (&ax)[kPairR], const float (&ay)[kPairR],
+                                           const float (&az)[kPairR], float (&m1)[kPairR], float (&m2)[kPairR],
+                                           const_ptr<float> q, int j, int cend, float2 *colp)
+{
+    float c1[8], c2[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int jj = TAIL ? min(j + u, cend - 1) : j + u;
+        float bx = q[3 * jj], by = q[3 * jj + 1], bz = q[3 * jj + 2];
+        if (TAIL && j + u >= cend) // wave-uniform
+            bx = by = bz = -kInf;
+        c1[u] = c2[u] = kInf;
+#pragma unroll
+        for (int v = 0; v < kPairR; ++v) {
+            const float s = sqdist_f32(ax[v], ay[v], az[v], bx, by, bz);
+            m2[v] = __builtin_amdgcn_fmed3f(m1[v], m2[v], s);
+            m1[v] = fminf(m1[v], s);
+            c2[u] = __builtin_amdgcn_fmed3f(c1[u], c2[u], s);
+            c1[u] = fminf(c1[u], s);
         }
     }
-    for (; j < j1; ++j) {
-        const float s = sqdist_f32(ax, ay, az, q[3 * j], q[3 * j + 1], q[3 * j + 2]);
-        m2 = __builtin_amdgcn_fmed3f(m1, m2, s);
-        m1 = fminf(m1, s);
+    float o1, o2;
+    batch_merge(c1, c2, o1, o2);
+    const int lane = threadIdx.x & 63;
+    if ((lane & 7) == 0) {
+        const int col = j + 2 * (lane >> 4) + ((lane >> 3) & 1);
+        if (!TAIL || col < cend)
+            colp[col] = make_float2(o1, o2);
     }
-    if (valid)
-        d.partial[(size_t)ch * args.B * d.n_own + (size_t)b * d.n_own + a] = make_float2(m1, m2);
+}
+
+__global__ __launch_bounds__(kPairThreads) void k_top2_pairs(PairScan a)
+{
+    int t = blockIdx.x;
+    const int cb = t % a.S_r;
+    t /= a.S_r;
+    const int groups = (a.S_c + kPairWaves - 1) / kPairWaves;
+    const int g = t % groups, b = t / groups;
+    const int lane = threadIdx.x & 63;
+    // row block of this wave: lane l holds its rows l, l + 64, ...
+    const int rblk = g * kPairWaves + (int)(threadIdx.x >> 6);
+    if (rblk >= a.S_c) // the whole wave
+        return;
+    float ax[kPairR], ay[kPairR], az[kPairR], m1[kPairR], m2[kPairR];
+    const int rbase = rblk * 64 * kPairR;
+#pragma unroll
+    for (int v = 0; v < kPairR; ++v) {
+        const int i = rbase + v * 64 + lane;
+        if (i < a.N) {
+            const float *p = a.x + ((size_t)b * a.N + i) * 3;
+            ax[v] = p[0];
+            ay[v] = p[1];
+            az[v] = p[2];
+        } else {
+            ax[v] = ay[v] = az[v] = kInf;
+        }
+        m1[v] = m2[v] = kInf;
+    }
+    const int c0 = cb * a.chunk, cend = min(a.M, c0 + a.chunk);
+    const const_ptr<float> q = as_const(a.y + (size_t)b * a.M * 3);
+    float2 *colp = a.col_partial + ((size_t)rblk * a.B + b) * a.M;
+    int j = c0;
+    for (; j + 8 <= cend; j += 8)
+        pair_batch<false>(ax, ay, az, m1, m2, q, j, cend, colp);
+    if (j < cend)
+        pair_batch<true>(ax, ay, az, m1, m2, q, j, cend, colp);
+#pragma unroll
+    for (int v = 0; v < kPairR; ++v) {
+        const int i = rbase + v * 64 + lane;
+        if (i < a.N)
+            a.row_partial[(size_t)cb * a.B * a.N + (size_t)b * a.N + i] = make_float2(m1[v], m2[v]);
+    }
 }
 
 struct FinalizeArgs {
@@ -327,10 +463,26 @@ __global__ __launch_bounds__(kFusedT) void k_emit_compact_place(EmitArgs a, DevP
 
 } // namespace
 
-void launch_top2(const ScanDir &rows, const ScanDir &cols, int B, hipStream_t s)
+void choose_pair_scan(PairScan &p, int B, int N, int M)
 {
-    Top2Args a{{rows, cols}, B};
-    hipLaunchKernelGGL(k_top2, dim3(rows.tiles + cols.tiles), dim3(kBlock), 0, s, a);
+    // about kPairTargetWaves waves; chunks of 8 to kPairMaxChunk columns
+    p.B = B;
+    p.N = N;
+    p.M = M;
+    p.S_c = (N + 64 * kPairR - 1) / (64 * kPairR);
+    const int64_t blocks = (int64_t)B * p.S_c;
+    const int batches = (M + 7) / 8;
+    int64_t s = std::max<int64_t>(1, (kPairTargetWaves + blocks - 1) / blocks);
+    s = std::max<int64_t>(s, (batches + kPairMaxChunk / 8 - 1) / (kPairMaxChunk / 8));
+    s = std::min<int64_t>(s, batches);
+    p.chunk = (int)((batches + s - 1) / s) * 8;
+    p.S_r = (M + p.chunk - 1) / p.chunk;
+}
+
+void launch_top2_pairs(const PairScan &p, hipStream_t s)
+{
+    const int groups = (p.S_c + kPairWaves - 1) / kPairWaves;
+    hipLaunchKernelGGL(k_top2_pairs, dim3((unsigned)((int64_t)p.B * groups * p.S_r)), dim3(kPairThreads), 0, s, p);
 }
 
 void launch_finalize(const FinalizeDir &rows, const FinalizeDir &cols, int B, const Params &p,
