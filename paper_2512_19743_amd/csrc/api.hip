@@ -613,15 +613,17 @@ apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t
         if (tmp.failed || dense_tmp.failed || keep.failed)
             return fail(APML_ERR_OUT_OF_MEMORY, "device allocation failed (statistics)");
         {
+            // the statistics phase: the scan and the merge of its partials
             PhaseTimer pt(PH_STATS, s, timed);
             launch_top2_pairs(ps, s);
             HIP_TRY(hipGetLastError());
+            FinalizeDir fr{ps.row_partial, x, dv.m12_row, E_row, nullptr, nullptr, nullptr, N, ps.S_r, kp.lk_row};
+            FinalizeDir fc{ps.col_partial, y, dv.m12_col, nullptr, ypack, col_cnt, ba.col_fill, M, ps.S_c,
+                           kp.lk_col};
+            launch_finalize(fr, fc, B, kp, dv.ctr, s); // also clears the counters
+            HIP_TRY(hipGetLastError());
             pt.stop();
         }
-        FinalizeDir fr{ps.row_partial, x, dv.m12_row, E_row, nullptr, nullptr, nullptr, N, ps.S_r, kp.lk_row};
-        FinalizeDir fc{ps.col_partial, y, dv.m12_col, nullptr, ypack, col_cnt, ba.col_fill, M, ps.S_c, kp.lk_col};
-        launch_finalize(fr, fc, B, kp, dv.ctr, s); // also clears the counters
-        HIP_TRY(hipGetLastError());
 
         // ---- dense scan 2: candidate support -----------------------------
         ea.x = x;
@@ -707,13 +709,13 @@ apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t
             launch_batch_boxes(sa.box_x, sa.box_y, batch_x, batch_y, B, pad_x, pad_y, false, s);
             launch_cull_top2(crows, ccols, B, dv.ctr, s);
             HIP_TRY(hipGetLastError());
+            CullFinalizeDir fr{crows.m12s, sa.sx, dv.m12_row, E_row, nullptr, nullptr, nullptr, nullptr, N, pad_x,
+                               kp.lk_row};
+            CullFinalizeDir fc{ccols.m12s, sa.sy, dv.m12_col, nullptr, ypack, sa.box_y, col_cnt, ba.col_fill, M,
+                               pad_y, kp.lk_col};
+            launch_cull_finalize(fr, fc, B, kp, s);
             pt.stop();
         }
-        CullFinalizeDir fr{crows.m12s, sa.sx, dv.m12_row, E_row, nullptr, nullptr, nullptr, nullptr, N, pad_x,
-                           kp.lk_row};
-        CullFinalizeDir fc{ccols.m12s, sa.sy, dv.m12_col, nullptr, ypack, sa.box_y, col_cnt, ba.col_fill, M, pad_y,
-                           kp.lk_col};
-        launch_cull_finalize(fr, fc, B, kp, s);
         // the column batches again, now with their largest emission threshold
         launch_batch_boxes(sa.box_x, sa.box_y, batch_x, batch_y, B, pad_x, pad_y, true, s);
         HIP_TRY(hipGetLastError());

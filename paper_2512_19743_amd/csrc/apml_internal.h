@@ -83,22 +83,22 @@ struct FinalizeDir {
 };
 
 
-// The minimum scan with one evaluation per pair (k_top2_pairs): each wave
-// takes a block of 64 kPairR rows (x) and one chunk of columns (y); its
-// per-row partials are the row direction's chunk partials (S = S_r), its
+// The minimum scan with one evaluation per pair (k_top2_pairs): each
+// workgroup takes a block of 64 kPairR rows (x) and one chunk of columns (y);
+// its per-row partials are the row direction's chunk partials (S = S_r), its
 // per-column partials those of the column direction (S = S_c, one per row
 // block).
 constexpr int kPairR = 8;            // rows per lane
-constexpr int kPairWaves = 4;        // waves (row blocks) per workgroup
+constexpr int kPairWaves = 4;        // waves per workgroup (a quarter of the chunk each)
 constexpr int kPairThreads = 64 * kPairWaves;
-constexpr int kPairMaxChunk = 2048;  // columns per chunk at most
+constexpr int kPairMaxChunk = 4096;  // columns per chunk at most
 constexpr int kPairTargetWaves = 8192;
 struct PairScan {
     const float *x, *y;  // [B, N, 3], [B, M, 3]
     float2 *row_partial; // [S_r][B * N]
     float2 *col_partial; // [S_c][B * M]
     int B, N, M;
-    int chunk, S_r;      // columns per chunk (a multiple of 8) and chunks
+    int chunk, S_r;      // columns per chunk (a multiple of 32) and chunks
     int S_c;             // row blocks of 64 kPairR rows
 };
 void choose_pair_scan(PairScan &p, int B, int N, int M);

@@ -35,9 +35,10 @@ namespace {
 // the minimum scan with one evaluation per pair
 // ---------------------------------------------------------------------------
 //
-// Each wave takes kPairR rows per lane (64 kPairR rows of a sample) and one
-// chunk of columns, which it streams through scalar registers in batches of
-// eight, as the support scan streams them. A pair costs the six operations
+// A workgroup takes 64 kPairR rows of a sample, held by each of its waves
+// (kPairR per lane), and one chunk of columns, a quarter per wave, which a
+// wave streams through scalar registers in batches of eight, as the support
+// scan streams them; the waves' row statistics are merged in LDS at the end. A pair costs the six operations
 // of its distance, two for its row's statistics (in the lane's registers)
 // and two for its column's statistics over the lane's rows, against 16 when
 // rows and columns are scanned separately. After each batch the eight
@@ -162,18 +163,16 @@ __device__ __forceinline__ void pair_batch(const float (&ax)[kPairR], const floa
     }
 }
 
-__global__ __launch_bounds__(kPairThreads) void k_top2_pairs(PairScan a)
+__global__ __launch_bounds__(kPairThreads, 4) void k_top2_pairs(PairScan a)
 {
+    __shared__ float2 rows[kPairWaves][64 * kPairR]; // the waves' row statistics, merged at the end
     int t = blockIdx.x;
     const int cb = t % a.S_r;
     t /= a.S_r;
-    const int groups = (a.S_c + kPairWaves - 1) / kPairWaves;
-    const int g = t % groups, b = t / groups;
-    const int lane = threadIdx.x & 63;
-    // row block of this wave: lane l holds its rows l, l + 64, ...
-    const int rblk = g * kPairWaves + (int)(threadIdx.x >> 6);
-    if (rblk >= a.S_c) // the whole wave
-        return;
+    const int rblk = t % a.S_c, b = t / a.S_c;
+    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    // the workgroup's 64 kPairR rows, lane l holding rows l, l + 64, ... in
+    // every wave; wave w takes the w-th quarter of the workgroup's columns
     float ax[kPairR], ay[kPairR], az[kPairR], m1[kPairR], m2[kPairR];
     const int rbase = rblk * 64 * kPairR;
 #pragma unroll
@@ -189,7 +188,8 @@ __global__ __launch_bounds__(kPairThreads) void k_top2_pairs(PairScan a)
         }
         m1[v] = m2[v] = kInf;
     }
-    const int c0 = cb * a.chunk, cend = min(a.M, c0 + a.chunk);
+    const int sub = a.chunk / kPairWaves;
+    const int c0 = cb * a.chunk + w * sub, cend = min(a.M, c0 + sub);
     const const_ptr<float> q = as_const(a.y + (size_t)b * a.M * 3);
     float2 *colp = a.col_partial + ((size_t)rblk * a.B + b) * a.M;
     int j = c0;
@@ -198,10 +198,21 @@ __global__ __launch_bounds__(kPairThreads) void k_top2_pairs(PairScan a)
     if (j < cend)
         pair_batch<true>(ax, ay, az, m1, m2, q, j, cend, colp);
 #pragma unroll
-    for (int v = 0; v < kPairR; ++v) {
-        const int i = rbase + v * 64 + lane;
-        if (i < a.N)
-            a.row_partial[(size_t)cb * a.B * a.N + (size_t)b * a.N + i] = make_float2(m1[v], m2[v]);
+    for (int v = 0; v < kPairR; ++v)
+        rows[w][v * 64 + lane] = make_float2(m1[v], m2[v]);
+    __syncthreads();
+    for (int k = threadIdx.x; k < 64 * kPairR; k += kPairThreads) {
+        const int i = rbase + k;
+        if (i >= a.N)
+            break;
+        float r1 = kInf, r2 = kInf;
+#pragma unroll
+        for (int u = 0; u < kPairWaves; ++u) { // top-2 of the union of the waves' top-2 multisets
+            const float2 e = rows[u][k];
+            r2 = fminf(fmaxf(r1, e.x), fminf(r2, e.y));
+            r1 = fminf(r1, e.x);
+        }
+        a.row_partial[(size_t)cb * a.B * a.N + (size_t)b * a.N + i] = make_float2(r1, r2);
     }
 }
 
@@ -465,24 +476,24 @@ __global__ __launch_bounds__(kFusedT) void k_emit_compact_place(EmitArgs a, DevP
 
 void choose_pair_scan(PairScan &p, int B, int N, int M)
 {
-    // about kPairTargetWaves waves; chunks of 8 to kPairMaxChunk columns
+    // about kPairTargetWaves waves; each workgroup's chunk a multiple of 32
+    // columns (eight per wave and batch), at most kPairMaxChunk
     p.B = B;
     p.N = N;
     p.M = M;
     p.S_c = (N + 64 * kPairR - 1) / (64 * kPairR);
     const int64_t blocks = (int64_t)B * p.S_c;
-    const int batches = (M + 7) / 8;
-    int64_t s = std::max<int64_t>(1, (kPairTargetWaves + blocks - 1) / blocks);
-    s = std::max<int64_t>(s, (batches + kPairMaxChunk / 8 - 1) / (kPairMaxChunk / 8));
-    s = std::min<int64_t>(s, batches);
-    p.chunk = (int)((batches + s - 1) / s) * 8;
+    const int unit = 8 * kPairWaves, units = (M + unit - 1) / unit;
+    int64_t s = std::max<int64_t>(1, (kPairTargetWaves / kPairWaves + blocks - 1) / blocks);
+    s = std::max<int64_t>(s, (units + kPairMaxChunk / unit - 1) / (kPairMaxChunk / unit));
+    s = std::min<int64_t>(s, units);
+    p.chunk = (int)((units + s - 1) / s) * unit;
     p.S_r = (M + p.chunk - 1) / p.chunk;
 }
 
 void launch_top2_pairs(const PairScan &p, hipStream_t s)
 {
-    const int groups = (p.S_c + kPairWaves - 1) / kPairWaves;
-    hipLaunchKernelGGL(k_top2_pairs, dim3((unsigned)((int64_t)p.B * groups * p.S_r)), dim3(kPairThreads), 0, s, p);
+    hipLaunchKernelGGL(k_top2_pairs, dim3((unsigned)((int64_t)p.B * p.S_c * p.S_r)), dim3(kPairThreads), 0, s, p);
 }
 
 void launch_finalize(const FinalizeDir &rows, const FinalizeDir &cols, int B, const Params &p,
