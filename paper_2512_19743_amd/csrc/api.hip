@@ -1056,8 +1056,8 @@ apml_status run_backward(apml_plan *plan, const float *x, const float *y, const 
             dv.rz = dv.adj;
             dv.kz = c.take<double>(plan->stored);
             dv.cbar = dv.kz;
-            dv.xyr = c.take<float4>((size_t)plan->B * plan->N);
-            dv.xyc = c.take<float4>((size_t)plan->B * plan->M);
+            dv.xyr = c.take<double4>((size_t)plan->B * plan->N);
+            dv.xyc = c.take<double4>((size_t)plan->B * plan->M);
         } else {
             dv.cbar = c.take<double>(plan->stored);
         }

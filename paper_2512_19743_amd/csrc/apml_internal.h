@@ -318,7 +318,7 @@ struct DevPlan {
     float *grad_x, *grad_y;
     double *adj, *cbar;           // [nnz] row-major
     double *dvec;                 // [B*N] row losses of the per-iteration forward kernels
-    float4 *xyr, *xyc;            // [B*N], [B*M] per-owner values of the per-iteration reverse sweeps: X, Y and
+    double4 *xyr, *xyc;           // [B*N], [B*M] per-owner values of the per-iteration reverse sweeps: X, Y and
                                   // the reciprocal of the owner's scaling
     double *rz, *kz;              // [nnz] reverse-sweep adjoints in row and in column order (per-iteration
                                   // kernels; rz shares adj's memory and cbar kz's)

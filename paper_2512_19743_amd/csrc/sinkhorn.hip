@@ -1542,9 +1542,10 @@ __global__ __launch_bounds__(kBlock) void k_zero_u32(uint32_t *a, int n)
 // per-iteration kernels (any N, M): one launch per sweep
 // ---------------------------------------------------------------------------
 //
-// kSG lanes per owner (row or column); each lane issues the loads of kSB of
-// its pairs together before using them. Sums are per lane in pair order,
-// then a butterfly over the group, so results do not depend on scheduling.
+// G lanes per owner (row or column; steps_lanes); each lane issues the loads
+// of kSB of its pairs together before using them. Sums are per lane in pair
+// order, then a butterfly over the group, so results do not depend on
+// scheduling.
 constexpr int kSG = 4;
 constexpr int kSB = 8;
 
@@ -1557,30 +1558,30 @@ __global__ __launch_bounds__(kBlock) void k_fill_ones(double *a, int n)
 
 // Sum over owner o's pairs k = lg, lg + kSG, ... of f(k, position) with the
 // loads of kSB pairs in flight at once.
-template <class Load, class Use>
+template <int G = kSG, class Load, class Use>
 __device__ __forceinline__ double owner_sum(int n, int lg, Load load, Use use)
 {
     double acc = 0.0;
-    for (int k0 = lg; k0 < n; k0 += kSG * kSB) {
+    for (int k0 = lg; k0 < n; k0 += G * kSB) {
         decltype(load(0)) v[kSB];
 #pragma unroll
         for (int u = 0; u < kSB; ++u)
-            v[u] = load(k0 + kSG * u < n ? k0 + kSG * u : -1);
+            v[u] = load(k0 + G * u < n ? k0 + G * u : -1);
 #pragma unroll
         for (int u = 0; u < kSB; ++u)
-            if (k0 + kSG * u < n)
+            if (k0 + G * u < n)
                 acc += use(v[u]);
     }
-    return group_sum<kSG>(acc);
+    return group_sum<G>(acc);
 }
 
 // Column step (Eq. 3, COL) or row step (Eq. 4) of iteration l for all owners.
-template <bool COL> __global__ __launch_bounds__(kBlock) void k_sink_step(DevPlan d, int l, double eps)
+template <bool COL, int G> __global__ __launch_bounds__(kBlock) void k_sink_step(DevPlan d, int l, double eps)
 {
     // each XCD takes a contiguous range of owners: its L2 holds only the
     // other side's scalings of those owners' samples
     const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x;
-    const int o = gid / kSG, lg = gid % kSG;
+    const int o = gid / G, lg = gid % G;
     const int n_own = COL ? d.M : d.N, n_oth = COL ? d.N : d.M;
     if (o >= d.B * n_own)
         return;
@@ -1599,7 +1600,7 @@ template <bool COL> __global__ __launch_bounds__(kBlock) void k_sink_step(DevPla
         float p;
         double x;
     };
-    const double acc = owner_sum(n, lg,
+    const double acc = owner_sum<G>(n, lg,
                                  [&](int k) {
                                      V v{0.0f, 0.0};
                                      if (k >= 0) {
@@ -1615,10 +1616,10 @@ template <bool COL> __global__ __launch_bounds__(kBlock) void k_sink_step(DevPla
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_loss_rows(DevPlan d, double *loss_rows)
+template <int G> __global__ __launch_bounds__(kBlock) void k_loss_rows(DevPlan d, double *loss_rows)
 {
     const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // as in k_sink_step
-    const int r = gid / kSG, lg = gid % kSG;
+    const int r = gid / G, lg = gid % G;
     if (r >= d.B * d.N)
         return;
     const int b = r / d.N;
@@ -1629,7 +1630,7 @@ __global__ __launch_bounds__(kBlock) void k_loss_rows(DevPlan d, double *loss_ro
         float p;
         double bc;
     };
-    const double acc = owner_sum(n, lg,
+    const double acc = owner_sum<G>(n, lg,
                                  [&](int k) {
                                      V v{0.0f, 0.0};
                                      if (k >= 0) {
@@ -1684,9 +1685,9 @@ __global__ __launch_bounds__(kLossT) void k_loss_reduce(DevPlan d, const double 
 // where the row update of iteration l is z' = (z / alpha^l_i) X_j - Y_j with
 // the column values published last, and the column update z' = (z / beta^l_j)
 // X_i - Y_i with the row values of iteration l. The other side's values of a
-// pair arrive in one 16-byte gather; sums and updates are double.
-__device__ __forceinline__ float rinv(double v) { return __builtin_amdgcn_rcpf((float)v); }
-
+// pair arrive in one 32-byte gather; values, sums and updates are double
+// (single-precision factors left gradient errors of 1e-5 that moved with the
+// rounding of the sums).
 __global__ __launch_bounds__(kBlock) void k_bwd_init(DevPlan d)
 {
     const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
@@ -1700,33 +1701,33 @@ __global__ __launch_bounds__(kBlock) void k_bwd_init(DevPlan d)
     }
     if (g < (int64_t)BM) { // no pending column update before the last iteration
         const double bl = d.beta[(size_t)d.L * BM + g];
-        d.xyc[g] = make_float4((float)bl, 0.0f, rinv(bl), 0.0f);
+        d.xyc[g] = make_double4(bl, 0.0, 1.0 / bl, 0.0);
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_bwd_rows(DevPlan d, int l)
+template <int G> __global__ __launch_bounds__(kBlock) void k_bwd_rows(DevPlan d, int l)
 {
     const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // as in k_sink_step
-    const int r = gid / kSG, lg = gid % kSG;
+    const int r = gid / G, lg = gid % G;
     if (r >= d.B * d.N)
         return;
     const int b = r / d.N;
     const size_t BN = (size_t)d.B * d.N;
-    const float4 *xyc = d.xyc + (size_t)b * d.M;
+    const double4 *xyc = d.xyc + (size_t)b * d.M;
     const bool pending = l < d.L;
-    const float4 mine = pending ? d.xyr[r] : make_float4(0.0f, 0.0f, 0.0f, 0.0f); // row values of iteration l+1
+    const double4 mine = pending ? d.xyr[r] : make_double4(0.0, 0.0, 0.0, 0.0); // row values of iteration l+1
     const double al = d.alpha[(size_t)l * BN + r];
-    const double inv_a = (double)rinv(al);
+    const double inv_a = 1.0 / al;
     const int t0 = d.row_ptr[r], n = d.row_ptr[r + 1] - t0;
     struct V {
         double z;
         float p;
         int k;
-        float4 c;
+        double4 c;
     };
-    const double acc = owner_sum(n, lg,
+    const double acc = owner_sum<G>(n, lg,
                                  [&](int k) {
-                                     V v{0.0, 0.0f, k, make_float4(0.0f, 0.0f, 1.0f, 0.0f)};
+                                     V v{0.0, 0.0f, k, make_double4(0.0, 0.0, 1.0, 0.0)};
                                      if (k >= 0) {
                                          const int j = d.csr_col[t0 + k];
                                          v.z = d.rz[t0 + k];
@@ -1738,39 +1739,39 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(DevPlan d, int l)
                                  [&](const V &v) {
                                      double z = v.z;
                                      if (pending) // 1/beta^(l+1)_j
-                                         z = __builtin_fma(z * (double)v.c.z, (double)mine.x, -(double)mine.y);
-                                     z = __builtin_fma(z * inv_a, (double)v.c.x, -(double)v.c.y);
+                                         z = __builtin_fma(z * v.c.z, mine.x, -mine.y);
+                                     z = __builtin_fma(z * inv_a, v.c.x, -v.c.y);
                                      d.rz[t0 + v.k] = z;
                                      return z * (double)v.p;
                                  });
     if (lg == 0) { // adjoint of Eq. 4: d_i = alpha^l_i * sum
         const double dsum = al * acc;
-        d.xyr[r] = make_float4((float)al, (float)(dsum * al), (float)inv_a, 0.0f);
+        d.xyr[r] = make_double4(al, dsum * al, inv_a, 0.0);
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_bwd_cols(DevPlan d, int l)
+template <int G> __global__ __launch_bounds__(kBlock) void k_bwd_cols(DevPlan d, int l)
 {
     const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // as in k_sink_step
-    const int gc = gid / kSG, lg = gid % kSG;
+    const int gc = gid / G, lg = gid % G;
     if (gc >= d.B * d.M)
         return;
     const int b = gc / d.M;
     const size_t BM = (size_t)d.B * d.M;
-    const float4 *xyr = d.xyr + (size_t)b * d.N;
-    const float4 mine = d.xyc[gc]; // column values published last
+    const double4 *xyr = d.xyr + (size_t)b * d.N;
+    const double4 mine = d.xyc[gc]; // column values published last
     const double bl = d.beta[(size_t)l * BM + gc];
-    const double inv_b = (double)rinv(bl);
+    const double inv_b = 1.0 / bl;
     const int s0 = d.col_ptr[gc], n = d.col_ptr[gc + 1] - s0;
     struct V {
         double z;
         float p;
         int k;
-        float4 rw;
+        double4 rw;
     };
-    const double acc = owner_sum(n, lg,
+    const double acc = owner_sum<G>(n, lg,
                                  [&](int k) {
-                                     V v{0.0, 0.0f, k, make_float4(0.0f, 0.0f, 1.0f, 0.0f)};
+                                     V v{0.0, 0.0f, k, make_double4(0.0, 0.0, 1.0, 0.0)};
                                      if (k >= 0) {
                                          const int i = d.csc_row[s0 + k];
                                          v.z = d.kz[s0 + k];
@@ -1780,15 +1781,14 @@ __global__ __launch_bounds__(kBlock) void k_bwd_cols(DevPlan d, int l)
                                      return v;
                                  },
                                  [&](const V &v) { // v.rw.z = 1/alpha^l_i
-                                     double z = __builtin_fma(v.z * (double)v.rw.z, (double)mine.x,
-                                                              -(double)mine.y);
-                                     z = __builtin_fma(z * inv_b, (double)v.rw.x, -(double)v.rw.y);
+                                     double z = __builtin_fma(v.z * v.rw.z, mine.x, -mine.y);
+                                     z = __builtin_fma(z * inv_b, v.rw.x, -v.rw.y);
                                      d.kz[s0 + v.k] = z;
                                      return z * (double)v.p;
                                  });
     if (lg == 0) { // adjoint of Eq. 3: e_j = beta^l_j * sum
         const double esum = bl * acc;
-        d.xyc[gc] = make_float4((float)bl, (float)(esum * bl), (float)inv_b, 0.0f);
+        d.xyc[gc] = make_double4(bl, esum * bl, inv_b, 0.0);
     }
 }
 
@@ -1800,10 +1800,10 @@ __global__ __launch_bounds__(kBlock) void k_bwd_final(DevPlan d)
     if (t >= d.nnz)
         return;
     const int r = d.csr_row[t], b = r / d.N, j = d.csr_col[t];
-    const float4 rw = d.xyr[r];
-    const float4 c = d.xyc[(size_t)b * d.M + j]; // c.z = 1/beta^1_j
-    double z = __builtin_fma(d.rz[t] * (double)c.z, (double)rw.x, -(double)rw.y);
-    d.adj[t] = z * (double)c.x - (double)c.y;
+    const double4 rw = d.xyr[r];
+    const double4 c = d.xyc[(size_t)b * d.M + j]; // c.z = 1/beta^1_j
+    double z = __builtin_fma(d.rz[t] * c.z, rw.x, -rw.y);
+    d.adj[t] = z * c.x - c.y;
 }
 
 } // namespace
@@ -2004,29 +2004,60 @@ hipError_t launch_sinkhorn_bwd(const DevPlan &d, int64_t max_pairs, hipStream_t 
     return hipGetLastError();
 }
 
+namespace {
+
+// Lanes per owner of the per-iteration kernels: the largest power of two
+// up to the owners' mean pair count, within 4..16 (rows of 18 pairs on
+// average: 16 lanes took the sweeps of the unequal workload from 0.38 / 0.79
+// ms to 0.29 / 0.61 ms; at 5 pairs, 4 lanes stay the fastest).
+int steps_lanes(int64_t nnz, int64_t owners)
+{
+    int g = kSG;
+    while (g < 16 && (int64_t)g * 2 * owners <= nnz)
+        g *= 2;
+    return g;
+}
+
+template <template <int> class K, class... A>
+void launch_lanes(int g, int64_t owners, hipStream_t s, A... args)
+{
+    switch (g) {
+    case 8: hipLaunchKernelGGL(K<8>::fn, dim3(blocks_for(owners * 8, kBlock)), dim3(kBlock), 0, s, args...); break;
+    case 16: hipLaunchKernelGGL(K<16>::fn, dim3(blocks_for(owners * 16, kBlock)), dim3(kBlock), 0, s, args...); break;
+    default: hipLaunchKernelGGL(K<4>::fn, dim3(blocks_for(owners * 4, kBlock)), dim3(kBlock), 0, s, args...); break;
+    }
+}
+template <int G> struct ColStep { static constexpr auto fn = k_sink_step<true, G>; };
+template <int G> struct RowStep { static constexpr auto fn = k_sink_step<false, G>; };
+template <int G> struct BwdRows { static constexpr auto fn = k_bwd_rows<G>; };
+template <int G> struct BwdCols { static constexpr auto fn = k_bwd_cols<G>; };
+template <int G> struct LossRows { static constexpr auto fn = k_loss_rows<G>; };
+
+} // namespace
+
 void launch_sinkhorn_fwd_steps(const DevPlan &d, double eps, hipStream_t s)
 {
     const int BN = d.B * d.N, BM = d.B * d.M;
+    const int gr = steps_lanes(d.nnz, BN), gc = steps_lanes(d.nnz, BM);
     hipLaunchKernelGGL(k_fill_ones, dim3(blocks_for(BN, kBlock)), dim3(kBlock), 0, s, d.alpha, BN);
     hipLaunchKernelGGL(k_fill_ones, dim3(blocks_for(BM, kBlock)), dim3(kBlock), 0, s, d.beta, BM);
     for (int l = 1; l <= d.L; ++l) {
-        hipLaunchKernelGGL(k_sink_step<true>, dim3(blocks_for((int64_t)BM * kSG, kBlock)), dim3(kBlock), 0, s, d, l,
-                           eps);
-        hipLaunchKernelGGL(k_sink_step<false>, dim3(blocks_for((int64_t)BN * kSG, kBlock)), dim3(kBlock), 0, s, d, l,
-                           eps);
+        launch_lanes<ColStep>(gc, BM, s, d, l, eps);
+        launch_lanes<RowStep>(gr, BN, s, d, l, eps);
     }
     // the backward scratch is free during the forward pass: use it for the row losses
-    hipLaunchKernelGGL(k_loss_rows, dim3(blocks_for((int64_t)BN * kSG, kBlock)), dim3(kBlock), 0, s, d, d.dvec);
+    launch_lanes<LossRows>(gr, BN, s, d, d.dvec);
     hipLaunchKernelGGL(k_loss_reduce, dim3(d.B), dim3(kLossT), 0, s, d, (const double *)d.dvec);
 }
 
 void launch_sinkhorn_bwd_steps(const DevPlan &d, hipStream_t s)
 {
     const int BN = d.B * d.N, BM = d.B * d.M;
+    const int gr = steps_lanes(d.nnz, BN), gc = steps_lanes(d.nnz, BM);
     hipLaunchKernelGGL(k_bwd_init, dim3(blocks_for(std::max<int64_t>(d.nnz, BM), kBlock)), dim3(kBlock), 0, s, d);
     for (int l = d.L; l >= 1; --l) {
-        hipLaunchKernelGGL(k_bwd_rows, dim3(blocks_for((int64_t)BN * kSG, kBlock)), dim3(kBlock), 0, s, d, l);
-        hipLaunchKernelGGL(k_bwd_cols, dim3(blocks_for((int64_t)BM * kSG, kBlock)), dim3(kBlock), 0, s, d, l);
+        launch_lanes<BwdRows>(gr, BN, s, d, l);
+        launch_lanes<BwdCols>(gc, BM, s, d, l);
     }
     hipLaunchKernelGGL(k_bwd_final, dim3(blocks_for(d.nnz, kBlock)), dim3(kBlock), 0, s, d);
 }
