@@ -25,13 +25,20 @@
 namespace apml {
 namespace {
 
-// G lanes per owner: 4, or 8 where the grid of 8 stays within 2^21 lanes and
-// that of 4 would hold fewer than 2^19 + 1 (measured: 8 lanes were 45 us
-// faster on 4 x 65536 points and 100 us slower on 64 x 8192 points, where
-// they double an already full grid; on 32 x 2048 points no faster).
-__host__ inline int softmax_lanes(int64_t owners)
+// G lanes per owner: the larger of two rules. By grid: 8 where the grid of 8
+// stays within 2^21 lanes and that of 4 would hold fewer than 2^19 + 1
+// (measured: 8 lanes were 45 us faster on 4 x 65536 points and 100 us slower
+// on 64 x 8192 points, where they double an already full grid; on 32 x 2048
+// points no faster), else 4. By pairs: the largest power of two up to the
+// owners' mean pair count, at most 16 (rows of 18 pairs at the unequal
+// workload: forward softmax 187 -> 112 us and its adjoint 183 -> 136 us with
+// 16 lanes instead of 4).
+__host__ inline int softmax_lanes(int64_t owners, int64_t pairs)
 {
-    return owners * 8 <= (int64_t(1) << 21) && owners * 4 > (int64_t(1) << 19) ? 8 : kGroup;
+    int g = owners * 8 <= (int64_t(1) << 21) && owners * 4 > (int64_t(1) << 19) ? 8 : kGroup;
+    while (g < 16 && 2 * g * owners <= pairs)
+        g *= 2;
+    return g;
 }
 
 // The forward softmax of one owner (a row, or a column) by its group of G
@@ -558,11 +565,13 @@ bool csc_sample_fits(int N, int M, int64_t max_pairs)
 }
 
 // Launches kernel template K with the lanes per owner of `owners`.
-#define APML_LAUNCH_G(K, owners, per_block, shmem, s, ...)                                                          \
+#define APML_LAUNCH_G(K, owners, pairs, per_block, shmem, s, ...)                                                   \
     do {                                                                                                           \
-        const int g_ = softmax_lanes(owners);                                                                      \
+        const int g_ = softmax_lanes(owners, pairs);                                                               \
         const dim3 grid_(blocks_for((int64_t)(owners) * g_, per_block));                                           \
-        if (g_ == 8)                                                                                               \
+        if (g_ == 16)                                                                                              \
+            hipLaunchKernelGGL(K<16>, grid_, dim3(per_block), shmem, s, __VA_ARGS__);                              \
+        else if (g_ == 8)                                                                                          \
             hipLaunchKernelGGL(K<8>, grid_, dim3(per_block), shmem, s, __VA_ARGS__);                               \
         else                                                                                                       \
             hipLaunchKernelGGL(K<kGroup>, grid_, dim3(per_block), shmem, s, __VA_ARGS__);                          \
@@ -572,32 +581,36 @@ hipError_t launch_csc_and_softmax(const DevPlan &d, const Params &p, int64_t max
 {
     const size_t bytes = csc_sample_lds(d.M, max_pairs);
     const int64_t BN = (int64_t)d.B * d.N;
-    const int gr = softmax_lanes(BN);
-    const void *k = gr == 8 ? (const void *)k_csc_rows<8> : (const void *)k_csc_rows<kGroup>;
+    const int gr = softmax_lanes(BN, d.nnz);
+    const void *k = gr == 16  ? (const void *)k_csc_rows<16>
+                    : gr == 8 ? (const void *)k_csc_rows<8>
+                              : (const void *)k_csc_rows<kGroup>;
     hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess)
         return e;
     const unsigned rows = blocks_for(BN * gr, kCscT);
-    if (gr == 8)
+    if (gr == 16)
+        hipLaunchKernelGGL(k_csc_rows<16>, dim3(d.B + rows), dim3(kCscT), bytes, s, d, p);
+    else if (gr == 8)
         hipLaunchKernelGGL(k_csc_rows<8>, dim3(d.B + rows), dim3(kCscT), bytes, s, d, p);
     else
         hipLaunchKernelGGL(k_csc_rows<kGroup>, dim3(d.B + rows), dim3(kCscT), bytes, s, d, p);
-    APML_LAUNCH_G(k_col_softmax, (int64_t)d.B * d.M, kBlock, 0, s, d, p);
+    APML_LAUNCH_G(k_col_softmax, (int64_t)d.B * d.M, d.nnz, kBlock, 0, s, d, p);
     return hipGetLastError();
 }
 
 void launch_softmax(const DevPlan &d, const Params &p, hipStream_t s)
 {
-    APML_LAUNCH_G(k_row_softmax, (int64_t)d.B * d.N, kBlock, 0, s, d, p);
-    APML_LAUNCH_G(k_col_softmax, (int64_t)d.B * d.M, kBlock, 0, s, d, p);
+    APML_LAUNCH_G(k_row_softmax, (int64_t)d.B * d.N, d.nnz, kBlock, 0, s, d, p);
+    APML_LAUNCH_G(k_col_softmax, (int64_t)d.B * d.M, d.nnz, kBlock, 0, s, d, p);
 }
 
 void launch_bwd_softmax(const DevPlan &d, const Params &p, hipStream_t s)
 {
-    APML_LAUNCH_G(k_bwd_col_softmax, (int64_t)d.B * d.M, kBlock, 0, s, d, p);
-    APML_LAUNCH_G(k_bwd_row_softmax, (int64_t)d.B * d.N, kBlock, 0, s, d, p, d.grad_y != nullptr ? 1 : 0);
+    APML_LAUNCH_G(k_bwd_col_softmax, (int64_t)d.B * d.M, d.nnz, kBlock, 0, s, d, p);
+    APML_LAUNCH_G(k_bwd_row_softmax, (int64_t)d.B * d.N, d.nnz, kBlock, 0, s, d, p, d.grad_y != nullptr ? 1 : 0);
     if (d.grad_y)
-        APML_LAUNCH_G(k_bwd_grad_y, (int64_t)d.B * d.M, kBlock, 0, s, d, p);
+        APML_LAUNCH_G(k_bwd_grad_y, (int64_t)d.B * d.M, d.nnz, kBlock, 0, s, d, p);
 }
 
 #undef APML_LAUNCH_G
