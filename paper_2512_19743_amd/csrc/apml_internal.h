@@ -396,7 +396,8 @@ void launch_wide_pack(const DevPlan &d, int32_t *place, hipStream_t s);
 // Workgroups per sample of the split streamed kernels for a batch of B on the
 // current device (2..kSplitMax; every workgroup of the grid must be resident
 // at once), or 1 when the one-workgroup kernels are taken (also when the
-// environment sets APML_SINKHORN_SPLIT=0).
+// environment sets APML_SINKHORN_SPLIT=0; =streamed keeps the split kernels'
+// streamed variants at every share).
 constexpr int kSplitMax = 8;
 constexpr int kSplitSyncStride = 32; // counters 128 bytes apart
 int sinkhorn_split_factor(int B);

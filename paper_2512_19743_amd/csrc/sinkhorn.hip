@@ -1140,7 +1140,19 @@ template <typename T> __device__ __forceinline__ void split_gather(T *lds, const
                    "s"(bs[7]), [off] "v"(off)                                                                 \
                  : "memory")
 
-__device__ __forceinline__ void split_gather_factors(float2 *lds, const float *yv, const double *own_prev, int n,
+// The saved scalings of the previous iteration that a gather pairs with the
+// exchanged words. The forward kernel wrote them, so they are loaded before
+// the meeting, in its shadow.
+__device__ __forceinline__ void load_prev(float (&sp)[8], const double *own_prev, int n)
+{
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int o = u * kT + (int)threadIdx.x;
+        sp[u] = o < n ? (float)own_prev[o] : 0.0f;
+    }
+}
+
+__device__ __forceinline__ void split_gather_factors(float2 *lds, const float *yv, const float (&sp)[8], int n,
                                                      bool local)
 {
     static_assert(kSinkOwnersW / kT == 8, "eight words per lane");
@@ -1154,12 +1166,6 @@ __device__ __forceinline__ void split_gather_factors(float2 *lds, const float *y
     for (int u = 0; u < 8; ++u)
         bs[u] = reinterpret_cast<const void *>((uintptr_t)(base + (uint64_t)u * kT * 4u));
     const uint32_t off = threadIdx.x * 4u;
-    float sp[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-        const int o = u * kT + (int)threadIdx.x;
-        sp[u] = o < n ? (float)own_prev[o] : 0.0f;
-    }
     uint32_t y[8];
     if (local) {
         asm volatile("buffer_inv sc0" ::: "memory"); // no line of an earlier read may serve these loads
@@ -1263,16 +1269,19 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_ws(DevPlan d, int K)
         float *yr = d.yr + (size_t)(L - l) * (BN + kSinkOwnersW) + (size_t)b * N;
         wide_reverse<true>(d.wk_row, b, n_row, d.wr, fc, nullptr, alpha + l * BN, alpha + (l - 1) * BN, k, K, loc,
                            yr);
+        float sp[8];
+        load_prev(sp, alpha + (l - 1) * BN, N);
         if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
             return;
-        split_gather_factors(fr, yr, alpha + (l - 1) * BN, N, loc);
+        split_gather_factors(fr, yr, sp, N, loc);
         lds_barrier();
         float *yc = d.yc + (size_t)(L - l) * (BM + kSinkOwnersW) + (size_t)b * M;
         wide_reverse<true>(d.wk_col, b, n_col, d.wc, fr, nullptr, beta + l * BM, beta + (l - 1) * BM, k, K, loc,
                            yc);
+        load_prev(sp, beta + (l - 1) * BM, M);
         if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
             return;
-        split_gather_factors(fc, yc, beta + (l - 1) * BM, M, loc);
+        split_gather_factors(fc, yc, sp, M, loc);
         lds_barrier();
     }
     wide_reverse_end(d, b, n_row, fc, k, K);
@@ -1283,9 +1292,15 @@ __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_ws(DevPlan d, int K)
 // adjoint copies of its positions) are loaded once and kept in registers for
 // every sweep, so a half-sweep reads nothing from memory but the owners'
 // saved scalings and the exchanged vector. Same lanes, same arithmetic in the
-// same order as the streamed kernels: the same bits.
+// same order as the streamed kernels: the same bits. A reverse share of up to
+// kSplitAdjBwd slots keeps only the adjoint copies (the state the sweeps
+// write) in registers and loads its pieces again in every phase: 28 bytes
+// read per slot and phase instead of 60 read and written.
 constexpr int kSplitRegFwd = 3; // slots per lane and order held by the forward kernel
 constexpr int kSplitRegBwd = 2; // and by the reverse kernel
+// adjoint copies held by the reverse kernel, pieces loaded per phase (at 4
+// slots it spills: 72 x 8000 x 8000, 0.413 ms against 0.399 ms streamed)
+constexpr int kSplitAdjBwd = 3;
 
 // Slots of the calling wave that workgroup k of K takes (wave-uniform).
 __device__ __forceinline__ int split_slots(int n_used, int k, int K)
@@ -1301,6 +1316,50 @@ __device__ __forceinline__ void load_my_slots(WSlot (&w)[SW], const Order &pk, i
     for (int q = 0; q < SW; ++q)
         if (q < n)
             w[q] = load_wslot(pk, b, k + q * K);
+}
+
+// The same loads, for a kernel that repeats them in every phase. They are
+// raw buffer loads: one descriptor per array and sample (scalar registers),
+// the slot and word as a scalar offset, and one lane offset shared by every
+// load. Plain pointers let the compiler hoist all the per-word addresses out
+// of the sweeps' loop and keep them in vector registers, which spilled. The
+// descriptor's size also bounds every load to the sample's own positions.
+struct SlotRsrc {
+    __amdgpu_buffer_rsrc_t p0, gi, info;
+};
+
+constexpr int kBufFlags = 0x00020000; // word 3 of a raw 32-bit buffer descriptor (gfx9 family)
+
+template <class Order> __device__ __forceinline__ SlotRsrc slot_rsrc(const Order &pk, int b)
+{
+    const size_t bs = (size_t)b * pk.slots;
+    SlotRsrc r;
+    r.p0 = __builtin_amdgcn_make_buffer_rsrc(pk.p0 + bs * kP * kT, (short)0, pk.slots * kP * kT * 4, kBufFlags);
+    r.gi = __builtin_amdgcn_make_buffer_rsrc(pk.gi + bs * (kP / 2) * kT, (short)0, pk.slots * (kP / 2) * kT * 4,
+                                             kBufFlags);
+    r.info = __builtin_amdgcn_make_buffer_rsrc(pk.info + bs * kT, (short)0, pk.slots * kT * 4, kBufFlags);
+    return r;
+}
+
+template <int SW>
+__device__ __forceinline__ void stream_my_slots(WSlot (&w)[SW], const SlotRsrc &r, int n, int k, int K)
+{
+    const int lane = (int)threadIdx.x * 4;
+#pragma unroll
+    for (int q = 0; q < SW; ++q)
+        if (q < n) {
+            const int s = k + q * K;
+#pragma unroll
+            for (int e = 0; e < kP; ++e)
+                w[q].p0[e] = __builtin_bit_cast(
+                    float, __builtin_amdgcn_raw_buffer_load_b32(r.p0, lane, (s * kP + e) * kT * 4, 0));
+#pragma unroll
+            for (int e = 0; e < kP / 2; ++e)
+                w[q].gi[e] = __builtin_amdgcn_raw_buffer_load_b32(r.gi, lane, (s * (kP / 2) + e) * kT * 4, 0);
+            w[q].info = __builtin_amdgcn_raw_buffer_load_b32(r.info, lane, s * kT * 4, 0);
+        } else {
+            w[q] = WSlot{}; // not read; keeps the compiler from holding earlier contents
+        }
 }
 
 // One forward half-sweep over the slots held in registers (as wide_sweep).
@@ -1433,7 +1492,7 @@ __device__ __forceinline__ void owner_scalings(const WSlot (&w)[SW], int n, cons
         }
 }
 
-template <int SW> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_wr(DevPlan d, int K)
+template <int SW, bool HOLD> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_wr(DevPlan d, int K)
 {
     constexpr int OB = 13; // owner bits of the streamed layout's info word
     __shared__ float2 fr[kSinkOwnersW]; // row factors (Yr_i, alpha^(l-1)_i)
@@ -1494,22 +1553,41 @@ template <int SW> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_wr(DevPla
     if (!split_begin(cnt, K, k, &d.ctr->error, &stop, &local))
         return;
     const bool loc = local != 0;
+    const SlotRsrc rsr = slot_rsrc(d.wk_row, b), rsc = slot_rsrc(d.wk_col, b);
+    // Loads that do not depend on the exchange are issued ahead of it: a
+    // phase's pieces (when streamed) and the gather's saved scalings before
+    // the meeting, the owners' scalings before the gather.
+    double al[SW], alp[SW];
+    owner_scalings<SW, OB>(pr, mr, alpha + L * BN, alpha + (L - 1) * BN, al, alp);
     uint32_t t = 1;
     for (int l = L; l >= 1; --l) {
-        double al[SW] = {}, alp[SW] = {};
-        owner_scalings<SW, OB>(pr, mr, alpha + l * BN, alpha + (l - 1) * BN, al, alp);
         float *yr = d.yr + (size_t)(L - l) * (BN + kSinkOwnersW) + (size_t)b * N;
         reg_reverse<SW, OB>(pr, rr, mr, al, alp, fc, yr, loc); // reverse of Eq. 4
+        if constexpr (!HOLD)
+            stream_my_slots(pc, rsc, mc, k, K);
+        float sp[8];
+        if constexpr (HOLD)
+            load_prev(sp, alpha + (l - 1) * BN, N);
         if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
             return;
-        split_gather_factors(fr, yr, alpha + (l - 1) * BN, N, loc);
-        lds_barrier();
         owner_scalings<SW, OB>(pc, mc, beta + l * BM, beta + (l - 1) * BM, al, alp);
+        if constexpr (!HOLD)
+            load_prev(sp, alpha + (l - 1) * BN, N);
+        split_gather_factors(fr, yr, sp, N, loc);
+        lds_barrier();
         float *yc = d.yc + (size_t)(L - l) * (BM + kSinkOwnersW) + (size_t)b * M;
         reg_reverse<SW, OB>(pc, rc, mc, al, alp, fr, yc, loc); // reverse of Eq. 3
+        if constexpr (!HOLD)
+            stream_my_slots(pr, rsr, mr, k, K); // the next row phase's, or the closing pass's
+        if constexpr (HOLD)
+            load_prev(sp, beta + (l - 1) * BM, M);
         if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
             return;
-        split_gather_factors(fc, yc, beta + (l - 1) * BM, M, loc);
+        if (l > 1)
+            owner_scalings<SW, OB>(pr, mr, alpha + (l - 1) * BN, alpha + (l - 2) * BN, al, alp);
+        if constexpr (!HOLD)
+            load_prev(sp, beta + (l - 1) * BM, M);
+        split_gather_factors(fc, yc, sp, M, loc);
         lds_barrier();
     }
     // the adjoint with respect to P0, r - Yc_j, in row-major order
@@ -1891,10 +1969,21 @@ bool launch_split(const void *kernel, void **args, const DevPlan &d, int K, hipS
     return true;
 }
 
+// APML_SINKHORN_SPLIT=streamed keeps the split kernels but takes their
+// streamed variants at any share (the variants give the same bits; this
+// lets them be compared).
+bool split_streamed_only()
+{
+    const char *env = std::getenv("APML_SINKHORN_SPLIT");
+    return env && env[0] == 's';
+}
+
 // The split kernel for a workgroup share of sw slots per lane and order:
 // registers up to the limit, else streamed.
 const void *split_fwd_kernel(int sw)
 {
+    if (split_streamed_only())
+        return reinterpret_cast<const void *>(k_sinkhorn_fwd_ws);
     switch (sw) {
     case 1: return reinterpret_cast<const void *>(k_sinkhorn_fwd_wr<1>);
     case 2: return reinterpret_cast<const void *>(k_sinkhorn_fwd_wr<2>);
@@ -1905,14 +1994,17 @@ const void *split_fwd_kernel(int sw)
 
 const void *split_bwd_kernel(int sw)
 {
+    if (split_streamed_only())
+        return reinterpret_cast<const void *>(k_sinkhorn_bwd_ws);
     switch (sw) {
-    case 1: return reinterpret_cast<const void *>(k_sinkhorn_bwd_wr<1>);
-    case 2: return reinterpret_cast<const void *>(k_sinkhorn_bwd_wr<2>);
+    case 1: return reinterpret_cast<const void *>(k_sinkhorn_bwd_wr<1, true>);
+    case 2: return reinterpret_cast<const void *>(k_sinkhorn_bwd_wr<2, true>);
+    case 3: return reinterpret_cast<const void *>(k_sinkhorn_bwd_wr<3, false>);
     default: return reinterpret_cast<const void *>(k_sinkhorn_bwd_ws);
     }
 }
 
-static_assert(kSplitRegFwd == 3 && kSplitRegBwd == 2, "instances above");
+static_assert(kSplitRegFwd == 3 && kSplitRegBwd == 2 && kSplitAdjBwd == 3, "instances above");
 
 } // namespace
 

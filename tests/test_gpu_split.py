@@ -23,8 +23,11 @@ def _gpu():
     apml.load()
 
 
-def _run(X, Y, n_iter, split, monkeypatch):
-    monkeypatch.setenv("APML_SINKHORN_SPLIT", "1" if split else "0")
+def _run(X, Y, n_iter, mode, monkeypatch):
+    # mode "0": one workgroup per sample; "1": split, pieces (or the reverse
+    # adjoint) in registers where a workgroup's share allows; "streamed":
+    # split, streamed variants only
+    monkeypatch.setenv("APML_SINKHORN_SPLIT", mode)
     # an untimed call first: the phase times below are of loaded kernels
     run_gpu(X, Y, n_iter=n_iter)["plan"].close()
     torch.cuda.synchronize()
@@ -57,6 +60,9 @@ CASES = {
     # one sample with enough pieces for the split forward kernel, B N < 8192
     # (and B not a multiple of 8: seven of the grid's eight rounds end at once)
     "b1_n8000": lambda: custom(75, 1, 8000, 7990, reference="primitives", prediction="perm_noise", sigma=0.02),
+    # B = 72: three workgroups per sample (a grid of 216), a larger share of
+    # each sample's pieces per workgroup
+    "b72_n8000": lambda: custom(76, 72, 8000, 8000, reference="primitives", prediction="perm_noise", sigma=0.02),
 }
 
 
@@ -65,14 +71,16 @@ def test_split_matches_one_workgroup(case, monkeypatch):
     X, Y = CASES[case]()
     n_iter = 20 if case == "large_batch" else 10
     note(f"split streamed Sinkhorn: {case} B={X.shape[0]} N={X.shape[1]} M={Y.shape[1]} L={n_iter}")
-    one = _run(X, Y, n_iter, False, monkeypatch)
-    split = _run(X, Y, n_iter, True, monkeypatch)
-    note(f"{case}: Sinkhorn {one['ms'][0]:.3f} -> {split['ms'][0]:.3f} ms, "
-         f"reverse sweeps {one['ms'][1]:.3f} -> {split['ms'][1]:.3f} ms")
-    np.testing.assert_array_equal(split["nnz"], one["nnz"])
-    np.testing.assert_array_equal(split["loss"], one["loss"])
-    np.testing.assert_array_equal(split["gx"], one["gx"])
-    np.testing.assert_array_equal(split["gy"], one["gy"])
-    for b in range(X.shape[0]):
-        np.testing.assert_array_equal(split["v"][b], one["v"][b])
-    assert np.isfinite(split["loss"]).all()
+    one = _run(X, Y, n_iter, "0", monkeypatch)
+    streamed = _run(X, Y, n_iter, "streamed", monkeypatch)
+    split = _run(X, Y, n_iter, "1", monkeypatch)
+    note(f"{case}: Sinkhorn {one['ms'][0]:.3f} -> {streamed['ms'][0]:.3f} (streamed) / {split['ms'][0]:.3f} ms, "
+         f"reverse sweeps {one['ms'][1]:.3f} -> {streamed['ms'][1]:.3f} (streamed) / {split['ms'][1]:.3f} ms")
+    for other in (streamed, split):
+        np.testing.assert_array_equal(other["nnz"], one["nnz"])
+        np.testing.assert_array_equal(other["loss"], one["loss"])
+        np.testing.assert_array_equal(other["gx"], one["gx"])
+        np.testing.assert_array_equal(other["gy"], one["gy"])
+        for b in range(X.shape[0]):
+            np.testing.assert_array_equal(other["v"][b], one["v"][b])
+        assert np.isfinite(other["loss"]).all()
