@@ -19,8 +19,9 @@
 //              skipped when its gap exceeds the current second minimum of
 //              every owner of the wave: it cannot change either statistic.
 //              The run at the owners' own place along the curve goes first,
-//              then the remaining runs of each batch of 64 in increasing gap,
-//              so that the bound tightens as early as possible.
+//              then the batches of 64 runs in increasing gap and the runs of
+//              each batch in increasing gap, so that the bound tightens as
+//              early as possible.
 //   k_cull_finalize back in the original order, each row's and column's emission
 //              threshold: the kept set s >= tau is the ball
 //              C <= C1 + log(1/tau)/T (Sec. III-B, Eq. 1), widened by a small
@@ -214,44 +215,58 @@ __global__ __launch_bounds__(kBlock) void k_cull_top2(Top2Args args)
     const int home = min(nb - 1, (int)(((int64_t)g * kScanRows + kScanRows / 2) * d.n_bc / d.n_own / kRun));
     if (home % kWaves == wv)
         scan_run(home);
+    // Batches of 64 runs, 64 batches at a time (one per lane): the gaps of all
+    // of them are formed at once, then the batches within the current bound
+    // are visited nearest first. A batch beyond the bound costs one lane's
+    // box test instead of a pass of the wave's loop.
+    // The batch holding the home run goes first (its key 0; the others' keys
+    // order them by gap).
     const int nbatch = (nb + 63) / 64;
-    int base = home / 64 * 64;
-    const_ptr<f32x4> batch = as_const(reinterpret_cast<const f32x4 *>(d.bc_batch + (size_t)b * batches(d.pad_bc)));
-    for (int t = 0; t < nbatch; ++t, base = base + 64 >= nbatch * 64 ? 0 : base + 64) {
-        // the whole batch first: its box against the largest current bound
-        {
-            const f32x4 lo = batch[2 * (base / 64)], hi = batch[2 * (base / 64) + 1];
-            const float g2 = box_gap2(wb, make_float4(lo.x, lo.y, lo.z, 0.0f), make_float4(hi.x, hi.y, hi.z, 0.0f));
-            const float lb = bound();
-            if (g2 > wave_max_nonneg(valid ? lb : 0.0f))
-                continue;
+    const Box *bboxes = d.bc_batch + (size_t)b * batches(d.pad_bc);
+    for (int c0 = 0; c0 < nbatch; c0 += 64) {
+        bool blive = c0 + lane < nbatch;
+        float bgap = kInf;
+        if (blive) {
+            const Box bx = bboxes[c0 + lane];
+            bgap = box_gap2(wb, bx.lo, bx.hi);
         }
-        const int r = base + lane;
-        bool live = r < nb && r != home && r % kWaves == wv;
-        float4 blo = make_float4(0.0f, 0.0f, 0.0f, 0.0f), bhi = blo;
-        if (live) {
-            blo = boxes[r].lo;
-            bhi = boxes[r].hi;
-        }
-        const float gap = live ? box_gap2(wb, blo, bhi) : kInf;
+        const uint32_t bkey = c0 + lane == home / 64 ? 0u : __float_as_uint(bgap) + 1u;
         for (;;) {
-            const float lb = bound();
             // the largest current second minimum over the owners (a cross-lane
             // reduction: evaluated with every lane active, never under a condition)
-            const float wave_lb = wave_max_nonneg(valid ? lb : 0.0f);
-            live = live && !(gap > wave_lb);
-            const uint64_t todo = __ballot(live);
-            if (!todo)
+            const float wave_bb = wave_max_nonneg(valid ? bound() : 0.0f);
+            blive = blive && !(bgap > wave_bb);
+            if (!__ballot(blive))
                 break;
-            // the nearest remaining run next
-            const uint32_t gmin = wave_min_u32(live ? __float_as_uint(gap) : 0xFFFFFFFFu);
-            const uint64_t pick = __ballot(live && __float_as_uint(gap) == gmin);
-            const int i = __ffsll((unsigned long long)pick) - 1;
-            live = live && lane != i;
-            // and only if the run can matter to one of the owners themselves
-            const float pg = lane_box_gap2(a, blo, bhi, i);
-            if (__ballot(valid && !(pg > lb)))
-                scan_run(base + i);
+            const uint32_t bmin = wave_min_u32(blive ? bkey : 0xFFFFFFFFu);
+            const int bi = __ffsll((unsigned long long)__ballot(blive && bkey == bmin)) - 1;
+            blive = blive && lane != bi;
+            const int base = (c0 + bi) * 64;
+            const int r = base + lane;
+            bool live = r < nb && r != home && r % kWaves == wv;
+            float4 blo = make_float4(0.0f, 0.0f, 0.0f, 0.0f), bhi = blo;
+            if (live) {
+                blo = boxes[r].lo;
+                bhi = boxes[r].hi;
+            }
+            const float gap = live ? box_gap2(wb, blo, bhi) : kInf;
+            for (;;) {
+                const float lb = bound();
+                const float wave_lb = wave_max_nonneg(valid ? lb : 0.0f);
+                live = live && !(gap > wave_lb);
+                const uint64_t todo = __ballot(live);
+                if (!todo)
+                    break;
+                // the nearest remaining run next
+                const uint32_t gmin = wave_min_u32(live ? __float_as_uint(gap) : 0xFFFFFFFFu);
+                const uint64_t pick = __ballot(live && __float_as_uint(gap) == gmin);
+                const int i = __ffsll((unsigned long long)pick) - 1;
+                live = live && lane != i;
+                // and only if the run can matter to one of the owners themselves
+                const float pg = lane_box_gap2(a, blo, bhi, i);
+                if (__ballot(valid && !(pg > lb)))
+                    scan_run(base + i);
+            }
         }
     }
     __syncthreads();
@@ -361,57 +376,62 @@ template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_cull_emit(Cull
     if (wv == 0)
         acc[0][lane] = 0;
     __syncthreads();
-    const_ptr<f32x4> batch = as_const(reinterpret_cast<const f32x4 *>(a.batch_y + (size_t)b * batches(a.pad_y)));
-    for (int base = 0; base < nb; base += 64) {
-        { // the whole batch first
-            const f32x4 lo = batch[2 * (base / 64)], hi = batch[2 * (base / 64) + 1];
-            const float g2 = box_gap2(wb, make_float4(lo.x, lo.y, lo.z, 0.0f), make_float4(hi.x, hi.y, hi.z, 0.0f));
-            if (g2 > fmaxf(wave_E, hi.w))
-                continue;
+    // the batches of 64 runs first, 64 of them at a time (one per lane); the
+    // runs of the batches that can hold a hit then in increasing order
+    const Box *bboxes = a.batch_y + (size_t)b * batches(a.pad_y);
+    const int nbatch = (nb + 63) / 64;
+    for (int c0 = 0; c0 < nbatch; c0 += 64) {
+        bool reach = false;
+        if (c0 + lane < nbatch) {
+            const Box bx = bboxes[c0 + lane];
+            reach = !(box_gap2(wb, bx.lo, bx.hi) > fmaxf(wave_E, bx.hi.w));
         }
-        const int r = base + lane;
-        bool take = false;
-        float4 blo = make_float4(0.0f, 0.0f, 0.0f, 0.0f), bhi = blo;
-        if (r < nb && r % kWaves == wv) {
-            blo = boxes[r].lo;
-            bhi = boxes[r].hi;
-            take = !(box_gap2(wb, blo, bhi) > fmaxf(wave_E, bhi.w));
-        }
-        uint64_t todo = __ballot(take);
-        while (todo) {
-            const int rr = base + __ffsll((unsigned long long)todo) - 1;
-            todo &= todo - 1;
-            const int i = rr - base;
-            const float run_E = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bhi.w), i));
-            const float gap = lane_box_gap2(pa, blo, bhi, i);
-            if (!__ballot(valid && !(gap > fmaxf(E, run_E)))) // no row of the wave can reach the run
-                continue;
-            const int j0 = rr * kRun, n = min(kRun, a.M - j0);
-            // one bit per column, the run's first column in the top bit
-            uint32_t bits = 0;
-            if (n == kRun) {
-#pragma unroll
-                for (int u = 0; u < kRun; ++u)
-                    bits = shift_in_hit(bits, pa.x, pa.y, pa.z, E, yp[j0 + u]);
-            } else {
-                for (int u = 0; u < n; ++u)
-                    bits = shift_in_hit(bits, pa.x, pa.y, pa.z, E, yp[j0 + u]);
-                bits <<= kRun - n;
+        for (uint64_t btodo = __ballot(reach); btodo; btodo &= btodo - 1) {
+            const int base = (c0 + __ffsll((unsigned long long)btodo) - 1) * 64;
+            const int r = base + lane;
+            bool take = false;
+            float4 blo = make_float4(0.0f, 0.0f, 0.0f, 0.0f), bhi = blo;
+            if (r < nb && r % kWaves == wv) {
+                blo = boxes[r].lo;
+                bhi = boxes[r].hi;
+                take = !(box_gap2(wb, blo, bhi) > fmaxf(wave_E, bhi.w));
             }
-            bits &= keep;
-            cols += n;
-            while (bits) {
-                const int u = __clz(bits);
-                bits &= ~(0x80000000u >> u);
-                const int j = __float_as_int(sy[j0 + u].w);
-                const int slot = atomicAdd(&acc[0][lane], 1); // this row's hits over the waves
-                if (WRITE) {
-                    a.tmp_col[pos0 + slot] = j;
-                    a.csr_row[pos0 + slot] = row;
+            uint64_t todo = __ballot(take);
+            while (todo) {
+                const int rr = base + __ffsll((unsigned long long)todo) - 1;
+                todo &= todo - 1;
+                const int i = rr - base;
+                const float run_E = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bhi.w), i));
+                const float gap = lane_box_gap2(pa, blo, bhi, i);
+                if (!__ballot(valid && !(gap > fmaxf(E, run_E)))) // no row of the wave can reach the run
+                    continue;
+                const int j0 = rr * kRun, n = min(kRun, a.M - j0);
+                // one bit per column, the run's first column in the top bit
+                uint32_t bits = 0;
+                if (n == kRun) {
+#pragma unroll
+                    for (int u = 0; u < kRun; ++u)
+                        bits = shift_in_hit(bits, pa.x, pa.y, pa.z, E, yp[j0 + u]);
                 } else {
-                    if (slot < kCullStage)
-                        a.stage[(size_t)row * kCullStage + slot] = j;
-                    atomicAdd(&a.col_cnt[(size_t)b * a.M + j], 1);
+                    for (int u = 0; u < n; ++u)
+                        bits = shift_in_hit(bits, pa.x, pa.y, pa.z, E, yp[j0 + u]);
+                    bits <<= kRun - n;
+                }
+                bits &= keep;
+                cols += n;
+                while (bits) {
+                    const int u = __clz(bits);
+                    bits &= ~(0x80000000u >> u);
+                    const int j = __float_as_int(sy[j0 + u].w);
+                    const int slot = atomicAdd(&acc[0][lane], 1); // this row's hits over the waves
+                    if (WRITE) {
+                        a.tmp_col[pos0 + slot] = j;
+                        a.csr_row[pos0 + slot] = row;
+                    } else {
+                        if (slot < kCullStage)
+                            a.stage[(size_t)row * kCullStage + slot] = j;
+                        atomicAdd(&a.col_cnt[(size_t)b * a.M + j], 1);
+                    }
                 }
             }
         }
