@@ -599,8 +599,10 @@ apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t
                 const size_t staged = (size_t)BN * ea.S * ea.kst;
                 ea.stage = c.take<uint16_t>(ea.stage_narrow ? (staged + 1) / 2 : staged);
                 const size_t tiles = (size_t)B * ea.S * owner_blocks;
-                ea.spill = c.take<uint32_t>(tiles * kTileSpill);
-                ea.spill_n = c.take<int32_t>(tiles);
+                // a region's base is a 32-bit offset
+                ea.spill_cap = std::min<int64_t>((int64_t)tiles * kSpillPerTile, INT32_MAX - kBlock - kTileList);
+                ea.spill = c.take<uint16_t>((size_t)ea.spill_cap);
+                ea.spill_base = c.take<int32_t>(tiles);
             }
         };
         {

@@ -19,7 +19,9 @@ constexpr int kScanSlots = 64;
 struct Counters {
     unsigned int error;            // bit 0: a row's minima not found among its pairs; bit 1: a column's;
                                    // bit 2: a meeting of the split streamed Sinkhorn kernels timed out
-    unsigned int overflow;         // a (row, chunk) of the full support scan had more hits than its staging slots
+    unsigned int overflow;         // a tile of the full support scan (a row of the skipping one) is written by
+                                   // a second pass: its further hits did not fit
+    unsigned int spill_fill;       // entries taken from the full support scan's pool of further hits
     // pairs evaluated by the skipping scans (minimum scan, support scan), in
     // kScanSlots partial sums: workgroup w adds to slot w % kScanSlots, so
     // that no single address takes every workgroup's atomic
@@ -108,12 +110,15 @@ void launch_finalize(const FinalizeDir &rows, const FinalizeDir &cols, int B, co
 
 // The counting pass of the support scan keeps the first kst hits of every
 // (row, chunk) (kst = stage_slots(S), at most kStage: fewer when the columns
-// are cut into many chunks, each of which then holds few of a row's hits) and
-// the further hits of a tile (kBlock rows, one chunk) in a tile list of
-// kTileSpill entries; only when a tile list overflows does the writing pass
-// scan that tile again.
+// are cut into many chunks, each of which then holds few of a row's hits).
+// The further hits of a tile (kBlock rows, one chunk), up to kTileList, are
+// collected in LDS and, once the tile is scanned, written row by row into a
+// region of a shared pool (kSpillPerTile 16-bit entries per tile on
+// average): kBlock row starts, then the hits. Only a tile whose hits exceed
+// its list or find the pool full is scanned again by the writing pass.
 constexpr int kStage = 16;
-constexpr int kTileSpill = 512;
+constexpr int kTileList = 2048;
+constexpr int kSpillPerTile = 1024;
 inline int stage_slots(int S) { return S >= 32 ? 2 : S >= 16 ? 4 : S >= 8 ? 8 : kStage; }
 
 struct EmitArgs {
@@ -127,8 +132,9 @@ struct EmitArgs {
                          // one byte each when stage_narrow (chunks of at most 256 columns)
     int kst;             // staged hits per (row, chunk)
     int stage_narrow;
-    uint32_t *spill;     // [tiles][kTileSpill]: further hits, row within the tile << 16 | offset in the chunk
-    int32_t *spill_n;    // [tiles]: entries of the tile list (more than kTileSpill: overflowed)
+    uint16_t *spill;     // pool of further hits: per tile kBlock row starts, then the offsets in the chunk
+    int64_t spill_cap;   // entries of the pool
+    int32_t *spill_base; // [tiles]: the tile's region in the pool; -1: the tile is scanned again
     Counters *ctr;
     // second pass (or compaction of the staged hits)
     const int32_t *row_ptr; // [B*N+1]

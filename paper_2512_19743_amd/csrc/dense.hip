@@ -16,11 +16,13 @@
 //              column's threshold. Per pair 6 VALU ops for the distance, a max
 //              of the two radii, a compare and an add-with-carry that records
 //              the hit in a per-lane bitmask of 32 columns. A first pass counts
-//              the hits per (row, column chunk) and per column; once the
-//              offsets are known, a second pass writes each row's pairs, in
-//              column order, straight into the CSR arrays. The exact test
-//              s >= tau is applied later in double precision on this
-//              candidate set.
+//              the hits per (row, column chunk) and per column and keeps them
+//              (the first few of every (row, chunk) in its slots, the rest of
+//              a tile in a pool region); once the offsets are known, a
+//              compaction writes each row's pairs, in column order, into the
+//              CSR arrays. Only tiles whose hits did not fit are scanned a
+//              second time. The exact test s >= tau is applied later in
+//              double precision on this candidate set.
 #include <algorithm>
 #include <utility>
 
@@ -230,6 +232,7 @@ __global__ __launch_bounds__(kBlock) void k_finalize(FinalizeArgs args)
     if (k == 0) { // the full scans leave the skipping scans' counts unused
         args.ctr->error = 0;
         args.ctr->overflow = 0;
+        args.ctr->spill_fill = 0;
     }
     const int which = k < args.rows ? 0 : 1;
     if (which)
@@ -333,7 +336,8 @@ __device__ __forceinline__ int stage_get(const EmitArgs &a, size_t slot, int k)
 // same decisions.
 template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs a)
 {
-    __shared__ int n_spill;
+    __shared__ uint2 list[kTileList]; // further hits: row in the tile << 16 | offset, rank in the row's
+    __shared__ int row_start[kBlock], wave_sum[kBlock / 64], n_list, base_sh;
     const int t = blockIdx.x;
     const int ob = t % a.owner_blocks;
     const int rest = t / a.owner_blocks;
@@ -353,9 +357,8 @@ template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs 
         int32_t *col_cnt = a.col_cnt + (size_t)b * a.M;
         const bool stage = a.stage != nullptr;
         const size_t slot = (size_t)row * a.S + ch;
-        uint32_t *spill = a.stage ? a.spill + (size_t)t * kTileSpill : nullptr;
         if (threadIdx.x == 0)
-            n_spill = 0;
+            n_list = 0;
         __syncthreads();
         int cnt = 0;
         for_each_hit(ax, ay, az, E, q, j0, j1, keep, [&](int j) {
@@ -363,26 +366,66 @@ template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs 
             if (stage) {
                 if (cnt < a.kst) {
                     stage_put(a, slot, cnt, j - j0);
-                } else { // in increasing j for each row
-                    const int k = atomicAdd(&n_spill, 1);
-                    if (k < kTileSpill)
-                        spill[k] = (uint32_t)threadIdx.x << 16 | (uint32_t)(j - j0);
+                } else {
+                    const int k = atomicAdd(&n_list, 1);
+                    if (k < kTileList)
+                        list[k] = make_uint2((uint32_t)threadIdx.x << 16 | (uint32_t)(j - j0), cnt - a.kst);
                 }
             }
             ++cnt;
         });
         if (valid)
-            a.cnt[(size_t)row * a.S + ch] = cnt;
-        if (stage) {
+            a.cnt[slot] = cnt;
+        const int extra = max(cnt - a.kst, 0);
+        if (stage && !__syncthreads_or(extra > 0)) { // every hit of the tile in its slots
+            if (threadIdx.x == 0)
+                a.spill_base[t] = 0;
+        } else if (stage) {
+            // the rows' starts in the tile's region: an exclusive scan of
+            // their further hits over the workgroup
+            const int lane = lane_id(), wave = threadIdx.x >> 6;
+            int incl = extra;
+            for (int o = 1; o < 64; o <<= 1) {
+                const int v = __shfl_up(incl, o);
+                if (lane >= o)
+                    incl += v;
+            }
+            if (lane == 63)
+                wave_sum[wave] = incl;
             __syncthreads();
+            int before = 0, total = 0;
+#pragma unroll
+            for (int w = 0; w < kBlock / 64; ++w) {
+                before += w < wave ? wave_sum[w] : 0;
+                total += wave_sum[w];
+            }
+            row_start[threadIdx.x] = before + incl - extra;
             if (threadIdx.x == 0) {
-                a.spill_n[t] = n_spill;
-                if (n_spill > kTileSpill)
+                int base = total == 0 ? 0 : -1;
+                if (total > 0 && total <= kTileList) {
+                    const int64_t need = kBlock + total;
+                    const int64_t got = atomicAdd(&a.ctr->spill_fill, (unsigned int)need);
+                    if (got + need <= a.spill_cap)
+                        base = (int)got;
+                }
+                if (base < 0)
                     atomicOr(&a.ctr->overflow, 1u);
+                a.spill_base[t] = base;
+                base_sh = base;
+            }
+            __syncthreads();
+            const int base = base_sh;
+            if (total > 0 && base >= 0) {
+                uint16_t *reg = a.spill + base;
+                reg[threadIdx.x] = (uint16_t)row_start[threadIdx.x];
+                for (int u = threadIdx.x; u < total; u += kBlock) {
+                    const uint2 e = list[u];
+                    reg[kBlock + row_start[e.x >> 16] + (int)e.y] = (uint16_t)(e.x & 0xFFFFu);
+                }
             }
         }
     } else {
-        if (a.stage && a.spill_n[t] <= kTileSpill) // rescan only the tiles whose list overflowed
+        if (a.stage && a.spill_base[t] >= 0) // rescan only the tiles whose further hits did not fit
             return;
         int pos = a.row_ptr[row];
         for (int c = 0; c < ch; ++c)
@@ -397,7 +440,7 @@ template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs 
 
 // CSR from the staged hits: one thread per (row, chunk) writes its hits at
 // the row's offset plus the hits of the row's earlier chunks; hits beyond
-// kst come from the tile list, in list order (increasing column). With
+// kst come from the row's part of its tile's pool region (increasing column). With
 // PLACE, each pair also takes a slot in its column segment (k_csc_sort then
 // fixes the order inside the segment).
 template <bool PLACE>
@@ -425,8 +468,8 @@ template <bool PLACE> __device__ __forceinline__ void emit_compact_thread(const 
     for (int c = 0; c < ch; ++c)
         pos += cnt[c];
     const int n = cnt[ch];
-    const int n_spill = a.spill_n[t];
-    if (n_spill > kTileSpill) // the writing pass rescans this tile
+    const int base = a.spill_base[t];
+    if (base < 0) // the writing pass rescans this tile
         return;
     const int j0 = ch * a.chunk, gc0 = b * a.M + j0;
     const int ns = min(n, a.kst);
@@ -436,16 +479,13 @@ template <bool PLACE> __device__ __forceinline__ void emit_compact_thread(const 
             const int jj = stage_get(a, (size_t)g, k);
             emit_pair<PLACE>(a, pos + k, row, i, gc0 + jj, j0 + jj);
         }
-    if (n > a.kst) {
-        const uint32_t *sp = a.spill + (size_t)t * kTileSpill;
-        const uint32_t me = (uint32_t)(i % kBlock);
-        int k = a.kst;
-        for (int u = 0; u < n_spill; ++u)
-            if (sp[u] >> 16 == me) {
-                const int jj = (int)(sp[u] & 0xFFFFu);
-                emit_pair<PLACE>(a, pos + k, row, i, gc0 + jj, j0 + jj);
-                ++k;
-            }
+    if (n > a.kst) { // the row's further hits, in increasing column, from the tile's region
+        const uint16_t *reg = a.spill + base;
+        const uint16_t *mine = reg + kBlock + reg[i % kBlock];
+        for (int k = a.kst; k < n; ++k) {
+            const int jj = mine[k - a.kst];
+            emit_pair<PLACE>(a, pos + k, row, i, gc0 + jj, j0 + jj);
+        }
     }
 }
 
