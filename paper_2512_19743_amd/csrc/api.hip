@@ -1089,7 +1089,10 @@ apml_status run_backward(apml_plan *plan, const float *x, const float *y, const 
     }
     {
         PhaseTimer pt(PH_BWD_SOFTMAX, s, plan->timed);
-        launch_bwd_softmax(dv, plan->kp, s);
+        // double-precision P where the reverse sweeps keep the adjoint in
+        // double too (per-iteration sweeps), or where there are none
+        const bool double_p = dv.L == 0 || (!plan->sink_bwd && !plan->sink_wide);
+        launch_bwd_softmax(dv, plan->kp, double_p, s);
         HIP_TRY(hipGetLastError());
         pt.stop();
     }

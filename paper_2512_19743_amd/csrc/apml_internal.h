@@ -356,7 +356,10 @@ bool csc_sample_fits(int N, int M, int64_t max_pairs);
 hipError_t launch_csc_and_softmax(const DevPlan &d, const Params &p, int64_t max_pairs, hipStream_t s);
 
 void launch_softmax(const DevPlan &d, const Params &p, hipStream_t s);
-void launch_bwd_softmax(const DevPlan &d, const Params &p, hipStream_t s);
+// Backward of both softmaxes and the distance gradient. double_p: P formed
+// again in double precision from the stored costs (for plans whose reverse
+// sweeps keep the adjoint in double, or that have none), else read as stored.
+void launch_bwd_softmax(const DevPlan &d, const Params &p, bool double_p, hipStream_t s);
 
 // Sinkhorn. The per-sample kernels run all iterations in one workgroup per
 // sample with the sample's pairs in registers; the per-iteration kernels are

@@ -18,6 +18,8 @@
 //     of the minimum (-) unless the gap was clamped; plus the direct term
 //     grad_loss * v of loss = sum v C; the row kernel turns Cbar into grad_x
 //     with Eq. 5, k_bwd_grad_y into grad_y.
+#include <type_traits>
+
 #include "apml_internal.h"
 #include "device_common.h"
 #include "pieces.h"
@@ -343,13 +345,32 @@ __device__ __forceinline__ double p0bar(const DevPlan &d, int t, double gl)
 }
 
 // Backward of one owner's softmax by its group of G lanes, with the first
-// kSmCache pairs of each lane loaded up front (as in the forward).
+// pairs of each lane loaded up front (as in the forward).
 //   columns: cbar_t = -T P_col (Pbar_t - sigma) on kept pairs, plus the gap
 //            term at the two argmins; written per pair (cbar).
 //   rows:    the same for P_row, plus cbar from the columns and the direct
 //            term grad_loss * v; then Eq. 5 turns cbar into grad_x.
-template <int G> __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(DevPlan d, Params p)
+// DP: P in double, formed again as the forward formed it before storing it in
+// single precision (same operations and lane order, so the same sum Z). The
+// temperature adjoint cancels, and it reaches the argmins multiplied by T / g,
+// large for a small gap: with stored single-precision P the gradient error
+// reached 5e-4 there, and 9e-6 on 16 x 4096 x 16384 points (2e-8 with DP).
+// Taken where the reverse sweeps keep the adjoint in double (or there are
+// none); the sweeps that keep it in LDS store it in single precision, which
+// then bounds the error as much (shape-completion workload: 6.7e-6 either
+// way), and P is read as stored. DP caches 4 pairs per lane instead of 8, so
+// that its exponentials leave four waves per SIMD.
+constexpr int kBwdCache = 4;
+
+template <bool DP> struct BwdP {
+    static constexpr int kCache = DP ? kBwdCache : kSmCache;
+    using T = std::conditional_t<DP, double, float>; // type of the cached P
+};
+
+template <int G, bool DP> __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(DevPlan d, Params p)
 {
+    constexpr int NC = BwdP<DP>::kCache;
+    using PT = typename BwdP<DP>::T;
     const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // a sample's owners share an L2
     const int gc = gid / G, lg = gid % G;
     if (gc >= d.B * d.M)
@@ -364,19 +385,20 @@ template <int G> __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(Dev
     const float y0 = yc[0], y1 = yc[1], y2 = yc[2];
     const float *xb = d.x + (size_t)b * d.N * 3;
 
-    int tq[kSmCache], iq[kSmCache];
-    float pq[kSmCache];
+    int tq[NC], iq[NC];
+    PT pq[NC];
 #pragma unroll
-    for (int c = 0; c < kSmCache; ++c) {
+    for (int c = 0; c < NC; ++c) {
         const int k = lg + G * c;
         tq[c] = k < n ? d.csc_perm[s0 + k] : 0;
         iq[c] = k < n ? d.csc_row[s0 + k] : 0;
-        pq[c] = k < n ? d.p_col[s0 + k] : 0.0f;
+        if constexpr (!DP)
+            pq[c] = k < n ? d.p_col[s0 + k] : 0.0f;
     }
-    double aq[kSmCache], cq[kSmCache];
-    bool kq[kSmCache];
+    double aq[NC], cq[NC];
+    bool kq[NC];
 #pragma unroll
-    for (int c = 0; c < kSmCache; ++c) {
+    for (int c = 0; c < NC; ++c) {
         const int k = lg + G * c;
         const uint8_t f = k < n ? d.flags[tq[c]] : 0;
         kq[c] = (f & 2) != 0;
@@ -384,26 +406,50 @@ template <int G> __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(Dev
         const float *xi = xb + 3 * (size_t)iq[c];
         cq[c] = kq[c] ? dist3(xi[0], xi[1], xi[2], y0, y1, y2) : 0.0;
     }
+    double zsum = 0.0;
+    if constexpr (DP) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            pq[c] = kq[c] ? exp(-T * (cq[c] - c1)) : 0.0;
+            zsum += pq[c];
+        }
+        for (int k = lg + G * NC; k < n; k += G) {
+            const int t = d.csc_perm[s0 + k];
+            if (d.flags[t] & 2)
+                zsum += exp(-T * (d.cost[t] - c1));
+        }
+        zsum = group_sum<G>(zsum);
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+            pq[c] = kq[c] ? pq[c] / zsum : 0.0;
+    }
+    // P of a kept pair past the cached ones (column-major entry q, row-major position t)
+    auto p_at = [&](int q, int t) -> double {
+        if constexpr (DP)
+            return exp(-T * (d.cost[t] - c1)) / zsum;
+        else
+            return (double)d.p_col[q];
+    };
     double sigma = 0.0;
 #pragma unroll
-    for (int c = 0; c < kSmCache; ++c)
+    for (int c = 0; c < NC; ++c)
         sigma += kq[c] ? (double)pq[c] * aq[c] : 0.0;
-    for (int k = lg + G * kSmCache; k < n; k += G) {
+    for (int k = lg + G * NC; k < n; k += G) {
         const int t = d.csc_perm[s0 + k];
         const uint8_t f = d.flags[t];
         if (f & 2)
-            sigma += (double)d.p_col[s0 + k] * (sym_weight(p, f) * p0bar(d, t, gl));
+            sigma += p_at(s0 + k, t) * (sym_weight(p, f) * p0bar(d, t, gl));
     }
     sigma = group_sum<G>(sigma);
     double tbar = 0.0;
 #pragma unroll
-    for (int c = 0; c < kSmCache; ++c)
+    for (int c = 0; c < NC; ++c)
         tbar -= kq[c] ? (double)pq[c] * (aq[c] - sigma) * (cq[c] - c1) : 0.0;
-    for (int k = lg + G * kSmCache; k < n; k += G) {
+    for (int k = lg + G * NC; k < n; k += G) {
         const int t = d.csc_perm[s0 + k];
         const uint8_t f = d.flags[t];
         if (f & 2)
-            tbar -= (double)d.p_col[s0 + k] * (sym_weight(p, f) * p0bar(d, t, gl) - sigma) * (d.cost[t] - c1);
+            tbar -= p_at(s0 + k, t) * (sym_weight(p, f) * p0bar(d, t, gl) - sigma) * (d.cost[t] - c1);
     }
     tbar = group_sum<G>(tbar);
     const double gapbar = gapbar_scale * tbar;
@@ -415,21 +461,24 @@ template <int G> __global__ __launch_bounds__(kBlock) void k_bwd_col_softmax(Dev
         return cb;
     };
 #pragma unroll
-    for (int c = 0; c < kSmCache; ++c) {
+    for (int c = 0; c < NC; ++c) {
         const int k = lg + G * c;
         if (k < n)
             d.cbar[tq[c]] = gap_terms(s0 + k, kq[c] ? -T * (double)pq[c] * (aq[c] - sigma) : 0.0);
     }
-    for (int k = lg + G * kSmCache; k < n; k += G) {
+    for (int k = lg + G * NC; k < n; k += G) {
         const int t = d.csc_perm[s0 + k];
         const uint8_t f = d.flags[t];
-        const double cb = (f & 2) ? -T * (double)d.p_col[s0 + k] * (sym_weight(p, f) * p0bar(d, t, gl) - sigma) : 0.0;
+        const double cb = (f & 2) ? -T * p_at(s0 + k, t) * (sym_weight(p, f) * p0bar(d, t, gl) - sigma) : 0.0;
         d.cbar[t] = gap_terms(s0 + k, cb);
     }
 }
 
-template <int G> __global__ __launch_bounds__(kBlock) void k_bwd_row_softmax(DevPlan d, Params p, int keep_cbar)
+template <int G, bool DP>
+__global__ __launch_bounds__(kBlock) void k_bwd_row_softmax(DevPlan d, Params p, int keep_cbar)
 {
+    constexpr int NC = BwdP<DP>::kCache;
+    using PT = typename BwdP<DP>::T;
     const int gid = xcd_contiguous(blockIdx.x, gridDim.x) * kBlock + threadIdx.x; // a sample's owners share an L2
     const int r = gid / G, lg = gid % G;
     if (r >= d.B * d.N)
@@ -447,52 +496,77 @@ template <int G> __global__ __launch_bounds__(kBlock) void k_bwd_row_softmax(Dev
     const double al = d.alpha[(size_t)d.L * BN + r];
     const double *bl = d.beta + (size_t)d.L * BM + (size_t)b * d.M;
 
-    int jq[kSmCache];
-    bool kq[kSmCache];
-    float pq[kSmCache], p0q[kSmCache];
-    double aq[kSmCache], cq[kSmCache], cbq[kSmCache];
+    int jq[NC];
+    bool kq[NC];
+    float p0q[NC];
+    PT pq[NC];
+    double aq[NC], cq[NC], cbq[NC];
 #pragma unroll
-    for (int c = 0; c < kSmCache; ++c) {
+    for (int c = 0; c < NC; ++c) {
         const int k = lg + G * c, t = t0 + k;
         const bool in = k < n;
         jq[c] = in ? d.csr_col[t] : 0;
         const uint8_t f = in ? d.flags[t] : 0;
         kq[c] = (f & 1) != 0;
-        pq[c] = in ? d.p_row[t] : 0.0f;
+        if constexpr (!DP) {
+            pq[c] = in ? d.p_row[t] : 0.0f;
+            cbq[c] = in ? d.cbar[t] : 0.0; // DP reads it where it is used
+        }
         p0q[c] = in ? d.p0r[t] : 0.0f;
         aq[c] = in ? sym_weight(p, f) * p0bar(d, t, gl) : 0.0;
         cq[c] = in ? d.cost[t] : 1.0;
-        cbq[c] = in ? d.cbar[t] : 0.0;
     }
+    double zsum = 0.0;
+    if constexpr (DP) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            pq[c] = kq[c] ? exp(-T * (cq[c] - c1)) : 0.0;
+            zsum += pq[c];
+        }
+        for (int k = lg + G * NC; k < n; k += G)
+            if (d.flags[t0 + k] & 1)
+                zsum += exp(-T * (d.cost[t0 + k] - c1));
+        zsum = group_sum<G>(zsum);
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+            pq[c] = kq[c] ? pq[c] / zsum : 0.0;
+    }
+    // P of a kept pair past the cached ones
+    auto p_at = [&](int t) -> double {
+        if constexpr (DP)
+            return exp(-T * (d.cost[t] - c1)) / zsum;
+        else
+            return (double)d.p_row[t];
+    };
     double sigma = 0.0;
 #pragma unroll
-    for (int c = 0; c < kSmCache; ++c)
+    for (int c = 0; c < NC; ++c)
         sigma += kq[c] ? (double)pq[c] * aq[c] : 0.0;
-    for (int k = lg + G * kSmCache; k < n; k += G) {
+    for (int k = lg + G * NC; k < n; k += G) {
         const int t = t0 + k;
         const uint8_t f = d.flags[t];
         if (f & 1)
-            sigma += (double)d.p_row[t] * (sym_weight(p, f) * p0bar(d, t, gl));
+            sigma += p_at(t) * (sym_weight(p, f) * p0bar(d, t, gl));
     }
     sigma = group_sum<G>(sigma);
     double tbar = 0.0;
 #pragma unroll
-    for (int c = 0; c < kSmCache; ++c)
+    for (int c = 0; c < NC; ++c)
         tbar -= kq[c] ? (double)pq[c] * (aq[c] - sigma) * (cq[c] - c1) : 0.0;
-    for (int k = lg + G * kSmCache; k < n; k += G) {
+    for (int k = lg + G * NC; k < n; k += G) {
         const int t = t0 + k;
         const uint8_t f = d.flags[t];
         if (f & 1)
-            tbar -= (double)d.p_row[t] * (sym_weight(p, f) * p0bar(d, t, gl) - sigma) * (d.cost[t] - c1);
+            tbar -= p_at(t) * (sym_weight(p, f) * p0bar(d, t, gl) - sigma) * (d.cost[t] - c1);
     }
     tbar = group_sum<G>(tbar);
     const double gapbar = gscale * tbar;
     double gx = 0.0, gy = 0.0, gz = 0.0;
     // cbar of pair t (column part cb0, P_row, dL/dP0, cost, P0, column j) into grad_x (Eq. 5)
-    auto add = [&](int t, int j, double cb0, bool kept, float prow, double a, double c, float p0) {
+    auto add = [&](int t, int j, double cb0, bool kept, double prow, double a, double c, float p0) {
         double cb = cb0 + gl * (al * (double)p0 * bl[j]);
         if (kept)
-            cb -= T * (double)prow * (a - sigma);
+            cb -= T * prow * (a - sigma);
         if (t == q2)
             cb += gapbar;
         if (t == q1)
@@ -506,15 +580,16 @@ template <int G> __global__ __launch_bounds__(kBlock) void k_bwd_row_softmax(Dev
             d.cbar[t] = cb;
     };
 #pragma unroll
-    for (int c = 0; c < kSmCache; ++c) {
+    for (int c = 0; c < NC; ++c) {
         const int k = lg + G * c;
         if (k < n)
-            add(t0 + k, jq[c], cbq[c], kq[c], pq[c], aq[c], cq[c], p0q[c]);
+            add(t0 + k, jq[c], DP ? d.cbar[t0 + k] : cbq[c], kq[c], (double)pq[c], aq[c], cq[c], p0q[c]);
     }
-    for (int k = lg + G * kSmCache; k < n; k += G) {
+    for (int k = lg + G * NC; k < n; k += G) {
         const int t = t0 + k;
         const uint8_t f = d.flags[t];
-        add(t, d.csr_col[t], d.cbar[t], (f & 1) != 0, d.p_row[t], sym_weight(p, f) * p0bar(d, t, gl), d.cost[t],
+        const bool kept = (f & 1) != 0;
+        add(t, d.csr_col[t], d.cbar[t], kept, kept ? p_at(t) : 0.0, sym_weight(p, f) * p0bar(d, t, gl), d.cost[t],
             d.p0r[t]);
     }
     gx = group_sum<G>(gx);
@@ -577,6 +652,19 @@ bool csc_sample_fits(int N, int M, int64_t max_pairs)
             hipLaunchKernelGGL(K<kGroup>, grid_, dim3(per_block), shmem, s, __VA_ARGS__);                          \
     } while (0)
 
+// The same for a kernel template with a second, boolean parameter X.
+#define APML_LAUNCH_GP(K, X, owners, pairs, s, ...)                                                                 \
+    do {                                                                                                           \
+        const int g_ = softmax_lanes(owners, pairs);                                                               \
+        const dim3 grid_(blocks_for((int64_t)(owners) * g_, kBlock));                                              \
+        if (g_ == 16)                                                                                              \
+            hipLaunchKernelGGL((K<16, X>), grid_, dim3(kBlock), 0, s, __VA_ARGS__);                                \
+        else if (g_ == 8)                                                                                          \
+            hipLaunchKernelGGL((K<8, X>), grid_, dim3(kBlock), 0, s, __VA_ARGS__);                                 \
+        else                                                                                                       \
+            hipLaunchKernelGGL((K<kGroup, X>), grid_, dim3(kBlock), 0, s, __VA_ARGS__);                            \
+    } while (0)
+
 hipError_t launch_csc_and_softmax(const DevPlan &d, const Params &p, int64_t max_pairs, hipStream_t s)
 {
     const size_t bytes = csc_sample_lds(d.M, max_pairs);
@@ -605,14 +693,21 @@ void launch_softmax(const DevPlan &d, const Params &p, hipStream_t s)
     APML_LAUNCH_G(k_col_softmax, (int64_t)d.B * d.M, d.nnz, kBlock, 0, s, d, p);
 }
 
-void launch_bwd_softmax(const DevPlan &d, const Params &p, hipStream_t s)
+void launch_bwd_softmax(const DevPlan &d, const Params &p, bool double_p, hipStream_t s)
 {
-    APML_LAUNCH_G(k_bwd_col_softmax, (int64_t)d.B * d.M, d.nnz, kBlock, 0, s, d, p);
-    APML_LAUNCH_G(k_bwd_row_softmax, (int64_t)d.B * d.N, d.nnz, kBlock, 0, s, d, p, d.grad_y != nullptr ? 1 : 0);
+    const int keep = d.grad_y != nullptr ? 1 : 0;
+    if (double_p) {
+        APML_LAUNCH_GP(k_bwd_col_softmax, true, (int64_t)d.B * d.M, d.nnz, s, d, p);
+        APML_LAUNCH_GP(k_bwd_row_softmax, true, (int64_t)d.B * d.N, d.nnz, s, d, p, keep);
+    } else {
+        APML_LAUNCH_GP(k_bwd_col_softmax, false, (int64_t)d.B * d.M, d.nnz, s, d, p);
+        APML_LAUNCH_GP(k_bwd_row_softmax, false, (int64_t)d.B * d.N, d.nnz, s, d, p, keep);
+    }
     if (d.grad_y)
         APML_LAUNCH_G(k_bwd_grad_y, (int64_t)d.B * d.M, d.nnz, kBlock, 0, s, d, p);
 }
 
 #undef APML_LAUNCH_G
+#undef APML_LAUNCH_GP
 
 } // namespace apml

@@ -70,7 +70,7 @@ def _similarity(T, c1, C):
 
 
 def compare_sample(g: dict, b: int, x: np.ndarray, y: np.ndarray, ref: oracle.SampleResult, tau: float,
-                   check_grad_y: bool = True, prob_rtol: float = PROB_RTOL):
+                   check_grad_y: bool = True, prob_rtol: float = PROB_RTOL, grad_rtol: float = GRAD_RTOL):
     """Element-by-element comparison of sample b of a GPU run with the oracle."""
     N, M = x.shape[0], y.shape[0]
     plan: apml.Plan = g["plan"]
@@ -78,12 +78,12 @@ def compare_sample(g: dict, b: int, x: np.ndarray, y: np.ndarray, ref: oracle.Sa
     loss_rel = abs(g["loss"][b] - ref.loss) / abs(ref.loss)
     assert loss_rel <= LOSS_RTOL, (b, g["loss"][b], ref.loss)
     gx_rel = rel_norm(g["gx"][b], ref.grad_x)
-    assert gx_rel <= GRAD_RTOL, (b, "grad_x", gx_rel)
+    assert gx_rel <= grad_rtol, (b, "grad_x", gx_rel)
     gx_row = row_max_rel(g["gx"][b], ref.grad_x)
     gy_rel = gy_row = 0.0
     if check_grad_y and g["gy"] is not None:
         gy_rel = rel_norm(g["gy"][b], ref.grad_y)
-        assert gy_rel <= GRAD_RTOL, (b, "grad_y", gy_rel)
+        assert gy_rel <= grad_rtol, (b, "grad_y", gy_rel)
         gy_row = row_max_rel(g["gy"][b], ref.grad_y)
     # statistics: argmins bit-exact, temperatures to double precision
     st = plan.export_stats(b)
