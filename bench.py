@@ -89,13 +89,13 @@ PHASE_MODEL = {
 # workload, traffic is reported as null.
 TRAFFIC_WORKLOAD = 2
 TRAFFIC = {
-    "stats": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "ad8bf006f4a0b67c342c005a00d5b74d1844aabf0fa599c6fb52bb6c64f0ed62", "paper_2512_19743_amd/csrc/apml_internal.h": "40ede79ee7d5b227c2b5a9030b34993548b5b94dadfd4b9d6ff59a320b1540f0", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_top2_pairs", "k_finalize"], "bytes_per_launch": 32928969},
-    "support": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "ad8bf006f4a0b67c342c005a00d5b74d1844aabf0fa599c6fb52bb6c64f0ed62", "paper_2512_19743_amd/csrc/apml_internal.h": "40ede79ee7d5b227c2b5a9030b34993548b5b94dadfd4b9d6ff59a320b1540f0", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit"], "bytes_per_launch": 31184249},
-    "build": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "ad8bf006f4a0b67c342c005a00d5b74d1844aabf0fa599c6fb52bb6c64f0ed62", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "40ede79ee7d5b227c2b5a9030b34993548b5b94dadfd4b9d6ff59a320b1540f0", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit_compact_place"], "bytes_per_launch": 19009667},
-    "softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "0e36fa42a6e235cd54e206844926920163a21dadd0ae7404803cde2b5068b819", "paper_2512_19743_amd/csrc/apml_internal.h": "40ede79ee7d5b227c2b5a9030b34993548b5b94dadfd4b9d6ff59a320b1540f0", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_csc_rows", "k_col_softmax"], "bytes_per_launch": 45094581},
-    "sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "4ce80173e4b74b787a3ae107ab7958fc4cb3c55d522622507893578214932f66", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "40ede79ee7d5b227c2b5a9030b34993548b5b94dadfd4b9d6ff59a320b1540f0", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_sinkhorn_fwd"], "bytes_per_launch": 26088451},
-    "bwd_sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "4ce80173e4b74b787a3ae107ab7958fc4cb3c55d522622507893578214932f66", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "40ede79ee7d5b227c2b5a9030b34993548b5b94dadfd4b9d6ff59a320b1540f0", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 26058696},
-    "bwd_softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "0e36fa42a6e235cd54e206844926920163a21dadd0ae7404803cde2b5068b819", "paper_2512_19743_amd/csrc/apml_internal.h": "40ede79ee7d5b227c2b5a9030b34993548b5b94dadfd4b9d6ff59a320b1540f0", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 33342030},
+    "stats": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "d531211cd8a0e9f2b17708841c46531f04e7cd4d56a8173d36bfd36796c0f00b", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_top2_pairs", "k_finalize"], "bytes_per_launch": 32922761},
+    "support": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "d531211cd8a0e9f2b17708841c46531f04e7cd4d56a8173d36bfd36796c0f00b", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit"], "bytes_per_launch": 31251769},
+    "build": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "d531211cd8a0e9f2b17708841c46531f04e7cd4d56a8173d36bfd36796c0f00b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit_compact_place"], "bytes_per_launch": 19012675},
+    "softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "9639635f3d7c2e6d5c4d40b9bdf1f693857960a3a07a34ac8e023a13ff3c3743", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_csc_rows", "k_col_softmax"], "bytes_per_launch": 45082676},
+    "sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "3a1bfc305c57c7cdf98606ec09ecbb8496da5acbbaa04147a2e7f8966523a095", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_sinkhorn_fwd"], "bytes_per_launch": 26076932},
+    "bwd_sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "3a1bfc305c57c7cdf98606ec09ecbb8496da5acbbaa04147a2e7f8966523a095", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 26056904},
+    "bwd_softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "9639635f3d7c2e6d5c4d40b9bdf1f693857960a3a07a34ac8e023a13ff3c3743", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 33329743},
 }
 
 
