@@ -1492,6 +1492,16 @@ __device__ __forceinline__ void owner_scalings(const WSlot (&w)[SW], int n, cons
         }
 }
 
+// The owners' saved scalings of iteration l - 1 alone.
+template <int SW, int OB>
+__device__ __forceinline__ void owner_prev(const WSlot (&w)[SW], int n, const double *own_prev, double (&alp)[SW])
+{
+#pragma unroll
+    for (int q = 0; q < SW; ++q)
+        if (q < n)
+            alp[q] = own_prev[w[q].info & ((1u << OB) - 1u)];
+}
+
 template <int SW, bool HOLD> __global__ __launch_bounds__(kT) void k_sinkhorn_bwd_wr(DevPlan d, int K)
 {
     constexpr int OB = 13; // owner bits of the streamed layout's info word
@@ -1556,13 +1566,24 @@ template <int SW, bool HOLD> __global__ __launch_bounds__(kT) void k_sinkhorn_bw
     const SlotRsrc rsr = slot_rsrc(d.wk_row, b), rsc = slot_rsrc(d.wk_col, b);
     // Loads that do not depend on the exchange are issued ahead of it: a
     // phase's pieces (when streamed) and the gather's saved scalings before
-    // the meeting, the owners' scalings before the gather.
-    double al[SW], alp[SW];
-    owner_scalings<SW, OB>(pr, mr, alpha + L * BN, alpha + (L - 1) * BN, al, alp);
+    // the meeting, the owners' scalings before the gather. The owners of a
+    // workgroup's slots are the same in every phase, so each phase loads only
+    // their scalings of the previous iteration (alp); those of this iteration
+    // (ar for the row owners, ac for the column owners) are the previous
+    // phase's alp of the same side.
+    double ar[SW], ac[SW], alp[SW];
+    owner_scalings<SW, OB>(pr, mr, alpha + L * BN, alpha + (L - 1) * BN, ar, alp);
+    {
+        double unused[SW];
+        owner_scalings<SW, OB>(pc, mc, beta + L * BM, beta + L * BM, ac, unused);
+    }
     uint32_t t = 1;
     for (int l = L; l >= 1; --l) {
         float *yr = d.yr + (size_t)(L - l) * (BN + kSinkOwnersW) + (size_t)b * N;
-        reg_reverse<SW, OB>(pr, rr, mr, al, alp, fc, yr, loc); // reverse of Eq. 4
+        reg_reverse<SW, OB>(pr, rr, mr, ar, alp, fc, yr, loc); // reverse of Eq. 4
+#pragma unroll
+        for (int q = 0; q < SW; ++q)
+            ar[q] = alp[q];
         if constexpr (!HOLD)
             stream_my_slots(pc, rsc, mc, k, K);
         float sp[8];
@@ -1570,13 +1591,16 @@ template <int SW, bool HOLD> __global__ __launch_bounds__(kT) void k_sinkhorn_bw
             load_prev(sp, alpha + (l - 1) * BN, N);
         if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
             return;
-        owner_scalings<SW, OB>(pc, mc, beta + l * BM, beta + (l - 1) * BM, al, alp);
+        owner_prev<SW, OB>(pc, mc, beta + (l - 1) * BM, alp);
         if constexpr (!HOLD)
             load_prev(sp, alpha + (l - 1) * BN, N);
         split_gather_factors(fr, yr, sp, N, loc);
         lds_barrier();
         float *yc = d.yc + (size_t)(L - l) * (BM + kSinkOwnersW) + (size_t)b * M;
-        reg_reverse<SW, OB>(pc, rc, mc, al, alp, fr, yc, loc); // reverse of Eq. 3
+        reg_reverse<SW, OB>(pc, rc, mc, ac, alp, fr, yc, loc); // reverse of Eq. 3
+#pragma unroll
+        for (int q = 0; q < SW; ++q)
+            ac[q] = alp[q];
         if constexpr (!HOLD)
             stream_my_slots(pr, rsr, mr, k, K); // the next row phase's, or the closing pass's
         if constexpr (HOLD)
@@ -1584,7 +1608,7 @@ template <int SW, bool HOLD> __global__ __launch_bounds__(kT) void k_sinkhorn_bw
         if (!split_meet(cnt, (uint32_t)K * ++t, &d.ctr->error, &stop))
             return;
         if (l > 1)
-            owner_scalings<SW, OB>(pr, mr, alpha + (l - 1) * BN, alpha + (l - 2) * BN, al, alp);
+            owner_prev<SW, OB>(pr, mr, alpha + (l - 2) * BN, alp);
         if constexpr (!HOLD)
             load_prev(sp, beta + (l - 1) * BM, M);
         split_gather_factors(fc, yc, sp, M, loc);
