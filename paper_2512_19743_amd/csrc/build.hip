@@ -231,6 +231,7 @@ __global__ __launch_bounds__(kBlock) void k_csc_fill(DevPlan d, BuildArgs a)
 // and taken by an LDS atomic. The workgroup reads all of the sample's pairs
 // and places those of its columns.
 constexpr int kFillT = 1024;
+constexpr int kFillBatch = 8;
 
 __global__ __launch_bounds__(kFillT) void k_csc_fill_lds(DevPlan d, BuildArgs a, int ranges, int C)
 {
@@ -242,14 +243,25 @@ __global__ __launch_bounds__(kFillT) void k_csc_fill_lds(DevPlan d, BuildArgs a,
         next[j - j0] = d.col_ptr[gb + j];
     __syncthreads();
     const int lo = d.row_ptr[(size_t)b * d.N], hi = d.row_ptr[(size_t)(b + 1) * d.N];
-    for (int t = lo + (int)threadIdx.x; t < hi; t += kFillT) {
-        const int j = d.csr_col[t];
-        if (j < j0 || j >= j1)
-            continue;
-        const int p = atomicAdd(&next[j - j0], 1);
-        a.tmp_row[p] = d.csr_row[t] - b * d.N;
-        a.tmp_src[p] = t;
-        d.csc_col[p] = (int32_t)(gb + j);
+    // kFillBatch pairs per thread with their loads in flight together (the
+    // rows too, although only the pairs of this range use them)
+    for (int t0 = lo; t0 < hi; t0 += kFillBatch * kFillT) {
+        int j[kFillBatch], r[kFillBatch];
+#pragma unroll
+        for (int u = 0; u < kFillBatch; ++u) {
+            const int t = t0 + u * kFillT + (int)threadIdx.x;
+            j[u] = t < hi ? d.csr_col[t] : -1;
+            r[u] = t < hi ? d.csr_row[t] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < kFillBatch; ++u)
+            if (j[u] >= j0 && j[u] < j1) {
+                const int t = t0 + u * kFillT + (int)threadIdx.x;
+                const int p = atomicAdd(&next[j[u] - j0], 1);
+                a.tmp_row[p] = r[u] - b * d.N;
+                a.tmp_src[p] = t;
+                d.csc_col[p] = (int32_t)(gb + j[u]);
+            }
     }
 }
 
