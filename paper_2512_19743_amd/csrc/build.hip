@@ -275,9 +275,7 @@ __global__ __launch_bounds__(kBlock) void k_csc_sort(DevPlan d, BuildArgs a)
     const int gc = d.csc_col[p];
     const int s0 = d.col_ptr[gc], s1 = d.col_ptr[gc + 1];
     const int key = a.tmp_row[p];
-    int rank = 0;
-    for (int q = s0; q < s1; ++q)
-        rank += a.tmp_row[q] < key;
+    const int rank = count_below(a.tmp_row, s0, s1, key);
     d.csc_row[s0 + rank] = key;
     d.csc_perm[s0 + rank] = a.tmp_src[p];
 }

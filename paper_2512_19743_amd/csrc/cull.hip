@@ -468,9 +468,7 @@ __device__ __forceinline__ void rank_entry(const CullEmitArgs &a, int64_t e)
     if (s1 - s0 <= kCullStage) // ordered from the staging
         return;
     const int j = a.tmp_col[e];
-    int rank = 0;
-    for (int t = s0; t < s1; ++t)
-        rank += a.tmp_col[t] < j;
+    const int rank = count_below(a.tmp_col, s0, s1, j);
     a.csr_col[s0 + rank] = j;
 }
 

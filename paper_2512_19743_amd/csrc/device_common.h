@@ -36,6 +36,20 @@ __device__ __forceinline__ double dist_f64(const float *a, const float *b)
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 
+// Number of entries of a[s0, s1) below key: four loads in flight at a time
+// (a loop of one load per step waits out every load in turn).
+__device__ __forceinline__ int count_below(const int32_t *a, int s0, int s1, int key)
+{
+    int n = 0, q = s0;
+    for (; q + 4 <= s1; q += 4) {
+        const int v0 = a[q], v1 = a[q + 1], v2 = a[q + 2], v3 = a[q + 3];
+        n += (v0 < key) + (v1 < key) + (v2 < key) + (v3 < key);
+    }
+    for (; q < s1; ++q)
+        n += a[q] < key;
+    return n;
+}
+
 // Read-only data seen through the constant address space: wave-uniform loads
 // from it become scalar loads even in kernels that also store to memory.
 template <typename T> using const_ptr = const __attribute__((address_space(4))) T *;
