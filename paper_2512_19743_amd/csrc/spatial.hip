@@ -10,8 +10,8 @@
 //
 //   k_spatial_sort  one workgroup per (sample, cloud, chunk of 8192 points).
 //                   The frame is the bounding cube of both clouds of the
-//                   sample, quantized to 10 bits per axis; the 30-bit Hilbert keys are sorted by a
-//                   least-significant-digit radix sort (three 10-bit digits,
+//                   sample, quantized to 10 bits per axis; the upper 20 bits of the 30-bit Hilbert keys are sorted by a
+//                   least-significant-digit radix sort (two 10-bit digits,
 //                   stable: ranks within a wave from ballots, across waves
 //                   from per-wave digit counts in LDS). The sorted points are
 //                   written as (x, y, z, original index), with the bounding
@@ -32,6 +32,7 @@ constexpr int kSortWaves = kSortT / 64;
 constexpr int kDigitBits = 10;
 constexpr int kBins = 1 << kDigitBits; // == kSortT: one bin per thread in the scans
 constexpr int kPasses = 3;
+constexpr int kFirstPass = 1; // the lowest digit is not sorted (see k_spatial_sort)
 constexpr int kSuper = 8; // keys per thread held in registers between global round trips
 // Points sorted by one workgroup. A larger cloud is sorted in chunks of this
 // many points in parallel, and the chunks are then merged pairwise.
@@ -259,21 +260,27 @@ __global__ __launch_bounds__(kSortT) void k_spatial_sort(SpatialArgs a)
     const float ext = fmaxf(fmaxf(f[3] - f[0], f[4] - f[1]), f[5] - f[2]);
     const float scale = ext > 0.0f ? 1024.0f / ext : 0.0f;
 
-    // keys and the digit histograms of all passes (independent of the order)
+    // keys and the digit histograms of the passes (independent of the order).
+    // Only the upper 20 of the key's 30 bits are sorted (the lowest digit is
+    // cleared, so the merges of larger clouds compare the same keys): 2^20
+    // cells hold runs of 32 points about as compact as 2^30 for the clouds
+    // sorted here, and one radix pass fewer is needed. The order only decides
+    // which pairs the scans skip, never a result.
     for (int k = tid; k < n; k += kSortT) {
         const float *p = pts + 3 * (size_t)k;
         const uint32_t key =
-            hilbert_key(quantize(p[0], f[0], scale), quantize(p[1], f[1], scale), quantize(p[2], f[2], scale));
-        k0[k] = key;
-        v0[k] = (uint32_t)(c0 + k); // index within the sample
+            hilbert_key(quantize(p[0], f[0], scale), quantize(p[1], f[1], scale), quantize(p[2], f[2], scale)) &
+            ~(uint32_t)(kBins - 1);
+        k1[k] = key;
+        v1[k] = (uint32_t)(c0 + k); // index within the sample
 #pragma unroll
-        for (int q = 0; q < kPasses; ++q)
+        for (int q = kFirstPass; q < kPasses; ++q)
             atomicAdd(&s.base[q][(key >> (q * kDigitBits)) & (kBins - 1)], 1);
     }
     __syncthreads(); // the keys written above are read back by other threads
     // exclusive scans of the histograms: bin tid of every pass
 #pragma unroll
-    for (int q = 0; q < kPasses; ++q) {
+    for (int q = kFirstPass; q < kPasses; ++q) {
         const int c = s.base[q][tid];
         int inc = c;
 #pragma unroll
@@ -293,8 +300,7 @@ __global__ __launch_bounds__(kSortT) void k_spatial_sort(SpatialArgs a)
         s.base[q][tid] = before + inc - c;
     }
     lds_barrier();
-    radix_pass(s, 0, n, k0, v0, k1, v1);
-    __syncthreads();
+    static_assert(kPasses - kFirstPass == 2, "two passes: from the second buffers back to them");
     radix_pass(s, 1, n, k1, v1, k0, v0);
     __syncthreads();
     radix_pass(s, 2, n, k0, v0, k1, v1);
