@@ -89,13 +89,13 @@ PHASE_MODEL = {
 # workload, traffic is reported as null.
 TRAFFIC_WORKLOAD = 2
 TRAFFIC = {
-    "stats": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "d531211cd8a0e9f2b17708841c46531f04e7cd4d56a8173d36bfd36796c0f00b", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_top2_pairs", "k_finalize"], "bytes_per_launch": 32922761},
-    "support": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "d531211cd8a0e9f2b17708841c46531f04e7cd4d56a8173d36bfd36796c0f00b", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit"], "bytes_per_launch": 31251769},
-    "build": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "d531211cd8a0e9f2b17708841c46531f04e7cd4d56a8173d36bfd36796c0f00b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_emit_compact_place"], "bytes_per_launch": 19012675},
-    "softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "9639635f3d7c2e6d5c4d40b9bdf1f693857960a3a07a34ac8e023a13ff3c3743", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_csc_rows", "k_col_softmax"], "bytes_per_launch": 45082676},
-    "sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "3a1bfc305c57c7cdf98606ec09ecbb8496da5acbbaa04147a2e7f8966523a095", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_sinkhorn_fwd"], "bytes_per_launch": 26076932},
-    "bwd_sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "3a1bfc305c57c7cdf98606ec09ecbb8496da5acbbaa04147a2e7f8966523a095", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 26056904},
-    "bwd_softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "9639635f3d7c2e6d5c4d40b9bdf1f693857960a3a07a34ac8e023a13ff3c3743", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "4de73120c421b7e0af9f71c422c6f85ac615a9d9154719f1a1158a98c87c89a7"}, "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 33329743},
+    "stats": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "d531211cd8a0e9f2b17708841c46531f04e7cd4d56a8173d36bfd36796c0f00b", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_top2_pairs", "k_finalize"], "bytes_per_launch": 32933577},
+    "support": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "d531211cd8a0e9f2b17708841c46531f04e7cd4d56a8173d36bfd36796c0f00b", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_emit"], "bytes_per_launch": 31255576},
+    "build": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "d531211cd8a0e9f2b17708841c46531f04e7cd4d56a8173d36bfd36796c0f00b", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_emit_compact_place"], "bytes_per_launch": 19012099},
+    "softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "9639635f3d7c2e6d5c4d40b9bdf1f693857960a3a07a34ac8e023a13ff3c3743", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_csc_rows", "k_col_softmax"], "bytes_per_launch": 45089348},
+    "sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "6b870128602eba75668a6da7d24c51c4929486f69226342e678657215f2d2ea4", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_sinkhorn_fwd"], "bytes_per_launch": 26089219},
+    "bwd_sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "6b870128602eba75668a6da7d24c51c4929486f69226342e678657215f2d2ea4", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 26059848},
+    "bwd_softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "9639635f3d7c2e6d5c4d40b9bdf1f693857960a3a07a34ac8e023a13ff3c3743", "paper_2512_19743_amd/csrc/apml_internal.h": "4fed8534496fb1d10fed2ceb81d3cfa763919843b57100294eaa45fdd215646d", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 33329743},
 }
 
 
