@@ -21,11 +21,13 @@ struct Counters {
                                    // bit 2: a meeting of the split streamed Sinkhorn kernels timed out
     unsigned int overflow;         // a tile of the full support scan (a row of the skipping one) is written by
                                    // a second pass: its further hits did not fit
-    unsigned int spill_fill;       // entries taken from the full support scan's pool of further hits
     // pairs evaluated by the skipping scans (minimum scan, support scan), in
     // kScanSlots partial sums: workgroup w adds to slot w % kScanSlots, so
     // that no single address takes every workgroup's atomic
     unsigned long long scanned[2][kScanSlots];
+    // entries requested from the full support scan's pool of further hits
+    // (64-bit: tiles that find the pool full still add theirs)
+    unsigned long long spill_fill;
 };
 
 struct Params {

@@ -404,7 +404,7 @@ template <bool WRITE> __global__ __launch_bounds__(kBlock) void k_emit(EmitArgs 
                 int base = total == 0 ? 0 : -1;
                 if (total > 0 && total <= kTileList) {
                     const int64_t need = kBlock + total;
-                    const int64_t got = atomicAdd(&a.ctr->spill_fill, (unsigned int)need);
+                    const int64_t got = (int64_t)atomicAdd(&a.ctr->spill_fill, (unsigned long long)need);
                     if (got + need <= a.spill_cap)
                         base = (int)got;
                 }
