@@ -60,6 +60,11 @@ CASES = {
     # one sample with enough pieces for the split forward kernel, B N < 8192
     # (and B not a multiple of 8: seven of the grid's eight rounds end at once)
     "b1_n8000": lambda: custom(75, 1, 8000, 7990, reference="primitives", prediction="perm_noise", sigma=0.02),
+    # B = 37 (not a multiple of 8), four workgroups per sample, ragged
+    # clouds of 7000 and 6500 points: about three slots per workgroup, the
+    # reverse kernel that keeps the adjoint in registers and loads its
+    # pieces in every phase
+    "b37_ragged": lambda: custom(77, 37, 7000, 6500, reference="primitives", prediction="perm_noise", sigma=0.02),
     # B = 72: three workgroups per sample (a grid of 216), a larger share of
     # each sample's pieces per workgroup
     "b72_n8000": lambda: custom(76, 72, 8000, 8000, reference="primitives", prediction="perm_noise", sigma=0.02),
