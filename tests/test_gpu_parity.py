@@ -127,6 +127,15 @@ def test_support_scan_further_hits(prediction, sigma, tau, grad_rtol):
                  grad_rtol=grad_rtol)
 
 
+def test_temperature_gradient_near_tie_without_iterations():
+    # the near-degenerate sample above with L = 0: the loss is sum P0 C, and
+    # the backward forms P in double precision, so the gap terms that T / g
+    # amplifies keep their digits (stored single-precision P gave 5.5e-4)
+    X, Y = custom(90, 1, 1024, 4096, reference="primitives", prediction="uniform_cube", sigma=0.0)
+    _, res = _check_batch(X, Y, "near tie, L = 0", n_iter=0, scan="full")
+    assert res[0]["gy_rel"] <= 1e-6, res[0]
+
+
 @pytest.mark.parametrize("scan", ["full", "skip"])
 def test_threshold_one_is_half_chamfer(scan):
     X, Y = custom(27, 2, 150, 170, sigma=0.05)
