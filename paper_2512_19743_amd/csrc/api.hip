@@ -461,6 +461,24 @@ bool use_skipping_scans(const apml_params &p, int N, int M)
 
 } // namespace
 
+hipError_t apml::set_dynamic_lds(const void *k, size_t bytes)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    static std::mutex mu;
+    static std::map<std::pair<int, const void *>, size_t> set; // largest size set per device and kernel
+    std::lock_guard<std::mutex> lock(mu);
+    const auto key = std::make_pair(dev, k);
+    const auto it = set.find(key);
+    if (it != set.end() && it->second >= bytes)
+        return hipSuccess;
+    const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e == hipSuccess)
+        set[key] = bytes;
+    return e;
+}
+
 extern "C" {
 
 void apml_params_default(apml_params *p)

@@ -357,6 +357,11 @@ void launch_csc_sort(const DevPlan &d, const BuildArgs &a, hipStream_t s);
 bool csc_sample_fits(int N, int M, int64_t max_pairs);
 hipError_t launch_csc_and_softmax(const DevPlan &d, const Params &p, int64_t max_pairs, hipStream_t s);
 
+// hipFuncSetAttribute(k, MaxDynamicSharedMemorySize, bytes) on the current
+// device, made once per device and kernel for every larger size (the forward
+// and backward would otherwise make the runtime call on every call).
+hipError_t set_dynamic_lds(const void *k, size_t bytes);
+
 void launch_softmax(const DevPlan &d, const Params &p, hipStream_t s);
 // Backward of both softmaxes and the distance gradient. double_p: P formed
 // again in double precision from the stored costs (for plans whose reverse

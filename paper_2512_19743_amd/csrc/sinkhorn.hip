@@ -2113,7 +2113,7 @@ hipError_t launch_sinkhorn_bwd(const DevPlan &d, int64_t max_pairs, hipStream_t 
     (void)max_pairs;
     const size_t bytes = 4 * (size_t)(adj_slots(d.pk_row.slots) + 1); // beyond the static arrays
     const auto k = for_slots<BwdK>(d.pk_row.slots);
-    hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    hipError_t e = set_dynamic_lds((const void *)k, bytes);
     if (e != hipSuccess)
         return e;
     hipLaunchKernelGGL(k, dim3(d.B), dim3(kT), bytes, s, d);

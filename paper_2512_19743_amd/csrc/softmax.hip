@@ -673,7 +673,7 @@ hipError_t launch_csc_and_softmax(const DevPlan &d, const Params &p, int64_t max
     const void *k = gr == 16  ? (const void *)k_csc_rows<16>
                     : gr == 8 ? (const void *)k_csc_rows<8>
                               : (const void *)k_csc_rows<kGroup>;
-    hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    hipError_t e = set_dynamic_lds(k, bytes);
     if (e != hipSuccess)
         return e;
     const unsigned rows = blocks_for(BN * gr, kCscT);

@@ -468,10 +468,7 @@ void launch_batch_boxes(const Box *box_x, const Box *box_y, Box *batch_x, Box *b
 
 hipError_t launch_spatial_sort(const SpatialArgs &a, hipStream_t s)
 {
-    // set on every call: the attribute belongs to the current device, and a
-    // process may drive several
-    const hipError_t e = hipFuncSetAttribute((const void *)k_spatial_sort, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                             (int)sizeof(SortLds));
+    const hipError_t e = set_dynamic_lds((const void *)k_spatial_sort, sizeof(SortLds));
     if (e != hipSuccess)
         return e;
     const int n_max = std::max(a.N, a.M);
