@@ -358,12 +358,15 @@ __device__ __forceinline__ double p0bar(const DevPlan &d, int t, double gl)
 // Taken where the reverse sweeps keep the adjoint in double (or there are
 // none); the sweeps that keep it in LDS store it in single precision, which
 // then bounds the error as much (shape-completion workload: 6.7e-6 either
-// way), and P is read as stored. DP caches 4 pairs per lane instead of 8, so
-// that its exponentials leave four waves per SIMD.
+// way), and P is read as stored. Both cache 4 pairs per lane (the forward 8):
+// four or more waves per SIMD instead of three (the row kernel held 158
+// registers with 8), and owners rarely have more than 4 pairs per lane
+// (large-batch workload: adjoint 0.157 -> 0.134 ms; shape-completion:
+// 0.0338 -> 0.0331 ms).
 constexpr int kBwdCache = 4;
 
 template <bool DP> struct BwdP {
-    static constexpr int kCache = DP ? kBwdCache : kSmCache;
+    static constexpr int kCache = kBwdCache;
     using T = std::conditional_t<DP, double, float>; // type of the cached P
 };
 
