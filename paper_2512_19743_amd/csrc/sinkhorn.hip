@@ -1645,11 +1645,16 @@ __global__ __launch_bounds__(kBlock) void k_zero_u32(uint32_t *a, int n)
 // ---------------------------------------------------------------------------
 //
 // G lanes per owner (row or column; steps_lanes); each lane issues the loads
-// of kSB of its pairs together before using them. Sums are per lane in pair
-// order, then a butterfly over the group, so results do not depend on
-// scheduling.
+// of kSB of its pairs together before using them (kSBRev in the reverse
+// launches, whose pairs carry 12 registers each: with 8 they held 101
+// registers, four waves per SIMD; with 4, 61 and eight waves: reverse sweeps
+// 0.525 -> 0.474 ms on 16 x 4096 x 16384 points, 0.455 -> 0.444 ms on
+// 4 x 65536, measured A/B on one box; 2 was slower than 4). Sums are per
+// lane in pair order, then a butterfly over the group, so results do not
+// depend on scheduling.
 constexpr int kSG = 4;
 constexpr int kSB = 8;
+constexpr int kSBRev = 4;
 
 __global__ __launch_bounds__(kBlock) void k_fill_ones(double *a, int n)
 {
@@ -1660,17 +1665,17 @@ __global__ __launch_bounds__(kBlock) void k_fill_ones(double *a, int n)
 
 // Sum over owner o's pairs k = lg, lg + kSG, ... of f(k, position) with the
 // loads of kSB pairs in flight at once.
-template <int G = kSG, class Load, class Use>
+template <int G = kSG, int SB = kSB, class Load, class Use>
 __device__ __forceinline__ double owner_sum(int n, int lg, Load load, Use use)
 {
     double acc = 0.0;
-    for (int k0 = lg; k0 < n; k0 += G * kSB) {
-        decltype(load(0)) v[kSB];
+    for (int k0 = lg; k0 < n; k0 += G * SB) {
+        decltype(load(0)) v[SB];
 #pragma unroll
-        for (int u = 0; u < kSB; ++u)
+        for (int u = 0; u < SB; ++u)
             v[u] = load(k0 + G * u < n ? k0 + G * u : -1);
 #pragma unroll
-        for (int u = 0; u < kSB; ++u)
+        for (int u = 0; u < SB; ++u)
             if (k0 + G * u < n)
                 acc += use(v[u]);
     }
@@ -1827,25 +1832,25 @@ template <int G> __global__ __launch_bounds__(kBlock) void k_bwd_rows(DevPlan d,
         int k;
         double4 c;
     };
-    const double acc = owner_sum<G>(n, lg,
-                                 [&](int k) {
-                                     V v{0.0, 0.0f, k, make_double4(0.0, 0.0, 1.0, 0.0)};
-                                     if (k >= 0) {
-                                         const int j = d.csr_col[t0 + k];
-                                         v.z = d.rz[t0 + k];
-                                         v.p = d.p0r[t0 + k];
-                                         v.c = xyc[j];
-                                     }
-                                     return v;
-                                 },
-                                 [&](const V &v) {
-                                     double z = v.z;
-                                     if (pending) // 1/beta^(l+1)_j
-                                         z = __builtin_fma(z * v.c.z, mine.x, -mine.y);
-                                     z = __builtin_fma(z * inv_a, v.c.x, -v.c.y);
-                                     d.rz[t0 + v.k] = z;
-                                     return z * (double)v.p;
-                                 });
+    const double acc = owner_sum<G, kSBRev>(n, lg,
+                                         [&](int k) {
+                                             V v{0.0, 0.0f, k, make_double4(0.0, 0.0, 1.0, 0.0)};
+                                             if (k >= 0) {
+                                                 const int j = d.csr_col[t0 + k];
+                                                 v.z = d.rz[t0 + k];
+                                                 v.p = d.p0r[t0 + k];
+                                                 v.c = xyc[j];
+                                             }
+                                             return v;
+                                         },
+                                         [&](const V &v) {
+                                             double z = v.z;
+                                             if (pending) // 1/beta^(l+1)_j
+                                                 z = __builtin_fma(z * v.c.z, mine.x, -mine.y);
+                                             z = __builtin_fma(z * inv_a, v.c.x, -v.c.y);
+                                             d.rz[t0 + v.k] = z;
+                                             return z * (double)v.p;
+                                         });
     if (lg == 0) { // adjoint of Eq. 4: d_i = alpha^l_i * sum
         const double dsum = al * acc;
         d.xyr[r] = make_double4(al, dsum * al, inv_a, 0.0);
@@ -1871,23 +1876,23 @@ template <int G> __global__ __launch_bounds__(kBlock) void k_bwd_cols(DevPlan d,
         int k;
         double4 rw;
     };
-    const double acc = owner_sum<G>(n, lg,
-                                 [&](int k) {
-                                     V v{0.0, 0.0f, k, make_double4(0.0, 0.0, 1.0, 0.0)};
-                                     if (k >= 0) {
-                                         const int i = d.csc_row[s0 + k];
-                                         v.z = d.kz[s0 + k];
-                                         v.p = d.p0c[s0 + k];
-                                         v.rw = xyr[i];
-                                     }
-                                     return v;
-                                 },
-                                 [&](const V &v) { // v.rw.z = 1/alpha^l_i
-                                     double z = __builtin_fma(v.z * v.rw.z, mine.x, -mine.y);
-                                     z = __builtin_fma(z * inv_b, v.rw.x, -v.rw.y);
-                                     d.kz[s0 + v.k] = z;
-                                     return z * (double)v.p;
-                                 });
+    const double acc = owner_sum<G, kSBRev>(n, lg,
+                                         [&](int k) {
+                                             V v{0.0, 0.0f, k, make_double4(0.0, 0.0, 1.0, 0.0)};
+                                             if (k >= 0) {
+                                                 const int i = d.csc_row[s0 + k];
+                                                 v.z = d.kz[s0 + k];
+                                                 v.p = d.p0c[s0 + k];
+                                                 v.rw = xyr[i];
+                                             }
+                                             return v;
+                                         },
+                                         [&](const V &v) { // v.rw.z = 1/alpha^l_i
+                                             double z = __builtin_fma(v.z * v.rw.z, mine.x, -mine.y);
+                                             z = __builtin_fma(z * inv_b, v.rw.x, -v.rw.y);
+                                             d.kz[s0 + v.k] = z;
+                                             return z * (double)v.p;
+                                         });
     if (lg == 0) { // adjoint of Eq. 3: e_j = beta^l_j * sum
         const double esum = bl * acc;
         d.xyc[gc] = make_double4(bl, esum * bl, inv_b, 0.0);
