@@ -1649,7 +1649,7 @@ __global__ __launch_bounds__(kBlock) void k_zero_u32(uint32_t *a, int n)
 // launches, whose pairs carry 12 registers each: with 8 they held 101
 // registers, four waves per SIMD; with 4, 61 and eight waves: reverse sweeps
 // 0.525 -> 0.474 ms on 16 x 4096 x 16384 points, 0.455 -> 0.444 ms on
-// 4 x 65536, measured A/B on one box; 2 was slower than 4). Sums are per
+// 4 x 65536, measured side by side on one MI355X; 2 was slower than 4). Sums are per
 // lane in pair order, then a butterfly over the group, so results do not
 // depend on scheduling.
 constexpr int kSG = 4;

@@ -354,14 +354,14 @@ __device__ __forceinline__ double p0bar(const DevPlan &d, int t, double gl)
 // single precision (same operations and lane order, so the same sum Z). The
 // temperature adjoint cancels, and it reaches the argmins multiplied by T / g,
 // large for a small gap: with stored single-precision P the gradient error
-// reached 5e-4 there, and 9e-6 on 16 x 4096 x 16384 points (2e-8 with DP).
+// reached 5e-4 there, and 9e-6 on 16 x 4096 x 16384 points (1.2e-7 with DP).
 // Taken where the reverse sweeps keep the adjoint in double (or there are
 // none); the sweeps that keep it in LDS store it in single precision, which
-// then bounds the error as much (shape-completion workload: 6.7e-6 either
+// then bounds the error as much (32 samples of 2048 points: 6.7e-6 either
 // way), and P is read as stored. Both cache 4 pairs per lane (the forward 8):
 // four or more waves per SIMD instead of three (the row kernel held 158
 // registers with 8), and owners rarely have more than 4 pairs per lane
-// (large-batch workload: adjoint 0.157 -> 0.134 ms; shape-completion:
+// (64 samples of 8192 points: adjoint 0.157 -> 0.134 ms; 32 of 2048:
 // 0.0338 -> 0.0331 ms).
 constexpr int kBwdCache = 4;
 
