@@ -877,7 +877,8 @@ apml_status run_forward(apml_plan *plan, const float *x, const float *y, int32_t
     // column-major view: per sample in LDS when it fits (with the row
     // softmax), else slots taken by global counters (in the full scan's
     // compaction when no tile is rescanned)
-    const bool csc_lds = csc_sample_fits(N, M, plan->max_sample);
+    const char *csc_env = std::getenv("APML_CSC"); // =global: never the per-sample LDS build
+    const bool csc_lds = !(csc_env && std::strcmp(csc_env, "global") == 0) && csc_sample_fits(N, M, plan->max_sample);
     const bool placed = !skip && !csc_lds && ea.stage && !rb->ctr.overflow;
     if (!csc_lds) {
         ba.tmp_row = tmp.get<int32_t>(nnz);
