@@ -89,10 +89,10 @@ PHASE_MODEL = {
 # workload, traffic is reported as null.
 TRAFFIC_WORKLOAD = 2
 TRAFFIC = {
-    "stats": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "7a43ac83cf26cdc470cf20022a550a2cb74ddc98dcb03aea03fd5398a1e18a96", "paper_2512_19743_amd/csrc/apml_internal.h": "9de09b22e2bb70db0e738b837406b4c22d17c6c43878bf853591214bca0bb461", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_top2_pairs", "k_finalize"], "bytes_per_launch": 32924264},
-    "support": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "7a43ac83cf26cdc470cf20022a550a2cb74ddc98dcb03aea03fd5398a1e18a96", "paper_2512_19743_amd/csrc/apml_internal.h": "9de09b22e2bb70db0e738b837406b4c22d17c6c43878bf853591214bca0bb461", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_emit"], "bytes_per_launch": 31256664},
-    "build": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "7a43ac83cf26cdc470cf20022a550a2cb74ddc98dcb03aea03fd5398a1e18a96", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "9de09b22e2bb70db0e738b837406b4c22d17c6c43878bf853591214bca0bb461", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_emit_compact_place"], "bytes_per_launch": 19012547},
-    "softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "28183ee496ceedff271bcff0dd2c7514af55af7c0c45ec3fb1acfae43e1015fe", "paper_2512_19743_amd/csrc/apml_internal.h": "9de09b22e2bb70db0e738b837406b4c22d17c6c43878bf853591214bca0bb461", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_csc_rows", "k_col_softmax"], "bytes_per_launch": 47738682},
+    "stats": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "b8ad8ac7143c0e550506b6e9f041715acbb53afe58979c162835c46acc143f29", "paper_2512_19743_amd/csrc/apml_internal.h": "9de09b22e2bb70db0e738b837406b4c22d17c6c43878bf853591214bca0bb461", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_top2_pairs", "k_finalize"], "bytes_per_launch": 32933544},
+    "support": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "b8ad8ac7143c0e550506b6e9f041715acbb53afe58979c162835c46acc143f29", "paper_2512_19743_amd/csrc/apml_internal.h": "9de09b22e2bb70db0e738b837406b4c22d17c6c43878bf853591214bca0bb461", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_emit"], "bytes_per_launch": 31271543},
+    "build": {"sources": {"paper_2512_19743_amd/csrc/dense.hip": "b8ad8ac7143c0e550506b6e9f041715acbb53afe58979c162835c46acc143f29", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "9de09b22e2bb70db0e738b837406b4c22d17c6c43878bf853591214bca0bb461", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_emit_compact_place"], "bytes_per_launch": 19027330},
+    "softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "28183ee496ceedff271bcff0dd2c7514af55af7c0c45ec3fb1acfae43e1015fe", "paper_2512_19743_amd/csrc/apml_internal.h": "9de09b22e2bb70db0e738b837406b4c22d17c6c43878bf853591214bca0bb461", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_csc_rows", "k_col_softmax"], "bytes_per_launch": 47747018},
     "sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "6a3a219f06db8722ed82302bacadd7d5d9a8d94492632d4a1c2cf2fc4b99ff33", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "9de09b22e2bb70db0e738b837406b4c22d17c6c43878bf853591214bca0bb461", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_sinkhorn_fwd"], "bytes_per_launch": 26089219},
     "bwd_sinkhorn": {"sources": {"paper_2512_19743_amd/csrc/sinkhorn.hip": "6a3a219f06db8722ed82302bacadd7d5d9a8d94492632d4a1c2cf2fc4b99ff33", "paper_2512_19743_amd/csrc/pieces.h": "f583f03e18c705c400d730c1898150e41963388a2bc4895a88aca2cb4a0f625b", "paper_2512_19743_amd/csrc/apml_internal.h": "9de09b22e2bb70db0e738b837406b4c22d17c6c43878bf853591214bca0bb461", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_sinkhorn_bwd"], "bytes_per_launch": 26059848},
     "bwd_softmax": {"sources": {"paper_2512_19743_amd/csrc/softmax.hip": "28183ee496ceedff271bcff0dd2c7514af55af7c0c45ec3fb1acfae43e1015fe", "paper_2512_19743_amd/csrc/apml_internal.h": "9de09b22e2bb70db0e738b837406b4c22d17c6c43878bf853591214bca0bb461", "paper_2512_19743_amd/csrc/device_common.h": "03dc51e197a1281c03edf6f18979a0e66674abec0a0da05b91d1f7efd31020c0"}, "kernels": ["k_bwd_col_softmax", "k_bwd_row_softmax"], "bytes_per_launch": 33406536},

@@ -241,12 +241,21 @@ __global__ __launch_bounds__(kBlock) void k_finalize(FinalizeArgs args)
     if (k >= args.B * d.n_own)
         return;
     const size_t stride = (size_t)args.B * d.n_own;
+    // the top-2 of a union of multisets does not depend on the order of the
+    // merges: the chunks' partials are loaded kFinBatch at a time, so their
+    // loads are in flight together
+    constexpr int kFinBatch = 8;
     float m1 = kInf, m2 = kInf;
-    for (int c = 0; c < d.S; ++c) {
-        const float2 v = d.partial[c * stride + k];
-        // top-2 of the union of two top-2 multisets
-        m2 = fminf(fmaxf(m1, v.x), fminf(m2, v.y));
-        m1 = fminf(m1, v.x);
+    for (int c0 = 0; c0 < d.S; c0 += kFinBatch) {
+        float2 v[kFinBatch];
+#pragma unroll
+        for (int u = 0; u < kFinBatch; ++u)
+            v[u] = c0 + u < d.S ? d.partial[(size_t)(c0 + u) * stride + k] : make_float2(kInf, kInf);
+#pragma unroll
+        for (int u = 0; u < kFinBatch; ++u) { // top-2 of the union of two top-2 multisets
+            m2 = fminf(fmaxf(m1, v[u].x), fminf(m2, v[u].y));
+            m1 = fminf(m1, v[u].x);
+        }
     }
     d.m12[k] = make_float2(m1, m2);
     const double e = emission_radius2(m1, m2, d.log_ratio, args.p);
